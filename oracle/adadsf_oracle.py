@@ -1,0 +1,409 @@
+"""CPU oracle for the AdaDSF depth-sparse layer stack.
+
+TEST INFRASTRUCTURE. Only the test suite, the smoke check and the benchmark's
+CPU-baseline leg may import this module. The product (the HIP library and its
+Python binding) never calls it. The two share no code: both are fed by the
+seeded generators in ``synthetic``, which hold no part of the method's
+arithmetic.
+
+Everything is computed in float64 with plain numpy; inputs that were rounded
+to bf16 or fp32 are widened exactly. Matrix products use numpy's matmul as a
+library primitive. There is no blocking, fusion or reordering beyond what each
+definition states, so each function can be checked against the paper by eye.
+
+Paper: "Adaptive Depth Sparse Framework: Similarity-Driven Resource Allocation
+for Pre-Trained LLMs" (AdaDSF).
+
+Readings taken where the paper is silent or ambiguous (each also in the design doc):
+
+* Eq. 4 is applied per token over the hidden dimension, then averaged over the
+  calibration tokens; a zero product of norms is guarded by 1e-8.
+* Eq. 8 can give r_i > 1. The default clip sets such layers to 1 and hands the
+  excess back to the other layers in proportion to r'_j, so sum(r) = tL still
+  holds.
+* K_i = floor(r_i T) (Section 3.4) is evaluated as floor(r_i T + 1e-6). This
+  guard absorbs fp64 representation error, e.g. floor(0.29 * 100) = 28.
+* Top-K ties go to the lower position; the kept positions are returned in
+  ascending order. -0.0 equals +0.0, and NaN ranks below every number.
+* Masked selection is read as compaction. The block runs on the kept rows
+  only, at their original positions, and kept tokens attend causally among
+  kept tokens. Skipped rows pass through unchanged, and the block output is
+  not gated by the router score.
+* The block is each model family's own pre-norm block. NeoX uses a parallel
+  residual, LayerNorm, exact-erf GELU and partial rotary. Qwen uses a
+  sequential residual, RMSNorm, SwiGLU, full rotary and GQA. Eq. 3 is a
+  post-norm schematic that matches neither model.
+* The router reads the raw residual-stream row: score = w2 . ReLU(W1 x + b1) + b2.
+
+Parity status: every function here is pinned by the CPU tests (closed forms,
+invariants, brute force, and library cross-checks against torch and the
+transformers GPT-NeoX / Qwen2 layers). The values against the paper's own
+trained models are unpinned, because the paper publishes no weights or worked
+examples.
+"""
+from __future__ import annotations
+
+import math
+from typing import Dict, List, Optional, Sequence, Tuple
+
+import numpy as np
+from scipy.special import erf
+
+NEOX = "neox_parallel"
+QWEN = "qwen_seq"
+
+COS_EPS = 1e-8
+K_GUARD = 1e-6
+
+
+def f64(a) -> np.ndarray:
+    """Widen a numpy array or CPU torch tensor to float64 exactly."""
+    if hasattr(a, "detach"):
+        a = a.detach().to("cpu")
+        import torch  # local: the oracle itself needs torch only for this conversion
+        a = a.to(torch.float64).numpy()
+    return np.asarray(a, dtype=np.float64)
+
+
+# ---------------------------------------------------------------------------
+# Rounding to the storage formats (used where a result is stored, e.g. scatter)
+# ---------------------------------------------------------------------------
+
+def round_bf16(v: np.ndarray) -> np.ndarray:
+    """Round float64 values to bfloat16 (8 significant bits), ties to even.
+
+    Written from the format's definition: mantissa in [0.5, 1) from frexp,
+    scaled to 8 bits, rounded half-to-even (numpy's rint), scaled back.
+    Valid for the normal range of bf16, which is fp32's exponent range.
+    """
+    v = np.asarray(v, dtype=np.float64)
+    m, e = np.frexp(v)
+    q = np.rint(m * 256.0)
+    return np.ldexp(q, e - 8)
+
+
+def round_f32(v: np.ndarray) -> np.ndarray:
+    return np.asarray(v, dtype=np.float64).astype(np.float32).astype(np.float64)
+
+
+def round_to(dtype: str, v: np.ndarray) -> np.ndarray:
+    return round_bf16(v) if dtype == "bf16" else round_f32(v)
+
+
+# ---------------------------------------------------------------------------
+# Section 3.3, Eq. 4: cosine similarity between a layer's input and output
+# ---------------------------------------------------------------------------
+
+def token_cosine(x_in, x_out, eps: float = COS_EPS) -> np.ndarray:
+    """Per-token cosine between input and output rows (Eq. 4 applied to one token).
+
+    x_in, x_out: [..., d]. Returns [...]. A product of norms below eps is
+    replaced by eps, so an all-zero row gives 0.
+    """
+    a = f64(x_in)
+    c = f64(x_out)
+    dot = np.sum(a * c, axis=-1)
+    na = np.sqrt(np.sum(a * a, axis=-1))
+    nc = np.sqrt(np.sum(c * c, axis=-1))
+    return dot / np.maximum(na * nc, eps)
+
+
+def similarity_accumulate(x_in, x_out) -> Tuple[float, int]:
+    """(sum of per-token cosines, number of tokens) for one layer on one batch."""
+    cos = token_cosine(x_in, x_out)
+    return float(np.sum(cos)), int(cos.size)
+
+
+def layer_similarity(sum_cos: float, n_tokens: int) -> float:
+    """s_i: the mean per-token cosine over the calibration tokens (Eq. 4)."""
+    return sum_cos / n_tokens
+
+
+# ---------------------------------------------------------------------------
+# Section 3.3, Eqs. 5-8: similarity -> layer-wise retention ratios
+# ---------------------------------------------------------------------------
+
+def retention_from_similarity(s: Sequence[float], t: float, tau: Optional[float],
+                              beta: float = 10.0, clip: str = "budget") -> np.ndarray:
+    """Retention ratio r_i per layer from similarities s_i.
+
+    Step 1 (Eq. 5): w~_i = exp((s_i - max s) / tau), w_i = w~_i / sum_j w~_j.
+    Step 2 (Eq. 6): z_i = beta * (mean_j w_j - w_i).
+    Step 3 (Eq. 7): r'_i = 0.05 + 0.9 * sigmoid(z_i).
+    Step 4 (Eq. 8): r_i = t L r'_i / sum_j r'_j, so sum_i r_i = t L.
+
+    tau=None is the ablation without the similarity temperature: uniform r = t.
+    clip="budget" caps r_i at 1 and hands the excess back to the other layers
+    in proportion to r'_j until no layer exceeds 1. clip="plain" only caps at 1.
+    clip="none" returns Eq. 8 as written.
+    """
+    s = f64(s)
+    L = s.size
+    if tau is None:
+        return np.full(L, float(t))
+    w_tilde = np.exp((s - np.max(s)) / tau)
+    w = w_tilde / np.sum(w_tilde)
+    z = beta * (np.mean(w) - w)
+    r_prime = 0.05 + 0.9 * (1.0 / (1.0 + np.exp(-z)))
+    r = (t * L / np.sum(r_prime)) * r_prime
+    if clip == "none":
+        return r
+    if clip == "plain":
+        return np.minimum(r, 1.0)
+    if clip != "budget":
+        raise ValueError(f"unknown clip mode {clip!r}")
+    capped = np.zeros(L, dtype=bool)
+    while np.any(r > 1.0):
+        capped |= r > 1.0
+        free = ~capped
+        budget = t * L - np.count_nonzero(capped)
+        r = np.where(capped, 1.0, 0.0)
+        if np.any(free):
+            r[free] = budget * r_prime[free] / np.sum(r_prime[free])
+    return r
+
+
+def k_from_retention(r: float, T: int, rounding: str = "floor") -> int:
+    """Kept tokens per sequence: K = floor(r T) (Section 3.4), with a 1e-6 guard.
+
+    rounding="ceil" gives ceil(r T - 1e-6) instead. The result is clamped to [0, T].
+    """
+    x = float(r) * T
+    if rounding == "floor":
+        k = math.floor(x + K_GUARD)
+    elif rounding == "ceil":
+        k = math.ceil(x - K_GUARD)
+    else:
+        raise ValueError(f"unknown rounding {rounding!r}")
+    return int(min(max(k, 0), T))
+
+
+# ---------------------------------------------------------------------------
+# Section 3.4: router, Top-K selection, masked selection / residual bypass
+# ---------------------------------------------------------------------------
+
+def router_scores(x, w1, b1, w2, b2: float = 0.0) -> np.ndarray:
+    """Token importance of a two-layer MLP router: w2 . ReLU(W1 x + b1) + b2.
+
+    x: [B, T, d]; w1: [d_r, d]; b1: [d_r] or None; w2: [d_r]. Returns [B, T].
+    """
+    x = f64(x)
+    hid = x @ f64(w1).T
+    if b1 is not None:
+        hid = hid + f64(b1)
+    hid = np.maximum(hid, 0.0)
+    return hid @ f64(w2) + float(b2)
+
+
+def topk_select(scores, k: int) -> np.ndarray:
+    """Top-K_i positions of each sequence, returned in ascending position order.
+
+    Order of preference: larger score first, then lower position. Returns
+    int64 [B, k]. Uses a lexicographic sort (library primitive) on
+    (-score, position); numpy treats -0.0 == +0.0 and sorts NaN last.
+    """
+    sc = f64(scores)
+    B, T = sc.shape
+    if not 0 <= k <= T:
+        raise ValueError("k out of range")
+    out = np.empty((B, k), dtype=np.int64)
+    pos = np.arange(T)
+    for b in range(B):
+        order = np.lexsort((pos, -sc[b]))
+        out[b] = np.sort(order[:k])
+    return out
+
+
+def gather_rows(x, idx) -> np.ndarray:
+    """x^ = the kept rows x[b, idx[b, j]] (masked selection as compaction)."""
+    x = f64(x)
+    idx = np.asarray(idx)
+    return np.stack([x[b, idx[b]] for b in range(x.shape[0])])
+
+
+def scatter_residual(x, delta, idx, dtype: Optional[str] = None) -> np.ndarray:
+    """y = x, with y[b, idx[b, j]] = x[b, idx[b, j]] + delta[b, j].
+
+    Skipped rows are untouched. With dtype given, the kept rows are rounded
+    to that storage format (bf16 or f32) after the exact add.
+    """
+    y = f64(x).copy()
+    delta = f64(delta)
+    idx = np.asarray(idx)
+    for b in range(y.shape[0]):
+        v = y[b, idx[b]] + delta[b]
+        y[b, idx[b]] = v if dtype is None else round_to(dtype, v)
+    return y
+
+
+# ---------------------------------------------------------------------------
+# Section 3.1, Eqs. 1-2: the decoder block run on the kept tokens
+# ---------------------------------------------------------------------------
+
+def layer_norm(x, w, b, eps: float) -> np.ndarray:
+    x = f64(x)
+    mu = np.mean(x, axis=-1, keepdims=True)
+    var = np.mean((x - mu) ** 2, axis=-1, keepdims=True)
+    y = (x - mu) / np.sqrt(var + eps) * f64(w)
+    return y if b is None else y + f64(b)
+
+
+def rms_norm(x, w, eps: float) -> np.ndarray:
+    x = f64(x)
+    ms = np.mean(x * x, axis=-1, keepdims=True)
+    return x / np.sqrt(ms + eps) * f64(w)
+
+
+def gelu(x) -> np.ndarray:
+    """Exact GELU: x * Phi(x), Phi the standard normal CDF."""
+    x = f64(x)
+    return 0.5 * x * (1.0 + erf(x / math.sqrt(2.0)))
+
+
+def silu(x) -> np.ndarray:
+    x = f64(x)
+    return x / (1.0 + np.exp(-x))
+
+
+def rope(x, pos, rotary_dims: int, theta: float) -> np.ndarray:
+    """Rotary position embedding (rotate-half form) on the first rotary_dims dims.
+
+    x: [n, H, hd]; pos: [n] original token positions. For i < R/2 the pair
+    (x_i, x_{i+R/2}) is rotated by the angle pos * theta^(-2i/R).
+    """
+    x = f64(x)
+    R = rotary_dims
+    half = R // 2
+    inv_freq = theta ** (-(2.0 * np.arange(half)) / R)
+    ang = np.asarray(pos, dtype=np.float64)[:, None] * inv_freq[None, :]
+    cos = np.cos(ang)[:, None, :]
+    sin = np.sin(ang)[:, None, :]
+    out = x.copy()
+    x1 = x[..., :half]
+    x2 = x[..., half:R]
+    out[..., :half] = x1 * cos - x2 * sin
+    out[..., half:R] = x2 * cos + x1 * sin
+    return out
+
+
+def causal_attention(q, k, v) -> np.ndarray:
+    """Eq. 1 with a causal mask over the given (kept) tokens.
+
+    q: [n, Hq, hd]; k, v: [n, Hkv, hd]; q head h reads kv head h // (Hq / Hkv).
+    Token j attends to tokens j' <= j. Returns [n, Hq * hd].
+    """
+    q, k, v = f64(q), f64(k), f64(v)
+    n, Hq, hd = q.shape
+    Hkv = k.shape[1]
+    group = Hq // Hkv
+    out = np.zeros((n, Hq, hd))
+    mask = np.triu(np.ones((n, n), dtype=bool), 1)
+    for h in range(Hq):
+        kh = h // group
+        s = (q[:, h, :] @ k[:, kh, :].T) / math.sqrt(hd)
+        s[mask] = -np.inf
+        s = s - np.max(s, axis=1, keepdims=True)
+        p = np.exp(s)
+        p = p / np.sum(p, axis=1, keepdims=True)
+        out[:, h, :] = p @ v[:, kh, :]
+    return out.reshape(n, Hq * hd)
+
+
+def block_delta(desc: Dict, W: Dict, xc, pos) -> np.ndarray:
+    """Residual update produced by one decoder block on one sequence's kept rows.
+
+    xc: [n, d] kept rows in position order; pos: [n] their original positions.
+    Returns delta [n, d] such that the block's output rows are xc + delta.
+    desc keys: block, n_heads, n_kv_heads, head_dim, d_ff, rotary_dims,
+    rope_theta, norm_eps.
+    """
+    xc = f64(xc)
+    n = xc.shape[0]
+    Hq, Hkv, hd = desc["n_heads"], desc["n_kv_heads"], desc["head_dim"]
+    f = desc["d_ff"]
+    eps = desc["norm_eps"]
+    neox = desc["block"] == NEOX
+
+    def linear(inp, wname, bname=None):
+        y = inp @ f64(W[wname]).T
+        b = W.get(bname) if bname else None
+        return y if b is None else y + f64(b)
+
+    a = layer_norm(xc, W["norm1_w"], W["norm1_b"], eps) if neox else rms_norm(xc, W["norm1_w"], eps)
+    qkv = linear(a, "w_qkv", "b_qkv")
+    q = qkv[:, :Hq * hd].reshape(n, Hq, hd)
+    k = qkv[:, Hq * hd:(Hq + Hkv) * hd].reshape(n, Hkv, hd)
+    v = qkv[:, (Hq + Hkv) * hd:].reshape(n, Hkv, hd)
+    q = rope(q, pos, desc["rotary_dims"], desc["rope_theta"])
+    k = rope(k, pos, desc["rotary_dims"], desc["rope_theta"])
+    attn = causal_attention(q, k, v)
+    ao = linear(attn, "w_o", "b_o")
+    if neox:
+        m = layer_norm(xc, W["norm2_w"], W["norm2_b"], eps)
+        mo = linear(gelu(linear(m, "w_up", "b_up")), "w_down", "b_down")
+    else:
+        h = xc + ao
+        m = rms_norm(h, W["norm2_w"], eps)
+        gu = linear(m, "w_up")
+        mo = linear(silu(gu[:, :f]) * gu[:, f:], "w_down")
+    return ao + mo
+
+
+# ---------------------------------------------------------------------------
+# Section 3.4: the sparse module (router -> Top-K -> block on kept rows -> bypass)
+# ---------------------------------------------------------------------------
+
+def routed_layer(desc: Dict, W: Dict, x, k: int, idx=None,
+                 out_dtype: Optional[str] = None) -> Dict[str, np.ndarray]:
+    """One sparse layer. Returns y, scores, idx and delta (kept rows, [B, k, d]).
+
+    idx given: teacher-forced selection (the router still scores every token).
+    out_dtype given: the kept rows of y are rounded to that storage format.
+    """
+    x = f64(x)
+    B, T, _ = x.shape
+    scores = router_scores(x, W["router_w1"], W["router_b1"], W["router_w2"],
+                           W.get("router_b2", 0.0))
+    if idx is None:
+        idx = topk_select(scores, k)
+    idx = np.asarray(idx, dtype=np.int64)
+    xc = gather_rows(x, idx)
+    delta = np.stack([block_delta(desc, W, xc[b], idx[b]) for b in range(B)]) if k > 0 \
+        else np.zeros((B, 0, x.shape[2]))
+    y = scatter_residual(x, delta, idx, out_dtype)
+    return {"y": y, "scores": scores, "idx": idx, "delta": delta}
+
+
+def dense_layer(desc: Dict, W: Dict, x) -> np.ndarray:
+    """The unmodified layer on every token: x + block(x) at positions 0..T-1."""
+    x = f64(x)
+    B, T, _ = x.shape
+    pos = np.arange(T)
+    return np.stack([x[b] + block_delta(desc, W, x[b], pos) for b in range(B)])
+
+
+def stack_forward(desc: Dict, Ws: List[Dict], x, ks: Sequence[int],
+                  out_dtype: Optional[str] = None) -> Tuple[np.ndarray, List[np.ndarray]]:
+    """Depth-sparse stack: x <- routed_layer_l(x, k_l) for l = 0..L-1.
+
+    Returns the final hidden states and the kept positions of every layer.
+    """
+    x = f64(x)
+    idxs = []
+    for W, k in zip(Ws, ks):
+        res = routed_layer(desc, W, x, int(k), out_dtype=out_dtype)
+        x = res["y"]
+        idxs.append(res["idx"])
+    return x, idxs
+
+
+def calibrate_similarity(desc: Dict, Ws: List[Dict], x) -> np.ndarray:
+    """Dense calibration pass: s_l for every layer (Eq. 4 on the dense stack)."""
+    x = f64(x)
+    s = []
+    for W in Ws:
+        y = dense_layer(desc, W, x)
+        tot, n = similarity_accumulate(x, y)
+        s.append(layer_similarity(tot, n))
+        x = y
+    return np.asarray(s)
