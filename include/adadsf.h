@@ -1,0 +1,266 @@
+/*
+ * adadsf.h - C ABI of the MI355X (gfx950) depth-sparse Transformer layer forward.
+ *
+ * The library computes AdaDSF's inference path ("Adaptive Depth Sparse
+ * Framework: Similarity-Driven Resource Allocation for Pre-Trained LLMs"):
+ *   - a per-layer cosine-similarity statistic between a layer's input and
+ *     output hidden states (Section 3.3, Eq. 4);
+ *   - retention ratios from those statistics (Section 3.3, Eqs. 5-8), and
+ *     K = floor(r * T) kept tokens per sequence (Section 3.4);
+ *   - a lightweight MLP router scoring every token and a per-sequence Top-K
+ *     (Section 3.4);
+ *   - the decoder block (Section 3.1, Eqs. 1-2) run on the kept tokens only,
+ *     with the skipped tokens passing through the residual path (Section 3.4).
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * Ownership. The caller owns every buffer. The library never allocates or
+ *   frees device memory. Scratch space is a caller-provided device
+ *   `workspace` of at least the size the matching *_workspace_size call returns.
+ * Streams. Device work is enqueued on the given hipStream_t (0 = the null
+ *   stream) and the call returns without waiting. The only exception is
+ *   dsf_sim_finalize, which waits for its copy.
+ * Errors. Every call returns a dsf_status and dsf_last_error() returns a
+ *   message for the calling thread. Arguments are checked on the host before
+ *   anything is enqueued, so an argument error (DSF_EINVAL, DSF_EUNSUPPORTED,
+ *   DSF_EWORKSPACE) launches nothing, writes no output and needs no GPU. Only
+ *   a HIP failure in the middle of a launch sequence (DSF_EHIP) can leave part
+ *   of the work enqueued.
+ * Positions. Caller-supplied positions (idx arguments) must lie in [0, T);
+ *   kernels clamp them into that range so that a bad value cannot address
+ *   memory outside the hidden-state rows (the result is then unspecified).
+ * Layouts. Row-major and contiguous. Hidden states are [B, T, d]. Kept
+ *   positions are int32 [B, k], strictly ascending within each sequence.
+ *   Weight matrices are [out, in] (the in dimension contiguous). Every device
+ *   pointer that is read or written as a vector must be 16-byte aligned.
+ * Types. dtype selects the element type of hidden states, weights and
+ *   activations: DSF_F32 (float) or DSF_BF16 (bfloat16 bits in uint16).
+ *   Router scores are float in both cases. Arithmetic is fp32 (bf16 MFMA with
+ *   fp32 accumulation on the bf16 path). The similarity statistic is fp64.
+ * Determinism. There are no floating-point atomics. Equal inputs on the same
+ *   device give bitwise-equal outputs.
+ */
+#ifndef ADADSF_H
+#define ADADSF_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DSF_VERSION 10000 /* major * 10000 + minor * 100 + patch */
+
+typedef enum dsf_status {
+  DSF_OK = 0,
+  DSF_EINVAL = 1,        /* null pointer, bad shape, k outside [0, T], misaligned pointer */
+  DSF_EUNSUPPORTED = 2,  /* dtype, head_dim, router width or d outside the supported set */
+  DSF_EWORKSPACE = 3,    /* workspace smaller than required */
+  DSF_EHIP = 4,          /* a HIP runtime call failed; the message holds hipGetErrorString */
+  DSF_ENODEVICE = 5      /* no usable GPU */
+} dsf_status;
+
+enum { DSF_F32 = 0, DSF_BF16 = 1 };
+
+/* Block templates (the model family's own pre-norm block).
+ * NEOX_PARALLEL: y = x + Attn(LN1(x)) + MLP_gelu(LN2(x)); LayerNorm with bias,
+ *   biases on every projection, rotary on the first rotary_dims of each head.
+ * QWEN_SEQ: h = x + Attn(RMS1(x)); y = h + MLP_swiglu(RMS2(h)); RMSNorm, bias on
+ *   the QKV projection only, grouped-query attention. */
+enum { DSF_BLOCK_NEOX_PARALLEL = 0, DSF_BLOCK_QWEN_SEQ = 1 };
+
+/* flags */
+enum { DSF_FLAG_DENSE = 1 }; /* run the unmodified layer on every token (no router, no Top-K) */
+
+/* clip modes for dsf_retention_from_similarity */
+enum { DSF_CLIP_NONE = 0, DSF_CLIP_PLAIN = 1, DSF_CLIP_BUDGET = 2 };
+/* rounding for dsf_k_from_retention */
+enum { DSF_ROUND_FLOOR = 0, DSF_ROUND_CEIL = 1 };
+
+/* Shape of one decoder layer. Every layer of a stack shares it. */
+typedef struct dsf_layer_desc {
+  int32_t block;        /* DSF_BLOCK_* */
+  int32_t d_model;      /* d, a multiple of 8 */
+  int32_t n_heads;      /* Hq */
+  int32_t n_kv_heads;   /* Hkv; Hq % Hkv == 0 (query head h reads kv head h / (Hq/Hkv)) */
+  int32_t head_dim;     /* hd in {32, 64, 128} */
+  int32_t d_ff;         /* f, a multiple of 64 */
+  int32_t rotary_dims;  /* R: even, 0 < R <= hd; rotate-half pairs (i, i + R/2) */
+  int32_t d_router;     /* router hidden width d_r in {16, 32, 48, 64} */
+  float norm_eps;       /* LayerNorm / RMSNorm epsilon */
+  float reserved;       /* must be 0 */
+  double rope_theta;    /* RoPE base; angle of pair i at position p is p * theta^(-2i/R) */
+} dsf_layer_desc;
+
+/* Device pointers of one layer's weights, all in the layer dtype.
+ * Nullable entries are marked; a null bias means zero. */
+typedef struct dsf_layer_weights {
+  const void* router_w1;  /* [d_r, d] */
+  const void* router_b1;  /* [d_r], nullable */
+  const void* router_w2;  /* [d_r] */
+  float router_b2;        /* scalar output bias */
+  float reserved;         /* must be 0 */
+  const void* norm1_w;    /* [d] */
+  const void* norm1_b;    /* [d], NEOX only (must be null for QWEN) */
+  const void* norm2_w;    /* [d] */
+  const void* norm2_b;    /* [d], NEOX only (must be null for QWEN) */
+  const void* w_qkv;      /* [(Hq + 2 Hkv) hd, d], rows in Q | K | V block order */
+  const void* b_qkv;      /* [(Hq + 2 Hkv) hd], nullable */
+  const void* w_o;        /* [d, Hq hd] */
+  const void* b_o;        /* [d], nullable (NEOX) */
+  const void* w_up;       /* NEOX: [f, d]; QWEN: [2f, d], gate rows then up rows */
+  const void* b_up;       /* [f], nullable (NEOX) */
+  const void* w_down;     /* [d, f] */
+  const void* b_down;     /* [d], nullable (NEOX) */
+} dsf_layer_weights;
+
+/* ---------------------------------------------------------------- library */
+
+int dsf_version(void);
+/* Message of the calling thread's last failed call ("" if none). Valid until
+ * that thread's next call into the library. */
+const char* dsf_last_error(void);
+
+/* ------------------------------------------- similarity statistic (Eq. 4) */
+
+/* Workspace bytes dsf_sim_stats needs for n_tokens rows. */
+size_t dsf_sim_workspace_size(int64_t n_tokens);
+
+/* Section 3.3, Eq. 4. For every token row a = x_in[t, :], c = x_out[t, :]
+ * (t < n_tokens, rows of d elements):
+ *   cos_t = <a, c> / max(|a| |c|, 1e-8)   (products and sums in fp64),
+ * then accum[0] += sum_t cos_t and accum[1] += n_tokens (fp64 device memory,
+ * which the caller zeroes once before a calibration pass). per_token_cos
+ * (nullable, device float [n_tokens]) receives cos_t. The sum is formed in a
+ * fixed order, so the result is deterministic. n_tokens == 0 is a no-op. */
+int dsf_sim_stats(const void* x_in, const void* x_out, int dtype, int64_t n_tokens, int d,
+                  float* per_token_cos, double* accum, void* workspace, size_t workspace_bytes,
+                  hipStream_t stream);
+
+/* s_host[l] = accum[l][0] / accum[l][1] for l < L (Eq. 4 averaged over the
+ * calibration tokens). accum_dev is device double [L][2], s_host host double
+ * [L]. Waits for the copy on `stream`. A layer with a zero count gives NaN. */
+int dsf_sim_finalize(const double* accum_dev, int L, double* s_host, hipStream_t stream);
+
+/* ------------------------------------- retention allocation (host, fp64) */
+
+/* Section 3.3, Eqs. 5-8, on the host in fp64:
+ *   w~_i = exp((s_i - max s) / tau), w_i = w~_i / sum w~;
+ *   z_i = beta (mean(w) - w_i);  r'_i = 0.05 + 0.9 / (1 + exp(-z_i));
+ *   r_i = t L r'_i / sum r'.
+ * tau <= 0 selects the ablation without temperature: r_i = t for every layer.
+ * clip_mode: DSF_CLIP_NONE returns Eq. 8 as is (r_i may exceed 1);
+ * DSF_CLIP_PLAIN caps at 1; DSF_CLIP_BUDGET caps at 1 and hands the excess to
+ * the uncapped layers in proportion to r'_i, repeating until none exceeds 1,
+ * so that sum r_i = t L still holds. Requires L >= 1, 0 < t <= 1, beta > 0,
+ * finite s. r_out is host double [L]. */
+int dsf_retention_from_similarity(const double* s, int L, double t, double tau, double beta,
+                                  int clip_mode, double* r_out);
+
+/* Section 3.4: K = floor(r T), evaluated as floor(r T + 1e-6) so that fp64
+ * representation error cannot drop a token (DSF_ROUND_FLOOR), or
+ * ceil(r T - 1e-6) (DSF_ROUND_CEIL); clamped to [0, T]. Returns k >= 0, or -1
+ * on a bad argument (r not finite, T < 0, unknown rounding). Host only. */
+int dsf_k_from_retention(double r, int T, int rounding);
+
+/* ------------------------------------------------ routing (Section 3.4) */
+
+/* Router scores: score[t] = sum_j w2[j] * ReLU(sum_i W1[j, i] x[t, i] + b1[j]) + b2
+ * for the n_tokens rows of x (raw residual-stream rows, [n_tokens, d]).
+ * W1 [d_r, d], b1 [d_r] (nullable), w2 [d_r] in dtype; scores device float
+ * [n_tokens]. */
+int dsf_router_score(const void* x, int dtype, int64_t n_tokens, int d, int d_r,
+                     const void* w1, const void* b1, const void* w2, float b2,
+                     float* scores, hipStream_t stream);
+
+/* Top-K_i per sequence. For each of the B sequences of T float scores,
+ * writes the k positions with the largest scores to idx[b, 0..k) in ascending
+ * position order. A larger score is preferred; equal scores prefer the lower
+ * position; -0.0 equals +0.0; NaN ranks below every number. The result is
+ * unique. scores device float [B, T], idx device int32 [B, k]. */
+int dsf_topk_select(const float* scores, int B, int T, int k, int32_t* idx, hipStream_t stream);
+
+/* Masked selection as compaction: out[b, j, :] = x[b, idx[b, j], :].
+ * x [B, T, d], out [B, k, d] in dtype; idx int32 [B, k] with values in [0, T). */
+int dsf_gather_rows(const void* x, int dtype, int B, int T, int d, const int32_t* idx, int k,
+                    void* out, hipStream_t stream);
+
+/* Residual bypass: x[b, idx[b, j], :] += delta[b, j, :] in place, the add in
+ * fp32 and rounded once to dtype (round to nearest even). Skipped rows are not
+ * touched. idx must hold distinct positions per sequence. */
+int dsf_scatter_residual(void* x, const void* delta, int dtype, int B, int T, int d,
+                         const int32_t* idx, int k, hipStream_t stream);
+
+/* ----------------------------------- attention over kept tokens (Eq. 1) */
+
+/* Eq. 1 with a causal mask over n kept tokens per sequence:
+ *   out[b, j, h*hd:(h+1)*hd] = sum_{j' <= j} softmax_j'(q_j . k_j' / sqrt(hd)) v_j'
+ * q [B, Hq, n, hd], k and v [B, Hkv, n, hd], out [B, n, Hq*hd], all dtype.
+ * Query head h reads kv head h / (Hq / Hkv). Rotary embedding, if any, must
+ * already be applied to q and k. hd in {32, 64, 128}. */
+int dsf_attention_forward(const void* q, const void* k, const void* v, int dtype, int B, int Hq,
+                          int Hkv, int n, int hd, void* out, hipStream_t stream);
+
+/* ----------------------------------------- the sparse layer and the stack */
+
+/* Workspace bytes that dsf_sparse_block_forward / dsf_stack_forward need for
+ * batch B, sequence length T and at most k_max kept tokens per sequence
+ * (k_max = T for DSF_FLAG_DENSE). with_similarity != 0 adds room to keep each
+ * layer's input for the similarity statistic. Returns 0 on a bad argument. */
+size_t dsf_workspace_size(const dsf_layer_desc* desc, int dtype, int B, int T, int k_max,
+                          int with_similarity);
+
+/* Section 3.4: one sparse layer, in place on x [B, T, d].
+ *   1. scores = router(x) for every token (skipped with DSF_FLAG_DENSE);
+ *   2. idx = Top-K(scores, k) per sequence, or idx_in if given (teacher forcing);
+ *   3. the block of Eqs. 1-2 runs on the kept rows only, at their original
+ *      positions (RoPE angle uses idx), with kept tokens attending causally to
+ *      kept tokens;
+ *   4. x[b, idx[b, j]] = x[b, idx[b, j]] + delta[b, j]; skipped rows unchanged.
+ * k in [0, T]; k == 0 leaves x untouched and launches nothing. With
+ * DSF_FLAG_DENSE, k must equal T and every token is processed at positions
+ * 0..T-1 (the unmodified layer). scores_out (device float [B, T]) and idx_out
+ * (device int32 [B, k]) are nullable copies of the routing decision; idx_in
+ * (nullable, device int32 [B, k], strictly ascending per sequence) replaces
+ * the router's choice. */
+int dsf_sparse_block_forward(const dsf_layer_desc* desc, const dsf_layer_weights* weights,
+                             int dtype, void* x, int B, int T, int k, int flags,
+                             float* scores_out, int32_t* idx_out, const int32_t* idx_in,
+                             void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* The depth-sparse stack: x <- layer_l(x, k[l]) for l = 0..L-1 (Section 3.4),
+ * with k a host int array [L] (fixed per layer, so the loop never waits on
+ * the GPU). weights is a host array [L] of device-pointer sets. With
+ * sim_accum (nullable, device double [L][2], zeroed by the caller) each
+ * layer's input is kept and dsf_sim_stats(input, output) accumulates into
+ * sim_accum[l]: run with DSF_FLAG_DENSE this is the calibration pass of Eq. 4. */
+int dsf_stack_forward(const dsf_layer_desc* desc, const dsf_layer_weights* weights, int L,
+                      int dtype, const int* k, void* x, int B, int T, int flags,
+                      double* sim_accum, void* workspace, size_t workspace_bytes,
+                      hipStream_t stream);
+
+/* ------------------------------------------------------- kernel timing */
+
+/* Per-kernel timing with HIP events recorded around each launch on the
+ * launch's own stream. Used by the benchmark to attribute time to kernels.
+ * dsf_timing_enable(n, mask) arms up to n launch records for the kernel
+ * classes whose bit (1 << DSF_KIND_*) is set in mask; n == 0 disarms and
+ * frees the events. dsf_timing_read waits for the recorded events and
+ * returns, for the kernel class `kind`, the number of launches and their
+ * summed duration in milliseconds, then clears that class. */
+enum {
+  DSF_KIND_SIM = 0, DSF_KIND_ROUTER = 1, DSF_KIND_TOPK = 2, DSF_KIND_NORM = 3,
+  DSF_KIND_GEMM_QKV = 4, DSF_KIND_ATTN = 5, DSF_KIND_GEMM_O = 6, DSF_KIND_GEMM_UP = 7,
+  DSF_KIND_GEMM_DOWN = 8, DSF_KIND_GATHER = 9, DSF_KIND_SCATTER = 10, DSF_KIND_OTHER = 11,
+  DSF_KIND_COUNT = 12
+};
+int dsf_timing_enable(int max_records, uint32_t kind_mask);
+int dsf_timing_read(int kind, int* launches, double* total_ms);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ADADSF_H */

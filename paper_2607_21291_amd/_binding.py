@@ -1,0 +1,266 @@
+"""ctypes binding of libadadsf.so: the C ABI in include/adadsf.h, one Python
+function per entry point, same names without the ``dsf_`` prefix.
+
+Argument marshalling only. Tensors are torch tensors on the GPU (torch owns
+device memory and streams); every computation runs in the library's HIP
+kernels. A missing library raises immediately: there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import torch  # loads the HIP runtime that the library binds to
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libadadsf.so")
+
+F32, BF16 = 0, 1
+BLOCK_NEOX_PARALLEL, BLOCK_QWEN_SEQ = 0, 1
+FLAG_DENSE = 1
+CLIP = {"none": 0, "plain": 1, "budget": 2}
+ROUNDING = {"floor": 0, "ceil": 1}
+KINDS = ["sim", "router", "topk", "norm", "gemm_qkv", "attn", "gemm_o", "gemm_up", "gemm_down",
+         "gather", "scatter", "other"]
+
+STATUS = {0: "DSF_OK", 1: "DSF_EINVAL", 2: "DSF_EUNSUPPORTED", 3: "DSF_EWORKSPACE", 4: "DSF_EHIP",
+          5: "DSF_ENODEVICE"}
+
+EXPORTS = [
+    "dsf_version", "dsf_last_error", "dsf_sim_workspace_size", "dsf_sim_stats", "dsf_sim_finalize",
+    "dsf_retention_from_similarity", "dsf_k_from_retention", "dsf_router_score", "dsf_topk_select",
+    "dsf_gather_rows", "dsf_scatter_residual", "dsf_attention_forward", "dsf_workspace_size",
+    "dsf_sparse_block_forward", "dsf_stack_forward", "dsf_timing_enable", "dsf_timing_read",
+]
+
+
+class DsfError(RuntimeError):
+    def __init__(self, fn: str, code: int, msg: str):
+        super().__init__(f"{fn} -> {STATUS.get(code, code)}: {msg}")
+        self.code = code
+
+
+class LayerDesc(ctypes.Structure):
+    _fields_ = [("block", ctypes.c_int32), ("d_model", ctypes.c_int32), ("n_heads", ctypes.c_int32),
+                ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32), ("d_ff", ctypes.c_int32),
+                ("rotary_dims", ctypes.c_int32), ("d_router", ctypes.c_int32), ("norm_eps", ctypes.c_float),
+                ("reserved", ctypes.c_float), ("rope_theta", ctypes.c_double)]
+
+
+_WEIGHT_FIELDS = ["router_w1", "router_b1", "router_w2", "router_b2", "reserved", "norm1_w", "norm1_b",
+                  "norm2_w", "norm2_b", "w_qkv", "b_qkv", "w_o", "b_o", "w_up", "b_up", "w_down", "b_down"]
+
+
+class LayerWeights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_float if n in ("router_b2", "reserved") else ctypes.c_void_p)
+                for n in _WEIGHT_FIELDS]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                           "(python -m paper_2607_21291_amd.build_lib)")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i32, i64, sz, f32, f64 = (ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_size_t,
+                                  ctypes.c_float, ctypes.c_double)
+    sig = {
+        "dsf_version": ([], i32),
+        "dsf_last_error": ([], ctypes.c_char_p),
+        "dsf_sim_workspace_size": ([i64], sz),
+        "dsf_sim_stats": ([vp, vp, i32, i64, i32, vp, vp, vp, sz, vp], i32),
+        "dsf_sim_finalize": ([vp, i32, vp, vp], i32),
+        "dsf_retention_from_similarity": ([vp, i32, f64, f64, f64, i32, vp], i32),
+        "dsf_k_from_retention": ([f64, i32, i32], i32),
+        "dsf_router_score": ([vp, i32, i64, i32, i32, vp, vp, vp, f32, vp, vp], i32),
+        "dsf_topk_select": ([vp, i32, i32, i32, vp, vp], i32),
+        "dsf_gather_rows": ([vp, i32, i32, i32, i32, vp, i32, vp, vp], i32),
+        "dsf_scatter_residual": ([vp, vp, i32, i32, i32, i32, vp, i32, vp], i32),
+        "dsf_attention_forward": ([vp, vp, vp, i32, i32, i32, i32, i32, i32, vp, vp], i32),
+        "dsf_workspace_size": ([vp, i32, i32, i32, i32, i32], sz),
+        "dsf_sparse_block_forward": ([vp, vp, i32, vp, i32, i32, i32, i32, vp, vp, vp, vp, sz, vp], i32),
+        "dsf_stack_forward": ([vp, vp, i32, i32, vp, vp, i32, i32, i32, vp, vp, sz, vp], i32),
+        "dsf_timing_enable": ([i32, ctypes.c_uint32], i32),
+        "dsf_timing_read": ([i32, vp, vp], i32),
+    }
+    for name, (args, res) in sig.items():
+        fn = getattr(L, name)
+        fn.argtypes = args
+        fn.restype = res
+    _lib = L
+    return L
+
+
+def _check(fn: str, rc: int):
+    if rc != 0:
+        raise DsfError(fn, rc, lib().dsf_last_error().decode())
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    if t is None:
+        return None
+    if not t.is_contiguous():
+        raise ValueError("tensors passed to the library must be contiguous")
+    return t.data_ptr()
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return F32
+    if t.dtype == torch.bfloat16:
+        return BF16
+    raise ValueError(f"unsupported dtype {t.dtype}")
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream
+
+
+# --------------------------------------------------------------- entry points
+
+def version() -> int:
+    return lib().dsf_version()
+
+
+def last_error() -> str:
+    return lib().dsf_last_error().decode()
+
+
+def sim_workspace_size(n_tokens: int) -> int:
+    return lib().dsf_sim_workspace_size(n_tokens)
+
+
+def sim_stats(x_in, x_out, accum, per_token_cos=None, workspace=None, stream=None):
+    d = x_in.shape[-1]
+    n = x_in.numel() // d
+    if workspace is None:
+        workspace = torch.empty(max(sim_workspace_size(n), 256), dtype=torch.uint8, device=x_in.device)
+    _check("dsf_sim_stats", lib().dsf_sim_stats(_ptr(x_in), _ptr(x_out), _dtype_code(x_in), n, d,
+                                                _ptr(per_token_cos), _ptr(accum), _ptr(workspace),
+                                                workspace.numel(), _stream(stream)))
+
+
+def sim_finalize(accum, stream=None):
+    L = accum.numel() // 2
+    out = (ctypes.c_double * max(L, 1))()
+    _check("dsf_sim_finalize", lib().dsf_sim_finalize(_ptr(accum), L, ctypes.addressof(out), _stream(stream)))
+    return [out[i] for i in range(L)]
+
+
+def retention_from_similarity(s: Sequence[float], t: float, tau: Optional[float], beta: float = 10.0,
+                              clip: str = "budget"):
+    L = len(s)
+    sin = (ctypes.c_double * max(L, 1))(*s)
+    rout = (ctypes.c_double * max(L, 1))()
+    _check("dsf_retention_from_similarity",
+           lib().dsf_retention_from_similarity(ctypes.addressof(sin), L, t, -1.0 if tau is None else tau, beta,
+                                               CLIP[clip], ctypes.addressof(rout)))
+    return [rout[i] for i in range(L)]
+
+
+def k_from_retention(r: float, T: int, rounding: str = "floor") -> int:
+    k = lib().dsf_k_from_retention(r, T, ROUNDING[rounding])
+    if k < 0:
+        raise DsfError("dsf_k_from_retention", 1, last_error())
+    return k
+
+
+def router_score(x, w1, b1, w2, b2: float, scores, stream=None):
+    d = x.shape[-1]
+    _check("dsf_router_score", lib().dsf_router_score(_ptr(x), _dtype_code(x), x.numel() // d, d, w1.shape[0],
+                                                      _ptr(w1), _ptr(b1), _ptr(w2), float(b2), _ptr(scores),
+                                                      _stream(stream)))
+
+
+def topk_select(scores, k: int, idx, stream=None):
+    B, T = scores.shape
+    _check("dsf_topk_select", lib().dsf_topk_select(_ptr(scores), B, T, k, _ptr(idx), _stream(stream)))
+
+
+def gather_rows(x, idx, out, stream=None):
+    B, T, d = x.shape
+    _check("dsf_gather_rows", lib().dsf_gather_rows(_ptr(x), _dtype_code(x), B, T, d, _ptr(idx), idx.shape[1],
+                                                    _ptr(out), _stream(stream)))
+
+
+def scatter_residual(x, delta, idx, stream=None):
+    B, T, d = x.shape
+    _check("dsf_scatter_residual", lib().dsf_scatter_residual(_ptr(x), _ptr(delta), _dtype_code(x), B, T, d,
+                                                              _ptr(idx), idx.shape[1], _stream(stream)))
+
+
+def attention_forward(q, k, v, out, stream=None):
+    B, Hq, n, hd = q.shape
+    _check("dsf_attention_forward", lib().dsf_attention_forward(_ptr(q), _ptr(k), _ptr(v), _dtype_code(q), B, Hq,
+                                                                k.shape[1], n, hd, _ptr(out), _stream(stream)))
+
+
+def workspace_size(desc: LayerDesc, dtype: int, B: int, T: int, k_max: int, with_similarity: bool = False) -> int:
+    return lib().dsf_workspace_size(ctypes.addressof(desc), dtype, B, T, k_max, int(with_similarity))
+
+
+def sparse_block_forward(desc: LayerDesc, weights: LayerWeights, x, k: int, workspace, flags: int = 0,
+                         scores_out=None, idx_out=None, idx_in=None, stream=None):
+    B, T, _ = x.shape
+    _check("dsf_sparse_block_forward",
+           lib().dsf_sparse_block_forward(ctypes.addressof(desc), ctypes.addressof(weights), _dtype_code(x),
+                                          _ptr(x), B, T, k, flags, _ptr(scores_out), _ptr(idx_out), _ptr(idx_in),
+                                          _ptr(workspace), workspace.numel(), _stream(stream)))
+
+
+def stack_forward(desc: LayerDesc, weights: Sequence[LayerWeights], ks: Sequence[int], x, workspace,
+                  flags: int = 0, sim_accum=None, stream=None):
+    B, T, _ = x.shape
+    L = len(weights)
+    arr = (LayerWeights * max(L, 1))(*weights)
+    karr = (ctypes.c_int * max(L, 1))(*[int(k) for k in ks])
+    _check("dsf_stack_forward",
+           lib().dsf_stack_forward(ctypes.addressof(desc), ctypes.addressof(arr), L, _dtype_code(x),
+                                   ctypes.addressof(karr), _ptr(x), B, T, flags, _ptr(sim_accum), _ptr(workspace),
+                                   workspace.numel(), _stream(stream)))
+
+
+def timing_enable(max_records: int, kinds: Optional[Sequence[str]] = None):
+    """Arm per-launch event timing for the named kernel classes (all if None)."""
+    mask = (1 << len(KINDS)) - 1 if kinds is None else sum(1 << KINDS.index(k) for k in kinds)
+    _check("dsf_timing_enable", lib().dsf_timing_enable(max_records, mask))
+
+
+def timing_read(kind: str):
+    n = ctypes.c_int(0)
+    ms = ctypes.c_double(0.0)
+    _check("dsf_timing_read", lib().dsf_timing_read(KINDS.index(kind), ctypes.addressof(n), ctypes.addressof(ms)))
+    return n.value, ms.value
+
+
+# ------------------------------------------------------ marshalling helpers
+
+def make_desc(block: str, d_model: int, n_heads: int, n_kv_heads: int, head_dim: int, d_ff: int,
+              rotary_dims: int, d_router: int, norm_eps: float, rope_theta: float) -> LayerDesc:
+    code = {"neox_parallel": BLOCK_NEOX_PARALLEL, "qwen_seq": BLOCK_QWEN_SEQ}[block]
+    return LayerDesc(code, d_model, n_heads, n_kv_heads, head_dim, d_ff, rotary_dims, d_router, norm_eps, 0.0,
+                     rope_theta)
+
+
+class DeviceLayer:
+    """Keeps one layer's device tensors alive and exposes them as LayerWeights."""
+
+    def __init__(self, tensors: dict, device):
+        self.tensors = {}
+        for name in _WEIGHT_FIELDS:
+            if name in ("router_b2", "reserved"):
+                continue
+            t = tensors.get(name)
+            self.tensors[name] = None if t is None else t.to(device).contiguous()
+        self.router_b2 = float(tensors.get("router_b2", 0.0))
+        kw = {n: _ptr(t) for n, t in self.tensors.items()}
+        self.weights = LayerWeights(router_b2=self.router_b2, reserved=0.0, **kw)

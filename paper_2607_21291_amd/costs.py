@@ -1,0 +1,63 @@
+"""Analytic work model of the depth-sparse stack: the FLOPs and bytes the
+method must compute or move, used for roofline fractions and the FLOP ratio.
+
+Only the layer stack is counted (no embedding, no LM head): the normalized
+FLOPs of the paper's tables (sparse over dense) are layer-stack savings.
+A layer keeping k of T tokens per sequence costs
+  projections: 2 B k [d (Hq + 2 Hkv) hd + Hq hd d + m d f], m = 2 (GELU) or 3 (SwiGLU);
+  attention:   4 hd Hq B k (k + 1) / 2 (causal, diagonal included);
+  router:      2 B T (d d_r + d_r) (sparse layers only).
+"""
+from __future__ import annotations
+
+from typing import Sequence
+
+NEOX = "neox_parallel"
+
+
+def proj_flops(w, B: int, k: int) -> float:
+    m = 2 if w.block == NEOX else 3
+    d, hd = w.d_model, w.head_dim
+    per_token = d * (w.n_heads + 2 * w.n_kv_heads) * hd + w.n_heads * hd * d + m * d * w.d_ff
+    return 2.0 * B * k * per_token
+
+
+def attn_flops(w, B: int, k: int) -> float:
+    return 4.0 * w.head_dim * w.n_heads * B * k * (k + 1) / 2.0
+
+
+def router_flops(w, B: int, T: int) -> float:
+    return 2.0 * B * T * (w.d_model * w.d_router + w.d_router)
+
+
+def layer_flops(w, B: int, T: int, k: int, sparse: bool = True) -> float:
+    f = proj_flops(w, B, k) + attn_flops(w, B, k)
+    return f + (router_flops(w, B, T) if sparse else 0.0)
+
+
+def stack_flops(w, B: int, T: int, ks: Sequence[int], sparse: bool = True) -> float:
+    return sum(layer_flops(w, B, T, k, sparse) for k in ks)
+
+
+def normalized_flops(w, T: int, ks: Sequence[int]) -> float:
+    """Sparse stack FLOPs over dense stack FLOPs (the paper's cost metric)."""
+    return stack_flops(w, 1, T, ks, True) / stack_flops(w, 1, T, [T] * len(ks), False)
+
+
+# ---- per-launch algorithmic work of the individual kernels (one layer) ----
+
+def gemm_down_flops(w, B: int, k: int) -> float:
+    """The last GEMM of a layer: [attn | act] . [W_o | W_down]^T (NeoX, fused) or act . W_down^T (Qwen)."""
+    d, f = w.d_model, w.d_ff
+    K = w.n_heads * w.head_dim + f if w.block == NEOX else f
+    return 2.0 * B * k * d * K
+
+
+def router_bytes(w, B: int, T: int) -> float:
+    eb = 4 if w.dtype == "f32" else 2
+    return eb * B * T * w.d_model + 4.0 * B * T
+
+
+def sim_bytes(w, B: int, T: int) -> float:
+    eb = 4 if w.dtype == "f32" else 2
+    return 2.0 * eb * B * T * w.d_model

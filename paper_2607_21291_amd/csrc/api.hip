@@ -1,0 +1,655 @@
+// C ABI of the depth-sparse layer library: argument checks, workspace plan,
+// the launch sequence of one sparse layer and of the stack, the host-side
+// retention allocation (Eqs. 5-8), and per-launch event timing.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "adadsf.h"
+#include "dsf_internal.h"
+
+using namespace dsf;
+
+// ------------------------------------------------------------------ errors
+
+static thread_local std::string g_err;
+
+static int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+#define DSF_CHECK(cond, code, ...) \
+  do {                             \
+    if (!(cond)) return fail(code, __VA_ARGS__); \
+  } while (0)
+
+#define DSF_HIP(expr)                                                              \
+  do {                                                                             \
+    hipError_t e_ = (expr);                                                        \
+    if (e_ != hipSuccess) return fail(DSF_EHIP, "%s: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+extern "C" int dsf_version(void) { return DSF_VERSION; }
+extern "C" const char* dsf_last_error(void) { return g_err.c_str(); }
+
+static bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// The current device must exist and be gfx950 (the only code object built).
+static int check_device() {
+  int n = 0;
+  if (hipGetDeviceCount(&n) != hipSuccess || n <= 0) {
+    (void)hipGetLastError();
+    return fail(DSF_ENODEVICE, "no GPU is visible");
+  }
+  int dev = 0;
+  DSF_HIP(hipGetDevice(&dev));
+  static std::mutex mu;
+  static std::vector<int> arch_ok;  // -1 unknown, 0 no, 1 yes
+  std::lock_guard<std::mutex> lock(mu);
+  if (int(arch_ok.size()) < n) arch_ok.resize(n, -1);
+  if (arch_ok[dev] < 0) {
+    hipDeviceProp_t prop;
+    DSF_HIP(hipGetDeviceProperties(&prop, dev));
+    arch_ok[dev] = std::strncmp(prop.gcnArchName, "gfx950", 6) == 0 ? 1 : 0;
+  }
+  if (!arch_ok[dev]) return fail(DSF_EUNSUPPORTED, "device %d is not gfx950 (MI355X)", dev);
+  return DSF_OK;
+}
+
+static int check_dtype(int dtype) {
+  DSF_CHECK(dtype == DSF_F32 || dtype == DSF_BF16, DSF_EUNSUPPORTED, "dtype %d is not DSF_F32 or DSF_BF16", dtype);
+  return DSF_OK;
+}
+
+static size_t elem_bytes(int dtype) { return dtype == DSF_BF16 ? 2 : 4; }
+
+// --------------------------------------------------------------- timing
+
+namespace {
+struct TimingRec {
+  int kind;
+  hipEvent_t start, stop;
+};
+std::mutex g_tmu;
+std::vector<TimingRec> g_recs;
+size_t g_used = 0;
+long g_open = -1;
+uint32_t g_mask = 0;
+}  // namespace
+
+namespace dsf {
+void timing_begin(int kind, hipStream_t s) {
+  std::lock_guard<std::mutex> lock(g_tmu);
+  if (g_used >= g_recs.size() || g_open >= 0 || !((g_mask >> kind) & 1u)) return;
+  g_recs[g_used].kind = kind;
+  if (hipEventRecord(g_recs[g_used].start, s) == hipSuccess) g_open = long(g_used);
+}
+void timing_end(int kind, hipStream_t s) {
+  std::lock_guard<std::mutex> lock(g_tmu);
+  if (g_open < 0 || g_recs[g_open].kind != kind) return;
+  if (hipEventRecord(g_recs[g_open].stop, s) == hipSuccess) ++g_used;
+  g_open = -1;
+}
+}  // namespace dsf
+
+extern "C" int dsf_timing_enable(int max_records, uint32_t kind_mask) {
+  DSF_CHECK(max_records >= 0, DSF_EINVAL, "max_records < 0");
+  std::lock_guard<std::mutex> lock(g_tmu);
+  for (auto& r : g_recs) {
+    (void)hipEventDestroy(r.start);
+    (void)hipEventDestroy(r.stop);
+  }
+  g_recs.clear();
+  g_used = 0;
+  g_open = -1;
+  g_mask = kind_mask;
+  if (max_records == 0) return DSF_OK;
+  int rc = check_device();
+  if (rc) return rc;
+  g_recs.resize(size_t(max_records));
+  for (auto& r : g_recs) {
+    r.kind = -1;
+    DSF_HIP(hipEventCreate(&r.start));
+    DSF_HIP(hipEventCreate(&r.stop));
+  }
+  return DSF_OK;
+}
+
+extern "C" int dsf_timing_read(int kind, int* launches, double* total_ms) {
+  DSF_CHECK(launches && total_ms, DSF_EINVAL, "null output pointer");
+  DSF_CHECK(kind >= 0 && kind < DSF_KIND_COUNT, DSF_EINVAL, "unknown kernel kind %d", kind);
+  std::lock_guard<std::mutex> lock(g_tmu);
+  int cnt = 0;
+  double tot = 0.0;
+  for (size_t i = 0; i < g_used; ++i) {
+    if (g_recs[i].kind != kind) continue;
+    DSF_HIP(hipEventSynchronize(g_recs[i].stop));
+    float ms = 0.f;
+    DSF_HIP(hipEventElapsedTime(&ms, g_recs[i].start, g_recs[i].stop));
+    tot += ms;
+    ++cnt;
+    g_recs[i].kind = -1;
+  }
+  *launches = cnt;
+  *total_ms = tot;
+  return DSF_OK;
+}
+
+// ---------------------------------------------- retention allocation, host
+
+extern "C" int dsf_retention_from_similarity(const double* s, int L, double t, double tau, double beta,
+                                             int clip_mode, double* r_out) {
+  DSF_CHECK(s && r_out, DSF_EINVAL, "null pointer");
+  DSF_CHECK(L >= 1, DSF_EINVAL, "L must be >= 1");
+  DSF_CHECK(t > 0.0 && t <= 1.0, DSF_EINVAL, "target retention t must be in (0, 1]");
+  DSF_CHECK(beta > 0.0 && std::isfinite(beta), DSF_EINVAL, "beta must be positive");
+  DSF_CHECK(clip_mode >= DSF_CLIP_NONE && clip_mode <= DSF_CLIP_BUDGET, DSF_EINVAL, "unknown clip mode");
+  for (int i = 0; i < L; ++i) DSF_CHECK(std::isfinite(s[i]), DSF_EINVAL, "s[%d] is not finite", i);
+  if (!(tau > 0.0)) {  // no temperature: uniform allocation
+    for (int i = 0; i < L; ++i) r_out[i] = t;
+    return DSF_OK;
+  }
+  std::vector<double> w(L), rp(L), r(L);
+  double smax = s[0];
+  for (int i = 1; i < L; ++i) smax = s[i] > smax ? s[i] : smax;
+  double wsum = 0.0;
+  for (int i = 0; i < L; ++i) {  // Eq. 5
+    w[i] = std::exp((s[i] - smax) / tau);
+    wsum += w[i];
+  }
+  double wmean = 0.0;
+  for (int i = 0; i < L; ++i) {
+    w[i] /= wsum;
+    wmean += w[i];
+  }
+  wmean /= L;
+  double rpsum = 0.0;
+  for (int i = 0; i < L; ++i) {
+    const double z = beta * (wmean - w[i]);        // Eq. 6
+    rp[i] = 0.05 + 0.9 / (1.0 + std::exp(-z));     // Eq. 7
+    rpsum += rp[i];
+  }
+  for (int i = 0; i < L; ++i) r[i] = t * L / rpsum * rp[i];  // Eq. 8
+  if (clip_mode == DSF_CLIP_PLAIN) {
+    for (int i = 0; i < L; ++i) r[i] = r[i] > 1.0 ? 1.0 : r[i];
+  } else if (clip_mode == DSF_CLIP_BUDGET) {
+    std::vector<char> capped(L, 0);
+    for (;;) {
+      bool over = false;
+      for (int i = 0; i < L; ++i)
+        if (r[i] > 1.0) {
+          capped[i] = 1;
+          over = true;
+        }
+      if (!over) break;
+      int ncap = 0;
+      double free_rp = 0.0;
+      for (int i = 0; i < L; ++i) {
+        if (capped[i]) ++ncap;
+        else free_rp += rp[i];
+      }
+      const double budget = t * L - ncap;
+      for (int i = 0; i < L; ++i) r[i] = capped[i] ? 1.0 : budget * rp[i] / free_rp;
+    }
+  }
+  for (int i = 0; i < L; ++i) r_out[i] = r[i];
+  return DSF_OK;
+}
+
+extern "C" int dsf_k_from_retention(double r, int T, int rounding) {
+  if (!std::isfinite(r) || T < 0 || (rounding != DSF_ROUND_FLOOR && rounding != DSF_ROUND_CEIL)) {
+    fail(DSF_EINVAL, "bad argument to dsf_k_from_retention");
+    return -1;
+  }
+  const double x = r * double(T);
+  double k = rounding == DSF_ROUND_FLOOR ? std::floor(x + 1e-6) : std::ceil(x - 1e-6);
+  if (k < 0) k = 0;
+  if (k > T) k = T;
+  return int(k);
+}
+
+// ------------------------------------------------------ similarity, Eq. 4
+
+extern "C" size_t dsf_sim_workspace_size(int64_t n_tokens) {
+  if (n_tokens < 0) return 0;
+  return ((size_t(sim_grid(n_tokens)) * sizeof(double) + 255) / 256) * 256;
+}
+
+extern "C" int dsf_sim_stats(const void* x_in, const void* x_out, int dtype, int64_t n_tokens, int d,
+                             float* per_token_cos, double* accum, void* workspace, size_t workspace_bytes,
+                             hipStream_t stream) {
+  int rc = check_dtype(dtype);
+  if (rc) return rc;
+  DSF_CHECK(n_tokens >= 0, DSF_EINVAL, "n_tokens < 0");
+  DSF_CHECK(d > 0 && d % 8 == 0, DSF_EUNSUPPORTED, "d must be a positive multiple of 8");
+  if (n_tokens == 0) return DSF_OK;
+  DSF_CHECK(x_in && x_out && accum, DSF_EINVAL, "null pointer");
+  DSF_CHECK(aligned16(x_in) && aligned16(x_out), DSF_EINVAL, "x_in / x_out must be 16-byte aligned");
+  DSF_CHECK(workspace && workspace_bytes >= dsf_sim_workspace_size(n_tokens), DSF_EWORKSPACE,
+            "workspace needs %zu bytes", dsf_sim_workspace_size(n_tokens));
+  rc = check_device();
+  if (rc) return rc;
+  DSF_HIP(launch_sim_stats(dtype, x_in, x_out, n_tokens, d, per_token_cos, (double*)workspace, accum, stream));
+  return DSF_OK;
+}
+
+extern "C" int dsf_sim_finalize(const double* accum_dev, int L, double* s_host, hipStream_t stream) {
+  DSF_CHECK(L >= 0, DSF_EINVAL, "L < 0");
+  if (L == 0) return DSF_OK;
+  DSF_CHECK(accum_dev && s_host, DSF_EINVAL, "null pointer");
+  int rc = check_device();
+  if (rc) return rc;
+  std::vector<double> buf(size_t(L) * 2);
+  DSF_HIP(hipMemcpyAsync(buf.data(), accum_dev, buf.size() * sizeof(double), hipMemcpyDeviceToHost, stream));
+  DSF_HIP(hipStreamSynchronize(stream));
+  for (int l = 0; l < L; ++l) s_host[l] = buf[2 * l] / buf[2 * l + 1];
+  return DSF_OK;
+}
+
+// ------------------------------------------------------------ routing
+
+extern "C" int dsf_router_score(const void* x, int dtype, int64_t n_tokens, int d, int d_r, const void* w1,
+                                const void* b1, const void* w2, float b2, float* scores, hipStream_t stream) {
+  int rc = check_dtype(dtype);
+  if (rc) return rc;
+  DSF_CHECK(n_tokens >= 0 && n_tokens < (int64_t(1) << 40), DSF_EINVAL, "bad n_tokens");
+  DSF_CHECK(d > 0 && d % 8 == 0, DSF_EUNSUPPORTED, "d must be a positive multiple of 8");
+  DSF_CHECK(d_r == 16 || d_r == 32 || d_r == 48 || d_r == 64, DSF_EUNSUPPORTED, "d_r must be 16, 32, 48 or 64");
+  if (n_tokens == 0) return DSF_OK;
+  DSF_CHECK(x && w1 && w2 && scores, DSF_EINVAL, "null pointer");
+  DSF_CHECK(aligned16(x) && aligned16(w1), DSF_EINVAL, "x and W1 must be 16-byte aligned");
+  rc = check_device();
+  if (rc) return rc;
+  DSF_HIP(launch_router(dtype, x, n_tokens, d, d_r, w1, b1, w2, b2, scores, stream));
+  return DSF_OK;
+}
+
+extern "C" int dsf_topk_select(const float* scores, int B, int T, int k, int32_t* idx, hipStream_t stream) {
+  DSF_CHECK(B >= 0 && T >= 0, DSF_EINVAL, "B and T must be >= 0");
+  DSF_CHECK(k >= 0 && k <= T, DSF_EINVAL, "k=%d outside [0, T=%d]", k, T);
+  if (B == 0 || k == 0) return DSF_OK;
+  DSF_CHECK(scores && idx, DSF_EINVAL, "null pointer");
+  int rc = check_device();
+  if (rc) return rc;
+  DSF_HIP(launch_topk(scores, B, T, k, idx, stream));
+  return DSF_OK;
+}
+
+static int check_rows(const void* x, const void* other, int dtype, int B, int T, int d, const int32_t* idx, int k) {
+  int rc = check_dtype(dtype);
+  if (rc) return rc;
+  DSF_CHECK(B >= 0 && T >= 0, DSF_EINVAL, "B and T must be >= 0");
+  DSF_CHECK(int64_t(B) * T < (int64_t(1) << 31), DSF_EINVAL, "B * T too large");
+  DSF_CHECK(k >= 0 && k <= T, DSF_EINVAL, "k=%d outside [0, T=%d]", k, T);
+  DSF_CHECK(d > 0 && d % 8 == 0, DSF_EUNSUPPORTED, "d must be a positive multiple of 8");
+  if (B == 0 || k == 0) return DSF_OK;
+  DSF_CHECK(x && other && idx, DSF_EINVAL, "null pointer");
+  DSF_CHECK(aligned16(x) && aligned16(other), DSF_EINVAL, "row buffers must be 16-byte aligned");
+  return DSF_OK;
+}
+
+extern "C" int dsf_gather_rows(const void* x, int dtype, int B, int T, int d, const int32_t* idx, int k, void* out,
+                               hipStream_t stream) {
+  int rc = check_rows(x, out, dtype, B, T, d, idx, k);
+  if (rc || B == 0 || k == 0) return rc;
+  rc = check_device();
+  if (rc) return rc;
+  DSF_HIP(launch_gather(dtype, x, B, T, d, idx, k, out, stream));
+  return DSF_OK;
+}
+
+extern "C" int dsf_scatter_residual(void* x, const void* delta, int dtype, int B, int T, int d, const int32_t* idx,
+                                    int k, hipStream_t stream) {
+  int rc = check_rows(x, delta, dtype, B, T, d, idx, k);
+  if (rc || B == 0 || k == 0) return rc;
+  rc = check_device();
+  if (rc) return rc;
+  DSF_HIP(launch_scatter(dtype, x, delta, B, T, d, idx, k, stream));
+  return DSF_OK;
+}
+
+extern "C" int dsf_attention_forward(const void* q, const void* k, const void* v, int dtype, int B, int Hq,
+                                     int Hkv, int n, int hd, void* out, hipStream_t stream) {
+  int rc = check_dtype(dtype);
+  if (rc) return rc;
+  DSF_CHECK(B >= 0 && n >= 0, DSF_EINVAL, "B and n must be >= 0");
+  DSF_CHECK(Hq > 0 && Hkv > 0 && Hq % Hkv == 0, DSF_EINVAL, "need Hq %% Hkv == 0");
+  DSF_CHECK(hd == 32 || hd == 64 || hd == 128, DSF_EUNSUPPORTED, "head_dim must be 32, 64 or 128");
+  DSF_CHECK(int64_t(B) * n * Hq < (int64_t(1) << 31), DSF_EINVAL, "problem too large");
+  if (B == 0 || n == 0) return DSF_OK;
+  DSF_CHECK(q && k && v && out, DSF_EINVAL, "null pointer");
+  DSF_CHECK(aligned16(q) && aligned16(k) && aligned16(v) && aligned16(out), DSF_EINVAL,
+            "q, k, v and out must be 16-byte aligned");
+  rc = check_device();
+  if (rc) return rc;
+  DSF_HIP(launch_attention(dtype, q, k, v, B, Hq, Hkv, n, hd, out, stream));
+  return DSF_OK;
+}
+
+// ------------------------------------------------------- workspace plan
+
+namespace {
+struct Plan {
+  size_t scores, idx, a1, a2, q, k, v, attn, act, h, m2, rope, xin, simpart, total;
+};
+
+size_t up256(size_t x) { return (x + 255) / 256 * 256; }
+
+Plan make_plan(const dsf_layer_desc& D, int dtype, int B, int T, int k_max, bool with_sim) {
+  const size_t eb = elem_bytes(dtype);
+  const size_t N = size_t(B) * size_t(k_max);
+  const bool qwen = D.block == DSF_BLOCK_QWEN_SEQ;
+  Plan p{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t o = off;
+    off += up256(bytes);
+    return o;
+  };
+  p.scores = take(4 * size_t(B) * T);
+  p.idx = take(4 * N);
+  p.a1 = take(eb * N * D.d_model);
+  p.a2 = qwen ? 0 : take(eb * N * D.d_model);
+  p.q = take(eb * N * D.n_heads * D.head_dim);
+  p.k = take(eb * N * D.n_kv_heads * D.head_dim);
+  p.v = take(eb * N * D.n_kv_heads * D.head_dim);
+  p.attn = take(eb * N * D.n_heads * D.head_dim);
+  p.act = take(eb * N * D.d_ff);
+  p.h = qwen ? take(eb * N * D.d_model) : 0;
+  p.m2 = qwen ? take(eb * N * D.d_model) : 0;
+  p.rope = take(4 * size_t(T) * D.rotary_dims);
+  p.xin = with_sim ? take(eb * size_t(B) * T * D.d_model) : 0;
+  p.simpart = with_sim ? take(dsf_sim_workspace_size(int64_t(B) * T)) : 0;
+  p.total = off;
+  return p;
+}
+
+int check_desc(const dsf_layer_desc* D) {
+  DSF_CHECK(D, DSF_EINVAL, "null layer descriptor");
+  DSF_CHECK(D->block == DSF_BLOCK_NEOX_PARALLEL || D->block == DSF_BLOCK_QWEN_SEQ, DSF_EUNSUPPORTED,
+            "unknown block template %d", D->block);
+  DSF_CHECK(D->d_model > 0 && D->d_model % 8 == 0, DSF_EUNSUPPORTED, "d_model must be a positive multiple of 8");
+  DSF_CHECK(D->d_model <= 8192, DSF_EUNSUPPORTED, "d_model above 8192");
+  DSF_CHECK(D->n_heads > 0 && D->n_kv_heads > 0 && D->n_heads % D->n_kv_heads == 0, DSF_EINVAL,
+            "need n_heads %% n_kv_heads == 0");
+  DSF_CHECK(D->head_dim == 32 || D->head_dim == 64 || D->head_dim == 128, DSF_EUNSUPPORTED,
+            "head_dim must be 32, 64 or 128");
+  DSF_CHECK(D->d_ff > 0 && D->d_ff % 64 == 0, DSF_EUNSUPPORTED, "d_ff must be a positive multiple of 64");
+  DSF_CHECK(D->rotary_dims > 0 && D->rotary_dims % 2 == 0 && D->rotary_dims <= D->head_dim, DSF_EINVAL,
+            "rotary_dims must be even and in (0, head_dim]");
+  DSF_CHECK(D->d_router == 16 || D->d_router == 32 || D->d_router == 48 || D->d_router == 64, DSF_EUNSUPPORTED,
+            "d_router must be 16, 32, 48 or 64");
+  DSF_CHECK(D->norm_eps > 0.f && std::isfinite(D->norm_eps), DSF_EINVAL, "norm_eps must be positive");
+  DSF_CHECK(D->rope_theta > 0.0 && std::isfinite(D->rope_theta), DSF_EINVAL, "rope_theta must be positive");
+  DSF_CHECK(D->reserved == 0.f, DSF_EINVAL, "reserved field must be 0");
+  return DSF_OK;
+}
+
+int check_weights(const dsf_layer_desc& D, const dsf_layer_weights* W, int l) {
+  DSF_CHECK(W, DSF_EINVAL, "null weights (layer %d)", l);
+  const void* req[] = {W->router_w1, W->router_w2, W->norm1_w, W->norm2_w, W->w_qkv, W->w_o, W->w_up, W->w_down};
+  const char* nm[] = {"router_w1", "router_w2", "norm1_w", "norm2_w", "w_qkv", "w_o", "w_up", "w_down"};
+  for (int i = 0; i < 8; ++i) {
+    DSF_CHECK(req[i], DSF_EINVAL, "layer %d: %s is null", l, nm[i]);
+    DSF_CHECK(aligned16(req[i]), DSF_EINVAL, "layer %d: %s is not 16-byte aligned", l, nm[i]);
+  }
+  const void* opt[] = {W->router_b1, W->norm1_b, W->norm2_b, W->b_qkv, W->b_o, W->b_up, W->b_down};
+  for (const void* p : opt) DSF_CHECK(aligned16(p), DSF_EINVAL, "layer %d: a bias is not 16-byte aligned", l);
+  if (D.block == DSF_BLOCK_QWEN_SEQ)
+    DSF_CHECK(!W->norm1_b && !W->norm2_b, DSF_EINVAL, "layer %d: RMSNorm takes no bias", l);
+  DSF_CHECK(W->reserved == 0.f, DSF_EINVAL, "layer %d: reserved field must be 0", l);
+  return DSF_OK;
+}
+}  // namespace
+
+extern "C" size_t dsf_workspace_size(const dsf_layer_desc* desc, int dtype, int B, int T, int k_max,
+                                     int with_similarity) {
+  if (check_desc(desc) || check_dtype(dtype) || B < 0 || T < 0 || k_max < 0 || k_max > T) return 0;
+  return make_plan(*desc, dtype, B, T, k_max, with_similarity != 0).total;
+}
+
+// --------------------------------------------------- one sparse layer
+
+namespace {
+struct Ctx {
+  const dsf_layer_desc* D;
+  int dtype, B, T;
+  char* ws;
+  Plan plan;
+  hipStream_t s;
+};
+
+template <typename P>
+P* at(const Ctx& c, size_t off) {
+  return reinterpret_cast<P*>(c.ws + off);
+}
+
+// Enqueue one layer. k > 0. dense: every token at positions 0..T-1.
+int run_layer(const Ctx& c, const dsf_layer_weights* W, void* x, int k, bool dense, float* scores_out,
+              int32_t* idx_out, const int32_t* idx_in) {
+  const dsf_layer_desc& D = *c.D;
+  const int B = c.B, T = c.T, d = D.d_model;
+  const int hd = D.head_dim, Hq = D.n_heads, Hkv = D.n_kv_heads, f = D.d_ff;
+  const bool qwen = D.block == DSF_BLOCK_QWEN_SEQ;
+  const int32_t* idx = nullptr;
+  if (!dense) {
+    float* scores = scores_out ? scores_out : at<float>(c, c.plan.scores);
+    DSF_HIP(launch_router(c.dtype, x, int64_t(B) * T, d, D.d_router, W->router_w1, W->router_b1, W->router_w2,
+                          W->router_b2, scores, c.s));
+    if (idx_in) {
+      idx = idx_in;
+      if (idx_out) DSF_HIP(hipMemcpyAsync(idx_out, idx_in, sizeof(int32_t) * size_t(B) * k, hipMemcpyDeviceToDevice, c.s));
+    } else {
+      int32_t* dst = idx_out ? idx_out : at<int32_t>(c, c.plan.idx);
+      DSF_HIP(launch_topk(scores, B, T, k, dst, c.s));
+      idx = dst;
+    }
+  }
+  const int kk = dense ? T : k;
+  const int M = B * kk;
+  const int dq = Hq * hd, dkv = Hkv * hd;
+
+  NormArgs na{};
+  na.dtype = c.dtype;
+  na.src = x;
+  na.src_rows = T;
+  na.idx = idx;
+  na.B = B;
+  na.kk = kk;
+  na.d = d;
+  na.eps = D.norm_eps;
+  na.rms = qwen;
+  na.w1 = W->norm1_w;
+  na.b1 = W->norm1_b;
+  na.out1 = at<char>(c, c.plan.a1);
+  if (!qwen) {
+    na.w2 = W->norm2_w;
+    na.b2 = W->norm2_b;
+    na.out2 = at<char>(c, c.plan.a2);
+  }
+  DSF_HIP(launch_norm(na, c.s));
+
+  GemmArgs g{};
+  g.dtype = c.dtype;
+  g.B = B;
+  g.kk = kk;
+  g.T = T;
+  g.idx = idx;
+  {  // QKV projection, bias, RoPE at the kept tokens' original positions
+    GemmArgs q = g;
+    q.M = M; q.N = dq + 2 * dkv; q.K = d; q.K1 = d;
+    q.a = na.out1; q.lda = d;
+    q.b = W->w_qkv; q.ldb = d;
+    q.epi = EPI_QKV_ROPE;
+    q.bias = W->b_qkv;
+    q.q = at<char>(c, c.plan.q); q.k = at<char>(c, c.plan.k); q.v = at<char>(c, c.plan.v);
+    q.Hq = Hq; q.Hkv = Hkv; q.hd = hd; q.R = D.rotary_dims;
+    q.rope = at<float>(c, c.plan.rope);
+    TimedScope ts(DSF_KIND_GEMM_QKV, c.s);
+    DSF_HIP(launch_gemm(q, c.s));
+  }
+  DSF_HIP(launch_attention(c.dtype, at<char>(c, c.plan.q), at<char>(c, c.plan.k), at<char>(c, c.plan.v), B, Hq,
+                           Hkv, kk, hd, at<char>(c, c.plan.attn), c.s));
+  if (!qwen) {
+    {  // FFN up + GELU on LN2 of the kept rows
+      GemmArgs u = g;
+      u.M = M; u.N = f; u.K = d; u.K1 = d;
+      u.a = na.out2; u.lda = d;
+      u.b = W->w_up; u.ldb = d;
+      u.epi = EPI_BIAS_GELU; u.bias = W->b_up;
+      u.out = at<char>(c, c.plan.act); u.ldo = f;
+      TimedScope ts(DSF_KIND_GEMM_UP, c.s);
+      DSF_HIP(launch_gemm(u, c.s));
+    }
+    {  // parallel residual: [attn | act] . [W_o | W_down]^T + b_o + b_down + x, scattered back
+      GemmArgs o = g;
+      o.M = M; o.N = d; o.K = dq + f; o.K1 = dq;
+      o.a = at<char>(c, c.plan.attn); o.lda = dq;
+      o.a2 = at<char>(c, c.plan.act); o.lda2 = f;
+      o.b = W->w_o; o.ldb = dq;
+      o.b2 = W->w_down; o.ldb2 = f;
+      o.epi = EPI_RESID_SCATTER; o.bias = W->b_o; o.bias2 = W->b_down;
+      o.x = x;
+      TimedScope ts(DSF_KIND_GEMM_DOWN, c.s);
+      DSF_HIP(launch_gemm(o, c.s));
+    }
+    return DSF_OK;
+  }
+  {  // h = x_kept + attn . W_o^T
+    GemmArgs o = g;
+    o.M = M; o.N = d; o.K = dq; o.K1 = dq;
+    o.a = at<char>(c, c.plan.attn); o.lda = dq;
+    o.b = W->w_o; o.ldb = dq;
+    o.epi = EPI_RESID_STORE; o.bias = W->b_o;
+    o.x = x; o.out = at<char>(c, c.plan.h); o.ldo = d;
+    TimedScope ts(DSF_KIND_GEMM_O, c.s);
+    DSF_HIP(launch_gemm(o, c.s));
+  }
+  NormArgs n2{};
+  n2.dtype = c.dtype;
+  n2.src = at<char>(c, c.plan.h);
+  n2.src_rows = 0;
+  n2.B = B;
+  n2.kk = kk;
+  n2.d = d;
+  n2.eps = D.norm_eps;
+  n2.rms = 1;
+  n2.w1 = W->norm2_w;
+  n2.out1 = at<char>(c, c.plan.m2);
+  DSF_HIP(launch_norm(n2, c.s));
+  {  // SwiGLU: silu(gate) * up
+    GemmArgs u = g;
+    u.M = M; u.N = f; u.K = d; u.K1 = d;
+    u.a = n2.out1; u.lda = d;
+    u.b = W->w_up; u.ldb = d;
+    u.epi = EPI_SWIGLU; u.f = f;
+    u.out = at<char>(c, c.plan.act); u.ldo = f;
+    TimedScope ts(DSF_KIND_GEMM_UP, c.s);
+    DSF_HIP(launch_gemm(u, c.s));
+  }
+  {  // y = h + act . W_down^T, scattered back
+    GemmArgs o = g;
+    o.M = M; o.N = d; o.K = f; o.K1 = f;
+    o.a = at<char>(c, c.plan.act); o.lda = f;
+    o.b = W->w_down; o.ldb = f;
+    o.epi = EPI_RESID_SCATTER; o.bias = W->b_down;
+    o.x = x; o.res = at<char>(c, c.plan.h);
+    TimedScope ts(DSF_KIND_GEMM_DOWN, c.s);
+    DSF_HIP(launch_gemm(o, c.s));
+  }
+  return DSF_OK;
+}
+
+int check_common(const dsf_layer_desc* desc, int dtype, void* x, int B, int T, int k_max, int flags,
+                 void* workspace, size_t workspace_bytes, bool with_sim, Plan* plan) {
+  int rc = check_desc(desc);
+  if (rc) return rc;
+  rc = check_dtype(dtype);
+  if (rc) return rc;
+  DSF_CHECK(B >= 0 && T >= 0, DSF_EINVAL, "B and T must be >= 0");
+  DSF_CHECK(int64_t(B) * T < (int64_t(1) << 31) / 8, DSF_EINVAL, "B * T too large");
+  DSF_CHECK((flags & ~DSF_FLAG_DENSE) == 0, DSF_EINVAL, "unknown flag bits 0x%x", flags);
+  if (B == 0 || T == 0 || k_max == 0) return DSF_OK;
+  DSF_CHECK(x, DSF_EINVAL, "x is null");
+  DSF_CHECK(aligned16(x), DSF_EINVAL, "x must be 16-byte aligned");
+  *plan = make_plan(*desc, dtype, B, T, k_max, with_sim);
+  DSF_CHECK(workspace_bytes >= plan->total, DSF_EWORKSPACE, "workspace needs %zu bytes, got %zu", plan->total,
+            workspace_bytes);
+  DSF_CHECK(workspace && (reinterpret_cast<uintptr_t>(workspace) & 255u) == 0, DSF_EINVAL,
+            "workspace must be non-null and 256-byte aligned");
+  return DSF_OK;
+}
+}  // namespace
+
+extern "C" int dsf_sparse_block_forward(const dsf_layer_desc* desc, const dsf_layer_weights* weights, int dtype,
+                                        void* x, int B, int T, int k, int flags, float* scores_out, int32_t* idx_out,
+                                        const int32_t* idx_in, void* workspace, size_t workspace_bytes,
+                                        hipStream_t stream) {
+  DSF_CHECK(k >= 0 && k <= T, DSF_EINVAL, "k=%d outside [0, T=%d]", k, T);
+  const bool dense = flags & DSF_FLAG_DENSE;
+  DSF_CHECK(!dense || k == T, DSF_EINVAL, "DSF_FLAG_DENSE requires k == T");
+  DSF_CHECK(!(dense && (scores_out || idx_out || idx_in)), DSF_EINVAL, "routing buffers are unused with DSF_FLAG_DENSE");
+  Plan plan{};
+  int rc = check_common(desc, dtype, x, B, T, k, flags, workspace, workspace_bytes, false, &plan);
+  if (rc) return rc;
+  if (B == 0 || T == 0 || k == 0) return DSF_OK;
+  rc = check_weights(*desc, weights, 0);
+  if (rc) return rc;
+  rc = check_device();
+  if (rc) return rc;
+  Ctx c{desc, dtype, B, T, (char*)workspace, plan, stream};
+  DSF_HIP(launch_rope_table(at<float>(c, plan.rope), T, desc->rotary_dims, desc->rope_theta, stream));
+  return run_layer(c, weights, x, k, dense, scores_out, idx_out, idx_in);
+}
+
+extern "C" int dsf_stack_forward(const dsf_layer_desc* desc, const dsf_layer_weights* weights, int L, int dtype,
+                                 const int* k, void* x, int B, int T, int flags, double* sim_accum, void* workspace,
+                                 size_t workspace_bytes, hipStream_t stream) {
+  DSF_CHECK(L >= 0, DSF_EINVAL, "L < 0");
+  DSF_CHECK(L == 0 || (weights && k), DSF_EINVAL, "null weights or k");
+  const bool dense = flags & DSF_FLAG_DENSE;
+  int k_max = 0;
+  for (int l = 0; l < L; ++l) {
+    DSF_CHECK(k[l] >= 0 && k[l] <= T, DSF_EINVAL, "k[%d]=%d outside [0, T=%d]", l, k[l], T);
+    DSF_CHECK(!dense || k[l] == T, DSF_EINVAL, "DSF_FLAG_DENSE requires k[l] == T");
+    k_max = k[l] > k_max ? k[l] : k_max;
+  }
+  const bool with_sim = sim_accum != nullptr;
+  if (with_sim && L > 0 && B > 0 && T > 0) k_max = k_max > 1 ? k_max : 1;  // workspace for the input copy
+  Plan plan{};
+  int rc = check_common(desc, dtype, x, B, T, k_max, flags, workspace, workspace_bytes, with_sim, &plan);
+  if (rc) return rc;
+  if (L == 0 || B == 0 || T == 0 || k_max == 0) return DSF_OK;
+  for (int l = 0; l < L; ++l) {
+    rc = check_weights(*desc, &weights[l], l);
+    if (rc) return rc;
+  }
+  rc = check_device();
+  if (rc) return rc;
+  Ctx c{desc, dtype, B, T, (char*)workspace, plan, stream};
+  DSF_HIP(launch_rope_table(at<float>(c, plan.rope), T, desc->rotary_dims, desc->rope_theta, stream));
+  const size_t xbytes = elem_bytes(dtype) * size_t(B) * T * desc->d_model;
+  for (int l = 0; l < L; ++l) {
+    if (with_sim) DSF_HIP(launch_copy(x, at<char>(c, plan.xin), xbytes, stream));
+    if (k[l] > 0) {
+      rc = run_layer(c, &weights[l], x, k[l], dense, nullptr, nullptr, nullptr);
+      if (rc) return rc;
+    }
+    if (with_sim)
+      DSF_HIP(launch_sim_stats(dtype, at<char>(c, plan.xin), x, int64_t(B) * T, desc->d_model, nullptr,
+                               at<double>(c, plan.simpart), sim_accum + 2 * l, stream));
+  }
+  return DSF_OK;
+}

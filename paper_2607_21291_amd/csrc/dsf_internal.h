@@ -1,0 +1,94 @@
+// Host-side declarations shared by the library's translation units: kernel
+// launchers (each defined next to its kernels) and the timing hooks.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "adadsf.h"
+
+namespace dsf {
+
+// ---- per-launch timing (api.hip) ----
+void timing_begin(int kind, hipStream_t s);
+void timing_end(int kind, hipStream_t s);
+
+struct TimedScope {
+  int kind;
+  hipStream_t s;
+  TimedScope(int k, hipStream_t st) : kind(k), s(st) { timing_begin(kind, s); }
+  ~TimedScope() { timing_end(kind, s); }
+};
+
+// ---- streaming kernels (kernels_misc.hip) ----
+// table[p][i] = (cos, sin)(p * theta^(-2i/R)), p < T, i < R/2, computed in fp64.
+hipError_t launch_rope_table(float* table, int T, int R, double theta, hipStream_t s);
+int sim_grid(int64_t n_tokens);
+hipError_t launch_sim_stats(int dtype, const void* a, const void* c, int64_t n, int d, float* per_tok,
+                            double* partial, double* accum, hipStream_t s);
+hipError_t launch_router(int dtype, const void* x, int64_t n, int d, int d_r, const void* w1,
+                         const void* b1, const void* w2, float b2, float* scores, hipStream_t s);
+hipError_t launch_topk(const float* scores, int B, int T, int k, int32_t* idx, hipStream_t s);
+hipError_t launch_gather(int dtype, const void* x, int B, int T, int d, const int32_t* idx, int k,
+                         void* out, hipStream_t s);
+hipError_t launch_scatter(int dtype, void* x, const void* delta, int B, int T, int d,
+                          const int32_t* idx, int k, hipStream_t s);
+hipError_t launch_copy(const void* src, void* dst, size_t bytes, hipStream_t s);
+
+// Row normalisation of gathered rows. Output row r = b * kk + j reads source
+// row src[b * src_rows + (idx ? idx[r] : j)] (src_rows = T for hidden states)
+// or, with src_rows == 0, the compact row src[r]. rms != 0 selects RMSNorm
+// (bias pointers must be null); out2 (nullable) receives a second
+// normalisation of the same rows with (w2, b2).
+struct NormArgs {
+  int dtype;
+  const void* src;
+  int src_rows;
+  const int32_t* idx;
+  int B, kk, d;
+  float eps;
+  int rms;
+  const void* w1; const void* b1; void* out1;
+  const void* w2; const void* b2; void* out2;
+};
+hipError_t launch_norm(const NormArgs& a, hipStream_t s);
+
+// ---- GEMMs with fused epilogues (kernels_gemm.hip) ----
+// C[M, N] = A[M, K] . B[N, K]^T in fp32, then one of the epilogues below.
+// Rows m < M are compacted tokens: m = b * kk + j at position pos = idx ? idx[m] : j.
+enum EpiKind {
+  EPI_QKV_ROPE = 0,   // + bias, RoPE on q/k heads, write q/k/v as [B, H, kk, hd]
+  EPI_BIAS_GELU = 1,  // out[m, n] = gelu(C + bias)
+  EPI_SWIGLU = 2,     // B rows interleaved gate/up; out[m, n] = silu(gate) * up, N = f
+  EPI_RESID_STORE = 3,    // out[m, n] = x[b, pos, n] + C (+ bias)
+  EPI_RESID_SCATTER = 4,  // x[b, pos, n] = resid + C + bias + bias2, resid = x[b, pos] or res[m]
+};
+
+struct GemmArgs {
+  int dtype;
+  int M, N, K;
+  // A: [M, K1] from a, then [M, K - K1] from a2 (K1 == K: single source)
+  const void* a; int lda; const void* a2; int lda2; int K1;
+  // B: [N, K1] from b, then [N, K - K1] from b2
+  const void* b; int ldb; const void* b2; int ldb2;
+  int epi;
+  const void* bias; const void* bias2;
+  // token mapping
+  int B, kk, T; const int32_t* idx;
+  // EPI_QKV_ROPE
+  void* q; void* k; void* v; int Hq, Hkv, hd, R; const float* rope;
+  // EPI_BIAS_GELU / EPI_SWIGLU / EPI_RESID_STORE output [M, ldo]
+  void* out; int ldo;
+  // EPI_RESID_*: hidden states x [B, T, d] (d = N); res (nullable) compact residual [M, N]
+  void* x; const void* res;
+  // EPI_SWIGLU: f (gate rows [0, f), up rows [f, 2f))
+  int f;
+};
+hipError_t launch_gemm(const GemmArgs& g, hipStream_t s);
+
+// ---- attention over kept tokens (kernels_attn.hip) ----
+// q [B, Hq, n, hd], k/v [B, Hkv, n, hd] -> out [B, n, Hq*hd], causal over the n tokens.
+hipError_t launch_attention(int dtype, const void* q, const void* k, const void* v, int B, int Hq,
+                            int Hkv, int n, int hd, void* out, hipStream_t s);
+
+}  // namespace dsf

@@ -1,0 +1,265 @@
+// Causal attention among the kept tokens (Eq. 1 over the compacted set) for
+// gfx950.
+//
+// bf16 path (flash-style, online softmax in fp32). A workgroup of four
+// wavefronts owns 64*NQ consecutive queries of one (sequence, query head); each
+// wavefront owns NQ groups of 16 queries. Key/value tiles of 64 tokens are
+// staged in LDS, K row-major (XOR-swizzled 16-byte chunks) and V transposed.
+//
+// Scores are formed transposed, S^T = K Q^T, with v_mfma_f32_16x16x32_bf16, so
+// a lane holds 16 scores of ONE query (its column): the row max and row sum
+// need only two cross-lane steps, and the probabilities already sit in the
+// layout of the B operand of O^T += V^T P^T. The MFMA's k slots there are
+// filled with keys in the order the lane holds them; V^T is read from LDS in
+// the same order, so the contraction over keys is unchanged.
+//
+// Kept positions ascend, so causal order over compacted indices is causal
+// order over original positions.
+#include "dsf_device.h"
+#include "dsf_internal.h"
+
+namespace dsf {
+
+constexpr int kKV = 64;             // keys per tile
+constexpr int kVtLD = kKV + 4;      // padded row of the transposed V tile (bf16 elements)
+
+template <int HD, int NQ>
+__global__ __launch_bounds__(256) void attn_bf16_kernel(const uint16_t* __restrict__ Q,
+                                                        const uint16_t* __restrict__ K,
+                                                        const uint16_t* __restrict__ V, int Hq, int Hkv,
+                                                        int n, uint16_t* __restrict__ out) {
+  constexpr int QB = 64 * NQ;          // queries per workgroup
+  constexpr int NCH = HD / 8;          // 16-byte chunks per row
+  constexpr int SWZ = (NCH < 8 ? NCH : 8) - 1;
+  constexpr int NS = HD / 32;          // MFMA k steps over the head dim
+  constexpr int ND = HD / 16;          // 16-row blocks of the head dim
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[kKV * HD];
+  __shared__ __attribute__((aligned(16))) uint16_t Vt[HD * kVtLD];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r16 = lane & 15, grp = lane >> 4;
+  const int nqb = (n + QB - 1) / QB;
+  const int qblk = nqb - 1 - int(blockIdx.x);  // longest rows first
+  const int h = blockIdx.y, b = blockIdx.z;
+  const int kvh = h / (Hq / Hkv);
+  const int q0 = qblk * QB;
+  const int qw0 = q0 + wave * 16 * NQ;
+
+  const uint16_t* Qh = Q + (int64_t(b) * Hq + h) * n * HD;
+  const uint16_t* Kh = K + (int64_t(b) * Hkv + kvh) * n * HD;
+  const uint16_t* Vh = V + (int64_t(b) * Hkv + kvh) * n * HD;
+
+  // Q^T operand: lane (query r16, group grp) holds Q[query][32 s + 8 grp .. +8]
+  bf16x8 qf[NQ][NS];
+#pragma unroll
+  for (int qi = 0; qi < NQ; ++qi) {
+    int qrow = qw0 + 16 * qi + r16;
+    if (qrow > n - 1) qrow = n - 1;
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+      qf[qi][s] = *reinterpret_cast<const bf16x8*>(Qh + int64_t(qrow) * HD + 32 * s + 8 * grp);
+  }
+
+  f32x4 o[NQ][ND];
+  float m_run[NQ], l_run[NQ];
+#pragma unroll
+  for (int qi = 0; qi < NQ; ++qi) {
+    m_run[qi] = -INFINITY;
+    l_run[qi] = 0.f;
+#pragma unroll
+    for (int db = 0; db < ND; ++db) o[qi][db] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  const float sc = 1.4426950408889634f / sqrtf(float(HD));  // log2(e) / sqrt(hd)
+
+  const int kend = min(n, q0 + QB);
+  const int ntiles = (kend + kKV - 1) / kKV;
+  const int wave_qmax = qw0 + 16 * NQ - 1;
+
+  for (int t = 0; t < ntiles; ++t) {
+    const int kb0 = t * kKV;
+    __syncthreads();
+    // K tile, row-major with swizzled chunks
+    for (int c = tid; c < kKV * NCH; c += 256) {
+      const int row = c / NCH, ch = c % NCH;
+      const int key = kb0 + row;
+      u32x4 val = key < n ? *reinterpret_cast<const u32x4*>(Kh + int64_t(key) * HD + ch * 8) : u32x4{0, 0, 0, 0};
+      *reinterpret_cast<u32x4*>(Ks + row * HD + ((ch ^ (row & SWZ)) << 3)) = val;
+    }
+    // V tile transposed: Vt[dim][key], two keys per 32-bit store
+    for (int c = tid; c < (kKV / 2) * NCH; c += 256) {
+      const int kp = c % (kKV / 2), ch = c / (kKV / 2);
+      const int key0 = kb0 + 2 * kp;
+      u32x4 v0 = key0 < n ? *reinterpret_cast<const u32x4*>(Vh + int64_t(key0) * HD + ch * 8) : u32x4{0, 0, 0, 0};
+      u32x4 v1 = key0 + 1 < n ? *reinterpret_cast<const u32x4*>(Vh + int64_t(key0 + 1) * HD + ch * 8)
+                              : u32x4{0, 0, 0, 0};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        uint32_t lo = (v0[e] & 0xffffu) | (v1[e] << 16);
+        uint32_t hi = (v0[e] >> 16) | (v1[e] & 0xffff0000u);
+        *reinterpret_cast<uint32_t*>(Vt + (ch * 8 + 2 * e) * kVtLD + 2 * kp) = lo;
+        *reinterpret_cast<uint32_t*>(Vt + (ch * 8 + 2 * e + 1) * kVtLD + 2 * kp) = hi;
+      }
+    }
+    __syncthreads();
+    if (kb0 > wave_qmax) continue;  // every key of this tile is in this wave's future
+
+    // S^T blocks: lane holds S[query 16 qi + r16][key kb0 + 16 kb + 4 grp + i]
+    f32x4 s[NQ][4];
+#pragma unroll
+    for (int qi = 0; qi < NQ; ++qi)
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) s[qi][kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+      const int row = 16 * kb + r16;
+#pragma unroll
+      for (int st = 0; st < NS; ++st) {
+        const int ch = 4 * st + grp;
+        bf16x8 kf = *reinterpret_cast<const bf16x8*>(Ks + row * HD + ((ch ^ (row & SWZ)) << 3));
+#pragma unroll
+        for (int qi = 0; qi < NQ; ++qi)
+          s[qi][kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[qi][st], s[qi][kb], 0, 0, 0);
+      }
+    }
+    const bool diag = kb0 + kKV - 1 > qw0 || kb0 + kKV > n;
+    bf16x8 pb[NQ][2];
+#pragma unroll
+    for (int qi = 0; qi < NQ; ++qi) {
+      const int qg = qw0 + 16 * qi + r16;
+      float mx = -INFINITY;
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          float v = s[qi][kb][i] * sc;
+          if (diag) {
+            const int key = kb0 + 16 * kb + 4 * grp + i;
+            if (key > qg || key >= n) v = -INFINITY;
+          }
+          s[qi][kb][i] = v;
+          mx = fmaxf(mx, v);
+        }
+      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      const float m_new = fmaxf(m_run[qi], mx);
+      const float base = m_new == -INFINITY ? 0.f : m_new;
+      const float alpha = exp2f(m_run[qi] - base);
+      float sum = 0.f;
+      float p[4][4];
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          p[kb][i] = exp2f(s[qi][kb][i] - base);
+          sum += p[kb][i];
+        }
+      sum += __shfl_xor(sum, 16, 64);
+      sum += __shfl_xor(sum, 32, 64);
+      l_run[qi] = l_run[qi] * alpha + sum;
+      m_run[qi] = m_new;
+#pragma unroll
+      for (int db = 0; db < ND; ++db) o[qi][db] *= alpha;
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          pb[qi][ks][i] = (__bf16)p[2 * ks][i];
+          pb[qi][ks][4 + i] = (__bf16)p[2 * ks + 1][i];
+        }
+    }
+    // O^T[dim 16 db + r16 .. ][query] += V^T P^T over this tile's 64 keys
+#pragma unroll
+    for (int db = 0; db < ND; ++db) {
+      const int dim = 16 * db + r16;
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+        const uint16_t* vrow = Vt + dim * kVtLD + 32 * ks + 4 * grp;
+        u32x2 lo = *reinterpret_cast<const u32x2*>(vrow);
+        u32x2 hi = *reinterpret_cast<const u32x2*>(vrow + 16);
+        u32x4 raw = {lo[0], lo[1], hi[0], hi[1]};
+        bf16x8 vf = __builtin_bit_cast(bf16x8, raw);
+#pragma unroll
+        for (int qi = 0; qi < NQ; ++qi)
+          o[qi][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pb[qi][ks], o[qi][db], 0, 0, 0);
+      }
+    }
+  }
+  // lane holds O^T[dim 16 db + 4 grp + i][query r16]
+#pragma unroll
+  for (int qi = 0; qi < NQ; ++qi) {
+    const int qg = qw0 + 16 * qi + r16;
+    if (qg >= n) continue;
+    const float inv = 1.0f / l_run[qi];
+    uint16_t* orow = out + (int64_t(b) * n + qg) * (int64_t(Hq) * HD) + int64_t(h) * HD;
+#pragma unroll
+    for (int db = 0; db < ND; ++db) {
+      u32x2 pk;
+      pk[0] = uint32_t(f2bf(o[qi][db][0] * inv)) | (uint32_t(f2bf(o[qi][db][1] * inv)) << 16);
+      pk[1] = uint32_t(f2bf(o[qi][db][2] * inv)) | (uint32_t(f2bf(o[qi][db][3] * inv)) << 16);
+      *reinterpret_cast<u32x2*>(orow + 16 * db + 4 * grp) = pk;
+    }
+  }
+}
+
+// fp32: one thread per query, online softmax over its causal prefix.
+template <int HD>
+__global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ Q, const float* __restrict__ K,
+                                                      const float* __restrict__ V, int Hq, int Hkv, int n,
+                                                      float* __restrict__ out) {
+  const int qi = blockIdx.x * 64 + threadIdx.x, h = blockIdx.y, b = blockIdx.z;
+  if (qi >= n) return;
+  const int kvh = h / (Hq / Hkv);
+  const float* qr = Q + ((int64_t(b) * Hq + h) * n + qi) * HD;
+  const float* Kh = K + (int64_t(b) * Hkv + kvh) * n * HD;
+  const float* Vh = V + (int64_t(b) * Hkv + kvh) * n * HD;
+  float qv[HD], o[HD];
+  for (int d = 0; d < HD; ++d) {
+    qv[d] = qr[d];
+    o[d] = 0.f;
+  }
+  const float scale = 1.0f / sqrtf(float(HD));
+  float m = -INFINITY, l = 0.f;
+  for (int j = 0; j <= qi; ++j) {
+    const float* kr = Kh + int64_t(j) * HD;
+    float s = 0.f;
+    for (int d = 0; d < HD; ++d) s = fmaf(qv[d], kr[d], s);
+    s *= scale;
+    const float mn = fmaxf(m, s);
+    const float c = expf(m - mn), p = expf(s - mn);
+    l = l * c + p;
+    const float* vr = Vh + int64_t(j) * HD;
+    for (int d = 0; d < HD; ++d) o[d] = o[d] * c + p * vr[d];
+    m = mn;
+  }
+  float* orow = out + (int64_t(b) * n + qi) * (int64_t(Hq) * HD) + int64_t(h) * HD;
+  for (int d = 0; d < HD; ++d) orow[d] = o[d] / l;
+}
+
+hipError_t launch_attention(int dtype, const void* q, const void* k, const void* v, int B, int Hq, int Hkv,
+                            int n, int hd, void* out, hipStream_t s) {
+  if (n == 0 || B == 0) return hipSuccess;
+  TimedScope ts(DSF_KIND_ATTN, s);
+  if (dtype == DSF_F32) {
+    dim3 grid((n + 63) / 64, Hq, B);
+    auto Qp = (const float*)q; auto Kp = (const float*)k; auto Vp = (const float*)v; auto O = (float*)out;
+    switch (hd) {
+      case 32: attn_f32_kernel<32><<<grid, 64, 0, s>>>(Qp, Kp, Vp, Hq, Hkv, n, O); break;
+      case 64: attn_f32_kernel<64><<<grid, 64, 0, s>>>(Qp, Kp, Vp, Hq, Hkv, n, O); break;
+      case 128: attn_f32_kernel<128><<<grid, 64, 0, s>>>(Qp, Kp, Vp, Hq, Hkv, n, O); break;
+      default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+  }
+  constexpr int NQ = 2;
+  dim3 grid((n + 64 * NQ - 1) / (64 * NQ), Hq, B);
+  auto Qp = (const uint16_t*)q; auto Kp = (const uint16_t*)k; auto Vp = (const uint16_t*)v; auto O = (uint16_t*)out;
+  switch (hd) {
+    case 32: attn_bf16_kernel<32, NQ><<<grid, 256, 0, s>>>(Qp, Kp, Vp, Hq, Hkv, n, O); break;
+    case 64: attn_bf16_kernel<64, NQ><<<grid, 256, 0, s>>>(Qp, Kp, Vp, Hq, Hkv, n, O); break;
+    case 128: attn_bf16_kernel<128, NQ><<<grid, 256, 0, s>>>(Qp, Kp, Vp, Hq, Hkv, n, O); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace dsf

@@ -1,0 +1,355 @@
+// Projection GEMMs of the decoder block on the kept tokens (Eqs. 1-2),
+// C[M, N] = A[M, K] . B[N, K]^T with fused epilogues, for gfx950.
+//
+// bf16 path: 128 x 128 x 64 workgroup tiles, four wavefronts of 64 x 64, each
+// built from v_mfma_f32_16x16x32_bf16. Global tiles are staged through LDS
+// (double buffered, 16-byte chunks XOR-swizzled by row so that the 16 rows an
+// MFMA operand read touches fall in distinct bank groups). The next tile's
+// global loads are in flight while the current tile is multiplied.
+//
+// After the K loop the fp32 tile is written to LDS and the epilogue reads it
+// back row-wise, so every epilogue (RoPE pairs dims i and i + R/2; SwiGLU
+// pairs gate and up columns) sees whole rows and stores 16-byte vectors.
+//
+// fp32 path: a plain LDS-tiled FMA kernel (32 x 128 tiles) that shares the
+// epilogue. It exists for the fp32 workload and is not tuned.
+#include "dsf_device.h"
+#include "dsf_internal.h"
+
+namespace dsf {
+
+// ------------------------------------------------------------- epilogue
+
+template <typename T>
+__device__ __forceinline__ void load8(const T* p, float* v) {
+  if constexpr (sizeof(T) == 2) {
+    load_vec(p, v);
+  } else {
+    load_vec(p, v);
+    load_vec(p + 4, v + 4);
+  }
+}
+template <typename T>
+__device__ __forceinline__ void store8(T* p, const float* v) {
+  if constexpr (sizeof(T) == 2) {
+    store_vec(p, v);
+  } else {
+    store_vec(p, v);
+    store_vec(p + 4, v + 4);
+  }
+}
+
+// stage: fp32 tile [BM][BN + 4] in LDS. tn, m0: tile origin.
+template <typename T, int BM, int BN, int NT>
+__device__ void gemm_epilogue(const GemmArgs& g, const float* stage, int m0, int tn) {
+  constexpr int LD = BN + 4;
+  if (g.epi == EPI_SWIGLU) {
+    constexpr int H = BN / 2;
+    for (int e = threadIdx.x; e < BM * (H / 8); e += NT) {
+      const int rr = e / (H / 8), cc = (e % (H / 8)) * 8;
+      const int m = m0 + rr;
+      if (m >= g.M) continue;
+      float y[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        float gate = stage[rr * LD + cc + i], up = stage[rr * LD + H + cc + i];
+        y[i] = silu(gate) * up;
+      }
+      store8((T*)g.out + int64_t(m) * g.ldo + tn * H + cc, y);
+    }
+    return;
+  }
+  const int n0 = tn * BN;
+  for (int e = threadIdx.x; e < BM * (BN / 8); e += NT) {
+    const int rr = e / (BN / 8), cc = (e % (BN / 8)) * 8;
+    const int m = m0 + rr, n = n0 + cc;
+    if (m >= g.M || n >= g.N) continue;
+    const int b = m / g.kk, j = m - b * g.kk;
+    const int pos = g.idx ? clamp_pos(g.idx[m], g.T) : j;
+    float v[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = stage[rr * LD + cc + i];
+    if (g.bias) {
+      float bv[8];
+      load8((const T*)g.bias + n, bv);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] += bv[i];
+    }
+    switch (g.epi) {
+      case EPI_QKV_ROPE: {
+        const int hd = g.hd, qcols = g.Hq * hd, kcols = g.Hkv * hd;
+        T* dst;
+        bool rot;
+        if (n < qcols) {
+          dst = (T*)g.q + ((int64_t(b) * g.Hq + n / hd) * g.kk + j) * hd + (n % hd);
+          rot = true;
+        } else if (n < qcols + kcols) {
+          const int c = n - qcols;
+          dst = (T*)g.k + ((int64_t(b) * g.Hkv + c / hd) * g.kk + j) * hd + (c % hd);
+          rot = true;
+        } else {
+          const int c = n - qcols - kcols;
+          dst = (T*)g.v + ((int64_t(b) * g.Hkv + c / hd) * g.kk + j) * hd + (c % hd);
+          rot = false;
+        }
+        const int dim0 = n % hd, half = g.R / 2;
+        if (rot && dim0 < g.R) {
+          float out[8];
+#pragma unroll
+          for (int i = 0; i < 8; ++i) {
+            const int dim = dim0 + i;
+            if (dim >= g.R) {
+              out[i] = v[i];
+              continue;
+            }
+            const bool lo = dim < half;
+            const int pdim = lo ? dim + half : dim - half;
+            float xp = stage[rr * LD + cc - dim0 + pdim];
+            if (g.bias) xp += Elem<T>::to_f(((const T*)g.bias)[n - dim0 + pdim]);
+            const float* cs = g.rope + (int64_t(pos) * half + (lo ? dim : dim - half)) * 2;
+            out[i] = lo ? v[i] * cs[0] - xp * cs[1] : v[i] * cs[0] + xp * cs[1];
+          }
+          store8(dst, out);
+        } else {
+          store8(dst, v);
+        }
+        break;
+      }
+      case EPI_BIAS_GELU: {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[i] = gelu_erf(v[i]);
+        store8((T*)g.out + int64_t(m) * g.ldo + n, v);
+        break;
+      }
+      case EPI_RESID_STORE: {
+        float xr[8];
+        load8((const T*)g.x + (int64_t(b) * g.T + pos) * g.N + n, xr);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[i] += xr[i];
+        store8((T*)g.out + int64_t(m) * g.ldo + n, v);
+        break;
+      }
+      case EPI_RESID_SCATTER: {
+        if (g.bias2) {
+          float bv[8];
+          load8((const T*)g.bias2 + n, bv);
+#pragma unroll
+          for (int i = 0; i < 8; ++i) v[i] += bv[i];
+        }
+        T* dst = (T*)g.x + (int64_t(b) * g.T + pos) * g.N + n;
+        float xr[8];
+        if (g.res) load8((const T*)g.res + int64_t(m) * g.N + n, xr);
+        else load8(dst, xr);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[i] += xr[i];
+        store8(dst, v);
+        break;
+      }
+      default: break;
+    }
+  }
+}
+
+// ----------------------------------------------------------- bf16 MFMA GEMM
+
+constexpr int kBM = 128, kBN = 128, kBK = 64;
+constexpr int kWM = 64, kWN = 64;
+constexpr int kThreads = 256;
+constexpr int kStageLD = kBN + 4;
+constexpr int kTileBytes = 2 * (kBM + kBN) * kBK * 2;       // double-buffered A and B tiles
+constexpr int kStageBytes = kBM * kStageLD * 4;             // fp32 epilogue tile
+constexpr int kSmemBytes = kTileBytes > kStageBytes ? kTileBytes : kStageBytes;
+
+// Row of the B operand (weight matrix) that tile row r of column tile tn reads.
+__device__ __forceinline__ int b_row(const GemmArgs& g, int tn, int r) {
+  if (g.epi == EPI_SWIGLU) {
+    constexpr int H = kBN / 2;
+    return r < H ? tn * H + r : g.f + tn * H + (r - H);
+  }
+  int n = tn * kBN + r;
+  return n < g.N ? n : g.N - 1;
+}
+
+__global__ __launch_bounds__(kThreads, 2) void gemm_bf16_kernel(GemmArgs g) {
+  __shared__ __attribute__((aligned(16))) char smem[kSmemBytes];
+  uint16_t* As = reinterpret_cast<uint16_t*>(smem);
+  uint16_t* Bs = As + 2 * kBM * kBK;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int r16 = lane & 15, grp = lane >> 4;
+  const int tn = blockIdx.x, tm = blockIdx.y;
+  const int m0 = tm * kBM;
+
+  // this thread's four A rows and four B rows (tile rows tid/8 + 32 i), chunk tid%8
+  const int lrow = tid >> 3, lch = tid & 7;
+  const uint16_t* arow[4];
+  const uint16_t* arow2[4];
+  const uint16_t* brow[4];
+  const uint16_t* brow2[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    int m = m0 + lrow + 32 * i;
+    if (m > g.M - 1) m = g.M - 1;
+    arow[i] = (const uint16_t*)g.a + int64_t(m) * g.lda;
+    arow2[i] = g.a2 ? (const uint16_t*)g.a2 + int64_t(m) * g.lda2 : nullptr;
+    const int n = b_row(g, tn, lrow + 32 * i);
+    brow[i] = (const uint16_t*)g.b + int64_t(n) * g.ldb;
+    brow2[i] = g.b2 ? (const uint16_t*)g.b2 + int64_t(n) * g.ldb2 : nullptr;
+  }
+
+  u32x4 ra[4], rb[4];
+  auto gload = [&](int kt) {
+    const int k0 = kt * kBK;
+    const bool second = k0 >= g.K1;
+    const int kc = (second ? k0 - g.K1 : k0) + lch * 8;
+    const bool ok = k0 + lch * 8 < g.K;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const uint16_t* pa = (second ? arow2[i] : arow[i]) + kc;
+      const uint16_t* pb = (second ? brow2[i] : brow[i]) + kc;
+      ra[i] = ok ? *reinterpret_cast<const u32x4*>(pa) : u32x4{0, 0, 0, 0};
+      rb[i] = ok ? *reinterpret_cast<const u32x4*>(pb) : u32x4{0, 0, 0, 0};
+    }
+  };
+  auto lstore = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = lrow + 32 * i;
+      const int off = row * kBK + ((lch ^ (row & 7)) << 3);
+      *reinterpret_cast<u32x4*>(As + buf * kBM * kBK + off) = ra[i];
+      *reinterpret_cast<u32x4*>(Bs + buf * kBN * kBK + off) = rb[i];
+    }
+  };
+
+  f32x4 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const int nk = (g.K + kBK - 1) / kBK;
+  gload(0);
+  lstore(0);
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    const int cur = kt & 1;
+    if (kt + 1 < nk) gload(kt + 1);
+    const uint16_t* At = As + cur * kBM * kBK;
+    const uint16_t* Bt = Bs + cur * kBN * kBK;
+#pragma unroll
+    for (int ks = 0; ks < kBK / 32; ++ks) {
+      bf16x8 af[4], bfr[4];
+      const int ch = ks * 4 + grp;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int ar = wm * kWM + i * 16 + r16;
+        af[i] = *reinterpret_cast<const bf16x8*>(At + ar * kBK + ((ch ^ (ar & 7)) << 3));
+        const int br = wn * kWN + i * 16 + r16;
+        bfr[i] = *reinterpret_cast<const bf16x8*>(Bt + br * kBK + ((ch ^ (br & 7)) << 3));
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+    }
+    if (kt + 1 < nk) lstore(cur ^ 1);
+    __syncthreads();
+  }
+
+  // accumulator element (i, j, e) is C[wm*64 + 16 i + 4 grp + e][wn*64 + 16 j + r16]
+  float* stage = reinterpret_cast<float*>(smem);
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        stage[(wm * kWM + 16 * i + 4 * grp + e) * kStageLD + wn * kWN + 16 * j + r16] = acc[i][j][e];
+  __syncthreads();
+  gemm_epilogue<uint16_t, kBM, kBN, kThreads>(g, stage, m0, tn);
+}
+
+// ------------------------------------------------------------ fp32 GEMM
+
+constexpr int kFBM = 32, kFBN = 128, kFBK = 32;
+
+__global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g) {
+  __shared__ float As[kFBK][kFBM + 4];
+  __shared__ float Bs[kFBK][kFBN + 4];
+  __shared__ float stage[kFBM * (kFBN + 4)];
+  const int tid = threadIdx.x;
+  const int tn = blockIdx.x, tm = blockIdx.y, m0 = tm * kFBM;
+  const int tr = tid / 32, tc = tid % 32;  // 4 rows x 4 cols per thread
+  float acc[4][4] = {};
+  for (int k0 = 0; k0 < g.K; k0 += kFBK) {
+    const bool second = k0 >= g.K1;
+    {  // A: 32 rows x 32 k, one float4 per thread
+      const int row = tid / 8, c4 = (tid % 8) * 4;
+      int m = m0 + row;
+      if (m > g.M - 1) m = g.M - 1;
+      float v[4] = {0.f, 0.f, 0.f, 0.f};
+      if (k0 + c4 < g.K) {
+        const float* p = second ? (const float*)g.a2 + int64_t(m) * g.lda2 + (k0 - g.K1) + c4
+                                : (const float*)g.a + int64_t(m) * g.lda + k0 + c4;
+        load_vec(p, v);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) As[c4 + i][row] = v[i];
+    }
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {  // B: 128 rows x 32 k
+      const int e = tid + 256 * t;
+      const int row = e / 8, c4 = (e % 8) * 4;
+      int n;
+      if (g.epi == EPI_SWIGLU) n = row < kFBN / 2 ? tn * (kFBN / 2) + row : g.f + tn * (kFBN / 2) + row - kFBN / 2;
+      else n = min(tn * kFBN + row, g.N - 1);
+      float v[4] = {0.f, 0.f, 0.f, 0.f};
+      if (k0 + c4 < g.K) {
+        const float* p = second ? (const float*)g.b2 + int64_t(n) * g.ldb2 + (k0 - g.K1) + c4
+                                : (const float*)g.b + int64_t(n) * g.ldb + k0 + c4;
+        load_vec(p, v);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) Bs[c4 + i][row] = v[i];
+    }
+    __syncthreads();
+#pragma unroll 8
+    for (int kk = 0; kk < kFBK; ++kk) {
+      float av[4], bv[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        av[i] = As[kk][tr * 4 + i];
+        bv[i] = Bs[kk][tc * 4 + i];
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(av[i], bv[j], acc[i][j]);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) stage[(tr * 4 + i) * (kFBN + 4) + tc * 4 + j] = acc[i][j];
+  __syncthreads();
+  gemm_epilogue<float, kFBM, kFBN, 256>(g, stage, m0, tn);
+}
+
+hipError_t launch_gemm(const GemmArgs& g, hipStream_t s) {
+  if (g.M == 0 || g.N == 0) return hipSuccess;
+  if (g.dtype == DSF_BF16) {
+    const int ntn = g.epi == EPI_SWIGLU ? g.f / (kBN / 2) : (g.N + kBN - 1) / kBN;
+    dim3 grid(ntn, (g.M + kBM - 1) / kBM);
+    gemm_bf16_kernel<<<grid, kThreads, 0, s>>>(g);
+  } else {
+    const int ntn = g.epi == EPI_SWIGLU ? g.f / (kFBN / 2) : (g.N + kFBN - 1) / kFBN;
+    dim3 grid(ntn, (g.M + kFBM - 1) / kFBM);
+    gemm_f32_kernel<<<grid, 256, 0, s>>>(g);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace dsf

@@ -1,0 +1,543 @@
+// Streaming kernels of the depth-sparse layer on gfx950: RoPE table,
+// similarity statistic (Eq. 4), router (Section 3.4), per-sequence Top-K,
+// gather / scatter of hidden rows, and fused gather + LayerNorm / RMSNorm.
+//
+// These kernels move far more bytes than they compute on, so they are written
+// for HBM: 16-byte vector accesses, one wavefront per row, deterministic
+// fixed-order reductions (no floating-point atomics).
+#include "dsf_device.h"
+#include "dsf_internal.h"
+
+namespace dsf {
+
+// --------------------------------------------------------------------- RoPE
+
+__global__ void rope_table_kernel(float* table, int T, int half, int R, double theta) {
+  int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= T * half) return;
+  int p = i / half, j = i % half;
+  double ang = double(p) * pow(theta, -2.0 * double(j) / double(R));
+  double sn, cs;
+  sincos(ang, &sn, &cs);
+  table[2 * i] = float(cs);
+  table[2 * i + 1] = float(sn);
+}
+
+hipError_t launch_rope_table(float* table, int T, int R, double theta, hipStream_t s) {
+  int half = R / 2, n = T * half;
+  if (n == 0) return hipSuccess;
+  TimedScope ts(DSF_KIND_OTHER, s);
+  rope_table_kernel<<<(n + 255) / 256, 256, 0, s>>>(table, T, half, R, theta);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------ similarity statistic, Eq. 4
+
+constexpr int kSimMaxGrid = 1024;
+
+int sim_grid(int64_t n_tokens) {
+  int64_t g = (n_tokens + 3) / 4;
+  return int(g < 1 ? 1 : (g > kSimMaxGrid ? kSimMaxGrid : g));
+}
+
+// One wavefront per token row; products and sums in fp64 (products of bf16 or
+// fp32 values are exact in fp64). Each block writes the sum of its tokens'
+// cosines, in a fixed order, to partial[blockIdx.x].
+template <typename T>
+__global__ __launch_bounds__(256) void sim_partial_kernel(const T* a, const T* c, int64_t n, int d,
+                                                          float* per_tok, double* partial) {
+  constexpr int V = Elem<T>::kVec;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int nvec = d / V;
+  double wave_acc = 0.0;
+  for (int64_t t = int64_t(blockIdx.x) * 4 + w; t < n; t += int64_t(gridDim.x) * 4) {
+    const T* ra = a + t * d;
+    const T* rc = c + t * d;
+    double dot = 0.0, aa = 0.0, cc = 0.0;
+    for (int ch = lane; ch < nvec; ch += 64) {
+      float va[V], vc[V];
+      load_vec(ra + ch * V, va);
+      load_vec(rc + ch * V, vc);
+#pragma unroll
+      for (int i = 0; i < V; ++i) {
+        double x = va[i], y = vc[i];
+        dot = fma(x, y, dot);
+        aa = fma(x, x, aa);
+        cc = fma(y, y, cc);
+      }
+    }
+    dot = wave_sum(dot);
+    aa = wave_sum(aa);
+    cc = wave_sum(cc);
+    double den = sqrt(aa) * sqrt(cc);
+    double cs = dot / (den > 1e-8 ? den : 1e-8);
+    if (lane == 0 && per_tok) per_tok[t] = float(cs);
+    wave_acc += cs;
+  }
+  __shared__ double wsum[4];
+  if (lane == 0) wsum[w] = wave_acc;
+  __syncthreads();
+  if (threadIdx.x == 0) partial[blockIdx.x] = ((wsum[0] + wsum[1]) + wsum[2]) + wsum[3];
+}
+
+// Single block: fixed-order sum of the partials, then accum += (sum, n).
+__global__ __launch_bounds__(256) void sim_finish_kernel(const double* partial, int np, int64_t n,
+                                                         double* accum) {
+  __shared__ double red[256];
+  double v = 0.0;
+  for (int i = threadIdx.x; i < np; i += 256) v += partial[i];
+  red[threadIdx.x] = v;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if (threadIdx.x < o) red[threadIdx.x] += red[threadIdx.x + o];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    accum[0] += red[0];
+    accum[1] += double(n);
+  }
+}
+
+hipError_t launch_sim_stats(int dtype, const void* a, const void* c, int64_t n, int d, float* per_tok,
+                            double* partial, double* accum, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  TimedScope ts(DSF_KIND_SIM, s);
+  int g = sim_grid(n);
+  if (dtype == DSF_BF16)
+    sim_partial_kernel<uint16_t><<<g, 256, 0, s>>>((const uint16_t*)a, (const uint16_t*)c, n, d, per_tok, partial);
+  else
+    sim_partial_kernel<float><<<g, 256, 0, s>>>((const float*)a, (const float*)c, n, d, per_tok, partial);
+  sim_finish_kernel<<<1, 256, 0, s>>>(partial, g, n, accum);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------ router, Sec. 3.4
+
+// bf16 router on MFMA. A wavefront scores 32 tokens (two 16-row MFMA blocks)
+// against all d_r hidden units (DR / 16 column blocks). Each lane streams 64
+// contiguous bytes of its token row per 128-wide k chunk; the MFMA's k slots
+// are filled in that streaming order and W1 is read with the same order, so
+// the contraction is unchanged.
+template <int DR>
+__global__ __launch_bounds__(256) void router_bf16_kernel(const uint16_t* __restrict__ x, int64_t n, int d,
+                                                          const uint16_t* __restrict__ w1,
+                                                          const uint16_t* __restrict__ b1,
+                                                          const uint16_t* __restrict__ w2, float b2,
+                                                          float* __restrict__ scores) {
+  constexpr int RB = 2, NB = DR / 16;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int r = lane & 15, g = lane >> 4;
+  const int64_t row0 = (int64_t(blockIdx.x) * 4 + w) * (16 * RB);
+  if (row0 >= n) return;
+  const uint16_t* xr[RB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    int64_t row = row0 + rb * 16 + r;
+    if (row > n - 1) row = n - 1;  // clamp: rows past the end are computed and dropped
+    xr[rb] = x + row * d;
+  }
+  f32x4 acc[RB][NB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) acc[rb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  int kc = 0;
+  for (; kc + 128 <= d; kc += 128) {
+    bf16x8 xa[RB][4], wb[NB][4];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+      for (int s4 = 0; s4 < 4; ++s4)
+        xa[rb][s4] = *reinterpret_cast<const bf16x8*>(xr[rb] + kc + 32 * g + 8 * s4);
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int s4 = 0; s4 < 4; ++s4)
+        wb[nb][s4] = *reinterpret_cast<const bf16x8*>(w1 + (16 * nb + r) * int64_t(d) + kc + 32 * g + 8 * s4);
+#pragma unroll
+    for (int s4 = 0; s4 < 4; ++s4)
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+          acc[rb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[rb][s4], wb[nb][s4], acc[rb][nb], 0, 0, 0);
+  }
+  // tail: 32-wide steps, 8-element pieces past d are zero
+  for (; kc < d; kc += 32) {
+    const int k0 = kc + 8 * g;
+    const bool ok = k0 < d;
+    bf16x8 zero = {};
+    bf16x8 xa[RB], wb[NB];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) xa[rb] = ok ? *reinterpret_cast<const bf16x8*>(xr[rb] + k0) : zero;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+      wb[nb] = ok ? *reinterpret_cast<const bf16x8*>(w1 + (16 * nb + r) * int64_t(d) + k0) : zero;
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+        acc[rb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[rb], wb[nb], acc[rb][nb], 0, 0, 0);
+  }
+  // lane holds hidden[token 16 rb + 4 g + i][unit 16 nb + r]
+  float wv[NB], bv[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    wv[nb] = bf2f(w2[16 * nb + r]);
+    bv[nb] = b1 ? bf2f(b1[16 * nb + r]) : 0.f;
+  }
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float v = 0.f;
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        float h = acc[rb][nb][i] + bv[nb];
+        v += wv[nb] * (h > 0.f ? h : 0.f);
+      }
+      v += __shfl_xor(v, 1, 64);
+      v += __shfl_xor(v, 2, 64);
+      v += __shfl_xor(v, 4, 64);
+      v += __shfl_xor(v, 8, 64);
+      int64_t row = row0 + rb * 16 + 4 * g + i;
+      if (r == 0 && row < n) scores[row] = v + b2;
+    }
+  }
+}
+
+// fp32 router: one wavefront per token, one hidden unit at a time.
+__global__ __launch_bounds__(256) void router_f32_kernel(const float* __restrict__ x, int64_t n, int d, int dr,
+                                                         const float* __restrict__ w1, const float* __restrict__ b1,
+                                                         const float* __restrict__ w2, float b2,
+                                                         float* __restrict__ scores) {
+  const int lane = threadIdx.x & 63;
+  const int64_t t = int64_t(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  if (t >= n) return;
+  const float* row = x + t * d;
+  float score = 0.f;
+  for (int j = 0; j < dr; ++j) {
+    const float* wr = w1 + int64_t(j) * d;
+    float h = 0.f;
+    for (int i = lane; i < d; i += 64) h = fmaf(row[i], wr[i], h);
+    h = wave_sum(h) + (b1 ? b1[j] : 0.f);
+    score = fmaf(w2[j], h > 0.f ? h : 0.f, score);
+  }
+  if (lane == 0) scores[t] = score + b2;
+}
+
+hipError_t launch_router(int dtype, const void* x, int64_t n, int d, int d_r, const void* w1,
+                         const void* b1, const void* w2, float b2, float* scores, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  TimedScope ts(DSF_KIND_ROUTER, s);
+  if (dtype == DSF_F32) {
+    router_f32_kernel<<<unsigned((n + 3) / 4), 256, 0, s>>>((const float*)x, n, d, d_r, (const float*)w1,
+                                                            (const float*)b1, (const float*)w2, b2, scores);
+    return hipGetLastError();
+  }
+  unsigned grid = unsigned((n + 127) / 128);
+  auto X = (const uint16_t*)x;
+  auto W1 = (const uint16_t*)w1;
+  auto B1 = (const uint16_t*)b1;
+  auto W2 = (const uint16_t*)w2;
+  switch (d_r) {
+    case 16: router_bf16_kernel<16><<<grid, 256, 0, s>>>(X, n, d, W1, B1, W2, b2, scores); break;
+    case 32: router_bf16_kernel<32><<<grid, 256, 0, s>>>(X, n, d, W1, B1, W2, b2, scores); break;
+    case 48: router_bf16_kernel<48><<<grid, 256, 0, s>>>(X, n, d, W1, B1, W2, b2, scores); break;
+    case 64: router_bf16_kernel<64><<<grid, 256, 0, s>>>(X, n, d, W1, B1, W2, b2, scores); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+// -------------------------------------------------------- Top-K, Section 3.4
+
+// Order-preserving key: larger score -> larger key; -0 == +0; NaN -> 0 (lowest).
+__device__ __forceinline__ uint32_t score_key(float f) {
+  if (f != f) return 0u;
+  uint32_t u = __float_as_uint(f);
+  if (u == 0x80000000u) u = 0u;
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+constexpr int kTopkThreads = 1024;
+constexpr int kTopkWaves = kTopkThreads / 64;
+
+// Exclusive count of `flag` over the block in thread order; `total` gets the
+// block's count. Uses wave ballots and one LDS slot per wave.
+__device__ __forceinline__ uint32_t block_excl_count(bool flag, uint32_t* wave_tot, uint32_t& total) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  uint64_t m = __ballot(flag);
+  uint32_t within = __popcll(m & ((uint64_t(1) << lane) - 1));
+  if (lane == 0) wave_tot[w] = __popcll(m);
+  __syncthreads();
+  uint32_t before = 0, tot = 0;
+#pragma unroll
+  for (int i = 0; i < kTopkWaves; ++i) {
+    uint32_t c = wave_tot[i];
+    before += (i < w) ? c : 0u;
+    tot += c;
+  }
+  __syncthreads();
+  total = tot;
+  return before + within;
+}
+
+// One block per sequence. Radix select (8 bits per pass, most significant
+// first) finds the key of the k-th largest score and how many of the keys
+// equal to it are kept; a final ordered pass keeps every larger key and the
+// lowest-positioned equal keys, writing positions in ascending order.
+__global__ __launch_bounds__(kTopkThreads) void topk_kernel(const float* __restrict__ scores, int T, int k,
+                                                            int32_t* __restrict__ idx) {
+  const float* sc = scores + int64_t(blockIdx.x) * T;
+  int32_t* out = idx + int64_t(blockIdx.x) * k;
+  __shared__ uint32_t hist[256];
+  __shared__ uint32_t wave_tot[kTopkWaves];
+  __shared__ uint32_t sh_digit, sh_remaining;
+  const int tid = threadIdx.x;
+
+  uint32_t prefix = 0, mask = 0, remaining = uint32_t(k);
+  for (int pass = 0; pass < 4; ++pass) {
+    const int shift = 24 - 8 * pass;
+    if (tid < 256) hist[tid] = 0;
+    __syncthreads();
+    for (int t = tid; t < T; t += kTopkThreads) {
+      uint32_t key = score_key(sc[t]);
+      if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+    }
+    __syncthreads();
+    if (tid < 64) {
+      // lane L owns digits 255-4L .. 252-4L (descending); exclusive scan over lanes
+      uint32_t c[4], tot = 0;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        c[e] = hist[255 - 4 * tid - e];
+        tot += c[e];
+      }
+      uint32_t incl = tot;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        uint32_t v = __shfl_up(incl, o, 64);
+        if (tid >= o) incl += v;
+      }
+      uint32_t cum = incl - tot;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        if (cum < remaining && remaining <= cum + c[e]) {
+          sh_digit = uint32_t(255 - 4 * tid - e);
+          sh_remaining = remaining - cum;
+        }
+        cum += c[e];
+      }
+    }
+    __syncthreads();
+    prefix |= sh_digit << shift;
+    mask |= 255u << shift;
+    remaining = sh_remaining;
+    __syncthreads();
+  }
+  // prefix is now the k-th largest key; `remaining` equal keys are kept.
+  uint32_t run_eq = 0, run_sel = 0;
+  for (int base = 0; base < T; base += kTopkThreads) {
+    const int t = base + tid;
+    const bool valid = t < T;
+    const uint32_t key = valid ? score_key(sc[t]) : 0u;
+    const bool eq = valid && key == prefix;
+    uint32_t tot_eq, tot_sel;
+    const uint32_t eq_before = run_eq + block_excl_count(eq, wave_tot, tot_eq);
+    const bool sel = valid && (key > prefix || (eq && eq_before < remaining));
+    const uint32_t sel_before = run_sel + block_excl_count(sel, wave_tot, tot_sel);
+    if (sel && sel_before < uint32_t(k)) out[sel_before] = t;
+    run_eq += tot_eq;
+    run_sel += tot_sel;
+  }
+}
+
+hipError_t launch_topk(const float* scores, int B, int T, int k, int32_t* idx, hipStream_t s) {
+  if (k == 0 || B == 0) return hipSuccess;
+  TimedScope ts(DSF_KIND_TOPK, s);
+  topk_kernel<<<B, kTopkThreads, 0, s>>>(scores, T, k, idx);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------- gather / scatter
+
+template <typename T>
+__global__ __launch_bounds__(256) void gather_kernel(const T* __restrict__ x, int Tlen, int d,
+                                                     const int32_t* __restrict__ idx, int k,
+                                                     T* __restrict__ out, int64_t nvec) {
+  constexpr int V = Elem<T>::kVec;
+  const int vpr = d / V;
+  for (int64_t v = int64_t(blockIdx.x) * 256 + threadIdx.x; v < nvec; v += int64_t(gridDim.x) * 256) {
+    int64_t row = v / vpr;
+    int c = int(v - row * vpr);
+    int64_t b = row / k;
+    const T* src = x + (b * Tlen + clamp_pos(idx[row], Tlen)) * d + c * V;
+    *reinterpret_cast<u32x4*>(out + row * d + c * V) = *reinterpret_cast<const u32x4*>(src);
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void scatter_kernel(T* __restrict__ x, const T* __restrict__ delta, int Tlen,
+                                                      int d, const int32_t* __restrict__ idx, int k,
+                                                      int64_t nvec) {
+  constexpr int V = Elem<T>::kVec;
+  const int vpr = d / V;
+  for (int64_t v = int64_t(blockIdx.x) * 256 + threadIdx.x; v < nvec; v += int64_t(gridDim.x) * 256) {
+    int64_t row = v / vpr;
+    int c = int(v - row * vpr);
+    int64_t b = row / k;
+    T* dst = x + (b * Tlen + clamp_pos(idx[row], Tlen)) * d + c * V;
+    float a[V], e[V];
+    load_vec(dst, a);
+    load_vec(delta + row * d + c * V, e);
+#pragma unroll
+    for (int i = 0; i < V; ++i) a[i] += e[i];
+    store_vec(dst, a);
+  }
+}
+
+static unsigned stream_grid(int64_t nvec) {
+  int64_t g = (nvec + 255) / 256;
+  return unsigned(g > 8192 ? 8192 : (g < 1 ? 1 : g));
+}
+
+hipError_t launch_gather(int dtype, const void* x, int B, int T, int d, const int32_t* idx, int k,
+                         void* out, hipStream_t s) {
+  int64_t rows = int64_t(B) * k;
+  if (rows == 0) return hipSuccess;
+  TimedScope ts(DSF_KIND_GATHER, s);
+  if (dtype == DSF_BF16) {
+    int64_t nvec = rows * (d / 8);
+    gather_kernel<uint16_t><<<stream_grid(nvec), 256, 0, s>>>((const uint16_t*)x, T, d, idx, k, (uint16_t*)out, nvec);
+  } else {
+    int64_t nvec = rows * (d / 4);
+    gather_kernel<float><<<stream_grid(nvec), 256, 0, s>>>((const float*)x, T, d, idx, k, (float*)out, nvec);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_scatter(int dtype, void* x, const void* delta, int B, int T, int d, const int32_t* idx,
+                          int k, hipStream_t s) {
+  int64_t rows = int64_t(B) * k;
+  if (rows == 0) return hipSuccess;
+  TimedScope ts(DSF_KIND_SCATTER, s);
+  if (dtype == DSF_BF16) {
+    int64_t nvec = rows * (d / 8);
+    scatter_kernel<uint16_t><<<stream_grid(nvec), 256, 0, s>>>((uint16_t*)x, (const uint16_t*)delta, T, d, idx, k, nvec);
+  } else {
+    int64_t nvec = rows * (d / 4);
+    scatter_kernel<float><<<stream_grid(nvec), 256, 0, s>>>((float*)x, (const float*)delta, T, d, idx, k, nvec);
+  }
+  return hipGetLastError();
+}
+
+__global__ __launch_bounds__(256) void copy_kernel(const u32x4* __restrict__ src, u32x4* __restrict__ dst, int64_t n) {
+  for (int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x; i < n; i += int64_t(gridDim.x) * 256) dst[i] = src[i];
+}
+
+hipError_t launch_copy(const void* src, void* dst, size_t bytes, hipStream_t s) {
+  int64_t n = int64_t(bytes / 16);
+  if (n == 0) return hipSuccess;
+  TimedScope ts(DSF_KIND_OTHER, s);
+  copy_kernel<<<stream_grid(n), 256, 0, s>>>((const u32x4*)src, (u32x4*)dst, n);
+  return hipGetLastError();
+}
+
+// ------------------------------------------- gather + LayerNorm / RMSNorm
+
+// One wavefront per output row; the row stays in registers (MAXC vectors per
+// lane) so it is read from HBM once for both normalisations.
+template <typename T, int MAXC>
+__global__ __launch_bounds__(256) void norm_kernel(NormArgs a) {
+  constexpr int V = Elem<T>::kVec;
+  const int lane = threadIdx.x & 63;
+  const int64_t rows = int64_t(a.B) * a.kk;
+  const int64_t r = int64_t(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  if (r >= rows) return;
+  const int d = a.d, nvec = d / V;
+  const T* src;
+  if (a.src_rows == 0) {
+    src = (const T*)a.src + r * d;
+  } else {
+    int64_t b = r / a.kk;
+    int64_t j = r - b * a.kk;
+    int64_t pos = a.idx ? clamp_pos(a.idx[r], a.src_rows) : j;
+    src = (const T*)a.src + (b * a.src_rows + pos) * d;
+  }
+  float v[MAXC][V];
+  float sum = 0.f;
+#pragma unroll
+  for (int c = 0; c < MAXC; ++c) {
+    int ch = lane + 64 * c;
+    if (ch < nvec) {
+      load_vec(src + ch * V, v[c]);
+#pragma unroll
+      for (int i = 0; i < V; ++i) sum += v[c][i];
+    }
+  }
+  float mean = 0.f, var;
+  if (a.rms) {
+    float sq = 0.f;
+#pragma unroll
+    for (int c = 0; c < MAXC; ++c)
+      if (lane + 64 * c < nvec)
+#pragma unroll
+        for (int i = 0; i < V; ++i) sq += v[c][i] * v[c][i];
+    var = wave_sum(sq) / float(d);
+  } else {
+    mean = wave_sum(sum) / float(d);
+    float sq = 0.f;
+#pragma unroll
+    for (int c = 0; c < MAXC; ++c)
+      if (lane + 64 * c < nvec)
+#pragma unroll
+        for (int i = 0; i < V; ++i) {
+          float t = v[c][i] - mean;
+          sq += t * t;
+        }
+    var = wave_sum(sq) / float(d);
+  }
+  const float rstd = 1.0f / sqrtf(var + a.eps);
+  for (int o = 0; o < 2; ++o) {
+    const T* w = (const T*)(o == 0 ? a.w1 : a.w2);
+    const T* bb = (const T*)(o == 0 ? a.b1 : a.b2);
+    T* out = (T*)(o == 0 ? a.out1 : a.out2);
+    if (!out) continue;
+#pragma unroll
+    for (int c = 0; c < MAXC; ++c) {
+      int ch = lane + 64 * c;
+      if (ch < nvec) {
+        float wv[V], bv[V], y[V];
+        load_vec(w + ch * V, wv);
+        if (bb) load_vec(bb + ch * V, bv);
+#pragma unroll
+        for (int i = 0; i < V; ++i) y[i] = (v[c][i] - mean) * rstd * wv[i] + (bb ? bv[i] : 0.f);
+        store_vec(out + r * d + ch * V, y);
+      }
+    }
+  }
+}
+
+template <typename T>
+static hipError_t launch_norm_t(const NormArgs& a, hipStream_t s) {
+  constexpr int V = Elem<T>::kVec;
+  int per_lane = (a.d / V + 63) / 64;
+  unsigned grid = unsigned((int64_t(a.B) * a.kk + 3) / 4);
+  if (per_lane <= 1) norm_kernel<T, 1><<<grid, 256, 0, s>>>(a);
+  else if (per_lane <= 2) norm_kernel<T, 2><<<grid, 256, 0, s>>>(a);
+  else if (per_lane <= 4) norm_kernel<T, 4><<<grid, 256, 0, s>>>(a);
+  else if (per_lane <= 8) norm_kernel<T, 8><<<grid, 256, 0, s>>>(a);
+  else if (per_lane <= 16) norm_kernel<T, 16><<<grid, 256, 0, s>>>(a);
+  else return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t launch_norm(const NormArgs& a, hipStream_t s) {
+  if (int64_t(a.B) * a.kk == 0) return hipSuccess;
+  TimedScope ts(DSF_KIND_NORM, s);
+  return a.dtype == DSF_BF16 ? launch_norm_t<uint16_t>(a, s) : launch_norm_t<float>(a, s);
+}
+
+}  // namespace dsf
