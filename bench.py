@@ -1,0 +1,258 @@
+#!/usr/bin/env python3
+"""Depth-sparse stack throughput on one MI355X.
+
+One step is one forward pass of the whole depth-sparse stack (router, Top-K,
+gather + norm, QKV + RoPE, attention over kept tokens, output and FFN
+projections, residual scatter, for every layer) over one batch of synthetic
+hidden states at fixed per-layer retention. The retention ratios come from
+the allocation of Eqs. 5-8 (run by the library's host code) on the
+workload's similarity profile, or on similarities measured by the GPU
+calibration pass (similarity statistic of Eq. 4 on the dense stack), which is
+timed separately and reported as `calibration_ms`.
+
+Inputs are resident in HBM before the timed region: every timed step runs on
+its own pristine copy of the hidden states, prepared beforehand.
+
+Prints one JSON line. `roofline` is for the dominant kernel (the last GEMM
+of each layer, which for GPT-NeoX fuses the attention-output and FFN-down
+projections along K), timed with HIP events around each of its launches
+inside the timed region. `cpu_baseline` times the CPU oracle on a bounded
+sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "depth-sparse stack tokens/sec at fixed r_l; MFMA util % and HBM GB/s % of peak"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def retention(P, w, calib_s=None):
+    if w.retention is not None:
+        return list(w.retention)
+    s = calib_s if w.similarity is None else list(w.similarity)
+    return P.retention_from_similarity(s, w.target, w.tau)
+
+
+def cpu_baseline(w, ks, layers, min_seconds=10.0):
+    """The oracle, as it stands, on whole sequences through `layers` layers.
+
+    Sequences 0, 1, ... are run one after another until at least
+    `min_seconds` have elapsed or the batch is exhausted, which bounds the
+    sample to roughly 10-30 s of CPU work on any host.
+    """
+    from threadpoolctl import threadpool_info
+
+    import synthetic as S
+    from oracle import adadsf_oracle as O
+
+    desc = dict(block=w.block, n_heads=w.n_heads, n_kv_heads=w.n_kv_heads, head_dim=w.head_dim, d_ff=w.d_ff,
+                rotary_dims=w.rotary_dims, rope_theta=w.rope_theta, norm_eps=w.norm_eps)
+    Ws = [{k: (O.f64(v) if hasattr(v, "detach") else v) for k, v in S.layer_weights(w, l).items()}
+          for l in range(layers)]
+    xall = S.hidden_states(w)
+    dt, nseq = 0.0, 0
+    while nseq < w.batch and dt < min_seconds:
+        x = O.f64(xall[nseq:nseq + 1])
+        t0 = time.perf_counter()
+        for l in range(layers):
+            x = O.routed_layer(desc, Ws[l], x, ks[l])["y"]
+        dt += time.perf_counter() - t0
+        nseq += 1
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    tokens = nseq * w.seq * layers / w.n_layers        # stack-equivalent tokens
+    return {"value": tokens / dt, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"sequences 0..{nseq - 1} of {w.batch} ({w.seq} tokens each) through layers 0..{layers - 1} "
+                      f"of {w.n_layers}, run until >= {min_seconds:.0f} s; {dt:.1f} s for {tokens:.0f} "
+                      f"stack-equivalent tokens",
+            "seconds": dt, "cpu_count": os.cpu_count()}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="neox160m")
+    ap.add_argument("--cpu-layers", type=int, default=None, help="layers of the CPU oracle sample (default all)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-dense", action="store_true", help="skip the dense-stack comparison run")
+    ap.add_argument("--only-sparse", action="store_true",
+                    help="launch only the sparse stack (warmup + timed steps): no calibration pass when the "
+                         "workload fixes its similarity profile, no dense run, no breakdown pass, no CPU "
+                         "baseline; used under rocprofv3 so every launch it sees is a timed-shape launch")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: the depth-sparse stack is data-parallel over sequences with no "
+              "exchange in the forward pass, so this build runs and reports the single-GPU shard "
+              "(--gpus 1).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2607_21291_amd as P
+    import synthetic as S
+    from paper_2607_21291_amd import costs as C
+
+    dev = torch.device("cuda:0")
+    w = S.WORKLOADS[args.workload]
+    B, T, L = w.batch, w.seq, w.n_layers
+    dt = w.torch_dtype
+    dcode = P.F32 if w.dtype == "f32" else P.BF16
+    desc = P.make_desc(w.block, w.d_model, w.n_heads, w.n_kv_heads, w.head_dim, w.d_ff, w.rotary_dims,
+                       w.d_router, w.norm_eps, w.rope_theta)
+    log(f"workload {w.name}: L={L} d={w.d_model} B={B} T={T} dtype={w.dtype}")
+    layers = [P.DeviceLayer(S.layer_weights(w, l), dev) for l in range(L)]
+    weights = [dl.weights for dl in layers]
+    x0 = S.hidden_states(w).to(dev)
+    stream = torch.cuda.current_stream()
+
+    if args.only_sparse:
+        args.no_dense = args.no_cpu_baseline = True
+    # calibration pass: dense stack + on-GPU similarity statistic (Eq. 4), allocation (Eqs. 5-8)
+    s_meas, t_cal = None, None
+    if not (args.only_sparse and w.similarity is not None):
+        ws_cal = torch.empty(P.workspace_size(desc, dcode, B, T, T, True), dtype=torch.uint8, device=dev)
+        accum = torch.zeros(L, 2, dtype=torch.float64, device=dev)
+        xc = x0.clone()
+        P.stack_forward(desc, weights, [T] * L, xc, ws_cal, flags=P.FLAG_DENSE, sim_accum=accum)  # warm
+        accum.zero_()
+        xc.copy_(x0)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        P.stack_forward(desc, weights, [T] * L, xc, ws_cal, flags=P.FLAG_DENSE, sim_accum=accum)
+        s_meas = P.sim_finalize(accum)
+        t_cal = time.perf_counter() - t0
+        del ws_cal, xc
+        log(f"calibration pass {t_cal * 1e3:.2f} ms; measured similarity {[round(v, 4) for v in s_meas]}")
+    r = retention(P, w, s_meas)
+    ks = [P.k_from_retention(v, T) for v in r]
+    log(f"k per layer {ks}")
+
+    ws = torch.empty(P.workspace_size(desc, dcode, B, T, max(ks)), dtype=torch.uint8, device=dev)
+    xs = [x0.clone() for _ in range(args.steps)]
+    xw = x0.clone()
+    for _ in range(args.warmup):
+        xw.copy_(x0)
+        P.stack_forward(desc, weights, ks, xw, ws)
+    torch.cuda.synchronize()
+
+    # timed region: K steps, dominant-kernel launches bracketed by HIP events
+    P.timing_enable(args.steps * L + 8, ["gemm_down"])
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        P.stack_forward(desc, weights, ks, xs[i], ws)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    n_dom, ms_dom = P.timing_read("gemm_down")
+    P.timing_enable(0)
+    ms_step = elapsed * 1e3 / args.steps
+    tokens_per_s = B * T / (ms_step / 1e3)
+    log(f"sparse stack {ms_step:.3f} ms/step, {tokens_per_s / 1e6:.3f} M tokens/s")
+
+    # roofline of the dominant kernel: algorithmic FLOPs per launch / its average duration
+    flops_dom = sum(C.gemm_down_flops(w, B, k) for k in ks if k > 0) * args.steps
+    avg_ms = ms_dom / max(n_dom, 1)
+    achieved = flops_dom / (ms_dom / 1e3) / 1e12 if ms_dom > 0 else 0.0
+    roofline = {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+                "kernel": "gemm_bf16_kernel<4> (last GEMM of a layer, residual-scatter epilogue)",
+                "launches": n_dom, "avg_launch_us": avg_ms * 1e3,
+                "flops_per_launch": flops_dom / max(n_dom, 1)}
+
+    # per-kernel breakdown (a separate instrumented pass, every launch bracketed)
+    breakdown = {}
+    if not args.only_sparse:
+        nb = min(args.steps, 10)
+        P.timing_enable(nb * L * 16 + 64)
+        for i in range(nb):
+            xw.copy_(x0)
+            P.stack_forward(desc, weights, ks, xw, ws)
+        torch.cuda.synchronize()
+        for kind in P.KINDS:
+            n, ms = P.timing_read(kind)
+            if n:
+                breakdown[kind] = {"ms_per_step": ms / nb, "launches_per_step": n / nb}
+        P.timing_enable(0)
+
+    # work and achieved rates of the whole step
+    sparse_flops = C.stack_flops(w, B, T, ks, True)
+    gemm_flops = sum(C.proj_flops(w, B, k) for k in ks)
+    attn_flops = sum(C.attn_flops(w, B, k) for k in ks)
+    gemm_ms = sum(v["ms_per_step"] for k, v in breakdown.items() if k.startswith("gemm"))
+    attn_ms = breakdown.get("attn", {}).get("ms_per_step", 0.0)
+    router_ms = breakdown.get("router", {}).get("ms_per_step", 0.0)
+    rates = {
+        "step_tflops": sparse_flops / (ms_step / 1e3) / 1e12,
+        "gemm_tflops": gemm_flops / (gemm_ms / 1e3) / 1e12 if gemm_ms else None,
+        "attn_tflops": attn_flops / (attn_ms / 1e3) / 1e12 if attn_ms else None,
+        "router_gbs": sum(C.router_bytes(w, B, T) for k in ks if k > 0) / (router_ms / 1e3) / 1e9 if router_ms else None,
+    }
+
+    dense = None
+    if not args.no_dense:
+        xd = x0.clone()
+        wsd = torch.empty(P.workspace_size(desc, dcode, B, T, T), dtype=torch.uint8, device=dev)
+        P.stack_forward(desc, weights, [T] * L, xd, wsd, flags=P.FLAG_DENSE)
+        nd = max(3, args.steps // 3)
+        xds = [x0.clone() for _ in range(nd)]
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(nd):
+            P.stack_forward(desc, weights, [T] * L, xds[i], wsd, flags=P.FLAG_DENSE)
+        torch.cuda.synchronize()
+        dense_ms = (time.perf_counter() - t0) * 1e3 / nd
+        dense = {"ms_per_step": dense_ms, "speedup_sparse_vs_dense": dense_ms / ms_step,
+                 "flop_ratio_sparse_over_dense": C.stack_flops(w, B, T, ks, True) / C.stack_flops(w, B, T, [T] * L, False)}
+        log(f"dense stack {dense_ms:.3f} ms/step, speedup {dense_ms / ms_step:.2f}x")
+        del xds, wsd, xd
+
+    out = {
+        "metric": METRIC,
+        "value": tokens_per_s,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic (seeded N(0, 0.02) hidden states and random-init weights of the stated shape)",
+        "config": {"workload": f"{w.name}: {L}-layer {w.block} stack, d={w.d_model}, heads {w.n_heads}/{w.n_kv_heads}"
+                               f"x{w.head_dim}, FFN {w.d_ff}, batch {B} x seq {T}",
+                   "global_batch": B, "seq_len": T, "layers": L, "parallelism": "single GPU",
+                   "mean_retention": sum(r) / L, "k_per_layer": ks},
+        "roofline": roofline,
+        "cpu_baseline": None,
+        "kernel_breakdown": breakdown,
+        "rates": rates,
+        "dense": dense,
+        "calibration_ms": None if t_cal is None else t_cal * 1e3,
+        "similarity_measured": s_meas,
+        "hip_runtime": torch.version.hip,
+    }
+    if not args.no_cpu_baseline:
+        layers_cpu = L if args.cpu_layers is None else min(args.cpu_layers, L)
+        log(f"cpu oracle baseline over {layers_cpu} layers of one sequence")
+        out["cpu_baseline"] = cpu_baseline(w, ks, layers_cpu)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -39,11 +39,39 @@ __device__ __forceinline__ void store8(T* p, const float* v) {
   }
 }
 
-// stage: fp32 tile [BM][BN + 4] in LDS. tn, m0: tile origin.
-template <typename T, int BM, int BN, int NT>
+// RoPE (rotate-half) of the 8 values of one q/k chunk at columns dim0..dim0+7
+// of a head, at position pos. Partner dims (i, i + R/2) are read from the
+// staged row, so any R works. Dims >= R pass through.
+template <typename T>
+__device__ __forceinline__ void rope_chunk(const GemmArgs& g, const float* row, int cc, int n, int dim0, int pos,
+                                           float* v) {
+  const int half = g.R / 2;
+  float out[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int dim = dim0 + i;
+    if (dim >= g.R) {
+      out[i] = v[i];
+      continue;
+    }
+    const bool lo = dim < half;
+    const int pdim = lo ? dim + half : dim - half;
+    float xp = row[cc - dim0 + pdim];
+    if (g.bias) xp += Elem<T>::to_f(((const T*)g.bias)[n - dim0 + pdim]);
+    const float* cs = g.rope + (int64_t(pos) * half + (lo ? dim : dim - half)) * 2;
+    out[i] = lo ? v[i] * cs[0] - xp * cs[1] : v[i] * cs[0] + xp * cs[1];
+  }
+#pragma unroll
+  for (int i = 0; i < 8; ++i) v[i] = out[i];
+}
+
+// stage: fp32 tile [BM][BN + 4] in LDS; tile origin (m0, tn). Each thread
+// handles 8 consecutive columns of a row at a time. EPI is an EpiKind.
+template <typename T, int BM, int BN, int NT, int EPI>
 __device__ void gemm_epilogue(const GemmArgs& g, const float* stage, int m0, int tn) {
   constexpr int LD = BN + 4;
-  if (g.epi == EPI_SWIGLU) {
+  if constexpr (EPI == EPI_SWIGLU) {
+    // tile columns [0, BN/2) are gate units, [BN/2, BN) the matching up units
     constexpr int H = BN / 2;
     for (int e = threadIdx.x; e < BM * (H / 8); e += NT) {
       const int rr = e / (H / 8), cc = (e % (H / 8)) * 8;
@@ -51,10 +79,7 @@ __device__ void gemm_epilogue(const GemmArgs& g, const float* stage, int m0, int
       if (m >= g.M) continue;
       float y[8];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        float gate = stage[rr * LD + cc + i], up = stage[rr * LD + H + cc + i];
-        y[i] = silu(gate) * up;
-      }
+      for (int i = 0; i < 8; ++i) y[i] = silu(stage[rr * LD + cc + i]) * stage[rr * LD + H + cc + i];
       store8((T*)g.out + int64_t(m) * g.ldo + tn * H + cc, y);
     }
     return;
@@ -75,77 +100,45 @@ __device__ void gemm_epilogue(const GemmArgs& g, const float* stage, int m0, int
 #pragma unroll
       for (int i = 0; i < 8; ++i) v[i] += bv[i];
     }
-    switch (g.epi) {
-      case EPI_QKV_ROPE: {
-        const int hd = g.hd, qcols = g.Hq * hd, kcols = g.Hkv * hd;
-        T* dst;
-        bool rot;
-        if (n < qcols) {
-          dst = (T*)g.q + ((int64_t(b) * g.Hq + n / hd) * g.kk + j) * hd + (n % hd);
-          rot = true;
-        } else if (n < qcols + kcols) {
-          const int c = n - qcols;
-          dst = (T*)g.k + ((int64_t(b) * g.Hkv + c / hd) * g.kk + j) * hd + (c % hd);
-          rot = true;
-        } else {
-          const int c = n - qcols - kcols;
-          dst = (T*)g.v + ((int64_t(b) * g.Hkv + c / hd) * g.kk + j) * hd + (c % hd);
-          rot = false;
-        }
-        const int dim0 = n % hd, half = g.R / 2;
-        if (rot && dim0 < g.R) {
-          float out[8];
-#pragma unroll
-          for (int i = 0; i < 8; ++i) {
-            const int dim = dim0 + i;
-            if (dim >= g.R) {
-              out[i] = v[i];
-              continue;
-            }
-            const bool lo = dim < half;
-            const int pdim = lo ? dim + half : dim - half;
-            float xp = stage[rr * LD + cc - dim0 + pdim];
-            if (g.bias) xp += Elem<T>::to_f(((const T*)g.bias)[n - dim0 + pdim]);
-            const float* cs = g.rope + (int64_t(pos) * half + (lo ? dim : dim - half)) * 2;
-            out[i] = lo ? v[i] * cs[0] - xp * cs[1] : v[i] * cs[0] + xp * cs[1];
-          }
-          store8(dst, out);
-        } else {
-          store8(dst, v);
-        }
-        break;
+    if constexpr (EPI == EPI_QKV_ROPE) {
+      // columns: Q heads, then K heads, then V heads; written head-major [B, H, kk, hd]
+      const int hd = g.hd, qcols = g.Hq * hd, kcols = g.Hkv * hd;
+      const int dim0 = n % hd;
+      T* dst;
+      if (n < qcols) {
+        dst = (T*)g.q + ((int64_t(b) * g.Hq + n / hd) * g.kk + j) * hd + dim0;
+        if (dim0 < g.R) rope_chunk<T>(g, stage + rr * LD, cc, n, dim0, pos, v);
+      } else if (n < qcols + kcols) {
+        dst = (T*)g.k + ((int64_t(b) * g.Hkv + (n - qcols) / hd) * g.kk + j) * hd + dim0;
+        if (dim0 < g.R) rope_chunk<T>(g, stage + rr * LD, cc, n, dim0, pos, v);
+      } else {
+        dst = (T*)g.v + ((int64_t(b) * g.Hkv + (n - qcols - kcols) / hd) * g.kk + j) * hd + dim0;
       }
-      case EPI_BIAS_GELU: {
+      store8(dst, v);
+    } else if constexpr (EPI == EPI_BIAS_GELU) {
 #pragma unroll
-        for (int i = 0; i < 8; ++i) v[i] = gelu_erf(v[i]);
-        store8((T*)g.out + int64_t(m) * g.ldo + n, v);
-        break;
+      for (int i = 0; i < 8; ++i) v[i] = gelu_erf(v[i]);
+      store8((T*)g.out + int64_t(m) * g.ldo + n, v);
+    } else if constexpr (EPI == EPI_RESID_STORE) {
+      float xr[8];
+      load8((const T*)g.x + (int64_t(b) * g.T + pos) * g.N + n, xr);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] += xr[i];
+      store8((T*)g.out + int64_t(m) * g.ldo + n, v);
+    } else {  // EPI_RESID_SCATTER
+      if (g.bias2) {
+        float bv[8];
+        load8((const T*)g.bias2 + n, bv);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[i] += bv[i];
       }
-      case EPI_RESID_STORE: {
-        float xr[8];
-        load8((const T*)g.x + (int64_t(b) * g.T + pos) * g.N + n, xr);
+      T* dst = (T*)g.x + (int64_t(b) * g.T + pos) * g.N + n;
+      float xr[8];
+      if (g.res) load8((const T*)g.res + int64_t(m) * g.N + n, xr);
+      else load8(dst, xr);
 #pragma unroll
-        for (int i = 0; i < 8; ++i) v[i] += xr[i];
-        store8((T*)g.out + int64_t(m) * g.ldo + n, v);
-        break;
-      }
-      case EPI_RESID_SCATTER: {
-        if (g.bias2) {
-          float bv[8];
-          load8((const T*)g.bias2 + n, bv);
-#pragma unroll
-          for (int i = 0; i < 8; ++i) v[i] += bv[i];
-        }
-        T* dst = (T*)g.x + (int64_t(b) * g.T + pos) * g.N + n;
-        float xr[8];
-        if (g.res) load8((const T*)g.res + int64_t(m) * g.N + n, xr);
-        else load8(dst, xr);
-#pragma unroll
-        for (int i = 0; i < 8; ++i) v[i] += xr[i];
-        store8(dst, v);
-        break;
-      }
-      default: break;
+      for (int i = 0; i < 8; ++i) v[i] += xr[i];
+      store8(dst, v);
     }
   }
 }
@@ -161,8 +154,9 @@ constexpr int kStageBytes = kBM * kStageLD * 4;             // fp32 epilogue til
 constexpr int kSmemBytes = kTileBytes > kStageBytes ? kTileBytes : kStageBytes;
 
 // Row of the B operand (weight matrix) that tile row r of column tile tn reads.
+template <int EPI>
 __device__ __forceinline__ int b_row(const GemmArgs& g, int tn, int r) {
-  if (g.epi == EPI_SWIGLU) {
+  if constexpr (EPI == EPI_SWIGLU) {
     constexpr int H = kBN / 2;
     return r < H ? tn * H + r : g.f + tn * H + (r - H);
   }
@@ -170,6 +164,7 @@ __device__ __forceinline__ int b_row(const GemmArgs& g, int tn, int r) {
   return n < g.N ? n : g.N - 1;
 }
 
+template <int EPI>
 __global__ __launch_bounds__(kThreads, 2) void gemm_bf16_kernel(GemmArgs g) {
   __shared__ __attribute__((aligned(16))) char smem[kSmemBytes];
   uint16_t* As = reinterpret_cast<uint16_t*>(smem);
@@ -193,7 +188,7 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_bf16_kernel(GemmArgs g) {
     if (m > g.M - 1) m = g.M - 1;
     arow[i] = (const uint16_t*)g.a + int64_t(m) * g.lda;
     arow2[i] = g.a2 ? (const uint16_t*)g.a2 + int64_t(m) * g.lda2 : nullptr;
-    const int n = b_row(g, tn, lrow + 32 * i);
+    const int n = b_row<EPI>(g, tn, lrow + 32 * i);
     brow[i] = (const uint16_t*)g.b + int64_t(n) * g.ldb;
     brow2[i] = g.b2 ? (const uint16_t*)g.b2 + int64_t(n) * g.ldb2 : nullptr;
   }
@@ -268,13 +263,14 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_bf16_kernel(GemmArgs g) {
       for (int e = 0; e < 4; ++e)
         stage[(wm * kWM + 16 * i + 4 * grp + e) * kStageLD + wn * kWN + 16 * j + r16] = acc[i][j][e];
   __syncthreads();
-  gemm_epilogue<uint16_t, kBM, kBN, kThreads>(g, stage, m0, tn);
+  gemm_epilogue<uint16_t, kBM, kBN, kThreads, EPI>(g, stage, m0, tn);
 }
 
 // ------------------------------------------------------------ fp32 GEMM
 
 constexpr int kFBM = 32, kFBN = 128, kFBK = 32;
 
+template <int EPI>
 __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g) {
   __shared__ float As[kFBK][kFBM + 4];
   __shared__ float Bs[kFBK][kFBN + 4];
@@ -303,7 +299,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g) {
       const int e = tid + 256 * t;
       const int row = e / 8, c4 = (e % 8) * 4;
       int n;
-      if (g.epi == EPI_SWIGLU) n = row < kFBN / 2 ? tn * (kFBN / 2) + row : g.f + tn * (kFBN / 2) + row - kFBN / 2;
+      if constexpr (EPI == EPI_SWIGLU) n = row < kFBN / 2 ? tn * (kFBN / 2) + row : g.f + tn * (kFBN / 2) + row - kFBN / 2;
       else n = min(tn * kFBN + row, g.N - 1);
       float v[4] = {0.f, 0.f, 0.f, 0.f};
       if (k0 + c4 < g.K) {
@@ -335,19 +331,31 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) stage[(tr * 4 + i) * (kFBN + 4) + tc * 4 + j] = acc[i][j];
   __syncthreads();
-  gemm_epilogue<float, kFBM, kFBN, 256>(g, stage, m0, tn);
+  gemm_epilogue<float, kFBM, kFBN, 256, EPI>(g, stage, m0, tn);
+}
+
+template <int EPI>
+static void launch_gemm_t(const GemmArgs& g, hipStream_t s) {
+  if (g.dtype == DSF_BF16) {
+    const int ntn = EPI == EPI_SWIGLU ? g.f / (kBN / 2) : (g.N + kBN - 1) / kBN;
+    dim3 grid(ntn, (g.M + kBM - 1) / kBM);
+    gemm_bf16_kernel<EPI><<<grid, kThreads, 0, s>>>(g);
+  } else {
+    const int ntn = EPI == EPI_SWIGLU ? g.f / (kFBN / 2) : (g.N + kFBN - 1) / kFBN;
+    dim3 grid(ntn, (g.M + kFBM - 1) / kFBM);
+    gemm_f32_kernel<EPI><<<grid, 256, 0, s>>>(g);
+  }
 }
 
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t s) {
   if (g.M == 0 || g.N == 0) return hipSuccess;
-  if (g.dtype == DSF_BF16) {
-    const int ntn = g.epi == EPI_SWIGLU ? g.f / (kBN / 2) : (g.N + kBN - 1) / kBN;
-    dim3 grid(ntn, (g.M + kBM - 1) / kBM);
-    gemm_bf16_kernel<<<grid, kThreads, 0, s>>>(g);
-  } else {
-    const int ntn = g.epi == EPI_SWIGLU ? g.f / (kFBN / 2) : (g.N + kFBN - 1) / kFBN;
-    dim3 grid(ntn, (g.M + kFBM - 1) / kFBM);
-    gemm_f32_kernel<<<grid, 256, 0, s>>>(g);
+  switch (g.epi) {
+    case EPI_QKV_ROPE: launch_gemm_t<EPI_QKV_ROPE>(g, s); break;
+    case EPI_BIAS_GELU: launch_gemm_t<EPI_BIAS_GELU>(g, s); break;
+    case EPI_SWIGLU: launch_gemm_t<EPI_SWIGLU>(g, s); break;
+    case EPI_RESID_STORE: launch_gemm_t<EPI_RESID_STORE>(g, s); break;
+    case EPI_RESID_SCATTER: launch_gemm_t<EPI_RESID_SCATTER>(g, s); break;
+    default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
