@@ -266,6 +266,142 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_bf16_kernel(GemmArgs g) {
   gemm_epilogue<uint16_t, kBM, kBN, kThreads, EPI>(g, stage, m0, tn);
 }
 
+// ------------------------------------------- bf16 MFMA GEMM, LDS-DMA ring
+
+// Tiles arrive in LDS straight from global memory (global_load_lds_dwordx4:
+// each lane moves 16 bytes, a wavefront fills 1 KiB = 8 tile rows of 64 bf16
+// at a wave-uniform LDS address). The lane picks WHICH global chunk it loads,
+// so the LDS copy comes out XOR-swizzled without passing through registers.
+// NS stages form a ring: while tile kt is multiplied, tiles kt+1 .. kt+NS-1
+// are in flight, which covers HBM/MALL latency with compute. Requires
+// K % 64 == 0 and K1 % 64 == 0.
+template <int BM, int BN, int WM, int WN, int NS>
+struct DmaCfg {
+  static constexpr int kWaves = (BM / WM) * (BN / WN);
+  static constexpr int kThreads = kWaves * 64;
+  static constexpr int kStage = (BM + BN) * kBK * 2;                 // bytes per stage
+  static constexpr int kLoadsA = BM / 8 / kWaves;                    // 1 KiB loads per wave per tile
+  static constexpr int kLoadsB = BN / 8 / kWaves;
+  static constexpr int kLoads = kLoadsA + kLoadsB;
+  static constexpr int kStageLD = BN + 4;
+  static constexpr int kSmem = NS * kStage > BM * kStageLD * 4 ? NS * kStage : BM * kStageLD * 4;
+  static_assert(BM % (8 * kWaves) == 0 && BN % (8 * kWaves) == 0, "tile rows must split evenly over waves");
+  static_assert((NS - 2) * kLoads < 64, "vmcnt range");
+};
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  // the memory clobber orders the compiler's LDS reads after the DMA has landed
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// 16 bytes per lane from global memory into LDS at lds + 16 * lane (lds is
+// wave-uniform). Kept out of lambdas: the builtin exists only for the device.
+__device__ __forceinline__ void dma16(const void* gptr, char* lds) {
+  __builtin_amdgcn_global_load_lds(gptr, (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
+}
+
+template <int EPI, int BM, int BN, int WM, int WN, int NS>
+__global__ __launch_bounds__((DmaCfg<BM, BN, WM, WN, NS>::kThreads)) void gemm_bf16_dma_kernel(GemmArgs g) {
+  using C = DmaCfg<BM, BN, WM, WN, NS>;
+  constexpr int MI = WM / 16, NI = WN / 16;
+  __shared__ __attribute__((aligned(1024))) char smem[C::kSmem];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / (BN / WN), wn = wave % (BN / WN);
+  const int r16 = lane & 15, grp = lane >> 4;
+  const int tn = blockIdx.x, tm = blockIdx.y;
+  const int m0 = tm * BM;
+
+  // DMA source pointers. Load i of this wave fills tile rows 8 (wave + kWaves i) .. +8;
+  // lane -> row + lane/8, physical chunk lane%8 holds logical chunk (lane%8) ^ (lane/8).
+  const int lr = lane >> 3, lc = (lane & 7) ^ (lane >> 3);
+  const uint16_t* pa[C::kLoadsA];
+  const uint16_t* pa2[C::kLoadsA];
+  const uint16_t* pb[C::kLoadsB];
+  const uint16_t* pb2[C::kLoadsB];
+#pragma unroll
+  for (int i = 0; i < C::kLoadsA; ++i) {
+    int m = m0 + 8 * (wave + C::kWaves * i) + lr;
+    if (m > g.M - 1) m = g.M - 1;
+    pa[i] = (const uint16_t*)g.a + int64_t(m) * g.lda + lc * 8;
+    pa2[i] = g.a2 ? (const uint16_t*)g.a2 + int64_t(m) * g.lda2 + lc * 8 : nullptr;
+  }
+#pragma unroll
+  for (int i = 0; i < C::kLoadsB; ++i) {
+    const int r = 8 * (wave + C::kWaves * i) + lr;
+    int n;
+    if constexpr (EPI == EPI_SWIGLU) n = r < BN / 2 ? tn * (BN / 2) + r : g.f + tn * (BN / 2) + (r - BN / 2);
+    else n = min(tn * BN + r, g.N - 1);
+    pb[i] = (const uint16_t*)g.b + int64_t(n) * g.ldb + lc * 8;
+    pb2[i] = g.b2 ? (const uint16_t*)g.b2 + int64_t(n) * g.ldb2 + lc * 8 : nullptr;
+  }
+  auto issue = [&](int kt) {
+    const int k0 = kt * kBK;
+    const bool second = k0 >= g.K1;
+    const int kc = second ? k0 - g.K1 : k0;
+    char* st = smem + (kt % NS) * C::kStage;
+#pragma unroll
+    for (int i = 0; i < C::kLoadsA; ++i)
+      dma16((second ? pa2[i] : pa[i]) + kc, st + 1024 * (wave + C::kWaves * i));
+#pragma unroll
+    for (int i = 0; i < C::kLoadsB; ++i)
+      dma16((second ? pb2[i] : pb[i]) + kc, st + BM * kBK * 2 + 1024 * (wave + C::kWaves * i));
+  };
+
+  f32x4 acc[MI][NI];
+#pragma unroll
+  for (int i = 0; i < MI; ++i)
+#pragma unroll
+    for (int j = 0; j < NI; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const int nk = g.K / kBK;
+#pragma unroll
+  for (int s = 0; s < NS - 1; ++s)
+    if (s < nk) issue(s);
+  for (int kt = 0; kt < nk; ++kt) {
+    // tile kt has landed once at most (tiles issued after it) * kLoads loads remain
+    if (kt + NS - 2 < nk) wait_vmcnt<(NS - 2) * C::kLoads>();
+    else wait_vmcnt<0>();
+    __syncthreads();  // every wave's part of tile kt is visible; tile kt-1's buffer is free
+    if (kt + NS - 1 < nk) issue(kt + NS - 1);
+    const uint16_t* At = reinterpret_cast<const uint16_t*>(smem + (kt % NS) * C::kStage);
+    const uint16_t* Bt = At + BM * kBK;
+#pragma unroll
+    for (int ks = 0; ks < kBK / 32; ++ks) {
+      const int ch = ks * 4 + grp;
+      bf16x8 af[MI], bfr[NI];
+#pragma unroll
+      for (int i = 0; i < MI; ++i) {
+        const int ar = wm * WM + i * 16 + r16;
+        af[i] = *reinterpret_cast<const bf16x8*>(At + ar * kBK + ((ch ^ (ar & 7)) << 3));
+      }
+#pragma unroll
+      for (int j = 0; j < NI; ++j) {
+        const int br = wn * WN + j * 16 + r16;
+        bfr[j] = *reinterpret_cast<const bf16x8*>(Bt + br * kBK + ((ch ^ (br & 7)) << 3));
+      }
+#pragma unroll
+      for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int j = 0; j < NI; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+    }
+  }
+  __syncthreads();  // all waves are done reading the ring before it becomes the epilogue tile
+  float* stage = reinterpret_cast<float*>(smem);
+#pragma unroll
+  for (int i = 0; i < MI; ++i)
+#pragma unroll
+    for (int j = 0; j < NI; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        stage[(wm * WM + 16 * i + 4 * grp + e) * C::kStageLD + wn * WN + 16 * j + r16] = acc[i][j][e];
+  __syncthreads();
+  gemm_epilogue<uint16_t, BM, BN, C::kThreads, EPI>(g, stage, m0, tn);
+}
+
 // ------------------------------------------------------------ fp32 GEMM
 
 constexpr int kFBM = 32, kFBN = 128, kFBK = 32;
@@ -334,9 +470,28 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g) {
   gemm_epilogue<float, kFBM, kFBN, 256, EPI>(g, stage, m0, tn);
 }
 
+// Build-time tile configuration of the LDS-DMA GEMM (DSF_GEMM_USE_DMA=0 keeps
+// every bf16 GEMM on the register-staged kernel).
+#ifndef DSF_GEMM_USE_DMA
+#define DSF_GEMM_USE_DMA 1
+#endif
+#ifndef DSF_GEMM_BM
+#define DSF_GEMM_BM 128
+#define DSF_GEMM_BN 128
+#define DSF_GEMM_WM 64
+#define DSF_GEMM_WN 64
+#define DSF_GEMM_NS 2
+#endif
+
 template <int EPI>
 static void launch_gemm_t(const GemmArgs& g, hipStream_t s) {
-  if (g.dtype == DSF_BF16) {
+  if (DSF_GEMM_USE_DMA && g.dtype == DSF_BF16 && g.K % kBK == 0 && g.K1 % kBK == 0) {
+    constexpr int BM = DSF_GEMM_BM, BN = DSF_GEMM_BN;
+    using Cfg = DmaCfg<BM, BN, DSF_GEMM_WM, DSF_GEMM_WN, DSF_GEMM_NS>;
+    const int ntn = EPI == EPI_SWIGLU ? g.f / (BN / 2) : (g.N + BN - 1) / BN;
+    dim3 grid(ntn, (g.M + BM - 1) / BM);
+    gemm_bf16_dma_kernel<EPI, BM, BN, DSF_GEMM_WM, DSF_GEMM_WN, DSF_GEMM_NS><<<grid, Cfg::kThreads, 0, s>>>(g);
+  } else if (g.dtype == DSF_BF16) {
     const int ntn = EPI == EPI_SWIGLU ? g.f / (kBN / 2) : (g.N + kBN - 1) / kBN;
     dim3 grid(ntn, (g.M + kBM - 1) / kBM);
     gemm_bf16_kernel<EPI><<<grid, kThreads, 0, s>>>(g);
