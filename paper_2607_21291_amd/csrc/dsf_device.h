@@ -79,6 +79,34 @@ __device__ __forceinline__ double wave_sum(double v) {
   return v;
 }
 
+// Reductions over the four 16-lane rows of a wavefront (lanes l, l^16, l^32,
+// l^48) with gfx950's row-swap permutes: VALU only, no LDS round trip. After
+// the 32-swap each lane holds its own value and that of lane l^32 (in either
+// order), after the 16-swap those of lane l^16; max and + are symmetric.
+__device__ __forceinline__ float rows4_max(float v) {
+  auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float rows4_sum(float v) {
+  auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
+// MI355X dispatches consecutive workgroup ids round-robin over its 8 XCDs,
+// each with its own L2. xcd_remap turns launch index L (of W) into a work
+// index so that every XCD receives one contiguous range of work items (a
+// bijection on [0, W)): neighbouring items, which share operands, then share
+// an L2.
+constexpr int kXcds = 8;
+__device__ __forceinline__ int xcd_remap(int L, int W) {
+  const int q = W / kXcds, r = W % kXcds, x = L % kXcds;
+  return x * q + (x < r ? x : r) + L / kXcds;
+}
+
 // Positions supplied by a caller are clamped into [0, T) so that a bad index
 // cannot address memory outside the hidden-state rows.
 __device__ __forceinline__ int clamp_pos(int p, int T) { return p < 0 ? 0 : (p >= T ? T - 1 : p); }

@@ -83,6 +83,8 @@ struct GemmArgs {
   void* x; const void* res;
   // EPI_SWIGLU: f (gate rows [0, f), up rows [f, 2f))
   int f;
+  // set by the launcher: number of M tiles of the grid
+  int ntm;
 };
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t s);
 

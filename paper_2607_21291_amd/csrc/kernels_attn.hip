@@ -23,24 +23,94 @@ namespace dsf {
 constexpr int kKV = 64;             // keys per tile
 constexpr int kVtLD = kKV + 4;      // padded row of the transposed V tile (bf16 elements)
 
+template <int HD>
+struct AttnTile {
+  static constexpr int kNch = HD / 8;                              // 16-byte chunks per row
+  static constexpr int kSwz = (kNch < 8 ? kNch : 8) - 1;
+  static constexpr int kKChunks = kKV * kNch;                      // K tile chunks
+  static constexpr int kVPairs = (kKV / 2) * kNch;                 // V tile: two keys per item
+  static constexpr int kKIter = (kKChunks + 255) / 256;
+  static constexpr int kVIter = (kVPairs + 255) / 256;
+  static constexpr int kKBytes = kKV * HD * 2;
+  static constexpr int kVBytes = HD * kVtLD * 2;
+  static constexpr int kStage = kKBytes + kVBytes;
+};
+
+// The next K/V tile is held in registers while the current one is multiplied
+// (loads in flight during compute), then written to the other LDS buffer:
+// one barrier per tile.
+template <int HD>
+struct AttnPrefetch {
+  using A = AttnTile<HD>;
+  u32x4 k[A::kKIter];
+  u32x4 v0[A::kVIter], v1[A::kVIter];
+
+  __device__ __forceinline__ void load(const uint16_t* Kh, const uint16_t* Vh, int kb0, int n, int tid) {
+#pragma unroll
+    for (int i = 0; i < A::kKIter; ++i) {
+      const int c = tid + 256 * i;
+      const int key = kb0 + c / A::kNch;
+      k[i] = (c < A::kKChunks && key < n) ? *reinterpret_cast<const u32x4*>(Kh + int64_t(key) * HD + (c % A::kNch) * 8)
+                                          : u32x4{0, 0, 0, 0};
+    }
+#pragma unroll
+    for (int i = 0; i < A::kVIter; ++i) {
+      const int c = tid + 256 * i;
+      const int kp = c % (kKV / 2), ch = c / (kKV / 2);
+      const int key0 = kb0 + 2 * kp;
+      const bool ok = c < A::kVPairs;
+      v0[i] = (ok && key0 < n) ? *reinterpret_cast<const u32x4*>(Vh + int64_t(key0) * HD + ch * 8) : u32x4{0, 0, 0, 0};
+      v1[i] = (ok && key0 + 1 < n) ? *reinterpret_cast<const u32x4*>(Vh + int64_t(key0 + 1) * HD + ch * 8)
+                                   : u32x4{0, 0, 0, 0};
+    }
+  }
+  // K row-major with swizzled chunks; V transposed, Vt[dim][key], two keys per 32-bit store
+  __device__ __forceinline__ void store(uint16_t* Ks, uint16_t* Vt, int tid) const {
+#pragma unroll
+    for (int i = 0; i < A::kKIter; ++i) {
+      const int c = tid + 256 * i;
+      if (c < A::kKChunks) {
+        const int row = c / A::kNch, ch = c % A::kNch;
+        *reinterpret_cast<u32x4*>(Ks + row * HD + ((ch ^ (row & A::kSwz)) << 3)) = k[i];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < A::kVIter; ++i) {
+      const int c = tid + 256 * i;
+      if (c < A::kVPairs) {
+        const int kp = c % (kKV / 2), ch = c / (kKV / 2);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const uint32_t lo = (v0[i][e] & 0xffffu) | (v1[i][e] << 16);
+          const uint32_t hi = (v0[i][e] >> 16) | (v1[i][e] & 0xffff0000u);
+          *reinterpret_cast<uint32_t*>(Vt + (ch * 8 + 2 * e) * kVtLD + 2 * kp) = lo;
+          *reinterpret_cast<uint32_t*>(Vt + (ch * 8 + 2 * e + 1) * kVtLD + 2 * kp) = hi;
+        }
+      }
+    }
+  }
+};
+
 template <int HD, int NQ>
 __global__ __launch_bounds__(256) void attn_bf16_kernel(const uint16_t* __restrict__ Q,
                                                         const uint16_t* __restrict__ K,
                                                         const uint16_t* __restrict__ V, int Hq, int Hkv,
                                                         int n, uint16_t* __restrict__ out) {
+  using A = AttnTile<HD>;
   constexpr int QB = 64 * NQ;          // queries per workgroup
-  constexpr int NCH = HD / 8;          // 16-byte chunks per row
-  constexpr int SWZ = (NCH < 8 ? NCH : 8) - 1;
   constexpr int NS = HD / 32;          // MFMA k steps over the head dim
   constexpr int ND = HD / 16;          // 16-row blocks of the head dim
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[kKV * HD];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[HD * kVtLD];
+  __shared__ __attribute__((aligned(16))) char smem[2 * A::kStage];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r16 = lane & 15, grp = lane >> 4;
+  // one work item per (sequence, head, query block); the query blocks of one
+  // (sequence, head) share K/V, so they are kept on one XCD (longest first)
   const int nqb = (n + QB - 1) / QB;
-  const int qblk = nqb - 1 - int(blockIdx.x);  // longest rows first
-  const int h = blockIdx.y, b = blockIdx.z;
+  const int item = xcd_remap(int(blockIdx.x), int(gridDim.x));
+  const int bh = item / nqb;
+  const int qblk = nqb - 1 - (item - bh * nqb);
+  const int h = bh % Hq, b = bh / Hq;
   const int kvh = h / (Hq / Hkv);
   const int q0 = qblk * QB;
   const int qw0 = q0 + wave * 16 * NQ;
@@ -48,6 +118,11 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const uint16_t* __restri
   const uint16_t* Qh = Q + (int64_t(b) * Hq + h) * n * HD;
   const uint16_t* Kh = K + (int64_t(b) * Hkv + kvh) * n * HD;
   const uint16_t* Vh = V + (int64_t(b) * Hkv + kvh) * n * HD;
+
+  const int kend = min(n, q0 + QB);
+  const int ntiles = (kend + kKV - 1) / kKV;
+  AttnPrefetch<HD> pf;
+  pf.load(Kh, Vh, 0, n, tid);
 
   // Q^T operand: lane (query r16, group grp) holds Q[query][32 s + 8 grp .. +8]
   bf16x8 qf[NQ][NS];
@@ -70,119 +145,97 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const uint16_t* __restri
     for (int db = 0; db < ND; ++db) o[qi][db] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
   const float sc = 1.4426950408889634f / sqrtf(float(HD));  // log2(e) / sqrt(hd)
-
-  const int kend = min(n, q0 + QB);
-  const int ntiles = (kend + kKV - 1) / kKV;
   const int wave_qmax = qw0 + 16 * NQ - 1;
 
+  pf.store(reinterpret_cast<uint16_t*>(smem), reinterpret_cast<uint16_t*>(smem + A::kKBytes), tid);
+  __syncthreads();
   for (int t = 0; t < ntiles; ++t) {
     const int kb0 = t * kKV;
-    __syncthreads();
-    // K tile, row-major with swizzled chunks
-    for (int c = tid; c < kKV * NCH; c += 256) {
-      const int row = c / NCH, ch = c % NCH;
-      const int key = kb0 + row;
-      u32x4 val = key < n ? *reinterpret_cast<const u32x4*>(Kh + int64_t(key) * HD + ch * 8) : u32x4{0, 0, 0, 0};
-      *reinterpret_cast<u32x4*>(Ks + row * HD + ((ch ^ (row & SWZ)) << 3)) = val;
-    }
-    // V tile transposed: Vt[dim][key], two keys per 32-bit store
-    for (int c = tid; c < (kKV / 2) * NCH; c += 256) {
-      const int kp = c % (kKV / 2), ch = c / (kKV / 2);
-      const int key0 = kb0 + 2 * kp;
-      u32x4 v0 = key0 < n ? *reinterpret_cast<const u32x4*>(Vh + int64_t(key0) * HD + ch * 8) : u32x4{0, 0, 0, 0};
-      u32x4 v1 = key0 + 1 < n ? *reinterpret_cast<const u32x4*>(Vh + int64_t(key0 + 1) * HD + ch * 8)
-                              : u32x4{0, 0, 0, 0};
+    const uint16_t* Ks = reinterpret_cast<const uint16_t*>(smem + (t & 1) * A::kStage);
+    const uint16_t* Vt = reinterpret_cast<const uint16_t*>(smem + (t & 1) * A::kStage + A::kKBytes);
+    if (t + 1 < ntiles) pf.load(Kh, Vh, kb0 + kKV, n, tid);
+    if (kb0 <= wave_qmax) {  // otherwise every key of this tile is in this wave's future
+      // S^T blocks: lane holds S[query 16 qi + r16][key kb0 + 16 kb + 4 grp + i]
+      f32x4 s[NQ][4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        uint32_t lo = (v0[e] & 0xffffu) | (v1[e] << 16);
-        uint32_t hi = (v0[e] >> 16) | (v1[e] & 0xffff0000u);
-        *reinterpret_cast<uint32_t*>(Vt + (ch * 8 + 2 * e) * kVtLD + 2 * kp) = lo;
-        *reinterpret_cast<uint32_t*>(Vt + (ch * 8 + 2 * e + 1) * kVtLD + 2 * kp) = hi;
+      for (int qi = 0; qi < NQ; ++qi)
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) s[qi][kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) {
+        const int row = 16 * kb + r16;
+#pragma unroll
+        for (int st = 0; st < NS; ++st) {
+          const int ch = 4 * st + grp;
+          bf16x8 kf = *reinterpret_cast<const bf16x8*>(Ks + row * HD + ((ch ^ (row & A::kSwz)) << 3));
+#pragma unroll
+          for (int qi = 0; qi < NQ; ++qi)
+            s[qi][kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[qi][st], s[qi][kb], 0, 0, 0);
+        }
       }
-    }
-    __syncthreads();
-    if (kb0 > wave_qmax) continue;  // every key of this tile is in this wave's future
-
-    // S^T blocks: lane holds S[query 16 qi + r16][key kb0 + 16 kb + 4 grp + i]
-    f32x4 s[NQ][4];
+      const bool diag = kb0 + kKV - 1 > qw0 || kb0 + kKV > n;
+      bf16x8 pb[NQ][2];
 #pragma unroll
-    for (int qi = 0; qi < NQ; ++qi)
+      for (int qi = 0; qi < NQ; ++qi) {
+        const int qg = qw0 + 16 * qi + r16;
+        float mx = -INFINITY;
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb) s[qi][kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
-      const int row = 16 * kb + r16;
-#pragma unroll
-      for (int st = 0; st < NS; ++st) {
-        const int ch = 4 * st + grp;
-        bf16x8 kf = *reinterpret_cast<const bf16x8*>(Ks + row * HD + ((ch ^ (row & SWZ)) << 3));
-#pragma unroll
-        for (int qi = 0; qi < NQ; ++qi)
-          s[qi][kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[qi][st], s[qi][kb], 0, 0, 0);
-      }
-    }
-    const bool diag = kb0 + kKV - 1 > qw0 || kb0 + kKV > n;
-    bf16x8 pb[NQ][2];
-#pragma unroll
-    for (int qi = 0; qi < NQ; ++qi) {
-      const int qg = qw0 + 16 * qi + r16;
-      float mx = -INFINITY;
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          float v = s[qi][kb][i] * sc;
-          if (diag) {
-            const int key = kb0 + 16 * kb + 4 * grp + i;
-            if (key > qg || key >= n) v = -INFINITY;
+          for (int i = 0; i < 4; ++i) {
+            if (diag) {
+              const int key = kb0 + 16 * kb + 4 * grp + i;
+              if (key > qg || key >= n) s[qi][kb][i] = -INFINITY;
+            }
+            mx = fmaxf(mx, s[qi][kb][i]);
           }
-          s[qi][kb][i] = v;
-          mx = fmaxf(mx, v);
+        // running max in log2 units of the scaled scores (sc > 0 keeps the order)
+        const float m_new = fmaxf(m_run[qi], rows4_max(mx) * sc);
+        const float base = m_new == -INFINITY ? 0.f : m_new;
+        const float alpha = __builtin_amdgcn_exp2f(m_run[qi] - base);
+        float sum = 0.f;
+        float p[4][4];
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            p[kb][i] = __builtin_amdgcn_exp2f(fmaf(s[qi][kb][i], sc, -base));
+            sum += p[kb][i];
+          }
+        l_run[qi] = l_run[qi] * alpha + rows4_sum(sum);
+        m_run[qi] = m_new;
+#pragma unroll
+        for (int db = 0; db < ND; ++db) o[qi][db] *= alpha;
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            pb[qi][ks][i] = (__bf16)p[2 * ks][i];
+            pb[qi][ks][4 + i] = (__bf16)p[2 * ks + 1][i];
+          }
+      }
+      // O^T[dim 16 db + r16 .. ][query] += V^T P^T over this tile's 64 keys
+#pragma unroll
+      for (int db = 0; db < ND; ++db) {
+        const int dim = 16 * db + r16;
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+          const uint16_t* vrow = Vt + dim * kVtLD + 32 * ks + 4 * grp;
+          u32x2 lo = *reinterpret_cast<const u32x2*>(vrow);
+          u32x2 hi = *reinterpret_cast<const u32x2*>(vrow + 16);
+          u32x4 raw = {lo[0], lo[1], hi[0], hi[1]};
+          bf16x8 vf = __builtin_bit_cast(bf16x8, raw);
+#pragma unroll
+          for (int qi = 0; qi < NQ; ++qi)
+            o[qi][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pb[qi][ks], o[qi][db], 0, 0, 0);
         }
-      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      const float m_new = fmaxf(m_run[qi], mx);
-      const float base = m_new == -INFINITY ? 0.f : m_new;
-      const float alpha = exp2f(m_run[qi] - base);
-      float sum = 0.f;
-      float p[4][4];
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          p[kb][i] = exp2f(s[qi][kb][i] - base);
-          sum += p[kb][i];
-        }
-      sum += __shfl_xor(sum, 16, 64);
-      sum += __shfl_xor(sum, 32, 64);
-      l_run[qi] = l_run[qi] * alpha + sum;
-      m_run[qi] = m_new;
-#pragma unroll
-      for (int db = 0; db < ND; ++db) o[qi][db] *= alpha;
-#pragma unroll
-      for (int ks = 0; ks < 2; ++ks)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          pb[qi][ks][i] = (__bf16)p[2 * ks][i];
-          pb[qi][ks][4 + i] = (__bf16)p[2 * ks + 1][i];
-        }
-    }
-    // O^T[dim 16 db + r16 .. ][query] += V^T P^T over this tile's 64 keys
-#pragma unroll
-    for (int db = 0; db < ND; ++db) {
-      const int dim = 16 * db + r16;
-#pragma unroll
-      for (int ks = 0; ks < 2; ++ks) {
-        const uint16_t* vrow = Vt + dim * kVtLD + 32 * ks + 4 * grp;
-        u32x2 lo = *reinterpret_cast<const u32x2*>(vrow);
-        u32x2 hi = *reinterpret_cast<const u32x2*>(vrow + 16);
-        u32x4 raw = {lo[0], lo[1], hi[0], hi[1]};
-        bf16x8 vf = __builtin_bit_cast(bf16x8, raw);
-#pragma unroll
-        for (int qi = 0; qi < NQ; ++qi)
-          o[qi][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pb[qi][ks], o[qi][db], 0, 0, 0);
       }
     }
+    if (t + 1 < ntiles) {
+      pf.store(reinterpret_cast<uint16_t*>(smem + ((t + 1) & 1) * A::kStage),
+               reinterpret_cast<uint16_t*>(smem + ((t + 1) & 1) * A::kStage + A::kKBytes), tid);
+    }
+    __syncthreads();
   }
   // lane holds O^T[dim 16 db + 4 grp + i][query r16]
 #pragma unroll
@@ -250,8 +303,11 @@ hipError_t launch_attention(int dtype, const void* q, const void* k, const void*
     }
     return hipGetLastError();
   }
-  constexpr int NQ = 2;
-  dim3 grid((n + 64 * NQ - 1) / (64 * NQ), Hq, B);
+#ifndef DSF_ATTN_NQ
+#define DSF_ATTN_NQ 1
+#endif
+  constexpr int NQ = DSF_ATTN_NQ;
+  dim3 grid(((n + 64 * NQ - 1) / (64 * NQ)) * Hq * B);
   auto Qp = (const uint16_t*)q; auto Kp = (const uint16_t*)k; auto Vp = (const uint16_t*)v; auto O = (uint16_t*)out;
   switch (hd) {
     case 32: attn_bf16_kernel<32, NQ><<<grid, 256, 0, s>>>(Qp, Kp, Vp, Hq, Hkv, n, O); break;

@@ -311,7 +311,11 @@ __global__ __launch_bounds__((DmaCfg<BM, BN, WM, WN, NS>::kThreads)) void gemm_b
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / (BN / WN), wn = wave % (BN / WN);
   const int r16 = lane & 15, grp = lane >> 4;
-  const int tn = blockIdx.x, tm = blockIdx.y;
+  // tiles in row-major (M-tile, N-tile) order, one contiguous range per XCD:
+  // an XCD streams its own rows of A once and keeps them in its L2
+  const int ntn = int(gridDim.x) / g.ntm;
+  const int item = xcd_remap(int(blockIdx.x), int(gridDim.x));
+  const int tm = item / ntn, tn = item - tm * ntn;
   const int m0 = tm * BM;
 
   // DMA source pointers. Load i of this wave fills tile rows 8 (wave + kWaves i) .. +8;
@@ -489,8 +493,10 @@ static void launch_gemm_t(const GemmArgs& g, hipStream_t s) {
     constexpr int BM = DSF_GEMM_BM, BN = DSF_GEMM_BN;
     using Cfg = DmaCfg<BM, BN, DSF_GEMM_WM, DSF_GEMM_WN, DSF_GEMM_NS>;
     const int ntn = EPI == EPI_SWIGLU ? g.f / (BN / 2) : (g.N + BN - 1) / BN;
-    dim3 grid(ntn, (g.M + BM - 1) / BM);
-    gemm_bf16_dma_kernel<EPI, BM, BN, DSF_GEMM_WM, DSF_GEMM_WN, DSF_GEMM_NS><<<grid, Cfg::kThreads, 0, s>>>(g);
+    GemmArgs ga = g;
+    ga.ntm = (g.M + BM - 1) / BM;
+    dim3 grid(ntn * ga.ntm);
+    gemm_bf16_dma_kernel<EPI, BM, BN, DSF_GEMM_WM, DSF_GEMM_WN, DSF_GEMM_NS><<<grid, Cfg::kThreads, 0, s>>>(ga);
   } else if (g.dtype == DSF_BF16) {
     const int ntn = EPI == EPI_SWIGLU ? g.f / (kBN / 2) : (g.N + kBN - 1) / kBN;
     dim3 grid(ntn, (g.M + kBM - 1) / kBM);
