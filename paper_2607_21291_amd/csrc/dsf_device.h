@@ -111,7 +111,21 @@ __device__ __forceinline__ int xcd_remap(int L, int W) {
 // cannot address memory outside the hidden-state rows.
 __device__ __forceinline__ int clamp_pos(int p, int T) { return p < 0 ? 0 : (p >= T ? T - 1 : p); }
 
-__device__ __forceinline__ float gelu_erf(float x) { return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f)); }
+// erf by Abramowitz & Stegun, Handbook of Mathematical Functions, formula
+// 7.1.26: erf(z) = 1 - (a1 t + a2 t^2 + a3 t^3 + a4 t^4 + a5 t^5) exp(-z^2),
+// t = 1 / (1 + p z), for z >= 0 (odd extension below), |error| <= 1.5e-7.
+__device__ __forceinline__ float erf_as7126(float x) {
+  const float z = fabsf(x);
+  const float t = 1.0f / fmaf(0.3275911f, z, 1.0f);
+  float poly = fmaf(1.061405429f, t, -1.453152027f);
+  poly = fmaf(poly, t, 1.421413741f);
+  poly = fmaf(poly, t, -0.284496736f);
+  poly = fmaf(poly, t, 0.254829592f);
+  const float y = 1.0f - poly * t * __expf(-z * z);
+  return copysignf(y, x);
+}
+// GELU(x) = x Phi(x) = x (1 + erf(x / sqrt 2)) / 2
+__device__ __forceinline__ float gelu_erf(float x) { return 0.5f * x * (1.0f + erf_as7126(x * 0.70710678118654752f)); }
 __device__ __forceinline__ float silu(float x) { return x / (1.0f + expf(-x)); }
 
 }  // namespace dsf

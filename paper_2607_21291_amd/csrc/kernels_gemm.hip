@@ -39,44 +39,21 @@ __device__ __forceinline__ void store8(T* p, const float* v) {
   }
 }
 
-// RoPE (rotate-half) of the 8 values of one q/k chunk at columns dim0..dim0+7
-// of a head, at position pos. Partner dims (i, i + R/2) are read from the
-// staged row, so any R works. Dims >= R pass through.
-template <typename T>
-__device__ __forceinline__ void rope_chunk(const GemmArgs& g, const float* row, int cc, int n, int dim0, int pos,
-                                           float* v) {
-  const int half = g.R / 2;
-  float out[8];
-#pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int dim = dim0 + i;
-    if (dim >= g.R) {
-      out[i] = v[i];
-      continue;
-    }
-    const bool lo = dim < half;
-    const int pdim = lo ? dim + half : dim - half;
-    float xp = row[cc - dim0 + pdim];
-    if (g.bias) xp += Elem<T>::to_f(((const T*)g.bias)[n - dim0 + pdim]);
-    const float* cs = g.rope + (int64_t(pos) * half + (lo ? dim : dim - half)) * 2;
-    out[i] = lo ? v[i] * cs[0] - xp * cs[1] : v[i] * cs[0] + xp * cs[1];
-  }
-#pragma unroll
-  for (int i = 0; i < 8; ++i) v[i] = out[i];
-}
-
-// stage: fp32 tile [BM][BN + 4] in LDS; tile origin (m0, tn). Each thread
-// handles 8 consecutive columns of a row at a time. EPI is an EpiKind.
+// stage: fp32 tile [BM][BN + 4] in LDS; tile origin (m0, tn). Each thread owns
+// one 8-column chunk and walks the tile's rows, so everything that depends
+// only on the column (bias, head, RoPE partner) is computed once. EPI is an
+// EpiKind.
 template <typename T, int BM, int BN, int NT, int EPI>
 __device__ void gemm_epilogue(const GemmArgs& g, const float* stage, int m0, int tn) {
   constexpr int LD = BN + 4;
   if constexpr (EPI == EPI_SWIGLU) {
     // tile columns [0, BN/2) are gate units, [BN/2, BN) the matching up units
-    constexpr int H = BN / 2;
-    for (int e = threadIdx.x; e < BM * (H / 8); e += NT) {
-      const int rr = e / (H / 8), cc = (e % (H / 8)) * 8;
+    constexpr int H = BN / 2, CPR = H / 8, RSTEP = NT / CPR;
+    static_assert(NT % CPR == 0, "threads must tile the chunk columns");
+    const int cc = (threadIdx.x % CPR) * 8;
+    for (int rr = threadIdx.x / CPR; rr < BM; rr += RSTEP) {
       const int m = m0 + rr;
-      if (m >= g.M) continue;
+      if (m >= g.M) break;
       float y[8];
 #pragma unroll
       for (int i = 0; i < 8; ++i) y[i] = silu(stage[rr * LD + cc + i]) * stage[rr * LD + H + cc + i];
@@ -84,37 +61,84 @@ __device__ void gemm_epilogue(const GemmArgs& g, const float* stage, int m0, int
     }
     return;
   }
-  const int n0 = tn * BN;
-  for (int e = threadIdx.x; e < BM * (BN / 8); e += NT) {
-    const int rr = e / (BN / 8), cc = (e % (BN / 8)) * 8;
-    const int m = m0 + rr, n = n0 + cc;
-    if (m >= g.M || n >= g.N) continue;
+  constexpr int CPR = BN / 8, RSTEP = NT / CPR;
+  static_assert(NT % CPR == 0, "threads must tile the chunk columns");
+  const int cc = (threadIdx.x % CPR) * 8;
+  const int n = tn * BN + cc;
+  if (n >= g.N) return;
+  float bias[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) bias[i] = 0.f;
+  if (g.bias) load8((const T*)g.bias + n, bias);
+  if constexpr (EPI == EPI_RESID_SCATTER) {
+    if (g.bias2) {
+      float b2[8];
+      load8((const T*)g.bias2 + n, b2);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) bias[i] += b2[i];
+    }
+  }
+  // QKV: which section (q, k, v), head and dims this chunk holds; hd is a power of two
+  T* sec = nullptr;
+  int heads = 0, head = 0, dim0 = 0, hshift = 0;
+  bool rot = false;
+  float pbias[8];
+  if constexpr (EPI == EPI_QKV_ROPE) {
+    hshift = 31 - __clz(g.hd);
+    const int qcols = g.Hq << hshift, kcols = g.Hkv << hshift;
+    int c = n;
+    if (c < qcols) {
+      sec = (T*)g.q; heads = g.Hq; rot = true;
+    } else if (c < qcols + kcols) {
+      sec = (T*)g.k; heads = g.Hkv; c -= qcols; rot = true;
+    } else {
+      sec = (T*)g.v; heads = g.Hkv; c -= qcols + kcols;
+    }
+    head = c >> hshift;
+    dim0 = c & (g.hd - 1);
+    rot = rot && dim0 < g.R;
+    if (rot) {  // bias of each element's rotation partner (dims i and i + R/2)
+      const int half = g.R / 2;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int dim = dim0 + i;
+        const int pdim = dim < half ? dim + half : dim - half;
+        pbias[i] = (g.bias && dim < g.R) ? Elem<T>::to_f(((const T*)g.bias)[n - dim0 + pdim]) : 0.f;
+      }
+    }
+  }
+  for (int rr = threadIdx.x / CPR; rr < BM; rr += RSTEP) {
+    const int m = m0 + rr;
+    if (m >= g.M) break;
     const int b = m / g.kk, j = m - b * g.kk;
     const int pos = g.idx ? clamp_pos(g.idx[m], g.T) : j;
+    const float* row = stage + rr * LD;
     float v[8];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) v[i] = stage[rr * LD + cc + i];
-    if (g.bias) {
-      float bv[8];
-      load8((const T*)g.bias + n, bv);
-#pragma unroll
-      for (int i = 0; i < 8; ++i) v[i] += bv[i];
-    }
+    for (int i = 0; i < 8; ++i) v[i] = row[cc + i] + bias[i];
     if constexpr (EPI == EPI_QKV_ROPE) {
       // columns: Q heads, then K heads, then V heads; written head-major [B, H, kk, hd]
-      const int hd = g.hd, qcols = g.Hq * hd, kcols = g.Hkv * hd;
-      const int dim0 = n % hd;
-      T* dst;
-      if (n < qcols) {
-        dst = (T*)g.q + ((int64_t(b) * g.Hq + n / hd) * g.kk + j) * hd + dim0;
-        if (dim0 < g.R) rope_chunk<T>(g, stage + rr * LD, cc, n, dim0, pos, v);
-      } else if (n < qcols + kcols) {
-        dst = (T*)g.k + ((int64_t(b) * g.Hkv + (n - qcols) / hd) * g.kk + j) * hd + dim0;
-        if (dim0 < g.R) rope_chunk<T>(g, stage + rr * LD, cc, n, dim0, pos, v);
+      T* dst = sec + ((int64_t(b) * heads + head) * g.kk + j) * g.hd + dim0;
+      if (rot) {
+        const int half = g.R / 2;
+        float out[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const int dim = dim0 + i;
+          if (dim >= g.R) {
+            out[i] = v[i];
+            continue;
+          }
+          const bool lo = dim < half;
+          const int pdim = lo ? dim + half : dim - half;
+          const float xp = row[cc - dim0 + pdim] + pbias[i];
+          const float* cs = g.rope + (int64_t(pos) * half + (lo ? dim : dim - half)) * 2;
+          out[i] = lo ? v[i] * cs[0] - xp * cs[1] : v[i] * cs[0] + xp * cs[1];
+        }
+        store8(dst, out);
       } else {
-        dst = (T*)g.v + ((int64_t(b) * g.Hkv + (n - qcols - kcols) / hd) * g.kk + j) * hd + dim0;
+        store8(dst, v);
       }
-      store8(dst, v);
     } else if constexpr (EPI == EPI_BIAS_GELU) {
 #pragma unroll
       for (int i = 0; i < 8; ++i) v[i] = gelu_erf(v[i]);
@@ -126,12 +150,6 @@ __device__ void gemm_epilogue(const GemmArgs& g, const float* stage, int m0, int
       for (int i = 0; i < 8; ++i) v[i] += xr[i];
       store8((T*)g.out + int64_t(m) * g.ldo + n, v);
     } else {  // EPI_RESID_SCATTER
-      if (g.bias2) {
-        float bv[8];
-        load8((const T*)g.bias2 + n, bv);
-#pragma unroll
-        for (int i = 0; i < 8; ++i) v[i] += bv[i];
-      }
       T* dst = (T*)g.x + (int64_t(b) * g.T + pos) * g.N + n;
       float xr[8];
       if (g.res) load8((const T*)g.res + int64_t(m) * g.N + n, xr);
