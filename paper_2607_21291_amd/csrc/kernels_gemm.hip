@@ -44,14 +44,14 @@ __device__ __forceinline__ void store8(T* p, const float* v) {
 // only on the column (bias, head, RoPE partner) is computed once. EPI is an
 // EpiKind.
 template <typename T, int BM, int BN, int NT, int EPI>
-__device__ void gemm_epilogue(const GemmArgs& g, const float* stage, int m0, int tn) {
+__device__ void gemm_epilogue(const GemmArgs& g, const float* stage, int m0, int tn, int tid) {
   constexpr int LD = BN + 4;
   if constexpr (EPI == EPI_SWIGLU) {
     // tile columns [0, BN/2) are gate units, [BN/2, BN) the matching up units
     constexpr int H = BN / 2, CPR = H / 8, RSTEP = NT / CPR;
     static_assert(NT % CPR == 0, "threads must tile the chunk columns");
-    const int cc = (threadIdx.x % CPR) * 8;
-    for (int rr = threadIdx.x / CPR; rr < BM; rr += RSTEP) {
+    const int cc = (tid % CPR) * 8;
+    for (int rr = tid / CPR; rr < BM; rr += RSTEP) {
       const int m = m0 + rr;
       if (m >= g.M) break;
       float y[8];
@@ -63,7 +63,7 @@ __device__ void gemm_epilogue(const GemmArgs& g, const float* stage, int m0, int
   }
   constexpr int CPR = BN / 8, RSTEP = NT / CPR;
   static_assert(NT % CPR == 0, "threads must tile the chunk columns");
-  const int cc = (threadIdx.x % CPR) * 8;
+  const int cc = (tid % CPR) * 8;
   const int n = tn * BN + cc;
   if (n >= g.N) return;
   float bias[8];
@@ -107,7 +107,7 @@ __device__ void gemm_epilogue(const GemmArgs& g, const float* stage, int m0, int
       }
     }
   }
-  for (int rr = threadIdx.x / CPR; rr < BM; rr += RSTEP) {
+  for (int rr = tid / CPR; rr < BM; rr += RSTEP) {
     const int m = m0 + rr;
     if (m >= g.M) break;
     const int b = m / g.kk, j = m - b * g.kk;
@@ -281,31 +281,61 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_bf16_kernel(GemmArgs g) {
       for (int e = 0; e < 4; ++e)
         stage[(wm * kWM + 16 * i + 4 * grp + e) * kStageLD + wn * kWN + 16 * j + r16] = acc[i][j][e];
   __syncthreads();
-  gemm_epilogue<uint16_t, kBM, kBN, kThreads, EPI>(g, stage, m0, tn);
+  gemm_epilogue<uint16_t, kBM, kBN, kThreads, EPI>(g, stage, m0, tn, threadIdx.x);
 }
 
 // ------------------------------------------- bf16 MFMA GEMM, LDS-DMA ring
 
 // Tiles arrive in LDS straight from global memory (global_load_lds_dwordx4:
-// each lane moves 16 bytes, a wavefront fills 1 KiB = 8 tile rows of 64 bf16
+// each lane moves 16 bytes, a wavefront fills 1 KiB of consecutive tile rows
 // at a wave-uniform LDS address). The lane picks WHICH global chunk it loads,
 // so the LDS copy comes out XOR-swizzled without passing through registers.
-// NS stages form a ring: while tile kt is multiplied, tiles kt+1 .. kt+NS-1
-// are in flight, which covers HBM/MALL latency with compute. Requires
-// K % 64 == 0 and K1 % 64 == 0.
-template <int BM, int BN, int WM, int WN, int NS>
+// NS stages of BK columns form a ring: while tile kt is multiplied, tiles
+// kt+1 .. kt+NS-1 are in flight. Requires K % BK == 0 and K1 % BK == 0.
+//
+// Swizzle: a tile row is BK/8 chunks of 16 bytes. With BK = 64 (128-byte rows)
+// chunk c of row r sits at c ^ (r & 7); with BK = 32 (64-byte rows, two rows
+// per 128-byte bank line) at c ^ ((r >> 1) & 3). Either way the 8 lanes that
+// one 128-byte LDS cycle serves (8 consecutive rows, one logical chunk) hit 8
+// distinct bank groups.
+template <int BK>
+__device__ __forceinline__ int swz(int row, int ch) {
+  if constexpr (BK == 64) return ch ^ (row & 7);
+  else return ch ^ ((row >> 1) & 3);
+}
+
+template <int BM, int BN, int WM, int WN, int NS, int BK>
 struct DmaCfg {
   static constexpr int kWaves = (BM / WM) * (BN / WN);
   static constexpr int kThreads = kWaves * 64;
-  static constexpr int kStage = (BM + BN) * kBK * 2;                 // bytes per stage
-  static constexpr int kLoadsA = BM / 8 / kWaves;                    // 1 KiB loads per wave per tile
-  static constexpr int kLoadsB = BN / 8 / kWaves;
+  static constexpr int kRowBytes = BK * 2;
+  static constexpr int kRowsPerLoad = 1024 / kRowBytes;             // tile rows one wavefront load fills
+  static constexpr int kStage = (BM + BN) * kRowBytes;              // bytes per stage
+  static constexpr int kLoadsA = BM / kRowsPerLoad / kWaves;        // loads per wave per tile
+  static constexpr int kLoadsB = BN / kRowsPerLoad / kWaves;
   static constexpr int kLoads = kLoadsA + kLoadsB;
-  static constexpr int kStageLD = BN + 4;
-  static constexpr int kSmem = NS * kStage > BM * kStageLD * 4 ? NS * kStage : BM * kStageLD * 4;
-  static_assert(BM % (8 * kWaves) == 0 && BN % (8 * kWaves) == 0, "tile rows must split evenly over waves");
+  // Epilogue staging: the whole fp32 tile, or (wave tiles 128 wide) each wave
+  // stages 32 rows x WN of its own tile at a time.
+  static constexpr bool kWaveEpi = WN == 128;
+  static constexpr int kStageLD = (kWaveEpi ? WN : BN) + 4;
+  static constexpr int kStageBytes = kWaveEpi ? kWaves * 32 * kStageLD * 4 : BM * kStageLD * 4;
+  static constexpr int kSmem = NS * kStage > kStageBytes ? NS * kStage : kStageBytes;
+  static_assert(BK == 32 || BK == 64, "BK");
+  static_assert(BM % (kRowsPerLoad * kWaves) == 0 && BN % (kRowsPerLoad * kWaves) == 0,
+                "tile rows must split evenly over waves");
   static_assert((NS - 2) * kLoads < 64, "vmcnt range");
 };
+
+// Scheduling fence (no instruction moves across it), used to keep the next
+// substep's LDS reads ahead of the current substep's MFMAs.
+#ifndef DSF_SCHED_FENCES
+#define DSF_SCHED_FENCES 1
+#endif
+#if DSF_SCHED_FENCES
+#define DSF_SCHED_FENCE() __builtin_amdgcn_sched_barrier(0)
+#else
+#define DSF_SCHED_FENCE() ((void)0)
+#endif
 
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
@@ -320,10 +350,12 @@ __device__ __forceinline__ void dma16(const void* gptr, char* lds) {
   __builtin_amdgcn_global_load_lds(gptr, (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
 }
 
-template <int EPI, int BM, int BN, int WM, int WN, int NS>
-__global__ __launch_bounds__((DmaCfg<BM, BN, WM, WN, NS>::kThreads)) void gemm_bf16_dma_kernel(GemmArgs g) {
-  using C = DmaCfg<BM, BN, WM, WN, NS>;
+template <int EPI, int BM, int BN, int WM, int WN, int NS, int BK>
+__global__ __launch_bounds__((DmaCfg<BM, BN, WM, WN, NS, BK>::kThreads)) void gemm_bf16_dma_kernel(GemmArgs g) {
+  using C = DmaCfg<BM, BN, WM, WN, NS, BK>;
   constexpr int MI = WM / 16, NI = WN / 16;
+  constexpr int CPR = BK / 8;                 // chunks per tile row
+  constexpr int RPL = C::kRowsPerLoad;
   __shared__ __attribute__((aligned(1024))) char smem[C::kSmem];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -336,40 +368,45 @@ __global__ __launch_bounds__((DmaCfg<BM, BN, WM, WN, NS>::kThreads)) void gemm_b
   const int tm = item / ntn, tn = item - tm * ntn;
   const int m0 = tm * BM;
 
-  // DMA source pointers. Load i of this wave fills tile rows 8 (wave + kWaves i) .. +8;
-  // lane -> row + lane/8, physical chunk lane%8 holds logical chunk (lane%8) ^ (lane/8).
-  const int lr = lane >> 3, lc = (lane & 7) ^ (lane >> 3);
+  // DMA source pointers. Load i of this wave fills tile rows RPL (wave + kWaves i) .. +RPL;
+  // lane -> row lane / CPR, physical chunk lane % CPR holding logical chunk swz^-1.
+  const int lr = lane / CPR;
+  const int lc = swz<BK>(lr, lane % CPR);     // swz is an involution for a fixed row
   const uint16_t* pa[C::kLoadsA];
   const uint16_t* pa2[C::kLoadsA];
   const uint16_t* pb[C::kLoadsB];
   const uint16_t* pb2[C::kLoadsB];
 #pragma unroll
   for (int i = 0; i < C::kLoadsA; ++i) {
-    int m = m0 + 8 * (wave + C::kWaves * i) + lr;
+    int m = m0 + RPL * (wave + C::kWaves * i) + lr;
     if (m > g.M - 1) m = g.M - 1;
     pa[i] = (const uint16_t*)g.a + int64_t(m) * g.lda + lc * 8;
     pa2[i] = g.a2 ? (const uint16_t*)g.a2 + int64_t(m) * g.lda2 + lc * 8 : nullptr;
   }
 #pragma unroll
   for (int i = 0; i < C::kLoadsB; ++i) {
-    const int r = 8 * (wave + C::kWaves * i) + lr;
+    const int r = RPL * (wave + C::kWaves * i) + lr;
     int n;
-    if constexpr (EPI == EPI_SWIGLU) n = r < BN / 2 ? tn * (BN / 2) + r : g.f + tn * (BN / 2) + (r - BN / 2);
-    else n = min(tn * BN + r, g.N - 1);
+    if constexpr (EPI == EPI_SWIGLU) {
+      // each 128-row block of the B tile holds 64 gate units then the same 64 up units
+      const int blk = r / 128, rr = r % 128, u0 = (tn * (BN / 128) + blk) * 64;
+      n = rr < 64 ? u0 + rr : g.f + u0 + (rr - 64);
+    } else {
+      n = min(tn * BN + r, g.N - 1);
+    }
     pb[i] = (const uint16_t*)g.b + int64_t(n) * g.ldb + lc * 8;
     pb2[i] = g.b2 ? (const uint16_t*)g.b2 + int64_t(n) * g.ldb2 + lc * 8 : nullptr;
   }
   auto issue = [&](int kt) {
-    const int k0 = kt * kBK;
+    const int k0 = kt * BK;
     const bool second = k0 >= g.K1;
     const int kc = second ? k0 - g.K1 : k0;
     char* st = smem + (kt % NS) * C::kStage;
 #pragma unroll
-    for (int i = 0; i < C::kLoadsA; ++i)
-      dma16((second ? pa2[i] : pa[i]) + kc, st + 1024 * (wave + C::kWaves * i));
+    for (int i = 0; i < C::kLoadsA; ++i) dma16((second ? pa2[i] : pa[i]) + kc, st + 1024 * (wave + C::kWaves * i));
 #pragma unroll
     for (int i = 0; i < C::kLoadsB; ++i)
-      dma16((second ? pb2[i] : pb[i]) + kc, st + BM * kBK * 2 + 1024 * (wave + C::kWaves * i));
+      dma16((second ? pb2[i] : pb[i]) + kc, st + BM * C::kRowBytes + 1024 * (wave + C::kWaves * i));
   };
 
   f32x4 acc[MI][NI];
@@ -378,7 +415,7 @@ __global__ __launch_bounds__((DmaCfg<BM, BN, WM, WN, NS>::kThreads)) void gemm_b
 #pragma unroll
     for (int j = 0; j < NI; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const int nk = g.K / kBK;
+  const int nk = g.K / BK;
 #pragma unroll
   for (int s = 0; s < NS - 1; ++s)
     if (s < nk) issue(s);
@@ -389,39 +426,82 @@ __global__ __launch_bounds__((DmaCfg<BM, BN, WM, WN, NS>::kThreads)) void gemm_b
     __syncthreads();  // every wave's part of tile kt is visible; tile kt-1's buffer is free
     if (kt + NS - 1 < nk) issue(kt + NS - 1);
     const uint16_t* At = reinterpret_cast<const uint16_t*>(smem + (kt % NS) * C::kStage);
-    const uint16_t* Bt = At + BM * kBK;
-#pragma unroll
-    for (int ks = 0; ks < kBK / 32; ++ks) {
+    const uint16_t* Bt = At + BM * BK;
+    // Software pipeline over (substep ks, A fragment i): the read of the next A
+    // fragment is issued before the NI MFMAs of the current one, and the next
+    // substep's B fragments are read halfway through the current substep, so
+    // every LDS wait finds its data already there and the MFMA pipe (whose
+    // issue is blocking) does not idle behind a late read.
+    constexpr int KS = BK / 32;
+    bf16x8 bq[2][NI];
+    auto read_b = [&](int ks, int buf) {
       const int ch = ks * 4 + grp;
-      bf16x8 af[MI], bfr[NI];
-#pragma unroll
-      for (int i = 0; i < MI; ++i) {
-        const int ar = wm * WM + i * 16 + r16;
-        af[i] = *reinterpret_cast<const bf16x8*>(At + ar * kBK + ((ch ^ (ar & 7)) << 3));
-      }
 #pragma unroll
       for (int j = 0; j < NI; ++j) {
         const int br = wn * WN + j * 16 + r16;
-        bfr[j] = *reinterpret_cast<const bf16x8*>(Bt + br * kBK + ((ch ^ (br & 7)) << 3));
+        bq[buf][j] = *reinterpret_cast<const bf16x8*>(Bt + br * BK + (swz<BK>(br, ch) << 3));
       }
+    };
+    auto read_a = [&](int ks, int i) -> bf16x8 {
+      const int ar = wm * WM + i * 16 + r16;
+      return *reinterpret_cast<const bf16x8*>(At + ar * BK + (swz<BK>(ar, ks * 4 + grp) << 3));
+    };
+    read_b(0, 0);
+    bf16x8 a_cur = read_a(0, 0);
 #pragma unroll
-      for (int i = 0; i < MI; ++i)
+    for (int ks = 0; ks < KS; ++ks) {
 #pragma unroll
-        for (int j = 0; j < NI; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+      for (int i = 0; i < MI; ++i) {
+        // the LDS wait before this group's first MFMA covers only reads issued
+        // one group earlier; this group's reads go out right after it
+        acc[i][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_cur, bq[ks & 1][0], acc[i][0], 0, 0, 0);
+        DSF_SCHED_FENCE();
+        bf16x8 a_nxt = a_cur;
+        if (i + 1 < MI) a_nxt = read_a(ks, i + 1);
+        else if (ks + 1 < KS) a_nxt = read_a(ks + 1, 0);
+        if (i == MI / 2 && ks + 1 < KS) read_b(ks + 1, (ks + 1) & 1);
+        DSF_SCHED_FENCE();
+#pragma unroll
+        for (int j = 1; j < NI; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_cur, bq[ks & 1][j], acc[i][j], 0, 0, 0);
+        DSF_SCHED_FENCE();
+        a_cur = a_nxt;
+      }
     }
   }
   __syncthreads();  // all waves are done reading the ring before it becomes the epilogue tile
-  float* stage = reinterpret_cast<float*>(smem);
+  if constexpr (C::kWaveEpi) {
+    // each wave stages and finishes its own tile, 32 rows at a time, as a
+    // 32 x 128 virtual tile whose column index is 2 tn + wn (BN = 256) or tn
+    float* stage = reinterpret_cast<float*>(smem) + wave * 32 * C::kStageLD;
+    const int vtn = tn * (BN / 128) + wn;
 #pragma unroll
-  for (int i = 0; i < MI; ++i)
+    for (int rnd = 0; rnd < MI / 2; ++rnd) {
 #pragma unroll
-    for (int j = 0; j < NI; ++j)
+      for (int ii = 0; ii < 2; ++ii)
 #pragma unroll
-      for (int e = 0; e < 4; ++e)
-        stage[(wm * WM + 16 * i + 4 * grp + e) * C::kStageLD + wn * WN + 16 * j + r16] = acc[i][j][e];
-  __syncthreads();
-  gemm_epilogue<uint16_t, BM, BN, C::kThreads, EPI>(g, stage, m0, tn);
+        for (int j = 0; j < NI; ++j)
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            stage[(16 * ii + 4 * grp + e) * C::kStageLD + 16 * j + r16] = acc[2 * rnd + ii][j][e];
+      __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS writes are done
+      __builtin_amdgcn_wave_barrier();
+      gemm_epilogue<uint16_t, 32, 128, 64, EPI>(g, stage, m0 + wm * WM + 32 * rnd, vtn, lane);
+      __builtin_amdgcn_s_waitcnt(0xc07f);
+      __builtin_amdgcn_wave_barrier();
+    }
+  } else {
+    float* stage = reinterpret_cast<float*>(smem);
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+      for (int j = 0; j < NI; ++j)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          stage[(wm * WM + 16 * i + 4 * grp + e) * C::kStageLD + wn * WN + 16 * j + r16] = acc[i][j][e];
+    __syncthreads();
+    gemm_epilogue<uint16_t, BM, BN, C::kThreads, EPI>(g, stage, m0, tn, threadIdx.x);
+  }
 }
 
 // ------------------------------------------------------------ fp32 GEMM
@@ -489,7 +569,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) stage[(tr * 4 + i) * (kFBN + 4) + tc * 4 + j] = acc[i][j];
   __syncthreads();
-  gemm_epilogue<float, kFBM, kFBN, 256, EPI>(g, stage, m0, tn);
+  gemm_epilogue<float, kFBM, kFBN, 256, EPI>(g, stage, m0, tn, threadIdx.x);
 }
 
 // Build-time tile configuration of the LDS-DMA GEMM (DSF_GEMM_USE_DMA=0 keeps
@@ -499,22 +579,33 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g) {
 #endif
 #ifndef DSF_GEMM_BM
 #define DSF_GEMM_BM 128
+#endif
+#ifndef DSF_GEMM_BN
 #define DSF_GEMM_BN 128
+#endif
+#ifndef DSF_GEMM_WM
 #define DSF_GEMM_WM 64
+#endif
+#ifndef DSF_GEMM_WN
 #define DSF_GEMM_WN 64
+#endif
+#ifndef DSF_GEMM_NS
 #define DSF_GEMM_NS 2
+#endif
+#ifndef DSF_GEMM_BK
+#define DSF_GEMM_BK 64
 #endif
 
 template <int EPI>
 static void launch_gemm_t(const GemmArgs& g, hipStream_t s) {
-  if (DSF_GEMM_USE_DMA && g.dtype == DSF_BF16 && g.K % kBK == 0 && g.K1 % kBK == 0) {
+  if (DSF_GEMM_USE_DMA && g.dtype == DSF_BF16 && g.K % DSF_GEMM_BK == 0 && g.K1 % DSF_GEMM_BK == 0) {
     constexpr int BM = DSF_GEMM_BM, BN = DSF_GEMM_BN;
-    using Cfg = DmaCfg<BM, BN, DSF_GEMM_WM, DSF_GEMM_WN, DSF_GEMM_NS>;
+    using Cfg = DmaCfg<BM, BN, DSF_GEMM_WM, DSF_GEMM_WN, DSF_GEMM_NS, DSF_GEMM_BK>;
     const int ntn = EPI == EPI_SWIGLU ? g.f / (BN / 2) : (g.N + BN - 1) / BN;
     GemmArgs ga = g;
     ga.ntm = (g.M + BM - 1) / BM;
     dim3 grid(ntn * ga.ntm);
-    gemm_bf16_dma_kernel<EPI, BM, BN, DSF_GEMM_WM, DSF_GEMM_WN, DSF_GEMM_NS><<<grid, Cfg::kThreads, 0, s>>>(ga);
+    gemm_bf16_dma_kernel<EPI, BM, BN, DSF_GEMM_WM, DSF_GEMM_WN, DSF_GEMM_NS, DSF_GEMM_BK><<<grid, Cfg::kThreads, 0, s>>>(ga);
   } else if (g.dtype == DSF_BF16) {
     const int ntn = EPI == EPI_SWIGLU ? g.f / (kBN / 2) : (g.N + kBN - 1) / kBN;
     dim3 grid(ntn, (g.M + kBM - 1) / kBM);

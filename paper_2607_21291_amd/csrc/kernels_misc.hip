@@ -113,21 +113,22 @@ hipError_t launch_sim_stats(int dtype, const void* a, const void* c, int64_t n, 
 
 // ------------------------------------------------------------ router, Sec. 3.4
 
-// bf16 router on MFMA. A wavefront scores 32 tokens (two 16-row MFMA blocks)
-// against all d_r hidden units (DR / 16 column blocks). Each lane streams 64
+// bf16 router on MFMA. A wavefront (one per workgroup, so the grid has one
+// workgroup per 16 tokens) scores 16 tokens against all d_r hidden units
+// (DR / 16 column blocks). Each lane streams 64
 // contiguous bytes of its token row per 128-wide k chunk; the MFMA's k slots
 // are filled in that streaming order and W1 is read with the same order, so
 // the contraction is unchanged.
 template <int DR>
-__global__ __launch_bounds__(256) void router_bf16_kernel(const uint16_t* __restrict__ x, int64_t n, int d,
+__global__ __launch_bounds__(64) void router_bf16_kernel(const uint16_t* __restrict__ x, int64_t n, int d,
                                                           const uint16_t* __restrict__ w1,
                                                           const uint16_t* __restrict__ b1,
                                                           const uint16_t* __restrict__ w2, float b2,
                                                           float* __restrict__ scores) {
-  constexpr int RB = 2, NB = DR / 16;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  constexpr int RB = 1, NB = DR / 16;
+  const int lane = threadIdx.x & 63;
   const int r = lane & 15, g = lane >> 4;
-  const int64_t row0 = (int64_t(blockIdx.x) * 4 + w) * (16 * RB);
+  const int64_t row0 = int64_t(blockIdx.x) * (16 * RB);
   if (row0 >= n) return;
   const uint16_t* xr[RB];
 #pragma unroll
@@ -236,16 +237,16 @@ hipError_t launch_router(int dtype, const void* x, int64_t n, int d, int d_r, co
                                                             (const float*)b1, (const float*)w2, b2, scores);
     return hipGetLastError();
   }
-  unsigned grid = unsigned((n + 127) / 128);
+  unsigned grid = unsigned((n + 15) / 16);
   auto X = (const uint16_t*)x;
   auto W1 = (const uint16_t*)w1;
   auto B1 = (const uint16_t*)b1;
   auto W2 = (const uint16_t*)w2;
   switch (d_r) {
-    case 16: router_bf16_kernel<16><<<grid, 256, 0, s>>>(X, n, d, W1, B1, W2, b2, scores); break;
-    case 32: router_bf16_kernel<32><<<grid, 256, 0, s>>>(X, n, d, W1, B1, W2, b2, scores); break;
-    case 48: router_bf16_kernel<48><<<grid, 256, 0, s>>>(X, n, d, W1, B1, W2, b2, scores); break;
-    case 64: router_bf16_kernel<64><<<grid, 256, 0, s>>>(X, n, d, W1, B1, W2, b2, scores); break;
+    case 16: router_bf16_kernel<16><<<grid, 64, 0, s>>>(X, n, d, W1, B1, W2, b2, scores); break;
+    case 32: router_bf16_kernel<32><<<grid, 64, 0, s>>>(X, n, d, W1, B1, W2, b2, scores); break;
+    case 48: router_bf16_kernel<48><<<grid, 64, 0, s>>>(X, n, d, W1, B1, W2, b2, scores); break;
+    case 64: router_bf16_kernel<64><<<grid, 64, 0, s>>>(X, n, d, W1, B1, W2, b2, scores); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -284,27 +285,46 @@ __device__ __forceinline__ uint32_t block_excl_count(bool flag, uint32_t* wave_t
   return before + within;
 }
 
-// One block per sequence. Radix select (8 bits per pass, most significant
-// first) finds the key of the k-th largest score and how many of the keys
-// equal to it are kept; a final ordered pass keeps every larger key and the
+// One block per sequence. The order-preserving keys of the sequence are kept
+// in LDS (read from global memory once). Radix select (8 bits per pass, most
+// significant first) finds the key of the k-th largest score and how many of
+// the keys equal to it are kept; each wavefront counts into its own histogram
+// so that equal digits (frequent in the top byte) do not serialise on one LDS
+// address. A final ordered pass keeps every larger key and the
 // lowest-positioned equal keys, writing positions in ascending order.
+constexpr int kTopkLdsKeys = 16384;  // sequences up to this length keep their keys in LDS
+
+template <bool KEYS_IN_LDS>
 __global__ __launch_bounds__(kTopkThreads) void topk_kernel(const float* __restrict__ scores, int T, int k,
                                                             int32_t* __restrict__ idx) {
   const float* sc = scores + int64_t(blockIdx.x) * T;
   int32_t* out = idx + int64_t(blockIdx.x) * k;
+  __shared__ uint32_t keys[KEYS_IN_LDS ? kTopkLdsKeys : 1];
+  __shared__ uint32_t whist[kTopkWaves][256];
   __shared__ uint32_t hist[256];
   __shared__ uint32_t wave_tot[kTopkWaves];
   __shared__ uint32_t sh_digit, sh_remaining;
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, wave = tid >> 6;
+  auto key_at = [&](int t) -> uint32_t { return KEYS_IN_LDS ? keys[t] : score_key(sc[t]); };
 
+  if constexpr (KEYS_IN_LDS) {
+    for (int t = tid; t < T; t += kTopkThreads) keys[t] = score_key(sc[t]);
+  }
   uint32_t prefix = 0, mask = 0, remaining = uint32_t(k);
   for (int pass = 0; pass < 4; ++pass) {
     const int shift = 24 - 8 * pass;
-    if (tid < 256) hist[tid] = 0;
+    for (int i = tid; i < kTopkWaves * 256; i += kTopkThreads) (&whist[0][0])[i] = 0;
     __syncthreads();
     for (int t = tid; t < T; t += kTopkThreads) {
-      uint32_t key = score_key(sc[t]);
-      if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+      const uint32_t key = key_at(t);
+      if ((key & mask) == prefix) atomicAdd(&whist[wave][(key >> shift) & 255u], 1u);
+    }
+    __syncthreads();
+    if (tid < 256) {
+      uint32_t c = 0;
+#pragma unroll
+      for (int w = 0; w < kTopkWaves; ++w) c += whist[w][tid];
+      hist[tid] = c;
     }
     __syncthreads();
     if (tid < 64) {
@@ -335,14 +355,13 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(const float* __restr
     prefix |= sh_digit << shift;
     mask |= 255u << shift;
     remaining = sh_remaining;
-    __syncthreads();
   }
   // prefix is now the k-th largest key; `remaining` equal keys are kept.
   uint32_t run_eq = 0, run_sel = 0;
   for (int base = 0; base < T; base += kTopkThreads) {
     const int t = base + tid;
     const bool valid = t < T;
-    const uint32_t key = valid ? score_key(sc[t]) : 0u;
+    const uint32_t key = valid ? key_at(t) : 0u;
     const bool eq = valid && key == prefix;
     uint32_t tot_eq, tot_sel;
     const uint32_t eq_before = run_eq + block_excl_count(eq, wave_tot, tot_eq);
@@ -357,7 +376,8 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(const float* __restr
 hipError_t launch_topk(const float* scores, int B, int T, int k, int32_t* idx, hipStream_t s) {
   if (k == 0 || B == 0) return hipSuccess;
   TimedScope ts(DSF_KIND_TOPK, s);
-  topk_kernel<<<B, kTopkThreads, 0, s>>>(scores, T, k, idx);
+  if (T <= kTopkLdsKeys) topk_kernel<true><<<B, kTopkThreads, 0, s>>>(scores, T, k, idx);
+  else topk_kernel<false><<<B, kTopkThreads, 0, s>>>(scores, T, k, idx);
   return hipGetLastError();
 }
 

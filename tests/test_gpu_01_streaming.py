@@ -79,7 +79,7 @@ def _check_topk(dev, scores: torch.Tensor, k: int):
     np.testing.assert_array_equal(idx[:, :k].cpu().numpy(), ref)
 
 
-@pytest.mark.parametrize("B,T", [(1, 1), (3, 64), (2, 1000), (8, 2048), (4, 8192), (1, 12345)])
+@pytest.mark.parametrize("B,T", [(1, 1), (3, 64), (2, 1000), (8, 2048), (4, 8192), (1, 12345), (2, 20000)])
 def test_topk_random(dev, B, T):
     sc = S.random_scores(B, T, seed=B * T)
     for k in sorted({0, 1, T // 3, T // 2, T - 1, T}):
