@@ -18,6 +18,9 @@ BUILD = os.path.join(ROOT, "_build", "adadsf")
 LIB = os.path.join(PKG, "libadadsf.so")
 
 SOURCES = ["api.hip", "kernels_misc.hip", "kernels_gemm.hip", "kernels_attn.hip"]
+# per-source extra flags: attention keeps its MFMA accumulators in ordinary
+# VGPRs, so the softmax reads scores and rescales outputs without AGPR moves
+EXTRA = {"kernels_attn.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
 ARCH = "gfx950"
 CFLAGS = [
@@ -58,7 +61,7 @@ def build(verbose: bool = False) -> str:
         for src in SOURCES:
             obj = os.path.join(BUILD, src.replace(".hip", ".o"))
             objs.append(obj)
-            cmd = [cc, *CFLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+            cmd = [cc, *CFLAGS, *EXTRA.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
             jobs.append(ex.submit(_run, cmd, verbose))
         for j in jobs:
             j.result()

@@ -107,6 +107,20 @@ __device__ __forceinline__ int xcd_remap(int L, int W) {
   return x * q + (x < r ? x : r) + L / kXcds;
 }
 
+// Sum over the 16 lanes of each row with DPP lane moves (VALU only):
+// xor 1 and xor 2 via quad permutes, then the half-row mirror pairs the two
+// quads of each 8 lanes and the row mirror the two halves of the row. Every
+// lane of the row ends with the same value (+ is commutative).
+#define DSF_DPP(v, ctrl) __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), (ctrl), 0xF, 0xF, false))
+__device__ __forceinline__ float row16_sum(float v) {
+  v += DSF_DPP(v, 0xB1);   // quad_perm [1,0,3,2]: lane ^ 1
+  v += DSF_DPP(v, 0x4E);   // quad_perm [2,3,0,1]: lane ^ 2
+  v += DSF_DPP(v, 0x141);  // row_half_mirror
+  v += DSF_DPP(v, 0x140);  // row_mirror
+  return v;
+}
+__device__ __forceinline__ float wave_sum_fast(float v) { return rows4_sum(row16_sum(v)); }
+
 // Positions supplied by a caller are clamped into [0, T) so that a bad index
 // cannot address memory outside the hidden-state rows.
 __device__ __forceinline__ int clamp_pos(int p, int T) { return p < 0 ? 0 : (p >= T ? T - 1 : p); }

@@ -45,23 +45,26 @@ struct AttnPrefetch {
   u32x4 k[A::kKIter];
   u32x4 v0[A::kVIter], v1[A::kVIter];
 
+  // Rows past the last key are loaded from row n - 1 (always valid memory):
+  // their scores are masked to -inf and their V rows are weighted by zero.
   __device__ __forceinline__ void load(const uint16_t* Kh, const uint16_t* Vh, int kb0, int n, int tid) {
 #pragma unroll
     for (int i = 0; i < A::kKIter; ++i) {
       const int c = tid + 256 * i;
-      const int key = kb0 + c / A::kNch;
-      k[i] = (c < A::kKChunks && key < n) ? *reinterpret_cast<const u32x4*>(Kh + int64_t(key) * HD + (c % A::kNch) * 8)
-                                          : u32x4{0, 0, 0, 0};
+      if (A::kKChunks % 256 == 0 || c < A::kKChunks) {
+        const int key = min(kb0 + c / A::kNch, n - 1);
+        k[i] = *reinterpret_cast<const u32x4*>(Kh + int64_t(key) * HD + (c % A::kNch) * 8);
+      }
     }
 #pragma unroll
     for (int i = 0; i < A::kVIter; ++i) {
       const int c = tid + 256 * i;
-      const int kp = c % (kKV / 2), ch = c / (kKV / 2);
-      const int key0 = kb0 + 2 * kp;
-      const bool ok = c < A::kVPairs;
-      v0[i] = (ok && key0 < n) ? *reinterpret_cast<const u32x4*>(Vh + int64_t(key0) * HD + ch * 8) : u32x4{0, 0, 0, 0};
-      v1[i] = (ok && key0 + 1 < n) ? *reinterpret_cast<const u32x4*>(Vh + int64_t(key0 + 1) * HD + ch * 8)
-                                   : u32x4{0, 0, 0, 0};
+      if (A::kVPairs % 256 == 0 || c < A::kVPairs) {
+        const int kp = c % (kKV / 2), ch = c / (kKV / 2);
+        const int key0 = min(kb0 + 2 * kp, n - 1), key1 = min(kb0 + 2 * kp + 1, n - 1);
+        v0[i] = *reinterpret_cast<const u32x4*>(Vh + int64_t(key0) * HD + ch * 8);
+        v1[i] = *reinterpret_cast<const u32x4*>(Vh + int64_t(key1) * HD + ch * 8);
+      }
     }
   }
   // K row-major with swizzled chunks; V transposed, Vt[dim][key], two keys per 32-bit store
@@ -81,8 +84,9 @@ struct AttnPrefetch {
         const int kp = c % (kKV / 2), ch = c / (kKV / 2);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const uint32_t lo = (v0[i][e] & 0xffffu) | (v1[i][e] << 16);
-          const uint32_t hi = (v0[i][e] >> 16) | (v1[i][e] & 0xffff0000u);
+          // lo = (v0.lo16, v1.lo16), hi = (v0.hi16, v1.hi16), one byte permute each
+          const uint32_t lo = __builtin_amdgcn_perm(v1[i][e], v0[i][e], 0x05040100u);
+          const uint32_t hi = __builtin_amdgcn_perm(v1[i][e], v0[i][e], 0x07060302u);
           *reinterpret_cast<uint32_t*>(Vt + (ch * 8 + 2 * e) * kVtLD + 2 * kp) = lo;
           *reinterpret_cast<uint32_t*>(Vt + (ch * 8 + 2 * e + 1) * kVtLD + 2 * kp) = hi;
         }
@@ -102,7 +106,8 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const uint16_t* __restri
   constexpr int ND = HD / 16;          // 16-row blocks of the head dim
   __shared__ __attribute__((aligned(16))) char smem[2 * A::kStage];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: keeps tile tests scalar
   const int r16 = lane & 15, grp = lane >> 4;
   // one work item per (sequence, head, query block); the query blocks of one
   // (sequence, head) share K/V, so they are kept on one XCD (longest first)
@@ -173,26 +178,27 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const uint16_t* __restri
             s[qi][kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[qi][st], s[qi][kb], 0, 0, 0);
         }
       }
-      const bool diag = kb0 + kKV - 1 > qw0 || kb0 + kKV > n;
+      const bool diag = kb0 + kKV - 1 > qw0 || kb0 + kKV > n;  // wave-uniform
       bf16x8 pb[NQ][2];
 #pragma unroll
       for (int qi = 0; qi < NQ; ++qi) {
-        const int qg = qw0 + 16 * qi + r16;
+        if (diag) {
+          // key kb0 + 4 grp + (16 kb + i) is visible to query qg iff 16 kb + i <= lim
+          const int qg = qw0 + 16 * qi + r16;
+          const int lim = min(qg, n - 1) - (kb0 + 4 * grp);
+#pragma unroll
+          for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) s[qi][kb][i] = (16 * kb + i > lim) ? -INFINITY : s[qi][kb][i];
+        }
         float mx = -INFINITY;
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            if (diag) {
-              const int key = kb0 + 16 * kb + 4 * grp + i;
-              if (key > qg || key >= n) s[qi][kb][i] = -INFINITY;
-            }
-            mx = fmaxf(mx, s[qi][kb][i]);
-          }
+          for (int i = 0; i < 4; ++i) mx = fmaxf(mx, s[qi][kb][i]);
         // running max in log2 units of the scaled scores (sc > 0 keeps the order)
         const float m_new = fmaxf(m_run[qi], rows4_max(mx) * sc);
         const float base = m_new == -INFINITY ? 0.f : m_new;
-        const float alpha = __builtin_amdgcn_exp2f(m_run[qi] - base);
         float sum = 0.f;
         float p[4][4];
 #pragma unroll
@@ -202,10 +208,16 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const uint16_t* __restri
             p[kb][i] = __builtin_amdgcn_exp2f(fmaf(s[qi][kb][i], sc, -base));
             sum += p[kb][i];
           }
-        l_run[qi] = l_run[qi] * alpha + rows4_sum(sum);
-        m_run[qi] = m_new;
+        sum = rows4_sum(sum);
+        // rescale the running sums only when some lane's max moved (rare after the first tiles)
+        if (__builtin_amdgcn_ballot_w64(m_new != m_run[qi])) {
+          const float alpha = __builtin_amdgcn_exp2f(m_run[qi] - base);
+          l_run[qi] *= alpha;
 #pragma unroll
-        for (int db = 0; db < ND; ++db) o[qi][db] *= alpha;
+          for (int db = 0; db < ND; ++db) o[qi][db] *= alpha;
+        }
+        l_run[qi] += sum;
+        m_run[qi] = m_new;
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks)
 #pragma unroll

@@ -113,44 +113,37 @@ hipError_t launch_sim_stats(int dtype, const void* a, const void* c, int64_t n, 
 
 // ------------------------------------------------------------ router, Sec. 3.4
 
-// bf16 router on MFMA. A wavefront (one per workgroup, so the grid has one
-// workgroup per 16 tokens) scores 16 tokens against all d_r hidden units
-// (DR / 16 column blocks). Each lane streams 64
-// contiguous bytes of its token row per 128-wide k chunk; the MFMA's k slots
-// are filled in that streaming order and W1 is read with the same order, so
-// the contraction is unchanged.
+// bf16 router on MFMA. A workgroup of four wavefronts scores 16 tokens
+// against all d_r hidden units (DR / 16 column blocks of
+// v_mfma_f32_16x16x32_bf16); the reduction over d is split between the
+// wavefronts (wavefront w takes 128-wide chunks w, w + 4, ...), which keeps
+// many independent row streams in flight, and the partial hidden sums meet in
+// LDS. Within a chunk each lane streams 64 contiguous bytes of its row; the
+// MFMA's k slots are filled in that order and W1 is read in the same order,
+// so the contraction is unchanged.
 template <int DR>
-__global__ __launch_bounds__(64) void router_bf16_kernel(const uint16_t* __restrict__ x, int64_t n, int d,
+__global__ __launch_bounds__(256) void router_bf16_kernel(const uint16_t* __restrict__ x, int64_t n, int d,
                                                           const uint16_t* __restrict__ w1,
                                                           const uint16_t* __restrict__ b1,
                                                           const uint16_t* __restrict__ w2, float b2,
                                                           float* __restrict__ scores) {
-  constexpr int RB = 1, NB = DR / 16;
-  const int lane = threadIdx.x & 63;
+  constexpr int NB = DR / 16, NW = 4;
+  __shared__ float part[NW][16][DR + 1];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int r = lane & 15, g = lane >> 4;
-  const int64_t row0 = int64_t(blockIdx.x) * (16 * RB);
-  if (row0 >= n) return;
-  const uint16_t* xr[RB];
+  const int64_t row0 = int64_t(blockIdx.x) * 16;
+  int64_t row = row0 + r;
+  if (row > n - 1) row = n - 1;  // clamp: rows past the end are computed and dropped
+  const uint16_t* xr = x + row * d;
+  f32x4 acc[NB];
 #pragma unroll
-  for (int rb = 0; rb < RB; ++rb) {
-    int64_t row = row0 + rb * 16 + r;
-    if (row > n - 1) row = n - 1;  // clamp: rows past the end are computed and dropped
-    xr[rb] = x + row * d;
-  }
-  f32x4 acc[RB][NB];
-#pragma unroll
-  for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) acc[rb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  int kc = 0;
-  for (; kc + 128 <= d; kc += 128) {
-    bf16x8 xa[RB][4], wb[NB][4];
+  const int dfull = (d / 128) * 128;
+  for (int kc = 128 * w; kc < dfull; kc += 128 * NW) {
+    bf16x8 xa[4], wb[NB][4];
 #pragma unroll
-    for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-      for (int s4 = 0; s4 < 4; ++s4)
-        xa[rb][s4] = *reinterpret_cast<const bf16x8*>(xr[rb] + kc + 32 * g + 8 * s4);
+    for (int s4 = 0; s4 < 4; ++s4) xa[s4] = *reinterpret_cast<const bf16x8*>(xr + kc + 32 * g + 8 * s4);
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
@@ -159,29 +152,28 @@ __global__ __launch_bounds__(64) void router_bf16_kernel(const uint16_t* __restr
 #pragma unroll
     for (int s4 = 0; s4 < 4; ++s4)
 #pragma unroll
-      for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb)
-          acc[rb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[rb][s4], wb[nb][s4], acc[rb][nb], 0, 0, 0);
+      for (int nb = 0; nb < NB; ++nb)
+        acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[s4], wb[nb][s4], acc[nb], 0, 0, 0);
   }
-  // tail: 32-wide steps, 8-element pieces past d are zero
-  for (; kc < d; kc += 32) {
+  // tail (d % 128): 32-wide steps split the same way; 8-element pieces past d are zero
+  for (int kc = dfull + 32 * w; kc < d; kc += 32 * NW) {
     const int k0 = kc + 8 * g;
     const bool ok = k0 < d;
-    bf16x8 zero = {};
-    bf16x8 xa[RB], wb[NB];
+    const bf16x8 zero = {};
+    const bf16x8 xa = ok ? *reinterpret_cast<const bf16x8*>(xr + k0) : zero;
 #pragma unroll
-    for (int rb = 0; rb < RB; ++rb) xa[rb] = ok ? *reinterpret_cast<const bf16x8*>(xr[rb] + k0) : zero;
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
-      wb[nb] = ok ? *reinterpret_cast<const bf16x8*>(w1 + (16 * nb + r) * int64_t(d) + k0) : zero;
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
-        acc[rb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[rb], wb[nb], acc[rb][nb], 0, 0, 0);
+    for (int nb = 0; nb < NB; ++nb) {
+      const bf16x8 wb = ok ? *reinterpret_cast<const bf16x8*>(w1 + (16 * nb + r) * int64_t(d) + k0) : zero;
+      acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa, wb, acc[nb], 0, 0, 0);
+    }
   }
-  // lane holds hidden[token 16 rb + 4 g + i][unit 16 nb + r]
+  // lane holds partial hidden[token 4 g + i][unit 16 nb + r]
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) part[w][4 * g + i][16 * nb + r] = acc[nb][i];
+  __syncthreads();
+  if (w != 0) return;
   float wv[NB], bv[NB];
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
@@ -189,22 +181,18 @@ __global__ __launch_bounds__(64) void router_bf16_kernel(const uint16_t* __restr
     bv[nb] = b1 ? bf2f(b1[16 * nb + r]) : 0.f;
   }
 #pragma unroll
-  for (int rb = 0; rb < RB; ++rb) {
+  for (int i = 0; i < 4; ++i) {
+    const int t = 4 * g + i;
+    float v = 0.f;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      float v = 0.f;
+    for (int nb = 0; nb < NB; ++nb) {
+      float h = bv[nb];
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        float h = acc[rb][nb][i] + bv[nb];
-        v += wv[nb] * (h > 0.f ? h : 0.f);
-      }
-      v += __shfl_xor(v, 1, 64);
-      v += __shfl_xor(v, 2, 64);
-      v += __shfl_xor(v, 4, 64);
-      v += __shfl_xor(v, 8, 64);
-      int64_t row = row0 + rb * 16 + 4 * g + i;
-      if (r == 0 && row < n) scores[row] = v + b2;
+      for (int ww = 0; ww < NW; ++ww) h += part[ww][t][16 * nb + r];
+      v += wv[nb] * (h > 0.f ? h : 0.f);
     }
+    v = row16_sum(v);
+    if (r == 0 && row0 + t < n) scores[row0 + t] = v + b2;
   }
 }
 
@@ -243,10 +231,10 @@ hipError_t launch_router(int dtype, const void* x, int64_t n, int d, int d_r, co
   auto B1 = (const uint16_t*)b1;
   auto W2 = (const uint16_t*)w2;
   switch (d_r) {
-    case 16: router_bf16_kernel<16><<<grid, 64, 0, s>>>(X, n, d, W1, B1, W2, b2, scores); break;
-    case 32: router_bf16_kernel<32><<<grid, 64, 0, s>>>(X, n, d, W1, B1, W2, b2, scores); break;
-    case 48: router_bf16_kernel<48><<<grid, 64, 0, s>>>(X, n, d, W1, B1, W2, b2, scores); break;
-    case 64: router_bf16_kernel<64><<<grid, 64, 0, s>>>(X, n, d, W1, B1, W2, b2, scores); break;
+    case 16: router_bf16_kernel<16><<<grid, 256, 0, s>>>(X, n, d, W1, B1, W2, b2, scores); break;
+    case 32: router_bf16_kernel<32><<<grid, 256, 0, s>>>(X, n, d, W1, B1, W2, b2, scores); break;
+    case 48: router_bf16_kernel<48><<<grid, 256, 0, s>>>(X, n, d, W1, B1, W2, b2, scores); break;
+    case 64: router_bf16_kernel<64><<<grid, 256, 0, s>>>(X, n, d, W1, B1, W2, b2, scores); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -505,9 +493,9 @@ __global__ __launch_bounds__(256) void norm_kernel(NormArgs a) {
       if (lane + 64 * c < nvec)
 #pragma unroll
         for (int i = 0; i < V; ++i) sq += v[c][i] * v[c][i];
-    var = wave_sum(sq) / float(d);
+    var = wave_sum_fast(sq) / float(d);
   } else {
-    mean = wave_sum(sum) / float(d);
+    mean = wave_sum_fast(sum) / float(d);
     float sq = 0.f;
 #pragma unroll
     for (int c = 0; c < MAXC; ++c)
@@ -517,7 +505,7 @@ __global__ __launch_bounds__(256) void norm_kernel(NormArgs a) {
           float t = v[c][i] - mean;
           sq += t * t;
         }
-    var = wave_sum(sq) / float(d);
+    var = wave_sum_fast(sq) / float(d);
   }
   const float rstd = 1.0f / sqrtf(var + a.eps);
   for (int o = 0; o < 2; ++o) {
