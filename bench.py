@@ -35,6 +35,30 @@ PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 
 
+# HBM traffic of the dominant kernel, from two rocprofv3 passes (FETCH_SIZE,
+# then WRITE_SIZE, per dispatch) scaled by what the same counters read for the
+# library's plain copy kernel of known size. It holds only for the workload
+# and the GEMM source it was measured on (SHA-256 of kernels_gemm.hip); for
+# anything else `traffic` is null.
+TRAFFIC_MEASURED = {"workload": "neox160m", "bytes_per_launch": 2.035e+08,
+                    "gemm_source_sha256": "1c55c6d343d7153c80243325670439a6d107f172a724124a5167f0da5243cfa8",
+                    "profile": "profiles/gemm_down_neox160m.md"}
+
+
+def gemm_source_sha256():
+    import hashlib
+    path = os.path.join(ROOT, "paper_2607_21291_amd", "csrc", "kernels_gemm.hip")
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def measured_traffic(workload):
+    t = TRAFFIC_MEASURED
+    if not t or t["workload"] != workload or t["gemm_source_sha256"] != gemm_source_sha256():
+        return None
+    return t["bytes_per_launch"]
+
+
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
@@ -169,8 +193,10 @@ def main():
     avg_ms = ms_dom / max(n_dom, 1)
     achieved = flops_dom / (ms_dom / 1e3) / 1e12 if ms_dom > 0 else 0.0
     roofline = {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
-                "kernel": "gemm_bf16_kernel<4> (last GEMM of a layer, residual-scatter epilogue)",
+                "frac": achieved / PEAK_BF16_TFLOPS, "traffic": measured_traffic(w.name),
+                "kernel": "down projection: gemm_bf16_dma_kernel<4, 128, 128, 64, 64, 2, 64> (one tile per "
+                          "workgroup) or gemm_bf16_sk_kernel<4, 128, 128, 64, 64, 2, 64> (stream-K, on layers "
+                          "whose tiles leave a short last round); residual-scatter epilogue",
                 "launches": n_dom, "avg_launch_us": avg_ms * 1e3,
                 "flops_per_launch": flops_dom / max(n_dom, 1)}
 

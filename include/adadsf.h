@@ -208,7 +208,19 @@ int dsf_attention_forward(const void* q, const void* k, const void* v, int dtype
 /* Workspace bytes that dsf_sparse_block_forward / dsf_stack_forward need for
  * batch B, sequence length T and at most k_max kept tokens per sequence
  * (k_max = T for DSF_FLAG_DENSE). with_similarity != 0 adds room to keep each
- * layer's input for the similarity statistic. Returns 0 on a bad argument. */
+ * layer's input for the similarity statistic. For DSF_BF16 it includes a
+ * fixed 32 MiB (+ 2 KiB) for the partial sums and flags of the stream-K
+ * projection schedule. The contents need no initialisation; each call
+ * resets what it uses, so two calls that overlap in time (on different
+ * streams) need two workspaces. Returns 0 on a bad argument.
+ *
+ * Projection schedule. Each bf16 projection GEMM runs either one output tile
+ * per workgroup or, when that would end in a short last round of tiles on a
+ * long reduction, a stream-K grid (workgroups split the k-iterations of the
+ * last tiles and add their partial sums in a fixed order). Both are
+ * deterministic; they round differently. The environment variable
+ * DSF_GEMM_SCHEDULE=classic or =streamk, read at every launch, forces one of
+ * them (testing and tuning). */
 size_t dsf_workspace_size(const dsf_layer_desc* desc, int dtype, int B, int T, int k_max,
                           int with_similarity);
 

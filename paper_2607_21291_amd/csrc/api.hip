@@ -81,6 +81,8 @@ namespace {
 struct TimingRec {
   int kind;
   hipEvent_t start, stop;
+  bool deferred;  // opened without a start event: the launcher records both (timing_claim)
+  bool claimed;
 };
 std::mutex g_tmu;
 std::vector<TimingRec> g_recs;
@@ -90,16 +92,30 @@ uint32_t g_mask = 0;
 }  // namespace
 
 namespace dsf {
-void timing_begin(int kind, hipStream_t s) {
+void timing_begin(int kind, hipStream_t s, bool deferred) {
   std::lock_guard<std::mutex> lock(g_tmu);
   if (g_used >= g_recs.size() || g_open >= 0 || !((g_mask >> kind) & 1u)) return;
-  g_recs[g_used].kind = kind;
-  if (hipEventRecord(g_recs[g_used].start, s) == hipSuccess) g_open = long(g_used);
+  TimingRec& r = g_recs[g_used];
+  r.kind = kind;
+  r.deferred = deferred;
+  r.claimed = false;
+  if (deferred || hipEventRecord(r.start, s) == hipSuccess) g_open = long(g_used);
+}
+bool timing_claim(hipEvent_t* start, hipEvent_t* stop) {
+  std::lock_guard<std::mutex> lock(g_tmu);
+  if (g_open < 0) return false;
+  TimingRec& r = g_recs[g_open];
+  if (!r.deferred || r.claimed) return false;
+  r.claimed = true;
+  *start = r.start;
+  *stop = r.stop;
+  return true;
 }
 void timing_end(int kind, hipStream_t s) {
   std::lock_guard<std::mutex> lock(g_tmu);
   if (g_open < 0 || g_recs[g_open].kind != kind) return;
-  if (hipEventRecord(g_recs[g_open].stop, s) == hipSuccess) ++g_used;
+  TimingRec& r = g_recs[g_open];
+  if (r.deferred ? r.claimed : hipEventRecord(r.stop, s) == hipSuccess) ++g_used;
   g_open = -1;
 }
 }  // namespace dsf
@@ -121,6 +137,7 @@ extern "C" int dsf_timing_enable(int max_records, uint32_t kind_mask) {
   g_recs.resize(size_t(max_records));
   for (auto& r : g_recs) {
     r.kind = -1;
+    r.deferred = r.claimed = false;
     DSF_HIP(hipEventCreate(&r.start));
     DSF_HIP(hipEventCreate(&r.stop));
   }
@@ -342,7 +359,7 @@ extern "C" int dsf_attention_forward(const void* q, const void* k, const void* v
 
 namespace {
 struct Plan {
-  size_t scores, idx, a1, a2, q, k, v, attn, act, h, m2, rope, xin, simpart, total;
+  size_t scores, idx, a1, a2, q, k, v, attn, act, h, m2, rope, xin, simpart, skpart, skflags, total;
 };
 
 size_t up256(size_t x) { return (x + 255) / 256 * 256; }
@@ -372,6 +389,9 @@ Plan make_plan(const dsf_layer_desc& D, int dtype, int B, int T, int k_max, bool
   p.rope = take(4 * size_t(T) * D.rotary_dims);
   p.xin = with_sim ? take(eb * size_t(B) * T * D.d_model) : 0;
   p.simpart = with_sim ? take(dsf_sim_workspace_size(int64_t(B) * T)) : 0;
+  // stream-K partial tiles and their flags (bf16 GEMMs)
+  p.skpart = dtype == DSF_BF16 ? take(gemm_partial_bytes()) : 0;
+  p.skflags = dtype == DSF_BF16 ? take(sizeof(uint32_t) * gemm_flag_count()) : 0;
   p.total = off;
   return p;
 }
@@ -429,7 +449,26 @@ struct Ctx {
   char* ws;
   Plan plan;
   hipStream_t s;
+  mutable uint32_t epoch;  // last stream-K epoch handed out since the flags were zeroed
 };
+
+uint32_t* at_flags(const Ctx& c) { return reinterpret_cast<uint32_t*>(c.ws + c.plan.skflags); }
+
+// Zero the stream-K flags at the start of a call; GEMM launches then take
+// epochs 1, 2, ... (the flags of a finished launch never equal a later epoch).
+int reset_stream_k(const Ctx& c) {
+  c.epoch = 0;
+  if (c.dtype == DSF_BF16) DSF_HIP(launch_zero_u32(at_flags(c), gemm_flag_count(), c.s));
+  return DSF_OK;
+}
+
+// The stream-K fields of a GEMM launch on this call's workspace.
+void use_stream_k(const Ctx& c, GemmArgs& g) {
+  if (c.dtype != DSF_BF16) return;
+  g.part = reinterpret_cast<float*>(c.ws + c.plan.skpart);
+  g.flags = at_flags(c);
+  g.epoch = ++c.epoch;
+}
 
 template <typename P>
 P* at(const Ctx& c, size_t off) {
@@ -497,7 +536,8 @@ int run_layer(const Ctx& c, const dsf_layer_weights* W, void* x, int k, bool den
     q.q = at<char>(c, c.plan.q); q.k = at<char>(c, c.plan.k); q.v = at<char>(c, c.plan.v);
     q.Hq = Hq; q.Hkv = Hkv; q.hd = hd; q.R = D.rotary_dims;
     q.rope = at<float>(c, c.plan.rope);
-    TimedScope ts(DSF_KIND_GEMM_QKV, c.s);
+    TimedScope ts(DSF_KIND_GEMM_QKV, c.s, true);
+    use_stream_k(c, q);
     DSF_HIP(launch_gemm(q, c.s));
   }
   DSF_HIP(launch_attention(c.dtype, at<char>(c, c.plan.q), at<char>(c, c.plan.k), at<char>(c, c.plan.v), B, Hq,
@@ -510,7 +550,8 @@ int run_layer(const Ctx& c, const dsf_layer_weights* W, void* x, int k, bool den
       u.b = W->w_up; u.ldb = d;
       u.epi = EPI_BIAS_GELU; u.bias = W->b_up;
       u.out = at<char>(c, c.plan.act); u.ldo = f;
-      TimedScope ts(DSF_KIND_GEMM_UP, c.s);
+      TimedScope ts(DSF_KIND_GEMM_UP, c.s, true);
+      use_stream_k(c, u);
       DSF_HIP(launch_gemm(u, c.s));
     }
     {  // parallel residual: [attn | act] . [W_o | W_down]^T + b_o + b_down + x, scattered back
@@ -522,7 +563,8 @@ int run_layer(const Ctx& c, const dsf_layer_weights* W, void* x, int k, bool den
       o.b2 = W->w_down; o.ldb2 = f;
       o.epi = EPI_RESID_SCATTER; o.bias = W->b_o; o.bias2 = W->b_down;
       o.x = x;
-      TimedScope ts(DSF_KIND_GEMM_DOWN, c.s);
+      TimedScope ts(DSF_KIND_GEMM_DOWN, c.s, true);
+      use_stream_k(c, o);
       DSF_HIP(launch_gemm(o, c.s));
     }
     return DSF_OK;
@@ -534,7 +576,8 @@ int run_layer(const Ctx& c, const dsf_layer_weights* W, void* x, int k, bool den
     o.b = W->w_o; o.ldb = dq;
     o.epi = EPI_RESID_STORE; o.bias = W->b_o;
     o.x = x; o.out = at<char>(c, c.plan.h); o.ldo = d;
-    TimedScope ts(DSF_KIND_GEMM_O, c.s);
+    TimedScope ts(DSF_KIND_GEMM_O, c.s, true);
+    use_stream_k(c, o);
     DSF_HIP(launch_gemm(o, c.s));
   }
   NormArgs n2{};
@@ -556,7 +599,8 @@ int run_layer(const Ctx& c, const dsf_layer_weights* W, void* x, int k, bool den
     u.b = W->w_up; u.ldb = d;
     u.epi = EPI_SWIGLU; u.f = f;
     u.out = at<char>(c, c.plan.act); u.ldo = f;
-    TimedScope ts(DSF_KIND_GEMM_UP, c.s);
+    TimedScope ts(DSF_KIND_GEMM_UP, c.s, true);
+    use_stream_k(c, u);
     DSF_HIP(launch_gemm(u, c.s));
   }
   {  // y = h + act . W_down^T, scattered back
@@ -566,7 +610,8 @@ int run_layer(const Ctx& c, const dsf_layer_weights* W, void* x, int k, bool den
     o.b = W->w_down; o.ldb = f;
     o.epi = EPI_RESID_SCATTER; o.bias = W->b_down;
     o.x = x; o.res = at<char>(c, c.plan.h);
-    TimedScope ts(DSF_KIND_GEMM_DOWN, c.s);
+    TimedScope ts(DSF_KIND_GEMM_DOWN, c.s, true);
+    use_stream_k(c, o);
     DSF_HIP(launch_gemm(o, c.s));
   }
   return DSF_OK;
@@ -609,7 +654,9 @@ extern "C" int dsf_sparse_block_forward(const dsf_layer_desc* desc, const dsf_la
   if (rc) return rc;
   rc = check_device();
   if (rc) return rc;
-  Ctx c{desc, dtype, B, T, (char*)workspace, plan, stream};
+  Ctx c{desc, dtype, B, T, (char*)workspace, plan, stream, 0};
+  rc = reset_stream_k(c);
+  if (rc) return rc;
   DSF_HIP(launch_rope_table(at<float>(c, plan.rope), T, desc->rotary_dims, desc->rope_theta, stream));
   return run_layer(c, weights, x, k, dense, scores_out, idx_out, idx_in);
 }
@@ -638,7 +685,9 @@ extern "C" int dsf_stack_forward(const dsf_layer_desc* desc, const dsf_layer_wei
   }
   rc = check_device();
   if (rc) return rc;
-  Ctx c{desc, dtype, B, T, (char*)workspace, plan, stream};
+  Ctx c{desc, dtype, B, T, (char*)workspace, plan, stream, 0};
+  rc = reset_stream_k(c);
+  if (rc) return rc;
   DSF_HIP(launch_rope_table(at<float>(c, plan.rope), T, desc->rotary_dims, desc->rope_theta, stream));
   const size_t xbytes = elem_bytes(dtype) * size_t(B) * T * desc->d_model;
   for (int l = 0; l < L; ++l) {

@@ -10,13 +10,19 @@
 namespace dsf {
 
 // ---- per-launch timing (api.hip) ----
-void timing_begin(int kind, hipStream_t s);
+// A scope brackets one launch with a start and a stop event. A deferred
+// scope records neither itself: the launcher inside it takes the events with
+// timing_claim and hands them to hipExtLaunchKernelGGL, which timestamps the
+// kernel's own dispatch (no launch overhead inside the interval); if no
+// launcher claims them the record is dropped.
+void timing_begin(int kind, hipStream_t s, bool deferred);
+bool timing_claim(hipEvent_t* start, hipEvent_t* stop);
 void timing_end(int kind, hipStream_t s);
 
 struct TimedScope {
   int kind;
   hipStream_t s;
-  TimedScope(int k, hipStream_t st) : kind(k), s(st) { timing_begin(kind, s); }
+  TimedScope(int k, hipStream_t st, bool deferred = false) : kind(k), s(st) { timing_begin(kind, s, deferred); }
   ~TimedScope() { timing_end(kind, s); }
 };
 
@@ -34,6 +40,8 @@ hipError_t launch_gather(int dtype, const void* x, int B, int T, int d, const in
 hipError_t launch_scatter(int dtype, void* x, const void* delta, int B, int T, int d,
                           const int32_t* idx, int k, hipStream_t s);
 hipError_t launch_copy(const void* src, void* dst, size_t bytes, hipStream_t s);
+// dst[0 .. n) = 0 with a kernel (no memset node, so the call can be captured)
+hipError_t launch_zero_u32(uint32_t* dst, int64_t n, hipStream_t s);
 
 // Row normalisation of gathered rows. Output row r = b * kk + j reads source
 // row src[b * src_rows + (idx ? idx[r] : j)] (src_rows = T for hidden states)
@@ -83,10 +91,17 @@ struct GemmArgs {
   void* x; const void* res;
   // EPI_SWIGLU: f (gate rows [0, f), up rows [f, 2f))
   int f;
-  // set by the launcher: number of M tiles of the grid
-  int ntm;
+  // Stream-K workspace (nullable: then every launch is one tile per workgroup):
+  // part holds gemm_partial_bytes(), flags gemm_flag_count() words that were
+  // zeroed before the first launch using them; epoch is nonzero and distinct
+  // for every launch between two zeroings.
+  float* part; uint32_t* flags; uint32_t epoch;
+  // set by the launcher: number of M tiles; workgroups per XCD of a stream-K grid
+  int ntm; int px;
 };
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t s);
+size_t gemm_partial_bytes();
+int gemm_flag_count();
 
 // ---- attention over kept tokens (kernels_attn.hip) ----
 // q [B, Hq, n, hd], k/v [B, Hkv, n, hd] -> out [B, n, Hq*hd], causal over the n tokens.

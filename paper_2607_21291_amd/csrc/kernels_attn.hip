@@ -15,6 +15,8 @@
 //
 // Kept positions ascend, so causal order over compacted indices is causal
 // order over original positions.
+#include <hip/hip_ext.h>
+
 #include "dsf_device.h"
 #include "dsf_internal.h"
 
@@ -300,17 +302,26 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ 
   for (int d = 0; d < HD; ++d) orow[d] = o[d] / l;
 }
 
+// Launch kern<<<grid, block>>>(args...), through hipExtLaunchKernelGGL when
+// the enclosing timing scope hands over its events.
+template <typename K, typename... A>
+static void launch_timed(K kern, dim3 grid, dim3 block, hipStream_t s, A... args) {
+  hipEvent_t e0, e1;
+  if (timing_claim(&e0, &e1)) hipExtLaunchKernelGGL(kern, grid, block, 0, s, e0, e1, 0, args...);
+  else kern<<<grid, block, 0, s>>>(args...);
+}
+
 hipError_t launch_attention(int dtype, const void* q, const void* k, const void* v, int B, int Hq, int Hkv,
                             int n, int hd, void* out, hipStream_t s) {
   if (n == 0 || B == 0) return hipSuccess;
-  TimedScope ts(DSF_KIND_ATTN, s);
+  TimedScope ts(DSF_KIND_ATTN, s, true);
   if (dtype == DSF_F32) {
     dim3 grid((n + 63) / 64, Hq, B);
     auto Qp = (const float*)q; auto Kp = (const float*)k; auto Vp = (const float*)v; auto O = (float*)out;
     switch (hd) {
-      case 32: attn_f32_kernel<32><<<grid, 64, 0, s>>>(Qp, Kp, Vp, Hq, Hkv, n, O); break;
-      case 64: attn_f32_kernel<64><<<grid, 64, 0, s>>>(Qp, Kp, Vp, Hq, Hkv, n, O); break;
-      case 128: attn_f32_kernel<128><<<grid, 64, 0, s>>>(Qp, Kp, Vp, Hq, Hkv, n, O); break;
+      case 32: launch_timed(attn_f32_kernel<32>, grid, dim3(64), s, Qp, Kp, Vp, Hq, Hkv, n, O); break;
+      case 64: launch_timed(attn_f32_kernel<64>, grid, dim3(64), s, Qp, Kp, Vp, Hq, Hkv, n, O); break;
+      case 128: launch_timed(attn_f32_kernel<128>, grid, dim3(64), s, Qp, Kp, Vp, Hq, Hkv, n, O); break;
       default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -322,9 +333,9 @@ hipError_t launch_attention(int dtype, const void* q, const void* k, const void*
   dim3 grid(((n + 64 * NQ - 1) / (64 * NQ)) * Hq * B);
   auto Qp = (const uint16_t*)q; auto Kp = (const uint16_t*)k; auto Vp = (const uint16_t*)v; auto O = (uint16_t*)out;
   switch (hd) {
-    case 32: attn_bf16_kernel<32, NQ><<<grid, 256, 0, s>>>(Qp, Kp, Vp, Hq, Hkv, n, O); break;
-    case 64: attn_bf16_kernel<64, NQ><<<grid, 256, 0, s>>>(Qp, Kp, Vp, Hq, Hkv, n, O); break;
-    case 128: attn_bf16_kernel<128, NQ><<<grid, 256, 0, s>>>(Qp, Kp, Vp, Hq, Hkv, n, O); break;
+    case 32: launch_timed(attn_bf16_kernel<32, NQ>, grid, dim3(256), s, Qp, Kp, Vp, Hq, Hkv, n, O); break;
+    case 64: launch_timed(attn_bf16_kernel<64, NQ>, grid, dim3(256), s, Qp, Kp, Vp, Hq, Hkv, n, O); break;
+    case 128: launch_timed(attn_bf16_kernel<128, NQ>, grid, dim3(256), s, Qp, Kp, Vp, Hq, Hkv, n, O); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

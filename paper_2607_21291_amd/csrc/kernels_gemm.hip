@@ -13,6 +13,14 @@
 //
 // fp32 path: a plain LDS-tiled FMA kernel (32 x 128 tiles) that shares the
 // epilogue. It exists for the fp32 workload and is not tuned.
+#include <algorithm>
+#include <atomic>
+#include <cstdlib>
+#include <cstring>
+#include <type_traits>
+
+#include <hip/hip_ext.h>
+
 #include "dsf_device.h"
 #include "dsf_internal.h"
 
@@ -344,163 +352,363 @@ __device__ __forceinline__ void wait_vmcnt() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
+// Workgroup barrier of the DMA ring. __syncthreads() would also wait for every
+// outstanding global access (vmcnt(0)), draining the tiles still in flight and
+// reducing any ring to double buffering; here each wave has already waited for
+// its own share of the tile it needs. The memory clobber keeps the compiler's
+// LDS reads of the new tile below the barrier.
+__device__ __forceinline__ void ring_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
 // 16 bytes per lane from global memory into LDS at lds + 16 * lane (lds is
 // wave-uniform). Kept out of lambdas: the builtin exists only for the device.
 __device__ __forceinline__ void dma16(const void* gptr, char* lds) {
   __builtin_amdgcn_global_load_lds(gptr, (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
 }
 
+// Device-side pieces of the LDS-DMA GEMM: the main loop over a range of
+// k-tiles of one output tile, and the fused epilogue of a finished tile.
 template <int EPI, int BM, int BN, int WM, int WN, int NS, int BK>
-__global__ __launch_bounds__((DmaCfg<BM, BN, WM, WN, NS, BK>::kThreads)) void gemm_bf16_dma_kernel(GemmArgs g) {
+struct DmaGemm {
   using C = DmaCfg<BM, BN, WM, WN, NS, BK>;
-  constexpr int MI = WM / 16, NI = WN / 16;
-  constexpr int CPR = BK / 8;                 // chunks per tile row
-  constexpr int RPL = C::kRowsPerLoad;
-  __shared__ __attribute__((aligned(1024))) char smem[C::kSmem];
+  static constexpr int MI = WM / 16, NI = WN / 16;
+  static constexpr int CPR = BK / 8;  // chunks per tile row
+  static constexpr int RPL = C::kRowsPerLoad;
+  typedef f32x4 Acc[MI][NI];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / (BN / WN), wn = wave % (BN / WN);
-  const int r16 = lane & 15, grp = lane >> 4;
-  // tiles in row-major (M-tile, N-tile) order, one contiguous range per XCD:
-  // an XCD streams its own rows of A once and keeps them in its L2
-  const int ntn = int(gridDim.x) / g.ntm;
-  const int item = xcd_remap(int(blockIdx.x), int(gridDim.x));
-  const int tm = item / ntn, tn = item - tm * ntn;
-  const int m0 = tm * BM;
-
-  // DMA source pointers. Load i of this wave fills tile rows RPL (wave + kWaves i) .. +RPL;
-  // lane -> row lane / CPR, physical chunk lane % CPR holding logical chunk swz^-1.
-  const int lr = lane / CPR;
-  const int lc = swz<BK>(lr, lane % CPR);     // swz is an involution for a fixed row
-  const uint16_t* pa[C::kLoadsA];
-  const uint16_t* pa2[C::kLoadsA];
-  const uint16_t* pb[C::kLoadsB];
-  const uint16_t* pb2[C::kLoadsB];
+  // acc = A[rows of tile tm, k-tiles kb..ke-1] . B[rows of tile tn, same]^T.
+  // Starts with a barrier, so the ring may still hold the previous tile.
+  __device__ static __forceinline__ void mainloop(const GemmArgs& g, char* smem, int tm, int tn, int kb, int ke,
+                                                  Acc& acc) {
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave / (BN / WN), wn = wave % (BN / WN);
+    const int r16 = lane & 15, grp = lane >> 4;
+    const int m0 = tm * BM;
+    // DMA source pointers. Load i of this wave fills tile rows RPL (wave + kWaves i) .. +RPL;
+    // lane -> row lane / CPR, physical chunk lane % CPR holding logical chunk swz^-1.
+    const int lr = lane / CPR;
+    const int lc = swz<BK>(lr, lane % CPR);  // swz is an involution for a fixed row
+    const uint16_t* pa[C::kLoadsA];
+    const uint16_t* pa2[C::kLoadsA];
+    const uint16_t* pb[C::kLoadsB];
+    const uint16_t* pb2[C::kLoadsB];
 #pragma unroll
-  for (int i = 0; i < C::kLoadsA; ++i) {
-    int m = m0 + RPL * (wave + C::kWaves * i) + lr;
-    if (m > g.M - 1) m = g.M - 1;
-    pa[i] = (const uint16_t*)g.a + int64_t(m) * g.lda + lc * 8;
-    pa2[i] = g.a2 ? (const uint16_t*)g.a2 + int64_t(m) * g.lda2 + lc * 8 : nullptr;
+    for (int i = 0; i < C::kLoadsA; ++i) {
+      int m = m0 + RPL * (wave + C::kWaves * i) + lr;
+      if (m > g.M - 1) m = g.M - 1;
+      pa[i] = (const uint16_t*)g.a + int64_t(m) * g.lda + lc * 8;
+      pa2[i] = g.a2 ? (const uint16_t*)g.a2 + int64_t(m) * g.lda2 + lc * 8 : nullptr;
+    }
+#pragma unroll
+    for (int i = 0; i < C::kLoadsB; ++i) {
+      const int r = RPL * (wave + C::kWaves * i) + lr;
+      int n;
+      if constexpr (EPI == EPI_SWIGLU) {
+        // each 128-row block of the B tile holds 64 gate units then the same 64 up units
+        const int blk = r / 128, rr = r % 128, u0 = (tn * (BN / 128) + blk) * 64;
+        n = rr < 64 ? u0 + rr : g.f + u0 + (rr - 64);
+      } else {
+        n = min(tn * BN + r, g.N - 1);
+      }
+      pb[i] = (const uint16_t*)g.b + int64_t(n) * g.ldb + lc * 8;
+      pb2[i] = g.b2 ? (const uint16_t*)g.b2 + int64_t(n) * g.ldb2 + lc * 8 : nullptr;
+    }
+    auto issue = [&](int kt) {
+      const int k0 = kt * BK;
+      const bool second = k0 >= g.K1;
+      const int kc = second ? k0 - g.K1 : k0;
+      char* st = smem + (kt % NS) * C::kStage;
+#pragma unroll
+      for (int i = 0; i < C::kLoadsA; ++i) dma16((second ? pa2[i] : pa[i]) + kc, st + 1024 * (wave + C::kWaves * i));
+#pragma unroll
+      for (int i = 0; i < C::kLoadsB; ++i)
+        dma16((second ? pb2[i] : pb[i]) + kc, st + BM * C::kRowBytes + 1024 * (wave + C::kWaves * i));
+    };
+
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+      for (int j = 0; j < NI; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    // Everything this wave issued before (stores of an earlier tile) has
+    // completed, so the counts below cover only the ring's loads; and every
+    // wave is done with the LDS before the ring is refilled.
+    wait_vmcnt<0>();
+    ring_barrier();
+#pragma unroll
+    for (int s = 0; s < NS - 1; ++s)
+      if (kb + s < ke) issue(kb + s);
+    for (int kt = kb; kt < ke; ++kt) {
+      // tile kt has landed once at most (tiles issued after it) * kLoads loads remain
+      if (kt + NS - 2 < ke) wait_vmcnt<(NS - 2) * C::kLoads>();
+      else wait_vmcnt<0>();
+      ring_barrier();  // every wave's part of tile kt is visible; tile kt-1's buffer is free
+      // tile kt + NS - 1 goes into tile kt-1's buffer; all its loads leave before
+      // the compute so that they get the whole tile's MFMA time to land
+      if (kt + NS - 1 < ke) issue(kt + NS - 1);
+      const uint16_t* At = reinterpret_cast<const uint16_t*>(smem + (kt % NS) * C::kStage);
+      const uint16_t* Bt = At + BM * BK;
+      // Software pipeline over (substep ks, A fragment i): the read of the next A
+      // fragment is issued before the NI MFMAs of the current one, and the next
+      // substep's B fragments are read halfway through the current substep, so
+      // every LDS wait finds its data already there and the MFMA pipe (whose
+      // issue is blocking) does not idle behind a late read.
+      constexpr int KS = BK / 32;
+      bf16x8 bq[2][NI];
+      auto read_b = [&](int ks, int buf) {
+        const int ch = ks * 4 + grp;
+#pragma unroll
+        for (int j = 0; j < NI; ++j) {
+          const int br = wn * WN + j * 16 + r16;
+          bq[buf][j] = *reinterpret_cast<const bf16x8*>(Bt + br * BK + (swz<BK>(br, ch) << 3));
+        }
+      };
+      auto read_a = [&](int ks, int i) -> bf16x8 {
+        const int ar = wm * WM + i * 16 + r16;
+        return *reinterpret_cast<const bf16x8*>(At + ar * BK + (swz<BK>(ar, ks * 4 + grp) << 3));
+      };
+      read_b(0, 0);
+      bf16x8 a_cur = read_a(0, 0);
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+#pragma unroll
+        for (int i = 0; i < MI; ++i) {
+          // the LDS wait before this group's first MFMA covers only reads issued
+          // one group earlier; this group's reads go out right after it
+          acc[i][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_cur, bq[ks & 1][0], acc[i][0], 0, 0, 0);
+          DSF_SCHED_FENCE();
+          bf16x8 a_nxt = a_cur;
+          if (i + 1 < MI) a_nxt = read_a(ks, i + 1);
+          else if (ks + 1 < KS) a_nxt = read_a(ks + 1, 0);
+          if (i == MI / 2 && ks + 1 < KS) read_b(ks + 1, (ks + 1) & 1);
+          DSF_SCHED_FENCE();
+#pragma unroll
+          for (int j = 1; j < NI; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_cur, bq[ks & 1][j], acc[i][j], 0, 0, 0);
+          DSF_SCHED_FENCE();
+          a_cur = a_nxt;
+        }
+      }
+    }
   }
+
+  // Stage the finished tile (tm, tn) through LDS and apply the fused epilogue.
+  __device__ static __forceinline__ void epilogue(const GemmArgs& g, char* smem, int tm, int tn, Acc& acc) {
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave / (BN / WN), wn = wave % (BN / WN);
+    const int r16 = lane & 15, grp = lane >> 4;
+    const int m0 = tm * BM;
+    __syncthreads();  // all waves are done reading the ring before it becomes the epilogue tile
+    if constexpr (C::kWaveEpi) {
+      // each wave stages and finishes its own tile, 32 rows at a time, as a
+      // 32 x 128 virtual tile whose column index is 2 tn + wn (BN = 256) or tn
+      float* stage = reinterpret_cast<float*>(smem) + wave * 32 * C::kStageLD;
+      const int vtn = tn * (BN / 128) + wn;
 #pragma unroll
-  for (int i = 0; i < C::kLoadsB; ++i) {
-    const int r = RPL * (wave + C::kWaves * i) + lr;
-    int n;
-    if constexpr (EPI == EPI_SWIGLU) {
-      // each 128-row block of the B tile holds 64 gate units then the same 64 up units
-      const int blk = r / 128, rr = r % 128, u0 = (tn * (BN / 128) + blk) * 64;
-      n = rr < 64 ? u0 + rr : g.f + u0 + (rr - 64);
+      for (int rnd = 0; rnd < MI / 2; ++rnd) {
+#pragma unroll
+        for (int ii = 0; ii < 2; ++ii)
+#pragma unroll
+          for (int j = 0; j < NI; ++j)
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              stage[(16 * ii + 4 * grp + e) * C::kStageLD + 16 * j + r16] = acc[2 * rnd + ii][j][e];
+        __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS writes are done
+        __builtin_amdgcn_wave_barrier();
+        gemm_epilogue<uint16_t, 32, 128, 64, EPI>(g, stage, m0 + wm * WM + 32 * rnd, vtn, lane);
+        __builtin_amdgcn_s_waitcnt(0xc07f);
+        __builtin_amdgcn_wave_barrier();
+      }
     } else {
-      n = min(tn * BN + r, g.N - 1);
-    }
-    pb[i] = (const uint16_t*)g.b + int64_t(n) * g.ldb + lc * 8;
-    pb2[i] = g.b2 ? (const uint16_t*)g.b2 + int64_t(n) * g.ldb2 + lc * 8 : nullptr;
-  }
-  auto issue = [&](int kt) {
-    const int k0 = kt * BK;
-    const bool second = k0 >= g.K1;
-    const int kc = second ? k0 - g.K1 : k0;
-    char* st = smem + (kt % NS) * C::kStage;
+      float* stage = reinterpret_cast<float*>(smem);
 #pragma unroll
-    for (int i = 0; i < C::kLoadsA; ++i) dma16((second ? pa2[i] : pa[i]) + kc, st + 1024 * (wave + C::kWaves * i));
-#pragma unroll
-    for (int i = 0; i < C::kLoadsB; ++i)
-      dma16((second ? pb2[i] : pb[i]) + kc, st + BM * C::kRowBytes + 1024 * (wave + C::kWaves * i));
-  };
-
-  f32x4 acc[MI][NI];
-#pragma unroll
-  for (int i = 0; i < MI; ++i)
-#pragma unroll
-    for (int j = 0; j < NI; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  const int nk = g.K / BK;
-#pragma unroll
-  for (int s = 0; s < NS - 1; ++s)
-    if (s < nk) issue(s);
-  for (int kt = 0; kt < nk; ++kt) {
-    // tile kt has landed once at most (tiles issued after it) * kLoads loads remain
-    if (kt + NS - 2 < nk) wait_vmcnt<(NS - 2) * C::kLoads>();
-    else wait_vmcnt<0>();
-    __syncthreads();  // every wave's part of tile kt is visible; tile kt-1's buffer is free
-    if (kt + NS - 1 < nk) issue(kt + NS - 1);
-    const uint16_t* At = reinterpret_cast<const uint16_t*>(smem + (kt % NS) * C::kStage);
-    const uint16_t* Bt = At + BM * BK;
-    // Software pipeline over (substep ks, A fragment i): the read of the next A
-    // fragment is issued before the NI MFMAs of the current one, and the next
-    // substep's B fragments are read halfway through the current substep, so
-    // every LDS wait finds its data already there and the MFMA pipe (whose
-    // issue is blocking) does not idle behind a late read.
-    constexpr int KS = BK / 32;
-    bf16x8 bq[2][NI];
-    auto read_b = [&](int ks, int buf) {
-      const int ch = ks * 4 + grp;
-#pragma unroll
-      for (int j = 0; j < NI; ++j) {
-        const int br = wn * WN + j * 16 + r16;
-        bq[buf][j] = *reinterpret_cast<const bf16x8*>(Bt + br * BK + (swz<BK>(br, ch) << 3));
-      }
-    };
-    auto read_a = [&](int ks, int i) -> bf16x8 {
-      const int ar = wm * WM + i * 16 + r16;
-      return *reinterpret_cast<const bf16x8*>(At + ar * BK + (swz<BK>(ar, ks * 4 + grp) << 3));
-    };
-    read_b(0, 0);
-    bf16x8 a_cur = read_a(0, 0);
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-#pragma unroll
-      for (int i = 0; i < MI; ++i) {
-        // the LDS wait before this group's first MFMA covers only reads issued
-        // one group earlier; this group's reads go out right after it
-        acc[i][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_cur, bq[ks & 1][0], acc[i][0], 0, 0, 0);
-        DSF_SCHED_FENCE();
-        bf16x8 a_nxt = a_cur;
-        if (i + 1 < MI) a_nxt = read_a(ks, i + 1);
-        else if (ks + 1 < KS) a_nxt = read_a(ks + 1, 0);
-        if (i == MI / 2 && ks + 1 < KS) read_b(ks + 1, (ks + 1) & 1);
-        DSF_SCHED_FENCE();
-#pragma unroll
-        for (int j = 1; j < NI; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_cur, bq[ks & 1][j], acc[i][j], 0, 0, 0);
-        DSF_SCHED_FENCE();
-        a_cur = a_nxt;
-      }
-    }
-  }
-  __syncthreads();  // all waves are done reading the ring before it becomes the epilogue tile
-  if constexpr (C::kWaveEpi) {
-    // each wave stages and finishes its own tile, 32 rows at a time, as a
-    // 32 x 128 virtual tile whose column index is 2 tn + wn (BN = 256) or tn
-    float* stage = reinterpret_cast<float*>(smem) + wave * 32 * C::kStageLD;
-    const int vtn = tn * (BN / 128) + wn;
-#pragma unroll
-    for (int rnd = 0; rnd < MI / 2; ++rnd) {
-#pragma unroll
-      for (int ii = 0; ii < 2; ++ii)
+      for (int i = 0; i < MI; ++i)
 #pragma unroll
         for (int j = 0; j < NI; ++j)
 #pragma unroll
           for (int e = 0; e < 4; ++e)
-            stage[(16 * ii + 4 * grp + e) * C::kStageLD + 16 * j + r16] = acc[2 * rnd + ii][j][e];
-      __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS writes are done
-      __builtin_amdgcn_wave_barrier();
-      gemm_epilogue<uint16_t, 32, 128, 64, EPI>(g, stage, m0 + wm * WM + 32 * rnd, vtn, lane);
-      __builtin_amdgcn_s_waitcnt(0xc07f);
-      __builtin_amdgcn_wave_barrier();
+            stage[(wm * WM + 16 * i + 4 * grp + e) * C::kStageLD + wn * WN + 16 * j + r16] = acc[i][j][e];
+      __syncthreads();
+      gemm_epilogue<uint16_t, BM, BN, C::kThreads, EPI>(g, stage, m0, tn, threadIdx.x);
     }
-  } else {
-    float* stage = reinterpret_cast<float*>(smem);
+  }
+
+  // Partial tiles of the stream-K schedule live in slot-major order, each in
+  // the accumulators' own register layout: (slot, wave, i, j, lane) -> f32x4.
+  __device__ static __forceinline__ f32x4* slot_ptr(const GemmArgs& g, int slot) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    return reinterpret_cast<f32x4*>(g.part) + (int64_t(slot) * C::kWaves + wave) * (MI * NI * 64) + lane;
+  }
+
+  // The partial sums go from one workgroup to another, possibly on another
+  // XCD (each XCD has its own L2). They are stored and loaded with
+  // device-scope coherent accesses (sc1), which is what the relaxed
+  // device-scope atomics on the flags use as well, so the hand-over needs only
+  // a completion wait: no write-back of the writer's whole L2 before the flag,
+  // no invalidation of the reader's L2 after it (both would cost every other
+  // workgroup on those XCDs its cached tiles).
+  // Fragment f = i * NI + j of a wave's partial sits at slot_ptr + 64 f. The
+  // accesses go 16 fragments per statement (4 address registers, immediate
+  // offsets of 1, 2, 3 KiB), and each statement waits for its own accesses, so
+  // no register it names is touched while its memory operation is in flight.
+  static_assert((MI * NI) % 16 == 0, "partials move in groups of 16 fragments");
+
+  __device__ static __forceinline__ void store_partial(const GemmArgs& g, const Acc& acc) {
+    const f32x4* a = &acc[0][0];
+    f32x4* p = slot_ptr(g, int(blockIdx.x));
 #pragma unroll
-    for (int i = 0; i < MI; ++i)
+    for (int c = 0; c < MI * NI; c += 16) {
+      const f32x4* v = a + c;
+      asm volatile(
+          "global_store_dwordx4 %0, %4, off sc1\n\t"
+          "global_store_dwordx4 %0, %5, off offset:1024 sc1\n\t"
+          "global_store_dwordx4 %0, %6, off offset:2048 sc1\n\t"
+          "global_store_dwordx4 %0, %7, off offset:3072 sc1\n\t"
+          "global_store_dwordx4 %1, %8, off sc1\n\t"
+          "global_store_dwordx4 %1, %9, off offset:1024 sc1\n\t"
+          "global_store_dwordx4 %1, %10, off offset:2048 sc1\n\t"
+          "global_store_dwordx4 %1, %11, off offset:3072 sc1\n\t"
+          "global_store_dwordx4 %2, %12, off sc1\n\t"
+          "global_store_dwordx4 %2, %13, off offset:1024 sc1\n\t"
+          "global_store_dwordx4 %2, %14, off offset:2048 sc1\n\t"
+          "global_store_dwordx4 %2, %15, off offset:3072 sc1\n\t"
+          "global_store_dwordx4 %3, %16, off sc1\n\t"
+          "global_store_dwordx4 %3, %17, off offset:1024 sc1\n\t"
+          "global_store_dwordx4 %3, %18, off offset:2048 sc1\n\t"
+          "global_store_dwordx4 %3, %19, off offset:3072 sc1\n\t"
+          "s_waitcnt vmcnt(0)"
+          :
+          : "v"(p + (c + 0) * 64), "v"(p + (c + 4) * 64), "v"(p + (c + 8) * 64), "v"(p + (c + 12) * 64),
+            "v"(v[0]), "v"(v[1]), "v"(v[2]), "v"(v[3]), "v"(v[4]), "v"(v[5]), "v"(v[6]), "v"(v[7]),
+            "v"(v[8]), "v"(v[9]), "v"(v[10]), "v"(v[11]), "v"(v[12]), "v"(v[13]), "v"(v[14]), "v"(v[15])
+          : "memory");
+    }
+  }
+
+  // acc += the partial in slot (published before this call)
+  __device__ static __forceinline__ void add_partial(const GemmArgs& g, int slot, Acc& acc) {
+    f32x4* a = &acc[0][0];
+    const f32x4* p = slot_ptr(g, slot);
 #pragma unroll
-      for (int j = 0; j < NI; ++j)
+    for (int c = 0; c < MI * NI; c += 16) {
+      f32x4 v[16];
+      asm volatile(
+          "global_load_dwordx4 %0, %16, off sc1\n\t"
+          "global_load_dwordx4 %1, %16, off offset:1024 sc1\n\t"
+          "global_load_dwordx4 %2, %16, off offset:2048 sc1\n\t"
+          "global_load_dwordx4 %3, %16, off offset:3072 sc1\n\t"
+          "global_load_dwordx4 %4, %17, off sc1\n\t"
+          "global_load_dwordx4 %5, %17, off offset:1024 sc1\n\t"
+          "global_load_dwordx4 %6, %17, off offset:2048 sc1\n\t"
+          "global_load_dwordx4 %7, %17, off offset:3072 sc1\n\t"
+          "global_load_dwordx4 %8, %18, off sc1\n\t"
+          "global_load_dwordx4 %9, %18, off offset:1024 sc1\n\t"
+          "global_load_dwordx4 %10, %18, off offset:2048 sc1\n\t"
+          "global_load_dwordx4 %11, %18, off offset:3072 sc1\n\t"
+          "global_load_dwordx4 %12, %19, off sc1\n\t"
+          "global_load_dwordx4 %13, %19, off offset:1024 sc1\n\t"
+          "global_load_dwordx4 %14, %19, off offset:2048 sc1\n\t"
+          "global_load_dwordx4 %15, %19, off offset:3072 sc1\n\t"
+          "s_waitcnt vmcnt(0)"
+          : "=&v"(v[0]), "=&v"(v[1]), "=&v"(v[2]), "=&v"(v[3]), "=&v"(v[4]), "=&v"(v[5]), "=&v"(v[6]),
+            "=&v"(v[7]), "=&v"(v[8]), "=&v"(v[9]), "=&v"(v[10]), "=&v"(v[11]), "=&v"(v[12]), "=&v"(v[13]),
+            "=&v"(v[14]), "=&v"(v[15])
+          : "v"(p + (c + 0) * 64), "v"(p + (c + 4) * 64), "v"(p + (c + 8) * 64), "v"(p + (c + 12) * 64)
+          : "memory");
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
-          stage[(wm * WM + 16 * i + 4 * grp + e) * C::kStageLD + wn * WN + 16 * j + r16] = acc[i][j][e];
-    __syncthreads();
-    gemm_epilogue<uint16_t, BM, BN, C::kThreads, EPI>(g, stage, m0, tn, threadIdx.x);
+      for (int f = 0; f < 16; ++f) a[c + f] = a[c + f] + v[f];
+    }
+  }
+};
+
+// One output tile per workgroup (grid = tiles), tiles in row-major (M-tile,
+// N-tile) order with one contiguous range per XCD: an XCD streams its own rows
+// of A once and keeps them in its L2.
+template <int EPI, int BM, int BN, int WM, int WN, int NS, int BK>
+__global__ __launch_bounds__((DmaCfg<BM, BN, WM, WN, NS, BK>::kThreads)) void gemm_bf16_dma_kernel(GemmArgs g) {
+  using G = DmaGemm<EPI, BM, BN, WM, WN, NS, BK>;
+  __shared__ __attribute__((aligned(1024))) char smem[G::C::kSmem];
+  const int ntn = int(gridDim.x) / g.ntm;
+  const int item = xcd_remap(int(blockIdx.x), int(gridDim.x));
+  const int tm = item / ntn, tn = item - tm * ntn;
+  typename G::Acc acc;
+  G::mainloop(g, smem, tm, tn, 0, g.K / BK, acc);
+  G::epilogue(g, smem, tm, tn, acc);
+}
+
+// Stream-K schedule (persistent grid of 8 * px workgroups; workgroup w runs
+// on XCD w % 8 as the hardware deals workgroups to the 8 XCDs in turn).
+// The tiles, in row-major order, are cut into 8 contiguous ranges, one per
+// XCD; each XCD's px workgroups then share its range as an independent
+// problem: whole tiles while at least two full rounds remain, then the
+// remaining k-iterations (tiles x K/BK) in px equal contiguous pieces.
+// A piece that covers only part of a tile leaves a partial sum: the
+// workgroup holding the tile's last k-iteration finishes it, adding the
+// partials of the lower-numbered workgroups that hold its earlier iterations
+// (a fixed order, so results do not depend on timing). Each workgroup walks
+// its piece from the end backwards, so the one partial it can leave (at the
+// top of its piece) is written first, and it waits only for lower-numbered
+// workgroups of its own XCD, which are dispatched before it and never wait
+// before writing their partial: the waits always end. A bounded spin keeps
+// even a broken dispatch order from hanging the device.
+template <int EPI, int BM, int BN, int WM, int WN, int NS, int BK>
+__global__ __launch_bounds__((DmaCfg<BM, BN, WM, WN, NS, BK>::kThreads)) void gemm_bf16_sk_kernel(GemmArgs g) {
+  using G = DmaGemm<EPI, BM, BN, WM, WN, NS, BK>;
+  __shared__ __attribute__((aligned(1024))) char smem[G::C::kSmem];
+  __shared__ int spin_failed;
+  const int ntn = EPI == EPI_SWIGLU ? g.f / (BN / 2) : (g.N + BN - 1) / BN;
+  const int nt = g.ntm * ntn, nk = g.K / BK, px = g.px;
+  const int x = int(blockIdx.x) % kXcds, j = int(blockIdx.x) / kXcds;
+  const int t0 = int(int64_t(nt) * x / kXcds), ntx = int(int64_t(nt) * (x + 1) / kXcds) - t0;
+  const int full = ntx / px, rem = ntx % px;
+  const int dp = rem == 0 ? ntx : (full >= 1 ? (full - 1) * px : 0);
+  typename G::Acc acc;
+  for (int t = j; t < dp; t += px) {
+    const int tile = t0 + t, tm = tile / ntn, tn = tile - tm * ntn;
+    G::mainloop(g, smem, tm, tn, 0, nk, acc);
+    G::epilogue(g, smem, tm, tn, acc);
+  }
+  const int64_t usk = int64_t(ntx - dp) * nk;
+  auto piece = [&](int w) { return usk * w / px; };  // first k-iteration of workgroup w's piece
+  const int64_t a = piece(j);
+  int64_t u = piece(j + 1);
+  while (u > a) {
+    const int st = int((u - 1) / nk);
+    const int64_t tb = int64_t(st) * nk;
+    const int kb = int((a > tb ? a : tb) - tb), ke = int(u - tb);
+    const int tile = t0 + dp + st, tm = tile / ntn, tn = tile - tm * ntn;
+    G::mainloop(g, smem, tm, tn, kb, ke, acc);
+    if (ke < nk) {
+      // top of the piece, short of the tile's end: publish the partial sum
+      G::store_partial(g, acc);
+      __syncthreads();  // every wave's partial stores have completed
+      if (threadIdx.x == 0) __hip_atomic_store(g.flags + blockIdx.x, g.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    } else {
+      // this workgroup holds the tile's last iteration: add the earlier pieces
+      for (int w = j - 1; kb > 0 && w >= 0; --w) {
+        const int64_t pw = piece(w), pe = piece(w + 1);
+        if (pe <= tb) break;     // w's piece ends before this tile, and so do all below it
+        if (pw == pe) continue;  // empty piece: no partial
+        const int slot = w * kXcds + x;
+        if (threadIdx.x == 0) {
+          int ok = 0;
+          for (int it = 0; it < (1 << 22); ++it) {
+            if (__hip_atomic_load(g.flags + slot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == g.epoch) {
+              ok = 1;
+              break;
+            }
+            __builtin_amdgcn_s_sleep(2);
+          }
+          spin_failed = !ok;
+        }
+        __syncthreads();  // the partial's loads below are issued after its flag was seen
+        if (spin_failed) break;  // left unfinished rather than hang
+        G::add_partial(g, slot, acc);
+      }
+      G::epilogue(g, smem, tm, tn, acc);
+    }
+    u = tb + kb;
   }
 }
 
@@ -596,24 +804,102 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g) {
 #define DSF_GEMM_BK 64
 #endif
 
+// Stream-K partial tiles: one slot per workgroup of a persistent grid, at
+// most kSkMaxSlots workgroups (2 per CU on a 256-CU device).
+constexpr int kSkMaxSlots = 512;
+constexpr int kSkMinIters = 8;  // mean k-iterations per workgroup below which one tile per workgroup is kept
+constexpr int kSkMinK = 32;     // k-iterations per tile below which the partial sums cost more than they save
+
+size_t gemm_partial_bytes() { return size_t(kSkMaxSlots) * DSF_GEMM_BM * DSF_GEMM_BN * sizeof(float); }
+int gemm_flag_count() { return kSkMaxSlots; }
+
+// DSF_GEMM_SCHEDULE=classic|streamk overrides the automatic choice (tests and
+// tuning); read at every launch so that a process can switch between calls.
+static int schedule_override() {
+  const char* e = getenv("DSF_GEMM_SCHEDULE");
+  if (!e) return 0;
+  if (!strcmp(e, "classic")) return 1;
+  if (!strcmp(e, "streamk")) return 2;
+  return 0;
+}
+
+// Resident workgroups of kernel fn on the current device, capped at
+// kSkMaxSlots (one cache per instantiation: each kernel has its own count).
+template <typename Tag>
+static int resident_slots(const void* fn, int threads) {
+  static std::atomic<int> cache[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  int v = cache[dev].load(std::memory_order_relaxed);
+  if (v) return v;
+  int per_cu = 0, cus = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, threads, 0) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    return 0;
+  v = std::min(per_cu * cus, kSkMaxSlots);
+  cache[dev].store(v, std::memory_order_relaxed);
+  return v;
+}
+
+// Workgroups per XCD of a stream-K grid for nt tiles of nk k-iterations, or 0
+// for one tile per workgroup. Stream-K is taken when one tile per workgroup
+// would end in a short last round (at most a quarter of the resident slots
+// busy after at least one full round): then most CUs idle while it runs,
+// whereas a partial first round (fewer tiles than slots) already runs its
+// lone workgroups faster and does not gain from splitting. It is also left
+// out when the pieces would be too short to pay for their partial sums, and
+// for short reductions (fewer than kSkMinK k-iterations per tile), where the
+// extra pipeline starts and the partial hand-over cost more than the idle
+// CUs of the last round (measured on the 768-deep projections of a
+// 768-wide model).
+static int stream_k_px(int nt, int nk, int slots) {
+  const int px = slots / kXcds;
+  if (px < 1) return 0;
+  const int mode = schedule_override();
+  if (mode == 1) return 0;
+  if (mode == 2) return px;
+  const int64_t P = int64_t(px) * kXcds;
+  const int64_t last = nt % P;
+  if (nk < kSkMinK || nt <= P || last == 0 || 4 * last > P) return 0;
+  if (int64_t(nt) * nk < P * kSkMinIters) return 0;
+  return px;
+}
+
+// Launch kern<<<grid, block>>>(g), through hipExtLaunchKernelGGL when an
+// enclosing timing scope hands over its events.
+template <typename K>
+static void launch_timed(K kern, dim3 grid, dim3 block, hipStream_t s, const GemmArgs& g) {
+  hipEvent_t e0, e1;
+  if (timing_claim(&e0, &e1)) hipExtLaunchKernelGGL(kern, grid, block, 0, s, e0, e1, 0, g);
+  else kern<<<grid, block, 0, s>>>(g);
+}
+
 template <int EPI>
 static void launch_gemm_t(const GemmArgs& g, hipStream_t s) {
   if (DSF_GEMM_USE_DMA && g.dtype == DSF_BF16 && g.K % DSF_GEMM_BK == 0 && g.K1 % DSF_GEMM_BK == 0) {
-    constexpr int BM = DSF_GEMM_BM, BN = DSF_GEMM_BN;
-    using Cfg = DmaCfg<BM, BN, DSF_GEMM_WM, DSF_GEMM_WN, DSF_GEMM_NS, DSF_GEMM_BK>;
+    constexpr int BM = DSF_GEMM_BM, BN = DSF_GEMM_BN, WM = DSF_GEMM_WM, WN = DSF_GEMM_WN;
+    constexpr int NS = DSF_GEMM_NS, BK = DSF_GEMM_BK;
+    using Cfg = DmaCfg<BM, BN, WM, WN, NS, BK>;
     const int ntn = EPI == EPI_SWIGLU ? g.f / (BN / 2) : (g.N + BN - 1) / BN;
     GemmArgs ga = g;
     ga.ntm = (g.M + BM - 1) / BM;
-    dim3 grid(ntn * ga.ntm);
-    gemm_bf16_dma_kernel<EPI, BM, BN, DSF_GEMM_WM, DSF_GEMM_WN, DSF_GEMM_NS, DSF_GEMM_BK><<<grid, Cfg::kThreads, 0, s>>>(ga);
+    ga.px = 0;
+    if (g.part && g.flags) {
+      auto fn = gemm_bf16_sk_kernel<EPI, BM, BN, WM, WN, NS, BK>;
+      ga.px = stream_k_px(ntn * ga.ntm, g.K / BK,
+                          resident_slots<std::integral_constant<int, EPI>>((const void*)fn, Cfg::kThreads));
+      if (ga.px > 0) {
+        launch_timed(fn, dim3(ga.px * kXcds), dim3(Cfg::kThreads), s, ga);
+        return;
+      }
+    }
+    launch_timed(gemm_bf16_dma_kernel<EPI, BM, BN, WM, WN, NS, BK>, dim3(ntn * ga.ntm), dim3(Cfg::kThreads), s, ga);
   } else if (g.dtype == DSF_BF16) {
     const int ntn = EPI == EPI_SWIGLU ? g.f / (kBN / 2) : (g.N + kBN - 1) / kBN;
-    dim3 grid(ntn, (g.M + kBM - 1) / kBM);
-    gemm_bf16_kernel<EPI><<<grid, kThreads, 0, s>>>(g);
+    launch_timed(gemm_bf16_kernel<EPI>, dim3(ntn, (g.M + kBM - 1) / kBM), dim3(kThreads), s, g);
   } else {
     const int ntn = EPI == EPI_SWIGLU ? g.f / (kFBN / 2) : (g.N + kFBN - 1) / kFBN;
-    dim3 grid(ntn, (g.M + kFBM - 1) / kFBM);
-    gemm_f32_kernel<EPI><<<grid, 256, 0, s>>>(g);
+    launch_timed(gemm_f32_kernel<EPI>, dim3(ntn, (g.M + kFBM - 1) / kFBM), dim3(256), s, g);
   }
 }
 

@@ -453,6 +453,16 @@ hipError_t launch_copy(const void* src, void* dst, size_t bytes, hipStream_t s) 
   return hipGetLastError();
 }
 
+__global__ __launch_bounds__(256) void zero_u32_kernel(uint32_t* __restrict__ dst, int64_t n) {
+  for (int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x; i < n; i += int64_t(gridDim.x) * 256) dst[i] = 0u;
+}
+
+hipError_t launch_zero_u32(uint32_t* dst, int64_t n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  zero_u32_kernel<<<stream_grid(n), 256, 0, s>>>(dst, n);
+  return hipGetLastError();
+}
+
 // ------------------------------------------- gather + LayerNorm / RMSNorm
 
 // One wavefront per output row; the row stays in registers (MAXC vectors per

@@ -6,6 +6,7 @@ import torch
 
 import paper_2607_21291_amd as P
 import synthetic as S
+from oracle import adadsf_oracle as O
 
 U32 = 2.0 ** -24  # unit roundoff of fp32
 
@@ -62,3 +63,68 @@ def router_bound(x, W, dtype: str) -> np.ndarray:
     n = x.shape[-1] + w1.shape[0] + 4
     gamma = n * U32 / (1 - n * U32)
     return gamma * ((x @ w1.T + b1) @ w2 + abs(W.get("router_b2", 0.0))) + 1e-30
+
+
+# ---------------------------------------------------------------- layers
+
+TOL = {"f32": 1e-4, "bf16": 2e-2}
+
+# Small bf16 shapes that still span several GEMM tiles and ragged tails.
+SMALL = {
+    "neox_bf16_small": S.WORKLOADS["neox160m"].replace(
+        name="neox_bf16_small", n_layers=2, d_model=256, n_heads=4, n_kv_heads=4, head_dim=64, d_ff=1024,
+        rotary_dims=16, batch=2, seq=300),
+    "qwen_bf16_small": S.WORKLOADS["qwen05b"].replace(
+        name="qwen_bf16_small", n_layers=2, d_model=256, n_heads=4, n_kv_heads=2, head_dim=64, d_ff=512,
+        rotary_dims=64, batch=2, seq=300),
+    "neox_bf16_hd128": S.WORKLOADS["neox14b"].replace(
+        name="neox_bf16_hd128", n_layers=2, d_model=512, n_heads=4, n_kv_heads=4, head_dim=128, d_ff=1024,
+        rotary_dims=32, batch=2, seq=200),
+    "qwen_bf16_hd128": S.WORKLOADS["qwen7b"].replace(
+        name="qwen_bf16_hd128", n_layers=2, d_model=512, n_heads=8, n_kv_heads=2, head_dim=128, d_ff=768,
+        rotary_dims=128, batch=1, seq=257),
+}
+
+
+def workload(name):
+    return S.WORKLOADS[name] if name in S.WORKLOADS else SMALL[name]
+
+
+def run_layer(dev, w, W, x, k, flags=0, idx_in=None):
+    B, T = x.shape[0], x.shape[1]
+    dl = P.DeviceLayer(W, dev)
+    xd = x.to(dev).contiguous()
+    scores = torch.empty(B, T, dtype=torch.float32, device=dev)
+    idx = torch.empty(B, max(k, 1), dtype=torch.int32, device=dev)
+    ws = workspace(w, B, T, k, dev)
+    dense = flags & P.FLAG_DENSE
+    P.sparse_block_forward(make_desc(w), dl.weights, xd, k, ws, flags=flags,
+                           scores_out=None if dense else scores,
+                           idx_out=None if (dense or k == 0) else idx[:, :k],
+                           idx_in=None if idx_in is None else idx_in.to(dev))
+    torch.cuda.synchronize()
+    return xd, scores, idx[:, :k]
+
+
+def check_layer(w, W, x, y_gpu, scores_gpu, idx_gpu, k, sample=None):
+    """Layer protocol: router scores within the fp32 bound and the oracle's
+    Top-K of the GPU's scores equal to the GPU's indices (every sequence),
+    skipped rows bitwise unchanged (every sequence), and the kept rows
+    against the oracle teacher-forced with the GPU's indices, for the
+    sequences in `sample` (None: all of them)."""
+    xs = to_np(x)
+    sc = scores_gpu.cpu().numpy()
+    ref_scores = O.router_scores(x, W["router_w1"], W["router_b1"], W["router_w2"], W["router_b2"])
+    assert np.all(np.abs(sc - ref_scores) <= router_bound(xs, W, w.dtype))
+    idx = idx_gpu.cpu().numpy().astype(np.int64)
+    np.testing.assert_array_equal(idx, O.topk_select(sc, k))
+    y = to_np(y_gpu)
+    B, T, _ = xs.shape
+    kept = np.zeros((B, T), dtype=bool)
+    for b in range(B):
+        kept[b, idx[b]] = True
+        np.testing.assert_array_equal(y[b][~kept[b]], xs[b][~kept[b]])
+    for b in (range(B) if sample is None else sample):
+        res = O.routed_layer(desc_dict(w), W, xs[b:b + 1], k, idx=idx[b:b + 1])
+        assert rel_inf(y[b][kept[b]] - xs[b][kept[b]], res["delta"][0]) < TOL[w.dtype]
+        assert rel_inf(y[b], res["y"][0]) < TOL[w.dtype]

@@ -19,66 +19,10 @@ import paper_2607_21291_amd as P
 import synthetic as S
 from oracle import adadsf_oracle as O
 
-from gpu_util import announce, desc_dict, dtype_code, make_desc, rel_inf, router_bound, to_np, workspace
+from gpu_util import (TOL, announce, check_layer, desc_dict, make_desc, rel_inf, run_layer, to_np, workload,
+                      workspace)
 
 pytestmark = pytest.mark.gpu
-
-TOL = {"f32": 1e-4, "bf16": 2e-2}
-
-# Small bf16 shapes that still span several GEMM tiles and ragged tails.
-SMALL = {
-    "neox_bf16_small": S.WORKLOADS["neox160m"].replace(
-        name="neox_bf16_small", n_layers=2, d_model=256, n_heads=4, n_kv_heads=4, head_dim=64, d_ff=1024,
-        rotary_dims=16, batch=2, seq=300),
-    "qwen_bf16_small": S.WORKLOADS["qwen05b"].replace(
-        name="qwen_bf16_small", n_layers=2, d_model=256, n_heads=4, n_kv_heads=2, head_dim=64, d_ff=512,
-        rotary_dims=64, batch=2, seq=300),
-    "neox_bf16_hd128": S.WORKLOADS["neox14b"].replace(
-        name="neox_bf16_hd128", n_layers=2, d_model=512, n_heads=4, n_kv_heads=4, head_dim=128, d_ff=1024,
-        rotary_dims=32, batch=2, seq=200),
-    "qwen_bf16_hd128": S.WORKLOADS["qwen7b"].replace(
-        name="qwen_bf16_hd128", n_layers=2, d_model=512, n_heads=8, n_kv_heads=2, head_dim=128, d_ff=768,
-        rotary_dims=128, batch=1, seq=257),
-}
-
-
-def workload(name):
-    return S.WORKLOADS[name] if name in S.WORKLOADS else SMALL[name]
-
-
-def run_layer(dev, w, W, x, k, flags=0, idx_in=None):
-    B, T = x.shape[0], x.shape[1]
-    dl = P.DeviceLayer(W, dev)
-    xd = x.to(dev).contiguous()
-    scores = torch.empty(B, T, dtype=torch.float32, device=dev)
-    idx = torch.empty(B, max(k, 1), dtype=torch.int32, device=dev)
-    ws = workspace(w, B, T, k, dev)
-    dense = flags & P.FLAG_DENSE
-    P.sparse_block_forward(make_desc(w), dl.weights, xd, k, ws, flags=flags,
-                           scores_out=None if dense else scores,
-                           idx_out=None if (dense or k == 0) else idx[:, :k],
-                           idx_in=None if idx_in is None else idx_in.to(dev))
-    torch.cuda.synchronize()
-    return xd, scores, idx[:, :k]
-
-
-def check_layer(w, W, x, y_gpu, scores_gpu, idx_gpu, k):
-    xs = to_np(x)
-    sc = scores_gpu.cpu().numpy()
-    ref_scores = O.router_scores(x, W["router_w1"], W["router_b1"], W["router_w2"], W["router_b2"])
-    assert np.all(np.abs(sc - ref_scores) <= router_bound(xs, W, w.dtype))
-    idx = idx_gpu.cpu().numpy().astype(np.int64)
-    np.testing.assert_array_equal(idx, O.topk_select(sc, k))
-    res = O.routed_layer(desc_dict(w), W, xs, k, idx=idx)
-    y = to_np(y_gpu)
-    B, T, _ = xs.shape
-    for b in range(B):
-        kept = np.zeros(T, dtype=bool)
-        kept[idx[b]] = True
-        np.testing.assert_array_equal(y[b][~kept], xs[b][~kept])
-        assert rel_inf(y[b][kept] - xs[b][kept], res["delta"][b]) < TOL[w.dtype]
-    assert rel_inf(y, res["y"]) < TOL[w.dtype]
-
 
 CASES = [("tiny_neox_f32", 32), ("tiny_qwen_f32", 32), ("tiny_neox_f32", 1), ("tiny_qwen_f32", 63),
          ("neox_bf16_small", 150), ("qwen_bf16_small", 150), ("neox_bf16_small", 1), ("qwen_bf16_small", 299),

@@ -1,0 +1,77 @@
+"""The two schedules of the bf16 projection GEMMs give the layer the oracle
+computes: one tile per workgroup, and stream-K (a persistent grid whose
+workgroups split the k-iterations of the last tiles and add partial sums in
+a fixed order). DSF_GEMM_SCHEDULE forces one of them; on these small shapes
+the forced stream-K grid leaves most workgroups a short or empty piece, so
+the partial-sum paths (many contributors per tile, empty pieces) all run.
+
+Stream-K adds the partials in an order fixed by the shape, so repeated runs
+are bitwise equal; the two schedules round differently, and each is held to
+the oracle at the bf16 tolerance.
+"""
+import pytest
+import torch
+
+import paper_2607_21291_amd as P
+import synthetic as S
+
+from gpu_util import TOL, announce, check_layer, make_desc, rel_inf, run_layer, to_np, workload, workspace
+
+pytestmark = pytest.mark.gpu
+
+CASES = [("neox_bf16_small", 150), ("qwen_bf16_small", 299), ("neox_bf16_hd128", 97), ("qwen_bf16_hd128", 129),
+         ("neox_bf16_small", 1)]
+
+
+@pytest.mark.parametrize("name,k", CASES)
+def test_stream_k_layer_matches_oracle(dev, monkeypatch, name, k):
+    w = workload(name)
+    W = S.layer_weights(w, 0)
+    x = S.hidden_states(w)
+    monkeypatch.setenv("DSF_GEMM_SCHEDULE", "streamk")
+    announce(f"stream-K layer {name} k={k}")
+    y, scores, idx = run_layer(dev, w, W, x, k)
+    check_layer(w, W, x, y, scores, idx, k)
+    y2, _, _ = run_layer(dev, w, W, x, k)
+    assert torch.equal(y, y2)
+    monkeypatch.setenv("DSF_GEMM_SCHEDULE", "classic")
+    announce(f"classic layer {name} k={k}")
+    yc, _, idxc = run_layer(dev, w, W, x, k)
+    assert torch.equal(idx, idxc)
+    assert rel_inf(to_np(y) - to_np(x), to_np(yc) - to_np(x)) < TOL[w.dtype]
+
+
+@pytest.mark.parametrize("name", ["neox_bf16_small", "qwen_bf16_small"])
+def test_stream_k_stack_matches_layerwise(dev, monkeypatch, name):
+    w = workload(name).replace(n_layers=3)
+    monkeypatch.setenv("DSF_GEMM_SCHEDULE", "streamk")
+    announce(f"stream-K stack {name}")
+    Ws = S.stack_weights(w)
+    x = S.hidden_states(w)
+    T = w.seq
+    ks = [T // 2, T - 3, max(1, T // 5)]
+    dls = [P.DeviceLayer(W, dev) for W in Ws]
+    xd = x.to(dev)
+    ws = workspace(w, w.batch, T, max(ks), dev)
+    P.stack_forward(make_desc(w), [dl.weights for dl in dls], ks, xd, ws)
+    cur = x
+    for W, k in zip(Ws, ks):
+        y, _, _ = run_layer(dev, w, W, cur, k)
+        cur = y.cpu()
+    torch.cuda.synchronize()
+    assert torch.equal(xd.cpu(), cur)
+
+
+def test_full_size_schedules_agree(dev, monkeypatch):
+    # the down projection of the first neox160m layer (M = 8 x 1563 rows,
+    # 588 tiles) is where the automatic choice takes stream-K
+    w = S.WORKLOADS["neox160m"]
+    W = S.layer_weights(w, 0)
+    x = S.hidden_states(w)
+    k = 1563
+    announce("full-size neox160m layer 0: auto vs classic schedule")
+    ya, _, idxa = run_layer(dev, w, W, x, k)
+    monkeypatch.setenv("DSF_GEMM_SCHEDULE", "classic")
+    yc, _, idxc = run_layer(dev, w, W, x, k)
+    assert torch.equal(idxa, idxc)
+    assert rel_inf(to_np(ya) - to_np(x), to_np(yc) - to_np(x)) < TOL[w.dtype]
