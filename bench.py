@@ -40,8 +40,8 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 # library's plain copy kernel of known size. It holds only for the workload
 # and the GEMM source it was measured on (SHA-256 of kernels_gemm.hip); for
 # anything else `traffic` is null.
-TRAFFIC_MEASURED = {"workload": "neox160m", "bytes_per_launch": 2.035e+08,
-                    "gemm_source_sha256": "1c55c6d343d7153c80243325670439a6d107f172a724124a5167f0da5243cfa8",
+TRAFFIC_MEASURED = {"workload": "neox160m", "bytes_per_launch": 2.103e+08,
+                    "gemm_source_sha256": "a4434b5d48e22095874b556945c312013c0b1a66b7cf27c8c0488bec32befccd",
                     "profile": "profiles/gemm_down_neox160m.md"}
 
 

@@ -20,7 +20,8 @@ LIB = os.path.join(PKG, "libadadsf.so")
 SOURCES = ["api.hip", "kernels_misc.hip", "kernels_gemm.hip", "kernels_attn.hip"]
 # per-source extra flags: attention keeps its MFMA accumulators in ordinary
 # VGPRs, so the softmax reads scores and rescales outputs without AGPR moves
-EXTRA = {"kernels_attn.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+EXTRA = {"kernels_attn.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+         "kernels_gemm.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
 ARCH = "gfx950"
 CFLAGS = [

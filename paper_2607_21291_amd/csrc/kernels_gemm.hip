@@ -331,7 +331,7 @@ struct DmaCfg {
   static_assert(BK == 32 || BK == 64, "BK");
   static_assert(BM % (kRowsPerLoad * kWaves) == 0 && BN % (kRowsPerLoad * kWaves) == 0,
                 "tile rows must split evenly over waves");
-  static_assert((NS - 2) * kLoads < 64, "vmcnt range");
+  static_assert(NS >= 2 && (NS - 1) * kLoads < 64, "vmcnt range");
 };
 
 // Scheduling fence (no instruction moves across it), used to keep the next
@@ -361,10 +361,23 @@ __device__ __forceinline__ void ring_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
-// 16 bytes per lane from global memory into LDS at lds + 16 * lane (lds is
-// wave-uniform). Kept out of lambdas: the builtin exists only for the device.
-__device__ __forceinline__ void dma16(const void* gptr, char* lds) {
-  __builtin_amdgcn_global_load_lds(gptr, (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
+// A row-major bf16 matrix as a DMA source: a buffer resource covering its
+// rows x ld elements (range-checked: loads past the end read as zeros).
+struct RowSrc {
+  __amdgpu_buffer_rsrc_t rsrc;
+  int ld;
+  __device__ RowSrc(const void* p, int rows, int ld_) : ld(ld_) {
+    const int64_t bytes = p ? int64_t(rows) * ld_ * 2 : 0;
+    rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, int(bytes), 0x00020000);
+  }
+};
+
+// 16 bytes per lane from byte offset voff + soff of src into LDS at
+// lds + 16 * lane (lds and soff are wave-uniform). Kept out of lambdas: the
+// builtin exists only for the device.
+__device__ __forceinline__ void dma16(const RowSrc& src, uint32_t voff, uint32_t soff, char* lds) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(src.rsrc, (__attribute__((address_space(3))) void*)lds, 16, int(voff),
+                                           int(soff), 0, 0);
 }
 
 // Device-side pieces of the LDS-DMA GEMM: the main loop over a range of
@@ -381,49 +394,50 @@ struct DmaGemm {
   // Starts with a barrier, so the ring may still hold the previous tile.
   __device__ static __forceinline__ void mainloop(const GemmArgs& g, char* smem, int tm, int tn, int kb, int ke,
                                                   Acc& acc) {
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave / (BN / WN), wn = wave % (BN / WN);
     const int r16 = lane & 15, grp = lane >> 4;
     const int m0 = tm * BM;
-    // DMA source pointers. Load i of this wave fills tile rows RPL (wave + kWaves i) .. +RPL;
-    // lane -> row lane / CPR, physical chunk lane % CPR holding logical chunk swz^-1.
+    // DMA sources are buffer resources over A, A2, B, B2 whose size is the
+    // matrix's rows x leading dimension: a row beyond M (or N) is out of range
+    // and reads as zeros, so ragged tiles need no clamping. Load i of this
+    // wave fills tile rows RPL (wave + kWaves i) .. + RPL; the lane part of
+    // the offset (row lane / CPR, physical chunk lane % CPR holding logical
+    // chunk swz^-1) is the same for every load, the row base is uniform.
     const int lr = lane / CPR;
     const int lc = swz<BK>(lr, lane % CPR);  // swz is an involution for a fixed row
-    const uint16_t* pa[C::kLoadsA];
-    const uint16_t* pa2[C::kLoadsA];
-    const uint16_t* pb[C::kLoadsB];
-    const uint16_t* pb2[C::kLoadsB];
-#pragma unroll
-    for (int i = 0; i < C::kLoadsA; ++i) {
-      int m = m0 + RPL * (wave + C::kWaves * i) + lr;
-      if (m > g.M - 1) m = g.M - 1;
-      pa[i] = (const uint16_t*)g.a + int64_t(m) * g.lda + lc * 8;
-      pa2[i] = g.a2 ? (const uint16_t*)g.a2 + int64_t(m) * g.lda2 + lc * 8 : nullptr;
-    }
-#pragma unroll
-    for (int i = 0; i < C::kLoadsB; ++i) {
-      const int r = RPL * (wave + C::kWaves * i) + lr;
-      int n;
+    const RowSrc sa{g.a, g.M, g.lda}, sa2{g.a2, g.M, g.lda2};
+    const int nrows_b = EPI == EPI_SWIGLU ? 2 * g.f : g.N;
+    const RowSrc sb{g.b, nrows_b, g.ldb}, sb2{g.b2, nrows_b, g.ldb2};
+    const uint32_t va = uint32_t(lr * g.lda + lc * 8) * 2u, va2 = uint32_t(lr * g.lda2 + lc * 8) * 2u;
+    const uint32_t vb = uint32_t(lr * g.ldb + lc * 8) * 2u, vb2 = uint32_t(lr * g.ldb2 + lc * 8) * 2u;
+    // first B row of load i (uniform)
+    auto brow = [&](int i) {
+      const int r = RPL * (wave + C::kWaves * i);
       if constexpr (EPI == EPI_SWIGLU) {
         // each 128-row block of the B tile holds 64 gate units then the same 64 up units
         const int blk = r / 128, rr = r % 128, u0 = (tn * (BN / 128) + blk) * 64;
-        n = rr < 64 ? u0 + rr : g.f + u0 + (rr - 64);
+        return rr < 64 ? u0 + rr : g.f + u0 + (rr - 64);
       } else {
-        n = min(tn * BN + r, g.N - 1);
+        return tn * BN + r;
       }
-      pb[i] = (const uint16_t*)g.b + int64_t(n) * g.ldb + lc * 8;
-      pb2[i] = g.b2 ? (const uint16_t*)g.b2 + int64_t(n) * g.ldb2 + lc * 8 : nullptr;
-    }
+    };
     auto issue = [&](int kt) {
       const int k0 = kt * BK;
       const bool second = k0 >= g.K1;
       const int kc = second ? k0 - g.K1 : k0;
       char* st = smem + (kt % NS) * C::kStage;
+      const RowSrc& A = second ? sa2 : sa;
+      const RowSrc& Bm = second ? sb2 : sb;
+      const uint32_t vA = second ? va2 : va, vB = second ? vb2 : vb;
 #pragma unroll
-      for (int i = 0; i < C::kLoadsA; ++i) dma16((second ? pa2[i] : pa[i]) + kc, st + 1024 * (wave + C::kWaves * i));
+      for (int i = 0; i < C::kLoadsA; ++i)
+        dma16(A, vA, uint32_t((m0 + RPL * (wave + C::kWaves * i)) * A.ld + kc) * 2u,
+              st + 1024 * (wave + C::kWaves * i));
 #pragma unroll
       for (int i = 0; i < C::kLoadsB; ++i)
-        dma16((second ? pb2[i] : pb[i]) + kc, st + BM * C::kRowBytes + 1024 * (wave + C::kWaves * i));
+        dma16(Bm, vB, uint32_t(brow(i) * Bm.ld + kc) * 2u, st + BM * C::kRowBytes + 1024 * (wave + C::kWaves * i));
     };
 
 #pragma unroll
@@ -436,60 +450,85 @@ struct DmaGemm {
     // wave is done with the LDS before the ring is refilled.
     wait_vmcnt<0>();
     ring_barrier();
+    // Ring of NS buffers, all filled ahead: tile kt lives in buffer kt % NS,
+    // and tile kt + NS is issued into it as soon as tile kt has been read.
 #pragma unroll
-    for (int s = 0; s < NS - 1; ++s)
+    for (int s = 0; s < NS; ++s)
       if (kb + s < ke) issue(kb + s);
-    for (int kt = kb; kt < ke; ++kt) {
-      // tile kt has landed once at most (tiles issued after it) * kLoads loads remain
-      if (kt + NS - 2 < ke) wait_vmcnt<(NS - 2) * C::kLoads>();
-      else wait_vmcnt<0>();
-      ring_barrier();  // every wave's part of tile kt is visible; tile kt-1's buffer is free
-      // tile kt + NS - 1 goes into tile kt-1's buffer; all its loads leave before
-      // the compute so that they get the whole tile's MFMA time to land
-      if (kt + NS - 1 < ke) issue(kt + NS - 1);
-      const uint16_t* At = reinterpret_cast<const uint16_t*>(smem + (kt % NS) * C::kStage);
+    if (kb + NS - 1 < ke) wait_vmcnt<(NS - 1) * C::kLoads>();  // tile kb has landed
+    else wait_vmcnt<0>();
+    ring_barrier();
+
+    constexpr int KS = BK / 32;   // 32-deep MFMA substeps per tile
+    constexpr int G = KS * MI;    // MFMA groups per tile (one A fragment each)
+    auto tileA = [&](int kt) { return reinterpret_cast<const uint16_t*>(smem + (kt % NS) * C::kStage); };
+    bf16x8 bq[2][NI];             // B fragments of the current and the next substep
+    auto read_b = [&](const uint16_t* At, int ks, int buf) {
       const uint16_t* Bt = At + BM * BK;
-      // Software pipeline over (substep ks, A fragment i): the read of the next A
-      // fragment is issued before the NI MFMAs of the current one, and the next
-      // substep's B fragments are read halfway through the current substep, so
-      // every LDS wait finds its data already there and the MFMA pipe (whose
-      // issue is blocking) does not idle behind a late read.
-      constexpr int KS = BK / 32;
-      bf16x8 bq[2][NI];
-      auto read_b = [&](int ks, int buf) {
-        const int ch = ks * 4 + grp;
+      const int ch = ks * 4 + grp;
 #pragma unroll
-        for (int j = 0; j < NI; ++j) {
-          const int br = wn * WN + j * 16 + r16;
-          bq[buf][j] = *reinterpret_cast<const bf16x8*>(Bt + br * BK + (swz<BK>(br, ch) << 3));
-        }
-      };
-      auto read_a = [&](int ks, int i) -> bf16x8 {
-        const int ar = wm * WM + i * 16 + r16;
-        return *reinterpret_cast<const bf16x8*>(At + ar * BK + (swz<BK>(ar, ks * 4 + grp) << 3));
-      };
-      read_b(0, 0);
-      bf16x8 a_cur = read_a(0, 0);
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-#pragma unroll
-        for (int i = 0; i < MI; ++i) {
-          // the LDS wait before this group's first MFMA covers only reads issued
-          // one group earlier; this group's reads go out right after it
-          acc[i][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_cur, bq[ks & 1][0], acc[i][0], 0, 0, 0);
-          DSF_SCHED_FENCE();
-          bf16x8 a_nxt = a_cur;
-          if (i + 1 < MI) a_nxt = read_a(ks, i + 1);
-          else if (ks + 1 < KS) a_nxt = read_a(ks + 1, 0);
-          if (i == MI / 2 && ks + 1 < KS) read_b(ks + 1, (ks + 1) & 1);
-          DSF_SCHED_FENCE();
-#pragma unroll
-          for (int j = 1; j < NI; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_cur, bq[ks & 1][j], acc[i][j], 0, 0, 0);
-          DSF_SCHED_FENCE();
-          a_cur = a_nxt;
-        }
+      for (int j = 0; j < NI; ++j) {
+        const int br = wn * WN + j * 16 + r16;
+        bq[buf][j] = *reinterpret_cast<const bf16x8*>(Bt + br * BK + (swz<BK>(br, ch) << 3));
       }
+    };
+    auto read_a = [&](const uint16_t* At, int ks, int i) -> bf16x8 {
+      const int ar = wm * WM + i * 16 + r16;
+      return *reinterpret_cast<const bf16x8*>(At + ar * BK + (swz<BK>(ar, ks * 4 + grp) << 3));
+    };
+    read_b(tileA(kb), 0, 0);
+    bf16x8 a_cur = read_a(tileA(kb), 0, 0);
+
+    // One tile. Software pipeline over its MFMA groups: the next A fragment is
+    // read before the NI MFMAs of the current one, and the next substep's B
+    // fragments halfway through the current substep. In the last group the
+    // workgroup moves on to tile kt + 1: wait for its loads, one barrier (all
+    // reads of tile kt are complete, so its buffer takes tile kt + NS), and
+    // read tile kt + 1's first fragments under the group's remaining MFMAs,
+    // so no tile starts with an exposed LDS wait. B fragments alternate
+    // between the two register sets by substep; P is the tile's parity
+    // relative to kb, which makes every index below a compile-time constant.
+    auto step = [&](int kt, auto Pc) {
+      constexpr int P = decltype(Pc)::value;
+      const uint16_t* At = tileA(kt);
+      const bool has_next = kt + 1 < ke;
+#pragma unroll
+      for (int gi = 0; gi < G; ++gi) {
+        const int ks = gi / MI, i = gi % MI;
+        const int cb = (P * KS + ks) & 1;
+        acc[i][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_cur, bq[cb][0], acc[i][0], 0, 0, 0);
+        DSF_SCHED_FENCE();
+        bf16x8 a_nxt = a_cur;
+        if (gi + 1 < G) {
+          a_nxt = read_a(At, (gi + 1) / MI, (gi + 1) % MI);
+          if (i == MI / 2 && ks + 1 < KS) read_b(At, ks + 1, (P * KS + ks + 1) & 1);
+        } else if (has_next) {
+          // tile kt + 1 has landed once the tiles issued after it are all that remain
+          if (kt + NS - 1 < ke) wait_vmcnt<(NS - 2) * C::kLoads>();
+          else wait_vmcnt<0>();
+          ring_barrier();
+          if (kt + NS < ke) issue(kt + NS);
+          const uint16_t* An = tileA(kt + 1);
+          read_b(An, 0, ((P + 1) * KS) & 1);
+          a_nxt = read_a(An, 0, 0);
+        }
+        DSF_SCHED_FENCE();
+#pragma unroll
+        for (int j = 1; j < NI; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_cur, bq[cb][j], acc[i][j], 0, 0, 0);
+        DSF_SCHED_FENCE();
+        a_cur = a_nxt;
+      }
+    };
+    if constexpr (KS % 2 == 0) {
+      for (int kt = kb; kt < ke; ++kt) step(kt, std::integral_constant<int, 0>());
+    } else {
+      int kt = kb;
+      for (; kt + 1 < ke; kt += 2) {
+        step(kt, std::integral_constant<int, 0>());
+        step(kt + 1, std::integral_constant<int, 1>());
+      }
+      if (kt < ke) step(kt, std::integral_constant<int, 0>());
     }
   }
 
@@ -549,39 +588,30 @@ struct DmaGemm {
   // no invalidation of the reader's L2 after it (both would cost every other
   // workgroup on those XCDs its cached tiles).
   // Fragment f = i * NI + j of a wave's partial sits at slot_ptr + 64 f. The
-  // accesses go 16 fragments per statement (4 address registers, immediate
+  // accesses go 8 fragments per statement (2 address registers, immediate
   // offsets of 1, 2, 3 KiB), and each statement waits for its own accesses, so
   // no register it names is touched while its memory operation is in flight.
-  static_assert((MI * NI) % 16 == 0, "partials move in groups of 16 fragments");
+  static_assert((MI * NI) % 8 == 0, "partials move in groups of 8 fragments");
 
   __device__ static __forceinline__ void store_partial(const GemmArgs& g, const Acc& acc) {
     const f32x4* a = &acc[0][0];
     f32x4* p = slot_ptr(g, int(blockIdx.x));
 #pragma unroll
-    for (int c = 0; c < MI * NI; c += 16) {
+    for (int c = 0; c < MI * NI; c += 8) {
       const f32x4* v = a + c;
       asm volatile(
-          "global_store_dwordx4 %0, %4, off sc1\n\t"
-          "global_store_dwordx4 %0, %5, off offset:1024 sc1\n\t"
-          "global_store_dwordx4 %0, %6, off offset:2048 sc1\n\t"
-          "global_store_dwordx4 %0, %7, off offset:3072 sc1\n\t"
-          "global_store_dwordx4 %1, %8, off sc1\n\t"
-          "global_store_dwordx4 %1, %9, off offset:1024 sc1\n\t"
-          "global_store_dwordx4 %1, %10, off offset:2048 sc1\n\t"
-          "global_store_dwordx4 %1, %11, off offset:3072 sc1\n\t"
-          "global_store_dwordx4 %2, %12, off sc1\n\t"
-          "global_store_dwordx4 %2, %13, off offset:1024 sc1\n\t"
-          "global_store_dwordx4 %2, %14, off offset:2048 sc1\n\t"
-          "global_store_dwordx4 %2, %15, off offset:3072 sc1\n\t"
-          "global_store_dwordx4 %3, %16, off sc1\n\t"
-          "global_store_dwordx4 %3, %17, off offset:1024 sc1\n\t"
-          "global_store_dwordx4 %3, %18, off offset:2048 sc1\n\t"
-          "global_store_dwordx4 %3, %19, off offset:3072 sc1\n\t"
+          "global_store_dwordx4 %0, %2, off sc1\n\t"
+          "global_store_dwordx4 %0, %3, off offset:1024 sc1\n\t"
+          "global_store_dwordx4 %0, %4, off offset:2048 sc1\n\t"
+          "global_store_dwordx4 %0, %5, off offset:3072 sc1\n\t"
+          "global_store_dwordx4 %1, %6, off sc1\n\t"
+          "global_store_dwordx4 %1, %7, off offset:1024 sc1\n\t"
+          "global_store_dwordx4 %1, %8, off offset:2048 sc1\n\t"
+          "global_store_dwordx4 %1, %9, off offset:3072 sc1\n\t"
           "s_waitcnt vmcnt(0)"
           :
-          : "v"(p + (c + 0) * 64), "v"(p + (c + 4) * 64), "v"(p + (c + 8) * 64), "v"(p + (c + 12) * 64),
-            "v"(v[0]), "v"(v[1]), "v"(v[2]), "v"(v[3]), "v"(v[4]), "v"(v[5]), "v"(v[6]), "v"(v[7]),
-            "v"(v[8]), "v"(v[9]), "v"(v[10]), "v"(v[11]), "v"(v[12]), "v"(v[13]), "v"(v[14]), "v"(v[15])
+          : "v"(p + (c + 0) * 64), "v"(p + (c + 4) * 64), "v"(v[0]), "v"(v[1]), "v"(v[2]), "v"(v[3]), "v"(v[4]),
+            "v"(v[5]), "v"(v[6]), "v"(v[7])
           : "memory");
     }
   }
@@ -591,33 +621,24 @@ struct DmaGemm {
     f32x4* a = &acc[0][0];
     const f32x4* p = slot_ptr(g, slot);
 #pragma unroll
-    for (int c = 0; c < MI * NI; c += 16) {
-      f32x4 v[16];
+    for (int c = 0; c < MI * NI; c += 8) {
+      f32x4 v[8];
       asm volatile(
-          "global_load_dwordx4 %0, %16, off sc1\n\t"
-          "global_load_dwordx4 %1, %16, off offset:1024 sc1\n\t"
-          "global_load_dwordx4 %2, %16, off offset:2048 sc1\n\t"
-          "global_load_dwordx4 %3, %16, off offset:3072 sc1\n\t"
-          "global_load_dwordx4 %4, %17, off sc1\n\t"
-          "global_load_dwordx4 %5, %17, off offset:1024 sc1\n\t"
-          "global_load_dwordx4 %6, %17, off offset:2048 sc1\n\t"
-          "global_load_dwordx4 %7, %17, off offset:3072 sc1\n\t"
-          "global_load_dwordx4 %8, %18, off sc1\n\t"
-          "global_load_dwordx4 %9, %18, off offset:1024 sc1\n\t"
-          "global_load_dwordx4 %10, %18, off offset:2048 sc1\n\t"
-          "global_load_dwordx4 %11, %18, off offset:3072 sc1\n\t"
-          "global_load_dwordx4 %12, %19, off sc1\n\t"
-          "global_load_dwordx4 %13, %19, off offset:1024 sc1\n\t"
-          "global_load_dwordx4 %14, %19, off offset:2048 sc1\n\t"
-          "global_load_dwordx4 %15, %19, off offset:3072 sc1\n\t"
+          "global_load_dwordx4 %0, %8, off sc1\n\t"
+          "global_load_dwordx4 %1, %8, off offset:1024 sc1\n\t"
+          "global_load_dwordx4 %2, %8, off offset:2048 sc1\n\t"
+          "global_load_dwordx4 %3, %8, off offset:3072 sc1\n\t"
+          "global_load_dwordx4 %4, %9, off sc1\n\t"
+          "global_load_dwordx4 %5, %9, off offset:1024 sc1\n\t"
+          "global_load_dwordx4 %6, %9, off offset:2048 sc1\n\t"
+          "global_load_dwordx4 %7, %9, off offset:3072 sc1\n\t"
           "s_waitcnt vmcnt(0)"
           : "=&v"(v[0]), "=&v"(v[1]), "=&v"(v[2]), "=&v"(v[3]), "=&v"(v[4]), "=&v"(v[5]), "=&v"(v[6]),
-            "=&v"(v[7]), "=&v"(v[8]), "=&v"(v[9]), "=&v"(v[10]), "=&v"(v[11]), "=&v"(v[12]), "=&v"(v[13]),
-            "=&v"(v[14]), "=&v"(v[15])
-          : "v"(p + (c + 0) * 64), "v"(p + (c + 4) * 64), "v"(p + (c + 8) * 64), "v"(p + (c + 12) * 64)
+            "=&v"(v[7])
+          : "v"(p + (c + 0) * 64), "v"(p + (c + 4) * 64)
           : "memory");
 #pragma unroll
-      for (int f = 0; f < 16; ++f) a[c + f] = a[c + f] + v[f];
+      for (int f = 0; f < 8; ++f) a[c + f] = a[c + f] + v[f];
     }
   }
 };
@@ -874,9 +895,20 @@ static void launch_timed(K kern, dim3 grid, dim3 block, hipStream_t s, const Gem
   else kern<<<grid, block, 0, s>>>(g);
 }
 
+// The DMA kernels address each operand through a buffer resource with a
+// 32-bit byte range and 32-bit offsets: every operand, padded to whole tiles,
+// must stay below 4 GiB.
+static bool dma_addressable(const GemmArgs& g, int rows_b) {
+  const int64_t lim = (int64_t(1) << 32) - 1024;
+  const int64_t mp = int64_t(g.M + DSF_GEMM_BM), np = int64_t(rows_b + DSF_GEMM_BN);
+  return mp * g.lda * 2 < lim && (!g.a2 || mp * g.lda2 * 2 < lim) && np * g.ldb * 2 < lim &&
+         (!g.b2 || np * g.ldb2 * 2 < lim);
+}
+
 template <int EPI>
 static void launch_gemm_t(const GemmArgs& g, hipStream_t s) {
-  if (DSF_GEMM_USE_DMA && g.dtype == DSF_BF16 && g.K % DSF_GEMM_BK == 0 && g.K1 % DSF_GEMM_BK == 0) {
+  if (DSF_GEMM_USE_DMA && g.dtype == DSF_BF16 && g.K % DSF_GEMM_BK == 0 && g.K1 % DSF_GEMM_BK == 0 &&
+      dma_addressable(g, EPI == EPI_SWIGLU ? 2 * g.f : g.N)) {
     constexpr int BM = DSF_GEMM_BM, BN = DSF_GEMM_BN, WM = DSF_GEMM_WM, WN = DSF_GEMM_WN;
     constexpr int NS = DSF_GEMM_NS, BK = DSF_GEMM_BK;
     using Cfg = DmaCfg<BM, BN, WM, WN, NS, BK>;
