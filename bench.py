@@ -110,6 +110,10 @@ def main():
     ap.add_argument("--steps", type=int, default=30)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="neox160m")
+    ap.add_argument("--retention", type=float, default=None,
+                    help="uniform retention r for every layer (skips the allocation and the calibration pass)")
+    ap.add_argument("--batch", type=int, default=None, help="override the workload's batch")
+    ap.add_argument("--seq", type=int, default=None, help="override the workload's sequence length")
     ap.add_argument("--cpu-layers", type=int, default=None, help="layers of the CPU oracle sample (default all)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true", help="skip the dense-stack comparison run")
@@ -133,6 +137,14 @@ def main():
 
     dev = torch.device("cuda:0")
     w = S.WORKLOADS[args.workload]
+    if args.batch or args.seq:
+        w = w.replace(batch=args.batch or w.batch, seq=args.seq or w.seq)
+        w = w.replace(name=f"{w.name}_B{w.batch}_T{w.seq}")
+    if args.retention is not None:
+        if not 0.0 < args.retention <= 1.0:
+            ap.error("--retention must be in (0, 1]")
+        w = w.replace(name=f"{w.name}_r{args.retention:g}", retention=(args.retention,) * w.n_layers,
+                      similarity=None)
     B, T, L = w.batch, w.seq, w.n_layers
     dt = w.torch_dtype
     dcode = P.F32 if w.dtype == "f32" else P.BF16
@@ -148,7 +160,7 @@ def main():
         args.no_dense = args.no_cpu_baseline = True
     # calibration pass: dense stack + on-GPU similarity statistic (Eq. 4), allocation (Eqs. 5-8)
     s_meas, t_cal = None, None
-    if not (args.only_sparse and w.similarity is not None):
+    if args.retention is None and not (args.only_sparse and w.similarity is not None):
         ws_cal = torch.empty(P.workspace_size(desc, dcode, B, T, T, True), dtype=torch.uint8, device=dev)
         accum = torch.zeros(L, 2, dtype=torch.float64, device=dev)
         xc = x0.clone()

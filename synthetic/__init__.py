@@ -87,7 +87,7 @@ def _linspace(a, b, n):
     return tuple(float(v) for v in np.linspace(a, b, n))
 
 
-# The five workloads. Shapes follow the public configurations of the model
+# The workloads. Shapes follow the public configurations of the model
 # families the paper evaluates (GPT-NeoX, Qwen2.5); weights are random.
 WORKLOADS: Dict[str, Workload] = {
     # Tiny single routed layer, fp32, NeoX-style block at d=128.
@@ -110,6 +110,16 @@ WORKLOADS: Dict[str, Workload] = {
     "neox14b": Workload(
         "neox14b", NEOX, 24, 2048, 16, 16, 128, 8192, 32, 10000.0, 1e-5, 32,
         4, 2048, "bf16", retention=(0.5,) * 24),
+    # The paper's own evaluation models at uniform retention (Tables 1-2):
+    # GPT-NeoX-130M (its shape is not given; the 12 x 768 GPT-NeoX shape is
+    # used) on 16 sequences of 1024 tokens, and Qwen2.5-1.5B (28 x 1536,
+    # 12 q / 2 kv heads of 128, SwiGLU 8960) on 8 sequences of 2048.
+    "neox130m": Workload(
+        "neox130m", NEOX, 12, 768, 12, 12, 64, 3072, 16, 10000.0, 1e-5, 32,
+        16, 1024, "bf16", retention=(0.8,) * 12),
+    "qwen15b": Workload(
+        "qwen15b", QWEN, 28, 1536, 12, 2, 128, 8960, 128, 1e6, 1e-6, 32,
+        8, 2048, "bf16", retention=(0.8,) * 28),
     # Qwen2.5-7B shape: 28 x 3584, 28 q / 4 kv heads of 128, SwiGLU 18944.
     # Retention comes from similarities measured on the stack itself.
     "qwen7b": Workload(
