@@ -61,3 +61,44 @@ def router_bytes(w, B: int, T: int) -> float:
 def sim_bytes(w, B: int, T: int) -> float:
     eb = 4 if w.dtype == "f32" else 2
     return 2.0 * eb * B * T * w.d_model
+
+
+def topk_bytes(w, B: int, T: int, k: int) -> float:
+    """Scores read, kept positions written."""
+    return 4.0 * B * T + 4.0 * B * k
+
+
+def norm_bytes(w, B: int, k: int) -> float:
+    """Gather + normalisation kernels of one layer: NeoX reads each kept row once
+    and writes LN1 and LN2 of it; Qwen writes RMS1 of the kept row, then reads h
+    and writes RMS2(h). Plus the kept positions."""
+    eb = 4 if w.dtype == "f32" else 2
+    rows = eb * B * k * w.d_model
+    return (3.0 if w.block == NEOX else 4.0) * rows + 4.0 * B * k
+
+
+def kind_work(w, kind: str, B: int, T: int, k: int):
+    """(work, unit) of one layer's launches of a kernel kind: flops for the
+    MFMA kernels, bytes for the streaming ones; None for kinds not modelled."""
+    d, hd, f = w.d_model, w.head_dim, w.d_ff
+    dq, dkv = w.n_heads * hd, w.n_kv_heads * hd
+    M = B * k
+    if kind == "gemm_qkv":
+        return 2.0 * M * d * (dq + 2 * dkv), "flop"
+    if kind == "gemm_up":
+        return 2.0 * M * d * f * (1 if w.block == NEOX else 2), "flop"
+    if kind == "gemm_o":
+        return 2.0 * M * dq * d, "flop"
+    if kind == "gemm_down":
+        return gemm_down_flops(w, B, k), "flop"
+    if kind == "attn":
+        return attn_flops(w, B, k), "flop"
+    if kind == "router":
+        return router_bytes(w, B, T), "byte"
+    if kind == "topk":
+        return topk_bytes(w, B, T, k), "byte"
+    if kind == "norm":
+        return norm_bytes(w, B, k), "byte"
+    if kind == "sim":
+        return sim_bytes(w, B, T), "byte"
+    return None

@@ -115,56 +115,99 @@ __device__ void gemm_epilogue(const GemmArgs& g, const float* stage, int m0, int
       }
     }
   }
-  for (int rr = tid / CPR; rr < BM; rr += RSTEP) {
-    const int m = m0 + rr;
-    if (m >= g.M) break;
-    const int b = m / g.kk, j = m - b * g.kk;
-    const int pos = g.idx ? clamp_pos(g.idx[m], g.T) : j;
-    const float* row = stage + rr * LD;
+  // Rows of this thread: rr0, rr0 + RSTEP, ... All their positions, and for
+  // the residual kinds all their residual rows, are requested before any row
+  // is finished, so the rows' memory latencies overlap instead of adding up.
+  constexpr int RPT = (BM + RSTEP - 1) / RSTEP;
+  const int rr0 = tid / CPR;
+  int bq[RPT], jq[RPT], pq[RPT];
+  bool live[RPT];
+#pragma unroll
+  for (int q = 0; q < RPT; ++q) {
+    const int m = m0 + rr0 + q * RSTEP;
+    live[q] = rr0 + q * RSTEP < BM && m < g.M;
+    const int mm = live[q] ? m : m0;  // m0 < M: a valid row to read for dead slots
+    bq[q] = mm / g.kk;
+    jq[q] = mm - bq[q] * g.kk;
+    pq[q] = g.idx ? clamp_pos(g.idx[mm], g.T) : jq[q];
+  }
+  if constexpr (EPI == EPI_RESID_STORE || EPI == EPI_RESID_SCATTER) {
+    float xr[RPT][8];
+#pragma unroll
+    for (int q = 0; q < RPT; ++q) {
+      if (!live[q]) continue;
+      const int m = m0 + rr0 + q * RSTEP;
+      const T* src = (EPI == EPI_RESID_SCATTER && g.res) ? (const T*)g.res + int64_t(m) * g.N + n
+                                                         : (const T*)g.x + (int64_t(bq[q]) * g.T + pq[q]) * g.N + n;
+      load8(src, xr[q]);
+    }
+#pragma unroll
+    for (int q = 0; q < RPT; ++q) {
+      if (!live[q]) continue;
+      const int m = m0 + rr0 + q * RSTEP;
+      const float* row = stage + (rr0 + q * RSTEP) * LD;
+      float v[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] = row[cc + i] + bias[i] + xr[q][i];
+      if constexpr (EPI == EPI_RESID_STORE) store8((T*)g.out + int64_t(m) * g.ldo + n, v);
+      else store8((T*)g.x + (int64_t(bq[q]) * g.T + pq[q]) * g.N + n, v);
+    }
+    return;
+  }
+#pragma unroll
+  for (int q = 0; q < RPT; ++q) {
+    if (!live[q]) continue;
+    const int m = m0 + rr0 + q * RSTEP;
+    const float* row = stage + (rr0 + q * RSTEP) * LD;
     float v[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) v[i] = row[cc + i] + bias[i];
     if constexpr (EPI == EPI_QKV_ROPE) {
       // columns: Q heads, then K heads, then V heads; written head-major [B, H, kk, hd]
-      T* dst = sec + ((int64_t(b) * heads + head) * g.kk + j) * g.hd + dim0;
+      T* dst = sec + ((int64_t(bq[q]) * heads + head) * g.kk + jq[q]) * g.hd + dim0;
       if (rot) {
         const int half = g.R / 2;
         float out[8];
+        if ((g.R & 15) == 0) {
+          // the chunk's 8 dims lie in one half: their (cos, sin) pairs are 64
+          // contiguous bytes of the table, their partners the chunk half a span away
+          const bool lo = dim0 < half;
+          const int off = lo ? half : -half;
+          const float4* cs = reinterpret_cast<const float4*>(g.rope + (int64_t(pq[q]) * half + (lo ? dim0 : dim0 - half)) * 2);
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const int dim = dim0 + i;
-          if (dim >= g.R) {
-            out[i] = v[i];
-            continue;
+          for (int p2 = 0; p2 < 4; ++p2) {
+            const float4 c = cs[p2];
+#pragma unroll
+            for (int e = 0; e < 2; ++e) {
+              const int i = 2 * p2 + e;
+              const float cv = e ? c.z : c.x, sv = e ? c.w : c.y;
+              const float xp = row[cc + off + i] + pbias[i];
+              out[i] = lo ? v[i] * cv - xp * sv : v[i] * cv + xp * sv;
+            }
           }
-          const bool lo = dim < half;
-          const int pdim = lo ? dim + half : dim - half;
-          const float xp = row[cc - dim0 + pdim] + pbias[i];
-          const float* cs = g.rope + (int64_t(pos) * half + (lo ? dim : dim - half)) * 2;
-          out[i] = lo ? v[i] * cs[0] - xp * cs[1] : v[i] * cs[0] + xp * cs[1];
+        } else {
+#pragma unroll
+          for (int i = 0; i < 8; ++i) {
+            const int dim = dim0 + i;
+            if (dim >= g.R) {
+              out[i] = v[i];
+              continue;
+            }
+            const bool lo = dim < half;
+            const int pdim = lo ? dim + half : dim - half;
+            const float xp = row[cc - dim0 + pdim] + pbias[i];
+            const float* cs = g.rope + (int64_t(pq[q]) * half + (lo ? dim : dim - half)) * 2;
+            out[i] = lo ? v[i] * cs[0] - xp * cs[1] : v[i] * cs[0] + xp * cs[1];
+          }
         }
         store8(dst, out);
       } else {
         store8(dst, v);
       }
-    } else if constexpr (EPI == EPI_BIAS_GELU) {
+    } else {  // EPI_BIAS_GELU
 #pragma unroll
       for (int i = 0; i < 8; ++i) v[i] = gelu_erf(v[i]);
       store8((T*)g.out + int64_t(m) * g.ldo + n, v);
-    } else if constexpr (EPI == EPI_RESID_STORE) {
-      float xr[8];
-      load8((const T*)g.x + (int64_t(b) * g.T + pos) * g.N + n, xr);
-#pragma unroll
-      for (int i = 0; i < 8; ++i) v[i] += xr[i];
-      store8((T*)g.out + int64_t(m) * g.ldo + n, v);
-    } else {  // EPI_RESID_SCATTER
-      T* dst = (T*)g.x + (int64_t(b) * g.T + pos) * g.N + n;
-      float xr[8];
-      if (g.res) load8((const T*)g.res + int64_t(m) * g.N + n, xr);
-      else load8(dst, xr);
-#pragma unroll
-      for (int i = 0; i < 8; ++i) v[i] += xr[i];
-      store8(dst, v);
     }
   }
 }

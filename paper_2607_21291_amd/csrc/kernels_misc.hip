@@ -127,73 +127,67 @@ __global__ __launch_bounds__(256) void router_bf16_kernel(const uint16_t* __rest
                                                           const uint16_t* __restrict__ b1,
                                                           const uint16_t* __restrict__ w2, float b2,
                                                           float* __restrict__ scores) {
-  constexpr int NB = DR / 16, NW = 4;
-  __shared__ float part[NW][16][DR + 1];
+  // 64 tokens per workgroup in 4 blocks of 16; wave w takes the 32-wide
+  // column slices w, w + 4, ... of all four blocks, so each W1 fragment it
+  // loads serves 64 tokens (W1 traffic is a quarter of x's at d_r = 32).
+  constexpr int NB = DR / 16, NW = 4, MT = 4;
+  __shared__ float part[NW][16 * MT][DR + 1];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int r = lane & 15, g = lane >> 4;
-  const int64_t row0 = int64_t(blockIdx.x) * 16;
-  int64_t row = row0 + r;
-  if (row > n - 1) row = n - 1;  // clamp: rows past the end are computed and dropped
-  const uint16_t* xr = x + row * d;
-  f32x4 acc[NB];
+  const int64_t row0 = int64_t(blockIdx.x) * (16 * MT);
+  const uint16_t* xr[MT];
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  const int dfull = (d / 128) * 128;
-  for (int kc = 128 * w; kc < dfull; kc += 128 * NW) {
-    bf16x8 xa[4], wb[NB][4];
+  for (int mt = 0; mt < MT; ++mt) {
+    int64_t row = row0 + 16 * mt + r;
+    if (row > n - 1) row = n - 1;  // clamp: rows past the end are computed and dropped
+    xr[mt] = x + row * d;
+  }
+  f32x4 acc[MT][NB];
 #pragma unroll
-    for (int s4 = 0; s4 < 4; ++s4) xa[s4] = *reinterpret_cast<const bf16x8*>(xr + kc + 32 * g + 8 * s4);
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) acc[mt][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const bf16x8 zero = {};
+#pragma unroll 3
+  for (int kc = 32 * w; kc < d; kc += 32 * NW) {
+    // d is a multiple of 8, so each lane's 8-element piece is wholly inside or past the end
+    const int k0 = kc + 8 * g;
+    const bool ok = k0 < d;
+    bf16x8 wb[NB], xa[MT];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+      wb[nb] = ok ? *reinterpret_cast<const bf16x8*>(w1 + (16 * nb + r) * int64_t(d) + k0) : zero;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) xa[mt] = ok ? *reinterpret_cast<const bf16x8*>(xr[mt] + k0) : zero;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+        acc[mt][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[mt], wb[nb], acc[mt][nb], 0, 0, 0);
+  }
+  // lane holds wave w's partial hidden[token 16 mt + 4 g + i][unit 16 nb + r]
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-      for (int s4 = 0; s4 < 4; ++s4)
-        wb[nb][s4] = *reinterpret_cast<const bf16x8*>(w1 + (16 * nb + r) * int64_t(d) + kc + 32 * g + 8 * s4);
-#pragma unroll
-    for (int s4 = 0; s4 < 4; ++s4)
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
-        acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[s4], wb[nb][s4], acc[nb], 0, 0, 0);
-  }
-  // tail (d % 128): 32-wide steps split the same way; 8-element pieces past d are zero
-  for (int kc = dfull + 32 * w; kc < d; kc += 32 * NW) {
-    const int k0 = kc + 8 * g;
-    const bool ok = k0 < d;
-    const bf16x8 zero = {};
-    const bf16x8 xa = ok ? *reinterpret_cast<const bf16x8*>(xr + k0) : zero;
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      const bf16x8 wb = ok ? *reinterpret_cast<const bf16x8*>(w1 + (16 * nb + r) * int64_t(d) + k0) : zero;
-      acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa, wb, acc[nb], 0, 0, 0);
-    }
-  }
-  // lane holds partial hidden[token 4 g + i][unit 16 nb + r]
-#pragma unroll
-  for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) part[w][4 * g + i][16 * nb + r] = acc[nb][i];
+      for (int i = 0; i < 4; ++i) part[w][16 * mt + 4 * g + i][16 * nb + r] = acc[mt][nb][i];
   __syncthreads();
-  if (w != 0) return;
-  float wv[NB], bv[NB];
+  // thread t: token t / 4, units q DR/4 .. (q + 1) DR/4 - 1 with q = t % 4; the
+  // four partial sums of a token are then added in a fixed order
+  const int t = threadIdx.x >> 2, q = threadIdx.x & 3;
+  float v = 0.f;
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    wv[nb] = bf2f(w2[16 * nb + r]);
-    bv[nb] = b1 ? bf2f(b1[16 * nb + r]) : 0.f;
+  for (int jj = 0; jj < DR / 4; ++jj) {
+    const int j = q * (DR / 4) + jj;
+    float h = b1 ? bf2f(b1[j]) : 0.f;
+#pragma unroll
+    for (int ww = 0; ww < NW; ++ww) h += part[ww][t][j];
+    v = fmaf(bf2f(w2[j]), h > 0.f ? h : 0.f, v);
   }
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int t = 4 * g + i;
-    float v = 0.f;
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      float h = bv[nb];
-#pragma unroll
-      for (int ww = 0; ww < NW; ++ww) h += part[ww][t][16 * nb + r];
-      v += wv[nb] * (h > 0.f ? h : 0.f);
-    }
-    v = row16_sum(v);
-    if (r == 0 && row0 + t < n) scores[row0 + t] = v + b2;
-  }
+  v += __shfl_xor(v, 1);
+  v += __shfl_xor(v, 2);
+  if (q == 0 && row0 + t < n) scores[row0 + t] = v + b2;
 }
 
 // fp32 router: one wavefront per token, one hidden unit at a time.
@@ -225,7 +219,7 @@ hipError_t launch_router(int dtype, const void* x, int64_t n, int d, int d_r, co
                                                             (const float*)b1, (const float*)w2, b2, scores);
     return hipGetLastError();
   }
-  unsigned grid = unsigned((n + 15) / 16);
+  unsigned grid = unsigned((n + 63) / 64);
   auto X = (const uint16_t*)x;
   auto W1 = (const uint16_t*)w1;
   auto B1 = (const uint16_t*)b1;
