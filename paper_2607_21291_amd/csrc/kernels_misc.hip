@@ -459,74 +459,108 @@ hipError_t launch_zero_u32(uint32_t* dst, int64_t n, hipStream_t s) {
 
 // ------------------------------------------- gather + LayerNorm / RMSNorm
 
-// One wavefront per output row; the row stays in registers (MAXC vectors per
-// lane) so it is read from HBM once for both normalisations.
-template <typename T, int MAXC>
+// RPW rows per wavefront; each row stays in registers (MAXC vectors per lane)
+// so it is read from HBM once for both normalisations. All of a wave's
+// positions, rows and (narrow rows) weights are requested before the first
+// reduction, so their memory latencies overlap.
+template <typename T, int MAXC, int RPW>
 __global__ __launch_bounds__(256) void norm_kernel(NormArgs a) {
   constexpr int V = Elem<T>::kVec;
   const int lane = threadIdx.x & 63;
   const int64_t rows = int64_t(a.B) * a.kk;
-  const int64_t r = int64_t(blockIdx.x) * 4 + (threadIdx.x >> 6);
-  if (r >= rows) return;
+  const int64_t r0 = (int64_t(blockIdx.x) * 4 + (threadIdx.x >> 6)) * RPW;
+  if (r0 >= rows) return;
   const int d = a.d, nvec = d / V;
-  const T* src;
-  if (a.src_rows == 0) {
-    src = (const T*)a.src + r * d;
-  } else {
-    int64_t b = r / a.kk;
-    int64_t j = r - b * a.kk;
-    int64_t pos = a.idx ? clamp_pos(a.idx[r], a.src_rows) : j;
-    src = (const T*)a.src + (b * a.src_rows + pos) * d;
-  }
-  float v[MAXC][V];
-  float sum = 0.f;
+  const T* src[RPW];
 #pragma unroll
-  for (int c = 0; c < MAXC; ++c) {
-    int ch = lane + 64 * c;
-    if (ch < nvec) {
-      load_vec(src + ch * V, v[c]);
-#pragma unroll
-      for (int i = 0; i < V; ++i) sum += v[c][i];
+  for (int q = 0; q < RPW; ++q) {
+    const int64_t r = r0 + q < rows ? r0 + q : rows - 1;  // dead slots re-read the last row
+    if (a.src_rows == 0) {
+      src[q] = (const T*)a.src + r * d;
+    } else {
+      const int64_t b = r / a.kk, j = r - b * a.kk;
+      const int64_t pos = a.idx ? clamp_pos(a.idx[r], a.src_rows) : j;
+      src[q] = (const T*)a.src + (b * a.src_rows + pos) * d;
     }
   }
-  float mean = 0.f, var;
-  if (a.rms) {
-    float sq = 0.f;
+  // The normalisation weights do not depend on the row. For narrow rows they
+  // are requested up front; wide rows would need too many registers.
+  constexpr bool kHoist = MAXC <= 2;
+  constexpr int HC = kHoist ? MAXC : 1;
+  float wv[2][HC][V], bv[2][HC][V];
+  auto load_wb = [&](int o, int c, float* w_out, float* b_out) {
+    const T* w = (const T*)(o == 0 ? a.w1 : a.w2);
+    const T* bb = (const T*)(o == 0 ? a.b1 : a.b2);
+    const int ch = lane + 64 * c;
 #pragma unroll
-    for (int c = 0; c < MAXC; ++c)
-      if (lane + 64 * c < nvec)
+    for (int i = 0; i < V; ++i) w_out[i] = b_out[i] = 0.f;
+    load_vec(w + ch * V, w_out);
+    if (bb) load_vec(bb + ch * V, b_out);
+  };
+  if constexpr (kHoist) {
 #pragma unroll
-        for (int i = 0; i < V; ++i) sq += v[c][i] * v[c][i];
-    var = wave_sum_fast(sq) / float(d);
-  } else {
-    mean = wave_sum_fast(sum) / float(d);
+    for (int o = 0; o < 2; ++o)
+#pragma unroll
+      for (int c = 0; c < MAXC; ++c)
+        if ((o == 0 ? a.out1 : a.out2) != nullptr && lane + 64 * c < nvec) load_wb(o, c, wv[o][c], bv[o][c]);
+  }
+  float v[RPW][MAXC][V];
+#pragma unroll
+  for (int q = 0; q < RPW; ++q)
+#pragma unroll
+    for (int c = 0; c < MAXC; ++c) {
+      const int ch = lane + 64 * c;
+      if (ch < nvec) load_vec(src[q] + ch * V, v[q][c]);
+    }
+  float mean[RPW], rstd[RPW];
+#pragma unroll
+  for (int q = 0; q < RPW; ++q) {
+    float m = 0.f;
+    if (!a.rms) {
+      float sum = 0.f;
+#pragma unroll
+      for (int c = 0; c < MAXC; ++c)
+        if (lane + 64 * c < nvec)
+#pragma unroll
+          for (int i = 0; i < V; ++i) sum += v[q][c][i];
+      m = wave_sum_fast(sum) / float(d);
+    }
     float sq = 0.f;
 #pragma unroll
     for (int c = 0; c < MAXC; ++c)
       if (lane + 64 * c < nvec)
 #pragma unroll
         for (int i = 0; i < V; ++i) {
-          float t = v[c][i] - mean;
+          const float t = v[q][c][i] - m;
           sq += t * t;
         }
-    var = wave_sum_fast(sq) / float(d);
+    mean[q] = m;
+    rstd[q] = 1.0f / sqrtf(wave_sum_fast(sq) / float(d) + a.eps);
   }
-  const float rstd = 1.0f / sqrtf(var + a.eps);
+#pragma unroll
   for (int o = 0; o < 2; ++o) {
-    const T* w = (const T*)(o == 0 ? a.w1 : a.w2);
-    const T* bb = (const T*)(o == 0 ? a.b1 : a.b2);
     T* out = (T*)(o == 0 ? a.out1 : a.out2);
     if (!out) continue;
 #pragma unroll
     for (int c = 0; c < MAXC; ++c) {
-      int ch = lane + 64 * c;
-      if (ch < nvec) {
-        float wv[V], bv[V], y[V];
-        load_vec(w + ch * V, wv);
-        if (bb) load_vec(bb + ch * V, bv);
+      const int ch = lane + 64 * c;
+      if (ch >= nvec) continue;
+      float wl[V], bl[V];
+      const float* wc = wl;
+      const float* bc = bl;
+      if constexpr (kHoist) {
+        wc = wv[o][c];
+        bc = bv[o][c];
+      } else {
+        load_wb(o, c, wl, bl);
+      }
 #pragma unroll
-        for (int i = 0; i < V; ++i) y[i] = (v[c][i] - mean) * rstd * wv[i] + (bb ? bv[i] : 0.f);
-        store_vec(out + r * d + ch * V, y);
+      for (int q = 0; q < RPW; ++q) {
+        if (r0 + q >= rows) break;
+        float y[V];
+#pragma unroll
+        for (int i = 0; i < V; ++i) y[i] = (v[q][c][i] - mean[q]) * rstd[q] * wc[i] + bc[i];
+        store_vec(out + (r0 + q) * d + ch * V, y);
       }
     }
   }
@@ -535,13 +569,15 @@ __global__ __launch_bounds__(256) void norm_kernel(NormArgs a) {
 template <typename T>
 static hipError_t launch_norm_t(const NormArgs& a, hipStream_t s) {
   constexpr int V = Elem<T>::kVec;
-  int per_lane = (a.d / V + 63) / 64;
-  unsigned grid = unsigned((int64_t(a.B) * a.kk + 3) / 4);
-  if (per_lane <= 1) norm_kernel<T, 1><<<grid, 256, 0, s>>>(a);
-  else if (per_lane <= 2) norm_kernel<T, 2><<<grid, 256, 0, s>>>(a);
-  else if (per_lane <= 4) norm_kernel<T, 4><<<grid, 256, 0, s>>>(a);
-  else if (per_lane <= 8) norm_kernel<T, 8><<<grid, 256, 0, s>>>(a);
-  else if (per_lane <= 16) norm_kernel<T, 16><<<grid, 256, 0, s>>>(a);
+  const int per_lane = (a.d / V + 63) / 64;
+  const int64_t rows = int64_t(a.B) * a.kk;
+  auto grid = [&](int rpw) { return unsigned((rows + 4 * rpw - 1) / (4 * rpw)); };
+  // one row per wave: more rows per wave cost occupancy and measured slower
+  if (per_lane <= 1) norm_kernel<T, 1, 1><<<grid(1), 256, 0, s>>>(a);
+  else if (per_lane <= 2) norm_kernel<T, 2, 1><<<grid(1), 256, 0, s>>>(a);
+  else if (per_lane <= 4) norm_kernel<T, 4, 1><<<grid(1), 256, 0, s>>>(a);
+  else if (per_lane <= 8) norm_kernel<T, 8, 1><<<grid(1), 256, 0, s>>>(a);
+  else if (per_lane <= 16) norm_kernel<T, 16, 1><<<grid(1), 256, 0, s>>>(a);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }

@@ -4,7 +4,11 @@ on B = 8 sequences of T = 2048 tokens, one stack call with the per-layer k
 that Eqs. 5-8 give for its similarity profile; and one Qwen-0.5B-shaped layer
 (d 896, 14 / 2 heads, SwiGLU 4864) on B = 8, T = 4096.
 
-The oracle needs about 2-5 s per sequence per layer here, so it checks
+The two larger shapes get one layer each: GPT-NeoX-1.4B (d 2048, 16 x 128
+heads, d_ff 8192, B 4, T 2048) at its fixed r = 0.5, and Qwen2.5-7B (d 3584,
+28 / 4 heads of 128, SwiGLU 18944, B 4, T 8192) at r = 0.5.
+
+The oracle needs from 2 s to about a minute per sequence per layer here, so it checks
 sampled (layer, sequence) pairs, teacher-forced with the GPU's indices; the
 rest is covered by properties that hold at any size, for every sequence of
 every layer: router scores within the fp32 bound, the GPU's indices equal to
@@ -57,3 +61,24 @@ def test_qwen05b_layer_full_size(dev):
     x = S.hidden_states(w)
     y, scores, idx = run_layer(dev, w, W, x, k)
     check_layer(w, W, x, y, scores, idx, k, sample=[0, 5])
+
+
+def test_neox14b_layer_full_size(dev):
+    w = S.WORKLOADS["neox14b"]
+    k = P.k_from_retention(w.retention[0], w.seq)
+    announce(f"full-size layer neox14b B={w.batch} T={w.seq} k={k}")
+    W = S.layer_weights(w, 0)
+    x = S.hidden_states(w)
+    y, scores, idx = run_layer(dev, w, W, x, k)
+    check_layer(w, W, x, y, scores, idx, k, sample=[3])
+
+
+def test_qwen7b_layer_full_size(dev):
+    w = S.WORKLOADS["qwen7b"]
+    k = P.k_from_retention(w.target, w.seq)
+    announce(f"full-size layer qwen7b B={w.batch} T={w.seq} k={k}")
+    W = S.layer_weights(w, 0)
+    x = S.hidden_states(w)
+    y, scores, idx = run_layer(dev, w, W, x, k)
+    check_layer(w, W, x, y, scores, idx, k, sample=[1])
+
