@@ -70,6 +70,59 @@ def retention(P, w, calib_s=None):
     return P.retention_from_similarity(s, w.target, w.tau)
 
 
+def streaming_rates(P, C, w, k, dev, weights0, reps=3):
+    """The HBM-bound entry points standalone, against HBM peak: router, Top-K,
+    gather, scatter and the similarity statistic, on one layer's shapes
+    (B, T, d, k). "cold": each launch reads its own input buffer, cycling
+    through copies that together exceed 1 GiB (more than the 256 MB MALL),
+    so reads come from HBM; "hot": every launch on the same buffer."""
+    import torch
+    B, T, d = w.batch, w.seq, w.d_model
+    eb = 4 if w.dtype == "f32" else 2
+    xbytes = B * T * d * eb
+    R = max(4, -(-(1 << 30) // xbytes) + 1)
+    xs = [torch.randn(B, T, d, device=dev).mul_(0.02).to(w.torch_dtype) for _ in range(R)]
+    scs = [torch.randn(B, T, device=dev) for _ in range(R)]
+    idx = torch.stack([torch.sort(torch.randperm(T, device=dev)[:k])[0] for _ in range(B)]).to(torch.int32)
+    delta = torch.randn(B, k, d, device=dev).mul_(0.02).to(w.torch_dtype)
+    gout = torch.empty(B, k, d, device=dev, dtype=w.torch_dtype)
+    scores = torch.empty(B, T, device=dev)
+    idx_out = torch.empty(B, k, dtype=torch.int32, device=dev)
+    accum = torch.zeros(2, dtype=torch.float64, device=dev)
+    simws = torch.empty(max(P.sim_workspace_size(B * T), 256), dtype=torch.uint8, device=dev)
+    W = {key: (v.to(dev) if hasattr(v, "to") else v) for key, v in weights0.items()
+         if key.startswith("router_")}
+    ops = {
+        "router": (lambda i: P.router_score(xs[i], W["router_w1"], W["router_b1"], W["router_w2"],
+                                            float(W["router_b2"]), scores), C.router_bytes(w, B, T)),
+        "topk": (lambda i: P.topk_select(scs[i], k, idx_out), C.topk_bytes(w, B, T, k)),
+        "gather": (lambda i: P.gather_rows(xs[i], idx, gout), 2.0 * eb * B * k * d + 4.0 * B * k),
+        "scatter": (lambda i: P.scatter_residual(xs[i], delta, idx), 3.0 * eb * B * k * d + 4.0 * B * k),
+        "sim": (lambda i: P.sim_stats(xs[i], xs[(i + 1) % R], accum, workspace=simws), C.sim_bytes(w, B, T)),
+    }
+    out = {}
+    for name, (fn, nbytes) in ops.items():
+        res = {"bytes_per_launch": nbytes}
+        for mode in ("cold", "hot"):
+            for i in range(min(R, 4)):
+                fn(i if mode == "cold" else 0)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            n = R * reps
+            torch.cuda.synchronize()
+            e0.record()
+            for i in range(n):
+                fn(i % R if mode == "cold" else 0)
+            e1.record()
+            torch.cuda.synchronize()
+            us = e0.elapsed_time(e1) * 1e3 / n
+            gbs = nbytes / (us * 1e-6) / 1e9
+            res[mode] = {"us": us, "GB/s": gbs, "frac_of_hbm_peak": gbs / PEAK_HBM_GBS}
+        out[name] = res
+    del xs, scs
+    torch.cuda.empty_cache()
+    return out
+
+
 def cpu_baseline(w, ks, layers, min_seconds=10.0):
     """The oracle, as it stands, on whole sequences through `layers` layers.
 
@@ -320,6 +373,10 @@ def main():
         "similarity_measured": s_meas,
         "hip_runtime": torch.version.hip,
     }
+    if not args.only_sparse:
+        kmean = int(round(sum(ks) / len(ks)))
+        log(f"streaming entry points standalone (B={B}, T={T}, k={kmean}), cold and hot inputs")
+        out["streaming_kernels"] = streaming_rates(P, C, w, kmean, dev, S.layer_weights(w, 0))
     if not args.no_cpu_baseline:
         layers_cpu = L if args.cpu_layers is None else min(args.cpu_layers, L)
         log(f"cpu oracle baseline over {layers_cpu} layers of one sequence")

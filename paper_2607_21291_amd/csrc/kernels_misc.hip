@@ -121,16 +121,19 @@ hipError_t launch_sim_stats(int dtype, const void* a, const void* c, int64_t n, 
 // LDS. Within a chunk each lane streams 64 contiguous bytes of its row; the
 // MFMA's k slots are filled in that order and W1 is read in the same order,
 // so the contraction is unchanged.
+constexpr int kRouterWaves = 8;  // waves per 64-token workgroup, each on 1/8 of the columns
+
 template <int DR>
-__global__ __launch_bounds__(256) void router_bf16_kernel(const uint16_t* __restrict__ x, int64_t n, int d,
+__global__ __launch_bounds__(64 * kRouterWaves) void router_bf16_kernel(const uint16_t* __restrict__ x, int64_t n, int d,
                                                           const uint16_t* __restrict__ w1,
                                                           const uint16_t* __restrict__ b1,
                                                           const uint16_t* __restrict__ w2, float b2,
                                                           float* __restrict__ scores) {
   // 64 tokens per workgroup in 4 blocks of 16; wave w takes the 32-wide
-  // column slices w, w + 4, ... of all four blocks, so each W1 fragment it
-  // loads serves 64 tokens (W1 traffic is a quarter of x's at d_r = 32).
-  constexpr int NB = DR / 16, NW = 4, MT = 4;
+  // column slices w, w + NW, ... of all four blocks, so each W1 fragment it
+  // loads serves 64 tokens (W1 traffic is a quarter of x's at d_r = 32), and
+  // the short per-wave loop keeps many loads in flight per CU.
+  constexpr int NB = DR / 16, NW = kRouterWaves, MT = 4;
   __shared__ float part[NW][16 * MT][DR + 1];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int r = lane & 15, g = lane >> 4;
@@ -148,7 +151,7 @@ __global__ __launch_bounds__(256) void router_bf16_kernel(const uint16_t* __rest
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) acc[mt][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
   const bf16x8 zero = {};
-#pragma unroll 3
+#pragma unroll 4
   for (int kc = 32 * w; kc < d; kc += 32 * NW) {
     // d is a multiple of 8, so each lane's 8-element piece is wholly inside or past the end
     const int k0 = kc + 8 * g;
@@ -173,8 +176,9 @@ __global__ __launch_bounds__(256) void router_bf16_kernel(const uint16_t* __rest
 #pragma unroll
       for (int i = 0; i < 4; ++i) part[w][16 * mt + 4 * g + i][16 * nb + r] = acc[mt][nb][i];
   __syncthreads();
-  // thread t: token t / 4, units q DR/4 .. (q + 1) DR/4 - 1 with q = t % 4; the
-  // four partial sums of a token are then added in a fixed order
+  // threads 0..255: token t / 4, units q DR/4 .. (q + 1) DR/4 - 1 with
+  // q = t % 4; the partial sums of a token are then added in a fixed order
+  if (threadIdx.x >= 256) return;
   const int t = threadIdx.x >> 2, q = threadIdx.x & 3;
   float v = 0.f;
 #pragma unroll
@@ -225,10 +229,10 @@ hipError_t launch_router(int dtype, const void* x, int64_t n, int d, int d_r, co
   auto B1 = (const uint16_t*)b1;
   auto W2 = (const uint16_t*)w2;
   switch (d_r) {
-    case 16: router_bf16_kernel<16><<<grid, 256, 0, s>>>(X, n, d, W1, B1, W2, b2, scores); break;
-    case 32: router_bf16_kernel<32><<<grid, 256, 0, s>>>(X, n, d, W1, B1, W2, b2, scores); break;
-    case 48: router_bf16_kernel<48><<<grid, 256, 0, s>>>(X, n, d, W1, B1, W2, b2, scores); break;
-    case 64: router_bf16_kernel<64><<<grid, 256, 0, s>>>(X, n, d, W1, B1, W2, b2, scores); break;
+    case 16: router_bf16_kernel<16><<<grid, 64 * kRouterWaves, 0, s>>>(X, n, d, W1, B1, W2, b2, scores); break;
+    case 32: router_bf16_kernel<32><<<grid, 64 * kRouterWaves, 0, s>>>(X, n, d, W1, B1, W2, b2, scores); break;
+    case 48: router_bf16_kernel<48><<<grid, 64 * kRouterWaves, 0, s>>>(X, n, d, W1, B1, W2, b2, scores); break;
+    case 64: router_bf16_kernel<64><<<grid, 64 * kRouterWaves, 0, s>>>(X, n, d, W1, B1, W2, b2, scores); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
