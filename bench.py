@@ -40,8 +40,8 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 # library's plain copy kernel of known size. It holds only for the workload
 # and the GEMM source it was measured on (SHA-256 of kernels_gemm.hip); for
 # anything else `traffic` is null.
-TRAFFIC_MEASURED = {"workload": "neox160m", "bytes_per_launch": 2.103e+08,
-                    "gemm_source_sha256": "a4434b5d48e22095874b556945c312013c0b1a66b7cf27c8c0488bec32befccd",
+TRAFFIC_MEASURED = {"workload": "neox160m", "bytes_per_launch": 1.489e+08,
+                    "gemm_source_sha256": "acb473846bf63a5548e5fb530a938507692fce9118fb958cafa22f01fe61176e",
                     "profile": "profiles/gemm_down_neox160m.md"}
 
 
