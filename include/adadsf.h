@@ -214,13 +214,14 @@ int dsf_attention_forward(const void* q, const void* k, const void* v, int dtype
  * resets what it uses, so two calls that overlap in time (on different
  * streams) need two workspaces. Returns 0 on a bad argument.
  *
- * Projection schedule. Each bf16 projection GEMM runs either one output tile
- * per workgroup or, when that would end in a short last round of tiles on a
- * long reduction, a stream-K grid (workgroups split the k-iterations of the
- * last tiles and add their partial sums in a fixed order). Both are
- * deterministic; they round differently. The environment variable
- * DSF_GEMM_SCHEDULE=classic or =streamk, read at every launch, forces one of
- * them (testing and tuning). */
+ * Projection schedule. Each bf16 projection GEMM runs one output tile per
+ * workgroup; or, with more tiles than resident workgroups, a persistent grid
+ * taking whole tiles (same arithmetic); or, when that would end in a short
+ * last round of tiles on a long reduction, a stream-K grid (workgroups split
+ * the k-iterations of the last tiles and add their partial sums in a fixed
+ * order, which rounds differently). All are deterministic. The environment
+ * variable DSF_GEMM_SCHEDULE=classic, =persistent or =streamk, read at every
+ * launch, forces one of them (testing and tuning). */
 size_t dsf_workspace_size(const dsf_layer_desc* desc, int dtype, int B, int T, int k_max,
                           int with_similarity);
 

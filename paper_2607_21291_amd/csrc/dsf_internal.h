@@ -96,8 +96,9 @@ struct GemmArgs {
   // zeroed before the first launch using them; epoch is nonzero and distinct
   // for every launch between two zeroings.
   float* part; uint32_t* flags; uint32_t epoch;
-  // set by the launcher: number of M tiles; workgroups per XCD of a stream-K grid
-  int ntm; int px;
+  // set by the launcher: number of M tiles; workgroups per XCD of a persistent
+  // grid (0: one tile per workgroup); 1 if its last round is split along K
+  int ntm; int px; int split;
 };
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t s);
 size_t gemm_partial_bytes();

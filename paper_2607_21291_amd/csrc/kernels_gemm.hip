@@ -488,10 +488,10 @@ struct DmaGemm {
 #pragma unroll
       for (int j = 0; j < NI; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    // Everything this wave issued before (stores of an earlier tile) has
-    // completed, so the counts below cover only the ring's loads; and every
-    // wave is done with the LDS before the ring is refilled.
-    wait_vmcnt<0>();
+    // Every wave is done with the LDS before the ring is refilled. Stores of
+    // an earlier tile may still be in flight: they only add to the counter,
+    // so each wait below still covers the loads it is for (whether or not the
+    // stores retire in order), and they drain under this tile's first loads.
     ring_barrier();
     // Ring of NS buffers, all filled ahead: tile kt lives in buffer kt % NS,
     // and tile kt + NS is issued into it as soon as tile kt has been read.
@@ -701,12 +701,15 @@ __global__ __launch_bounds__((DmaCfg<BM, BN, WM, WN, NS, BK>::kThreads)) void ge
   G::epilogue(g, smem, tm, tn, acc);
 }
 
-// Stream-K schedule (persistent grid of 8 * px workgroups; workgroup w runs
-// on XCD w % 8 as the hardware deals workgroups to the 8 XCDs in turn).
-// The tiles, in row-major order, are cut into 8 contiguous ranges, one per
-// XCD; each XCD's px workgroups then share its range as an independent
-// problem: whole tiles while at least two full rounds remain, then the
-// remaining k-iterations (tiles x K/BK) in px equal contiguous pieces.
+// Persistent grid of 8 * px workgroups (workgroup w runs on XCD w % 8 as the
+// hardware deals workgroups to the 8 XCDs in turn). The tiles, in row-major
+// order, are cut into 8 contiguous ranges, one per XCD, and each XCD's px
+// workgroups share its range as an independent problem. With g.split == 0
+// they take whole tiles only (tile j, j + px, ...): a workgroup moves on to
+// its next tile while its last tile's stores drain. With g.split == 1
+// (stream-K) they take whole tiles while at least two full rounds remain,
+// then the remaining k-iterations (tiles x K/BK) in px equal contiguous
+// pieces.
 // A piece that covers only part of a tile leaves a partial sum: the
 // workgroup holding the tile's last k-iteration finishes it, adding the
 // partials of the lower-numbered workgroups that hold its earlier iterations
@@ -726,7 +729,8 @@ __global__ __launch_bounds__((DmaCfg<BM, BN, WM, WN, NS, BK>::kThreads)) void ge
   const int x = int(blockIdx.x) % kXcds, j = int(blockIdx.x) / kXcds;
   const int t0 = int(int64_t(nt) * x / kXcds), ntx = int(int64_t(nt) * (x + 1) / kXcds) - t0;
   const int full = ntx / px, rem = ntx % px;
-  const int dp = rem == 0 ? ntx : (full >= 1 ? (full - 1) * px : 0);
+  // whole tiles only (g.split == 0), or whole tiles while two or more rounds remain
+  const int dp = (!g.split || rem == 0) ? ntx : (full >= 1 ? (full - 1) * px : 0);
   typename G::Acc acc;
   for (int t = j; t < dp; t += px) {
     const int tile = t0 + t, tm = tile / ntn, tn = tile - tm * ntn;
@@ -884,6 +888,7 @@ static int schedule_override() {
   if (!e) return 0;
   if (!strcmp(e, "classic")) return 1;
   if (!strcmp(e, "streamk")) return 2;
+  if (!strcmp(e, "persistent")) return 3;
   return 0;
 }
 
@@ -905,37 +910,36 @@ static int resident_slots(const void* fn, int threads) {
   return v;
 }
 
-// Workgroups per XCD of a stream-K grid for nt tiles of nk k-iterations, or 0
-// for one tile per workgroup. Stream-K is taken when one tile per workgroup
-// would end in a short last round (at most a quarter of the resident slots
-// busy after at least one full round): then most CUs idle while it runs,
-// whereas a partial first round (fewer tiles than slots) already runs its
-// lone workgroups faster and does not gain from splitting. It is also left
-// out when the pieces would be too short to pay for their partial sums, and
-// for short reductions (fewer than kSkMinK k-iterations per tile), where the
-// extra pipeline starts and the partial hand-over cost more than the idle
-// CUs of the last round (measured on the 768-deep projections of a
-// 768-wide model).
-static int stream_k_px(int nt, int nk, int slots) {
+// Schedule of a launch: px = workgroups per XCD of a persistent grid (0: one
+// tile per workgroup) and split (1: stream-K split of the last round).
+//  - Long reductions (at least kSkMinK k-iterations per tile) whose last
+//    round of tiles would be at most a quarter full: stream-K. Then most CUs
+//    would idle through that round, whereas a partial first round (fewer
+//    tiles than slots) already runs its lone workgroups faster.
+//  - Otherwise one tile per workgroup. For short reductions a persistent
+//    grid over whole tiles (forced with DSF_GEMM_SCHEDULE=persistent) was
+//    6 % faster alone but 10-15 % slower inside the layer stack, and stream-K
+//    pieces cost more than the idle tail saves.
+// Stream-K is also left out when the pieces would be too short to pay for
+// their partial sums.
+struct Schedule {
+  int px, split;
+};
+static Schedule choose_schedule(int nt, int nk, int slots) {
   const int px = slots / kXcds;
-  if (px < 1) return 0;
+  if (px < 1) return {0, 0};
   const int mode = schedule_override();
-  if (mode == 1) return 0;
-  if (mode == 2) return px;
+  if (mode == 1) return {0, 0};
+  if (mode == 2) return {px, 1};
+  if (mode == 3) return {px, 0};
   const int64_t P = int64_t(px) * kXcds;
   const int64_t last = nt % P;
-  if (nk < kSkMinK || nt <= P || last == 0 || 4 * last > P) return 0;
-  if (int64_t(nt) * nk < P * kSkMinIters) return 0;
-  return px;
-}
-
-// Launch kern<<<grid, block>>>(g), through hipExtLaunchKernelGGL when an
-// enclosing timing scope hands over its events.
-template <typename K>
-static void launch_timed(K kern, dim3 grid, dim3 block, hipStream_t s, const GemmArgs& g) {
-  hipEvent_t e0, e1;
-  if (timing_claim(&e0, &e1)) hipExtLaunchKernelGGL(kern, grid, block, 0, s, e0, e1, 0, g);
-  else kern<<<grid, block, 0, s>>>(g);
+  if (nk >= kSkMinK) {
+    if (nt <= P || last == 0 || 4 * last > P) return {0, 0};
+    if (int64_t(nt) * nk < P * kSkMinIters) return {0, 0};
+    return {px, 1};
+  }
+  return {0, 0};
 }
 
 // The DMA kernels address each operand through a buffer resource with a
@@ -946,6 +950,15 @@ static bool dma_addressable(const GemmArgs& g, int rows_b) {
   const int64_t mp = int64_t(g.M + DSF_GEMM_BM), np = int64_t(rows_b + DSF_GEMM_BN);
   return mp * g.lda * 2 < lim && (!g.a2 || mp * g.lda2 * 2 < lim) && np * g.ldb * 2 < lim &&
          (!g.b2 || np * g.ldb2 * 2 < lim);
+}
+
+// Launch kern<<<grid, block>>>(g), through hipExtLaunchKernelGGL when an
+// enclosing timing scope hands over its events.
+template <typename K>
+static void launch_timed(K kern, dim3 grid, dim3 block, hipStream_t s, const GemmArgs& g) {
+  hipEvent_t e0, e1;
+  if (timing_claim(&e0, &e1)) hipExtLaunchKernelGGL(kern, grid, block, 0, s, e0, e1, 0, g);
+  else kern<<<grid, block, 0, s>>>(g);
 }
 
 template <int EPI>
@@ -961,8 +974,10 @@ static void launch_gemm_t(const GemmArgs& g, hipStream_t s) {
     ga.px = 0;
     if (g.part && g.flags) {
       auto fn = gemm_bf16_sk_kernel<EPI, BM, BN, WM, WN, NS, BK>;
-      ga.px = stream_k_px(ntn * ga.ntm, g.K / BK,
-                          resident_slots<std::integral_constant<int, EPI>>((const void*)fn, Cfg::kThreads));
+      const Schedule sch = choose_schedule(ntn * ga.ntm, g.K / BK,
+                                           resident_slots<std::integral_constant<int, EPI>>((const void*)fn, Cfg::kThreads));
+      ga.px = sch.px;
+      ga.split = sch.split;
       if (ga.px > 0) {
         launch_timed(fn, dim3(ga.px * kXcds), dim3(Cfg::kThreads), s, ga);
         return;

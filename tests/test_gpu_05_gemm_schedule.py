@@ -1,13 +1,15 @@
-"""The two schedules of the bf16 projection GEMMs give the layer the oracle
-computes: one tile per workgroup, and stream-K (a persistent grid whose
-workgroups split the k-iterations of the last tiles and add partial sums in
-a fixed order). DSF_GEMM_SCHEDULE forces one of them; on these small shapes
-the forced stream-K grid leaves most workgroups a short or empty piece, so
-the partial-sum paths (many contributors per tile, empty pieces) all run.
+"""The schedules of the bf16 projection GEMMs give the layer the oracle
+computes: one tile per workgroup; a persistent grid taking whole tiles; and
+stream-K (a persistent grid whose workgroups split the k-iterations of the
+last tiles and add partial sums in a fixed order). DSF_GEMM_SCHEDULE forces
+one of them. On these small shapes the forced persistent grids leave most
+workgroups no tile or a short or empty piece, so those paths all run, as do
+the partial sums with many contributors per tile.
 
 Stream-K adds the partials in an order fixed by the shape, so repeated runs
-are bitwise equal; the two schedules round differently, and each is held to
-the oracle at the bf16 tolerance.
+are bitwise equal. Whole tiles round exactly as one tile per workgroup. The
+split schedule rounds differently, and every schedule is held to the oracle
+at the bf16 tolerance.
 """
 import pytest
 import torch
@@ -23,13 +25,14 @@ CASES = [("neox_bf16_small", 150), ("qwen_bf16_small", 299), ("neox_bf16_hd128",
          ("neox_bf16_small", 1)]
 
 
+@pytest.mark.parametrize("schedule", ["streamk", "persistent"])
 @pytest.mark.parametrize("name,k", CASES)
-def test_stream_k_layer_matches_oracle(dev, monkeypatch, name, k):
+def test_persistent_schedules_match_oracle(dev, monkeypatch, name, k, schedule):
     w = workload(name)
     W = S.layer_weights(w, 0)
     x = S.hidden_states(w)
-    monkeypatch.setenv("DSF_GEMM_SCHEDULE", "streamk")
-    announce(f"stream-K layer {name} k={k}")
+    monkeypatch.setenv("DSF_GEMM_SCHEDULE", schedule)
+    announce(f"{schedule} layer {name} k={k}")
     y, scores, idx = run_layer(dev, w, W, x, k)
     check_layer(w, W, x, y, scores, idx, k)
     y2, _, _ = run_layer(dev, w, W, x, k)
@@ -38,14 +41,17 @@ def test_stream_k_layer_matches_oracle(dev, monkeypatch, name, k):
     announce(f"classic layer {name} k={k}")
     yc, _, idxc = run_layer(dev, w, W, x, k)
     assert torch.equal(idx, idxc)
+    if schedule == "persistent":
+        assert torch.equal(y, yc)  # whole tiles: the same arithmetic as one tile per workgroup
     assert rel_inf(to_np(y) - to_np(x), to_np(yc) - to_np(x)) < TOL[w.dtype]
 
 
+@pytest.mark.parametrize("schedule", ["streamk", "persistent"])
 @pytest.mark.parametrize("name", ["neox_bf16_small", "qwen_bf16_small"])
-def test_stream_k_stack_matches_layerwise(dev, monkeypatch, name):
+def test_persistent_stack_matches_layerwise(dev, monkeypatch, name, schedule):
     w = workload(name).replace(n_layers=3)
-    monkeypatch.setenv("DSF_GEMM_SCHEDULE", "streamk")
-    announce(f"stream-K stack {name}")
+    monkeypatch.setenv("DSF_GEMM_SCHEDULE", schedule)
+    announce(f"{schedule} stack {name}")
     Ws = S.stack_weights(w)
     x = S.hidden_states(w)
     T = w.seq
@@ -63,8 +69,8 @@ def test_stream_k_stack_matches_layerwise(dev, monkeypatch, name):
 
 
 def test_full_size_schedules_agree(dev, monkeypatch):
-    # the down projection of the first neox160m layer (M = 8 x 1563 rows,
-    # 588 tiles) is where the automatic choice takes stream-K
+    # in the first neox160m layer (M = 8 x 1563 rows) the automatic choice
+    # takes stream-K for the down projection (588 tiles)
     w = S.WORKLOADS["neox160m"]
     W = S.layer_weights(w, 0)
     x = S.hidden_states(w)
