@@ -354,11 +354,14 @@ def block_delta(desc: Dict, W: Dict, xc, pos) -> np.ndarray:
 # ---------------------------------------------------------------------------
 
 def routed_layer(desc: Dict, W: Dict, x, k: int, idx=None,
-                 out_dtype: Optional[str] = None) -> Dict[str, np.ndarray]:
+                 out_dtype: Optional[str] = None, gate: bool = False) -> Dict[str, np.ndarray]:
     """One sparse layer. Returns y, scores, idx and delta (kept rows, [B, k, d]).
 
     idx given: teacher-forced selection (the router still scores every token).
     out_dtype given: the kept rows of y are rounded to that storage format.
+    gate: the block's update of a kept token is scaled by sigmoid(score), the
+    router-score pathway kept differentiable in training (Section 3.4,
+    MoD-style); `delta` is then the ungated update.
     """
     x = f64(x)
     B, T, _ = x.shape
@@ -370,7 +373,11 @@ def routed_layer(desc: Dict, W: Dict, x, k: int, idx=None,
     xc = gather_rows(x, idx)
     delta = np.stack([block_delta(desc, W, xc[b], idx[b]) for b in range(B)]) if k > 0 \
         else np.zeros((B, 0, x.shape[2]))
-    y = scatter_residual(x, delta, idx, out_dtype)
+    if gate:
+        g = sigmoid(np.stack([scores[b, idx[b]] for b in range(B)]))
+        y = scatter_residual(x, g[..., None] * delta, idx, out_dtype)
+    else:
+        y = scatter_residual(x, delta, idx, out_dtype)
     return {"y": y, "scores": scores, "idx": idx, "delta": delta}
 
 
@@ -407,3 +414,54 @@ def calibrate_similarity(desc: Dict, Ws: List[Dict], x) -> np.ndarray:
         s.append(layer_similarity(tot, n))
         x = y
     return np.asarray(s)
+
+
+# ---------------------------------------------------------------------------
+# Section 3.4, training side: gradients along the router-score pathway
+# ---------------------------------------------------------------------------
+
+def sigmoid(v) -> np.ndarray:
+    """Logistic function 1 / (1 + e^-v)."""
+    v = f64(v)
+    return 1.0 / (1.0 + np.exp(-v))
+
+
+def gate_score_grad(dy, x_in, x_out, scores, idx) -> np.ndarray:
+    """dL/ds for every token of a gated routed layer (routed_layer(gate=True)).
+
+    dy: gradient of the loss with respect to the layer output, [B, T, d];
+    x_in, x_out: the layer's input and output; scores [B, T]; idx [B, k].
+    A kept token p has y_p = x_p + sigmoid(s_p) delta_p, so
+    dL/ds_p = sigmoid'(s_p) <dy_p, delta_p> = (1 - sigmoid(s_p)) <dy_p, y_p - x_p>.
+    The selection itself is piecewise constant in the scores: skipped tokens
+    get 0. Returns [B, T].
+    """
+    dy, x_in, x_out, sc = f64(dy), f64(x_in), f64(x_out), f64(scores)
+    idx = np.asarray(idx)
+    out = np.zeros(sc.shape)
+    for b in range(sc.shape[0]):
+        p = idx[b]
+        out[b, p] = (1.0 - sigmoid(sc[b, p])) * np.sum(dy[b, p] * (x_out[b, p] - x_in[b, p]), axis=-1)
+    return out
+
+
+def router_backward(x, w1, b1, w2, dscore) -> Dict[str, np.ndarray]:
+    """Gradients through score = w2 . ReLU(W1 x + b1) + b2 given dL/dscore.
+
+    x: [..., d] tokens, dscore: [...] (same leading shape). Returns dw1 [d_r, d],
+    db1 [d_r], dw2 [d_r], db2 (scalar) and dx [..., d] (the router's share of
+    the input gradient). The ReLU's derivative at 0 is taken as 0.
+    """
+    x = f64(x)
+    d = x.shape[-1]
+    xt = x.reshape(-1, d)
+    ds = f64(dscore).reshape(-1)
+    w1, w2 = f64(w1), f64(w2)
+    z = xt @ w1.T
+    if b1 is not None:
+        z = z + f64(b1)
+    h = np.maximum(z, 0.0)
+    dz = ds[:, None] * w2[None, :] * (z > 0.0)
+    return {"dw1": dz.T @ xt, "db1": dz.sum(axis=0), "dw2": h.T @ ds, "db2": float(ds.sum()),
+            "dx": (dz @ w1).reshape(x.shape)}
+
