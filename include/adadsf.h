@@ -72,7 +72,14 @@ enum { DSF_F32 = 0, DSF_BF16 = 1 };
 enum { DSF_BLOCK_NEOX_PARALLEL = 0, DSF_BLOCK_QWEN_SEQ = 1 };
 
 /* flags */
-enum { DSF_FLAG_DENSE = 1 }; /* run the unmodified layer on every token (no router, no Top-K) */
+enum {
+  DSF_FLAG_DENSE = 1, /* run the unmodified layer on every token (no router, no Top-K) */
+  /* Score-gated update, the training-side router-score pathway of Section
+   * 3.4: a kept row becomes x + sigmoid(score) * delta instead of x + delta,
+   * so that the loss depends on the router scores differentiably (see
+   * dsf_gate_score_grad). Skipped rows are unchanged. Not with DSF_FLAG_DENSE. */
+  DSF_FLAG_GATE = 2
+};
 
 /* clip modes for dsf_retention_from_similarity */
 enum { DSF_CLIP_NONE = 0, DSF_CLIP_PLAIN = 1, DSF_CLIP_BUDGET = 2 };
@@ -175,6 +182,43 @@ int dsf_router_score(const void* x, int dtype, int64_t n_tokens, int d, int d_r,
                      const void* w1, const void* b1, const void* w2, float b2,
                      float* scores, hipStream_t stream);
 
+/* Gradient of a loss L with respect to the router scores through the
+ * score-gated update (DSF_FLAG_GATE, Section 3.4). A kept row is
+ * y = x + sigmoid(s) delta, so dL/ds = sigmoid'(s) <dy, delta>, which equals
+ * (1 - sigmoid(s)) <dy, y - x>; skipped rows do not depend on s.
+ *   dscore[b, t] = (1 - sigmoid(scores[b, t])) * sum_c dy[b, t, c] (x_out - x_in)[b, t, c]
+ *                  for t in idx[b, :], and 0 for every other position.
+ * dy, x_in (the layer input), x_out (the gated layer output): device [B, T, d]
+ * in dtype, 16-byte aligned; scores: device float [B, T] (the scores the
+ * layer used); idx: device int32 [B, k] (the kept positions, distinct per
+ * sequence; entries outside [0, T) are ignored); dscore: device float
+ * [B, T], fully overwritten. Products and the sum are in fp32. */
+int dsf_gate_score_grad(const void* dy, const void* x_in, const void* x_out, int dtype,
+                        const float* scores, const int32_t* idx, int B, int T, int k, int d,
+                        float* dscore, hipStream_t stream);
+
+/* Workspace bytes of dsf_router_backward (0 on a bad argument). */
+size_t dsf_router_backward_workspace_size(int64_t n_tokens, int d, int d_r);
+
+/* Backward of the router MLP (Section 3.4) given dscore = dL/dscore per token:
+ * with z = W1 x + b1,
+ *   dz = dscore * w2 * [z > 0],  dW1 = sum_t dz_t x_t^T,  db1 = sum_t dz_t,
+ *   dw2 = sum_t dscore_t ReLU(z_t),  db2 = sum_t dscore_t,  dx_t += W1^T dz_t.
+ * z is recomputed with the arithmetic of dsf_router_score, so the ReLU
+ * decisions are those of the forward call. x [n_tokens, d], W1 [d_r, d], b1
+ * [d_r] (nullable), w2 [d_r] in dtype; dscore device float [n_tokens]. The
+ * weight gradients are device float: dW1 [d_r, d], db1 [d_r] (nullable; 0 is
+ * not written when b1 is absent), dw2 [d_r], db2 [1], all overwritten. dx
+ * (nullable) is device [n_tokens, d] in dtype and ACCUMULATED into (the
+ * router's share of the input gradient is added, in fp32, then rounded once).
+ * Sums run in an order fixed by the shape: repeated calls give identical bits.
+ * The workspace (dsf_router_backward_workspace_size bytes, 256-byte aligned)
+ * needs no initialisation; calls that overlap in time need separate ones. */
+int dsf_router_backward(const void* x, int dtype, int64_t n_tokens, int d, int d_r,
+                        const void* w1, const void* b1, const void* w2, const float* dscore,
+                        float* dw1, float* db1, float* dw2, float* db2, void* dx,
+                        void* workspace, size_t workspace_bytes, hipStream_t stream);
+
 /* Top-K_i per sequence. For each of the B sequences of T float scores,
  * writes the k positions with the largest scores to idx[b, 0..k) in ascending
  * position order. A larger score is preferred; equal scores prefer the lower
@@ -231,7 +275,8 @@ size_t dsf_workspace_size(const dsf_layer_desc* desc, int dtype, int B, int T, i
  *   3. the block of Eqs. 1-2 runs on the kept rows only, at their original
  *      positions (RoPE angle uses idx), with kept tokens attending causally to
  *      kept tokens;
- *   4. x[b, idx[b, j]] = x[b, idx[b, j]] + delta[b, j]; skipped rows unchanged.
+ *   4. x[b, idx[b, j]] = x[b, idx[b, j]] + delta[b, j] (with DSF_FLAG_GATE
+ *      + sigmoid(scores[b, idx[b, j]]) delta[b, j]); skipped rows unchanged.
  * k in [0, T]; k == 0 leaves x untouched and launches nothing. With
  * DSF_FLAG_DENSE, k must equal T and every token is processed at positions
  * 0..T-1 (the unmodified layer). scores_out (device float [B, T]) and idx_out
@@ -267,7 +312,7 @@ enum {
   DSF_KIND_SIM = 0, DSF_KIND_ROUTER = 1, DSF_KIND_TOPK = 2, DSF_KIND_NORM = 3,
   DSF_KIND_GEMM_QKV = 4, DSF_KIND_ATTN = 5, DSF_KIND_GEMM_O = 6, DSF_KIND_GEMM_UP = 7,
   DSF_KIND_GEMM_DOWN = 8, DSF_KIND_GATHER = 9, DSF_KIND_SCATTER = 10, DSF_KIND_OTHER = 11,
-  DSF_KIND_COUNT = 12
+  DSF_KIND_BACKWARD = 12, DSF_KIND_COUNT = 13
 };
 int dsf_timing_enable(int max_records, uint32_t kind_mask);
 int dsf_timing_read(int kind, int* launches, double* total_ms);

@@ -18,11 +18,11 @@ LIB_PATH = os.path.join(_HERE, "libadadsf.so")
 
 F32, BF16 = 0, 1
 BLOCK_NEOX_PARALLEL, BLOCK_QWEN_SEQ = 0, 1
-FLAG_DENSE = 1
+FLAG_DENSE, FLAG_GATE = 1, 2
 CLIP = {"none": 0, "plain": 1, "budget": 2}
 ROUNDING = {"floor": 0, "ceil": 1}
 KINDS = ["sim", "router", "topk", "norm", "gemm_qkv", "attn", "gemm_o", "gemm_up", "gemm_down",
-         "gather", "scatter", "other"]
+         "gather", "scatter", "other", "backward"]
 
 STATUS = {0: "DSF_OK", 1: "DSF_EINVAL", 2: "DSF_EUNSUPPORTED", 3: "DSF_EWORKSPACE", 4: "DSF_EHIP",
           5: "DSF_ENODEVICE"}
@@ -32,6 +32,7 @@ EXPORTS = [
     "dsf_retention_from_similarity", "dsf_k_from_retention", "dsf_router_score", "dsf_topk_select",
     "dsf_gather_rows", "dsf_scatter_residual", "dsf_attention_forward", "dsf_workspace_size",
     "dsf_sparse_block_forward", "dsf_stack_forward", "dsf_timing_enable", "dsf_timing_read",
+    "dsf_gate_score_grad", "dsf_router_backward_workspace_size", "dsf_router_backward",
 ]
 
 
@@ -89,6 +90,9 @@ def lib() -> ctypes.CDLL:
         "dsf_stack_forward": ([vp, vp, i32, i32, vp, vp, i32, i32, i32, vp, vp, sz, vp], i32),
         "dsf_timing_enable": ([i32, ctypes.c_uint32], i32),
         "dsf_timing_read": ([i32, vp, vp], i32),
+        "dsf_gate_score_grad": ([vp, vp, vp, i32, vp, vp, i32, i32, i32, i32, vp, vp], i32),
+        "dsf_router_backward_workspace_size": ([i64, i32, i32], sz),
+        "dsf_router_backward": ([vp, i32, i64, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp], i32),
     }
     for name, (args, res) in sig.items():
         fn = getattr(L, name)
@@ -179,6 +183,30 @@ def router_score(x, w1, b1, w2, b2: float, scores, stream=None):
     _check("dsf_router_score", lib().dsf_router_score(_ptr(x), _dtype_code(x), x.numel() // d, d, w1.shape[0],
                                                       _ptr(w1), _ptr(b1), _ptr(w2), float(b2), _ptr(scores),
                                                       _stream(stream)))
+
+
+def gate_score_grad(dy, x_in, x_out, scores, idx, dscore, stream=None):
+    B, T, d = dy.shape
+    _check("dsf_gate_score_grad",
+           lib().dsf_gate_score_grad(_ptr(dy), _ptr(x_in), _ptr(x_out), _dtype_code(dy), _ptr(scores), _ptr(idx),
+                                     B, T, idx.shape[1], d, _ptr(dscore), _stream(stream)))
+
+
+def router_backward_workspace_size(n_tokens: int, d: int, d_r: int) -> int:
+    return lib().dsf_router_backward_workspace_size(n_tokens, d, d_r)
+
+
+def router_backward(x, w1, b1, w2, dscore, dw1, db1, dw2, db2, dx=None, workspace=None, stream=None):
+    d = x.shape[-1]
+    n = x.numel() // d
+    d_r = w1.shape[0]
+    if workspace is None:
+        workspace = torch.empty(max(router_backward_workspace_size(n, d, d_r), 256), dtype=torch.uint8,
+                                device=x.device)
+    _check("dsf_router_backward",
+           lib().dsf_router_backward(_ptr(x), _dtype_code(x), n, d, d_r, _ptr(w1), _ptr(b1), _ptr(w2), _ptr(dscore),
+                                     _ptr(dw1), _ptr(db1), _ptr(dw2), _ptr(db2), _ptr(dx), _ptr(workspace),
+                                     workspace.numel(), _stream(stream)))
 
 
 def topk_select(scores, k: int, idx, stream=None):

@@ -293,6 +293,79 @@ extern "C" int dsf_router_score(const void* x, int dtype, int64_t n_tokens, int 
   return DSF_OK;
 }
 
+// ------------------------------------------- router-score pathway (training)
+
+extern "C" int dsf_gate_score_grad(const void* dy, const void* x_in, const void* x_out, int dtype,
+                                   const float* scores, const int32_t* idx, int B, int T, int k, int d,
+                                   float* dscore, hipStream_t stream) {
+  int rc = check_dtype(dtype);
+  if (rc) return rc;
+  DSF_CHECK(B >= 0 && T >= 0, DSF_EINVAL, "B and T must be >= 0");
+  DSF_CHECK(int64_t(B) * T < (int64_t(1) << 31), DSF_EINVAL, "B * T too large");
+  DSF_CHECK(k >= 0 && k <= T, DSF_EINVAL, "k=%d outside [0, T=%d]", k, T);
+  DSF_CHECK(d > 0 && d % 8 == 0, DSF_EUNSUPPORTED, "d must be a positive multiple of 8");
+  if (B == 0 || T == 0) return DSF_OK;
+  DSF_CHECK(dscore, DSF_EINVAL, "dscore is null");
+  if (k > 0) {
+    DSF_CHECK(dy && x_in && x_out && scores && idx, DSF_EINVAL, "null pointer");
+    DSF_CHECK(aligned16(dy) && aligned16(x_in) && aligned16(x_out), DSF_EINVAL,
+              "dy, x_in and x_out must be 16-byte aligned");
+  }
+  rc = check_device();
+  if (rc) return rc;
+  DSF_HIP(launch_gate_grad(dtype, dy, x_in, x_out, scores, idx, B, T, k, d, dscore, stream));
+  return DSF_OK;
+}
+
+static bool router_width_ok(int d_r) { return d_r == 16 || d_r == 32 || d_r == 48 || d_r == 64; }
+
+extern "C" size_t dsf_router_backward_workspace_size(int64_t n_tokens, int d, int d_r) {
+  if (n_tokens < 0 || n_tokens >= (int64_t(1) << 31) || d <= 0 || d % 8 != 0 || !router_width_ok(d_r)) return 0;
+  return router_bwd_workspace_bytes(n_tokens, d, d_r);
+}
+
+extern "C" int dsf_router_backward(const void* x, int dtype, int64_t n_tokens, int d, int d_r, const void* w1,
+                                   const void* b1, const void* w2, const float* dscore, float* dw1, float* db1,
+                                   float* dw2, float* db2, void* dx, void* workspace, size_t workspace_bytes,
+                                   hipStream_t stream) {
+  int rc = check_dtype(dtype);
+  if (rc) return rc;
+  DSF_CHECK(n_tokens >= 0 && n_tokens < (int64_t(1) << 31), DSF_EINVAL, "bad n_tokens");
+  DSF_CHECK(d > 0 && d % 8 == 0, DSF_EUNSUPPORTED, "d must be a positive multiple of 8");
+  DSF_CHECK(router_width_ok(d_r), DSF_EUNSUPPORTED, "d_r must be 16, 32, 48 or 64");
+  DSF_CHECK(w1 && w2 && dw1 && dw2 && db2, DSF_EINVAL, "null pointer");
+  DSF_CHECK(!db1 || b1, DSF_EINVAL, "db1 needs b1");
+  if (n_tokens > 0) {
+    DSF_CHECK(x && dscore, DSF_EINVAL, "null pointer");
+    DSF_CHECK(aligned16(x) && aligned16(w1) && (!dx || aligned16(dx)), DSF_EINVAL,
+              "x, W1 and dx must be 16-byte aligned");
+    const size_t need = router_bwd_workspace_bytes(n_tokens, d, d_r);
+    DSF_CHECK(workspace_bytes >= need, DSF_EWORKSPACE, "workspace needs %zu bytes, got %zu", need,
+              workspace_bytes);
+    DSF_CHECK(workspace && (reinterpret_cast<uintptr_t>(workspace) & 255u) == 0, DSF_EINVAL,
+              "workspace must be non-null and 256-byte aligned");
+  }
+  rc = check_device();
+  if (rc) return rc;
+  if (n_tokens == 0) {  // empty sums: every gradient is zero
+    DSF_HIP(launch_zero_u32(reinterpret_cast<uint32_t*>(dw1), int64_t(d_r) * d, stream));
+    if (db1) DSF_HIP(launch_zero_u32(reinterpret_cast<uint32_t*>(db1), d_r, stream));
+    DSF_HIP(launch_zero_u32(reinterpret_cast<uint32_t*>(dw2), d_r, stream));
+    DSF_HIP(launch_zero_u32(reinterpret_cast<uint32_t*>(db2), 1, stream));
+    return DSF_OK;
+  }
+  RouterBwdArgs a{};
+  a.dtype = dtype;
+  a.x = x; a.n = n_tokens; a.d = d; a.d_r = d_r;
+  a.w1 = w1; a.b1 = b1; a.w2 = w2;
+  a.dscore = dscore;
+  a.dw1 = dw1; a.db1 = db1; a.dw2 = dw2; a.db2 = db2;
+  a.dx = dx;
+  a.workspace = workspace;
+  DSF_HIP(launch_router_backward(a, stream));
+  return DSF_OK;
+}
+
 extern "C" int dsf_topk_select(const float* scores, int B, int T, int k, int32_t* idx, hipStream_t stream) {
   DSF_CHECK(B >= 0 && T >= 0, DSF_EINVAL, "B and T must be >= 0");
   DSF_CHECK(k >= 0 && k <= T, DSF_EINVAL, "k=%d outside [0, T=%d]", k, T);
@@ -476,15 +549,16 @@ P* at(const Ctx& c, size_t off) {
 }
 
 // Enqueue one layer. k > 0. dense: every token at positions 0..T-1.
-int run_layer(const Ctx& c, const dsf_layer_weights* W, void* x, int k, bool dense, float* scores_out,
+int run_layer(const Ctx& c, const dsf_layer_weights* W, void* x, int k, bool dense, bool gate, float* scores_out,
               int32_t* idx_out, const int32_t* idx_in) {
   const dsf_layer_desc& D = *c.D;
   const int B = c.B, T = c.T, d = D.d_model;
   const int hd = D.head_dim, Hq = D.n_heads, Hkv = D.n_kv_heads, f = D.d_ff;
   const bool qwen = D.block == DSF_BLOCK_QWEN_SEQ;
   const int32_t* idx = nullptr;
+  float* scores = nullptr;
   if (!dense) {
-    float* scores = scores_out ? scores_out : at<float>(c, c.plan.scores);
+    scores = scores_out ? scores_out : at<float>(c, c.plan.scores);
     DSF_HIP(launch_router(c.dtype, x, int64_t(B) * T, d, D.d_router, W->router_w1, W->router_b1, W->router_w2,
                           W->router_b2, scores, c.s));
     if (idx_in) {
@@ -561,8 +635,8 @@ int run_layer(const Ctx& c, const dsf_layer_weights* W, void* x, int k, bool den
       o.a2 = at<char>(c, c.plan.act); o.lda2 = f;
       o.b = W->w_o; o.ldb = dq;
       o.b2 = W->w_down; o.ldb2 = f;
-      o.epi = EPI_RESID_SCATTER; o.bias = W->b_o; o.bias2 = W->b_down;
-      o.x = x;
+      o.epi = gate ? EPI_RESID_SCATTER_GATE : EPI_RESID_SCATTER; o.bias = W->b_o; o.bias2 = W->b_down;
+      o.x = x; o.gate = scores;
       TimedScope ts(DSF_KIND_GEMM_DOWN, c.s, true);
       use_stream_k(c, o);
       DSF_HIP(launch_gemm(o, c.s));
@@ -608,8 +682,8 @@ int run_layer(const Ctx& c, const dsf_layer_weights* W, void* x, int k, bool den
     o.M = M; o.N = d; o.K = f; o.K1 = f;
     o.a = at<char>(c, c.plan.act); o.lda = f;
     o.b = W->w_down; o.ldb = f;
-    o.epi = EPI_RESID_SCATTER; o.bias = W->b_down;
-    o.x = x; o.res = at<char>(c, c.plan.h);
+    o.epi = gate ? EPI_RESID_SCATTER_GATE : EPI_RESID_SCATTER; o.bias = W->b_down;
+    o.x = x; o.res = at<char>(c, c.plan.h); o.gate = scores;
     TimedScope ts(DSF_KIND_GEMM_DOWN, c.s, true);
     use_stream_k(c, o);
     DSF_HIP(launch_gemm(o, c.s));
@@ -625,7 +699,9 @@ int check_common(const dsf_layer_desc* desc, int dtype, void* x, int B, int T, i
   if (rc) return rc;
   DSF_CHECK(B >= 0 && T >= 0, DSF_EINVAL, "B and T must be >= 0");
   DSF_CHECK(int64_t(B) * T < (int64_t(1) << 31) / 8, DSF_EINVAL, "B * T too large");
-  DSF_CHECK((flags & ~DSF_FLAG_DENSE) == 0, DSF_EINVAL, "unknown flag bits 0x%x", flags);
+  DSF_CHECK((flags & ~(DSF_FLAG_DENSE | DSF_FLAG_GATE)) == 0, DSF_EINVAL, "unknown flag bits 0x%x", flags);
+  DSF_CHECK((flags & (DSF_FLAG_DENSE | DSF_FLAG_GATE)) != (DSF_FLAG_DENSE | DSF_FLAG_GATE), DSF_EINVAL,
+            "DSF_FLAG_GATE needs router scores: it cannot be combined with DSF_FLAG_DENSE");
   if (B == 0 || T == 0 || k_max == 0) return DSF_OK;
   DSF_CHECK(x, DSF_EINVAL, "x is null");
   DSF_CHECK(aligned16(x), DSF_EINVAL, "x must be 16-byte aligned");
@@ -658,7 +734,7 @@ extern "C" int dsf_sparse_block_forward(const dsf_layer_desc* desc, const dsf_la
   rc = reset_stream_k(c);
   if (rc) return rc;
   DSF_HIP(launch_rope_table(at<float>(c, plan.rope), T, desc->rotary_dims, desc->rope_theta, stream));
-  return run_layer(c, weights, x, k, dense, scores_out, idx_out, idx_in);
+  return run_layer(c, weights, x, k, dense, (flags & DSF_FLAG_GATE) != 0, scores_out, idx_out, idx_in);
 }
 
 extern "C" int dsf_stack_forward(const dsf_layer_desc* desc, const dsf_layer_weights* weights, int L, int dtype,
@@ -693,7 +769,7 @@ extern "C" int dsf_stack_forward(const dsf_layer_desc* desc, const dsf_layer_wei
   for (int l = 0; l < L; ++l) {
     if (with_sim) DSF_HIP(launch_copy(x, at<char>(c, plan.xin), xbytes, stream));
     if (k[l] > 0) {
-      rc = run_layer(c, &weights[l], x, k[l], dense, nullptr, nullptr, nullptr);
+      rc = run_layer(c, &weights[l], x, k[l], dense, (flags & DSF_FLAG_GATE) != 0, nullptr, nullptr, nullptr);
       if (rc) return rc;
     }
     if (with_sim)

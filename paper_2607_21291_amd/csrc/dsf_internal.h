@@ -26,14 +26,30 @@ struct TimedScope {
   ~TimedScope() { timing_end(kind, s); }
 };
 
+// ---- router forward and backward (kernels_router.hip) ----
+hipError_t launch_router(int dtype, const void* x, int64_t n, int d, int d_r, const void* w1,
+                         const void* b1, const void* w2, float b2, float* scores, hipStream_t s);
+// dscore[B, T] = 0, then at kept positions (1 - sigmoid(s)) <dy, x_out - x_in>
+hipError_t launch_gate_grad(int dtype, const void* dy, const void* x_in, const void* x_out, const float* scores,
+                            const int32_t* idx, int B, int T, int k, int d, float* dscore, hipStream_t s);
+struct RouterBwdArgs {
+  int dtype;
+  const void* x; int64_t n; int d; int d_r;
+  const void* w1; const void* b1; const void* w2;
+  const float* dscore;
+  float* dw1; float* db1; float* dw2; float* db2;  // db1 nullable
+  void* dx;                                        // nullable; accumulated into
+  void* workspace;                                 // router_bwd_workspace_bytes(n, d, d_r)
+};
+size_t router_bwd_workspace_bytes(int64_t n, int d, int d_r);
+hipError_t launch_router_backward(const RouterBwdArgs& a, hipStream_t s);
+
 // ---- streaming kernels (kernels_misc.hip) ----
 // table[p][i] = (cos, sin)(p * theta^(-2i/R)), p < T, i < R/2, computed in fp64.
 hipError_t launch_rope_table(float* table, int T, int R, double theta, hipStream_t s);
 int sim_grid(int64_t n_tokens);
 hipError_t launch_sim_stats(int dtype, const void* a, const void* c, int64_t n, int d, float* per_tok,
                             double* partial, double* accum, hipStream_t s);
-hipError_t launch_router(int dtype, const void* x, int64_t n, int d, int d_r, const void* w1,
-                         const void* b1, const void* w2, float b2, float* scores, hipStream_t s);
 hipError_t launch_topk(const float* scores, int B, int T, int k, int32_t* idx, hipStream_t s);
 hipError_t launch_gather(int dtype, const void* x, int B, int T, int d, const int32_t* idx, int k,
                          void* out, hipStream_t s);
@@ -70,6 +86,7 @@ enum EpiKind {
   EPI_SWIGLU = 2,     // B rows interleaved gate/up; out[m, n] = silu(gate) * up, N = f
   EPI_RESID_STORE = 3,    // out[m, n] = x[b, pos, n] + C (+ bias)
   EPI_RESID_SCATTER = 4,  // x[b, pos, n] = resid + C + bias + bias2, resid = x[b, pos] or res[m]
+  EPI_RESID_SCATTER_GATE = 5,  // x[b, pos, n] += sigmoid(gate[b, pos]) * (resid + C + bias + bias2 - x[b, pos])
 };
 
 struct GemmArgs {
@@ -89,6 +106,8 @@ struct GemmArgs {
   void* out; int ldo;
   // EPI_RESID_*: hidden states x [B, T, d] (d = N); res (nullable) compact residual [M, N]
   void* x; const void* res;
+  // EPI_RESID_SCATTER_GATE: router scores [B, T] (fp32)
+  const float* gate;
   // EPI_SWIGLU: f (gate rows [0, f), up rows [f, 2f))
   int f;
   // Stream-K workspace (nullable: then every launch is one tile per workgroup):

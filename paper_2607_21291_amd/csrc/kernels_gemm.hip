@@ -47,6 +47,33 @@ __device__ __forceinline__ void store8(T* p, const float* v) {
   }
 }
 
+// Eight elements of a row as raw 16-byte vectors (one for bf16, two for
+// fp32), widened to fp32 only where they are used.
+template <typename T>
+struct Raw8 {
+  u32x4 v[sizeof(T) / 2];
+};
+template <typename T>
+__device__ __forceinline__ Raw8<T> load_raw8(const T* p) {
+  Raw8<T> r;
+#pragma unroll
+  for (int i = 0; i < int(sizeof(T)) / 2; ++i) r.v[i] = reinterpret_cast<const u32x4*>(p)[i];
+  return r;
+}
+template <typename T>
+__device__ __forceinline__ void unpack8(const Raw8<T>& r, float* out) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    if constexpr (sizeof(T) == 2) {
+      out[2 * i] = __uint_as_float(r.v[0][i] << 16);
+      out[2 * i + 1] = __uint_as_float(r.v[0][i] & 0xffff0000u);
+    } else {
+      out[i] = __uint_as_float(r.v[0][i]);
+      out[4 + i] = __uint_as_float(r.v[1][i]);
+    }
+  }
+}
+
 // stage: fp32 tile [BM][BN + 4] in LDS; tile origin (m0, tn). Each thread owns
 // one 8-column chunk and walks the tile's rows, so everything that depends
 // only on the column (bias, head, RoPE partner) is computed once. EPI is an
@@ -78,7 +105,7 @@ __device__ void gemm_epilogue(const GemmArgs& g, const float* stage, int m0, int
 #pragma unroll
   for (int i = 0; i < 8; ++i) bias[i] = 0.f;
   if (g.bias) load8((const T*)g.bias + n, bias);
-  if constexpr (EPI == EPI_RESID_SCATTER) {
+  if constexpr (EPI == EPI_RESID_SCATTER || EPI == EPI_RESID_SCATTER_GATE) {
     if (g.bias2) {
       float b2[8];
       load8((const T*)g.bias2 + n, b2);
@@ -130,6 +157,43 @@ __device__ void gemm_epilogue(const GemmArgs& g, const float* stage, int m0, int
     bq[q] = mm / g.kk;
     jq[q] = mm - bq[q] * g.kk;
     pq[q] = g.idx ? clamp_pos(g.idx[mm], g.T) : jq[q];
+  }
+  if constexpr (EPI == EPI_RESID_SCATTER_GATE) {
+    // Gated scatter (Section 3.4): the block's update of each kept row,
+    // delta = (resid + C + biases) - x[b, pos], is scaled by sigmoid of the
+    // token's router score before it is added to x[b, pos]. The rows are held
+    // as raw 16-byte vectors until used, which keeps this variant within the
+    // register budget of the plain scatter.
+    Raw8<T> rr[RPT], ro[RPT];
+    float gs[RPT];
+#pragma unroll
+    for (int q = 0; q < RPT; ++q) {
+      if (!live[q]) continue;
+      const int m = m0 + rr0 + q * RSTEP;
+      const int64_t xrow = int64_t(bq[q]) * g.T + pq[q];
+      rr[q] = load_raw8(g.res ? (const T*)g.res + int64_t(m) * g.N + n : (const T*)g.x + xrow * g.N + n);
+      if (g.res) ro[q] = load_raw8((const T*)g.x + xrow * g.N + n);
+      gs[q] = g.gate[xrow];
+    }
+#pragma unroll
+    for (int q = 0; q < RPT; ++q) {
+      if (!live[q]) continue;
+      const float* row = stage + (rr0 + q * RSTEP) * LD;
+      const float sg = 1.f / (1.f + expf(-gs[q]));
+      float r[8], v[8];
+      unpack8(rr[q], r);
+      if (g.res) {
+        float o[8];
+        unpack8(ro[q], o);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[i] = o[i] + sg * ((row[cc + i] + bias[i]) + (r[i] - o[i]));
+      } else {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[i] = r[i] + sg * (row[cc + i] + bias[i]);
+      }
+      store8((T*)g.x + (int64_t(bq[q]) * g.T + pq[q]) * g.N + n, v);
+    }
+    return;
   }
   if constexpr (EPI == EPI_RESID_STORE || EPI == EPI_RESID_SCATTER) {
     float xr[RPT][8];
@@ -1001,6 +1065,7 @@ hipError_t launch_gemm(const GemmArgs& g, hipStream_t s) {
     case EPI_SWIGLU: launch_gemm_t<EPI_SWIGLU>(g, s); break;
     case EPI_RESID_STORE: launch_gemm_t<EPI_RESID_STORE>(g, s); break;
     case EPI_RESID_SCATTER: launch_gemm_t<EPI_RESID_SCATTER>(g, s); break;
+    case EPI_RESID_SCATTER_GATE: launch_gemm_t<EPI_RESID_SCATTER_GATE>(g, s); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -1,5 +1,5 @@
 // Streaming kernels of the depth-sparse layer on gfx950: RoPE table,
-// similarity statistic (Eq. 4), router (Section 3.4), per-sequence Top-K,
+// similarity statistic (Eq. 4), per-sequence Top-K (Section 3.4),
 // gather / scatter of hidden rows, and fused gather + LayerNorm / RMSNorm.
 //
 // These kernels move far more bytes than they compute on, so they are written
@@ -108,133 +108,6 @@ hipError_t launch_sim_stats(int dtype, const void* a, const void* c, int64_t n, 
   else
     sim_partial_kernel<float><<<g, 256, 0, s>>>((const float*)a, (const float*)c, n, d, per_tok, partial);
   sim_finish_kernel<<<1, 256, 0, s>>>(partial, g, n, accum);
-  return hipGetLastError();
-}
-
-// ------------------------------------------------------------ router, Sec. 3.4
-
-// bf16 router on MFMA. A workgroup of four wavefronts scores 16 tokens
-// against all d_r hidden units (DR / 16 column blocks of
-// v_mfma_f32_16x16x32_bf16); the reduction over d is split between the
-// wavefronts (wavefront w takes 128-wide chunks w, w + 4, ...), which keeps
-// many independent row streams in flight, and the partial hidden sums meet in
-// LDS. Within a chunk each lane streams 64 contiguous bytes of its row; the
-// MFMA's k slots are filled in that order and W1 is read in the same order,
-// so the contraction is unchanged.
-constexpr int kRouterWaves = 8;  // waves per 64-token workgroup, each on 1/8 of the columns
-
-template <int DR>
-__global__ __launch_bounds__(64 * kRouterWaves) void router_bf16_kernel(const uint16_t* __restrict__ x, int64_t n, int d,
-                                                          const uint16_t* __restrict__ w1,
-                                                          const uint16_t* __restrict__ b1,
-                                                          const uint16_t* __restrict__ w2, float b2,
-                                                          float* __restrict__ scores) {
-  // 64 tokens per workgroup in 4 blocks of 16; wave w takes the 32-wide
-  // column slices w, w + NW, ... of all four blocks, so each W1 fragment it
-  // loads serves 64 tokens (W1 traffic is a quarter of x's at d_r = 32), and
-  // the short per-wave loop keeps many loads in flight per CU.
-  constexpr int NB = DR / 16, NW = kRouterWaves, MT = 4;
-  __shared__ float part[NW][16 * MT][DR + 1];
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int r = lane & 15, g = lane >> 4;
-  const int64_t row0 = int64_t(blockIdx.x) * (16 * MT);
-  const uint16_t* xr[MT];
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt) {
-    int64_t row = row0 + 16 * mt + r;
-    if (row > n - 1) row = n - 1;  // clamp: rows past the end are computed and dropped
-    xr[mt] = x + row * d;
-  }
-  f32x4 acc[MT][NB];
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) acc[mt][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const bf16x8 zero = {};
-#pragma unroll 4
-  for (int kc = 32 * w; kc < d; kc += 32 * NW) {
-    // d is a multiple of 8, so each lane's 8-element piece is wholly inside or past the end
-    const int k0 = kc + 8 * g;
-    const bool ok = k0 < d;
-    bf16x8 wb[NB], xa[MT];
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
-      wb[nb] = ok ? *reinterpret_cast<const bf16x8*>(w1 + (16 * nb + r) * int64_t(d) + k0) : zero;
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) xa[mt] = ok ? *reinterpret_cast<const bf16x8*>(xr[mt] + k0) : zero;
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
-        acc[mt][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[mt], wb[nb], acc[mt][nb], 0, 0, 0);
-  }
-  // lane holds wave w's partial hidden[token 16 mt + 4 g + i][unit 16 nb + r]
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) part[w][16 * mt + 4 * g + i][16 * nb + r] = acc[mt][nb][i];
-  __syncthreads();
-  // threads 0..255: token t / 4, units q DR/4 .. (q + 1) DR/4 - 1 with
-  // q = t % 4; the partial sums of a token are then added in a fixed order
-  if (threadIdx.x >= 256) return;
-  const int t = threadIdx.x >> 2, q = threadIdx.x & 3;
-  float v = 0.f;
-#pragma unroll
-  for (int jj = 0; jj < DR / 4; ++jj) {
-    const int j = q * (DR / 4) + jj;
-    float h = b1 ? bf2f(b1[j]) : 0.f;
-#pragma unroll
-    for (int ww = 0; ww < NW; ++ww) h += part[ww][t][j];
-    v = fmaf(bf2f(w2[j]), h > 0.f ? h : 0.f, v);
-  }
-  v += __shfl_xor(v, 1);
-  v += __shfl_xor(v, 2);
-  if (q == 0 && row0 + t < n) scores[row0 + t] = v + b2;
-}
-
-// fp32 router: one wavefront per token, one hidden unit at a time.
-__global__ __launch_bounds__(256) void router_f32_kernel(const float* __restrict__ x, int64_t n, int d, int dr,
-                                                         const float* __restrict__ w1, const float* __restrict__ b1,
-                                                         const float* __restrict__ w2, float b2,
-                                                         float* __restrict__ scores) {
-  const int lane = threadIdx.x & 63;
-  const int64_t t = int64_t(blockIdx.x) * 4 + (threadIdx.x >> 6);
-  if (t >= n) return;
-  const float* row = x + t * d;
-  float score = 0.f;
-  for (int j = 0; j < dr; ++j) {
-    const float* wr = w1 + int64_t(j) * d;
-    float h = 0.f;
-    for (int i = lane; i < d; i += 64) h = fmaf(row[i], wr[i], h);
-    h = wave_sum(h) + (b1 ? b1[j] : 0.f);
-    score = fmaf(w2[j], h > 0.f ? h : 0.f, score);
-  }
-  if (lane == 0) scores[t] = score + b2;
-}
-
-hipError_t launch_router(int dtype, const void* x, int64_t n, int d, int d_r, const void* w1,
-                         const void* b1, const void* w2, float b2, float* scores, hipStream_t s) {
-  if (n == 0) return hipSuccess;
-  TimedScope ts(DSF_KIND_ROUTER, s);
-  if (dtype == DSF_F32) {
-    router_f32_kernel<<<unsigned((n + 3) / 4), 256, 0, s>>>((const float*)x, n, d, d_r, (const float*)w1,
-                                                            (const float*)b1, (const float*)w2, b2, scores);
-    return hipGetLastError();
-  }
-  unsigned grid = unsigned((n + 63) / 64);
-  auto X = (const uint16_t*)x;
-  auto W1 = (const uint16_t*)w1;
-  auto B1 = (const uint16_t*)b1;
-  auto W2 = (const uint16_t*)w2;
-  switch (d_r) {
-    case 16: router_bf16_kernel<16><<<grid, 64 * kRouterWaves, 0, s>>>(X, n, d, W1, B1, W2, b2, scores); break;
-    case 32: router_bf16_kernel<32><<<grid, 64 * kRouterWaves, 0, s>>>(X, n, d, W1, B1, W2, b2, scores); break;
-    case 48: router_bf16_kernel<48><<<grid, 64 * kRouterWaves, 0, s>>>(X, n, d, W1, B1, W2, b2, scores); break;
-    case 64: router_bf16_kernel<64><<<grid, 64 * kRouterWaves, 0, s>>>(X, n, d, W1, B1, W2, b2, scores); break;
-    default: return hipErrorInvalidValue;
-  }
   return hipGetLastError();
 }
 

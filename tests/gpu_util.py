@@ -106,12 +106,12 @@ def run_layer(dev, w, W, x, k, flags=0, idx_in=None):
     return xd, scores, idx[:, :k]
 
 
-def check_layer(w, W, x, y_gpu, scores_gpu, idx_gpu, k, sample=None):
+def check_layer(w, W, x, y_gpu, scores_gpu, idx_gpu, k, sample=None, gate=False):
     """Layer protocol: router scores within the fp32 bound and the oracle's
     Top-K of the GPU's scores equal to the GPU's indices (every sequence),
     skipped rows bitwise unchanged (every sequence), and the kept rows
     against the oracle teacher-forced with the GPU's indices, for the
-    sequences in `sample` (None: all of them)."""
+    sequences in `sample` (None: all of them). gate: the score-gated layer."""
     xs = to_np(x)
     sc = scores_gpu.cpu().numpy()
     ref_scores = O.router_scores(x, W["router_w1"], W["router_b1"], W["router_w2"], W["router_b2"])
@@ -125,6 +125,7 @@ def check_layer(w, W, x, y_gpu, scores_gpu, idx_gpu, k, sample=None):
         kept[b, idx[b]] = True
         np.testing.assert_array_equal(y[b][~kept[b]], xs[b][~kept[b]])
     for b in (range(B) if sample is None else sample):
-        res = O.routed_layer(desc_dict(w), W, xs[b:b + 1], k, idx=idx[b:b + 1])
-        assert rel_inf(y[b][kept[b]] - xs[b][kept[b]], res["delta"][0]) < TOL[w.dtype]
+        res = O.routed_layer(desc_dict(w), W, xs[b:b + 1], k, idx=idx[b:b + 1], gate=gate)
+        upd = res["y"][0][kept[b]] - xs[b][kept[b]]
+        assert rel_inf(y[b][kept[b]] - xs[b][kept[b]], upd) < TOL[w.dtype]
         assert rel_inf(y[b], res["y"][0]) < TOL[w.dtype]

@@ -125,6 +125,7 @@ def test_error_paths_launch_nothing():
         (dict(k=-1), 1),
         (dict(flags=1, k=32), 1),
         (dict(flags=4), 1),
+        (dict(flags=3, k=64), 1),  # gating needs the router: not with DSF_FLAG_DENSE
         (dict(dtype=7), 2),
         (dict(ws_bytes=1024), 3),
         (dict(x=FAKE + 4), 1),
@@ -158,6 +159,26 @@ def test_error_paths_of_the_kernel_calls():
     assert L.dsf_sim_stats(FAKE, FAKE, 1, 100, 64, None, FAKE, FAKE, 0, None) == 3
     arr = (ctypes.c_double * 2)()
     assert L.dsf_retention_from_similarity(ctypes.addressof(arr), 2, 1.5, 0.1, 10.0, 2, ctypes.addressof(arr)) == 1
+    # router-score pathway
+    assert L.dsf_gate_score_grad(FAKE, FAKE, FAKE, 1, FAKE, FAKE, 2, 10, 3, 12, FAKE, None) == 2   # d % 8
+    assert L.dsf_gate_score_grad(FAKE, FAKE, FAKE, 1, FAKE, FAKE, 2, 10, 11, 16, FAKE, None) == 1  # k > T
+    assert L.dsf_gate_score_grad(FAKE + 4, FAKE, FAKE, 1, FAKE, FAKE, 2, 10, 3, 16, FAKE, None) == 1
+    assert L.dsf_gate_score_grad(FAKE, FAKE, FAKE, 1, FAKE, FAKE, 2, 10, 3, 16, None, None) == 1
+    assert L.dsf_router_backward_workspace_size(100, 64, 40) == 0
+    assert L.dsf_router_backward_workspace_size(100, 60, 32) == 0
+    assert L.dsf_router_backward_workspace_size(-1, 64, 32) == 0
+    ws = L.dsf_router_backward_workspace_size(1000, 64, 32)
+    assert ws >= 4 * (1000 * 32 + 16 * 65 + 32 * 64) and ws % 256 == 0
+    rb = L.dsf_router_backward
+    assert rb(FAKE, 1, 1000, 64, 40, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, ws, None) == 2
+    assert rb(FAKE, 1, 1000, 64, 32, FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, ws, None) == 1
+    assert rb(FAKE, 1, 1000, 64, 32, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, ws - 4,
+              None) == 3
+    assert rb(FAKE, 1, 1000, 64, 32, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE + 16, ws,
+              None) == 1
+    assert rb(FAKE, 1, 1000, 64, 32, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE + 8, FAKE, ws,
+              None) == 1
+    assert rb(FAKE, 1, 1000, 64, 32, FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE, FAKE, None, FAKE, ws, None) == 1
     # empty problems are valid no-ops
     assert L.dsf_topk_select(None, 0, 10, 3, None, None) == 0
     assert L.dsf_gather_rows(None, 1, 2, 10, 16, None, 0, None, None) == 0
