@@ -123,6 +123,92 @@ def streaming_rates(P, C, w, k, dev, weights0, reps=3):
     return out
 
 
+def _timed(fn, n_calls, reps_of):
+    """Mean microseconds per call of fn(i) over n_calls calls (torch events)."""
+    import torch
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for i in range(n_calls):
+        fn(reps_of(i))
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) * 1e3 / n_calls
+
+
+def router_pathway(P, C, w, ks, dev, desc, weights, x0, ws, ms_plain, steps, weights0):
+    """The training-side router-score pathway (Section 3.4): the score-gated
+    stack against the plain one, and the gate score gradient and the router
+    backward standalone on one layer's shapes, cold (inputs cycled through
+    more than 1 GiB of copies) and hot."""
+    import torch
+    B, T, d = w.batch, w.seq, w.d_model
+    eb = 4 if w.dtype == "f32" else 2
+    out = {}
+    # gated stack, same k per layer
+    xg = [x0.clone() for _ in range(steps)]
+    xw = x0.clone()
+    P.stack_forward(desc, weights, ks, xw, ws, flags=P.FLAG_GATE)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        P.stack_forward(desc, weights, ks, xg[i], ws, flags=P.FLAG_GATE)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    out["gated_stack"] = {"ms_per_step": ms, "tokens_per_s": B * T / (ms / 1e3), "vs_plain": ms / ms_plain}
+    del xg, xw
+    # gate score gradient at the mean k
+    k = int(round(sum(ks) / len(ks)))
+    rows = B * T * d * eb
+    R = max(4, -(-(1 << 30) // (3 * rows)) + 1)
+    dys = [torch.randn(B, T, d, device=dev).to(w.torch_dtype) for _ in range(R)]
+    xis = [torch.randn(B, T, d, device=dev).to(w.torch_dtype) for _ in range(R)]
+    xos = [torch.randn(B, T, d, device=dev).to(w.torch_dtype) for _ in range(R)]
+    sc = torch.randn(B, T, device=dev)
+    idx = torch.stack([torch.sort(torch.randperm(T, device=dev)[:k])[0] for _ in range(B)]).to(torch.int32)
+    dsc = torch.empty(B, T, device=dev)
+    fn = lambda i: P.gate_score_grad(dys[i], xis[i], xos[i], sc, idx, dsc)
+    nbytes = C.gate_grad_bytes(w, B, T, k)
+    res = {"k": k, "bytes_per_call": nbytes}
+    for mode in ("cold", "hot"):
+        fn(0)
+        us = _timed(fn, 3 * R, (lambda i: i % R) if mode == "cold" else (lambda i: 0))
+        res[mode] = {"us": us, "GB/s": nbytes / (us * 1e-6) / 1e9, "frac_of_hbm_peak": nbytes / (us * 1e-6) / 1e9 / PEAK_HBM_GBS}
+    out["gate_score_grad"] = res
+    del dys, xis, xos
+    # router backward over every token of the batch
+    n = B * T
+    W = {key: v.to(dev) for key, v in weights0.items() if key.startswith("router_") and hasattr(v, "to")}
+    R = max(4, -(-(1 << 30) // (2 * rows)) + 1)
+    xr = [torch.randn(B, T, d, device=dev).mul_(0.02).to(w.torch_dtype) for _ in range(R)]
+    dxr = [torch.zeros(B, T, d, device=dev, dtype=w.torch_dtype) for _ in range(R)]
+    dsr = torch.randn(n, device=dev)
+    g = {name: torch.empty(shape, device=dev) for name, shape in
+         (("dw1", (w.d_router, d)), ("db1", (w.d_router,)), ("dw2", (w.d_router,)), ("db2", (1,)))}
+    rws = torch.empty(P.router_backward_workspace_size(n, d, w.d_router), dtype=torch.uint8, device=dev)
+    fn = lambda i: P.router_backward(xr[i], W["router_w1"], W["router_b1"], W["router_w2"], dsr, g["dw1"], g["db1"],
+                                     g["dw2"], g["db2"], dx=dxr[i], workspace=rws)
+    nbytes, nflops = C.router_bwd_bytes(w, n), C.router_bwd_flops(w, n)
+    res = {"n_tokens": n, "bytes_per_call": nbytes, "flops_per_call": nflops}
+    for mode in ("cold", "hot"):
+        fn(0)
+        us = _timed(fn, 3 * R, (lambda i: i % R) if mode == "cold" else (lambda i: 0))
+        res[mode] = {"us": us, "GB/s": nbytes / (us * 1e-6) / 1e9, "frac_of_hbm_peak": nbytes / (us * 1e-6) / 1e9 / PEAK_HBM_GBS,
+                     "TFLOP/s": nflops / (us * 1e-6) / 1e12}
+    # the three launches of one call, on the library's event timing
+    P.timing_enable(64, ["backward"])
+    for i in range(8):
+        fn(i % R)
+    torch.cuda.synchronize()
+    nb, msb = P.timing_read("backward")
+    P.timing_enable(0)
+    res["timed_calls"] = {"calls": nb, "us_per_call": msb * 1e3 / max(nb, 1)}
+    out["router_backward"] = res
+    del xr, dxr
+    torch.cuda.empty_cache()
+    return out
+
+
 def cpu_baseline(w, ks, layers, min_seconds=10.0):
     """The oracle, as it stands, on whole sequences through `layers` layers.
 
@@ -377,6 +463,10 @@ def main():
         kmean = int(round(sum(ks) / len(ks)))
         log(f"streaming entry points standalone (B={B}, T={T}, k={kmean}), cold and hot inputs")
         out["streaming_kernels"] = streaming_rates(P, C, w, kmean, dev, S.layer_weights(w, 0))
+    if not args.only_sparse:
+        log("router-score pathway: gated stack, gate score gradient, router backward")
+        out["router_score_pathway"] = router_pathway(P, C, w, ks, dev, desc, weights, x0, ws, ms_step,
+                                                     max(3, args.steps // 3), S.layer_weights(w, 0))
     if not args.no_cpu_baseline:
         layers_cpu = L if args.cpu_layers is None else min(args.cpu_layers, L)
         log(f"cpu oracle baseline over {layers_cpu} layers of one sequence")

@@ -77,6 +77,26 @@ def norm_bytes(w, B: int, k: int) -> float:
     return (3.0 if w.block == NEOX else 4.0) * rows + 4.0 * B * k
 
 
+def gate_grad_bytes(w, B: int, T: int, k: int) -> float:
+    """Gate score gradient: dy, x_in and x_out rows of the kept tokens and
+    their scores and positions read; the [B, T] score gradient written."""
+    eb = 4 if w.dtype == "f32" else 2
+    return 3.0 * eb * B * k * w.d_model + 8.0 * B * k + 4.0 * B * T
+
+
+def router_bwd_bytes(w, n: int) -> float:
+    """Router backward over n tokens: x and dscore read, dx read and written
+    (accumulated), W1 and w2 read, the fp32 weight gradients written."""
+    eb = 4 if w.dtype == "f32" else 2
+    d, dr = w.d_model, w.d_router
+    return eb * n * d + 4.0 * n + 2.0 * eb * n * d + eb * dr * (d + 2) + 4.0 * (dr * d + 2 * dr + 1)
+
+
+def router_bwd_flops(w, n: int) -> float:
+    """Three n x d x d_r contractions: the hidden units recomputed, dW1, dx."""
+    return 6.0 * n * w.d_model * w.d_router
+
+
 def kind_work(w, kind: str, B: int, T: int, k: int):
     """(work, unit) of one layer's launches of a kernel kind: flops for the
     MFMA kernels, bytes for the streaming ones; None for kinds not modelled."""

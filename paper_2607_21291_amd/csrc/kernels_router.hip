@@ -24,7 +24,11 @@ namespace dsf {
 // k slots are filled in that order and W1 is read in the same order, so the
 // contraction is unchanged. The partial hidden sums meet in LDS.
 constexpr int kRouterWaves = 8;
-constexpr int kRouterTokens = 64;
+#ifndef DSF_ROUTER_TOKENS
+#define DSF_ROUTER_TOKENS 64
+#endif
+constexpr int kRouterTokens = DSF_ROUTER_TOKENS;  // tokens per workgroup, a multiple of 16
+static_assert(kRouterTokens % 16 == 0 && kRouterTokens <= 128, "token blocks of 16");
 
 template <int DR>
 using RouterPart = float[kRouterWaves][kRouterTokens][DR + 1];
@@ -98,9 +102,9 @@ __global__ __launch_bounds__(64 * kRouterWaves) void router_bf16_kernel(const ui
   const int64_t row0 = int64_t(blockIdx.x) * kRouterTokens;
   router_hidden_partials<DR>(x, n, d, w1, row0, part);
   __syncthreads();
-  // threads 0..255: token t / 4, units q DR/4 .. (q + 1) DR/4 - 1 with
+  // threads 0..4 TM - 1: token t / 4, units q DR/4 .. (q + 1) DR/4 - 1 with
   // q = t % 4; the partial sums of a token are then added in a fixed order
-  if (threadIdx.x >= 256) return;
+  if (threadIdx.x >= 4 * kRouterTokens) return;
   const int t = threadIdx.x >> 2, q = threadIdx.x & 3;
   float v = 0.f;
 #pragma unroll
@@ -224,55 +228,63 @@ hipError_t launch_gate_grad(int dtype, const void* dy, const void* x_in, const v
 // With z = W1 x + b1 and s = w2 . ReLU(z) + b2, and ds = dL/ds per token:
 //   dz = ds * w2 * [z > 0]          dW1 = sum_t dz_t x_t^T    db1 = sum_t dz_t
 //   dw2 = sum_t ds_t ReLU(z_t)       db2 = sum_t ds_t          dx_t = W1^T dz_t
-// Three launches:
+// Launches:
 //   tokens: per 64-token chunk, recompute z (same arithmetic and order as the
-//     forward, hence the same ReLU decisions), write dz [n, DR], the chunk's
-//     sums of dz, ds ReLU(z) and ds, and add W1^T dz into dx;
-//   weights: dW1 partials over (128-column slab, token range);
+//     forward, hence the same ReLU decisions), then dz, the chunk's sums of
+//     dz, ds ReLU(z) and ds, and dx += W1^T dz;
+//   weights: partial dW1 over (column slab, token range);
 //   reduce: the partials in fixed order into dW1, db1, dw2, db2.
+// bf16 runs both contractions on MFMA. MFMA takes its k dimension
+// contiguous in each lane's operand, so the tokens kernel multiplies
+// W1^T (transposed once per call, k = units) by dz, and the weights kernel
+// multiplies dz^T (written by the tokens kernel, k = tokens) by x tiles
+// transposed through LDS. dz enters both as a bf16 pair hi + lo (hi = dz
+// rounded to bf16, lo = the remainder rounded to bf16), which keeps about
+// 16 significant bits: the products keep fp32-level accuracy. fp32 runs the
+// same steps on the vector ALUs.
 
 constexpr int kBwdTerms = 2;  // per-chunk sums: dz (db1) and ds ReLU(z) (dw2), then ds (db2)
+constexpr int kBwdMaxSplits = 64;
 
-template <int DR>
-constexpr int bwd_terms_per_chunk() { return kBwdTerms * DR + 1; }
-
+// Token ranges of the weights kernel (a function of n only, so the summation
+// order, and with it the result, does not depend on the device).
 int router_bwd_splits(int64_t n) {
   const int64_t s = n / 256;
-  return int(s < 1 ? 1 : (s > 64 ? 64 : s));
+  return int(s < 1 ? 1 : (s > kBwdMaxSplits ? kBwdMaxSplits : s));
 }
 
-size_t router_bwd_workspace_bytes(int64_t n, int d, int d_r) {
+// Workspace: dz (fp32 [n, DR], or bf16 hi and lo [DR, npad] with npad = n
+// rounded up to 32) | chunk terms | dW1 partials | W1^T (bf16 [d, DR]).
+struct BwdLayout {
+  size_t dz, terms, pw1, w1t, total;
+  int64_t chunks, npad;
+  int splits;
+};
+static BwdLayout bwd_layout(int64_t n, int d, int d_r) {
   auto up = [](size_t b) { return (b + 255) / 256 * 256; };
-  const int64_t chunks = (n + kRouterTokens - 1) / kRouterTokens;
-  return up(sizeof(float) * size_t(n) * d_r) + up(sizeof(float) * size_t(chunks) * (kBwdTerms * d_r + 1)) +
-         up(sizeof(float) * size_t(router_bwd_splits(n)) * d_r * d);
+  BwdLayout L{};
+  L.chunks = (n + kRouterTokens - 1) / kRouterTokens;
+  L.npad = (n + 31) / 32 * 32;
+  L.splits = router_bwd_splits(n);
+  L.dz = 0;
+  L.terms = up(sizeof(float) * size_t(L.npad) * d_r);
+  L.pw1 = L.terms + up(sizeof(float) * size_t(L.chunks) * (kBwdTerms * d_r + 1));
+  L.w1t = L.pw1 + up(sizeof(float) * size_t(L.splits) * d_r * d);
+  L.total = L.w1t + up(sizeof(uint16_t) * size_t(d) * d_r);
+  return L;
 }
 
-template <typename T, int DR>
-__global__ __launch_bounds__(64 * kRouterWaves) void router_bwd_tokens_kernel(
-    const T* __restrict__ x, int64_t n, int d, const T* __restrict__ w1, const T* __restrict__ b1,
-    const T* __restrict__ w2, const float* __restrict__ ds, T* __restrict__ dx, float* __restrict__ dz,
-    float* __restrict__ terms) {
+size_t router_bwd_workspace_bytes(int64_t n, int d, int d_r) { return bwd_layout(n, d, d_r).total; }
+
+// z, dz and the per-chunk terms of a 64-token chunk, shared by both dtypes:
+// dzs[t][j] = dz, part[1][t][j] = ds ReLU(z), ssum[t] = ds (0 past n). The
+// hidden sums are in part (bf16: wave partials; fp32: part[0] holds z).
+template <typename T, int DR, int LDZ>
+__device__ __forceinline__ void router_bwd_chunk(RouterPart<DR>& part, float (*dzs)[LDZ], float* ssum,
+                                                 const T* __restrict__ b1, const T* __restrict__ w2,
+                                                 const float* __restrict__ ds, int64_t n, int64_t row0,
+                                                 float* __restrict__ terms) {
   constexpr int NT = 64 * kRouterWaves, TM = kRouterTokens;
-  __shared__ RouterPart<DR> part;
-  __shared__ __align__(16) float dzs[TM][DR];
-  __shared__ float ssum[TM];
-  const int64_t row0 = int64_t(blockIdx.x) * TM;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  if constexpr (sizeof(T) == 2) {
-    router_hidden_partials<DR>(x, n, d, w1, row0, part);
-  } else {
-    // one wavefront per token, as in the fp32 forward; the full sum (bias
-    // included) goes to part[0]
-    for (int t = w; t < TM; t += kRouterWaves) {
-      const int64_t row = row0 + t < n ? row0 + t : n - 1;
-      for (int j = 0; j < DR; ++j) {
-        const float h = router_hidden_f32(x + row * d, d, w1, b1, j, lane);
-        if (lane == 0) part[0][t][j] = h;
-      }
-    }
-  }
-  __syncthreads();
   for (int e = threadIdx.x; e < TM * DR; e += NT) {
     const int t = e / DR, j = e - t * DR;
     float h;
@@ -280,16 +292,11 @@ __global__ __launch_bounds__(64 * kRouterWaves) void router_bwd_tokens_kernel(
     else h = part[0][t][j];
     const float sv = row0 + t < n ? ds[row0 + t] : 0.f;
     const bool on = h > 0.f;
-    const float g = on ? sv * Elem<T>::to_f(w2[j]) : 0.f;
-    dzs[t][j] = g;
+    dzs[t][j] = on ? sv * Elem<T>::to_f(w2[j]) : 0.f;
     part[1][t][j] = on ? sv * h : 0.f;  // only this thread reads or writes entry (t, j)
     if (j == 0) ssum[t] = sv;
   }
   __syncthreads();
-  for (int e = threadIdx.x; e < TM * DR; e += NT) {
-    const int t = e / DR;
-    if (row0 + t < n) dz[row0 * DR + e] = dzs[t][e - t * DR];
-  }
   if (threadIdx.x < kBwdTerms * DR + 1) {
     const int j = threadIdx.x;
     float a = 0.f;
@@ -302,6 +309,221 @@ __global__ __launch_bounds__(64 * kRouterWaves) void router_bwd_tokens_kernel(
     }
     terms[int64_t(blockIdx.x) * (kBwdTerms * DR + 1) + j] = a;
   }
+}
+
+// ---- bf16 on MFMA
+
+template <int DR>
+__global__ __launch_bounds__(256) void router_w1t_kernel(const uint16_t* __restrict__ w1, int d,
+                                                         uint16_t* __restrict__ w1t) {
+  const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;  // = c * DR + j
+  if (i >= int64_t(d) * DR) return;
+  const int c = int(i / DR), j = int(i - int64_t(c) * DR);
+  w1t[i] = w1[int64_t(j) * d + c];
+}
+
+// v ~ hi + lo: hi = v rounded to bf16, lo = the remainder (exact in fp32) rounded to bf16
+__device__ __forceinline__ __bf16 bf16_hi(float v) { return (__bf16)v; }
+__device__ __forceinline__ __bf16 bf16_lo(float v, __bf16 hi) { return (__bf16)(v - (float)hi); }
+
+template <int DR>
+__global__ __launch_bounds__(64 * kRouterWaves) void router_bwd_tokens_bf16_kernel(
+    const uint16_t* __restrict__ x, int64_t n, int d, const uint16_t* __restrict__ w1,
+    const uint16_t* __restrict__ w1t, const uint16_t* __restrict__ b1, const uint16_t* __restrict__ w2,
+    const float* __restrict__ ds, uint16_t* __restrict__ dx, uint16_t* __restrict__ dzt_hi,
+    uint16_t* __restrict__ dzt_lo, int64_t npad, float* __restrict__ terms) {
+  constexpr int NT = 64 * kRouterWaves, TM = kRouterTokens, KS = (DR + 31) / 32;
+  __shared__ RouterPart<DR> part;
+  __shared__ float dzs[TM][DR + 1];
+  __shared__ float ssum[TM];
+  const int64_t row0 = int64_t(blockIdx.x) * TM;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int r = lane & 15, g = lane >> 4;
+  router_hidden_partials<DR>(x, n, d, w1, row0, part);
+  __syncthreads();
+  router_bwd_chunk<uint16_t, DR, DR + 1>(part, dzs, ssum, b1, w2, ds, n, row0, terms);
+  // dz^T as bf16 hi and lo, [DR, npad], for the weights kernel
+  for (int e = threadIdx.x; e < TM * DR; e += NT) {
+    const int j = e / TM, t = e - j * TM;
+    if (row0 + t < n) {
+      const float v = dzs[t][j];
+      const __bf16 hi = bf16_hi(v);
+      dzt_hi[j * npad + row0 + t] = __builtin_bit_cast(uint16_t, hi);
+      dzt_lo[j * npad + row0 + t] = __builtin_bit_cast(uint16_t, bf16_lo(v, hi));
+    }
+  }
+  if (!dx) return;
+  // dx^T tiles: D[c][t] = sum_j W1^T[c][j] dz[t][j], 16 columns x 16 tokens
+  // per MFMA; the lane holding D[4g + i][r] adds it to dx[t = 16 tb + r]
+  // [c = 16 cb + 4g + i], i = 0..3 (one 8-byte read-modify-write)
+  constexpr int TB = TM / 16;
+  bf16x8 bh[TB][KS], bl[TB][KS];
+#pragma unroll
+  for (int tb = 0; tb < TB; ++tb)
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int j = 32 * ks + 8 * g + i;
+        const float v = j < DR ? dzs[16 * tb + r][j] : 0.f;
+        const __bf16 hi = bf16_hi(v);
+        bh[tb][ks][i] = hi;
+        bl[tb][ks][i] = bf16_lo(v, hi);
+      }
+  const bf16x8 zero = {};
+  const int ncb = (d + 15) / 16;
+  // software pipelined over this wave's column blocks: the W1^T fragments
+  // and old dx values of block cb + NW are requested before block cb is
+  // multiplied and stored
+  bf16x8 a[KS], an[KS];
+  u32x2 old[TB], on[TB];
+  auto fetch = [&](int cb, bf16x8 (&aa)[KS], u32x2 (&oo)[TB]) {
+    const int c = 16 * cb + r, c4 = 16 * cb + 4 * g;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const int j0 = 32 * ks + 8 * g;
+      aa[ks] = (c < d && j0 < DR) ? *reinterpret_cast<const bf16x8*>(w1t + int64_t(c) * DR + j0) : zero;
+    }
+#pragma unroll
+    for (int tb = 0; tb < TB; ++tb) {
+      const int64_t t = row0 + 16 * tb + r;
+      oo[tb] = (t < n && c4 < d) ? *reinterpret_cast<const u32x2*>(dx + t * d + c4) : u32x2{0u, 0u};
+    }
+  };
+  if (w < ncb) fetch(w, a, old);
+  for (int cb = w; cb < ncb; cb += kRouterWaves) {
+    if (cb + kRouterWaves < ncb) fetch(cb + kRouterWaves, an, on);
+    const int c4 = 16 * cb + 4 * g;
+#pragma unroll
+    for (int tb = 0; tb < TB; ++tb) {
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[ks], bh[tb][ks], acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[ks], bl[tb][ks], acc, 0, 0, 0);
+      }
+      const int64_t t = row0 + 16 * tb + r;
+      if (t < n && c4 < d) {
+        const float v0 = bf2f(uint16_t(old[tb][0] & 0xffffu)) + acc[0];
+        const float v1 = bf2f(uint16_t(old[tb][0] >> 16)) + acc[1];
+        const float v2 = bf2f(uint16_t(old[tb][1] & 0xffffu)) + acc[2];
+        const float v3 = bf2f(uint16_t(old[tb][1] >> 16)) + acc[3];
+        *reinterpret_cast<u32x2*>(dx + t * d + c4) =
+            u32x2{uint32_t(f2bf(v0)) | (uint32_t(f2bf(v1)) << 16), uint32_t(f2bf(v2)) | (uint32_t(f2bf(v3)) << 16)};
+      }
+    }
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) a[ks] = an[ks];
+#pragma unroll
+    for (int tb = 0; tb < TB; ++tb) old[tb] = on[tb];
+  }
+}
+
+// Partial dW1 of token range s over a 64-column slab: D[j][c] =
+// sum_t dz^T[j][t] x[t][c], k = 32 tokens per step. Wave w takes columns
+// 16 w .. 16 w + 15 of the slab and every unit block. The x tile [32 tokens,
+// 64 columns] is loaded one step ahead into registers and transposed through
+// LDS (double buffered); the dz^T operands come straight from the workspace.
+template <int DR>
+__global__ __launch_bounds__(256) void router_bwd_w1_bf16_kernel(const uint16_t* __restrict__ x, int64_t n, int d,
+                                                                 const uint16_t* __restrict__ dzt_hi,
+                                                                 const uint16_t* __restrict__ dzt_lo, int64_t npad,
+                                                                 int splits, float* __restrict__ pw1) {
+  constexpr int NJ = DR / 16, P = 68;  // LDS row pitch in bf16 (136 bytes: spreads the column reads over banks)
+  __shared__ __align__(16) uint16_t xt[2][32 * P];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int r = lane & 15, g = lane >> 4;
+  const int c0 = blockIdx.x * 64;
+  const int s = blockIdx.y;
+  const int64_t nk = (n + 31) / 32;
+  const int64_t k0 = nk * s / splits, k1 = nk * (s + 1) / splits;
+  const int lr = threadIdx.x >> 3, lc = (threadIdx.x & 7) * 8;
+  auto load_tile = [&](int64_t kt) -> u32x4 {
+    const int64_t t = kt * 32 + lr;
+    const int c = c0 + lc;
+    return (t < n && c < d) ? *reinterpret_cast<const u32x4*>(x + t * d + c) : u32x4{0u, 0u, 0u, 0u};
+  };
+  f32x4 acc[NJ];
+#pragma unroll
+  for (int jb = 0; jb < NJ; ++jb) acc[jb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // dz^T operands of step kt: rows j = 16 jb + r, tokens 32 kt + 8 g .. + 7
+  // (inside the padded row; the pad past n holds no dz and is masked)
+  auto load_dz = [&](int64_t kt, bf16x8 (&ah)[NJ], bf16x8 (&al)[NJ]) {
+    const int64_t t8 = kt * 32 + 8 * g;
+#pragma unroll
+    for (int jb = 0; jb < NJ; ++jb) {
+      const int64_t off = int64_t(16 * jb + r) * npad + t8;
+      ah[jb] = *reinterpret_cast<const bf16x8*>(dzt_hi + off);
+      al[jb] = *reinterpret_cast<const bf16x8*>(dzt_lo + off);
+      if (t8 + 8 > n) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+          if (t8 + i >= n) ah[jb][i] = al[jb][i] = (__bf16)0.f;
+      }
+    }
+  };
+  u32x4 nxt = k0 < k1 ? load_tile(k0) : u32x4{0u, 0u, 0u, 0u};
+  bf16x8 ah[NJ], al[NJ], ahn[NJ], aln[NJ];
+  if (k0 < k1) load_dz(k0, ah, al);
+  for (int64_t kt = k0; kt < k1; ++kt) {
+    uint16_t* buf = xt[(kt - k0) & 1];
+    *reinterpret_cast<u32x2*>(buf + lr * P + lc) = u32x2{nxt[0], nxt[1]};
+    *reinterpret_cast<u32x2*>(buf + lr * P + lc + 4) = u32x2{nxt[2], nxt[3]};
+    __syncthreads();
+    if (kt + 1 < k1) {
+      nxt = load_tile(kt + 1);
+      load_dz(kt + 1, ahn, aln);
+    }
+    bf16x8 bx;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) bx[i] = __builtin_bit_cast(__bf16, buf[(8 * g + i) * P + 16 * w + r]);
+#pragma unroll
+    for (int jb = 0; jb < NJ; ++jb) {
+      acc[jb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah[jb], bx, acc[jb], 0, 0, 0);
+      acc[jb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al[jb], bx, acc[jb], 0, 0, 0);
+    }
+#pragma unroll
+    for (int jb = 0; jb < NJ; ++jb) {
+      ah[jb] = ahn[jb];
+      al[jb] = aln[jb];
+    }
+  }
+  // lane holds D[j = 16 jb + 4 g + i][c = c0 + 16 w + r]
+  const int c = c0 + 16 * w + r;
+  if (c >= d) return;
+#pragma unroll
+  for (int jb = 0; jb < NJ; ++jb)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) pw1[(int64_t(s) * DR + 16 * jb + 4 * g + i) * d + c] = acc[jb][i];
+}
+
+// ---- fp32 on the vector ALUs
+
+template <int DR>
+__global__ __launch_bounds__(64 * kRouterWaves) void router_bwd_tokens_f32_kernel(
+    const float* __restrict__ x, int64_t n, int d, const float* __restrict__ w1, const float* __restrict__ b1,
+    const float* __restrict__ w2, const float* __restrict__ ds, float* __restrict__ dx, float* __restrict__ dz,
+    float* __restrict__ terms) {
+  constexpr int NT = 64 * kRouterWaves, TM = kRouterTokens;
+  __shared__ RouterPart<DR> part;
+  __shared__ __align__(16) float dzs[TM][DR];
+  __shared__ float ssum[TM];
+  const int64_t row0 = int64_t(blockIdx.x) * TM;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  // one wavefront per token, as in the fp32 forward; z (bias included) goes to part[0]
+  for (int t = w; t < TM; t += kRouterWaves) {
+    const int64_t row = row0 + t < n ? row0 + t : n - 1;
+    for (int j = 0; j < DR; ++j) {
+      const float h = router_hidden_f32(x + row * d, d, w1, b1, j, lane);
+      if (lane == 0) part[0][t][j] = h;
+    }
+  }
+  __syncthreads();
+  router_bwd_chunk<float, DR, DR>(part, dzs, ssum, b1, w2, ds, n, row0, terms);
+  for (int e = threadIdx.x; e < TM * DR; e += NT) {
+    const int t = e / DR;
+    if (row0 + t < n) dz[row0 * DR + e] = dzs[t][e - t * DR];
+  }
   if (!dx) return;
   // dx[t, c:c+2] += sum_j dz[t, j] W1[j, c:c+2], two columns per thread
   const int tmax = n - row0 < TM ? int(n - row0) : TM;
@@ -309,47 +531,33 @@ __global__ __launch_bounds__(64 * kRouterWaves) void router_bwd_tokens_kernel(
     float wa[DR], wb[DR];
 #pragma unroll
     for (int j = 0; j < DR; ++j) {
-      wa[j] = Elem<T>::to_f(w1[int64_t(j) * d + c]);
-      wb[j] = Elem<T>::to_f(w1[int64_t(j) * d + c + 1]);
+      wa[j] = w1[int64_t(j) * d + c];
+      wb[j] = w1[int64_t(j) * d + c + 1];
     }
     for (int t = 0; t < tmax; ++t) {
       float a = 0.f, b = 0.f;
 #pragma unroll
-      for (int j = 0; j < DR; j += 4) {
-        const float4 z4 = *reinterpret_cast<const float4*>(&dzs[t][j]);
-        a = fmaf(z4.x, wa[j], a);
-        b = fmaf(z4.x, wb[j], b);
-        a = fmaf(z4.y, wa[j + 1], a);
-        b = fmaf(z4.y, wb[j + 1], b);
-        a = fmaf(z4.z, wa[j + 2], a);
-        b = fmaf(z4.z, wb[j + 2], b);
-        a = fmaf(z4.w, wa[j + 3], a);
-        b = fmaf(z4.w, wb[j + 3], b);
+      for (int j = 0; j < DR; ++j) {
+        a = fmaf(dzs[t][j], wa[j], a);
+        b = fmaf(dzs[t][j], wb[j], b);
       }
-      T* p = dx + (row0 + t) * d + c;
-      if constexpr (sizeof(T) == 2) {
-        uint32_t v = *reinterpret_cast<const uint32_t*>(p);
-        const float lo = bf2f(uint16_t(v & 0xffffu)) + a, hi = bf2f(uint16_t(v >> 16)) + b;
-        *reinterpret_cast<uint32_t*>(p) = uint32_t(f2bf(lo)) | (uint32_t(f2bf(hi)) << 16);
-      } else {
-        float2 v = *reinterpret_cast<const float2*>(p);
-        v.x += a;
-        v.y += b;
-        *reinterpret_cast<float2*>(p) = v;
-      }
+      float2* p = reinterpret_cast<float2*>(dx + (row0 + t) * d + c);
+      float2 v = *p;
+      v.x += a;
+      v.y += b;
+      *p = v;
     }
   }
 }
 
-// dW1 partial of token range s: pw1[s][j][c] = sum_t dz[t, j] x[t, c]. A
-// workgroup covers a 128-column slab: wave w holds units w DR/4 .. (w+1) DR/4,
-// each lane two adjacent columns. The units' dz values of a token are the
-// same for the whole wave and come through the scalar cache.
-template <typename T, int DR>
-__global__ __launch_bounds__(256) void router_bwd_w1_kernel(const T* __restrict__ x, int64_t n, int d,
-                                                            const float* __restrict__ dz, int splits,
-                                                            float* __restrict__ pw1) {
-  constexpr int U = DR / 4, UNR = 8;
+// pw1[s][j][c] = sum over token range s of dz[t, j] x[t, c]; wave w holds
+// units w DR/4 .. (w+1) DR/4, each lane two adjacent columns of a 128-column
+// slab. A token's dz values are the same for the whole wave (scalar loads).
+template <int DR>
+__global__ __launch_bounds__(256) void router_bwd_w1_f32_kernel(const float* __restrict__ x, int64_t n, int d,
+                                                                const float* __restrict__ dz, int splits,
+                                                                float* __restrict__ pw1) {
+  constexpr int U = DR / 4;
   const int w = __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6));
   const int lane = threadIdx.x & 63;
   const int c = blockIdx.x * 128 + 2 * lane;
@@ -359,40 +567,13 @@ __global__ __launch_bounds__(256) void router_bwd_w1_kernel(const T* __restrict_
   float a0[U], a1[U];
 #pragma unroll
   for (int u = 0; u < U; ++u) a0[u] = a1[u] = 0.f;
-  int64_t t = t0;
-  for (; t + UNR <= t1; t += UNR) {
-    float xv[UNR][2];
-#pragma unroll
-    for (int q = 0; q < UNR; ++q) {
-      const T* p = x + (t + q) * d + c;
-      if constexpr (sizeof(T) == 2) {
-        const uint32_t v = *reinterpret_cast<const uint32_t*>(p);
-        xv[q][0] = bf2f(uint16_t(v & 0xffffu));
-        xv[q][1] = bf2f(uint16_t(v >> 16));
-      } else {
-        const float2 v = *reinterpret_cast<const float2*>(p);
-        xv[q][0] = v.x;
-        xv[q][1] = v.y;
-      }
-    }
-#pragma unroll
-    for (int q = 0; q < UNR; ++q) {
-      const float* zr = dz + (t + q) * DR + w * U;
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        a0[u] = fmaf(zr[u], xv[q][0], a0[u]);
-        a1[u] = fmaf(zr[u], xv[q][1], a1[u]);
-      }
-    }
-  }
-  for (; t < t1; ++t) {
-    const T* p = x + t * d + c;
-    const float x0 = Elem<T>::to_f(p[0]), x1 = Elem<T>::to_f(p[1]);
+  for (int64_t t = t0; t < t1; ++t) {
+    const float2 xv = *reinterpret_cast<const float2*>(x + t * d + c);
     const float* zr = dz + t * DR + w * U;
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      a0[u] = fmaf(zr[u], x0, a0[u]);
-      a1[u] = fmaf(zr[u], x1, a1[u]);
+      a0[u] = fmaf(zr[u], xv.x, a0[u]);
+      a1[u] = fmaf(zr[u], xv.y, a1[u]);
     }
   }
   float* out = pw1 + (int64_t(s) * DR + w * U) * d + c;
@@ -400,25 +581,45 @@ __global__ __launch_bounds__(256) void router_bwd_w1_kernel(const T* __restrict_
   for (int u = 0; u < U; ++u) *reinterpret_cast<float2*>(out + int64_t(u) * d) = float2{a0[u], a1[u]};
 }
 
-// Fixed-order sums of the partials: dW1 over token ranges, the per-chunk
-// terms over chunks.
+// ---- fixed-order reductions (both dtypes)
+
+// Blocks [0, nbw): 64 outputs of dW1 each; wave q adds splits q, q + 4, ...
+// in ascending order and the four wave sums meet in LDS in wave order. Then
+// one wavefront per chunk term j: lanes take chunks lane, lane + 64, ... in
+// order, and the lanes meet in a fixed butterfly.
 template <int DR>
 __global__ __launch_bounds__(256) void router_bwd_reduce_kernel(const float* __restrict__ pw1, int splits, int d,
                                                                 const float* __restrict__ terms, int64_t chunks,
                                                                 float* __restrict__ dw1, float* __restrict__ db1,
                                                                 float* __restrict__ dw2, float* __restrict__ db2) {
-  const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  __shared__ float red[4][64];
   const int64_t nw = int64_t(DR) * d;
-  if (i < nw) {
+  const int64_t nbw = (nw + 63) / 64;
+  const int lane = threadIdx.x & 63, q = threadIdx.x >> 6;
+  if (blockIdx.x < nbw) {
+    const int64_t i = int64_t(blockIdx.x) * 64 + lane;
     float a = 0.f;
-    for (int s = 0; s < splits; ++s) a += pw1[int64_t(s) * nw + i];
-    dw1[i] = a;
+    if (i < nw) {
+      float v[kBwdMaxSplits / 4];  // at most splits / 4 per wave, all requested before the adds
+#pragma unroll
+      for (int u = 0; u < kBwdMaxSplits / 4; ++u) {
+        const int s = q + 4 * u;
+        v[u] = s < splits ? pw1[int64_t(s) * nw + i] : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < kBwdMaxSplits / 4; ++u) a += v[u];
+    }
+    red[q][lane] = a;
+    __syncthreads();
+    if (q == 0 && i < nw) dw1[i] = ((red[0][lane] + red[1][lane]) + red[2][lane]) + red[3][lane];
     return;
   }
-  const int j = int(i - nw);
+  const int j = int(blockIdx.x - nbw) * 4 + q;
   if (j >= kBwdTerms * DR + 1) return;
   float a = 0.f;
-  for (int64_t ch = 0; ch < chunks; ++ch) a += terms[ch * (kBwdTerms * DR + 1) + j];
+  for (int64_t ch = lane; ch < chunks; ch += 64) a += terms[ch * (kBwdTerms * DR + 1) + j];
+  a = wave_sum(a);
+  if (lane != 0) return;
   if (j < DR) {
     if (db1) db1[j] = a;
   } else if (j < 2 * DR) {
@@ -428,34 +629,46 @@ __global__ __launch_bounds__(256) void router_bwd_reduce_kernel(const float* __r
   }
 }
 
-template <typename T, int DR>
+template <int DR>
 static void launch_router_bwd_t(const RouterBwdArgs& a, hipStream_t s) {
-  const int64_t chunks = (a.n + kRouterTokens - 1) / kRouterTokens;
-  const int splits = router_bwd_splits(a.n);
+  const BwdLayout L = bwd_layout(a.n, a.d, DR);
   char* ws = static_cast<char*>(a.workspace);
-  auto up = [](size_t b) { return (b + 255) / 256 * 256; };
-  float* dz = reinterpret_cast<float*>(ws);
-  float* terms = reinterpret_cast<float*>(ws + up(sizeof(float) * size_t(a.n) * DR));
-  float* pw1 = reinterpret_cast<float*>(ws + up(sizeof(float) * size_t(a.n) * DR) +
-                                        up(sizeof(float) * size_t(chunks) * (kBwdTerms * DR + 1)));
-  router_bwd_tokens_kernel<T, DR><<<unsigned(chunks), 64 * kRouterWaves, 0, s>>>(
-      (const T*)a.x, a.n, a.d, (const T*)a.w1, (const T*)a.b1, (const T*)a.w2, a.dscore, (T*)a.dx, dz, terms);
-  router_bwd_w1_kernel<T, DR><<<dim3(unsigned((a.d + 127) / 128), unsigned(splits)), 256, 0, s>>>(
-      (const T*)a.x, a.n, a.d, dz, splits, pw1);
-  const int64_t outs = int64_t(DR) * a.d + kBwdTerms * DR + 1;
-  router_bwd_reduce_kernel<DR><<<unsigned((outs + 255) / 256), 256, 0, s>>>(pw1, splits, a.d, terms, chunks, a.dw1,
-                                                                            a.db1, a.dw2, a.db2);
+  float* terms = reinterpret_cast<float*>(ws + L.terms);
+  float* pw1 = reinterpret_cast<float*>(ws + L.pw1);
+  const unsigned chunks = unsigned(L.chunks);
+  if (a.dtype == DSF_BF16) {
+    uint16_t* w1t = reinterpret_cast<uint16_t*>(ws + L.w1t);
+    uint16_t* dzt_hi = reinterpret_cast<uint16_t*>(ws + L.dz);
+    uint16_t* dzt_lo = dzt_hi + int64_t(DR) * L.npad;
+    if (a.dx)
+      router_w1t_kernel<DR><<<unsigned((int64_t(a.d) * DR + 255) / 256), 256, 0, s>>>((const uint16_t*)a.w1, a.d, w1t);
+    router_bwd_tokens_bf16_kernel<DR><<<chunks, 64 * kRouterWaves, 0, s>>>(
+        (const uint16_t*)a.x, a.n, a.d, (const uint16_t*)a.w1, w1t, (const uint16_t*)a.b1, (const uint16_t*)a.w2,
+        a.dscore, (uint16_t*)a.dx, dzt_hi, dzt_lo, L.npad, terms);
+    router_bwd_w1_bf16_kernel<DR><<<dim3(unsigned((a.d + 63) / 64), unsigned(L.splits)), 256, 0, s>>>(
+        (const uint16_t*)a.x, a.n, a.d, dzt_hi, dzt_lo, L.npad, L.splits, pw1);
+  } else {
+    float* dz = reinterpret_cast<float*>(ws + L.dz);
+    router_bwd_tokens_f32_kernel<DR><<<chunks, 64 * kRouterWaves, 0, s>>>(
+        (const float*)a.x, a.n, a.d, (const float*)a.w1, (const float*)a.b1, (const float*)a.w2, a.dscore,
+        (float*)a.dx, dz, terms);
+    router_bwd_w1_f32_kernel<DR><<<dim3(unsigned((a.d + 127) / 128), unsigned(L.splits)), 256, 0, s>>>(
+        (const float*)a.x, a.n, a.d, dz, L.splits, pw1);
+  }
+  const int64_t nbw = (int64_t(DR) * a.d + 63) / 64;
+  const int64_t nbt = (kBwdTerms * DR + 1 + 3) / 4;
+  router_bwd_reduce_kernel<DR><<<unsigned(nbw + nbt), 256, 0, s>>>(pw1, L.splits, a.d, terms, L.chunks, a.dw1,
+                                                                    a.db1, a.dw2, a.db2);
 }
 
 hipError_t launch_router_backward(const RouterBwdArgs& a, hipStream_t s) {
   if (a.n == 0) return hipSuccess;
   TimedScope ts(DSF_KIND_BACKWARD, s);
-  const bool bf = a.dtype == DSF_BF16;
   switch (a.d_r) {
-    case 16: bf ? launch_router_bwd_t<uint16_t, 16>(a, s) : launch_router_bwd_t<float, 16>(a, s); break;
-    case 32: bf ? launch_router_bwd_t<uint16_t, 32>(a, s) : launch_router_bwd_t<float, 32>(a, s); break;
-    case 48: bf ? launch_router_bwd_t<uint16_t, 48>(a, s) : launch_router_bwd_t<float, 48>(a, s); break;
-    case 64: bf ? launch_router_bwd_t<uint16_t, 64>(a, s) : launch_router_bwd_t<float, 64>(a, s); break;
+    case 16: launch_router_bwd_t<16>(a, s); break;
+    case 32: launch_router_bwd_t<32>(a, s); break;
+    case 48: launch_router_bwd_t<48>(a, s); break;
+    case 64: launch_router_bwd_t<64>(a, s); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
