@@ -34,6 +34,9 @@ Readings taken where the paper is silent or ambiguous (each also in the design doc):
   sequential residual, RMSNorm, SwiGLU, full rotary and GQA. Eq. 3 is a
   post-norm schematic that matches neither model.
 * The router reads the raw residual-stream row: score = w2 . ReLU(W1 x + b1) + b2.
+* Eq. 9's softmax runs over the hidden dimension of each token, and its
+  2-norm is taken over the layer's whole hidden-state tensor. Eq. 10 is
+  evaluated per row of logits, with the classes on the last axis.
 
 Parity status: every function here is pinned by the CPU tests (closed forms,
 invariants, brute force, and library cross-checks against torch and the
@@ -465,3 +468,68 @@ def router_backward(x, w1, b1, w2, dscore) -> Dict[str, np.ndarray]:
     return {"dw1": dz.T @ xt, "db1": dz.sum(axis=0), "dw2": h.T @ ds, "db2": float(ds.sum()),
             "dx": (dz @ w1).reshape(x.shape)}
 
+
+
+# ---------------------------------------------------------------------------
+# Section 3.5: feature-preserving alignment (Eqs. 9-11)
+# ---------------------------------------------------------------------------
+
+def softmax_rows(h) -> np.ndarray:
+    """Softmax over the last axis, shifted by the row maximum."""
+    h = f64(h)
+    e = np.exp(h - h.max(axis=-1, keepdims=True))
+    return e / e.sum(axis=-1, keepdims=True)
+
+
+def hidden_align_sq(h_sparse, h_dense) -> np.ndarray:
+    """Per-token squared distance of Eq. 9: sum over the hidden dimension of
+    (Softmax(h_sparse) - Softmax(h_dense))^2, the softmax taken over the
+    hidden dimension of each token. Returns the leading shape of the inputs."""
+    d = softmax_rows(h_sparse) - softmax_rows(h_dense)
+    return np.sum(d * d, axis=-1)
+
+
+def hidden_align_loss(h_sparse, h_dense) -> float:
+    """Eq. 9 for one layer: the 2-norm of the difference of the per-token
+    softmaxes, over the whole [B, T, d] hidden-state tensor (the entrywise
+    norm of the matrix difference)."""
+    return float(math.sqrt(np.sum(hidden_align_sq(h_sparse, h_dense))))
+
+
+def log_softmax_rows(z) -> np.ndarray:
+    """log Softmax over the last axis: z - max - log sum exp(z - max)."""
+    z = f64(z)
+    m = z.max(axis=-1, keepdims=True)
+    return z - m - np.log(np.sum(np.exp(z - m), axis=-1, keepdims=True))
+
+
+def kl_align(logits_dense, logits_sparse) -> np.ndarray:
+    """Eq. 10 per row: sum_c P_dense(c) log(P_dense(c) / P_sparse(c)) with
+    P = Softmax(logits) over the classes (last axis)."""
+    lp = log_softmax_rows(logits_dense)
+    lq = log_softmax_rows(logits_sparse)
+    return np.sum(np.exp(lp) * (lp - lq), axis=-1)
+
+
+def total_objective(l_align: float, l_hid: Sequence[float]) -> float:
+    """Eq. 11: L_align + (1 / L) sum_l L_hid^(l)."""
+    return float(l_align + np.mean(np.asarray(l_hid, dtype=np.float64)))
+
+
+def align_stack(desc: Dict, Ws: List[Dict], x, ks: Sequence[int]) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
+    """Dense-teacher / sparse-student forward (Section 3.5): both stacks start
+    from the same input; after layer l, Eq. 9 compares the student's hidden
+    states (routed layers) with the teacher's (dense layers).
+
+    Returns (per-layer sums of the per-token squared distances, the student's
+    final hidden states, the teacher's). L_hid^(l) is the square root of the
+    l-th sum.
+    """
+    xs = f64(x)
+    xd = f64(x)
+    sums = []
+    for W, k in zip(Ws, ks):
+        xd = dense_layer(desc, W, xd)
+        xs = routed_layer(desc, W, xs, int(k))["y"] if k > 0 else xs
+        sums.append(float(np.sum(hidden_align_sq(xs, xd))))
+    return np.asarray(sums), xs, xd
