@@ -209,6 +209,67 @@ def router_pathway(P, C, w, ks, dev, desc, weights, x0, ws, ms_plain, steps, wei
     return out
 
 
+# vocabulary sizes of the two model families (logit rows of Eq. 10)
+VOCAB = {"neox_parallel": 50304, "qwen_seq": 151936}
+
+
+def alignment_objective(P, C, w, ks, dev, desc, weights, x0, ms_plain, steps):
+    """Section 3.5: the dense-teacher / sparse-student stack with Eq. 9 per
+    layer, against the sparse stack alone; and the Eq. 9 and Eq. 10 kernels
+    standalone (Eq. 10 on synthetic logits of the model family's vocabulary
+    for every token of the batch)."""
+    import torch
+    B, T, d = w.batch, w.seq, w.d_model
+    eb = 4 if w.dtype == "f32" else 2
+    dcode = P.F32 if w.dtype == "f32" else P.BF16
+    out = {}
+    ws = torch.empty(P.align_stack_workspace_size(desc, dcode, B, T), dtype=torch.uint8, device=dev)
+    hid = torch.zeros(w.n_layers, dtype=torch.float64, device=dev)
+    xs, xt = x0.clone(), x0.clone()
+    P.align_stack_forward(desc, weights, ks, xs, xt, hid, ws)
+    n_steps = max(2, steps)
+    pairs = [(x0.clone(), x0.clone()) for _ in range(n_steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for a, b in pairs:
+        P.align_stack_forward(desc, weights, ks, a, b, hid, ws)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / n_steps
+    out["align_stack"] = {"ms_per_step": ms, "tokens_per_s": B * T / (ms / 1e3), "vs_sparse_stack": ms / ms_plain,
+                          "note": "dense teacher + sparse student + Eq. 9 per layer"}
+    del pairs, ws
+    # Eq. 9 kernel standalone, cold (inputs cycled through > 1 GiB) and hot
+    n = B * T
+    nbytes = C.align_hidden_bytes(w, n)
+    R = max(4, -(-(1 << 30) // int(nbytes)) + 1)
+    hs = [torch.randn(B, T, d, device=dev).to(w.torch_dtype) for _ in range(R)]
+    hd = [torch.randn(B, T, d, device=dev).to(w.torch_dtype) for _ in range(R)]
+    acc = torch.zeros(1, dtype=torch.float64, device=dev)
+    aws = torch.empty(P.align_workspace_size(n), dtype=torch.uint8, device=dev)
+    fn = lambda i: P.align_hidden(hs[i], hd[i], acc, workspace=aws)
+    res = {"bytes_per_call": nbytes}
+    for mode in ("cold", "hot"):
+        fn(0)
+        us = _timed(fn, 3 * R, (lambda i: i % R) if mode == "cold" else (lambda i: 0))
+        res[mode] = {"us": us, "GB/s": nbytes / (us * 1e-6) / 1e9, "frac_of_hbm_peak": nbytes / (us * 1e-6) / 1e9 / PEAK_HBM_GBS}
+    out["align_hidden"] = res
+    del hs, hd
+    # Eq. 10 over B*T rows of the family's vocabulary (each call streams far more than the MALL)
+    V = VOCAB[w.block]
+    ld = torch.randn(n, V, device=dev).mul_(3.0).to(w.torch_dtype)
+    ls = (ld.float() + torch.randn(n, V, device=dev).mul_(0.5)).to(w.torch_dtype)
+    kws = torch.empty(P.align_workspace_size(n), dtype=torch.uint8, device=dev)
+    fn = lambda i: P.kl_align(ld, ls, acc, workspace=kws)
+    nbytes = C.kl_align_bytes(eb, n, V)
+    fn(0)
+    us = _timed(fn, 3, lambda i: 0)
+    out["kl_align"] = {"rows": n, "classes": V, "bytes_per_call": nbytes, "us": us,
+                       "GB/s": nbytes / (us * 1e-6) / 1e9, "frac_of_hbm_peak": nbytes / (us * 1e-6) / 1e9 / PEAK_HBM_GBS}
+    del ld, ls
+    torch.cuda.empty_cache()
+    return out
+
+
 def cpu_baseline(w, ks, layers, min_seconds=10.0):
     """The oracle, as it stands, on whole sequences through `layers` layers.
 
@@ -467,6 +528,10 @@ def main():
         log("router-score pathway: gated stack, gate score gradient, router backward")
         out["router_score_pathway"] = router_pathway(P, C, w, ks, dev, desc, weights, x0, ws, ms_step,
                                                      max(3, args.steps // 3), S.layer_weights(w, 0))
+    if not args.only_sparse:
+        log("alignment objective: teacher/student stack, Eq. 9 and Eq. 10 kernels")
+        out["alignment_objective"] = alignment_objective(P, C, w, ks, dev, desc, weights, x0, ms_step,
+                                                         max(3, args.steps // 3))
     if not args.no_cpu_baseline:
         layers_cpu = L if args.cpu_layers is None else min(args.cpu_layers, L)
         log(f"cpu oracle baseline over {layers_cpu} layers of one sequence")

@@ -299,6 +299,52 @@ int dsf_stack_forward(const dsf_layer_desc* desc, const dsf_layer_weights* weigh
                       double* sim_accum, void* workspace, size_t workspace_bytes,
                       hipStream_t stream);
 
+/* ------------------------- alignment objective (Section 3.5, Eqs. 9-11) */
+
+/* Workspace bytes of dsf_align_hidden and dsf_kl_align for n_rows rows (0 on
+ * a bad argument). No initialisation needed; overlapping calls need separate
+ * workspaces. */
+size_t dsf_align_workspace_size(int64_t n_rows);
+
+/* Eq. 9 summand: for each of n_tokens rows of h_sparse and h_dense ([n_tokens,
+ * d] in dtype, 16-byte aligned), with softmax over the row's d features,
+ *   sq[t] = sum_c (softmax(h_sparse[t])_c - softmax(h_dense[t])_c)^2,
+ * and accum[0] += sum_t sq[t] (device double, added to). The layer's loss is
+ * L_hid = sqrt(accum[0]) (the 2-norm over the whole hidden-state tensor).
+ * per_token_sq (nullable, device float [n_tokens]) receives sq. Exponentials
+ * in fp32, normalisers and sums in fp64, in an order fixed by the shape.
+ * d a multiple of 8, at most 8192 (bf16) / 4096 (fp32). */
+int dsf_align_hidden(const void* h_sparse, const void* h_dense, int dtype, int64_t n_tokens, int d,
+                     float* per_token_sq, double* accum, void* workspace, size_t workspace_bytes,
+                     hipStream_t stream);
+
+/* Eq. 10 per row: KL(P_dense || P_sparse) = sum_c P_dense(c) log(P_dense(c) / P_sparse(c))
+ * with P = softmax over the n_classes logits of a row. logits_dense and
+ * logits_sparse are [n_rows, n_classes] in dtype, 16-byte aligned, n_classes a
+ * multiple of 8. per_row_kl (nullable, device float [n_rows]) receives each
+ * row's KL; accum[0] += their sum (device double). One pass over the logits
+ * with an online maximum; exponentials fp32, sums fp64, fixed order. */
+int dsf_kl_align(const void* logits_dense, const void* logits_sparse, int dtype, int64_t n_rows,
+                 int n_classes, float* per_row_kl, double* accum, void* workspace,
+                 size_t workspace_bytes, hipStream_t stream);
+
+/* Workspace bytes of dsf_align_stack_forward (0 on a bad argument). */
+size_t dsf_align_stack_workspace_size(const dsf_layer_desc* desc, int dtype, int B, int T);
+
+/* Dense-teacher / sparse-student forward of Section 3.5. x_sparse and x_dense
+ * ([B, T, d] in dtype) hold the same input on entry. For l = 0..L-1:
+ *   x_dense <- dense layer l (every token), x_sparse <- sparse layer l with
+ *   k[l] kept tokens (as dsf_stack_forward), then
+ *   hid_accum[l] += sum over tokens of the Eq. 9 summand of (x_sparse, x_dense).
+ * L_hid^(l) = sqrt(hid_accum[l]); Eq. 11 is L_align + mean_l L_hid^(l).
+ * hid_accum: device double [L], added to. flags: 0 or DSF_FLAG_GATE (the
+ * student's gated update); DSF_FLAG_DENSE is rejected. d_model at most 8192
+ * (bf16) / 4096 (fp32). */
+int dsf_align_stack_forward(const dsf_layer_desc* desc, const dsf_layer_weights* weights, int L,
+                            int dtype, const int* k, void* x_sparse, void* x_dense, int B, int T,
+                            int flags, double* hid_accum, void* workspace, size_t workspace_bytes,
+                            hipStream_t stream);
+
 /* ------------------------------------------------------- kernel timing */
 
 /* Per-kernel timing with HIP events recorded around each launch on the
@@ -312,7 +358,7 @@ enum {
   DSF_KIND_SIM = 0, DSF_KIND_ROUTER = 1, DSF_KIND_TOPK = 2, DSF_KIND_NORM = 3,
   DSF_KIND_GEMM_QKV = 4, DSF_KIND_ATTN = 5, DSF_KIND_GEMM_O = 6, DSF_KIND_GEMM_UP = 7,
   DSF_KIND_GEMM_DOWN = 8, DSF_KIND_GATHER = 9, DSF_KIND_SCATTER = 10, DSF_KIND_OTHER = 11,
-  DSF_KIND_BACKWARD = 12, DSF_KIND_COUNT = 13
+  DSF_KIND_BACKWARD = 12, DSF_KIND_ALIGN = 13, DSF_KIND_COUNT = 14
 };
 int dsf_timing_enable(int max_records, uint32_t kind_mask);
 int dsf_timing_read(int kind, int* launches, double* total_ms);

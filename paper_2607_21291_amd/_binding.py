@@ -22,7 +22,7 @@ FLAG_DENSE, FLAG_GATE = 1, 2
 CLIP = {"none": 0, "plain": 1, "budget": 2}
 ROUNDING = {"floor": 0, "ceil": 1}
 KINDS = ["sim", "router", "topk", "norm", "gemm_qkv", "attn", "gemm_o", "gemm_up", "gemm_down",
-         "gather", "scatter", "other", "backward"]
+         "gather", "scatter", "other", "backward", "align"]
 
 STATUS = {0: "DSF_OK", 1: "DSF_EINVAL", 2: "DSF_EUNSUPPORTED", 3: "DSF_EWORKSPACE", 4: "DSF_EHIP",
           5: "DSF_ENODEVICE"}
@@ -33,6 +33,8 @@ EXPORTS = [
     "dsf_gather_rows", "dsf_scatter_residual", "dsf_attention_forward", "dsf_workspace_size",
     "dsf_sparse_block_forward", "dsf_stack_forward", "dsf_timing_enable", "dsf_timing_read",
     "dsf_gate_score_grad", "dsf_router_backward_workspace_size", "dsf_router_backward",
+    "dsf_align_workspace_size", "dsf_align_hidden", "dsf_kl_align", "dsf_align_stack_workspace_size",
+    "dsf_align_stack_forward",
 ]
 
 
@@ -93,6 +95,11 @@ def lib() -> ctypes.CDLL:
         "dsf_gate_score_grad": ([vp, vp, vp, i32, vp, vp, i32, i32, i32, i32, vp, vp], i32),
         "dsf_router_backward_workspace_size": ([i64, i32, i32], sz),
         "dsf_router_backward": ([vp, i32, i64, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp], i32),
+        "dsf_align_workspace_size": ([i64], sz),
+        "dsf_align_hidden": ([vp, vp, i32, i64, i32, vp, vp, vp, sz, vp], i32),
+        "dsf_kl_align": ([vp, vp, i32, i64, i32, vp, vp, vp, sz, vp], i32),
+        "dsf_align_stack_workspace_size": ([vp, i32, i32, i32], sz),
+        "dsf_align_stack_forward": ([vp, vp, i32, i32, vp, vp, vp, i32, i32, i32, vp, vp, sz, vp], i32),
     }
     for name, (args, res) in sig.items():
         fn = getattr(L, name)
@@ -255,6 +262,46 @@ def stack_forward(desc: LayerDesc, weights: Sequence[LayerWeights], ks: Sequence
            lib().dsf_stack_forward(ctypes.addressof(desc), ctypes.addressof(arr), L, _dtype_code(x),
                                    ctypes.addressof(karr), _ptr(x), B, T, flags, _ptr(sim_accum), _ptr(workspace),
                                    workspace.numel(), _stream(stream)))
+
+
+def align_workspace_size(n_rows: int) -> int:
+    return lib().dsf_align_workspace_size(n_rows)
+
+
+def align_hidden(h_sparse, h_dense, accum, per_token_sq=None, workspace=None, stream=None):
+    d = h_sparse.shape[-1]
+    n = h_sparse.numel() // d
+    if workspace is None:
+        workspace = torch.empty(align_workspace_size(n), dtype=torch.uint8, device=h_sparse.device)
+    _check("dsf_align_hidden", lib().dsf_align_hidden(_ptr(h_sparse), _ptr(h_dense), _dtype_code(h_sparse), n, d,
+                                                      _ptr(per_token_sq), _ptr(accum), _ptr(workspace),
+                                                      workspace.numel(), _stream(stream)))
+
+
+def kl_align(logits_dense, logits_sparse, accum, per_row_kl=None, workspace=None, stream=None):
+    C = logits_dense.shape[-1]
+    n = logits_dense.numel() // C
+    if workspace is None:
+        workspace = torch.empty(align_workspace_size(n), dtype=torch.uint8, device=logits_dense.device)
+    _check("dsf_kl_align", lib().dsf_kl_align(_ptr(logits_dense), _ptr(logits_sparse), _dtype_code(logits_dense), n,
+                                              C, _ptr(per_row_kl), _ptr(accum), _ptr(workspace), workspace.numel(),
+                                              _stream(stream)))
+
+
+def align_stack_workspace_size(desc: LayerDesc, dtype: int, B: int, T: int) -> int:
+    return lib().dsf_align_stack_workspace_size(ctypes.addressof(desc), dtype, B, T)
+
+
+def align_stack_forward(desc: LayerDesc, weights: Sequence[LayerWeights], ks: Sequence[int], x_sparse, x_dense,
+                        hid_accum, workspace, flags: int = 0, stream=None):
+    B, T, _ = x_sparse.shape
+    L = len(weights)
+    arr = (LayerWeights * max(L, 1))(*weights)
+    karr = (ctypes.c_int * max(L, 1))(*[int(k) for k in ks])
+    _check("dsf_align_stack_forward",
+           lib().dsf_align_stack_forward(ctypes.addressof(desc), ctypes.addressof(arr), L, _dtype_code(x_sparse),
+                                         ctypes.addressof(karr), _ptr(x_sparse), _ptr(x_dense), B, T, flags,
+                                         _ptr(hid_accum), _ptr(workspace), workspace.numel(), _stream(stream)))
 
 
 def timing_enable(max_records: int, kinds: Optional[Sequence[str]] = None):

@@ -97,6 +97,17 @@ def router_bwd_flops(w, n: int) -> float:
     return 6.0 * n * w.d_model * w.d_router
 
 
+def align_hidden_bytes(w, n: int) -> float:
+    """Eq. 9 summand over n tokens: both hidden rows read."""
+    eb = 4 if w.dtype == "f32" else 2
+    return 2.0 * eb * n * w.d_model
+
+
+def kl_align_bytes(eb: int, rows: int, classes: int) -> float:
+    """Eq. 10 over rows of logits: both logit rows read, one float written."""
+    return 2.0 * eb * rows * classes + 4.0 * rows
+
+
 def kind_work(w, kind: str, B: int, T: int, k: int):
     """(work, unit) of one layer's launches of a kernel kind: flops for the
     MFMA kernels, bytes for the streaming ones; None for kinds not modelled."""

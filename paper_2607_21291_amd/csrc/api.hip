@@ -432,12 +432,13 @@ extern "C" int dsf_attention_forward(const void* q, const void* k, const void* v
 
 namespace {
 struct Plan {
-  size_t scores, idx, a1, a2, q, k, v, attn, act, h, m2, rope, xin, simpart, skpart, skflags, total;
+  size_t scores, idx, a1, a2, q, k, v, attn, act, h, m2, rope, xin, simpart, alignpart, skpart, skflags, total;
 };
 
 size_t up256(size_t x) { return (x + 255) / 256 * 256; }
 
-Plan make_plan(const dsf_layer_desc& D, int dtype, int B, int T, int k_max, bool with_sim) {
+Plan make_plan(const dsf_layer_desc& D, int dtype, int B, int T, int k_max, bool with_sim,
+               bool with_align = false) {
   const size_t eb = elem_bytes(dtype);
   const size_t N = size_t(B) * size_t(k_max);
   const bool qwen = D.block == DSF_BLOCK_QWEN_SEQ;
@@ -462,6 +463,7 @@ Plan make_plan(const dsf_layer_desc& D, int dtype, int B, int T, int k_max, bool
   p.rope = take(4 * size_t(T) * D.rotary_dims);
   p.xin = with_sim ? take(eb * size_t(B) * T * D.d_model) : 0;
   p.simpart = with_sim ? take(dsf_sim_workspace_size(int64_t(B) * T)) : 0;
+  p.alignpart = with_align ? take(sizeof(double) * size_t(align_grid(int64_t(B) * T))) : 0;
   // stream-K partial tiles and their flags (bf16 GEMMs)
   p.skpart = dtype == DSF_BF16 ? take(gemm_partial_bytes()) : 0;
   p.skflags = dtype == DSF_BF16 ? take(sizeof(uint32_t) * gemm_flag_count()) : 0;
@@ -692,7 +694,7 @@ int run_layer(const Ctx& c, const dsf_layer_weights* W, void* x, int k, bool den
 }
 
 int check_common(const dsf_layer_desc* desc, int dtype, void* x, int B, int T, int k_max, int flags,
-                 void* workspace, size_t workspace_bytes, bool with_sim, Plan* plan) {
+                 void* workspace, size_t workspace_bytes, bool with_sim, Plan* plan, bool with_align = false) {
   int rc = check_desc(desc);
   if (rc) return rc;
   rc = check_dtype(dtype);
@@ -705,7 +707,7 @@ int check_common(const dsf_layer_desc* desc, int dtype, void* x, int B, int T, i
   if (B == 0 || T == 0 || k_max == 0) return DSF_OK;
   DSF_CHECK(x, DSF_EINVAL, "x is null");
   DSF_CHECK(aligned16(x), DSF_EINVAL, "x must be 16-byte aligned");
-  *plan = make_plan(*desc, dtype, B, T, k_max, with_sim);
+  *plan = make_plan(*desc, dtype, B, T, k_max, with_sim, with_align);
   DSF_CHECK(workspace_bytes >= plan->total, DSF_EWORKSPACE, "workspace needs %zu bytes, got %zu", plan->total,
             workspace_bytes);
   DSF_CHECK(workspace && (reinterpret_cast<uintptr_t>(workspace) & 255u) == 0, DSF_EINVAL,
@@ -775,6 +777,96 @@ extern "C" int dsf_stack_forward(const dsf_layer_desc* desc, const dsf_layer_wei
     if (with_sim)
       DSF_HIP(launch_sim_stats(dtype, at<char>(c, plan.xin), x, int64_t(B) * T, desc->d_model, nullptr,
                                at<double>(c, plan.simpart), sim_accum + 2 * l, stream));
+  }
+  return DSF_OK;
+}
+
+// ------------------------------------------- alignment objective (Sec. 3.5)
+
+extern "C" size_t dsf_align_workspace_size(int64_t n_rows) {
+  if (n_rows < 0) return 0;
+  return up256(sizeof(double) * size_t(n_rows > 0 ? n_rows : 1));
+}
+
+extern "C" int dsf_align_hidden(const void* h_sparse, const void* h_dense, int dtype, int64_t n_tokens, int d,
+                                float* per_token_sq, double* accum, void* workspace, size_t workspace_bytes,
+                                hipStream_t stream) {
+  int rc = check_dtype(dtype);
+  if (rc) return rc;
+  DSF_CHECK(n_tokens >= 0 && n_tokens < (int64_t(1) << 40), DSF_EINVAL, "bad n_tokens");
+  DSF_CHECK(d > 0 && d % 8 == 0 && d <= align_max_d(dtype), DSF_EUNSUPPORTED,
+            "d must be a positive multiple of 8, at most %d for this dtype", align_max_d(dtype));
+  if (n_tokens == 0) return DSF_OK;
+  DSF_CHECK(h_sparse && h_dense && accum, DSF_EINVAL, "null pointer");
+  DSF_CHECK(aligned16(h_sparse) && aligned16(h_dense), DSF_EINVAL, "hidden states must be 16-byte aligned");
+  DSF_CHECK(workspace && workspace_bytes >= dsf_align_workspace_size(n_tokens), DSF_EWORKSPACE,
+            "workspace needs %zu bytes", dsf_align_workspace_size(n_tokens));
+  rc = check_device();
+  if (rc) return rc;
+  DSF_HIP(launch_align_hidden(dtype, h_sparse, h_dense, n_tokens, d, per_token_sq, (double*)workspace, accum,
+                              stream));
+  return DSF_OK;
+}
+
+extern "C" int dsf_kl_align(const void* logits_dense, const void* logits_sparse, int dtype, int64_t n_rows,
+                            int n_classes, float* per_row_kl, double* accum, void* workspace, size_t workspace_bytes,
+                            hipStream_t stream) {
+  int rc = check_dtype(dtype);
+  if (rc) return rc;
+  DSF_CHECK(n_rows >= 0 && n_rows < (int64_t(1) << 31), DSF_EINVAL, "bad n_rows");
+  DSF_CHECK(n_classes > 0 && n_classes % 8 == 0, DSF_EUNSUPPORTED, "n_classes must be a positive multiple of 8");
+  if (n_rows == 0) return DSF_OK;
+  DSF_CHECK(logits_dense && logits_sparse && accum, DSF_EINVAL, "null pointer");
+  DSF_CHECK(aligned16(logits_dense) && aligned16(logits_sparse), DSF_EINVAL, "logits must be 16-byte aligned");
+  DSF_CHECK(workspace && workspace_bytes >= dsf_align_workspace_size(n_rows), DSF_EWORKSPACE,
+            "workspace needs %zu bytes", dsf_align_workspace_size(n_rows));
+  rc = check_device();
+  if (rc) return rc;
+  DSF_HIP(launch_kl_align(dtype, logits_dense, logits_sparse, n_rows, n_classes, per_row_kl, (double*)workspace,
+                          accum, stream));
+  return DSF_OK;
+}
+
+extern "C" size_t dsf_align_stack_workspace_size(const dsf_layer_desc* desc, int dtype, int B, int T) {
+  if (check_desc(desc) || check_dtype(dtype) || B < 0 || T < 0) return 0;
+  if (desc->d_model > align_max_d(dtype)) return 0;
+  return make_plan(*desc, dtype, B, T, T, false, true).total;
+}
+
+extern "C" int dsf_align_stack_forward(const dsf_layer_desc* desc, const dsf_layer_weights* weights, int L,
+                                       int dtype, const int* k, void* x_sparse, void* x_dense, int B, int T,
+                                       int flags, double* hid_accum, void* workspace, size_t workspace_bytes,
+                                       hipStream_t stream) {
+  DSF_CHECK(L >= 0, DSF_EINVAL, "L < 0");
+  DSF_CHECK(L == 0 || (weights && k && hid_accum), DSF_EINVAL, "null weights, k or hid_accum");
+  DSF_CHECK((flags & DSF_FLAG_DENSE) == 0, DSF_EINVAL, "the student cannot be dense (DSF_FLAG_DENSE)");
+  for (int l = 0; l < L; ++l) DSF_CHECK(k[l] >= 0 && k[l] <= T, DSF_EINVAL, "k[%d]=%d outside [0, T=%d]", l, k[l], T);
+  Plan plan{};
+  int rc = check_common(desc, dtype, x_sparse, B, T, T, flags, workspace, workspace_bytes, false, &plan, true);
+  if (rc) return rc;
+  if (L == 0 || B == 0 || T == 0) return DSF_OK;
+  DSF_CHECK(desc->d_model <= align_max_d(dtype), DSF_EUNSUPPORTED, "d_model above %d", align_max_d(dtype));
+  DSF_CHECK(x_dense && aligned16(x_dense), DSF_EINVAL, "x_dense must be non-null and 16-byte aligned");
+  for (int l = 0; l < L; ++l) {
+    rc = check_weights(*desc, &weights[l], l);
+    if (rc) return rc;
+  }
+  rc = check_device();
+  if (rc) return rc;
+  Ctx c{desc, dtype, B, T, (char*)workspace, plan, stream, 0};
+  rc = reset_stream_k(c);
+  if (rc) return rc;
+  DSF_HIP(launch_rope_table(at<float>(c, plan.rope), T, desc->rotary_dims, desc->rope_theta, stream));
+  const bool gate = (flags & DSF_FLAG_GATE) != 0;
+  for (int l = 0; l < L; ++l) {
+    rc = run_layer(c, &weights[l], x_dense, T, true, false, nullptr, nullptr, nullptr);  // teacher
+    if (rc) return rc;
+    if (k[l] > 0) {
+      rc = run_layer(c, &weights[l], x_sparse, k[l], false, gate, nullptr, nullptr, nullptr);  // student
+      if (rc) return rc;
+    }
+    DSF_HIP(launch_align_hidden(dtype, x_sparse, x_dense, int64_t(B) * T, desc->d_model, nullptr,
+                                at<double>(c, plan.alignpart), hid_accum + l, stream));
   }
   return DSF_OK;
 }

@@ -44,6 +44,16 @@ struct RouterBwdArgs {
 size_t router_bwd_workspace_bytes(int64_t n, int d, int d_r);
 hipError_t launch_router_backward(const RouterBwdArgs& a, hipStream_t s);
 
+// ---- alignment objective, Section 3.5 (kernels_align.hip) ----
+int align_grid(int64_t n_tokens);  // blocks of the Eq. 9 kernel (partials written)
+int align_max_d(int dtype);        // widest hidden row the Eq. 9 kernel keeps in registers
+// accum[0] += sum over tokens of sum_c (softmax(hs) - softmax(hd))^2; partial: align_grid(n) doubles
+hipError_t launch_align_hidden(int dtype, const void* hs, const void* hd, int64_t n, int d, float* per_tok,
+                               double* partial, double* accum, hipStream_t s);
+// accum[0] += sum over rows of KL(softmax(ld) || softmax(ls)); partial: rows doubles
+hipError_t launch_kl_align(int dtype, const void* ld, const void* ls, int64_t rows, int C, float* per_row,
+                           double* partial, double* accum, hipStream_t s);
+
 // ---- streaming kernels (kernels_misc.hip) ----
 // table[p][i] = (cos, sin)(p * theta^(-2i/R)), p < T, i < R/2, computed in fp64.
 hipError_t launch_rope_table(float* table, int T, int R, double theta, hipStream_t s);

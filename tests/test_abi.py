@@ -179,6 +179,27 @@ def test_error_paths_of_the_kernel_calls():
     assert rb(FAKE, 1, 1000, 64, 32, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE + 8, FAKE, ws,
               None) == 1
     assert rb(FAKE, 1, 1000, 64, 32, FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE, FAKE, None, FAKE, ws, None) == 1
+    # alignment objective
+    assert L.dsf_align_workspace_size(-1) == 0 and L.dsf_align_workspace_size(1000) >= 8000
+    assert L.dsf_align_hidden(FAKE, FAKE, 1, 100, 12, None, FAKE, FAKE, 1 << 20, None) == 2      # d % 8
+    assert L.dsf_align_hidden(FAKE, FAKE, 1, 100, 8200, None, FAKE, FAKE, 1 << 20, None) == 2    # d > 8192
+    assert L.dsf_align_hidden(FAKE, FAKE, 0, 100, 4104, None, FAKE, FAKE, 1 << 20, None) == 2    # fp32 d > 4096
+    assert L.dsf_align_hidden(FAKE, FAKE, 1, 100, 64, None, FAKE, FAKE, 16, None) == 3           # workspace
+    assert L.dsf_align_hidden(FAKE, FAKE, 1, 100, 64, None, None, FAKE, 1 << 20, None) == 1      # accum
+    assert L.dsf_kl_align(FAKE, FAKE, 1, 10, 50257, None, FAKE, FAKE, 1 << 20, None) == 2        # C % 8
+    assert L.dsf_kl_align(FAKE + 8, FAKE, 1, 10, 64, None, FAKE, FAKE, 1 << 20, None) == 1       # alignment
+    assert L.dsf_align_hidden(None, None, 1, 0, 64, None, None, None, 0, None) == 0              # empty
+    d = _desc()
+    ks = (ctypes.c_int * 2)(32, 16)
+    aws = L.dsf_align_stack_workspace_size(ctypes.addressof(d), P.F32, 2, 64)
+    assert aws >= P.workspace_size(d, P.F32, 2, 64, 64)
+    wts = (P.LayerWeights * 2)(_weights(), _weights())
+    assert L.dsf_align_stack_forward(ctypes.addressof(d), ctypes.addressof(wts), 2, P.F32, ctypes.addressof(ks),
+                                     FAKE, FAKE, 2, 64, 1, FAKE, FAKE, aws, None) == 1           # DENSE student
+    assert L.dsf_align_stack_forward(ctypes.addressof(d), ctypes.addressof(wts), 2, P.F32, ctypes.addressof(ks),
+                                     FAKE, FAKE, 2, 64, 0, FAKE, FAKE, aws - 256, None) == 3     # workspace
+    assert L.dsf_align_stack_forward(ctypes.addressof(d), ctypes.addressof(wts), 2, P.F32, ctypes.addressof(ks),
+                                     FAKE, FAKE, 2, 64, 0, None, FAKE, aws, None) == 1           # hid_accum
     # empty problems are valid no-ops
     assert L.dsf_topk_select(None, 0, 10, 3, None, None) == 0
     assert L.dsf_gather_rows(None, 1, 2, 10, 16, None, 0, None, None) == 0
