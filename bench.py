@@ -40,8 +40,8 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 # library's plain copy kernel of known size. It holds only for the workload
 # and the GEMM source it was measured on (SHA-256 of kernels_gemm.hip); for
 # anything else `traffic` is null.
-TRAFFIC_MEASURED = {"workload": "neox160m", "bytes_per_launch": 1.489e+08,
-                    "gemm_source_sha256": "acb473846bf63a5548e5fb530a938507692fce9118fb958cafa22f01fe61176e",
+TRAFFIC_MEASURED = {"workload": "neox160m", "bytes_per_launch": 2.099e+08,
+                    "gemm_source_sha256": "bcb1cc34e7e0bb760112d68a022bb7d4f288b0fe3509f7c178304c89f49522c2",
                     "profile": "profiles/gemm_down_neox160m.md"}
 
 
@@ -317,6 +317,9 @@ def main():
     ap.add_argument("--cpu-layers", type=int, default=None, help="layers of the CPU oracle sample (default all)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true", help="skip the dense-stack comparison run")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the standalone sections (streaming entry points, router-score pathway, alignment "
+                         "objective); used for the counter passes")
     ap.add_argument("--only-sparse", action="store_true",
                     help="launch only the sparse stack (warmup + timed steps): no calibration pass when the "
                          "workload fixes its similarity profile, no dense run, no breakdown pass, no CPU "
@@ -520,15 +523,15 @@ def main():
         "similarity_measured": s_meas,
         "hip_runtime": torch.version.hip,
     }
-    if not args.only_sparse:
+    if not (args.only_sparse or args.no_extras):
         kmean = int(round(sum(ks) / len(ks)))
         log(f"streaming entry points standalone (B={B}, T={T}, k={kmean}), cold and hot inputs")
         out["streaming_kernels"] = streaming_rates(P, C, w, kmean, dev, S.layer_weights(w, 0))
-    if not args.only_sparse:
+    if not (args.only_sparse or args.no_extras):
         log("router-score pathway: gated stack, gate score gradient, router backward")
         out["router_score_pathway"] = router_pathway(P, C, w, ks, dev, desc, weights, x0, ws, ms_step,
                                                      max(3, args.steps // 3), S.layer_weights(w, 0))
-    if not args.only_sparse:
+    if not (args.only_sparse or args.no_extras):
         log("alignment objective: teacher/student stack, Eq. 9 and Eq. 10 kernels")
         out["alignment_objective"] = alignment_objective(P, C, w, ks, dev, desc, weights, x0, ms_step,
                                                          max(3, args.steps // 3))

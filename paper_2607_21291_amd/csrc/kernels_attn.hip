@@ -74,7 +74,7 @@ struct AttnPrefetch {
 #pragma unroll
     for (int i = 0; i < A::kKIter; ++i) {
       const int c = tid + 256 * i;
-      if (c < A::kKChunks) {
+      if (A::kKChunks % 256 == 0 || c < A::kKChunks) {
         const int row = c / A::kNch, ch = c % A::kNch;
         *reinterpret_cast<u32x4*>(Ks + row * HD + ((ch ^ (row & A::kSwz)) << 3)) = k[i];
       }
@@ -82,7 +82,7 @@ struct AttnPrefetch {
 #pragma unroll
     for (int i = 0; i < A::kVIter; ++i) {
       const int c = tid + 256 * i;
-      if (c < A::kVPairs) {
+      if (A::kVPairs % 256 == 0 || c < A::kVPairs) {
         const int kp = c % (kKV / 2), ch = c / (kKV / 2);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -130,9 +130,13 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const uint16_t* __restri
   const int ntiles = (kend + kKV - 1) / kKV;
   // Two register sets prefetch K/V two tiles ahead: tile t + 1 is written to
   // LDS at the end of tile t, its loads having been issued during tile t - 1.
+  // Every load is issued unconditionally (tiles past the last are clamped to
+  // it, an L2 hit): with a fixed number of loads in flight the wait before a
+  // set is written covers exactly that set, not the set loaded after it.
+  const int last = ntiles - 1;
   AttnPrefetch<HD> pfA, pfB;
   pfA.load(Kh, Vh, 0, n, tid);
-  if (ntiles > 1) pfB.load(Kh, Vh, kKV, n, tid);
+  pfB.load(Kh, Vh, min(1, last) * kKV, n, tid);
 
   // Q^T operand: lane (query r16, group grp) holds Q[query][32 s + 8 grp .. +8]
   bf16x8 qf[NQ][NS];
@@ -159,7 +163,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const uint16_t* __restri
 
   pfA.store(reinterpret_cast<uint16_t*>(smem), reinterpret_cast<uint16_t*>(smem + A::kKBytes), tid);
   __syncthreads();
-  if (ntiles > 2) pfA.load(Kh, Vh, 2 * kKV, n, tid);
+  pfA.load(Kh, Vh, min(2, last) * kKV, n, tid);
   // one tile: scores, online softmax and P V over LDS buffer t & 1
   auto tile = [&](int t) {
     const int kb0 = t * kKV;
@@ -253,11 +257,10 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const uint16_t* __restri
   // after tile t: write tile t + 1 (held in `held`) to the other buffer, then
   // refill `held` with tile t + 3
   auto advance = [&](int t, AttnPrefetch<HD>& held) {
-    if (t + 1 < ntiles)
-      held.store(reinterpret_cast<uint16_t*>(smem + ((t + 1) & 1) * A::kStage),
-                 reinterpret_cast<uint16_t*>(smem + ((t + 1) & 1) * A::kStage + A::kKBytes), tid);
+    held.store(reinterpret_cast<uint16_t*>(smem + ((t + 1) & 1) * A::kStage),
+               reinterpret_cast<uint16_t*>(smem + ((t + 1) & 1) * A::kStage + A::kKBytes), tid);
     __syncthreads();
-    if (t + 3 < ntiles) held.load(Kh, Vh, (t + 3) * kKV, n, tid);
+    held.load(Kh, Vh, min(t + 3, last) * kKV, n, tid);
   };
   for (int t = 0; t < ntiles; t += 2) {
     tile(t);  // pfB holds tile t + 1, pfA tile t + 2
