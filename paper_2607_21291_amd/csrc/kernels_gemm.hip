@@ -270,7 +270,7 @@ __device__ void gemm_epilogue(const GemmArgs& g, const float* stage, int m0, int
       }
     } else {  // EPI_BIAS_GELU
 #pragma unroll
-      for (int i = 0; i < 8; ++i) v[i] = gelu_erf(v[i]);
+      for (int i = 0; i < 8; ++i) v[i] = sizeof(T) == 2 ? gelu_bf16(v[i]) : gelu_erf(v[i]);
       store8((T*)g.out + int64_t(m) * g.ldo + n, v);
     }
   }

@@ -81,3 +81,24 @@ def test_full_size_schedules_agree(dev, monkeypatch):
     yc, _, idxc = run_layer(dev, w, W, x, k)
     assert torch.equal(idxa, idxc)
     assert rel_inf(to_np(ya) - to_np(x), to_np(yc) - to_np(x)) < TOL[w.dtype]
+
+
+@pytest.mark.parametrize("name", ["neox_bf16_small", "tiny_neox_f32"])
+def test_second_stream_matches_one_stream(dev, monkeypatch, name):
+    # the NeoX up projection runs on the library's second stream beside QKV
+    # and attention; the same kernels on the same inputs give the same bits
+    w = workload(name).replace(n_layers=3)
+    Ws = S.stack_weights(w)
+    x = S.hidden_states(w)
+    T = w.seq
+    ks = [T // 2, T - 3, max(1, T // 5)]
+    dls = [P.DeviceLayer(W, dev) for W in Ws]
+    ws = workspace(w, w.batch, T, max(ks), dev)
+    announce(f"two streams vs one: {name}")
+    x2 = x.to(dev)
+    P.stack_forward(make_desc(w), [dl.weights for dl in dls], ks, x2, ws)
+    monkeypatch.setenv("DSF_SINGLE_STREAM", "1")
+    x1 = x.to(dev)
+    P.stack_forward(make_desc(w), [dl.weights for dl in dls], ks, x1, ws)
+    torch.cuda.synchronize()
+    assert torch.equal(x1, x2)
