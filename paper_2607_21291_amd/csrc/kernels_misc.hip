@@ -336,92 +336,106 @@ hipError_t launch_zero_u32(uint32_t* dst, int64_t n, hipStream_t s) {
 
 // ------------------------------------------- gather + LayerNorm / RMSNorm
 
-// RPW rows per wavefront; each row stays in registers (MAXC vectors per lane)
-// so it is read from HBM once for both normalisations. All of a wave's
-// positions, rows and (narrow rows) weights are requested before the first
-// reduction, so their memory latencies overlap.
-template <typename T, int MAXC, int RPW>
-__global__ __launch_bounds__(256) void norm_kernel(NormArgs a) {
-  constexpr int V = Elem<T>::kVec;
-  const int lane = threadIdx.x & 63;
-  const int64_t rows = int64_t(a.B) * a.kk;
-  const int64_t r0 = (int64_t(blockIdx.x) * 4 + (threadIdx.x >> 6)) * RPW;
-  if (r0 >= rows) return;
-  const int d = a.d, nvec = d / V;
-  const T* src[RPW];
-#pragma unroll
-  for (int q = 0; q < RPW; ++q) {
-    const int64_t r = r0 + q < rows ? r0 + q : rows - 1;  // dead slots re-read the last row
-    if (a.src_rows == 0) {
-      src[q] = (const T*)a.src + r * d;
-    } else {
-      const int64_t b = r / a.kk, j = r - b * a.kk;
-      const int64_t pos = a.idx ? clamp_pos(a.idx[r], a.src_rows) : j;
-      src[q] = (const T*)a.src + (b * a.src_rows + pos) * d;
-    }
+// Sum over the L-lane group of a lane (L = 16, 32 or 64; groups are aligned),
+// with the row-swap permutes of gfx950 (VALU only): within 16-lane rows,
+// then rows 0+1 and 2+3, then the two halves.
+template <int L>
+__device__ __forceinline__ float group_sum(float v) {
+  v = row16_sum(v);
+  if constexpr (L >= 32) {
+    auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = __uint_as_float(b[0]) + __uint_as_float(b[1]);
   }
-  // The normalisation weights do not depend on the row. For narrow rows they
-  // are requested up front; wide rows would need too many registers.
-  constexpr bool kHoist = MAXC <= 2;
-  constexpr int HC = kHoist ? MAXC : 1;
-  float wv[2][HC][V], bv[2][HC][V];
-  auto load_wb = [&](int o, int c, float* w_out, float* b_out) {
-    const T* w = (const T*)(o == 0 ? a.w1 : a.w2);
-    const T* bb = (const T*)(o == 0 ? a.b1 : a.b2);
-    const int ch = lane + 64 * c;
+  if constexpr (L == 64) {
+    auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  }
+  return v;
+}
+
+// The forms the layer uses: LayerNorm with gain and bias into two outputs
+// (NeoX: LN1 and LN2 of the same rows), the same without biases or with only
+// one of them, and RMSNorm with gain into one output (Qwen).
+enum NormMode { kNormLnBias2 = 0, kNormLn2 = 1, kNormRms1 = 2, kNormLnBiasMixed = 3 };
+
+// L lanes per row, 64 / L rows per wavefront; lane l of a row holds its
+// 16-byte vectors l, l + L, ... (C of them, the row in registers), so it is
+// read from HBM once for both normalisations. L is chosen so that the row's
+// vectors split evenly over the lanes (EXACT): no lane idles through the
+// loads and sums. One row per wavefront at d = 768 left half the lanes one
+// vector short and measured 1.6x slower. Short of an even split, trailing
+// lanes skip their last vector. The straight-line form (no branches around
+// loads, modes fixed at compile time) matters: the same steps with runtime
+// branches measured 1.2x slower.
+template <typename T, int L, int C, bool EXACT, int MODE>
+__global__ __launch_bounds__(256) void norm_kernel(NormArgs a) {
+  constexpr int V = Elem<T>::kVec, RW = 64 / L;
+  constexpr bool kRms = MODE == kNormRms1, kBias = MODE == kNormLnBias2 || MODE == kNormLnBiasMixed;
+  constexpr int NO = MODE == kNormRms1 ? 1 : 2;  // outputs
+  constexpr bool kHoist = C <= 3;
+  constexpr int HC = kHoist ? C : 1;
+  const int lane = threadIdx.x & 63, hl = lane % L;
+  const int64_t rows = int64_t(a.B) * a.kk;
+  const int64_t r = (int64_t(blockIdx.x) * 4 + (threadIdx.x >> 6)) * RW + lane / L;
+  const int64_t rr = r < rows ? r : rows - 1;  // dead rows re-read the last row, write nothing
+  const int d = a.d, nvec = d / V;
+  auto in = [&](int c) { return EXACT || hl + L * c < nvec; };
+  const int64_t b = rr / a.kk, j = rr - b * a.kk;
+  const int64_t pos = a.idx ? clamp_pos(a.idx[rr], a.src_rows) : j;
+  // src_rows == 0: compact rows (source row = output row)
+  const T* src = (const T*)a.src + (a.src_rows ? b * a.src_rows + pos : rr) * d;
+  float v[C][V];
 #pragma unroll
-    for (int i = 0; i < V; ++i) w_out[i] = b_out[i] = 0.f;
-    load_vec(w + ch * V, w_out);
-    if (bb) load_vec(bb + ch * V, b_out);
+  for (int c = 0; c < C; ++c)
+    if (in(c)) load_vec(src + (hl + L * c) * V, v[c]);
+  float wv[NO][HC][V], bv[NO][HC][V];
+  auto load_wb = [&](int o, int c, float* w_out, float* b_out) {
+    const int ch = hl + L * c;
+    const T* wp = (const T*)(o == 0 ? a.w1 : a.w2);
+    load_vec(wp + ch * V, w_out);
+    if constexpr (MODE == kNormLnBias2) load_vec((const T*)(o == 0 ? a.b1 : a.b2) + ch * V, b_out);
+    if constexpr (MODE == kNormLnBiasMixed) {  // a missing bias reads the gain and is discarded
+      const T* bp = (const T*)(o == 0 ? a.b1 : a.b2);
+      const bool hb = bp != nullptr;
+      load_vec((hb ? bp : wp) + ch * V, b_out);
+#pragma unroll
+      for (int i = 0; i < V; ++i) b_out[i] = hb ? b_out[i] : 0.f;
+    }
   };
   if constexpr (kHoist) {
 #pragma unroll
-    for (int o = 0; o < 2; ++o)
+    for (int o = 0; o < NO; ++o)
 #pragma unroll
-      for (int c = 0; c < MAXC; ++c)
-        if ((o == 0 ? a.out1 : a.out2) != nullptr && lane + 64 * c < nvec) load_wb(o, c, wv[o][c], bv[o][c]);
+      for (int c = 0; c < C; ++c)
+        if (in(c)) load_wb(o, c, wv[o][c], bv[o][c]);
   }
-  float v[RPW][MAXC][V];
+  float m = 0.f;
+  if constexpr (!kRms) {
+    float sum = 0.f;
 #pragma unroll
-  for (int q = 0; q < RPW; ++q)
+    for (int c = 0; c < C; ++c)
+      if (in(c))
 #pragma unroll
-    for (int c = 0; c < MAXC; ++c) {
-      const int ch = lane + 64 * c;
-      if (ch < nvec) load_vec(src[q] + ch * V, v[q][c]);
-    }
-  float mean[RPW], rstd[RPW];
-#pragma unroll
-  for (int q = 0; q < RPW; ++q) {
-    float m = 0.f;
-    if (!a.rms) {
-      float sum = 0.f;
-#pragma unroll
-      for (int c = 0; c < MAXC; ++c)
-        if (lane + 64 * c < nvec)
-#pragma unroll
-          for (int i = 0; i < V; ++i) sum += v[q][c][i];
-      m = wave_sum_fast(sum) / float(d);
-    }
-    float sq = 0.f;
-#pragma unroll
-    for (int c = 0; c < MAXC; ++c)
-      if (lane + 64 * c < nvec)
-#pragma unroll
-        for (int i = 0; i < V; ++i) {
-          const float t = v[q][c][i] - m;
-          sq += t * t;
-        }
-    mean[q] = m;
-    rstd[q] = 1.0f / sqrtf(wave_sum_fast(sq) / float(d) + a.eps);
+        for (int i = 0; i < V; ++i) sum += v[c][i];
+    m = group_sum<L>(sum) / float(d);
   }
+  float sq = 0.f;
 #pragma unroll
-  for (int o = 0; o < 2; ++o) {
+  for (int c = 0; c < C; ++c)
+    if (in(c))
+#pragma unroll
+      for (int i = 0; i < V; ++i) {
+        const float t = v[c][i] - m;
+        sq += t * t;
+      }
+  const float rstd = 1.0f / sqrtf(group_sum<L>(sq) / float(d) + a.eps);
+  if (r >= rows) return;
+#pragma unroll
+  for (int o = 0; o < NO; ++o) {
     T* out = (T*)(o == 0 ? a.out1 : a.out2);
-    if (!out) continue;
 #pragma unroll
-    for (int c = 0; c < MAXC; ++c) {
-      const int ch = lane + 64 * c;
-      if (ch >= nvec) continue;
+    for (int c = 0; c < C; ++c) {
+      if (!in(c)) continue;
       float wl[V], bl[V];
       const float* wc = wl;
       const float* bc = bl;
@@ -431,32 +445,59 @@ __global__ __launch_bounds__(256) void norm_kernel(NormArgs a) {
       } else {
         load_wb(o, c, wl, bl);
       }
+      float y[V];
 #pragma unroll
-      for (int q = 0; q < RPW; ++q) {
-        if (r0 + q >= rows) break;
-        float y[V];
-#pragma unroll
-        for (int i = 0; i < V; ++i) y[i] = (v[q][c][i] - mean[q]) * rstd[q] * wc[i] + bc[i];
-        store_vec(out + (r0 + q) * d + ch * V, y);
-      }
+      for (int i = 0; i < V; ++i) y[i] = (v[c][i] - m) * rstd * wc[i] + (kBias ? bc[i] : 0.f);
+      store_vec(out + r * d + (hl + L * c) * V, y);
     }
   }
 }
 
+template <typename T, int L, bool EXACT, int MODE>
+static hipError_t launch_norm_lm(const NormArgs& a, int chunks, hipStream_t s) {
+  const int64_t rows = int64_t(a.B) * a.kk;
+  const unsigned grid = unsigned((rows + 4 * (64 / L) - 1) / (4 * (64 / L)));
+  switch (chunks) {
+    case 1: norm_kernel<T, L, 1, EXACT, MODE><<<grid, 256, 0, s>>>(a); break;
+    case 2: norm_kernel<T, L, 2, EXACT, MODE><<<grid, 256, 0, s>>>(a); break;
+    case 3: norm_kernel<T, L, 3, EXACT, MODE><<<grid, 256, 0, s>>>(a); break;
+    case 4: norm_kernel<T, L, 4, EXACT, MODE><<<grid, 256, 0, s>>>(a); break;
+    case 5: norm_kernel<T, L, 5, EXACT, MODE><<<grid, 256, 0, s>>>(a); break;
+    case 6: norm_kernel<T, L, 6, EXACT, MODE><<<grid, 256, 0, s>>>(a); break;
+    case 7: norm_kernel<T, L, 7, EXACT, MODE><<<grid, 256, 0, s>>>(a); break;
+    case 8: norm_kernel<T, L, 8, EXACT, MODE><<<grid, 256, 0, s>>>(a); break;
+    default:
+      if constexpr (EXACT) return hipErrorInvalidValue;
+      if (chunks <= 12) norm_kernel<T, L, 12, false, MODE><<<grid, 256, 0, s>>>(a);
+      else if (chunks <= 16) norm_kernel<T, L, 16, false, MODE><<<grid, 256, 0, s>>>(a);
+      else return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+template <typename T, int L, bool EXACT>
+static hipError_t launch_norm_l(const NormArgs& a, int chunks, hipStream_t s) {
+  if (a.rms) {
+    if (a.out2 || a.b1) return hipErrorInvalidValue;
+    return launch_norm_lm<T, L, EXACT, kNormRms1>(a, chunks, s);
+  }
+  if (!a.out2) return hipErrorInvalidValue;
+  if (a.b1 && a.b2) return launch_norm_lm<T, L, EXACT, kNormLnBias2>(a, chunks, s);
+  if (!a.b1 && !a.b2) return launch_norm_lm<T, L, EXACT, kNormLn2>(a, chunks, s);
+  return launch_norm_lm<T, L, EXACT, kNormLnBiasMixed>(a, chunks, s);
+}
+
+// Lanes per row: the widest of 64, 32, 16 that splits the row's vectors
+// evenly into at most 8 per lane (fewer vectors per lane keep the weights in
+// registers); otherwise 64 lanes, the last vectors of the row on the first
+// lanes only.
 template <typename T>
 static hipError_t launch_norm_t(const NormArgs& a, hipStream_t s) {
-  constexpr int V = Elem<T>::kVec;
-  const int per_lane = (a.d / V + 63) / 64;
-  const int64_t rows = int64_t(a.B) * a.kk;
-  auto grid = [&](int rpw) { return unsigned((rows + 4 * rpw - 1) / (4 * rpw)); };
-  // one row per wave: more rows per wave cost occupancy and measured slower
-  if (per_lane <= 1) norm_kernel<T, 1, 1><<<grid(1), 256, 0, s>>>(a);
-  else if (per_lane <= 2) norm_kernel<T, 2, 1><<<grid(1), 256, 0, s>>>(a);
-  else if (per_lane <= 4) norm_kernel<T, 4, 1><<<grid(1), 256, 0, s>>>(a);
-  else if (per_lane <= 8) norm_kernel<T, 8, 1><<<grid(1), 256, 0, s>>>(a);
-  else if (per_lane <= 16) norm_kernel<T, 16, 1><<<grid(1), 256, 0, s>>>(a);
-  else return hipErrorInvalidValue;
-  return hipGetLastError();
+  const int nvec = a.d / Elem<T>::kVec;
+  if (nvec % 64 == 0 && nvec / 64 <= 8) return launch_norm_l<T, 64, true>(a, nvec / 64, s);
+  if (nvec % 32 == 0 && nvec / 32 <= 8) return launch_norm_l<T, 32, true>(a, nvec / 32, s);
+  if (nvec % 16 == 0 && nvec / 16 <= 8) return launch_norm_l<T, 16, true>(a, nvec / 16, s);
+  return launch_norm_l<T, 64, false>(a, (nvec + 63) / 64, s);
 }
 
 hipError_t launch_norm(const NormArgs& a, hipStream_t s) {
