@@ -106,6 +106,86 @@ __global__ __launch_bounds__(256) void align_hidden_kernel(const T* __restrict__
   if (threadIdx.x == 0) partial[blockIdx.x] = ((wsum[0] + wsum[1]) + wsum[2]) + wsum[3];
 }
 
+// The same over L-lane groups, 64 / L rows per wavefront, when the row splits
+// evenly into C <= 8 vectors per lane (no lane idles; one row per wavefront at
+// d = 768 left half the lanes a vector short).
+template <int L>
+__device__ __forceinline__ float group_max(float v) {
+#pragma unroll
+  for (int o = L / 2; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
+  return v;
+}
+template <int L>
+__device__ __forceinline__ double group_sum_d(double v) {
+#pragma unroll
+  for (int o = L / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+
+template <typename T, int L, int C>
+__global__ __launch_bounds__(256) void align_hidden_group_kernel(const T* __restrict__ hs, const T* __restrict__ hd,
+                                                                 int64_t n, int d, float* __restrict__ per_tok,
+                                                                 double* __restrict__ partial) {
+  constexpr int V = Elem<T>::kVec, RW = 64 / L;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, hl = lane % L;
+  double wave_acc = 0.0;
+  for (int64_t t0 = (int64_t(blockIdx.x) * 4 + w) * RW; t0 < n; t0 += int64_t(gridDim.x) * 4 * RW) {
+    const int64_t t = t0 + lane / L;
+    const int64_t tt = t < n ? t : n - 1;  // rows past the end are read again and dropped
+    float a[C][V], b[C][V];
+    float ma = -INFINITY, mb = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < C; ++i) {
+      load_vec(hs + tt * d + (hl + L * i) * V, a[i]);
+      load_vec(hd + tt * d + (hl + L * i) * V, b[i]);
+    }
+#pragma unroll
+    for (int i = 0; i < C; ++i)
+#pragma unroll
+      for (int e = 0; e < V; ++e) {
+        ma = fmaxf(ma, a[i][e]);
+        mb = fmaxf(mb, b[i][e]);
+      }
+    ma = group_max<L>(ma);
+    mb = group_max<L>(mb);
+    double za = 0.0, zb = 0.0;
+#pragma unroll
+    for (int i = 0; i < C; ++i)
+#pragma unroll
+      for (int e = 0; e < V; ++e) {
+        a[i][e] = exp_hw(a[i][e] - ma);
+        b[i][e] = exp_hw(b[i][e] - mb);
+        za += a[i][e];
+        zb += b[i][e];
+      }
+    za = group_sum_d<L>(za);
+    zb = group_sum_d<L>(zb);
+    const double ia = 1.0 / za, ib = 1.0 / zb;
+    double acc = 0.0;
+#pragma unroll
+    for (int i = 0; i < C; ++i)
+#pragma unroll
+      for (int e = 0; e < V; ++e) {
+        // both products rounded alike (no fused multiply-add), so that
+        // identical rows give exactly zero
+#pragma clang fp contract(off)
+        const double pa = double(a[i][e]) * ia;
+        const double pb = double(b[i][e]) * ib;
+        const double diff = pa - pb;
+        acc = fma(diff, diff, acc);
+      }
+    acc = group_sum_d<L>(acc);
+    const bool lead = hl == 0 && t < n;
+    if (lead && per_tok) per_tok[t] = float(acc);
+    wave_acc += lead ? acc : 0.0;
+  }
+  wave_acc = wave_sum(wave_acc);  // the rows' leaders, in a fixed order
+  __shared__ double wsum[4];
+  if (lane == 0) wsum[w] = wave_acc;
+  __syncthreads();
+  if (threadIdx.x == 0) partial[blockIdx.x] = ((wsum[0] + wsum[1]) + wsum[2]) + wsum[3];
+}
+
 // Single block: accum[0] += the partials, summed in a fixed order.
 __global__ __launch_bounds__(256) void sum_finish_kernel(const double* __restrict__ partial, int64_t np,
                                                          double* __restrict__ accum) {
@@ -123,10 +203,29 @@ __global__ __launch_bounds__(256) void sum_finish_kernel(const double* __restric
 
 int align_max_d(int dtype) { return 64 * 16 * (dtype == DSF_BF16 ? 8 : 4); }
 
+template <typename T, int L>
+static void launch_align_group(const T* hs, const T* hd, int64_t n, int d, float* per_tok, double* partial, int g,
+                               int c, hipStream_t s) {
+  switch (c) {
+    case 1: align_hidden_group_kernel<T, L, 1><<<g, 256, 0, s>>>(hs, hd, n, d, per_tok, partial); break;
+    case 2: align_hidden_group_kernel<T, L, 2><<<g, 256, 0, s>>>(hs, hd, n, d, per_tok, partial); break;
+    case 3: align_hidden_group_kernel<T, L, 3><<<g, 256, 0, s>>>(hs, hd, n, d, per_tok, partial); break;
+    case 4: align_hidden_group_kernel<T, L, 4><<<g, 256, 0, s>>>(hs, hd, n, d, per_tok, partial); break;
+    case 5: align_hidden_group_kernel<T, L, 5><<<g, 256, 0, s>>>(hs, hd, n, d, per_tok, partial); break;
+    case 6: align_hidden_group_kernel<T, L, 6><<<g, 256, 0, s>>>(hs, hd, n, d, per_tok, partial); break;
+    case 7: align_hidden_group_kernel<T, L, 7><<<g, 256, 0, s>>>(hs, hd, n, d, per_tok, partial); break;
+    default: align_hidden_group_kernel<T, L, 8><<<g, 256, 0, s>>>(hs, hd, n, d, per_tok, partial); break;
+  }
+}
+
 template <typename T>
 static void launch_align_hidden_t(const T* hs, const T* hd, int64_t n, int d, float* per_tok, double* partial,
                                   int g, hipStream_t s) {
-  const int chunks = (d / Elem<T>::kVec + 63) / 64;
+  const int nvec = d / Elem<T>::kVec;
+  if (nvec % 64 == 0 && nvec / 64 <= 8) return launch_align_group<T, 64>(hs, hd, n, d, per_tok, partial, g, nvec / 64, s);
+  if (nvec % 32 == 0 && nvec / 32 <= 8) return launch_align_group<T, 32>(hs, hd, n, d, per_tok, partial, g, nvec / 32, s);
+  if (nvec % 16 == 0 && nvec / 16 <= 8) return launch_align_group<T, 16>(hs, hd, n, d, per_tok, partial, g, nvec / 16, s);
+  const int chunks = (nvec + 63) / 64;
   if (chunks <= 1) align_hidden_kernel<T, 1><<<g, 256, 0, s>>>(hs, hd, n, d, per_tok, partial);
   else if (chunks <= 2) align_hidden_kernel<T, 2><<<g, 256, 0, s>>>(hs, hd, n, d, per_tok, partial);
   else if (chunks <= 4) align_hidden_kernel<T, 4><<<g, 256, 0, s>>>(hs, hd, n, d, per_tok, partial);

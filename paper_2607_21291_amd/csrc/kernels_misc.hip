@@ -33,18 +33,98 @@ hipError_t launch_rope_table(float* table, int T, int R, double theta, hipStream
 
 // ------------------------------------------------ similarity statistic, Eq. 4
 
-constexpr int kSimMaxGrid = 1024;
+constexpr int kSimMaxGrid = 16384;
 
 int sim_grid(int64_t n_tokens) {
   int64_t g = (n_tokens + 3) / 4;
   return int(g < 1 ? 1 : (g > kSimMaxGrid ? kSimMaxGrid : g));
 }
 
-// One wavefront per token row; products and sums in fp64 (products of bf16 or
+// fp64 sum over the L-lane group of a lane (aligned groups; xor offsets
+// below L stay inside the group).
+template <int L>
+__device__ __forceinline__ double group_sum_f64(double v) {
+#pragma unroll
+  for (int o = L / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+
+// L lanes per token row, 64 / L rows per wavefront (grid-stride over rows);
+// lane l of a row holds its 16-byte vectors l, l + L, ... (C of them; EXACT:
+// the row splits evenly, no per-lane guards). Products and sums in fp64
+// (products of bf16 or fp32 values are exact in fp64). Each block writes the
+// sum of its rows' cosines, in a fixed order, to partial[blockIdx.x].
+template <typename T, int L, int C, bool EXACT>
+__global__ __launch_bounds__(256) void sim_partial_kernel(const T* a, const T* c, int64_t n, int d,
+                                                          float* per_tok, double* partial) {
+  constexpr int V = Elem<T>::kVec, RW = 64 / L;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, hl = lane % L;
+  const int nvec = d / V;
+  auto in = [&](int ch) { return EXACT || hl + L * ch < nvec; };
+  double wave_acc = 0.0;
+  for (int64_t t0 = (int64_t(blockIdx.x) * 4 + w) * RW; t0 < n; t0 += int64_t(gridDim.x) * 4 * RW) {
+    const int64_t t = t0 + lane / L;
+    const int64_t tt = t < n ? t : n - 1;  // rows past the end are read again and dropped
+    const T* ra = a + tt * d;
+    const T* rc = c + tt * d;
+    float va[C][V], vc[C][V];
+#pragma unroll
+    for (int ch = 0; ch < C; ++ch)
+      if (in(ch)) {
+        load_vec(ra + (hl + L * ch) * V, va[ch]);
+        load_vec(rc + (hl + L * ch) * V, vc[ch]);
+      }
+    double dot = 0.0, aa = 0.0, cc = 0.0;
+#pragma unroll
+    for (int ch = 0; ch < C; ++ch)
+      if (in(ch))
+#pragma unroll
+        for (int i = 0; i < V; ++i) {
+          const double x = va[ch][i], y = vc[ch][i];
+          dot = fma(x, y, dot);
+          aa = fma(x, x, aa);
+          cc = fma(y, y, cc);
+        }
+    dot = group_sum_f64<L>(dot);
+    aa = group_sum_f64<L>(aa);
+    cc = group_sum_f64<L>(cc);
+    const double den = sqrt(aa) * sqrt(cc);
+    const double cs = dot / (den > 1e-8 ? den : 1e-8);
+    const bool lead = hl == 0 && t < n;
+    if (lead && per_tok) per_tok[t] = float(cs);
+    wave_acc += lead ? cs : 0.0;
+  }
+  wave_acc = wave_sum(wave_acc);  // the rows' leaders, in a fixed order
+  __shared__ double wsum[4];
+  if (lane == 0) wsum[w] = wave_acc;
+  __syncthreads();
+  if (threadIdx.x == 0) partial[blockIdx.x] = ((wsum[0] + wsum[1]) + wsum[2]) + wsum[3];
+}
+
+// Single block: fixed-order sum of the partials, then accum += (sum, n).
+__global__ __launch_bounds__(256) void sim_finish_kernel(const double* partial, int np, int64_t n,
+                                                         double* accum) {
+  __shared__ double red[256];
+  double v = 0.0;
+  for (int i = threadIdx.x; i < np; i += 256) v += partial[i];
+  red[threadIdx.x] = v;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if (threadIdx.x < o) red[threadIdx.x] += red[threadIdx.x + o];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    accum[0] += red[0];
+    accum[1] += double(n);
+  }
+}
+
+// Rows of any width: one wavefront per token row, the lanes stepping through
+// its vectors; products and sums in fp64 (products of bf16 or
 // fp32 values are exact in fp64). Each block writes the sum of its tokens'
 // cosines, in a fixed order, to partial[blockIdx.x].
 template <typename T>
-__global__ __launch_bounds__(256) void sim_partial_kernel(const T* a, const T* c, int64_t n, int d,
+__global__ __launch_bounds__(256) void sim_wide_kernel(const T* a, const T* c, int64_t n, int d,
                                                           float* per_tok, double* partial) {
   constexpr int V = Elem<T>::kVec;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -80,22 +160,32 @@ __global__ __launch_bounds__(256) void sim_partial_kernel(const T* a, const T* c
   if (threadIdx.x == 0) partial[blockIdx.x] = ((wsum[0] + wsum[1]) + wsum[2]) + wsum[3];
 }
 
-// Single block: fixed-order sum of the partials, then accum += (sum, n).
-__global__ __launch_bounds__(256) void sim_finish_kernel(const double* partial, int np, int64_t n,
-                                                         double* accum) {
-  __shared__ double red[256];
-  double v = 0.0;
-  for (int i = threadIdx.x; i < np; i += 256) v += partial[i];
-  red[threadIdx.x] = v;
-  __syncthreads();
-  for (int o = 128; o > 0; o >>= 1) {
-    if (threadIdx.x < o) red[threadIdx.x] += red[threadIdx.x + o];
-    __syncthreads();
+template <typename T, int L, bool EXACT>
+static void launch_sim_l(const T* a, const T* c, int64_t n, int d, float* per_tok, double* partial, int g,
+                         int chunks, hipStream_t s) {
+  switch (chunks) {
+    case 1: sim_partial_kernel<T, L, 1, EXACT><<<g, 256, 0, s>>>(a, c, n, d, per_tok, partial); break;
+    case 2: sim_partial_kernel<T, L, 2, EXACT><<<g, 256, 0, s>>>(a, c, n, d, per_tok, partial); break;
+    case 3: sim_partial_kernel<T, L, 3, EXACT><<<g, 256, 0, s>>>(a, c, n, d, per_tok, partial); break;
+    case 4: sim_partial_kernel<T, L, 4, EXACT><<<g, 256, 0, s>>>(a, c, n, d, per_tok, partial); break;
+    case 5: sim_partial_kernel<T, L, 5, EXACT><<<g, 256, 0, s>>>(a, c, n, d, per_tok, partial); break;
+    case 6: sim_partial_kernel<T, L, 6, EXACT><<<g, 256, 0, s>>>(a, c, n, d, per_tok, partial); break;
+    case 7: sim_partial_kernel<T, L, 7, EXACT><<<g, 256, 0, s>>>(a, c, n, d, per_tok, partial); break;
+    default: sim_partial_kernel<T, L, 8, EXACT><<<g, 256, 0, s>>>(a, c, n, d, per_tok, partial); break;
   }
-  if (threadIdx.x == 0) {
-    accum[0] += red[0];
-    accum[1] += double(n);
-  }
+}
+
+// Lanes per row as for the norm kernel: the widest of 64, 32, 16 that splits
+// the row evenly into at most 8 vectors per lane; otherwise 64 lanes looping
+// over groups of 8 vectors.
+template <typename T>
+static void launch_sim_t(const T* a, const T* c, int64_t n, int d, float* per_tok, double* partial, int g,
+                         hipStream_t s) {
+  const int nvec = d / Elem<T>::kVec;
+  if (nvec % 64 == 0 && nvec / 64 <= 8) launch_sim_l<T, 64, true>(a, c, n, d, per_tok, partial, g, nvec / 64, s);
+  else if (nvec % 32 == 0 && nvec / 32 <= 8) launch_sim_l<T, 32, true>(a, c, n, d, per_tok, partial, g, nvec / 32, s);
+  else if (nvec % 16 == 0 && nvec / 16 <= 8) launch_sim_l<T, 16, true>(a, c, n, d, per_tok, partial, g, nvec / 16, s);
+  else sim_wide_kernel<T><<<g, 256, 0, s>>>(a, c, n, d, per_tok, partial);
 }
 
 hipError_t launch_sim_stats(int dtype, const void* a, const void* c, int64_t n, int d, float* per_tok,
@@ -104,9 +194,9 @@ hipError_t launch_sim_stats(int dtype, const void* a, const void* c, int64_t n, 
   TimedScope ts(DSF_KIND_SIM, s);
   int g = sim_grid(n);
   if (dtype == DSF_BF16)
-    sim_partial_kernel<uint16_t><<<g, 256, 0, s>>>((const uint16_t*)a, (const uint16_t*)c, n, d, per_tok, partial);
+    launch_sim_t<uint16_t>((const uint16_t*)a, (const uint16_t*)c, n, d, per_tok, partial, g, s);
   else
-    sim_partial_kernel<float><<<g, 256, 0, s>>>((const float*)a, (const float*)c, n, d, per_tok, partial);
+    launch_sim_t<float>((const float*)a, (const float*)c, n, d, per_tok, partial, g, s);
   sim_finish_kernel<<<1, 256, 0, s>>>(partial, g, n, accum);
   return hipGetLastError();
 }

@@ -207,6 +207,68 @@ __global__ __launch_bounds__(256) void gate_grad_kernel(const T* __restrict__ dy
   if (lane == 0) dscore[row] = acc / (1.f + expf(scores[row]));
 }
 
+// The same with L lanes per kept token (64 / L tokens per wavefront) when the
+// row splits evenly into C <= 8 vectors per lane, so that no lane idles.
+template <typename T, int L, int C>
+__global__ __launch_bounds__(256) void gate_grad_group_kernel(const T* __restrict__ dy, const T* __restrict__ x_in,
+                                                              const T* __restrict__ x_out,
+                                                              const float* __restrict__ scores,
+                                                              const int32_t* __restrict__ idx, int B, int Tn, int k,
+                                                              int d, float* __restrict__ dscore) {
+  constexpr int V = Elem<T>::kVec, RW = 64 / L;
+  const int lane = threadIdx.x & 63, hl = lane % L;
+  const int64_t e = (int64_t(blockIdx.x) * 4 + (threadIdx.x >> 6)) * RW + lane / L;
+  const int64_t ee = e < int64_t(B) * k ? e : int64_t(B) * k - 1;
+  const int b = int(ee / k);
+  const int p = idx[ee];
+  const bool ok = e < int64_t(B) * k && p >= 0 && p < Tn;
+  const int64_t row = int64_t(b) * Tn + (ok ? p : 0);
+  float acc = 0.f;
+  float gv[C][V], av[C][V], ov[C][V];
+#pragma unroll
+  for (int c = 0; c < C; ++c) {
+    const int64_t off = row * d + (hl + L * c) * V;
+    load_vec(dy + off, gv[c]);
+    load_vec(x_in + off, av[c]);
+    load_vec(x_out + off, ov[c]);
+  }
+#pragma unroll
+  for (int c = 0; c < C; ++c)
+#pragma unroll
+    for (int i = 0; i < V; ++i) acc = fmaf(gv[c][i], ov[c][i] - av[c][i], acc);
+#pragma unroll
+  for (int o = L / 2; o > 0; o >>= 1) acc += __shfl_xor(acc, o, kWave);
+  if (hl == 0 && ok) dscore[row] = acc / (1.f + expf(scores[row]));
+}
+
+template <typename T, int L>
+static void launch_gate_group(const T* dy, const T* xi, const T* xo, const float* sc, const int32_t* idx, int B,
+                              int Tn, int k, int d, float* ds, int c, hipStream_t s) {
+  const unsigned grid = unsigned((int64_t(B) * k + 4 * (64 / L) - 1) / (4 * (64 / L)));
+  switch (c) {
+    case 1: gate_grad_group_kernel<T, L, 1><<<grid, 256, 0, s>>>(dy, xi, xo, sc, idx, B, Tn, k, d, ds); break;
+    case 2: gate_grad_group_kernel<T, L, 2><<<grid, 256, 0, s>>>(dy, xi, xo, sc, idx, B, Tn, k, d, ds); break;
+    case 3: gate_grad_group_kernel<T, L, 3><<<grid, 256, 0, s>>>(dy, xi, xo, sc, idx, B, Tn, k, d, ds); break;
+    case 4: gate_grad_group_kernel<T, L, 4><<<grid, 256, 0, s>>>(dy, xi, xo, sc, idx, B, Tn, k, d, ds); break;
+    case 5: gate_grad_group_kernel<T, L, 5><<<grid, 256, 0, s>>>(dy, xi, xo, sc, idx, B, Tn, k, d, ds); break;
+    case 6: gate_grad_group_kernel<T, L, 6><<<grid, 256, 0, s>>>(dy, xi, xo, sc, idx, B, Tn, k, d, ds); break;
+    case 7: gate_grad_group_kernel<T, L, 7><<<grid, 256, 0, s>>>(dy, xi, xo, sc, idx, B, Tn, k, d, ds); break;
+    default: gate_grad_group_kernel<T, L, 8><<<grid, 256, 0, s>>>(dy, xi, xo, sc, idx, B, Tn, k, d, ds); break;
+  }
+}
+
+// true if the rows were handled by a lane-group kernel
+template <typename T>
+static bool launch_gate_grouped(const T* dy, const T* xi, const T* xo, const float* sc, const int32_t* idx, int B,
+                                int Tn, int k, int d, float* ds, hipStream_t s) {
+  const int nvec = d / Elem<T>::kVec;
+  if (nvec % 64 == 0 && nvec / 64 <= 8) launch_gate_group<T, 64>(dy, xi, xo, sc, idx, B, Tn, k, d, ds, nvec / 64, s);
+  else if (nvec % 32 == 0 && nvec / 32 <= 8) launch_gate_group<T, 32>(dy, xi, xo, sc, idx, B, Tn, k, d, ds, nvec / 32, s);
+  else if (nvec % 16 == 0 && nvec / 16 <= 8) launch_gate_group<T, 16>(dy, xi, xo, sc, idx, B, Tn, k, d, ds, nvec / 16, s);
+  else return false;
+  return true;
+}
+
 hipError_t launch_gate_grad(int dtype, const void* dy, const void* x_in, const void* x_out, const float* scores,
                             const int32_t* idx, int B, int Tn, int k, int d, float* dscore, hipStream_t s) {
   if (int64_t(B) * Tn == 0) return hipSuccess;
@@ -214,12 +276,15 @@ hipError_t launch_gate_grad(int dtype, const void* dy, const void* x_in, const v
   hipError_t e = launch_zero_u32(reinterpret_cast<uint32_t*>(dscore), int64_t(B) * Tn, s);
   if (e != hipSuccess || k == 0) return e;
   const unsigned grid = unsigned((int64_t(B) * k + 3) / 4);
-  if (dtype == DSF_BF16)
-    gate_grad_kernel<uint16_t><<<grid, 256, 0, s>>>((const uint16_t*)dy, (const uint16_t*)x_in,
-                                                   (const uint16_t*)x_out, scores, idx, B, Tn, k, d, dscore);
-  else
-    gate_grad_kernel<float><<<grid, 256, 0, s>>>((const float*)dy, (const float*)x_in, (const float*)x_out, scores,
-                                                idx, B, Tn, k, d, dscore);
+  if (dtype == DSF_BF16) {
+    auto D = (const uint16_t*)dy; auto I = (const uint16_t*)x_in; auto O = (const uint16_t*)x_out;
+    if (!launch_gate_grouped(D, I, O, scores, idx, B, Tn, k, d, dscore, s))
+      gate_grad_kernel<uint16_t><<<grid, 256, 0, s>>>(D, I, O, scores, idx, B, Tn, k, d, dscore);
+  } else {
+    auto D = (const float*)dy; auto I = (const float*)x_in; auto O = (const float*)x_out;
+    if (!launch_gate_grouped(D, I, O, scores, idx, B, Tn, k, d, dscore, s))
+      gate_grad_kernel<float><<<grid, 256, 0, s>>>(D, I, O, scores, idx, B, Tn, k, d, dscore);
+  }
   return hipGetLastError();
 }
 
