@@ -17,6 +17,7 @@
 // order over original positions.
 #include <hip/hip_ext.h>
 
+#include "attn_sched.h"
 #include "dsf_device.h"
 #include "dsf_internal.h"
 
@@ -112,11 +113,11 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const uint16_t* __restri
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: keeps tile tests scalar
   const int r16 = lane & 15, grp = lane >> 4;
   // one work item per (sequence, head, query block); the query blocks of one
-  // (sequence, head) share K/V, so they are kept on one XCD (longest first)
+  // (sequence, head) share K/V, so they are kept on one XCD, and each XCD
+  // starts its longest blocks first
   const int nqb = (n + QB - 1) / QB;
-  const int item = xcd_remap(int(blockIdx.x), int(gridDim.x));
-  const int bh = item / nqb;
-  const int qblk = nqb - 1 - (item - bh * nqb);
+  const AttnItem it = attn_item(int(blockIdx.x), int(gridDim.x), nqb);
+  const int bh = it.bh, qblk = it.qblk;
   const int h = bh % Hq, b = bh / Hq;
   const int kvh = h / (Hq / Hkv);
   const int q0 = qblk * QB;
