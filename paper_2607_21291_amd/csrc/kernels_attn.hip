@@ -1,17 +1,29 @@
 // Causal attention among the kept tokens (Eq. 1 over the compacted set) for
 // gfx950.
 //
-// bf16 path (flash-style, online softmax in fp32). A workgroup of four
+// bf16 paths (flash-style, online softmax in fp32). A workgroup of four
 // wavefronts owns 64*NQ consecutive queries of one (sequence, query head); each
 // wavefront owns NQ groups of 16 queries. Key/value tiles of 64 tokens are
-// staged in LDS, K row-major (XOR-swizzled 16-byte chunks) and V transposed.
+// staged in LDS.
 //
 // Scores are formed transposed, S^T = K Q^T, with v_mfma_f32_16x16x32_bf16, so
-// a lane holds 16 scores of ONE query (its column): the row max and row sum
-// need only two cross-lane steps, and the probabilities already sit in the
-// layout of the B operand of O^T += V^T P^T. The MFMA's k slots there are
-// filled with keys in the order the lane holds them; V^T is read from LDS in
-// the same order, so the contraction over keys is unchanged.
+// a lane holds 16 scores of ONE query (its column): the row max needs only two
+// cross-lane steps, and the probabilities already sit in the layout of the B
+// operand of O^T += V^T P^T. The MFMA's k slots there are filled with keys in
+// the order the lane holds them, and V^T is read in the same order, so the
+// contraction over keys is unchanged. The row sums of P come from the matrix
+// cores as well: an A operand of ones gives, in every row of its output block,
+// sum_k P[query][k] over the same bf16 probabilities that weight V.
+//
+// Two ways of staging the tiles:
+// - DMA (attn_bf16_dma_kernel): K and V go global -> LDS by buffer DMA (no
+//   registers, no VALU), both row-major with each row's 16-byte chunks
+//   XOR-swizzled by the row index, in a ring of two stages; V^T is read with
+//   the LDS transpose load (ds_read_b64_tr_b16).
+// - Register prefetch (attn_bf16_staged_kernel): each tile is loaded into
+//   registers two tiles ahead and written to LDS by the waves, V transposed
+//   on the way (no transpose load needed), which leaves LDS for two query
+//   groups per wave at head dim 128.
 //
 // Kept positions ascend, so causal order over compacted indices is causal
 // order over original positions.
@@ -23,11 +35,264 @@
 
 namespace dsf {
 
-constexpr int kKV = 64;             // keys per tile
-constexpr int kVtLD = kKV + 4;      // padded row of the transposed V tile (bf16 elements)
+constexpr int kKV = 64;  // keys per tile
+
+// ------------------------------------------------------------------- DMA ring
+template <int HD>
+struct DmaTile {
+  static constexpr int kRowBytes = HD * 2;
+  static constexpr int kNch = HD / 8;                 // 16-byte chunks per row
+  static constexpr int kSwz = kNch - 1;               // chunk c of row r is stored at c ^ (r & kSwz)
+  static constexpr int kTileBytes = kKV * kRowBytes;  // one K or V tile
+  static constexpr int kStage = 2 * kTileBytes;       // K tile, then V tile
+  static constexpr int kDmaPerWave = kTileBytes / 1024 / 4;  // 1 KB per wave-wide DMA, 4 waves
+  static_assert(kDmaPerWave >= 1 && (kNch & (kNch - 1)) == 0, "head dim");
+};
+
+// LDS transpose load: within each 16-lane group G, lane 16G + 4a + b receives
+// element b of the 8-byte rows addressed by lanes 16G + a + 4j, j = 0..3.
+__device__ __forceinline__ bf16x4 lds_read_tr(const uint16_t* p) {
+  typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+  return __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+      (lds_bf16x4*)((__attribute__((address_space(3))) uint16_t*)(p)));
+}
+
+template <int HD, int NQ>
+__global__ __launch_bounds__(256) void attn_bf16_dma_kernel(const uint16_t* __restrict__ Q,
+                                                            const uint16_t* __restrict__ K,
+                                                            const uint16_t* __restrict__ V, int Hq, int Hkv,
+                                                            int n, uint16_t* __restrict__ out) {
+  using A = DmaTile<HD>;
+  constexpr int QB = 64 * NQ;          // queries per workgroup
+  constexpr int NS = HD / 32;          // MFMA k steps over the head dim
+  constexpr int ND = HD / 16;          // 16-row blocks of the head dim
+  __shared__ __attribute__((aligned(16))) char smem[2 * A::kStage];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: keeps tile tests scalar
+  const int r16 = lane & 15, grp = lane >> 4;
+  // one work item per (sequence, head, query block); the query blocks of one
+  // (sequence, head) share K/V, so they are kept on one XCD, and each XCD
+  // starts its longest blocks first
+  const int nqb = (n + QB - 1) / QB;
+  const AttnItem it = attn_item(int(blockIdx.x), int(gridDim.x), nqb);
+  const int bh = it.bh, qblk = it.qblk;
+  const int h = bh % Hq, b = bh / Hq;
+  const int kvh = h / (Hq / Hkv);
+  const int q0 = qblk * QB;
+  const int qw0 = q0 + wave * 16 * NQ;
+
+  const uint16_t* Qh = Q + (int64_t(b) * Hq + h) * n * HD;
+  const uint16_t* Kh = K + (int64_t(b) * Hkv + kvh) * n * HD;
+  const uint16_t* Vh = V + (int64_t(b) * Hkv + kvh) * n * HD;
+
+  const int kend = min(n, q0 + QB);
+  const int ntiles = (kend + kKV - 1) / kKV;
+
+  // DMA of tile t into stage t & 1. The buffer resources start at the tile's
+  // first key and end at key n - 1, so rows past the last key land as zeros
+  // (their scores are masked to -inf, their V rows weighted by zero). Lane
+  // `lane` of this wave's e-th DMA fills 16 bytes at tile byte
+  // 1024 (wave kDmaPerWave + e) + 16 lane: row r, chunk position c, which
+  // holds the row's global chunk c ^ (r & kSwz).
+  uint32_t dma_off[A::kDmaPerWave];
+#pragma unroll
+  for (int e = 0; e < A::kDmaPerWave; ++e) {
+    const int byte = 1024 * (wave * A::kDmaPerWave + e) + 16 * lane;
+    const int r = byte / A::kRowBytes, c = (byte % A::kRowBytes) / 16;
+    dma_off[e] = uint32_t(r * A::kRowBytes + ((c ^ (r & A::kSwz)) * 16));
+  }
+  auto issue = [&](int t) {
+    const int kb0 = t * kKV;
+    const int bytes = (n - kb0) * A::kRowBytes;
+    const auto kr = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(Kh + int64_t(kb0) * HD), (short)0,
+                                                      bytes, 0x00020000);
+    const auto vr = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(Vh + int64_t(kb0) * HD), (short)0,
+                                                      bytes, 0x00020000);
+    char* st = smem + (t & 1) * A::kStage + 1024 * (wave * A::kDmaPerWave);
+#pragma unroll
+    for (int e = 0; e < A::kDmaPerWave; ++e) {
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(kr, (__attribute__((address_space(3))) void*)(st + 1024 * e), 16,
+                                               int(dma_off[e]), 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          vr, (__attribute__((address_space(3))) void*)(st + A::kTileBytes + 1024 * e), 16, int(dma_off[e]), 0, 0, 0);
+    }
+  };
+  issue(0);
+
+  // Q^T operand: lane (query r16, group grp) holds Q[query][32 s + 8 grp .. +8]
+  bf16x8 qf[NQ][NS];
+#pragma unroll
+  for (int qi = 0; qi < NQ; ++qi) {
+    int qrow = qw0 + 16 * qi + r16;
+    if (qrow > n - 1) qrow = n - 1;
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+      qf[qi][s] = *reinterpret_cast<const bf16x8*>(Qh + int64_t(qrow) * HD + 32 * s + 8 * grp);
+  }
+
+  // all-ones A operand: l_run accumulates the row sums of P on the matrix cores
+  bf16x8 ones;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) ones[i] = (__bf16)1.0f;
+  f32x4 o[NQ][ND], l_run[NQ];
+  float m_run[NQ];
+#pragma unroll
+  for (int qi = 0; qi < NQ; ++qi) {
+    m_run[qi] = -INFINITY;
+    l_run[qi] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int db = 0; db < ND; ++db) o[qi][db] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  const float sc = 1.4426950408889634f / sqrtf(float(HD));  // log2(e) / sqrt(hd)
+  const int wave_qmax = qw0 + 16 * NQ - 1;
+
+  // lane-constant parts of the V^T transpose reads: lane (16 G + a + 4 j)
+  // addresses V row 4 G + j (+ 32 ks + 16 half) at dims 16 db + 4 a .. + 3,
+  // i.e. chunk (2 db + a / 2) ^ swz at byte (a & 1) * 8 of it
+  const int tg = lane >> 4, ta = lane & 3, tj = (lane >> 2) & 3;
+  const int vrow = 4 * tg + tj;
+  const int vbase = vrow * A::kRowBytes + (ta & 1) * 8;
+  const int vu = (ta >> 1) ^ (vrow & A::kSwz);
+
+  // V^T fragments of tile t: lane (dim r16 of block db, group grp) gets
+  // V[32 ks + 4 grp + j][16 db + r16] (j = 0..3) and the same 16 keys later
+  auto read_v = [&](int t, bf16x8 (&vf)[ND][2]) {
+    const uint16_t* Vs = reinterpret_cast<const uint16_t*>(smem + (t & 1) * A::kStage + A::kTileBytes + vbase);
+#pragma unroll
+    for (int db = 0; db < ND; ++db) {
+      const int coff = ((2 * db) ^ vu) * 8;  // elements
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+        const bf16x4 lo = lds_read_tr(Vs + (32 * ks) * HD + coff);
+        const bf16x4 hi = lds_read_tr(Vs + (32 * ks + 16) * HD + coff);
+        vf[db][ks] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+      }
+    }
+  };
+  // one tile: scores, online softmax and P V over LDS stage t & 1
+  auto tile = [&](int t, const bf16x8 (&vf)[ND][2]) {
+    const int kb0 = t * kKV;
+    const char* stage = smem + (t & 1) * A::kStage;
+    const uint16_t* Ks = reinterpret_cast<const uint16_t*>(stage);
+    {
+      // S^T blocks: lane holds S[query 16 qi + r16][key kb0 + 16 kb + 4 grp + i]
+      f32x4 s[NQ][4];
+#pragma unroll
+      for (int qi = 0; qi < NQ; ++qi)
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) s[qi][kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) {
+        const int row = 16 * kb + r16;
+#pragma unroll
+        for (int st = 0; st < NS; ++st) {
+          const int ch = 4 * st + grp;
+          bf16x8 kf = *reinterpret_cast<const bf16x8*>(Ks + row * HD + ((ch ^ (row & A::kSwz)) << 3));
+#pragma unroll
+          for (int qi = 0; qi < NQ; ++qi)
+            s[qi][kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[qi][st], s[qi][kb], 0, 0, 0);
+        }
+      }
+      const bool diag = kb0 + kKV - 1 > qw0 || kb0 + kKV > n;  // wave-uniform
+      bf16x8 pb[NQ][2];
+#pragma unroll
+      for (int qi = 0; qi < NQ; ++qi) {
+        if (diag) {
+          // key kb0 + 4 grp + (16 kb + i) is visible to query qg iff 16 kb + i <= lim
+          const int qg = qw0 + 16 * qi + r16;
+          const int lim = min(qg, n - 1) - (kb0 + 4 * grp);
+#pragma unroll
+          for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) s[qi][kb][i] = (16 * kb + i > lim) ? -INFINITY : s[qi][kb][i];
+        }
+        float mx = -INFINITY;
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) mx = fmaxf(mx, s[qi][kb][i]);
+        // running max in log2 units of the scaled scores (sc > 0 keeps the order)
+        const float m_new = fmaxf(m_run[qi], rows4_max(mx) * sc);
+        const float base = m_new == -INFINITY ? 0.f : m_new;
+        float p[4][4];
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) p[kb][i] = __builtin_amdgcn_exp2f(fmaf(s[qi][kb][i], sc, -base));
+        // rescale the running sums only when some lane's max moved (rare after the first tiles)
+        if (__builtin_amdgcn_ballot_w64(m_new != m_run[qi])) {
+          const float alpha = __builtin_amdgcn_exp2f(m_run[qi] - base);
+          l_run[qi] *= alpha;
+#pragma unroll
+          for (int db = 0; db < ND; ++db) o[qi][db] *= alpha;
+        }
+        m_run[qi] = m_new;
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            pb[qi][ks][i] = (__bf16)p[2 * ks][i];
+            pb[qi][ks][4 + i] = (__bf16)p[2 * ks + 1][i];
+          }
+      }
+      // O^T[dim 16 db + r16 .. ][query] += V^T P^T over this tile's 64 keys
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+        for (int qi = 0; qi < NQ; ++qi)
+          l_run[qi] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb[qi][ks], l_run[qi], 0, 0, 0);
+#pragma unroll
+      for (int db = 0; db < ND; ++db)
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+          for (int qi = 0; qi < NQ; ++qi)
+            o[qi][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[db][ks], pb[qi][ks], o[qi][db], 0, 0, 0);
+    }
+  };
+  // The barrier at the top of tile t publishes tile t and retires tile
+  // t - 1, whose stage the DMA of tile t + 1 then refills. Each wave first
+  // waits for its own DMA (__syncthreads does not wait for LDS DMA), so after
+  // the barrier every wave's share of the tile is in LDS. The V fragments are
+  // read before the next DMA is issued: a transpose read after it would wait
+  // for that DMA to land.
+  for (int t = 0; t < ntiles; ++t) {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (t * kKV <= wave_qmax) {  // otherwise every key of this tile is in this wave's future
+      bf16x8 vf[ND][2];
+      read_v(t, vf);
+      if (t + 1 < ntiles) issue(t + 1);
+      tile(t, vf);
+    } else if (t + 1 < ntiles) {
+      issue(t + 1);
+    }
+  }
+  // lane holds O^T[dim 16 db + 4 grp + i][query r16]
+#pragma unroll
+  for (int qi = 0; qi < NQ; ++qi) {
+    const int qg = qw0 + 16 * qi + r16;
+    if (qg >= n) continue;
+    const float inv = 1.0f / l_run[qi][0];
+    uint16_t* orow = out + (int64_t(b) * n + qg) * (int64_t(Hq) * HD) + int64_t(h) * HD;
+#pragma unroll
+    for (int db = 0; db < ND; ++db) {
+      u32x2 pk;
+      pk[0] = uint32_t(f2bf(o[qi][db][0] * inv)) | (uint32_t(f2bf(o[qi][db][1] * inv)) << 16);
+      pk[1] = uint32_t(f2bf(o[qi][db][2] * inv)) | (uint32_t(f2bf(o[qi][db][3] * inv)) << 16);
+      *reinterpret_cast<u32x2*>(orow + 16 * db + 4 * grp) = pk;
+    }
+  }
+}
+
+
+// ------------------------------------------------------ register prefetch
+
+constexpr int kVtLD = kKV + 4;  // padded row of the transposed V tile (bf16 elements)
 
 template <int HD>
-struct AttnTile {
+struct StagedTile {
   static constexpr int kNch = HD / 8;                              // 16-byte chunks per row
   static constexpr int kSwz = (kNch < 8 ? kNch : 8) - 1;
   static constexpr int kKChunks = kKV * kNch;                      // K tile chunks
@@ -43,30 +308,30 @@ struct AttnTile {
 // flight during compute), then written to the other LDS buffer: one barrier
 // per tile.
 template <int HD>
-struct AttnPrefetch {
-  using A = AttnTile<HD>;
+struct StagedPrefetch {
+  using A = StagedTile<HD>;
   u32x4 k[A::kKIter];
   u32x4 v0[A::kVIter], v1[A::kVIter];
 
-  // Rows past the last key are loaded from row n - 1 (always valid memory):
-  // their scores are masked to -inf and their V rows are weighted by zero.
-  __device__ __forceinline__ void load(const uint16_t* Kh, const uint16_t* Vh, int kb0, int n, int tid) {
+  // Tile rows are read through a buffer resource that starts at the tile's
+  // first key and ends at key n - 1: rows past the last key read as zeros
+  // (their scores are masked to -inf and their V rows weighted by zero), and
+  // each lane's offsets are the same for every tile.
+  __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t kr, __amdgpu_buffer_rsrc_t vr, int tid) {
 #pragma unroll
     for (int i = 0; i < A::kKIter; ++i) {
       const int c = tid + 256 * i;
-      if (A::kKChunks % 256 == 0 || c < A::kKChunks) {
-        const int key = min(kb0 + c / A::kNch, n - 1);
-        k[i] = *reinterpret_cast<const u32x4*>(Kh + int64_t(key) * HD + (c % A::kNch) * 8);
-      }
+      if (A::kKChunks % 256 == 0 || c < A::kKChunks)
+        k[i] = __builtin_amdgcn_raw_buffer_load_b128(kr, (c / A::kNch) * (HD * 2) + (c % A::kNch) * 16, 0, 0);
     }
 #pragma unroll
     for (int i = 0; i < A::kVIter; ++i) {
       const int c = tid + 256 * i;
       if (A::kVPairs % 256 == 0 || c < A::kVPairs) {
         const int kp = c % (kKV / 2), ch = c / (kKV / 2);
-        const int key0 = min(kb0 + 2 * kp, n - 1), key1 = min(kb0 + 2 * kp + 1, n - 1);
-        v0[i] = *reinterpret_cast<const u32x4*>(Vh + int64_t(key0) * HD + ch * 8);
-        v1[i] = *reinterpret_cast<const u32x4*>(Vh + int64_t(key1) * HD + ch * 8);
+        const int off = 2 * kp * (HD * 2) + ch * 16;
+        v0[i] = __builtin_amdgcn_raw_buffer_load_b128(vr, off, 0, 0);
+        v1[i] = __builtin_amdgcn_raw_buffer_load_b128(vr, off + HD * 2, 0, 0);
       }
     }
   }
@@ -99,11 +364,11 @@ struct AttnPrefetch {
 };
 
 template <int HD, int NQ>
-__global__ __launch_bounds__(256) void attn_bf16_kernel(const uint16_t* __restrict__ Q,
-                                                        const uint16_t* __restrict__ K,
-                                                        const uint16_t* __restrict__ V, int Hq, int Hkv,
-                                                        int n, uint16_t* __restrict__ out) {
-  using A = AttnTile<HD>;
+__global__ __launch_bounds__(256) void attn_bf16_staged_kernel(const uint16_t* __restrict__ Q,
+                                                               const uint16_t* __restrict__ K,
+                                                               const uint16_t* __restrict__ V, int Hq, int Hkv,
+                                                               int n, uint16_t* __restrict__ out) {
+  using A = StagedTile<HD>;
   constexpr int QB = 64 * NQ;          // queries per workgroup
   constexpr int NS = HD / 32;          // MFMA k steps over the head dim
   constexpr int ND = HD / 16;          // 16-row blocks of the head dim
@@ -135,9 +400,18 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const uint16_t* __restri
   // it, an L2 hit): with a fixed number of loads in flight the wait before a
   // set is written covers exactly that set, not the set loaded after it.
   const int last = ntiles - 1;
-  AttnPrefetch<HD> pfA, pfB;
-  pfA.load(Kh, Vh, 0, n, tid);
-  pfB.load(Kh, Vh, min(1, last) * kKV, n, tid);
+  // buffer resources over keys kb0 .. n - 1 of this (sequence, kv head)
+  auto rows_from = [&](const uint16_t* base, int kb0) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base + int64_t(kb0) * HD), (short)0,
+                                             (n - kb0) * (HD * 2), 0x00020000);
+  };
+  auto fetch = [&](StagedPrefetch<HD>& pf, int t) {
+    const int kb0 = min(t, last) * kKV;
+    pf.load(rows_from(Kh, kb0), rows_from(Vh, kb0), tid);
+  };
+  StagedPrefetch<HD> pfA, pfB;
+  fetch(pfA, 0);
+  fetch(pfB, 1);
 
   // Q^T operand: lane (query r16, group grp) holds Q[query][32 s + 8 grp .. +8]
   bf16x8 qf[NQ][NS];
@@ -150,12 +424,16 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const uint16_t* __restri
       qf[qi][s] = *reinterpret_cast<const bf16x8*>(Qh + int64_t(qrow) * HD + 32 * s + 8 * grp);
   }
 
-  f32x4 o[NQ][ND];
-  float m_run[NQ], l_run[NQ];
+  // all-ones A operand: l_run accumulates the row sums of P on the matrix cores
+  bf16x8 ones;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) ones[i] = (__bf16)1.0f;
+  f32x4 o[NQ][ND], l_run[NQ];
+  float m_run[NQ];
 #pragma unroll
   for (int qi = 0; qi < NQ; ++qi) {
     m_run[qi] = -INFINITY;
-    l_run[qi] = 0.f;
+    l_run[qi] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int db = 0; db < ND; ++db) o[qi][db] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
@@ -164,7 +442,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const uint16_t* __restri
 
   pfA.store(reinterpret_cast<uint16_t*>(smem), reinterpret_cast<uint16_t*>(smem + A::kKBytes), tid);
   __syncthreads();
-  pfA.load(Kh, Vh, min(2, last) * kKV, n, tid);
+  fetch(pfA, 2);
   // one tile: scores, online softmax and P V over LDS buffer t & 1
   auto tile = [&](int t) {
     const int kb0 = t * kKV;
@@ -210,16 +488,11 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const uint16_t* __restri
         // running max in log2 units of the scaled scores (sc > 0 keeps the order)
         const float m_new = fmaxf(m_run[qi], rows4_max(mx) * sc);
         const float base = m_new == -INFINITY ? 0.f : m_new;
-        float sum = 0.f;
         float p[4][4];
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            p[kb][i] = __builtin_amdgcn_exp2f(fmaf(s[qi][kb][i], sc, -base));
-            sum += p[kb][i];
-          }
-        sum = rows4_sum(sum);
+          for (int i = 0; i < 4; ++i) p[kb][i] = __builtin_amdgcn_exp2f(fmaf(s[qi][kb][i], sc, -base));
         // rescale the running sums only when some lane's max moved (rare after the first tiles)
         if (__builtin_amdgcn_ballot_w64(m_new != m_run[qi])) {
           const float alpha = __builtin_amdgcn_exp2f(m_run[qi] - base);
@@ -227,7 +500,6 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const uint16_t* __restri
 #pragma unroll
           for (int db = 0; db < ND; ++db) o[qi][db] *= alpha;
         }
-        l_run[qi] += sum;
         m_run[qi] = m_new;
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks)
@@ -238,6 +510,11 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const uint16_t* __restri
           }
       }
       // O^T[dim 16 db + r16 .. ][query] += V^T P^T over this tile's 64 keys
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+        for (int qi = 0; qi < NQ; ++qi)
+          l_run[qi] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb[qi][ks], l_run[qi], 0, 0, 0);
 #pragma unroll
       for (int db = 0; db < ND; ++db) {
         const int dim = 16 * db + r16;
@@ -257,11 +534,11 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const uint16_t* __restri
   };
   // after tile t: write tile t + 1 (held in `held`) to the other buffer, then
   // refill `held` with tile t + 3
-  auto advance = [&](int t, AttnPrefetch<HD>& held) {
+  auto advance = [&](int t, StagedPrefetch<HD>& held) {
     held.store(reinterpret_cast<uint16_t*>(smem + ((t + 1) & 1) * A::kStage),
                reinterpret_cast<uint16_t*>(smem + ((t + 1) & 1) * A::kStage + A::kKBytes), tid);
     __syncthreads();
-    held.load(Kh, Vh, min(t + 3, last) * kKV, n, tid);
+    fetch(held, t + 3);
   };
   for (int t = 0; t < ntiles; t += 2) {
     tile(t);  // pfB holds tile t + 1, pfA tile t + 2
@@ -275,7 +552,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const uint16_t* __restri
   for (int qi = 0; qi < NQ; ++qi) {
     const int qg = qw0 + 16 * qi + r16;
     if (qg >= n) continue;
-    const float inv = 1.0f / l_run[qi];
+    const float inv = 1.0f / l_run[qi][0];
     uint16_t* orow = out + (int64_t(b) * n + qg) * (int64_t(Hq) * HD) + int64_t(h) * HD;
 #pragma unroll
     for (int db = 0; db < ND; ++db) {
@@ -330,6 +607,8 @@ static void launch_timed(K kern, dim3 grid, dim3 block, hipStream_t s, A... args
   else kern<<<grid, block, 0, s>>>(args...);
 }
 
+constexpr int kAttnDmaMaxKeys = 2048;  // longest sequence sent to the DMA ring at head dim 64
+
 hipError_t launch_attention(int dtype, const void* q, const void* k, const void* v, int B, int Hq, int Hkv,
                             int n, int hd, void* out, hipStream_t s) {
   if (n == 0 || B == 0) return hipSuccess;
@@ -345,15 +624,23 @@ hipError_t launch_attention(int dtype, const void* q, const void* k, const void*
     }
     return hipGetLastError();
   }
-  // Query groups per wave: two at hd = 128, where sharing each K/V fragment
-  // between 32 queries measured 1.2-1.3x faster; one at hd <= 64, where it
-  // made no difference and one keeps more workgroups per CU.
+  // Measured choice between the two stagings: the DMA ring with one query
+  // group per wave is faster up to about 2k keys per sequence at head dim
+  // <= 64 (more, shorter workgroups and no staging VALU: -7 to -18 % at 600 -
+  // 1563 keys); beyond that, register prefetch with two query groups per wave,
+  // which shares each K/V tile between 128 queries, is faster (-4 to -12 % at
+  // 2362 - 3000 keys), and at head dim 128 it is the only one of the two that
+  // fits two waves per SIMD.
   auto grid = [&](int nq) { return dim3(((n + 64 * nq - 1) / (64 * nq)) * Hq * B); };
   auto Qp = (const uint16_t*)q; auto Kp = (const uint16_t*)k; auto Vp = (const uint16_t*)v; auto O = (uint16_t*)out;
+  const bool dma = n <= kAttnDmaMaxKeys;
   switch (hd) {
-    case 32: launch_timed(attn_bf16_kernel<32, 1>, grid(1), dim3(256), s, Qp, Kp, Vp, Hq, Hkv, n, O); break;
-    case 64: launch_timed(attn_bf16_kernel<64, 1>, grid(1), dim3(256), s, Qp, Kp, Vp, Hq, Hkv, n, O); break;
-    case 128: launch_timed(attn_bf16_kernel<128, 2>, grid(2), dim3(256), s, Qp, Kp, Vp, Hq, Hkv, n, O); break;
+    case 32: launch_timed(attn_bf16_dma_kernel<32, 1>, grid(1), dim3(256), s, Qp, Kp, Vp, Hq, Hkv, n, O); break;
+    case 64:
+      if (dma) launch_timed(attn_bf16_dma_kernel<64, 1>, grid(1), dim3(256), s, Qp, Kp, Vp, Hq, Hkv, n, O);
+      else launch_timed(attn_bf16_staged_kernel<64, 2>, grid(2), dim3(256), s, Qp, Kp, Vp, Hq, Hkv, n, O);
+      break;
+    case 128: launch_timed(attn_bf16_staged_kernel<128, 2>, grid(2), dim3(256), s, Qp, Kp, Vp, Hq, Hkv, n, O); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -40,6 +40,24 @@ def test_attention_matches_oracle(dev, dtype, hd, B, Hq, Hkv, n):
                                    np.repeat(to_np(v[b, :, 0]), Hq // Hkv, axis=0), rtol=TOL[dtype], atol=1e-2)
 
 
+@pytest.mark.parametrize("hd,Hq,Hkv,n", [(64, 2, 1, 2048), (64, 2, 1, 2049), (64, 3, 3, 2300), (32, 2, 2, 2100)])
+def test_attention_long_sequences(dev, hd, Hq, Hkv, n):
+    """Both bf16 stagings: up to 2048 keys per sequence (head dim 64) the DMA
+    ring runs, beyond it the register-prefetch kernel with two query groups
+    per wave; head dim 32 stays on the DMA ring at any length."""
+    announce(f"attention long hd={hd} Hq={Hq} Hkv={Hkv} n={n}")
+    g = torch.Generator().manual_seed(n + hd)
+    q = torch.randn(1, Hq, n, hd, generator=g).to(torch.bfloat16)
+    k = torch.randn(1, Hkv, n, hd, generator=g).to(torch.bfloat16)
+    v = torch.randn(1, Hkv, n, hd, generator=g).to(torch.bfloat16)
+    out = torch.empty(1, n, Hq * hd, dtype=torch.bfloat16, device=dev)
+    P.attention_forward(q.to(dev), k.to(dev), v.to(dev), out)
+    torch.cuda.synchronize()
+    ref = O.causal_attention(to_np(q[0]).transpose(1, 0, 2), to_np(k[0]).transpose(1, 0, 2),
+                             to_np(v[0]).transpose(1, 0, 2))
+    assert rel_inf(to_np(out)[0], ref) < TOL[torch.bfloat16]
+
+
 def test_attention_deterministic(dev):
     announce("attention determinism")
     g = torch.Generator().manual_seed(5)
