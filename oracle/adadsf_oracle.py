@@ -37,6 +37,13 @@ Readings taken where the paper is silent or ambiguous (each also in the design doc):
 * Eq. 9's softmax runs over the hidden dimension of each token, and its
   2-norm is taken over the layer's whole hidden-state tensor. Eq. 10 is
   evaluated per row of logits, with the classes on the last axis.
+* Decoding is not treated by the paper. Per-sequence Top-K needs the whole
+  sequence, so at decode time a new token is kept by a layer when its router
+  score is at least a per-(layer, sequence) threshold; a kept token joins the
+  layer's kept set at its original position and attends causally over it.
+  Every step of the layer is causal, so decoding token by token with given
+  keep decisions equals the stack over the whole sequence with the same kept
+  sets (decode_stack and kept_set_stack below; the CPU tests check this).
 
 Parity status: every function here is pinned by the CPU tests (closed forms,
 invariants, brute force, and library cross-checks against torch and the
@@ -533,3 +540,80 @@ def align_stack(desc: Dict, Ws: List[Dict], x, ks: Sequence[int]) -> Tuple[np.nd
         xs = routed_layer(desc, W, xs, int(k))["y"] if k > 0 else xs
         sums.append(float(np.sum(hidden_align_sq(xs, xd))))
     return np.asarray(sums), xs, xd
+
+
+# ---------------------------------------------------------------------------
+# Incremental decoding (not treated by the paper; see the reading in the
+# header): threshold routing of each new token and per-layer kept sets.
+# ---------------------------------------------------------------------------
+
+def keep_by_threshold(scores, thr) -> np.ndarray:
+    """A new token is kept iff its router score >= the threshold (NaN: not kept)."""
+    return np.asarray(scores, dtype=np.float64) >= np.asarray(thr, dtype=np.float64)
+
+
+def kept_set_layer(desc: Dict, W: Dict, x, keeps: Sequence[Sequence[int]],
+                   out_dtype: Optional[str] = None) -> np.ndarray:
+    """One layer with explicit kept positions per sequence (the sets may differ
+    in size): the block runs on each sequence's kept rows at their positions,
+    the other rows pass through unchanged (Section 3.4 with a given selection).
+    """
+    x = f64(x)
+    y = x.copy()
+    for b in range(x.shape[0]):
+        pos = np.asarray(sorted(keeps[b]), dtype=np.int64)
+        if pos.size == 0:
+            continue
+        rows = x[b, pos] + block_delta(desc, W, x[b, pos], pos)
+        y[b, pos] = rows if out_dtype is None else round_to(out_dtype, rows)
+    return y
+
+
+def kept_set_stack(desc: Dict, Ws: List[Dict], x, keeps_per_layer,
+                   out_dtype: Optional[str] = None) -> np.ndarray:
+    """kept_set_layer for l = 0..L-1; keeps_per_layer[l][b] = kept positions."""
+    x = f64(x)
+    for W, keeps in zip(Ws, keeps_per_layer):
+        x = kept_set_layer(desc, W, x, keeps, out_dtype)
+    return x
+
+
+def decode_stack(desc: Dict, Ws: List[Dict], x, thr=None, force=None,
+                 out_dtype: Optional[str] = None) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
+    """Tokens t = 0..T-1 of every sequence processed one at a time.
+
+    At layer l, token t's router score is taken on its current hidden state;
+    the token is kept iff score >= thr[l][b] (or force[l][b][t] when force is
+    given). A kept token's output is its row plus the block's update computed
+    over the layer's kept rows so far (their layer inputs at their positions),
+    itself last; a skipped token passes through. Returns (y [B, T, d],
+    keep [L, B, T] bool, scores [L, B, T]).
+    """
+    x = f64(x)
+    B, T, _ = x.shape
+    L = len(Ws)
+    y = x.copy()
+    keep = np.zeros((L, B, T), dtype=bool)
+    scores = np.zeros((L, B, T))
+    kept_in = [[[] for _ in range(B)] for _ in range(L)]  # layer inputs of the kept rows
+    kept_pos = [[[] for _ in range(B)] for _ in range(L)]
+    for t in range(T):
+        for b in range(B):
+            row = y[b, t].copy()
+            for l, W in enumerate(Ws):
+                s = router_scores(row[None, None, :], W["router_w1"], W["router_b1"], W["router_w2"],
+                                  W.get("router_b2", 0.0))[0, 0]
+                scores[l, b, t] = s
+                kl = bool(force[l][b][t]) if force is not None else bool(keep_by_threshold(s, thr[l][b]))
+                keep[l, b, t] = kl
+                if not kl:
+                    continue
+                kept_in[l][b].append(row)
+                kept_pos[l][b].append(t)
+                rows = np.stack(kept_in[l][b])
+                delta = block_delta(desc, W, rows, np.asarray(kept_pos[l][b]))[-1]
+                row = row + delta
+                if out_dtype is not None:
+                    row = round_to(out_dtype, row)
+            y[b, t] = row
+    return y, keep, scores
