@@ -299,6 +299,63 @@ int dsf_stack_forward(const dsf_layer_desc* desc, const dsf_layer_weights* weigh
                       double* sim_accum, void* workspace, size_t workspace_bytes,
                       hipStream_t stream);
 
+/* ---------------------- incremental decoding with kept-token KV caches */
+
+/* The paper treats the prefill only. Per-sequence Top-K (Section 3.4) needs
+ * the whole sequence, so at decode time a new token is kept by layer l iff its
+ * router score, taken on its hidden state at that layer, is >= a threshold
+ * thr[l][b]. Each layer holds a cache of its kept tokens' keys and values
+ * (after RoPE at their original positions): a kept token appends its key and
+ * value and attends causally over the cache; a skipped token passes the layer
+ * unchanged. Every step of the layer is causal, so decoding token by token
+ * with the keep decisions of a prefill's Top-K reproduces that prefill.
+ *
+ * Caches, per layer l: cache_k[l] and cache_v[l] (host arrays [L] of device
+ * pointers) are [B, Hkv, cap, hd] in dtype, 16-byte aligned, owned by the
+ * caller; cache_len (device int32 [L][B]) counts the valid slots of each
+ * (layer, sequence) and is updated by the calls. Slots at or beyond
+ * cache_len are never read. */
+
+/* Workspace bytes of dsf_decode_step for batch B, positions < max_pos and
+ * caches of cap slots (0 on a bad argument). No initialisation needed;
+ * overlapping calls need separate workspaces. */
+size_t dsf_decode_workspace_size(const dsf_layer_desc* desc, int dtype, int B, int max_pos, int cap);
+
+/* One decode step of the L-layer stack. x (device [B, d] in dtype, in place)
+ * holds each sequence's new token, at original position pos[b] (device int32
+ * [B]; clamped to [0, max_pos)). For l = 0..L-1, on the device:
+ *   1. s = router(x[b]); scores_out (nullable, device float [L][B]) gets s;
+ *   2. keep = s >= thr[l][b] (thr device float [L][B]: -inf keeps, +inf skips,
+ *      a NaN score is not kept); a token that would be kept while its cache is
+ *      full (cache_len == cap) is skipped; keep_out (nullable, device int32
+ *      [L][B]) gets 1 (kept), 0 (skipped) or 2 (skipped: cache full);
+ *   3. kept tokens: QKV with RoPE at pos[b]; key and value stored at slot
+ *      cache_len[l][b], which then grows by one; the query attends over slots
+ *      0..cache_len[l][b]-1 (itself included); x[b] += the block's update.
+ *      Skipped tokens: x[b] unchanged (bitwise).
+ * All B rows run through the projections and the keep flags are applied in
+ * the cache append and the residual update, so nothing waits for the host.
+ * Head dims 32, 64, 128. Errors: DSF_EINVAL for null or misaligned pointers
+ * and bad sizes, DSF_EWORKSPACE for a short workspace. */
+int dsf_decode_step(const dsf_layer_desc* desc, const dsf_layer_weights* weights, int L, int dtype,
+                    void* x, int B, const int32_t* pos, int max_pos, const float* thr,
+                    float* scores_out, int32_t* keep_out, void* const* cache_k, void* const* cache_v,
+                    int32_t* cache_len, int cap, void* workspace, size_t workspace_bytes,
+                    hipStream_t stream);
+
+/* Prefill into decode caches: dsf_stack_forward over x [B, T, d] with k[l]
+ * kept tokens per layer (no flags, no similarity) that also stores each
+ * layer's kept keys and values (RoPE at their positions, in position order)
+ * in slots 0..k[l]-1 of cache_k[l] / cache_v[l] and sets cache_len[l][b] =
+ * k[l] (k[l] <= cap). thr_out (nullable, device float [L][B]) gets the lowest
+ * router score among each sequence's kept tokens (+inf for k[l] = 0): the
+ * threshold that keeps a new token when it would rank among the prompt's
+ * selection. Workspace: dsf_workspace_size(desc, dtype, B, T, max k, 0). */
+int dsf_stack_prefill(const dsf_layer_desc* desc, const dsf_layer_weights* weights, int L,
+                      int dtype, const int* k, void* x, int B, int T, void* const* cache_k,
+                      void* const* cache_v, int32_t* cache_len, int cap, float* thr_out,
+                      void* workspace, size_t workspace_bytes, hipStream_t stream);
+
 /* ------------------------- alignment objective (Section 3.5, Eqs. 9-11) */
 
 /* Workspace bytes of dsf_align_hidden and dsf_kl_align for n_rows rows (0 on

@@ -34,7 +34,7 @@ EXPORTS = [
     "dsf_sparse_block_forward", "dsf_stack_forward", "dsf_timing_enable", "dsf_timing_read",
     "dsf_gate_score_grad", "dsf_router_backward_workspace_size", "dsf_router_backward",
     "dsf_align_workspace_size", "dsf_align_hidden", "dsf_kl_align", "dsf_align_stack_workspace_size",
-    "dsf_align_stack_forward",
+    "dsf_align_stack_forward", "dsf_decode_workspace_size", "dsf_decode_step", "dsf_stack_prefill",
 ]
 
 
@@ -100,6 +100,9 @@ def lib() -> ctypes.CDLL:
         "dsf_kl_align": ([vp, vp, i32, i64, i32, vp, vp, vp, sz, vp], i32),
         "dsf_align_stack_workspace_size": ([vp, i32, i32, i32], sz),
         "dsf_align_stack_forward": ([vp, vp, i32, i32, vp, vp, vp, i32, i32, i32, vp, vp, sz, vp], i32),
+        "dsf_decode_workspace_size": ([vp, i32, i32, i32, i32], sz),
+        "dsf_decode_step": ([vp, vp, i32, i32, vp, i32, vp, i32, vp, vp, vp, vp, vp, vp, i32, vp, sz, vp], i32),
+        "dsf_stack_prefill": ([vp, vp, i32, i32, vp, vp, i32, i32, vp, vp, vp, i32, vp, vp, sz, vp], i32),
     }
     for name, (args, res) in sig.items():
         fn = getattr(L, name)
@@ -302,6 +305,46 @@ def align_stack_forward(desc: LayerDesc, weights: Sequence[LayerWeights], ks: Se
            lib().dsf_align_stack_forward(ctypes.addressof(desc), ctypes.addressof(arr), L, _dtype_code(x_sparse),
                                          ctypes.addressof(karr), _ptr(x_sparse), _ptr(x_dense), B, T, flags,
                                          _ptr(hid_accum), _ptr(workspace), workspace.numel(), _stream(stream)))
+
+
+def decode_workspace_size(desc: LayerDesc, dtype: int, B: int, max_pos: int, cap: int) -> int:
+    return lib().dsf_decode_workspace_size(ctypes.addressof(desc), dtype, B, max_pos, cap)
+
+
+def _ptr_array(tensors):
+    return (ctypes.c_void_p * max(len(tensors), 1))(*[_ptr(t) for t in tensors])
+
+
+def decode_step(desc: LayerDesc, weights: Sequence[LayerWeights], x, pos, max_pos: int, thr, cache_k, cache_v,
+                cache_len, workspace, scores_out=None, keep_out=None, stream=None):
+    """x [B, d]; pos int32 [B]; thr float [L, B]; cache_k / cache_v: L tensors [B, Hkv, cap, hd];
+    cache_len int32 [L, B]."""
+    B = x.shape[0]
+    L = len(weights)
+    cap = cache_k[0].shape[2] if L else 1
+    arr = (LayerWeights * max(L, 1))(*weights)
+    ck, cv = _ptr_array(cache_k), _ptr_array(cache_v)
+    _check("dsf_decode_step",
+           lib().dsf_decode_step(ctypes.addressof(desc), ctypes.addressof(arr), L, _dtype_code(x), _ptr(x), B,
+                                 _ptr(pos), max_pos, _ptr(thr), _ptr(scores_out), _ptr(keep_out),
+                                 ctypes.addressof(ck), ctypes.addressof(cv), _ptr(cache_len), cap, _ptr(workspace),
+                                 workspace.numel(), _stream(stream)))
+
+
+def stack_prefill(desc: LayerDesc, weights: Sequence[LayerWeights], ks: Sequence[int], x, cache_k, cache_v,
+                  cache_len, workspace, thr_out=None, stream=None):
+    """dsf_stack_forward over x [B, T, d] that also fills the decode caches."""
+    B, T, _ = x.shape
+    L = len(weights)
+    cap = cache_k[0].shape[2] if L else 1
+    arr = (LayerWeights * max(L, 1))(*weights)
+    karr = (ctypes.c_int * max(L, 1))(*[int(k) for k in ks])
+    ck, cv = _ptr_array(cache_k), _ptr_array(cache_v)
+    _check("dsf_stack_prefill",
+           lib().dsf_stack_prefill(ctypes.addressof(desc), ctypes.addressof(arr), L, _dtype_code(x),
+                                   ctypes.addressof(karr), _ptr(x), B, T, ctypes.addressof(ck), ctypes.addressof(cv),
+                                   _ptr(cache_len), cap, _ptr(thr_out), _ptr(workspace), workspace.numel(),
+                                   _stream(stream)))
 
 
 def timing_enable(max_records: int, kinds: Optional[Sequence[str]] = None):

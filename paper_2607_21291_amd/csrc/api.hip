@@ -836,6 +836,278 @@ extern "C" int dsf_stack_forward(const dsf_layer_desc* desc, const dsf_layer_wei
   return DSF_OK;
 }
 
+// ------------------------------------------- incremental decoding
+
+namespace {
+struct DecodePlan {
+  size_t scores, keep, gate, a1, a2, q, k, v, attn, act, h, m2, rope, part, total;
+};
+
+DecodePlan make_decode_plan(const dsf_layer_desc& D, int dtype, int B, int max_pos, int cap) {
+  const size_t eb = elem_bytes(dtype), n = size_t(B);
+  const bool qwen = D.block == DSF_BLOCK_QWEN_SEQ;
+  DecodePlan p{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t o = off;
+    off += up256(bytes > 0 ? bytes : 1);
+    return o;
+  };
+  p.scores = take(4 * n);
+  p.keep = take(4 * n);
+  p.gate = take(4 * n);
+  p.a1 = take(eb * n * D.d_model);
+  p.a2 = qwen ? 0 : take(eb * n * D.d_model);
+  p.q = take(eb * n * D.n_heads * D.head_dim);
+  p.k = take(eb * n * D.n_kv_heads * D.head_dim);
+  p.v = take(eb * n * D.n_kv_heads * D.head_dim);
+  p.attn = take(eb * n * D.n_heads * D.head_dim);
+  p.act = take(eb * n * D.d_ff);
+  p.h = qwen ? take(eb * n * D.d_model) : 0;
+  p.m2 = qwen ? take(eb * n * D.d_model) : 0;
+  p.rope = take(4 * size_t(max_pos) * D.rotary_dims);
+  p.part = take(4 * n * D.n_heads * size_t(decode_attn_chunks(cap)) * (D.head_dim + 2));
+  p.total = off;
+  return p;
+}
+
+struct DecCtx {
+  const dsf_layer_desc* D;
+  int dtype, B, max_pos, cap;
+  char* ws;
+  DecodePlan plan;
+  hipStream_t s;
+};
+
+template <typename P>
+P* dat(const DecCtx& c, size_t off) {
+  return reinterpret_cast<P*>(c.ws + off);
+}
+
+// One layer of a decode step on the B new tokens (one row of x per sequence).
+// Every row runs through the projections; the keep flags select which rows
+// append to the cache and which receive the block's update (gate +inf / -inf
+// in the gated residual epilogue: exactly x + delta or x).
+int run_decode_layer(const DecCtx& c, const dsf_layer_weights* W, void* x, const int32_t* pos, const float* thr,
+                     float* scores_out, int32_t* keep_out, void* ck, void* cv, int32_t* len) {
+  const dsf_layer_desc& D = *c.D;
+  const int B = c.B, d = D.d_model, hd = D.head_dim, Hq = D.n_heads, Hkv = D.n_kv_heads, f = D.d_ff;
+  const int dq = Hq * hd, dkv = Hkv * hd;
+  const bool qwen = D.block == DSF_BLOCK_QWEN_SEQ;
+  float* scores = scores_out ? scores_out : dat<float>(c, c.plan.scores);
+  int32_t* keep = dat<int32_t>(c, c.plan.keep);
+  float* gate = dat<float>(c, c.plan.gate);
+  DSF_HIP(launch_router(c.dtype, x, B, d, D.d_router, W->router_w1, W->router_b1, W->router_w2, W->router_b2,
+                        scores, c.s));
+  DSF_HIP(launch_decode_route(scores, thr, B, len, c.cap, keep, gate, keep_out, c.s));
+
+  NormArgs na{};
+  na.dtype = c.dtype;
+  na.src = x;
+  na.src_rows = 0;  // compact rows: x [B, d]
+  na.B = B;
+  na.kk = 1;
+  na.d = d;
+  na.eps = D.norm_eps;
+  na.rms = qwen;
+  na.w1 = W->norm1_w;
+  na.b1 = W->norm1_b;
+  na.out1 = dat<char>(c, c.plan.a1);
+  if (!qwen) {
+    na.w2 = W->norm2_w;
+    na.b2 = W->norm2_b;
+    na.out2 = dat<char>(c, c.plan.a2);
+  }
+  DSF_HIP(launch_norm(na, c.s));
+
+  GemmArgs g{};
+  g.dtype = c.dtype;
+  g.B = B;
+  g.kk = 1;
+  g.T = 1;
+  g.M = B;
+  if (!qwen) {  // FFN up + GELU on LN2
+    GemmArgs u = g;
+    u.N = f; u.K = d; u.K1 = d;
+    u.a = na.out2; u.lda = d;
+    u.b = W->w_up; u.ldb = d;
+    u.epi = EPI_BIAS_GELU; u.bias = W->b_up;
+    u.out = dat<char>(c, c.plan.act); u.ldo = f;
+    DSF_HIP(launch_gemm(u, c.s));
+  }
+  {  // QKV, bias, RoPE at each new token's position
+    GemmArgs q = g;
+    q.T = c.max_pos;
+    q.idx = pos;
+    q.N = dq + 2 * dkv; q.K = d; q.K1 = d;
+    q.a = na.out1; q.lda = d;
+    q.b = W->w_qkv; q.ldb = d;
+    q.epi = EPI_QKV_ROPE;
+    q.bias = W->b_qkv;
+    q.q = dat<char>(c, c.plan.q); q.k = dat<char>(c, c.plan.k); q.v = dat<char>(c, c.plan.v);
+    q.Hq = Hq; q.Hkv = Hkv; q.hd = hd; q.R = D.rotary_dims;
+    q.rope = dat<float>(c, c.plan.rope);
+    DSF_HIP(launch_gemm(q, c.s));
+  }
+  DSF_HIP(launch_kv_append(c.dtype, dat<char>(c, c.plan.k), dat<char>(c, c.plan.v), keep, ck, cv, len, B, Hkv, hd,
+                           c.cap, c.s));
+  DSF_HIP(launch_decode_attention(c.dtype, dat<char>(c, c.plan.q), ck, cv, len, B, Hq, Hkv, hd, c.cap,
+                                  dat<float>(c, c.plan.part), dat<char>(c, c.plan.attn), c.s));
+  if (!qwen) {  // parallel residual: [attn | act] . [W_o | W_down]^T + biases, gated by keep
+    GemmArgs o = g;
+    o.N = d; o.K = dq + f; o.K1 = dq;
+    o.a = dat<char>(c, c.plan.attn); o.lda = dq;
+    o.a2 = dat<char>(c, c.plan.act); o.lda2 = f;
+    o.b = W->w_o; o.ldb = dq;
+    o.b2 = W->w_down; o.ldb2 = f;
+    o.epi = EPI_RESID_SCATTER_GATE; o.bias = W->b_o; o.bias2 = W->b_down;
+    o.x = x; o.gate = gate;
+    DSF_HIP(launch_gemm(o, c.s));
+    return DSF_OK;
+  }
+  {  // h = x + attn . W_o^T
+    GemmArgs o = g;
+    o.N = d; o.K = dq; o.K1 = dq;
+    o.a = dat<char>(c, c.plan.attn); o.lda = dq;
+    o.b = W->w_o; o.ldb = dq;
+    o.epi = EPI_RESID_STORE; o.bias = W->b_o;
+    o.x = x; o.out = dat<char>(c, c.plan.h); o.ldo = d;
+    DSF_HIP(launch_gemm(o, c.s));
+  }
+  NormArgs n2{};
+  n2.dtype = c.dtype;
+  n2.src = dat<char>(c, c.plan.h);
+  n2.src_rows = 0;
+  n2.B = B;
+  n2.kk = 1;
+  n2.d = d;
+  n2.eps = D.norm_eps;
+  n2.rms = 1;
+  n2.w1 = W->norm2_w;
+  n2.out1 = dat<char>(c, c.plan.m2);
+  DSF_HIP(launch_norm(n2, c.s));
+  {  // SwiGLU
+    GemmArgs u = g;
+    u.N = f; u.K = d; u.K1 = d;
+    u.a = n2.out1; u.lda = d;
+    u.b = W->w_up; u.ldb = d;
+    u.epi = EPI_SWIGLU; u.f = f;
+    u.out = dat<char>(c, c.plan.act); u.ldo = f;
+    DSF_HIP(launch_gemm(u, c.s));
+  }
+  {  // x + keep * ((h - x) + act . W_down^T)
+    GemmArgs o = g;
+    o.N = d; o.K = f; o.K1 = f;
+    o.a = dat<char>(c, c.plan.act); o.lda = f;
+    o.b = W->w_down; o.ldb = f;
+    o.epi = EPI_RESID_SCATTER_GATE; o.bias = W->b_down;
+    o.x = x; o.res = dat<char>(c, c.plan.h); o.gate = gate;
+    DSF_HIP(launch_gemm(o, c.s));
+  }
+  return DSF_OK;
+}
+
+int check_caches(void* const* cache_k, void* const* cache_v, int L) {
+  DSF_CHECK(cache_k && cache_v, DSF_EINVAL, "null cache pointer arrays");
+  for (int l = 0; l < L; ++l) {
+    DSF_CHECK(cache_k[l] && cache_v[l], DSF_EINVAL, "null cache for layer %d", l);
+    DSF_CHECK(aligned16(cache_k[l]) && aligned16(cache_v[l]), DSF_EINVAL, "caches of layer %d must be 16-byte aligned",
+              l);
+  }
+  return DSF_OK;
+}
+}  // namespace
+
+extern "C" size_t dsf_decode_workspace_size(const dsf_layer_desc* desc, int dtype, int B, int max_pos, int cap) {
+  if (check_desc(desc) || check_dtype(dtype) || B < 0 || max_pos < 1 || cap < 1) return 0;
+  return make_decode_plan(*desc, dtype, B, max_pos, cap).total;
+}
+
+extern "C" int dsf_decode_step(const dsf_layer_desc* desc, const dsf_layer_weights* weights, int L, int dtype,
+                               void* x, int B, const int32_t* pos, int max_pos, const float* thr, float* scores_out,
+                               int32_t* keep_out, void* const* cache_k, void* const* cache_v, int32_t* cache_len,
+                               int cap, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  int rc = check_desc(desc);
+  if (rc) return rc;
+  rc = check_dtype(dtype);
+  if (rc) return rc;
+  DSF_CHECK(L >= 0 && B >= 0, DSF_EINVAL, "L and B must be >= 0");
+  DSF_CHECK(B <= (1 << 20), DSF_EINVAL, "B too large");
+  DSF_CHECK(max_pos >= 1 && cap >= 1, DSF_EINVAL, "max_pos and cap must be >= 1");
+  DSF_CHECK(int64_t(B) * desc->n_kv_heads * cap * desc->head_dim < (int64_t(1) << 40), DSF_EINVAL, "cache too large");
+  if (L == 0 || B == 0) return DSF_OK;
+  DSF_CHECK(weights && x && pos && thr && cache_len, DSF_EINVAL, "null pointer");
+  DSF_CHECK(aligned16(x), DSF_EINVAL, "x must be 16-byte aligned");
+  rc = check_caches(cache_k, cache_v, L);
+  if (rc) return rc;
+  const DecodePlan plan = make_decode_plan(*desc, dtype, B, max_pos, cap);
+  DSF_CHECK(workspace_bytes >= plan.total, DSF_EWORKSPACE, "workspace needs %zu bytes, got %zu", plan.total,
+            workspace_bytes);
+  DSF_CHECK(workspace && (reinterpret_cast<uintptr_t>(workspace) & 255u) == 0, DSF_EINVAL,
+            "workspace must be non-null and 256-byte aligned");
+  for (int l = 0; l < L; ++l) {
+    rc = check_weights(*desc, &weights[l], l);
+    if (rc) return rc;
+  }
+  rc = check_device();
+  if (rc) return rc;
+  DecCtx c{desc, dtype, B, max_pos, cap, (char*)workspace, plan, stream};
+  DSF_HIP(launch_rope_table(dat<float>(c, plan.rope), max_pos, desc->rotary_dims, desc->rope_theta, stream));
+  for (int l = 0; l < L; ++l) {
+    rc = run_decode_layer(c, &weights[l], x, pos, thr + size_t(l) * B, scores_out ? scores_out + size_t(l) * B : nullptr,
+                          keep_out ? keep_out + size_t(l) * B : nullptr, cache_k[l], cache_v[l],
+                          cache_len + size_t(l) * B);
+    if (rc) return rc;
+  }
+  return DSF_OK;
+}
+
+extern "C" int dsf_stack_prefill(const dsf_layer_desc* desc, const dsf_layer_weights* weights, int L, int dtype,
+                                 const int* k, void* x, int B, int T, void* const* cache_k, void* const* cache_v,
+                                 int32_t* cache_len, int cap, float* thr_out, void* workspace, size_t workspace_bytes,
+                                 hipStream_t stream) {
+  DSF_CHECK(L >= 0, DSF_EINVAL, "L < 0");
+  DSF_CHECK(L == 0 || (weights && k), DSF_EINVAL, "null weights or k");
+  DSF_CHECK(cap >= 1, DSF_EINVAL, "cap must be >= 1");
+  int k_max = 0;
+  for (int l = 0; l < L; ++l) {
+    DSF_CHECK(k[l] >= 0 && k[l] <= T && k[l] <= cap, DSF_EINVAL, "k[%d]=%d outside [0, min(T=%d, cap=%d)]", l, k[l],
+              T, cap);
+    k_max = k[l] > k_max ? k[l] : k_max;
+  }
+  Plan plan{};
+  int rc = check_common(desc, dtype, x, B, T, k_max, 0, workspace, workspace_bytes, false, &plan);
+  if (rc) return rc;
+  if (L == 0 || B == 0) return DSF_OK;
+  DSF_CHECK(cache_len, DSF_EINVAL, "null cache_len");
+  rc = check_caches(cache_k, cache_v, L);
+  if (rc) return rc;
+  for (int l = 0; l < L; ++l) {
+    rc = check_weights(*desc, &weights[l], l);
+    if (rc) return rc;
+  }
+  rc = check_device();
+  if (rc) return rc;
+  Ctx c{desc, dtype, B, T, (char*)workspace, plan, stream, 0, nullptr};
+  rc = get_aux(&c.aux);
+  if (rc) return rc;
+  rc = reset_stream_k(c);
+  if (rc) return rc;
+  if (T > 0) DSF_HIP(launch_rope_table(at<float>(c, plan.rope), T, desc->rotary_dims, desc->rope_theta, stream));
+  for (int l = 0; l < L; ++l) {
+    if (k[l] > 0) {
+      rc = run_layer(c, &weights[l], x, k[l], false, false, nullptr, nullptr, nullptr);
+      if (rc) return rc;
+    }
+    DSF_HIP(launch_kv_fill(dtype, at<char>(c, plan.k), at<char>(c, plan.v), cache_k[l], cache_v[l],
+                           cache_len + size_t(l) * B, B, desc->n_kv_heads, desc->head_dim, k[l], cap, stream));
+    if (thr_out)
+      DSF_HIP(launch_kept_min_score(at<float>(c, plan.scores), at<int32_t>(c, plan.idx), B, T, k[l],
+                                    thr_out + size_t(l) * B, stream));
+  }
+  return DSF_OK;
+}
+
 // ------------------------------------------- alignment objective (Sec. 3.5)
 
 extern "C" size_t dsf_align_workspace_size(int64_t n_rows) {

@@ -138,4 +138,20 @@ int gemm_flag_count();
 hipError_t launch_attention(int dtype, const void* q, const void* k, const void* v, int B, int Hq,
                             int Hkv, int n, int hd, void* out, hipStream_t s);
 
+// ---- incremental decoding (kernels_decode.hip) ----
+hipError_t launch_decode_route(const float* scores, const float* thr, int B, const int32_t* cache_len, int cap,
+                               int32_t* keep, float* gate, int32_t* keep_out, hipStream_t s);
+hipError_t launch_kv_append(int dtype, const void* knew, const void* vnew, const int32_t* keep, void* ck, void* cv,
+                            int32_t* cache_len, int B, int Hkv, int hd, int cap, hipStream_t s);
+int decode_attn_chunks(int cap);
+// q [B, Hq, hd]; caches [B, Hkv, cap, hd] with cache_len[b] valid slots;
+// part: B * Hq * decode_attn_chunks(cap) * (hd + 2) floats; out [B, Hq * hd].
+hipError_t launch_decode_attention(int dtype, const void* q, const void* ck, const void* cv,
+                                   const int32_t* cache_len, int B, int Hq, int Hkv, int hd, int cap, float* part,
+                                   void* out, hipStream_t s);
+hipError_t launch_kv_fill(int dtype, const void* ks, const void* vs, void* ck, void* cv, int32_t* cache_len, int B,
+                          int Hkv, int hd, int k, int cap, hipStream_t s);
+hipError_t launch_kept_min_score(const float* scores, const int32_t* idx, int B, int T, int k, float* thr,
+                                 hipStream_t s);
+
 }  // namespace dsf

@@ -200,6 +200,36 @@ def test_error_paths_of_the_kernel_calls():
                                      FAKE, FAKE, 2, 64, 0, FAKE, FAKE, aws - 256, None) == 3     # workspace
     assert L.dsf_align_stack_forward(ctypes.addressof(d), ctypes.addressof(wts), 2, P.F32, ctypes.addressof(ks),
                                      FAKE, FAKE, 2, 64, 0, None, FAKE, aws, None) == 1           # hid_accum
+    # incremental decoding
+    dws = L.dsf_decode_workspace_size(ctypes.addressof(d), P.F32, 4, 128, 64)
+    assert dws > 0 and dws % 256 == 0
+    assert L.dsf_decode_workspace_size(ctypes.addressof(d), P.F32, 4, 0, 64) == 0         # max_pos
+    assert L.dsf_decode_workspace_size(ctypes.addressof(d), P.F32, 4, 128, 0) == 0        # cap
+    assert L.dsf_decode_workspace_size(ctypes.addressof(_desc(head_dim=48)), P.F32, 4, 128, 64) == 0
+    caches = (ctypes.c_void_p * 2)(FAKE, FAKE)
+    bad = (ctypes.c_void_p * 2)(FAKE, FAKE + 8)
+    ds = L.dsf_decode_step
+    dargs = lambda **kw: [kw.get(n, v) for n, v in [
+        ("desc", ctypes.addressof(d)), ("w", ctypes.addressof(wts)), ("L", 2), ("dtype", P.F32), ("x", FAKE),
+        ("B", 4), ("pos", FAKE), ("max_pos", 128), ("thr", FAKE), ("sc", None), ("keep", None),
+        ("ck", ctypes.addressof(caches)), ("cv", ctypes.addressof(caches)), ("len", FAKE), ("cap", 64),
+        ("ws", FAKE), ("wsb", dws), ("s", None)]]
+    assert ds(*dargs(ws=FAKE, wsb=dws - 256)) == 3                                         # workspace
+    assert ds(*dargs(cv=ctypes.addressof(bad))) == 1                                       # cache alignment
+    assert ds(*dargs(pos=None)) == 1
+    assert ds(*dargs(thr=None)) == 1
+    assert ds(*dargs(cap=0)) == 1
+    assert ds(*dargs(x=FAKE + 4)) == 1
+    assert ds(*dargs(dtype=7)) == 2
+    assert ds(*dargs(B=0, x=None, pos=None, thr=None)) == 0                                # empty
+    pws = P.workspace_size(d, P.F32, 2, 64, 32)
+    sp = L.dsf_stack_prefill
+    assert sp(ctypes.addressof(d), ctypes.addressof(wts), 2, P.F32, ctypes.addressof(ks), FAKE, 2, 64,
+              ctypes.addressof(caches), ctypes.addressof(caches), FAKE, 16, None, FAKE, pws, None) == 1  # k > cap
+    assert sp(ctypes.addressof(d), ctypes.addressof(wts), 2, P.F32, ctypes.addressof(ks), FAKE, 2, 64,
+              ctypes.addressof(caches), ctypes.addressof(caches), None, 64, None, FAKE, pws, None) == 1  # cache_len
+    assert sp(ctypes.addressof(d), ctypes.addressof(wts), 2, P.F32, ctypes.addressof(ks), FAKE, 2, 64,
+              ctypes.addressof(caches), ctypes.addressof(caches), FAKE, 64, None, FAKE, pws - 256, None) == 3
     # empty problems are valid no-ops
     assert L.dsf_topk_select(None, 0, 10, 3, None, None) == 0
     assert L.dsf_gather_rows(None, 1, 2, 10, 16, None, 0, None, None) == 0
