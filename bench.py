@@ -270,6 +270,64 @@ def alignment_objective(P, C, w, ks, dev, desc, weights, x0, ms_plain, steps):
     return out
 
 
+def decode_leg(P, C, w, ks, dev, desc, weights, x0, steps):
+    """Incremental decoding (the paper treats prefill only): the stack is
+    prefilled over the batch's T tokens into per-layer caches of the kept
+    tokens' keys and values, with thresholds = the lowest kept score of each
+    (layer, sequence); then decode steps of one new synthetic token per
+    sequence, routed by those thresholds on the device. Bytes per step: every
+    layer's weights once plus the cached keys and values the step reads."""
+    import torch
+    B, T, L = w.batch, w.seq, w.n_layers
+    dcode = P.F32 if w.dtype == "f32" else P.BF16
+    warm = 3
+    n = warm + steps
+    cap = T + n
+    ck = [torch.empty(B, w.n_kv_heads, cap, w.head_dim, dtype=w.torch_dtype, device=dev) for _ in range(L)]
+    cv = [torch.empty(B, w.n_kv_heads, cap, w.head_dim, dtype=w.torch_dtype, device=dev) for _ in range(L)]
+    clen = torch.zeros(L, B, dtype=torch.int32, device=dev)
+    thr = torch.empty(L, B, dtype=torch.float32, device=dev)
+    x = x0.clone()
+    wsp = torch.empty(P.workspace_size(desc, dcode, B, T, max(ks)), dtype=torch.uint8, device=dev)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    P.stack_prefill(desc, weights, ks, x, ck, cv, clen, wsp, thr_out=thr)
+    torch.cuda.synchronize()
+    prefill_ms = (time.perf_counter() - t0) * 1e3
+    del wsp
+    lens0 = clen.cpu().numpy()
+    ws = torch.empty(P.decode_workspace_size(desc, dcode, B, cap, cap), dtype=torch.uint8, device=dev)
+    g = torch.Generator().manual_seed(1234)
+    toks = [(torch.randn(B, w.d_model, generator=g) * 0.02).to(w.torch_dtype).to(dev) for _ in range(n)]
+    pos = [torch.full((B,), T + i, dtype=torch.int32, device=dev) for i in range(n)]
+    keep = torch.zeros(n, L, B, dtype=torch.int32, device=dev)
+    for i in range(warm):
+        P.decode_step(desc, weights, toks[i], pos[i], cap, thr, ck, cv, clen, ws, keep_out=keep[i])
+    lens_start = clen.cpu().numpy()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for i in range(warm, n):
+        P.decode_step(desc, weights, toks[i], pos[i], cap, thr, ck, cv, clen, ws, keep_out=keep[i])
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    lens_end = clen.cpu().numpy()
+    mean_lens = ((lens_start + lens_end) / 2.0).tolist()
+    nbytes = C.decode_step_bytes(w, B, mean_lens)
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    kept = keep[warm:].float().mean().item()
+    del ck, cv, toks, ws
+    torch.cuda.empty_cache()
+    return {"tokens_per_s": B / (ms / 1e3), "ms_per_step": ms, "batch": B, "prefill_tokens": T,
+            "prefill_ms": prefill_ms, "steps": steps, "cache_capacity": cap,
+            "cache_len_after_prefill_mean": float(lens0.mean()), "kept_fraction_decode": kept,
+            "roofline": {"bound": "hbm", "bytes_per_step": nbytes, "achieved": gbs, "peak": PEAK_HBM_GBS,
+                         "unit": "GB/s", "frac": gbs / PEAK_HBM_GBS},
+            "note": "routing rule at decode time (not in the paper): keep iff score >= the prefill's lowest kept "
+                    "score of that (layer, sequence)"}
+
+
 def cpu_baseline(w, ks, layers, min_seconds=10.0):
     """The oracle, as it stands, on whole sequences through `layers` layers.
 
@@ -535,6 +593,9 @@ def main():
         log("alignment objective: teacher/student stack, Eq. 9 and Eq. 10 kernels")
         out["alignment_objective"] = alignment_objective(P, C, w, ks, dev, desc, weights, x0, ms_step,
                                                          max(3, args.steps // 3))
+    if not (args.only_sparse or args.no_extras):
+        log("incremental decoding: prefill into kept-token caches, then threshold-routed decode steps")
+        out["decode"] = decode_leg(P, C, w, ks, dev, desc, weights, x0, max(10, args.steps))
     if not args.no_cpu_baseline:
         layers_cpu = L if args.cpu_layers is None else min(args.cpu_layers, L)
         log(f"cpu oracle baseline over {layers_cpu} layers of one sequence")

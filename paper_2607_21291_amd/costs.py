@@ -108,6 +108,30 @@ def kl_align_bytes(eb: int, rows: int, classes: int) -> float:
     return 2.0 * eb * rows * classes + 4.0 * rows
 
 
+def layer_weight_bytes(w) -> float:
+    """One layer's weights in the workload's storage format (projections,
+    router, norms and biases)."""
+    eb = 4 if w.dtype == "f32" else 2
+    m = 2 if w.block == NEOX else 3
+    d, hd = w.d_model, w.head_dim
+    proj = d * (w.n_heads + 2 * w.n_kv_heads) * hd + w.n_heads * hd * d + m * d * w.d_ff
+    router = w.d_router * d + 2 * w.d_router
+    norms = (4 if w.block == NEOX else 2) * d
+    qkv_bias = (w.n_heads + 2 * w.n_kv_heads) * hd  # both families bias the QKV projection
+    biases = qkv_bias + (2 * d + w.d_ff if w.block == NEOX else 0)
+    return float(eb * (proj + router + norms + biases))
+
+
+def decode_step_bytes(w, B: int, cache_lens) -> float:
+    """HBM bytes one decode step must move: every layer's weights once, the
+    keys and values of every cached kept token (cache_lens: [L][B] lengths
+    read by the step), and the B new rows in and out of each layer."""
+    eb = 4 if w.dtype == "f32" else 2
+    kv = sum(sum(lb) for lb in cache_lens) * 2.0 * w.n_kv_heads * w.head_dim * eb
+    rows = len(cache_lens) * 2.0 * B * w.d_model * eb
+    return len(cache_lens) * layer_weight_bytes(w) + kv + rows
+
+
 def kind_work(w, kind: str, B: int, T: int, k: int):
     """(work, unit) of one layer's launches of a kernel kind: flops for the
     MFMA kernels, bytes for the streaming ones; None for kinds not modelled."""

@@ -840,7 +840,7 @@ extern "C" int dsf_stack_forward(const dsf_layer_desc* desc, const dsf_layer_wei
 
 namespace {
 struct DecodePlan {
-  size_t scores, keep, gate, a1, a2, q, k, v, attn, act, h, m2, rope, part, total;
+  size_t scores, keep, gate, a1, a2, q, k, v, attn, act, h, m2, rope, part, spart, scount, total;
 };
 
 DecodePlan make_decode_plan(const dsf_layer_desc& D, int dtype, int B, int max_pos, int cap) {
@@ -867,6 +867,10 @@ DecodePlan make_decode_plan(const dsf_layer_desc& D, int dtype, int B, int max_p
   p.m2 = qwen ? take(eb * n * D.d_model) : 0;
   p.rope = take(4 * size_t(max_pos) * D.rotary_dims);
   p.part = take(4 * n * D.n_heads * size_t(decode_attn_chunks(cap)) * (D.head_dim + 2));
+  // few-row GEMMs (bf16, B <= 16): split-K partial tiles and tile counters
+  const bool few = dtype == DSF_BF16 && B <= 16;
+  p.spart = few ? take(gemm_skinny_partial_bytes()) : 0;
+  p.scount = few ? take(sizeof(uint32_t) * gemm_skinny_counters()) : 0;
   p.total = off;
   return p;
 }
@@ -926,6 +930,10 @@ int run_decode_layer(const DecCtx& c, const dsf_layer_weights* W, void* x, const
   g.kk = 1;
   g.T = 1;
   g.M = B;
+  if (c.plan.scount) {
+    g.spart = dat<float>(c, c.plan.spart);
+    g.scount = dat<uint32_t>(c, c.plan.scount);
+  }
   if (!qwen) {  // FFN up + GELU on LN2
     GemmArgs u = g;
     u.N = f; u.K = d; u.K1 = d;
@@ -1053,6 +1061,7 @@ extern "C" int dsf_decode_step(const dsf_layer_desc* desc, const dsf_layer_weigh
   if (rc) return rc;
   DecCtx c{desc, dtype, B, max_pos, cap, (char*)workspace, plan, stream};
   DSF_HIP(launch_rope_table(dat<float>(c, plan.rope), max_pos, desc->rotary_dims, desc->rope_theta, stream));
+  if (plan.scount) DSF_HIP(launch_zero_u32(dat<uint32_t>(c, plan.scount), gemm_skinny_counters(), stream));
   for (int l = 0; l < L; ++l) {
     rc = run_decode_layer(c, &weights[l], x, pos, thr + size_t(l) * B, scores_out ? scores_out + size_t(l) * B : nullptr,
                           keep_out ? keep_out + size_t(l) * B : nullptr, cache_k[l], cache_v[l],

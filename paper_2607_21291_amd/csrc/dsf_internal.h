@@ -125,6 +125,11 @@ struct GemmArgs {
   // zeroed before the first launch using them; epoch is nonzero and distinct
   // for every launch between two zeroings.
   float* part; uint32_t* flags; uint32_t epoch;
+  // Few-row workspace (nullable): with M <= 16 rows (decode steps) a bf16 GEMM
+  // splits K over workgroups; spart holds gemm_skinny_partial_bytes() and
+  // scount gemm_skinny_counters() words, zero before the first launch using
+  // them (each launch leaves them zero).
+  float* spart; uint32_t* scount;
   // set by the launcher: number of M tiles; workgroups per XCD of a persistent
   // grid (0: one tile per workgroup); 1 if its last round is split along K
   int ntm; int px; int split;
@@ -132,6 +137,8 @@ struct GemmArgs {
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t s);
 size_t gemm_partial_bytes();
 int gemm_flag_count();
+size_t gemm_skinny_partial_bytes();
+int gemm_skinny_counters();
 
 // ---- attention over kept tokens (kernels_attn.hip) ----
 // q [B, Hq, n, hd], k/v [B, Hkv, n, hd] -> out [B, n, Hq*hd], causal over the n tokens.

@@ -118,25 +118,29 @@ __device__ __forceinline__ float block4_sum(float v, float* red) {
 constexpr int kDecChunk = 256;  // keys per workgroup of the decode attention
 
 // Workgroup (chunk c, head h, sequence b): keys c*256 .. of the first
-// cache_len[b] slots of kv head h / (Hq / Hkv). Thread t scores key c*256 + t
-// (q . k / sqrt(hd), fp32), the chunk's max m and sum l of exp(s - m) are
-// formed, and o = sum_t exp(s_t - m) v_t with threads split into 256 / HD
-// groups of HD dims (group g takes keys t = g mod groups, then the groups add
-// in order). part[(b, h, c)] = {m, l, o[0..HD)}; an empty chunk stores
-// m = -inf, l = 0.
+// cache_len[b] slots of kv head h / (Hq / Hkv). Key and value rows are read as
+// 16-byte vectors, HD / 8 (bf16) or HD / 4 (fp32) lanes per row, so a group
+// of lanes reads one whole row: scores q . k / sqrt(hd) in fp32 (the group
+// adds its lanes' products with xor shuffles), the chunk's max m and sum l of
+// exp(s - m), then o = sum_t exp(s_t - m) v_t with each lane owning one
+// vector of dims and the row groups added in order through LDS.
+// part[(b, h, c)] = {m, l, o[0..HD)}; an empty chunk stores m = -inf, l = 0.
 template <typename T, int HD>
 __global__ __launch_bounds__(256) void decode_attn_part_kernel(const T* __restrict__ q, const T* __restrict__ ck,
                                                                const T* __restrict__ cv,
                                                                const int32_t* __restrict__ cache_len, int Hq,
                                                                int Hkv, int cap, float* __restrict__ part) {
-  constexpr int G = 256 / HD;  // dim groups of the P V product
-  __shared__ float qs[HD];
+  constexpr int VEC = 16 / int(sizeof(T));  // elements per 16-byte vector
+  constexpr int LPK = HD / VEC;             // lanes per key row
+  constexpr int KPP = 256 / LPK;            // rows per pass
+  constexpr int NPASS = kDecChunk / KPP;
+  static_assert(LPK <= 64 && 64 % LPK == 0, "row groups within a wavefront");
   __shared__ float ps[kDecChunk];
   __shared__ float red[4];
-  __shared__ float osum[G][HD];
+  __shared__ float osum[KPP][HD];
   const int c = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const int nch = gridDim.x;
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, sub = tid % LPK, row = tid / LPK;
   const int len = min(cache_len[b], cap);
   const int k0 = c * kDecChunk;
   float* dst = part + ((int64_t(b) * Hq + h) * nch + c) * (HD + 2);
@@ -149,34 +153,54 @@ __global__ __launch_bounds__(256) void decode_attn_part_kernel(const T* __restri
     return;
   }
   const int kvh = h / (Hq / Hkv);
-  const T* qr = q + (int64_t(b) * Hq + h) * HD;
-  if (tid < HD) qs[tid] = DecElem<T>::to_f(qr[tid]);
-  __syncthreads();
-  const T* kbase = ck + ((int64_t(b) * Hkv + kvh) * cap) * HD;
-  const T* vbase = cv + ((int64_t(b) * Hkv + kvh) * cap) * HD;
-  const int j = k0 + tid;
-  float s = -INFINITY;
-  if (j < len) {
-    const T* kr = kbase + int64_t(j) * HD;
+  const T* qr = q + (int64_t(b) * Hq + h) * HD + sub * VEC;
+  float qv[VEC];
+#pragma unroll
+  for (int i = 0; i < VEC; ++i) qv[i] = DecElem<T>::to_f(qr[i]);
+  const T* kbase = ck + ((int64_t(b) * Hkv + kvh) * cap) * HD + sub * VEC;
+  const T* vbase = cv + ((int64_t(b) * Hkv + kvh) * cap) * HD + sub * VEC;
+  const float scale = 1.0f / sqrtf(float(HD));
+#pragma unroll 4
+  for (int pass = 0; pass < NPASS; ++pass) {
+    const int j = pass * KPP + row, key = k0 + j;
     float acc = 0.f;
-#pragma unroll 8
-    for (int e = 0; e < HD; ++e) acc = fmaf(qs[e], DecElem<T>::to_f(kr[e]), acc);
-    s = acc * (1.0f / sqrtf(float(HD)));
+    if (key < len) {
+      T kv[VEC];
+      *reinterpret_cast<u32x4*>(kv) = *reinterpret_cast<const u32x4*>(kbase + int64_t(key) * HD);
+#pragma unroll
+      for (int i = 0; i < VEC; ++i) acc = fmaf(qv[i], DecElem<T>::to_f(kv[i]), acc);
+    }
+#pragma unroll
+    for (int o = LPK / 2; o > 0; o >>= 1) acc += __shfl_xor(acc, o, 64);
+    if (sub == 0) ps[j] = key < len ? acc * scale : -INFINITY;
   }
-  const float m = block4_max(s, red);
-  const float p = j < len ? expf(s - m) : 0.f;
+  __syncthreads();
+  const float sv = ps[tid];
+  const float m = block4_max(sv, red);
+  const float p = sv == -INFINITY ? 0.f : expf(sv - m);
   ps[tid] = p;
   const float l = block4_sum(p, red);  // its barriers also publish ps
-  const int g = tid / HD, dd = tid - g * HD;
-  const int nk = min(kDecChunk, len - k0);
-  float o = 0.f;
-  for (int t = g; t < nk; t += G) o = fmaf(ps[t], DecElem<T>::to_f(vbase[int64_t(k0 + t) * HD + dd]), o);
-  osum[g][dd] = o;
+  float o[VEC];
+#pragma unroll
+  for (int i = 0; i < VEC; ++i) o[i] = 0.f;
+#pragma unroll 4
+  for (int pass = 0; pass < NPASS; ++pass) {
+    const int j = pass * KPP + row, key = k0 + j;
+    if (key < len) {
+      T vv[VEC];
+      *reinterpret_cast<u32x4*>(vv) = *reinterpret_cast<const u32x4*>(vbase + int64_t(key) * HD);
+      const float pp = ps[j];
+#pragma unroll
+      for (int i = 0; i < VEC; ++i) o[i] = fmaf(pp, DecElem<T>::to_f(vv[i]), o[i]);
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < VEC; ++i) osum[row][sub * VEC + i] = o[i];
   __syncthreads();
   if (tid < HD) {
     float acc = 0.f;
-#pragma unroll
-    for (int gg = 0; gg < G; ++gg) acc += osum[gg][tid];
+#pragma unroll 8
+    for (int r = 0; r < KPP; ++r) acc += osum[r][tid];
     dst[2 + tid] = acc;
     if (tid == 0) {
       dst[0] = m;

@@ -1018,15 +1018,184 @@ static bool dma_addressable(const GemmArgs& g, int rows_b) {
 
 // Launch kern<<<grid, block>>>(g), through hipExtLaunchKernelGGL when an
 // enclosing timing scope hands over its events.
-template <typename K>
-static void launch_timed(K kern, dim3 grid, dim3 block, hipStream_t s, const GemmArgs& g) {
+template <typename K, typename... A>
+static void launch_timed(K kern, dim3 grid, dim3 block, hipStream_t s, const A&... args) {
   hipEvent_t e0, e1;
-  if (timing_claim(&e0, &e1)) hipExtLaunchKernelGGL(kern, grid, block, 0, s, e0, e1, 0, g);
-  else kern<<<grid, block, 0, s>>>(g);
+  if (timing_claim(&e0, &e1)) hipExtLaunchKernelGGL(kern, grid, block, 0, s, e0, e1, 0, args...);
+  else kern<<<grid, block, 0, s>>>(args...);
+}
+
+// ------------------------------------------- few-row GEMM (decode steps)
+
+// For M <= 16 rows the tile GEMMs leave most of the chip idle (N / 128
+// workgroups). Here a workgroup takes 128 output columns and one slice of K:
+// each of its four wavefronts computes a 16 x 32 block (two
+// v_mfma_f32_16x16x32_bf16 blocks) from operands loaded straight from global
+// memory (16 bytes per lane, 64 contiguous bytes per weight row and k-step),
+// so the weights stream once over ~256-512 workgroups. With one slice the
+// workgroup finishes its tile; otherwise it publishes its fp32 partial tile
+// with device-coherent stores, and the last of the tile's workgroups to
+// arrive (a device-scope counter, reset by that workgroup) adds the slices in
+// slice order (deterministic) and runs the same fused epilogue as the tile
+// GEMMs. No workgroup waits for another.
+constexpr int kSkinnyRows = 16, kSkinnyBN = 128;
+constexpr int kSkinnyMaxParts = 1024;   // partial tiles per launch
+constexpr int kSkinnyCounters = 1024;   // column tiles per launch
+
+size_t gemm_skinny_partial_bytes() { return size_t(kSkinnyMaxParts) * kSkinnyRows * kSkinnyBN * sizeof(float); }
+int gemm_skinny_counters() { return kSkinnyCounters; }
+
+template <int EPI>
+__global__ __launch_bounds__(256) void gemm_skinny_kernel(GemmArgs g, int splits, int kc) {
+  constexpr int LD = kSkinnyBN + 4;
+  __shared__ float stage[kSkinnyRows * LD];
+  __shared__ int is_last;
+  const int tn = int(blockIdx.x) / splits, sl = int(blockIdx.x) - tn * splits;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r16 = lane & 15, grp = lane >> 4;
+  const int k0 = sl * kc, k1 = min(g.K, k0 + kc);
+  // the B rows (output columns) of this lane in the wave's two 16-column blocks
+  const uint16_t* brow[2];
+  const uint16_t* brow2[2];
+  bool bok[2];
+#pragma unroll
+  for (int nb = 0; nb < 2; ++nb) {
+    const int c = wave * 32 + nb * 16 + r16;  // column within the tile
+    int r;
+    if constexpr (EPI == EPI_SWIGLU) {
+      // tile columns [0, 64) are gate units, [64, 128) the matching up units
+      r = c < kSkinnyBN / 2 ? tn * (kSkinnyBN / 2) + c : g.f + tn * (kSkinnyBN / 2) + (c - kSkinnyBN / 2);
+      bok[nb] = true;
+    } else {
+      r = tn * kSkinnyBN + c;
+      bok[nb] = r < g.N;
+      if (!bok[nb]) r = 0;
+    }
+    brow[nb] = (const uint16_t*)g.b + int64_t(r) * g.ldb;
+    brow2[nb] = g.b2 ? (const uint16_t*)g.b2 + int64_t(r) * g.ldb2 : nullptr;
+  }
+  const bool aok = r16 < g.M;
+  const uint16_t* arow = (const uint16_t*)g.a + int64_t(aok ? r16 : 0) * g.lda;
+  const uint16_t* arow2 = g.a2 ? (const uint16_t*)g.a2 + int64_t(aok ? r16 : 0) * g.lda2 : nullptr;
+  f32x4 acc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+  const bf16x8 zero = {};
+  // k-steps of 32 (the slice is a multiple of 32; k chunks of 8 never
+  // straddle K1, a multiple of 32), up to 8 at a time: every load of a group
+  // is issued before its MFMAs
+  constexpr int kGroup = 8;
+  const int nsteps = (k1 - k0) / 32;
+  for (int st0 = 0; st0 < nsteps; st0 += kGroup) {
+    bf16x8 af[kGroup], bf[kGroup][2];
+#pragma unroll
+    for (int it = 0; it < kGroup; ++it) {
+      const int k = k0 + 32 * min(st0 + it, nsteps - 1) + 8 * grp;  // past the end: repeat the last step (unused)
+      const bool first = k < g.K1;
+      const int kk = first ? k : k - g.K1;
+      af[it] = aok ? *reinterpret_cast<const bf16x8*>((first ? arow : arow2) + kk) : zero;
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb)
+        bf[it][nb] = bok[nb] ? *reinterpret_cast<const bf16x8*>((first ? brow[nb] : brow2[nb]) + kk) : zero;
+    }
+#pragma unroll
+    for (int it = 0; it < kGroup; ++it)
+      if (st0 + it < nsteps)
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb)
+          acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[it], bf[it][nb], acc[nb], 0, 0, 0);
+  }
+  // lane holds C[m = 4 grp + i][column wave*32 + nb*16 + r16]
+  if (splits == 1) {
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) stage[(4 * grp + i) * LD + wave * 32 + nb * 16 + r16] = acc[nb][i];
+    __syncthreads();
+    gemm_epilogue<uint16_t, kSkinnyRows, kSkinnyBN, 256, EPI>(g, stage, 0, tn, tid);
+    return;
+  }
+  float* part = g.spart + (int64_t(tn) * splits + sl) * (kSkinnyRows * kSkinnyBN);
+#pragma unroll
+  for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      __hip_atomic_store(part + (4 * grp + i) * kSkinnyBN + wave * 32 + nb * 16 + r16, acc[nb][i], __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+  // The device-coherent (sc1) stores have completed before the counter moves,
+  // and the last workgroup reads the partials with device-coherent loads, so
+  // no cache write-back or invalidate is needed (as in the stream-K GEMM).
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  if (tid == 0) {
+    const uint32_t old = __hip_atomic_fetch_add(g.scount + tn, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    is_last = old == uint32_t(splits - 1);
+    if (is_last) __hip_atomic_store(g.scount + tn, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  __syncthreads();
+  if (!is_last) return;
+  // 16 x 128 sums, 8 per thread, slices added in order; the slices' loads
+  // are issued four at a time (device-coherent) before one wait
+  const float* base = g.spart + int64_t(tn) * splits * (kSkinnyRows * kSkinnyBN);
+  const int e0 = tid * 8, m = e0 / kSkinnyBN, c0 = e0 % kSkinnyBN;
+  f32x4 vlo = {0.f, 0.f, 0.f, 0.f}, vhi = {0.f, 0.f, 0.f, 0.f};
+  for (int s0 = 0; s0 < splits; s0 += 4) {
+    f32x4 lo[4], hi[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const float* p = base + int64_t(min(s0 + j, splits - 1)) * (kSkinnyRows * kSkinnyBN) + e0;
+      asm volatile("global_load_dwordx4 %0, %2, off sc1\n\tglobal_load_dwordx4 %1, %2, off offset:16 sc1"
+                   : "=&v"(lo[j]), "=&v"(hi[j])
+                   : "v"(p)
+                   : "memory");
+    }
+    asm volatile("s_waitcnt vmcnt(0)"
+                 : "+v"(lo[0]), "+v"(hi[0]), "+v"(lo[1]), "+v"(hi[1]), "+v"(lo[2]), "+v"(hi[2]), "+v"(lo[3]),
+                   "+v"(hi[3])
+                 :
+                 : "memory");
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      if (s0 + j < splits) {
+        vlo += lo[j];
+        vhi += hi[j];
+      }
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    stage[m * LD + c0 + i] = vlo[i];
+    stage[m * LD + c0 + 4 + i] = vhi[i];
+  }
+  __syncthreads();
+  gemm_epilogue<uint16_t, kSkinnyRows, kSkinnyBN, 256, EPI>(g, stage, 0, tn, tid);
+}
+
+// Slices of K for a few-row launch: enough workgroups to cover the chip
+// (~384) where the reduction allows, each slice a multiple of 32 and at least
+// 128 deep, at most 16 slices (the last workgroup adds them), within the
+// partial-tile budget.
+static void skinny_split(int ntn, int K, int* splits, int* kc) {
+  int s = std::max(1, (384 + ntn - 1) / ntn);
+  s = std::min(s, std::max(1, K / 128));
+  s = std::min(s, 16);
+  s = std::min(s, std::max(1, kSkinnyMaxParts / ntn));
+  int c = (K + s - 1) / s;
+  c = (c + 31) / 32 * 32;
+  *kc = c;
+  *splits = (K + c - 1) / c;
 }
 
 template <int EPI>
 static void launch_gemm_t(const GemmArgs& g, hipStream_t s) {
+  if (g.dtype == DSF_BF16 && g.M <= kSkinnyRows && g.spart && g.scount && g.K % 32 == 0 && g.K1 % 32 == 0 &&
+      g.lda % 8 == 0 && g.ldb % 8 == 0 && (!g.a2 || g.lda2 % 8 == 0) && (!g.b2 || g.ldb2 % 8 == 0)) {
+    const int ntn = EPI == EPI_SWIGLU ? g.f / (kSkinnyBN / 2) : (g.N + kSkinnyBN - 1) / kSkinnyBN;
+    if (ntn <= kSkinnyCounters && (EPI != EPI_SWIGLU || g.f % (kSkinnyBN / 2) == 0)) {
+      int splits = 1, kc = g.K;
+      skinny_split(ntn, g.K, &splits, &kc);
+      launch_timed(gemm_skinny_kernel<EPI>, dim3(ntn * splits), dim3(256), s, g, splits, kc);
+      return;
+    }
+  }
+
   if (DSF_GEMM_USE_DMA && g.dtype == DSF_BF16 && g.K % DSF_GEMM_BK == 0 && g.K1 % DSF_GEMM_BK == 0 &&
       dma_addressable(g, EPI == EPI_SWIGLU ? 2 * g.f : g.N)) {
     constexpr int BM = DSF_GEMM_BM, BN = DSF_GEMM_BN, WM = DSF_GEMM_WM, WN = DSF_GEMM_WN;

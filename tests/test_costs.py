@@ -41,3 +41,21 @@ def test_dense_and_identity_limits():
     proj = 12 * 8 * 2048 * 2 * (768 * 2304 + 768 * 768 + 2 * 768 * 3072)
     attn = 12 * 4 * 64 * 12 * 8 * 2048 * 2049 / 2
     assert dense == pytest.approx(proj + attn, rel=1e-15)
+
+
+def test_layer_weight_bytes_count_the_synthetic_tensors():
+    import synthetic as S
+    for name in ("neox160m", "qwen05b", "tiny_neox_f32", "tiny_qwen_f32"):
+        w = S.WORKLOADS[name]
+        eb = 4 if w.dtype == "f32" else 2
+        W = S.layer_weights(w, 0)
+        n = sum(v.numel() for v in W.values() if hasattr(v, "numel"))
+        assert C.layer_weight_bytes(w) == n * eb, name
+
+
+def test_decode_step_bytes():
+    import synthetic as S
+    w = S.WORKLOADS["neox160m"]
+    lens = [[100] * 8] * 12
+    kv = 12 * 8 * 100 * 2 * w.n_kv_heads * w.head_dim * 2
+    assert C.decode_step_bytes(w, 8, lens) == 12 * C.layer_weight_bytes(w) + kv + 12 * 2 * 8 * w.d_model * 2

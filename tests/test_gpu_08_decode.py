@@ -54,23 +54,26 @@ def _delta_check(w, x, y, y_ref):
     assert rel_inf(to_np(y) - to_np(x), np.asarray(y_ref) - to_np(x)) < TOL[w.dtype]
 
 
-@pytest.mark.parametrize("name,T", [("tiny_neox_f32", 40), ("tiny_qwen_f32", 33), ("neox_bf16_small", 300),
-                                    ("qwen_bf16_small", 48), ("neox_bf16_hd128", 40), ("qwen_bf16_hd128", 37)])
-def test_decode_with_forced_keeps_matches_full_sequence(dev, name, T):
+@pytest.mark.parametrize("name,T,B", [("tiny_neox_f32", 40, 2), ("tiny_qwen_f32", 33, 2), ("neox_bf16_small", 300, 2),
+                                      ("qwen_bf16_small", 48, 2), ("neox_bf16_hd128", 40, 2),
+                                      ("qwen_bf16_hd128", 37, 2), ("neox_bf16_small", 24, 20),
+                                      ("qwen_bf16_small", 20, 17)])
+def test_decode_with_forced_keeps_matches_full_sequence(dev, name, T, B):
+    """B <= 16 runs the projections on the few-row split-K GEMM, B > 16 on the tile GEMMs."""
     w = workload(name).replace(n_layers=2)
-    L, B = 2, 2
+    L = 2
     Ws = S.stack_weights(w)
     dls = [P.DeviceLayer(W, dev) for W in Ws]
     x = S.hidden_states(w, batch=B, seq=T)
     g = np.random.default_rng(T)
     # kept sets of different sizes per (layer, sequence); token 0 skipped by every layer of sequence 1
-    keeps = [[np.sort(g.choice(np.arange(1 if b else 0, T), size=int(T * frac) - b, replace=False))
+    keeps = [[np.sort(g.choice(np.arange(1 if b else 0, T), size=max(1, int(T * frac) - b % 3), replace=False))
               for b in range(B)] for frac in (0.6, 0.35)]
     caches = Caches(w, B, T, L, dev)
     ws = torch.empty(P.decode_workspace_size(make_desc(w), dtype_code(w), B, T, T), dtype=torch.uint8, device=dev)
     y = torch.empty_like(x)
     keep_out = torch.empty(L, B, dtype=torch.int32, device=dev)
-    announce(f"decode forced {name} T={T}")
+    announce(f"decode forced {name} T={T} B={B}")
     for t in range(T):
         forced = np.array([[t in set(keeps[l][b].tolist()) for b in range(B)] for l in range(L)])
         thr = torch.tensor(np.where(forced, -np.inf, np.inf), dtype=torch.float32, device=dev)
