@@ -317,8 +317,8 @@ int dsf_stack_forward(const dsf_layer_desc* desc, const dsf_layer_weights* weigh
  * cache_len are never read. */
 
 /* Workspace bytes of dsf_decode_step for batch B, positions < max_pos and
- * caches of cap slots (0 on a bad argument). No initialisation needed;
- * overlapping calls need separate workspaces. */
+ * caches of cap slots (0 on a bad argument, or cap > 65536). No
+ * initialisation needed; overlapping calls need separate workspaces. */
 size_t dsf_decode_workspace_size(const dsf_layer_desc* desc, int dtype, int B, int max_pos, int cap);
 
 /* One decode step of the L-layer stack. x (device [B, d] in dtype, in place)
@@ -335,8 +335,9 @@ size_t dsf_decode_workspace_size(const dsf_layer_desc* desc, int dtype, int B, i
  *      Skipped tokens: x[b] unchanged (bitwise).
  * All B rows run through the projections and the keep flags are applied in
  * the cache append and the residual update, so nothing waits for the host.
- * Head dims 32, 64, 128. Errors: DSF_EINVAL for null or misaligned pointers
- * and bad sizes, DSF_EWORKSPACE for a short workspace. */
+ * Head dims 32, 64, 128; cap at most 65536 slots (DSF_EUNSUPPORTED above).
+ * Errors: DSF_EINVAL for null or misaligned pointers and bad sizes,
+ * DSF_EWORKSPACE for a short workspace. */
 int dsf_decode_step(const dsf_layer_desc* desc, const dsf_layer_weights* weights, int L, int dtype,
                     void* x, int B, const int32_t* pos, int max_pos, const float* thr,
                     float* scores_out, int32_t* keep_out, void* const* cache_k, void* const* cache_v,

@@ -840,7 +840,9 @@ extern "C" int dsf_stack_forward(const dsf_layer_desc* desc, const dsf_layer_wei
 
 namespace {
 struct DecodePlan {
-  size_t scores, keep, gate, a1, a2, q, k, v, attn, act, h, m2, rope, part, spart, scount, total;
+  size_t scores, keep, gate, a1, a2, q, k, v, attn, act, h, m2, rope, part, spart, counters, total;
+  size_t acount, scount;  // byte offsets within the counters block (zeroed together)
+  int64_t ncounters;
 };
 
 DecodePlan make_decode_plan(const dsf_layer_desc& D, int dtype, int B, int max_pos, int cap) {
@@ -867,10 +869,16 @@ DecodePlan make_decode_plan(const dsf_layer_desc& D, int dtype, int B, int max_p
   p.m2 = qwen ? take(eb * n * D.d_model) : 0;
   p.rope = take(4 * size_t(max_pos) * D.rotary_dims);
   p.part = take(4 * n * D.n_heads * size_t(decode_attn_chunks(cap)) * (D.head_dim + 2));
-  // few-row GEMMs (bf16, B <= 16): split-K partial tiles and tile counters
+  // few-row GEMMs (bf16, B <= 16): split-K partial tiles
   const bool few = dtype == DSF_BF16 && B <= 16;
   p.spart = few ? take(gemm_skinny_partial_bytes()) : 0;
-  p.scount = few ? take(sizeof(uint32_t) * gemm_skinny_counters()) : 0;
+  // counters, zero at the start of a step: decode attention (B * Hq), then the
+  // few-row GEMMs' tile counters
+  const int64_t na = int64_t(n) * D.n_heads, ns = few ? gemm_skinny_counters() : 0;
+  p.ncounters = na + ns;
+  p.counters = take(sizeof(uint32_t) * size_t(p.ncounters));
+  p.acount = p.counters;
+  p.scount = few ? p.counters + sizeof(uint32_t) * size_t(na) : 0;
   p.total = off;
   return p;
 }
@@ -901,9 +909,9 @@ int run_decode_layer(const DecCtx& c, const dsf_layer_weights* W, void* x, const
   float* scores = scores_out ? scores_out : dat<float>(c, c.plan.scores);
   int32_t* keep = dat<int32_t>(c, c.plan.keep);
   float* gate = dat<float>(c, c.plan.gate);
+  const RouteArgs ra{thr, len, c.cap, keep, gate, keep_out};
   DSF_HIP(launch_router(c.dtype, x, B, d, D.d_router, W->router_w1, W->router_b1, W->router_w2, W->router_b2,
-                        scores, c.s));
-  DSF_HIP(launch_decode_route(scores, thr, B, len, c.cap, keep, gate, keep_out, c.s));
+                        scores, c.s, &ra));
 
   NormArgs na{};
   na.dtype = c.dtype;
@@ -960,7 +968,8 @@ int run_decode_layer(const DecCtx& c, const dsf_layer_weights* W, void* x, const
   DSF_HIP(launch_kv_append(c.dtype, dat<char>(c, c.plan.k), dat<char>(c, c.plan.v), keep, ck, cv, len, B, Hkv, hd,
                            c.cap, c.s));
   DSF_HIP(launch_decode_attention(c.dtype, dat<char>(c, c.plan.q), ck, cv, len, B, Hq, Hkv, hd, c.cap,
-                                  dat<float>(c, c.plan.part), dat<char>(c, c.plan.attn), c.s));
+                                  dat<float>(c, c.plan.part), dat<uint32_t>(c, c.plan.acount),
+                                  dat<char>(c, c.plan.attn), c.s));
   if (!qwen) {  // parallel residual: [attn | act] . [W_o | W_down]^T + biases, gated by keep
     GemmArgs o = g;
     o.N = d; o.K = dq + f; o.K1 = dq;
@@ -1027,7 +1036,7 @@ int check_caches(void* const* cache_k, void* const* cache_v, int L) {
 }  // namespace
 
 extern "C" size_t dsf_decode_workspace_size(const dsf_layer_desc* desc, int dtype, int B, int max_pos, int cap) {
-  if (check_desc(desc) || check_dtype(dtype) || B < 0 || max_pos < 1 || cap < 1) return 0;
+  if (check_desc(desc) || check_dtype(dtype) || B < 0 || max_pos < 1 || cap < 1 || cap > kDecodeMaxCap) return 0;
   return make_decode_plan(*desc, dtype, B, max_pos, cap).total;
 }
 
@@ -1042,6 +1051,7 @@ extern "C" int dsf_decode_step(const dsf_layer_desc* desc, const dsf_layer_weigh
   DSF_CHECK(L >= 0 && B >= 0, DSF_EINVAL, "L and B must be >= 0");
   DSF_CHECK(B <= (1 << 20), DSF_EINVAL, "B too large");
   DSF_CHECK(max_pos >= 1 && cap >= 1, DSF_EINVAL, "max_pos and cap must be >= 1");
+  DSF_CHECK(cap <= kDecodeMaxCap, DSF_EUNSUPPORTED, "cache capacity %d above %d slots", cap, kDecodeMaxCap);
   DSF_CHECK(int64_t(B) * desc->n_kv_heads * cap * desc->head_dim < (int64_t(1) << 40), DSF_EINVAL, "cache too large");
   if (L == 0 || B == 0) return DSF_OK;
   DSF_CHECK(weights && x && pos && thr && cache_len, DSF_EINVAL, "null pointer");
@@ -1061,7 +1071,7 @@ extern "C" int dsf_decode_step(const dsf_layer_desc* desc, const dsf_layer_weigh
   if (rc) return rc;
   DecCtx c{desc, dtype, B, max_pos, cap, (char*)workspace, plan, stream};
   DSF_HIP(launch_rope_table(dat<float>(c, plan.rope), max_pos, desc->rotary_dims, desc->rope_theta, stream));
-  if (plan.scount) DSF_HIP(launch_zero_u32(dat<uint32_t>(c, plan.scount), gemm_skinny_counters(), stream));
+  DSF_HIP(launch_zero_u32(dat<uint32_t>(c, plan.counters), plan.ncounters, stream));
   for (int l = 0; l < L; ++l) {
     rc = run_decode_layer(c, &weights[l], x, pos, thr + size_t(l) * B, scores_out ? scores_out + size_t(l) * B : nullptr,
                           keep_out ? keep_out + size_t(l) * B : nullptr, cache_k[l], cache_v[l],

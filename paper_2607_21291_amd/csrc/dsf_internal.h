@@ -27,8 +27,21 @@ struct TimedScope {
 };
 
 // ---- router forward and backward (kernels_router.hip) ----
+// Decode-time routing of the scored tokens, folded into the router (thr null:
+// scores only): keep[t] = scores[t] >= thr[t] && len[t] < cap, gate[t] =
+// keep ? +inf : -inf, keep_out[t] (nullable) = 1 kept, 0 skipped, 2 skipped
+// because the cache is full.
+struct RouteArgs {
+  const float* thr;
+  const int32_t* len;
+  int cap;
+  int32_t* keep;
+  float* gate;
+  int32_t* keep_out;
+};
 hipError_t launch_router(int dtype, const void* x, int64_t n, int d, int d_r, const void* w1,
-                         const void* b1, const void* w2, float b2, float* scores, hipStream_t s);
+                         const void* b1, const void* w2, float b2, float* scores, hipStream_t s,
+                         const RouteArgs* route = nullptr);
 // dscore[B, T] = 0, then at kept positions (1 - sigmoid(s)) <dy, x_out - x_in>
 hipError_t launch_gate_grad(int dtype, const void* dy, const void* x_in, const void* x_out, const float* scores,
                             const int32_t* idx, int B, int T, int k, int d, float* dscore, hipStream_t s);
@@ -146,16 +159,16 @@ hipError_t launch_attention(int dtype, const void* q, const void* k, const void*
                             int Hkv, int n, int hd, void* out, hipStream_t s);
 
 // ---- incremental decoding (kernels_decode.hip) ----
-hipError_t launch_decode_route(const float* scores, const float* thr, int B, const int32_t* cache_len, int cap,
-                               int32_t* keep, float* gate, int32_t* keep_out, hipStream_t s);
 hipError_t launch_kv_append(int dtype, const void* knew, const void* vnew, const int32_t* keep, void* ck, void* cv,
                             int32_t* cache_len, int B, int Hkv, int hd, int cap, hipStream_t s);
 int decode_attn_chunks(int cap);
+constexpr int kDecodeMaxCap = 256 * 256;  // cache slots the decode attention supports
 // q [B, Hq, hd]; caches [B, Hkv, cap, hd] with cache_len[b] valid slots;
-// part: B * Hq * decode_attn_chunks(cap) * (hd + 2) floats; out [B, Hq * hd].
+// part: B * Hq * decode_attn_chunks(cap) * (hd + 2) floats; count: B * Hq
+// words, zero before the launch (the launch leaves them zero); out [B, Hq * hd].
 hipError_t launch_decode_attention(int dtype, const void* q, const void* ck, const void* cv,
                                    const int32_t* cache_len, int B, int Hq, int Hkv, int hd, int cap, float* part,
-                                   void* out, hipStream_t s);
+                                   uint32_t* count, void* out, hipStream_t s);
 hipError_t launch_kv_fill(int dtype, const void* ks, const void* vs, void* ck, void* cv, int32_t* cache_len, int B,
                           int Hkv, int hd, int k, int cap, hipStream_t s);
 hipError_t launch_kept_min_score(const float* scores, const int32_t* idx, int B, int T, int k, float* thr,

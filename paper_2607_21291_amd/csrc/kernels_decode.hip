@@ -3,13 +3,13 @@
 // threshold on the new token's router score, and a kept token attends
 // causally over the layer's cached kept tokens).
 //
-// The projections of a decode step reuse the prefill GEMMs on B rows; the
-// kernels here are the pieces decoding adds:
-// - the routing flags of the new tokens (threshold, cache capacity);
+// The projections of a decode step run on the few-row GEMM and the routing
+// flags come from the router kernel; the kernels here are the other pieces
+// decoding adds:
 // - the append of the kept tokens' keys and values to the caches;
 // - attention of one query per (sequence, head) over its cache, split into
-//   chunks of keys with a fixed-order combine (memory-bound: it reads the
-//   cache once);
+//   chunks of keys whose last-arriving workgroup combines them in chunk
+//   order (memory-bound: it reads the cache once);
 // - for a prefill: copying each layer's kept keys/values into the caches and
 //   the lowest kept score per sequence (the threshold that continues the
 //   prompt's selection).
@@ -19,29 +19,6 @@
 #include "dsf_internal.h"
 
 namespace dsf {
-
-// keep = score >= thr (NaN: not kept); a kept token whose cache is full is
-// skipped and reported as 2. gate = +inf / -inf for the gated residual update
-// (sigmoid gives exactly 1 / 0).
-__global__ void decode_route_kernel(const float* __restrict__ scores, const float* __restrict__ thr, int B,
-                                    const int32_t* __restrict__ cache_len, int cap, int32_t* __restrict__ keep,
-                                    float* __restrict__ gate, int32_t* __restrict__ keep_out) {
-  const int b = blockIdx.x * blockDim.x + threadIdx.x;
-  if (b >= B) return;
-  const bool want = scores[b] >= thr[b];
-  const bool room = cache_len[b] < cap;
-  const int k = want && room;
-  keep[b] = k;
-  gate[b] = k ? INFINITY : -INFINITY;
-  if (keep_out) keep_out[b] = want ? (room ? 1 : 2) : 0;
-}
-
-hipError_t launch_decode_route(const float* scores, const float* thr, int B, const int32_t* cache_len, int cap,
-                               int32_t* keep, float* gate, int32_t* keep_out, hipStream_t s) {
-  if (B == 0) return hipSuccess;
-  decode_route_kernel<<<(B + 255) / 256, 256, 0, s>>>(scores, thr, B, cache_len, cap, keep, gate, keep_out);
-  return hipGetLastError();
-}
 
 // One workgroup per sequence: a kept token's key and value rows (all kv heads)
 // go to slot cache_len[b] of its caches, then the length grows by one (after
@@ -123,37 +100,37 @@ constexpr int kDecChunk = 256;  // keys per workgroup of the decode attention
 // of lanes reads one whole row: scores q . k / sqrt(hd) in fp32 (the group
 // adds its lanes' products with xor shuffles), the chunk's max m and sum l of
 // exp(s - m), then o = sum_t exp(s_t - m) v_t with each lane owning one
-// vector of dims and the row groups added in order through LDS.
-// part[(b, h, c)] = {m, l, o[0..HD)}; an empty chunk stores m = -inf, l = 0.
+// vector of dims and the row groups added in order through LDS. The chunk
+// publishes {m, l, o[0..HD)} with device-coherent stores (an empty chunk:
+// m = -inf, l = 0, o = 0) and counts itself on a device-scope counter; the
+// last chunk of (b, h) to arrive resets the counter and combines the chunks in
+// chunk order: out = sum_c o_c e^(m_c - M) / sum_c l_c e^(m_c - M), M the
+// largest m_c (0 for an empty cache). No workgroup waits for another.
 template <typename T, int HD>
-__global__ __launch_bounds__(256) void decode_attn_part_kernel(const T* __restrict__ q, const T* __restrict__ ck,
-                                                               const T* __restrict__ cv,
-                                                               const int32_t* __restrict__ cache_len, int Hq,
-                                                               int Hkv, int cap, float* __restrict__ part) {
+__global__ __launch_bounds__(256) void decode_attn_kernel(const T* __restrict__ q, const T* __restrict__ ck,
+                                                          const T* __restrict__ cv,
+                                                          const int32_t* __restrict__ cache_len, int Hq, int Hkv,
+                                                          int cap, float* __restrict__ part,
+                                                          uint32_t* __restrict__ count, T* __restrict__ out) {
   constexpr int VEC = 16 / int(sizeof(T));  // elements per 16-byte vector
   constexpr int LPK = HD / VEC;             // lanes per key row
   constexpr int KPP = 256 / LPK;            // rows per pass
   constexpr int NPASS = kDecChunk / KPP;
+  constexpr int kMaxChunks = kDecodeMaxCap / kDecChunk;
   static_assert(LPK <= 64 && 64 % LPK == 0, "row groups within a wavefront");
   __shared__ float ps[kDecChunk];
   __shared__ float red[4];
   __shared__ float osum[KPP][HD];
+  __shared__ float cw[kMaxChunks];
+  __shared__ int is_last;
   const int c = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const int nch = gridDim.x;
   const int tid = threadIdx.x, sub = tid % LPK, row = tid / LPK;
   const int len = min(cache_len[b], cap);
   const int k0 = c * kDecChunk;
-  float* dst = part + ((int64_t(b) * Hq + h) * nch + c) * (HD + 2);
-  if (k0 >= len) {  // uniform
-    if (tid == 0) {
-      dst[0] = -INFINITY;
-      dst[1] = 0.f;
-    }
-    if (tid < HD) dst[2 + tid] = 0.f;
-    return;
-  }
+  const int64_t bh = int64_t(b) * Hq + h;
   const int kvh = h / (Hq / Hkv);
-  const T* qr = q + (int64_t(b) * Hq + h) * HD + sub * VEC;
+  const T* qr = q + bh * HD + sub * VEC;
   float qv[VEC];
 #pragma unroll
   for (int i = 0; i < VEC; ++i) qv[i] = DecElem<T>::to_f(qr[i]);
@@ -197,53 +174,72 @@ __global__ __launch_bounds__(256) void decode_attn_part_kernel(const T* __restri
 #pragma unroll
   for (int i = 0; i < VEC; ++i) osum[row][sub * VEC + i] = o[i];
   __syncthreads();
+  float* dst = part + (bh * nch + c) * (HD + 2);
   if (tid < HD) {
     float acc = 0.f;
 #pragma unroll 8
     for (int r = 0; r < KPP; ++r) acc += osum[r][tid];
-    dst[2 + tid] = acc;
+    __hip_atomic_store(dst + 2 + tid, acc, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (tid == 0) {
-      dst[0] = m;
-      dst[1] = l;
+      __hip_atomic_store(dst, m, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(dst + 1, l, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
-}
-
-// out[b, h*HD + d] = sum_c o_c[d] e^(m_c - M) / sum_c l_c e^(m_c - M), chunks in
-// order (0 when the cache is empty).
-template <typename T, int HD>
-__global__ __launch_bounds__(HD) void decode_attn_combine_kernel(const float* __restrict__ part, int Hq, int nch,
-                                                                 T* __restrict__ out) {
-  const int bh = blockIdx.x, d = threadIdx.x;
-  const float* p = part + int64_t(bh) * nch * (HD + 2);
+  // the device-coherent stores complete before the counter moves; the last
+  // chunk reads them back with device-coherent loads
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  if (tid == 0) {
+    const uint32_t old = __hip_atomic_fetch_add(count + bh, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    is_last = old == uint32_t(nch - 1);
+    if (is_last) __hip_atomic_store(count + bh, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  __syncthreads();
+  if (!is_last) return;
+  const float* pb = part + bh * nch * (HD + 2);
+  for (int cc = tid; cc < nch; cc += 256) {
+    ps[cc] = __hip_atomic_load(pb + int64_t(cc) * (HD + 2), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    cw[cc] = __hip_atomic_load(pb + int64_t(cc) * (HD + 2) + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  __syncthreads();
+  // every thread forms M and L in chunk order from LDS; ps[] holds m_c
   float M = -INFINITY;
-  for (int c = 0; c < nch; ++c) M = fmaxf(M, p[c * (HD + 2)]);
-  float L = 0.f, O = 0.f;
-  if (M != -INFINITY) {
-    for (int c = 0; c < nch; ++c) {
-      const float* pc = p + c * (HD + 2);
-      const float w = pc[0] == -INFINITY ? 0.f : expf(pc[0] - M);
-      L = fmaf(pc[1], w, L);
-      O = fmaf(pc[2 + d], w, O);
+  for (int cc = 0; cc < nch; ++cc) M = fmaxf(M, ps[cc]);
+  float L = 0.f;
+  if (M != -INFINITY)
+    for (int cc = 0; cc < nch; ++cc) L = fmaf(cw[cc], ps[cc] == -INFINITY ? 0.f : expf(ps[cc] - M), L);
+  if (tid < HD) {
+    float O = 0.f;
+    if (M != -INFINITY) {
+      for (int c0 = 0; c0 < nch; c0 += 8) {
+        float v[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          v[j] = __hip_atomic_load(pb + int64_t(min(c0 + j, nch - 1)) * (HD + 2) + 2 + tid, __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          if (c0 + j < nch && ps[c0 + j] != -INFINITY) O = fmaf(v[j], expf(ps[c0 + j] - M), O);
+      }
     }
+    out[bh * HD + tid] = DecElem<T>::from_f(L > 0.f ? O / L : 0.f);
   }
-  out[int64_t(bh) * HD + d] = DecElem<T>::from_f(L > 0.f ? O / L : 0.f);
 }
 
 int decode_attn_chunks(int cap) { return (cap + kDecChunk - 1) / kDecChunk; }
 
 hipError_t launch_decode_attention(int dtype, const void* q, const void* ck, const void* cv,
                                    const int32_t* cache_len, int B, int Hq, int Hkv, int hd, int cap, float* part,
-                                   void* out, hipStream_t s) {
+                                   uint32_t* count, void* out, hipStream_t s) {
   if (B == 0) return hipSuccess;
+  if (cap > kDecodeMaxCap) return hipErrorInvalidValue;
   const int nch = decode_attn_chunks(cap);
   const dim3 grid(nch, Hq, B);
   auto run = [&](auto tag, auto hdc) -> hipError_t {
     using T = decltype(tag);
     constexpr int HD = decltype(hdc)::value;
-    decode_attn_part_kernel<T, HD><<<grid, 256, 0, s>>>((const T*)q, (const T*)ck, (const T*)cv, cache_len, Hq, Hkv,
-                                                        cap, part);
-    decode_attn_combine_kernel<T, HD><<<B * Hq, HD, 0, s>>>(part, Hq, nch, (T*)out);
+    decode_attn_kernel<T, HD><<<grid, 256, 0, s>>>((const T*)q, (const T*)ck, (const T*)cv, cache_len, Hq, Hkv, cap,
+                                                   part, count, (T*)out);
     return hipGetLastError();
   };
   const bool bf = dtype == DSF_BF16;

@@ -92,12 +92,22 @@ __device__ __forceinline__ float router_hidden(const RouterPart<DR>& part, const
   return h;
 }
 
+// Decode-time routing of token t with score v (RouteArgs).
+__device__ __forceinline__ void route_token(const RouteArgs& ra, int64_t t, float v) {
+  const bool want = v >= ra.thr[t];
+  const bool room = ra.len[t] < ra.cap;
+  const int k = want && room;
+  ra.keep[t] = k;
+  ra.gate[t] = k ? INFINITY : -INFINITY;
+  if (ra.keep_out) ra.keep_out[t] = want ? (room ? 1 : 2) : 0;
+}
+
 template <int DR>
 __global__ __launch_bounds__(64 * kRouterWaves) void router_bf16_kernel(const uint16_t* __restrict__ x, int64_t n, int d,
                                                                          const uint16_t* __restrict__ w1,
                                                                          const uint16_t* __restrict__ b1,
                                                                          const uint16_t* __restrict__ w2, float b2,
-                                                                         float* __restrict__ scores) {
+                                                                         float* __restrict__ scores, RouteArgs ra) {
   __shared__ RouterPart<DR> part;
   const int64_t row0 = int64_t(blockIdx.x) * kRouterTokens;
   router_hidden_partials<DR>(x, n, d, w1, row0, part);
@@ -115,7 +125,10 @@ __global__ __launch_bounds__(64 * kRouterWaves) void router_bf16_kernel(const ui
   }
   v += __shfl_xor(v, 1);
   v += __shfl_xor(v, 2);
-  if (q == 0 && row0 + t < n) scores[row0 + t] = v + b2;
+  if (q == 0 && row0 + t < n) {
+    scores[row0 + t] = v + b2;
+    if (ra.thr) route_token(ra, row0 + t, v + b2);
+  }
 }
 
 // fp32 hidden pre-activation of unit j for one row, by one wavefront: lane
@@ -133,7 +146,7 @@ __device__ __forceinline__ float router_hidden_f32(const float* __restrict__ row
 __global__ __launch_bounds__(256) void router_f32_kernel(const float* __restrict__ x, int64_t n, int d, int dr,
                                                          const float* __restrict__ w1, const float* __restrict__ b1,
                                                          const float* __restrict__ w2, float b2,
-                                                         float* __restrict__ scores) {
+                                                         float* __restrict__ scores, RouteArgs ra) {
   const int lane = threadIdx.x & 63;
   const int64_t t = int64_t(blockIdx.x) * 4 + (threadIdx.x >> 6);
   if (t >= n) return;
@@ -143,16 +156,21 @@ __global__ __launch_bounds__(256) void router_f32_kernel(const float* __restrict
     const float h = router_hidden_f32(row, d, w1, b1, j, lane);
     score = fmaf(w2[j], h > 0.f ? h : 0.f, score);
   }
-  if (lane == 0) scores[t] = score + b2;
+  if (lane == 0) {
+    scores[t] = score + b2;
+    if (ra.thr) route_token(ra, t, score + b2);
+  }
 }
 
 hipError_t launch_router(int dtype, const void* x, int64_t n, int d, int d_r, const void* w1,
-                         const void* b1, const void* w2, float b2, float* scores, hipStream_t s) {
+                         const void* b1, const void* w2, float b2, float* scores, hipStream_t s,
+                         const RouteArgs* route) {
   if (n == 0) return hipSuccess;
   TimedScope ts(DSF_KIND_ROUTER, s);
+  const RouteArgs ra = route ? *route : RouteArgs{};
   if (dtype == DSF_F32) {
     router_f32_kernel<<<unsigned((n + 3) / 4), 256, 0, s>>>((const float*)x, n, d, d_r, (const float*)w1,
-                                                            (const float*)b1, (const float*)w2, b2, scores);
+                                                            (const float*)b1, (const float*)w2, b2, scores, ra);
     return hipGetLastError();
   }
   unsigned grid = unsigned((n + kRouterTokens - 1) / kRouterTokens);
@@ -161,10 +179,10 @@ hipError_t launch_router(int dtype, const void* x, int64_t n, int d, int d_r, co
   auto B1 = (const uint16_t*)b1;
   auto W2 = (const uint16_t*)w2;
   switch (d_r) {
-    case 16: router_bf16_kernel<16><<<grid, 64 * kRouterWaves, 0, s>>>(X, n, d, W1, B1, W2, b2, scores); break;
-    case 32: router_bf16_kernel<32><<<grid, 64 * kRouterWaves, 0, s>>>(X, n, d, W1, B1, W2, b2, scores); break;
-    case 48: router_bf16_kernel<48><<<grid, 64 * kRouterWaves, 0, s>>>(X, n, d, W1, B1, W2, b2, scores); break;
-    case 64: router_bf16_kernel<64><<<grid, 64 * kRouterWaves, 0, s>>>(X, n, d, W1, B1, W2, b2, scores); break;
+    case 16: router_bf16_kernel<16><<<grid, 64 * kRouterWaves, 0, s>>>(X, n, d, W1, B1, W2, b2, scores, ra); break;
+    case 32: router_bf16_kernel<32><<<grid, 64 * kRouterWaves, 0, s>>>(X, n, d, W1, B1, W2, b2, scores, ra); break;
+    case 48: router_bf16_kernel<48><<<grid, 64 * kRouterWaves, 0, s>>>(X, n, d, W1, B1, W2, b2, scores, ra); break;
+    case 64: router_bf16_kernel<64><<<grid, 64 * kRouterWaves, 0, s>>>(X, n, d, W1, B1, W2, b2, scores, ra); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

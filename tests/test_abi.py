@@ -205,6 +205,7 @@ def test_error_paths_of_the_kernel_calls():
     assert dws > 0 and dws % 256 == 0
     assert L.dsf_decode_workspace_size(ctypes.addressof(d), P.F32, 4, 0, 64) == 0         # max_pos
     assert L.dsf_decode_workspace_size(ctypes.addressof(d), P.F32, 4, 128, 0) == 0        # cap
+    assert L.dsf_decode_workspace_size(ctypes.addressof(d), P.F32, 4, 128, 65537) == 0    # cap above the limit
     assert L.dsf_decode_workspace_size(ctypes.addressof(_desc(head_dim=48)), P.F32, 4, 128, 64) == 0
     caches = (ctypes.c_void_p * 2)(FAKE, FAKE)
     bad = (ctypes.c_void_p * 2)(FAKE, FAKE + 8)
@@ -219,6 +220,7 @@ def test_error_paths_of_the_kernel_calls():
     assert ds(*dargs(pos=None)) == 1
     assert ds(*dargs(thr=None)) == 1
     assert ds(*dargs(cap=0)) == 1
+    assert ds(*dargs(cap=65537)) == 2
     assert ds(*dargs(x=FAKE + 4)) == 1
     assert ds(*dargs(dtype=7)) == 2
     assert ds(*dargs(B=0, x=None, pos=None, thr=None)) == 0                                # empty
