@@ -16,7 +16,11 @@ the oracle's header, where the CPU tests pin it. Here:
    score >= threshold) and the whole sequence then matches the oracle over
    the prefill's selections plus the decode decisions;
 3. a kept token meeting a full cache is skipped (reported as 2) and passes
-   through bitwise; repeated steps are deterministic.
+   through bitwise; repeated steps are deterministic;
+4. at the bench's decode shape (neox160m layer 0, 8 sequences, 2048-token
+   prompt): a forced-kept token matches the oracle's block over the prompt's
+   kept rows plus itself, and every routing decision, skipped row and cache
+   length holds.
 """
 import numpy as np
 import pytest
@@ -158,3 +162,54 @@ def test_full_cache_and_determinism(dev):
     c2.len.zero_()
     b = _decode(dev, w, dls, x[:, 0], 0, thr, c2, ws, 8)
     assert torch.equal(a, b) and torch.equal(a, outs[0])
+
+
+def test_neox160m_decode_full_size(dev):
+    """The bench's decode shape on layer 0 of the neox160m stack: prefill of
+    B = 8 sequences of 2048 tokens keeping k_0 = 1563, then one decode step at
+    position 2048. Sequence 0 is forced to keep its token: its output must
+    equal the oracle's block over the prompt's kept rows plus the new token,
+    at their positions (the new row last). The other sequences route by the
+    prefill's thresholds: each decision is score >= threshold, skipped rows
+    are bitwise unchanged, kept rows grow their cache by one."""
+    w = S.WORKLOADS["neox160m"].replace(n_layers=1)
+    B, T = w.batch, w.seq
+    k0 = 1563
+    W = S.layer_weights(w, 0)
+    dl = P.DeviceLayer(W, dev)
+    desc = make_desc(w)
+    x = S.hidden_states(w)
+    caches = Caches(w, B, T + 1, 1, dev)
+    thr = torch.empty(1, B, dtype=torch.float32, device=dev)
+    xp = x.to(dev).contiguous()
+    announce(f"full-size decode neox160m prefill k={k0}")
+    P.stack_prefill(desc, [dl.weights], [k0], xp, caches.k, caches.v, caches.len, workspace(w, B, T, k0, dev),
+                    thr_out=thr)
+    # the prefill's selection, by the single-layer entry point on the same input
+    idx = torch.empty(B, k0, dtype=torch.int32, device=dev)
+    xs = x.to(dev).contiguous()
+    P.sparse_block_forward(desc, dl.weights, xs, k0, workspace(w, B, T, k0, dev), idx_out=idx)
+    torch.cuda.synchronize()
+    assert torch.equal(xs, xp)
+    idx0 = idx[0].cpu().numpy()
+    g = torch.Generator().manual_seed(2048)
+    xn = (torch.randn(B, w.d_model, generator=g) * 0.02).to(w.torch_dtype)
+    thr_step = thr.clone()
+    thr_step[0, 0] = -float("inf")
+    ko = torch.empty(1, B, dtype=torch.int32, device=dev)
+    so = torch.empty(1, B, dtype=torch.float32, device=dev)
+    ws = torch.empty(P.decode_workspace_size(desc, dtype_code(w), B, T + 1, T + 1), dtype=torch.uint8, device=dev)
+    announce("full-size decode neox160m step")
+    y = _decode(dev, w, [dl], xn, T, thr_step, caches, ws, T + 1, keep_out=ko, scores_out=so)
+    kon, son, thn = ko.cpu().numpy()[0], so.cpu().numpy()[0], thr_step.cpu().numpy()[0]
+    np.testing.assert_array_equal(kon, (son >= thn).astype(np.int32))
+    assert kon[0] == 1
+    lens = caches.len.cpu().numpy()[0]
+    np.testing.assert_array_equal(lens, k0 + kon)
+    for b in range(B):
+        if not kon[b]:
+            assert torch.equal(y[b], xn[b])
+    rows = np.concatenate([O.f64(x[0])[idx0], O.f64(xn[0:1])])
+    pos = np.concatenate([idx0, [T]])
+    ref = O.f64(xn[0]) + O.block_delta(desc_dict(w), W, rows, pos)[-1]
+    assert rel_inf(to_np(y[0]) - O.f64(xn[0]), ref - O.f64(xn[0])) < TOL[w.dtype]
