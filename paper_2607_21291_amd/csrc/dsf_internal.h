@@ -146,6 +146,9 @@ struct GemmArgs {
   // set by the launcher: number of M tiles; workgroups per XCD of a persistent
   // grid (0: one tile per workgroup); 1 if its last round is split along K
   int ntm; int px; int split;
+  // set by the launcher for one-tile-per-workgroup grids: tiles are taken in
+  // bands of group_m tile rows, column by column (0: row-major)
+  int group_m;
 };
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t s);
 size_t gemm_partial_bytes();

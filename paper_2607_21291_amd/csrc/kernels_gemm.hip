@@ -23,6 +23,7 @@
 
 #include "dsf_device.h"
 #include "dsf_internal.h"
+#include "gemm_sched.h"
 
 namespace dsf {
 
@@ -750,16 +751,17 @@ struct DmaGemm {
   }
 };
 
-// One output tile per workgroup (grid = tiles), tiles in row-major (M-tile,
-// N-tile) order with one contiguous range per XCD: an XCD streams its own rows
-// of A once and keeps them in its L2.
+// One output tile per workgroup (grid = tiles). Each XCD takes one contiguous
+// range of the tile order (gemm_sched.h): row-major, or bands of g.group_m
+// tile rows walked column by column when the grid has more tiles than
+// resident workgroups.
 template <int EPI, int BM, int BN, int WM, int WN, int NS, int BK>
 __global__ __launch_bounds__((DmaCfg<BM, BN, WM, WN, NS, BK>::kThreads)) void gemm_bf16_dma_kernel(GemmArgs g) {
   using G = DmaGemm<EPI, BM, BN, WM, WN, NS, BK>;
   __shared__ __attribute__((aligned(1024))) char smem[G::C::kSmem];
   const int ntn = int(gridDim.x) / g.ntm;
-  const int item = xcd_remap(int(blockIdx.x), int(gridDim.x));
-  const int tm = item / ntn, tn = item - tm * ntn;
+  const GemmTile t = gemm_tile(xcd_remap(int(blockIdx.x), int(gridDim.x)), g.ntm, ntn, g.group_m);
+  const int tm = t.tm, tn = t.tn;
   typename G::Acc acc;
   G::mainloop(g, smem, tm, tn, 0, g.K / BK, acc);
   G::epilogue(g, smem, tm, tn, acc);
@@ -940,7 +942,8 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g) {
 // most kSkMaxSlots workgroups (2 per CU on a 256-CU device).
 constexpr int kSkMaxSlots = 512;
 constexpr int kSkMinIters = 8;  // mean k-iterations per workgroup below which one tile per workgroup is kept
-constexpr int kSkMinK = 32;     // k-iterations per tile below which the partial sums cost more than they save
+constexpr int kSkMinK = 32;
+constexpr int kGroupM = 4;      // tile rows per band of the grouped tile order     // k-iterations per tile below which the partial sums cost more than they save
 
 size_t gemm_partial_bytes() { return size_t(kSkMaxSlots) * DSF_GEMM_BM * DSF_GEMM_BN * sizeof(float); }
 int gemm_flag_count() { return kSkMaxSlots; }
@@ -1216,7 +1219,14 @@ static void launch_gemm_t(const GemmArgs& g, hipStream_t s) {
         return;
       }
     }
-    launch_timed(gemm_bf16_dma_kernel<EPI, BM, BN, WM, WN, NS, BK>, dim3(ntn * ga.ntm), dim3(Cfg::kThreads), s, ga);
+    // More tiles than resident workgroups: walk bands of kGroupM tile rows
+    // column by column, so that the workgroups resident on an XCD at one
+    // time cover a compact block of tiles (A rows and B rows both reused
+    // from its L2). A single round keeps row-major order.
+    auto fn = gemm_bf16_dma_kernel<EPI, BM, BN, WM, WN, NS, BK>;
+    const int slots = resident_slots<std::integral_constant<int, 16 + EPI>>((const void*)fn, Cfg::kThreads);
+    ga.group_m = ntn * ga.ntm > slots ? kGroupM : 0;
+    launch_timed(fn, dim3(ntn * ga.ntm), dim3(Cfg::kThreads), s, ga);
   } else if (g.dtype == DSF_BF16) {
     const int ntn = EPI == EPI_SWIGLU ? g.f / (kBN / 2) : (g.N + kBN - 1) / kBN;
     launch_timed(gemm_bf16_kernel<EPI>, dim3(ntn, (g.M + kBM - 1) / kBM), dim3(kThreads), s, g);
