@@ -467,7 +467,8 @@ Plan make_plan(const dsf_layer_desc& D, int dtype, int B, int T, int k_max, bool
   p.alignpart = with_align ? take(sizeof(double) * size_t(align_grid(int64_t(B) * T))) : 0;
   // stream-K partial tiles and their flags (bf16 GEMMs)
   p.skpart = dtype == DSF_BF16 ? take(gemm_partial_bytes()) : 0;
-  p.skflags = dtype == DSF_BF16 ? take(sizeof(uint32_t) * gemm_flag_count()) : 0;
+  // followed by the per-sequence counters of the router + Top-K launch
+  p.skflags = dtype == DSF_BF16 ? take(sizeof(uint32_t) * (size_t(gemm_flag_count()) + size_t(B))) : 0;
   p.total = off;
   return p;
 }
@@ -564,13 +565,24 @@ struct Ctx {
 };
 
 uint32_t* at_flags(const Ctx& c) { return reinterpret_cast<uint32_t*>(c.ws + c.plan.skflags); }
+// per-sequence counters of the router + Top-K launch (bf16), after the flags
+uint32_t* at_route_count(const Ctx& c) { return at_flags(c) + gemm_flag_count(); }
 
-// Zero the stream-K flags at the start of a call; GEMM launches then take
-// epochs 1, 2, ... (the flags of a finished launch never equal a later epoch).
+// Zero the stream-K flags and the router counters at the start of a call
+// (one launch); GEMM launches then take epochs 1, 2, ... (the flags of a
+// finished launch never equal a later epoch), and each router + Top-K launch
+// leaves its counters zero again.
 int reset_stream_k(const Ctx& c) {
   c.epoch = 0;
-  if (c.dtype == DSF_BF16) DSF_HIP(launch_zero_u32(at_flags(c), gemm_flag_count(), c.s));
+  if (c.dtype == DSF_BF16) DSF_HIP(launch_zero_u32(at_flags(c), int64_t(gemm_flag_count()) + c.B, c.s));
   return DSF_OK;
+}
+
+// DSF_UNFUSED_ROUTING=1 (read at every call) runs the router and the Top-K as
+// two launches.
+bool fused_routing() {
+  const char* e = getenv("DSF_UNFUSED_ROUTING");
+  return !(e && e[0] == '1');
 }
 
 // The stream-K fields of a GEMM launch on this call's workspace.
@@ -595,7 +607,14 @@ int run_layer(const Ctx& c, const dsf_layer_weights* W, void* x, int k, bool den
   const bool qwen = D.block == DSF_BLOCK_QWEN_SEQ;
   const int32_t* idx = nullptr;
   float* scores = nullptr;
-  if (!dense) {
+  if (!dense && !idx_in && router_topk_fusable(c.dtype, T, D.d_router) && fused_routing()) {
+    // router and Top-K in one launch (its last workgroup of each sequence selects)
+    scores = scores_out ? scores_out : at<float>(c, c.plan.scores);
+    int32_t* dst = idx_out ? idx_out : at<int32_t>(c, c.plan.idx);
+    DSF_HIP(launch_router_topk(x, B, T, d, D.d_router, W->router_w1, W->router_b1, W->router_w2, W->router_b2,
+                               scores, k, dst, at_route_count(c), c.s));
+    idx = dst;
+  } else if (!dense) {
     scores = scores_out ? scores_out : at<float>(c, c.plan.scores);
     DSF_HIP(launch_router(c.dtype, x, int64_t(B) * T, d, D.d_router, W->router_w1, W->router_b1, W->router_w2,
                           W->router_b2, scores, c.s));

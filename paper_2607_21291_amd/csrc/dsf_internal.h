@@ -42,6 +42,13 @@ struct RouteArgs {
 hipError_t launch_router(int dtype, const void* x, int64_t n, int d, int d_r, const void* w1,
                          const void* b1, const void* w2, float b2, float* scores, hipStream_t s,
                          const RouteArgs* route = nullptr);
+// Router scores of B sequences of T tokens and each sequence's Top-K in one
+// launch (bf16; router_topk_fusable). count: B words, zero before the launch
+// and left zero.
+bool router_topk_fusable(int dtype, int T, int d_r);
+hipError_t launch_router_topk(const void* x, int B, int T, int d, int d_r, const void* w1, const void* b1,
+                              const void* w2, float b2, float* scores, int k, int32_t* idx, uint32_t* count,
+                              hipStream_t s);
 // dscore[B, T] = 0, then at kept positions (1 - sigmoid(s)) <dy, x_out - x_in>
 hipError_t launch_gate_grad(int dtype, const void* dy, const void* x_in, const void* x_out, const float* scores,
                             const int32_t* idx, int B, int T, int k, int d, float* dscore, hipStream_t s);

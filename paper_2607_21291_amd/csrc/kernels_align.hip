@@ -190,8 +190,19 @@ __global__ __launch_bounds__(256) void align_hidden_group_kernel(const T* __rest
 __global__ __launch_bounds__(256) void sum_finish_kernel(const double* __restrict__ partial, int64_t np,
                                                          double* __restrict__ accum) {
   __shared__ double red[256];
+  // eight loads in flight per thread, then added in index order (the order
+  // depends only on np)
   double v = 0.0;
-  for (int64_t i = threadIdx.x; i < np; i += 256) v += partial[i];
+  for (int64_t base = 0; base < np; base += 8 * 256) {
+    double t[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int64_t i = base + 256 * j + threadIdx.x;
+      t[j] = i < np ? partial[i] : 0.0;
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v += t[j];
+  }
   red[threadIdx.x] = v;
   __syncthreads();
   for (int o = 128; o > 0; o >>= 1) {

@@ -7,6 +7,7 @@
 // fixed-order reductions (no floating-point atomics).
 #include "dsf_device.h"
 #include "dsf_internal.h"
+#include "topk_block.h"
 
 namespace dsf {
 
@@ -105,8 +106,19 @@ __global__ __launch_bounds__(256) void sim_partial_kernel(const T* a, const T* c
 __global__ __launch_bounds__(256) void sim_finish_kernel(const double* partial, int np, int64_t n,
                                                          double* accum) {
   __shared__ double red[256];
+  // eight loads in flight per thread, then added in index order (the order
+  // depends only on np)
   double v = 0.0;
-  for (int i = threadIdx.x; i < np; i += 256) v += partial[i];
+  for (int base = 0; base < np; base += 8 * 256) {
+    double t[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int i = base + 256 * j + int(threadIdx.x);
+      t[j] = i < np ? partial[i] : 0.0;
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v += t[j];
+  }
   red[threadIdx.x] = v;
   __syncthreads();
   for (int o = 128; o > 0; o >>= 1) {
@@ -161,8 +173,12 @@ __global__ __launch_bounds__(256) void sim_wide_kernel(const T* a, const T* c, i
 }
 
 template <typename T, int L, bool EXACT>
-static void launch_sim_l(const T* a, const T* c, int64_t n, int d, float* per_tok, double* partial, int g,
+static void launch_sim_l(const T* a, const T* c, int64_t n, int d, float* per_tok, double* partial, int& g,
                          int chunks, hipStream_t s) {
+  // one row group per wavefront: 4 * (64 / L) rows per block (at most the
+  // sim_grid blocks the workspace holds partials for)
+  const int64_t need = (n + 4 * (64 / L) - 1) / (4 * (64 / L));
+  if (need < g) g = int(need);
   switch (chunks) {
     case 1: sim_partial_kernel<T, L, 1, EXACT><<<g, 256, 0, s>>>(a, c, n, d, per_tok, partial); break;
     case 2: sim_partial_kernel<T, L, 2, EXACT><<<g, 256, 0, s>>>(a, c, n, d, per_tok, partial); break;
@@ -179,7 +195,7 @@ static void launch_sim_l(const T* a, const T* c, int64_t n, int d, float* per_to
 // the row evenly into at most 8 vectors per lane; otherwise 64 lanes looping
 // over groups of 8 vectors.
 template <typename T>
-static void launch_sim_t(const T* a, const T* c, int64_t n, int d, float* per_tok, double* partial, int g,
+static void launch_sim_t(const T* a, const T* c, int64_t n, int d, float* per_tok, double* partial, int& g,
                          hipStream_t s) {
   const int nvec = d / Elem<T>::kVec;
   if (nvec % 64 == 0 && nvec / 64 <= 8) launch_sim_l<T, 64, true>(a, c, n, d, per_tok, partial, g, nvec / 64, s);
@@ -203,123 +219,15 @@ hipError_t launch_sim_stats(int dtype, const void* a, const void* c, int64_t n, 
 
 // -------------------------------------------------------- Top-K, Section 3.4
 
-// Order-preserving key: larger score -> larger key; -0 == +0; NaN -> 0 (lowest).
-__device__ __forceinline__ uint32_t score_key(float f) {
-  if (f != f) return 0u;
-  uint32_t u = __float_as_uint(f);
-  if (u == 0x80000000u) u = 0u;
-  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-}
-
 constexpr int kTopkThreads = 1024;
-constexpr int kTopkWaves = kTopkThreads / 64;
 
-// Exclusive count of `flag` over the block in thread order; `total` gets the
-// block's count. Uses wave ballots and one LDS slot per wave.
-__device__ __forceinline__ uint32_t block_excl_count(bool flag, uint32_t* wave_tot, uint32_t& total) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  uint64_t m = __ballot(flag);
-  uint32_t within = __popcll(m & ((uint64_t(1) << lane) - 1));
-  if (lane == 0) wave_tot[w] = __popcll(m);
-  __syncthreads();
-  uint32_t before = 0, tot = 0;
-#pragma unroll
-  for (int i = 0; i < kTopkWaves; ++i) {
-    uint32_t c = wave_tot[i];
-    before += (i < w) ? c : 0u;
-    tot += c;
-  }
-  __syncthreads();
-  total = tot;
-  return before + within;
-}
-
-// One block per sequence. The order-preserving keys of the sequence are kept
-// in LDS (read from global memory once). Radix select (8 bits per pass, most
-// significant first) finds the key of the k-th largest score and how many of
-// the keys equal to it are kept; each wavefront counts into its own histogram
-// so that equal digits (frequent in the top byte) do not serialise on one LDS
-// address. A final ordered pass keeps every larger key and the
-// lowest-positioned equal keys, writing positions in ascending order.
-constexpr int kTopkLdsKeys = 16384;  // sequences up to this length keep their keys in LDS
-
+// One block per sequence (topk_block.h).
 template <bool KEYS_IN_LDS>
 __global__ __launch_bounds__(kTopkThreads) void topk_kernel(const float* __restrict__ scores, int T, int k,
                                                             int32_t* __restrict__ idx) {
+  __shared__ TopkShared<kTopkThreads, KEYS_IN_LDS> sh;
   const float* sc = scores + int64_t(blockIdx.x) * T;
-  int32_t* out = idx + int64_t(blockIdx.x) * k;
-  __shared__ uint32_t keys[KEYS_IN_LDS ? kTopkLdsKeys : 1];
-  __shared__ uint32_t whist[kTopkWaves][256];
-  __shared__ uint32_t hist[256];
-  __shared__ uint32_t wave_tot[kTopkWaves];
-  __shared__ uint32_t sh_digit, sh_remaining;
-  const int tid = threadIdx.x, wave = tid >> 6;
-  auto key_at = [&](int t) -> uint32_t { return KEYS_IN_LDS ? keys[t] : score_key(sc[t]); };
-
-  if constexpr (KEYS_IN_LDS) {
-    for (int t = tid; t < T; t += kTopkThreads) keys[t] = score_key(sc[t]);
-  }
-  uint32_t prefix = 0, mask = 0, remaining = uint32_t(k);
-  for (int pass = 0; pass < 4; ++pass) {
-    const int shift = 24 - 8 * pass;
-    for (int i = tid; i < kTopkWaves * 256; i += kTopkThreads) (&whist[0][0])[i] = 0;
-    __syncthreads();
-    for (int t = tid; t < T; t += kTopkThreads) {
-      const uint32_t key = key_at(t);
-      if ((key & mask) == prefix) atomicAdd(&whist[wave][(key >> shift) & 255u], 1u);
-    }
-    __syncthreads();
-    if (tid < 256) {
-      uint32_t c = 0;
-#pragma unroll
-      for (int w = 0; w < kTopkWaves; ++w) c += whist[w][tid];
-      hist[tid] = c;
-    }
-    __syncthreads();
-    if (tid < 64) {
-      // lane L owns digits 255-4L .. 252-4L (descending); exclusive scan over lanes
-      uint32_t c[4], tot = 0;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        c[e] = hist[255 - 4 * tid - e];
-        tot += c[e];
-      }
-      uint32_t incl = tot;
-#pragma unroll
-      for (int o = 1; o < 64; o <<= 1) {
-        uint32_t v = __shfl_up(incl, o, 64);
-        if (tid >= o) incl += v;
-      }
-      uint32_t cum = incl - tot;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        if (cum < remaining && remaining <= cum + c[e]) {
-          sh_digit = uint32_t(255 - 4 * tid - e);
-          sh_remaining = remaining - cum;
-        }
-        cum += c[e];
-      }
-    }
-    __syncthreads();
-    prefix |= sh_digit << shift;
-    mask |= 255u << shift;
-    remaining = sh_remaining;
-  }
-  // prefix is now the k-th largest key; `remaining` equal keys are kept.
-  uint32_t run_eq = 0, run_sel = 0;
-  for (int base = 0; base < T; base += kTopkThreads) {
-    const int t = base + tid;
-    const bool valid = t < T;
-    const uint32_t key = valid ? key_at(t) : 0u;
-    const bool eq = valid && key == prefix;
-    uint32_t tot_eq, tot_sel;
-    const uint32_t eq_before = run_eq + block_excl_count(eq, wave_tot, tot_eq);
-    const bool sel = valid && (key > prefix || (eq && eq_before < remaining));
-    const uint32_t sel_before = run_sel + block_excl_count(sel, wave_tot, tot_sel);
-    if (sel && sel_before < uint32_t(k)) out[sel_before] = t;
-    run_eq += tot_eq;
-    run_sel += tot_sel;
-  }
+  topk_block<kTopkThreads, KEYS_IN_LDS>([&](int t) { return sc[t]; }, T, k, idx + int64_t(blockIdx.x) * k, sh);
 }
 
 hipError_t launch_topk(const float* scores, int B, int T, int k, int32_t* idx, hipStream_t s) {

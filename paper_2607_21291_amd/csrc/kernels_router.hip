@@ -9,6 +9,7 @@
 // floating-point atomics.
 #include "dsf_device.h"
 #include "dsf_internal.h"
+#include "topk_block.h"
 
 namespace dsf {
 
@@ -184,6 +185,89 @@ hipError_t launch_router(int dtype, const void* x, int64_t n, int d, int d_r, co
     case 48: router_bf16_kernel<48><<<grid, 64 * kRouterWaves, 0, s>>>(X, n, d, W1, B1, W2, b2, scores, ra); break;
     case 64: router_bf16_kernel<64><<<grid, 64 * kRouterWaves, 0, s>>>(X, n, d, W1, B1, W2, b2, scores, ra); break;
     default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+// Router and per-sequence Top-K in one launch. The workgroups score their 64
+// tokens as router_bf16_kernel does (same partials, same order: the scores
+// are bitwise those of the router alone), store them with device-coherent
+// stores and count themselves on their sequence's counter; the last of a
+// sequence's T / 64 workgroups to arrive resets the counter and runs the
+// Top-K of that sequence (topk_block.h, the same selection as the Top-K
+// kernel) on scores read back with device-coherent loads, in the LDS the
+// router partials used. No workgroup waits for another. Requires
+// T % kRouterTokens == 0 and T <= kTopkLdsKeys; count[B] is zero before the
+// launch and is left zero.
+constexpr int kRouterThreads = 64 * kRouterWaves;
+
+template <int DR>
+__global__ __launch_bounds__(kRouterThreads) void router_topk_bf16_kernel(
+    const uint16_t* __restrict__ x, int64_t n, int d, const uint16_t* __restrict__ w1,
+    const uint16_t* __restrict__ b1, const uint16_t* __restrict__ w2, float b2, float* __restrict__ scores, int T,
+    int k, int32_t* __restrict__ idx, uint32_t* __restrict__ count) {
+  union Shared {
+    RouterPart<DR> part;
+    TopkShared<kRouterThreads, true> topk;
+  };
+  __shared__ Shared sh;
+  __shared__ int is_last;
+  const int64_t row0 = int64_t(blockIdx.x) * kRouterTokens;
+  router_hidden_partials<DR>(x, n, d, w1, row0, sh.part);
+  __syncthreads();
+  if (threadIdx.x < 4 * kRouterTokens) {
+    const int t = threadIdx.x >> 2, q = threadIdx.x & 3;
+    float v = 0.f;
+#pragma unroll
+    for (int jj = 0; jj < DR / 4; ++jj) {
+      const int j = q * (DR / 4) + jj;
+      const float h = router_hidden<DR>(sh.part, b1, t, j);
+      v = fmaf(bf2f(w2[j]), h > 0.f ? h : 0.f, v);
+    }
+    v += __shfl_xor(v, 1);
+    v += __shfl_xor(v, 2);
+    if (q == 0 && row0 + t < n) __hip_atomic_store(scores + row0 + t, v + b2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  // the device-coherent stores complete before the counter moves; every wave
+  // is done with the partials before the LDS is reused
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  const int b = int(row0 / T);
+  if (threadIdx.x == 0) {
+    const uint32_t old = __hip_atomic_fetch_add(count + b, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    is_last = old == uint32_t(T / kRouterTokens - 1);
+    if (is_last) __hip_atomic_store(count + b, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  __syncthreads();
+  if (!is_last) return;
+  const float* sc = scores + int64_t(b) * T;
+  topk_block<kRouterThreads, true>(
+      [&](int t) { return __hip_atomic_load(sc + t, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }, T, k,
+      idx + int64_t(b) * k, sh.topk);
+}
+
+bool router_topk_fusable(int dtype, int T, int d_r) {
+  return dtype == DSF_BF16 && T % kRouterTokens == 0 && T <= kTopkLdsKeys &&
+         (d_r == 16 || d_r == 32 || d_r == 48 || d_r == 64);
+}
+
+hipError_t launch_router_topk(const void* x, int B, int T, int d, int d_r, const void* w1, const void* b1,
+                              const void* w2, float b2, float* scores, int k, int32_t* idx, uint32_t* count,
+                              hipStream_t s) {
+  if (B == 0 || T == 0) return hipSuccess;
+  if (!router_topk_fusable(DSF_BF16, T, d_r) || k < 1 || k > T) return hipErrorInvalidValue;
+  TimedScope ts(DSF_KIND_ROUTER, s);
+  const int64_t n = int64_t(B) * T;
+  const unsigned grid = unsigned(n / kRouterTokens);
+  auto X = (const uint16_t*)x;
+  auto W1 = (const uint16_t*)w1;
+  auto B1 = (const uint16_t*)b1;
+  auto W2 = (const uint16_t*)w2;
+  switch (d_r) {
+    case 16: router_topk_bf16_kernel<16><<<grid, kRouterThreads, 0, s>>>(X, n, d, W1, B1, W2, b2, scores, T, k, idx, count); break;
+    case 32: router_topk_bf16_kernel<32><<<grid, kRouterThreads, 0, s>>>(X, n, d, W1, B1, W2, b2, scores, T, k, idx, count); break;
+    case 48: router_topk_bf16_kernel<48><<<grid, kRouterThreads, 0, s>>>(X, n, d, W1, B1, W2, b2, scores, T, k, idx, count); break;
+    default: router_topk_bf16_kernel<64><<<grid, kRouterThreads, 0, s>>>(X, n, d, W1, B1, W2, b2, scores, T, k, idx, count); break;
   }
   return hipGetLastError();
 }
