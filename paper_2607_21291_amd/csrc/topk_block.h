@@ -74,7 +74,15 @@ __device__ void topk_block(Score score, int T, int k, int32_t* __restrict__ out,
 
   for (int i = tid; i < 2 * NW * 256; i += NT) (&sh.whist[0][0][0])[i] = 0;
   if constexpr (KEYS_IN_LDS) {
-    for (int t = tid; t < T; t += NT) sh.keys[t] = score_key(score(t));
+    // eight scores per thread in flight before the first is used
+    for (int t0 = tid; t0 < T; t0 += 8 * NT) {
+      float v[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) v[j] = t0 + j * NT < T ? score(t0 + j * NT) : 0.f;
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        if (t0 + j * NT < T) sh.keys[t0 + j * NT] = score_key(v[j]);
+    }
   }
   __syncthreads();
   uint32_t prefix = 0, mask = 0, remaining = uint32_t(k);
