@@ -282,7 +282,7 @@ def decode_leg(P, C, w, ks, dev, desc, weights, x0, steps):
     dcode = P.F32 if w.dtype == "f32" else P.BF16
     warm = 3
     n = warm + steps
-    cap = T + n
+    cap = T + n + steps + 1  # eager steps, then as many replays of a captured step
     ck = [torch.empty(B, w.n_kv_heads, cap, w.head_dim, dtype=w.torch_dtype, device=dev) for _ in range(L)]
     cv = [torch.empty(B, w.n_kv_heads, cap, w.head_dim, dtype=w.torch_dtype, device=dev) for _ in range(L)]
     clen = torch.zeros(L, B, dtype=torch.int32, device=dev)
@@ -317,9 +317,27 @@ def decode_leg(P, C, w, ks, dev, desc, weights, x0, steps):
     nbytes = C.decode_step_bytes(w, B, mean_lens)
     gbs = nbytes / (ms * 1e-3) / 1e9
     kept = keep[warm:].float().mean().item()
+    # the same step captured into a HIP graph and replayed, the next token
+    # and its position copied into the captured buffers before each replay
+    xg, posg, keepg = toks[0].clone(), pos[0].clone(), torch.zeros(L, B, dtype=torch.int32, device=dev)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        P.decode_step(desc, weights, xg, posg, cap, thr, ck, cv, clen, ws, keep_out=keepg)
+    torch.cuda.synchronize()
+    e0.record()
+    for i in range(steps):
+        xg.copy_(toks[i % n])
+        posg.fill_(T + n + i)
+        graph.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    ms_graph = e0.elapsed_time(e1) / steps
+    del graph
     del ck, cv, toks, ws
     torch.cuda.empty_cache()
     return {"tokens_per_s": B / (ms / 1e3), "ms_per_step": ms, "batch": B, "prefill_tokens": T,
+            "graph": {"ms_per_step": ms_graph, "tokens_per_s": B / (ms_graph / 1e3),
+                      "note": "one captured decode step replayed; each replay preceded by two small copies"},
             "prefill_ms": prefill_ms, "steps": steps, "cache_capacity": cap,
             "cache_len_after_prefill_mean": float(lens0.mean()), "kept_fraction_decode": kept,
             "roofline": {"bound": "hbm", "bytes_per_step": nbytes, "achieved": gbs, "peak": PEAK_HBM_GBS,
