@@ -254,9 +254,16 @@ int dsf_attention_forward(const void* q, const void* k, const void* v, int dtype
  * (k_max = T for DSF_FLAG_DENSE). with_similarity != 0 adds room to keep each
  * layer's input for the similarity statistic. For DSF_BF16 it includes a
  * fixed 32 MiB (+ 2 KiB) for the partial sums and flags of the stream-K
- * projection schedule. The contents need no initialisation; each call
+ * projection schedule, followed by 4 B bytes of per-sequence counters of the
+ * routing launch (below). The contents need no initialisation; each call
  * resets what it uses, so two calls that overlap in time (on different
  * streams) need two workspaces. Returns 0 on a bad argument.
+ *
+ * Routing launch. With DSF_BF16, T a multiple of 64 (at most 16384) and no
+ * idx_in, the router and the per-sequence Top-K run as one launch: the last
+ * of a sequence's router workgroups to finish selects its Top-K. Scores and
+ * indices are bitwise those of the two separate kernels; the environment
+ * variable DSF_UNFUSED_ROUTING=1, read at every call, runs those instead.
  *
  * Projection schedule. Each bf16 projection GEMM runs one output tile per
  * workgroup; or, with more tiles than resident workgroups, a persistent grid
