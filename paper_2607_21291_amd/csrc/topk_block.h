@@ -23,7 +23,7 @@ struct TopkShared {
   uint32_t keys[KEYS_IN_LDS ? kTopkLdsKeys : 1];
   uint32_t whist[2][NW][256];  // per-wave digit histograms, two buffers used by alternate passes
   uint32_t wave_tot[NW];
-  uint32_t digit, remaining;
+  uint32_t digit, remaining, whole;
 };
 
 // Exclusive prefix sum of v over the block in thread order; `total` gets the
@@ -117,6 +117,7 @@ __device__ void topk_block(Score score, int T, int k, int32_t* __restrict__ out,
         if (cum < remaining && remaining <= cum + c[e]) {
           sh.digit = uint32_t(255 - 4 * lane - e);
           sh.remaining = remaining - cum;
+          sh.whole = remaining == cum + c[e];  // every key of the digit's bucket is kept
         }
         cum += c[e];
       }
@@ -128,14 +129,16 @@ __device__ void topk_block(Score score, int T, int k, int32_t* __restrict__ out,
     prefix |= sh.digit << shift;
     mask |= 255u << shift;
     remaining = sh.remaining;
+    if (sh.whole) break;  // the bucket holding the k-th key is kept whole: no more digits needed
   }
-  // prefix is now the k-th largest key; `remaining` equal keys are kept, the
-  // lowest-positioned ones. Thread tid owns positions [t0, t1).
+  // The keys' top bits under mask select: those above prefix are kept, and of
+  // those equal to it (after four passes: the k-th largest key itself) the
+  // `remaining` lowest-positioned ones. Thread tid owns positions [t0, t1).
   const int run = (T + NT - 1) / NT;
   const int t0 = min(T, tid * run), t1 = min(T, t0 + run);
   uint32_t n_gt = 0, n_eq = 0;
   for (int t = t0; t < t1; ++t) {
-    const uint32_t key = key_at(t);
+    const uint32_t key = key_at(t) & mask;
     n_gt += key > prefix;
     n_eq += key == prefix;
   }
@@ -145,7 +148,7 @@ __device__ void topk_block(Score score, int T, int k, int32_t* __restrict__ out,
   const uint32_t sel_before = block_excl_sum<NW>(n_gt + eq_kept, sh.wave_tot, tot);
   uint32_t o = sel_before, eq_seen = 0;
   for (int t = t0; t < t1; ++t) {
-    const uint32_t key = key_at(t);
+    const uint32_t key = key_at(t) & mask;
     const bool eq = key == prefix;
     const bool sel = key > prefix || (eq && eq_seen < eq_kept);
     eq_seen += eq;
