@@ -768,8 +768,9 @@ __global__ __launch_bounds__((DmaCfg<BM, BN, WM, WN, NS, BK>::kThreads)) void ge
 }
 
 // Persistent grid of 8 * px workgroups (workgroup w runs on XCD w % 8 as the
-// hardware deals workgroups to the 8 XCDs in turn). The tiles, in row-major
-// order, are cut into 8 contiguous ranges, one per XCD, and each XCD's px
+// hardware deals workgroups to the 8 XCDs in turn). The tiles, in the order
+// of gemm_sched.h (bands of g.group_m tile rows), are cut into 8 contiguous
+// ranges, one per XCD, and each XCD's px
 // workgroups share its range as an independent problem. With g.split == 0
 // they take whole tiles only (tile j, j + px, ...): a workgroup moves on to
 // its next tile while its last tile's stores drain. With g.split == 1
@@ -799,7 +800,8 @@ __global__ __launch_bounds__((DmaCfg<BM, BN, WM, WN, NS, BK>::kThreads)) void ge
   const int dp = (!g.split || rem == 0) ? ntx : (full >= 1 ? (full - 1) * px : 0);
   typename G::Acc acc;
   for (int t = j; t < dp; t += px) {
-    const int tile = t0 + t, tm = tile / ntn, tn = tile - tm * ntn;
+    const GemmTile tt = gemm_tile(t0 + t, g.ntm, ntn, g.group_m);
+    const int tm = tt.tm, tn = tt.tn;
     G::mainloop(g, smem, tm, tn, 0, nk, acc);
     G::epilogue(g, smem, tm, tn, acc);
   }
@@ -811,7 +813,8 @@ __global__ __launch_bounds__((DmaCfg<BM, BN, WM, WN, NS, BK>::kThreads)) void ge
     const int st = int((u - 1) / nk);
     const int64_t tb = int64_t(st) * nk;
     const int kb = int((a > tb ? a : tb) - tb), ke = int(u - tb);
-    const int tile = t0 + dp + st, tm = tile / ntn, tn = tile - tm * ntn;
+    const GemmTile tt = gemm_tile(t0 + dp + st, g.ntm, ntn, g.group_m);
+    const int tm = tt.tm, tn = tt.tn;
     G::mainloop(g, smem, tm, tn, kb, ke, acc);
     if (ke < nk) {
       // top of the piece, short of the tile's end: publish the partial sum
@@ -1214,6 +1217,8 @@ static void launch_gemm_t(const GemmArgs& g, hipStream_t s) {
                                            resident_slots<std::integral_constant<int, EPI>>((const void*)fn, Cfg::kThreads));
       ga.px = sch.px;
       ga.split = sch.split;
+      // tile order as for one tile per workgroup (the grid has more tiles than slots)
+      ga.group_m = kGroupM;
       if (ga.px > 0) {
         launch_timed(fn, dim3(ga.px * kXcds), dim3(Cfg::kThreads), s, ga);
         return;
