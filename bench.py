@@ -40,8 +40,8 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 # library's plain copy kernel of known size. It holds only for the workload
 # and the GEMM source it was measured on (SHA-256 of kernels_gemm.hip); for
 # anything else `traffic` is null.
-TRAFFIC_MEASURED = {"workload": "neox160m", "bytes_per_launch": 2.093e+08,
-                    "gemm_source_sha256": "3c3310de9e853ccd09dcbc1543ca190fdd812aa1d3d05986d56edbebde447cb2",
+TRAFFIC_MEASURED = {"workload": "neox160m", "bytes_per_launch": 2.081e+08,
+                    "gemm_source_sha256": "4cfa901f97fd6118d3472e7a082a1b59925dfe53fabfeb111c792a6825a9b490",
                     "profile": "profiles/gemm_down_neox160m.md"}
 
 

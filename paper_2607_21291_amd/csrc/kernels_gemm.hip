@@ -946,7 +946,8 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g) {
 constexpr int kSkMaxSlots = 512;
 constexpr int kSkMinIters = 8;  // mean k-iterations per workgroup below which one tile per workgroup is kept
 constexpr int kSkMinK = 32;
-constexpr int kGroupM = 4;      // tile rows per band of the grouped tile order     // k-iterations per tile below which the partial sums cost more than they save
+constexpr int kGroupM = 4;      // tile rows per band of the grouped tile order
+constexpr int kGroupMinCols = 8;  // below this many tile columns row-major order is already compact     // k-iterations per tile below which the partial sums cost more than they save
 
 size_t gemm_partial_bytes() { return size_t(kSkMaxSlots) * DSF_GEMM_BM * DSF_GEMM_BN * sizeof(float); }
 int gemm_flag_count() { return kSkMaxSlots; }
@@ -1218,7 +1219,7 @@ static void launch_gemm_t(const GemmArgs& g, hipStream_t s) {
       ga.px = sch.px;
       ga.split = sch.split;
       // tile order as for one tile per workgroup (the grid has more tiles than slots)
-      ga.group_m = kGroupM;
+      ga.group_m = ntn >= kGroupMinCols ? kGroupM : 0;
       if (ga.px > 0) {
         launch_timed(fn, dim3(ga.px * kXcds), dim3(Cfg::kThreads), s, ga);
         return;
@@ -1227,10 +1228,13 @@ static void launch_gemm_t(const GemmArgs& g, hipStream_t s) {
     // More tiles than resident workgroups: walk bands of kGroupM tile rows
     // column by column, so that the workgroups resident on an XCD at one
     // time cover a compact block of tiles (A rows and B rows both reused
-    // from its L2). A single round keeps row-major order.
+    // from its L2). A single round, or a grid fewer than kGroupMinCols tiles
+    // wide (an XCD's row-major range is then already a compact block; banding
+    // it measured more L2 misses on the 768-wide down projection), keeps
+    // row-major order.
     auto fn = gemm_bf16_dma_kernel<EPI, BM, BN, WM, WN, NS, BK>;
     const int slots = resident_slots<std::integral_constant<int, 16 + EPI>>((const void*)fn, Cfg::kThreads);
-    ga.group_m = ntn * ga.ntm > slots ? kGroupM : 0;
+    ga.group_m = ntn * ga.ntm > slots && ntn >= kGroupMinCols ? kGroupM : 0;
     launch_timed(fn, dim3(ntn * ga.ntm), dim3(Cfg::kThreads), s, ga);
   } else if (g.dtype == DSF_BF16) {
     const int ntn = EPI == EPI_SWIGLU ? g.f / (kBN / 2) : (g.N + kBN - 1) / kBN;
