@@ -272,9 +272,30 @@ int dsf_attention_forward(const void* q, const void* k, const void* v, int dtype
  * the k-iterations of the last tiles and add their partial sums in a fixed
  * order, which rounds differently). All are deterministic. The environment
  * variable DSF_GEMM_SCHEDULE=classic, =persistent or =streamk, read at every
- * launch, forces one of them (testing and tuning). */
+ * launch, forces one of them (testing and tuning).
+ *
+ * Call status. The first 4 bytes of the workspace hold a status word that
+ * each call of dsf_sparse_block_forward, dsf_stack_forward,
+ * dsf_stack_prefill and dsf_align_stack_forward clears at its start and that
+ * its kernels OR bits into; read it with dsf_workspace_status once the call's
+ * work is enqueued. DSF_WS_STATUS_SK_TIMEOUT: a stream-K workgroup that must
+ * add an earlier workgroup's partial sum waits for it with a bounded spin of
+ * 2^22 polls of its flag (the partial is normally ready within microseconds,
+ * because the hardware dispatches workgroups in order); if the wait gives
+ * up, the tile is written without that partial, so the call's output is
+ * wrong, and this bit is set. The environment variable DSF_SK_SPIN_LIMIT
+ * (polls per wait, read at every launch) exists for testing this report. */
 size_t dsf_workspace_size(const dsf_layer_desc* desc, int dtype, int B, int T, int k_max,
                           int with_similarity);
+
+enum { DSF_WS_STATUS_SK_TIMEOUT = 1 };
+
+/* Status word of the last layer/stack call that used this workspace (see
+ * above). Enqueues a 4-byte device-to-host copy on stream and waits for the
+ * stream, so every call enqueued before it has finished. *status receives the
+ * word (0: no failure). Returns DSF_EINVAL for a null pointer, DSF_EHIP if the
+ * copy or the wait fails. */
+int dsf_workspace_status(const void* workspace, uint32_t* status, hipStream_t stream);
 
 /* Section 3.4: one sparse layer, in place on x [B, T, d].
  *   1. scores = router(x) for every token (skipped with DSF_FLAG_DENSE);

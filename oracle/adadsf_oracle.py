@@ -369,9 +369,9 @@ def routed_layer(desc: Dict, W: Dict, x, k: int, idx=None,
 
     idx given: teacher-forced selection (the router still scores every token).
     out_dtype given: the kept rows of y are rounded to that storage format.
-    gate: the block's update of a kept token is scaled by sigmoid(score), the
-    router-score pathway kept differentiable in training (Section 3.4,
-    MoD-style); `delta` is then the ungated update.
+    gate: sigmoid(score) scales each kept token's update, so the loss reaches
+    the router scores through a gradient (Section 3.4, read MoD-style);
+    `delta` is then the ungated update.
     """
     x = f64(x)
     B, T, _ = x.shape

@@ -35,7 +35,9 @@ EXPORTS = [
     "dsf_gate_score_grad", "dsf_router_backward_workspace_size", "dsf_router_backward",
     "dsf_align_workspace_size", "dsf_align_hidden", "dsf_kl_align", "dsf_align_stack_workspace_size",
     "dsf_align_stack_forward", "dsf_decode_workspace_size", "dsf_decode_step", "dsf_stack_prefill",
+    "dsf_workspace_status",
 ]
+WS_STATUS_SK_TIMEOUT = 1
 
 
 class DsfError(RuntimeError):
@@ -88,6 +90,7 @@ def lib() -> ctypes.CDLL:
         "dsf_scatter_residual": ([vp, vp, i32, i32, i32, i32, vp, i32, vp], i32),
         "dsf_attention_forward": ([vp, vp, vp, i32, i32, i32, i32, i32, i32, vp, vp], i32),
         "dsf_workspace_size": ([vp, i32, i32, i32, i32, i32], sz),
+        "dsf_workspace_status": ([vp, vp, vp], i32),
         "dsf_sparse_block_forward": ([vp, vp, i32, vp, i32, i32, i32, i32, vp, vp, vp, vp, sz, vp], i32),
         "dsf_stack_forward": ([vp, vp, i32, i32, vp, vp, i32, i32, i32, vp, vp, sz, vp], i32),
         "dsf_timing_enable": ([i32, ctypes.c_uint32], i32),
@@ -244,6 +247,13 @@ def attention_forward(q, k, v, out, stream=None):
 
 def workspace_size(desc: LayerDesc, dtype: int, B: int, T: int, k_max: int, with_similarity: bool = False) -> int:
     return lib().dsf_workspace_size(ctypes.addressof(desc), dtype, B, T, k_max, int(with_similarity))
+
+
+def workspace_status(workspace, stream=None) -> int:
+    """Status word of the last layer/stack call on this workspace (waits for the stream)."""
+    out = ctypes.c_uint32(0)
+    _check("dsf_workspace_status", lib().dsf_workspace_status(_ptr(workspace), ctypes.byref(out), _stream(stream)))
+    return int(out.value)
 
 
 def sparse_block_forward(desc: LayerDesc, weights: LayerWeights, x, k: int, workspace, flags: int = 0,

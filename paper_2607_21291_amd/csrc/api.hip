@@ -433,8 +433,15 @@ extern "C" int dsf_attention_forward(const void* q, const void* k, const void* v
 
 namespace {
 struct Plan {
-  size_t scores, idx, a1, a2, q, k, v, attn, act, h, m2, rope, xin, simpart, alignpart, skpart, skflags, total;
+  size_t ctl, scores, idx, a1, a2, q, k, v, attn, act, h, m2, rope, xin, simpart, alignpart, skpart, total;
 };
+
+// Control block at offset 0 of a layer/stack workspace, zeroed by one launch
+// at the start of every call: word 0 is the call's status word (read by
+// dsf_workspace_status), then the stream-K flags, then the per-sequence
+// counters of the router + Top-K launch.
+constexpr int kCtlFlagsWord = 64;
+size_t ctl_words(int B) { return size_t(kCtlFlagsWord) + size_t(gemm_flag_count()) + size_t(B); }
 
 size_t up256(size_t x) { return (x + 255) / 256 * 256; }
 
@@ -450,6 +457,7 @@ Plan make_plan(const dsf_layer_desc& D, int dtype, int B, int T, int k_max, bool
     off += up256(bytes);
     return o;
   };
+  p.ctl = take(sizeof(uint32_t) * ctl_words(B));
   p.scores = take(4 * size_t(B) * T);
   p.idx = take(4 * N);
   p.a1 = take(eb * N * D.d_model);
@@ -465,10 +473,8 @@ Plan make_plan(const dsf_layer_desc& D, int dtype, int B, int T, int k_max, bool
   p.xin = with_sim ? take(eb * size_t(B) * T * D.d_model) : 0;
   p.simpart = with_sim ? take(dsf_sim_workspace_size(int64_t(B) * T)) : 0;
   p.alignpart = with_align ? take(sizeof(double) * size_t(align_grid(int64_t(B) * T))) : 0;
-  // stream-K partial tiles and their flags (bf16 GEMMs)
+  // stream-K partial tiles (bf16 GEMMs); their flags are in the control block
   p.skpart = dtype == DSF_BF16 ? take(gemm_partial_bytes()) : 0;
-  // followed by the per-sequence counters of the router + Top-K launch
-  p.skflags = dtype == DSF_BF16 ? take(sizeof(uint32_t) * (size_t(gemm_flag_count()) + size_t(B))) : 0;
   p.total = off;
   return p;
 }
@@ -515,6 +521,15 @@ extern "C" size_t dsf_workspace_size(const dsf_layer_desc* desc, int dtype, int 
                                      int with_similarity) {
   if (check_desc(desc) || check_dtype(dtype) || B < 0 || T < 0 || k_max < 0 || k_max > T) return 0;
   return make_plan(*desc, dtype, B, T, k_max, with_similarity != 0).total;
+}
+
+extern "C" int dsf_workspace_status(const void* workspace, uint32_t* status, hipStream_t stream) {
+  DSF_CHECK(workspace && status, DSF_EINVAL, "null workspace or status pointer");
+  uint32_t v = 0;
+  DSF_HIP(hipMemcpyAsync(&v, workspace, sizeof(v), hipMemcpyDeviceToHost, stream));
+  DSF_HIP(hipStreamSynchronize(stream));
+  *status = v;
+  return DSF_OK;
 }
 
 // --------------------------------------------------- one sparse layer
@@ -564,17 +579,18 @@ struct Ctx {
   const AuxStream* aux;    // null: one stream
 };
 
-uint32_t* at_flags(const Ctx& c) { return reinterpret_cast<uint32_t*>(c.ws + c.plan.skflags); }
+uint32_t* at_status(const Ctx& c) { return reinterpret_cast<uint32_t*>(c.ws + c.plan.ctl); }
+uint32_t* at_flags(const Ctx& c) { return at_status(c) + kCtlFlagsWord; }
 // per-sequence counters of the router + Top-K launch (bf16), after the flags
 uint32_t* at_route_count(const Ctx& c) { return at_flags(c) + gemm_flag_count(); }
 
-// Zero the stream-K flags and the router counters at the start of a call
-// (one launch); GEMM launches then take epochs 1, 2, ... (the flags of a
-// finished launch never equal a later epoch), and each router + Top-K launch
-// leaves its counters zero again.
+// Zero the control block at the start of a call (one launch): the status
+// word, the stream-K flags and the router counters. GEMM launches then take
+// epochs 1, 2, ... (the flags of a finished launch never equal a later
+// epoch), and each router + Top-K launch leaves its counters zero again.
 int reset_stream_k(const Ctx& c) {
   c.epoch = 0;
-  if (c.dtype == DSF_BF16) DSF_HIP(launch_zero_u32(at_flags(c), int64_t(gemm_flag_count()) + c.B, c.s));
+  DSF_HIP(launch_zero_u32(at_status(c), int64_t(ctl_words(c.B)), c.s));
   return DSF_OK;
 }
 
@@ -590,6 +606,7 @@ void use_stream_k(const Ctx& c, GemmArgs& g) {
   if (c.dtype != DSF_BF16) return;
   g.part = reinterpret_cast<float*>(c.ws + c.plan.skpart);
   g.flags = at_flags(c);
+  g.status = at_status(c);
   g.epoch = ++c.epoch;
 }
 

@@ -145,6 +145,10 @@ struct GemmArgs {
   // zeroed before the first launch using them; epoch is nonzero and distinct
   // for every launch between two zeroings.
   float* part; uint32_t* flags; uint32_t epoch;
+  // Status word of the call (nullable): a stream-K finisher whose bounded
+  // wait for a partial sum gives up ORs DSF_WS_STATUS_SK_TIMEOUT into it.
+  // spin_limit is set by the launcher: polls of a flag before giving up.
+  uint32_t* status; int spin_limit;
   // Few-row workspace (nullable): with M <= 16 rows (decode steps) a bf16 GEMM
   // splits K over workgroups; spart holds gemm_skinny_partial_bytes() and
   // scount gemm_skinny_counters() words, zero before the first launch using

@@ -785,7 +785,9 @@ __global__ __launch_bounds__((DmaCfg<BM, BN, WM, WN, NS, BK>::kThreads)) void ge
 // top of its piece) is written first, and it waits only for lower-numbered
 // workgroups of its own XCD, which are dispatched before it and never wait
 // before writing their partial: the waits always end. A bounded spin keeps
-// even a broken dispatch order from hanging the device.
+// even a broken dispatch order from hanging the device: a finisher that gives
+// up leaves its tile without the missing partials and reports it in the
+// call's status word (g.status), which the host reads back.
 template <int EPI, int BM, int BN, int WM, int WN, int NS, int BK>
 __global__ __launch_bounds__((DmaCfg<BM, BN, WM, WN, NS, BK>::kThreads)) void gemm_bf16_sk_kernel(GemmArgs g) {
   using G = DmaGemm<EPI, BM, BN, WM, WN, NS, BK>;
@@ -830,7 +832,7 @@ __global__ __launch_bounds__((DmaCfg<BM, BN, WM, WN, NS, BK>::kThreads)) void ge
         const int slot = w * kXcds + x;
         if (threadIdx.x == 0) {
           int ok = 0;
-          for (int it = 0; it < (1 << 22); ++it) {
+          for (int it = 0; it < g.spin_limit; ++it) {
             if (__hip_atomic_load(g.flags + slot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == g.epoch) {
               ok = 1;
               break;
@@ -838,9 +840,12 @@ __global__ __launch_bounds__((DmaCfg<BM, BN, WM, WN, NS, BK>::kThreads)) void ge
             __builtin_amdgcn_s_sleep(2);
           }
           spin_failed = !ok;
+          if (!ok && g.status)
+            __hip_atomic_fetch_or(g.status, uint32_t(DSF_WS_STATUS_SK_TIMEOUT), __ATOMIC_RELAXED,
+                                  __HIP_MEMORY_SCOPE_AGENT);
         }
         __syncthreads();  // the partial's loads below are issued after its flag was seen
-        if (spin_failed) break;  // left unfinished rather than hang
+        if (spin_failed) break;  // left unfinished (and reported) rather than hang
         G::add_partial(g, slot, acc);
       }
       G::epilogue(g, smem, tm, tn, acc);
@@ -945,12 +950,23 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g) {
 // most kSkMaxSlots workgroups (2 per CU on a 256-CU device).
 constexpr int kSkMaxSlots = 512;
 constexpr int kSkMinIters = 8;  // mean k-iterations per workgroup below which one tile per workgroup is kept
-constexpr int kSkMinK = 32;
+constexpr int kSkMinK = 32;    // k-iterations per tile below which the partial sums cost more than they save
 constexpr int kGroupM = 4;      // tile rows per band of the grouped tile order
-constexpr int kGroupMinCols = 8;  // below this many tile columns row-major order is already compact     // k-iterations per tile below which the partial sums cost more than they save
+constexpr int kGroupMinCols = 8;  // below this many tile columns row-major order is already compact
 
 size_t gemm_partial_bytes() { return size_t(kSkMaxSlots) * DSF_GEMM_BM * DSF_GEMM_BN * sizeof(float); }
 int gemm_flag_count() { return kSkMaxSlots; }
+
+// Polls of a stream-K flag before a finisher gives up (2^22, each followed
+// by a short sleep). DSF_SK_SPIN_LIMIT, read at every launch, overrides it:
+// a test sets 0 so that every finisher with a predecessor gives up at once
+// and the status report can be checked without any wait being broken.
+static int spin_limit() {
+  const char* e = getenv("DSF_SK_SPIN_LIMIT");
+  if (!e || !*e) return 1 << 22;
+  const long v = strtol(e, nullptr, 10);
+  return v < 0 ? 0 : (v > (1L << 30) ? (1 << 30) : int(v));
+}
 
 // DSF_GEMM_SCHEDULE=classic|streamk overrides the automatic choice (tests and
 // tuning); read at every launch so that a process can switch between calls.
@@ -1218,6 +1234,7 @@ static void launch_gemm_t(const GemmArgs& g, hipStream_t s) {
                                            resident_slots<std::integral_constant<int, EPI>>((const void*)fn, Cfg::kThreads));
       ga.px = sch.px;
       ga.split = sch.split;
+      ga.spin_limit = spin_limit();
       // tile order as for one tile per workgroup (the grid has more tiles than slots)
       ga.group_m = ntn >= kGroupMinCols ? kGroupM : 0;
       if (ga.px > 0) {

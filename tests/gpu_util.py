@@ -103,6 +103,7 @@ def run_layer(dev, w, W, x, k, flags=0, idx_in=None):
                            idx_out=None if (dense or k == 0) else idx[:, :k],
                            idx_in=None if idx_in is None else idx_in.to(dev))
     torch.cuda.synchronize()
+    assert P.workspace_status(ws) == 0, "a stream-K wait gave up"
     return xd, scores, idx[:, :k]
 
 

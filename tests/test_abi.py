@@ -242,3 +242,12 @@ def test_error_paths_of_the_kernel_calls():
 def test_valid_arguments_without_gpu_report_no_device():
     assert _call_block(_desc(), _weights()) == 5
     assert "GPU" in P.last_error()
+
+
+def test_workspace_status_rejects_null_pointers():
+    L = P.lib()
+    out = ctypes.c_uint32(7)
+    assert L.dsf_workspace_status(None, ctypes.byref(out), None) == 1
+    assert "null" in P.last_error()
+    assert L.dsf_workspace_status(ctypes.c_void_p(256), None, None) == 1
+    assert out.value == 7  # nothing written on an argument error

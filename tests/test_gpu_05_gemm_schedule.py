@@ -102,3 +102,35 @@ def test_second_stream_matches_one_stream(dev, monkeypatch, name):
     P.stack_forward(make_desc(w), [dl.weights for dl in dls], ks, x1, ws)
     torch.cuda.synchronize()
     assert torch.equal(x1, x2)
+
+
+@pytest.mark.parametrize("name,k", [("neox_bf16_small", 150), ("qwen_bf16_small", 299)])
+def test_streamk_wait_timeout_is_reported(dev, monkeypatch, name, k):
+    # The stream-K finisher waits for earlier pieces' partial sums with a
+    # bounded spin. DSF_SK_SPIN_LIMIT=0 makes every such wait give up at once
+    # (nothing waits, every kernel exits normally): the tile is then written
+    # without the missing partials and the call's status word says so. With
+    # the default limit the same call reports nothing and matches the oracle.
+    w = workload(name)
+    W = S.layer_weights(w, 0)
+    x = S.hidden_states(w)
+    B, T = x.shape[0], x.shape[1]
+    dl = P.DeviceLayer(W, dev)
+    ws = workspace(w, B, T, k, dev)
+    monkeypatch.setenv("DSF_GEMM_SCHEDULE", "streamk")
+    monkeypatch.setenv("DSF_SK_SPIN_LIMIT", "0")
+    announce(f"stream-K give-up report {name} k={k}")
+    xg = x.to(dev)
+    P.sparse_block_forward(make_desc(w), dl.weights, xg, k, ws)
+    assert P.workspace_status(ws) & P.WS_STATUS_SK_TIMEOUT
+    monkeypatch.delenv("DSF_SK_SPIN_LIMIT")
+    announce(f"stream-K default wait {name} k={k}")
+    xd = x.to(dev)
+    scores = torch.empty(B, T, dtype=torch.float32, device=dev)
+    idx = torch.empty(B, k, dtype=torch.int32, device=dev)
+    P.sparse_block_forward(make_desc(w), dl.weights, xd, k, ws, scores_out=scores, idx_out=idx)
+    assert P.workspace_status(ws) == 0
+    check_layer(w, W, x, xd, scores, idx, k)
+    # the same stack call clears the word at its start
+    P.stack_forward(make_desc(w), [dl.weights], [k], x.to(dev), ws)
+    assert P.workspace_status(ws) == 0
