@@ -4,20 +4,23 @@
 One step is one forward pass of the whole depth-sparse stack (router, Top-K,
 gather + norm, QKV + RoPE, attention over kept tokens, output and FFN
 projections, residual scatter, for every layer) over one batch of synthetic
-hidden states at fixed per-layer retention. The retention ratios come from
-the allocation of Eqs. 5-8 (run by the library's host code) on the
-workload's similarity profile, or on similarities measured by the GPU
-calibration pass (similarity statistic of Eq. 4 on the dense stack), which is
-timed separately and reported as `calibration_ms`.
+hidden states at fixed per-layer retention. The headline workload is the
+Qwen2.5-7B-shaped stack (28 x 3584, 28 q / 4 kv heads of 128, SwiGLU 18944,
+batch 4 x 8192 tokens), whose retention ratios come from the allocation of
+Eqs. 5-8 on similarities measured by the GPU calibration pass (the
+similarity statistic of Eq. 4 on the dense stack, timed separately as
+`calibration_ms`).
 
 Inputs are resident in HBM before the timed region: every timed step runs on
 its own pristine copy of the hidden states, prepared beforehand.
 
-Prints one JSON line. `roofline` is for the dominant kernel (the last GEMM
-of each layer, which for GPT-NeoX fuses the attention-output and FFN-down
-projections along K), timed with HIP events around each of its launches
-inside the timed region. `cpu_baseline` times the CPU oracle on a bounded
-sample of the same workload.
+Prints one JSON line. `roofline` is for the kernel kind that takes the most
+GPU time per step (found by an instrumented pass before the timed region),
+timed with HIP events around each of its launches inside the timed region.
+`cpu_baseline` times the CPU oracle on one layer of one sequence at the full
+shape and extrapolates to the stack with the analytic FLOP model. The other
+workloads (GPT-NeoX-160M, Qwen2.5-0.5B, the GPT-NeoX-1.4B retention sweep and
+the paper's own model shapes at r = 0.9 / 0.8 / 0.7) are extra keys.
 """
 from __future__ import annotations
 
@@ -37,12 +40,10 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 
 # HBM traffic of the dominant kernel, from two rocprofv3 passes (FETCH_SIZE,
 # then WRITE_SIZE, per dispatch) scaled by what the same counters read for the
-# library's plain copy kernel of known size. It holds only for the workload
-# and the GEMM source it was measured on (SHA-256 of kernels_gemm.hip); for
-# anything else `traffic` is null.
-TRAFFIC_MEASURED = {"workload": "neox160m", "bytes_per_launch": 2.081e+08,
-                    "gemm_source_sha256": "4cfa901f97fd6118d3472e7a082a1b59925dfe53fabfeb111c792a6825a9b490",
-                    "profile": "profiles/gemm_down_neox160m.md"}
+# library's plain copy kernel of known size. A figure holds only for the
+# workload, kernel kind and GEMM source it was measured on (SHA-256 of
+# kernels_gemm.hip); for anything else `traffic` is null.
+TRAFFIC_MEASURED = []
 
 
 def gemm_source_sha256():
@@ -52,11 +53,12 @@ def gemm_source_sha256():
         return hashlib.sha256(f.read()).hexdigest()
 
 
-def measured_traffic(workload):
-    t = TRAFFIC_MEASURED
-    if not t or t["workload"] != workload or t["gemm_source_sha256"] != gemm_source_sha256():
-        return None
-    return t["bytes_per_launch"]
+def measured_traffic(workload, kind):
+    sha = gemm_source_sha256()
+    for t in TRAFFIC_MEASURED:
+        if t["workload"] == workload and t["kind"] == kind and t["gemm_source_sha256"] == sha:
+            return t["bytes_per_launch"]
+    return None
 
 
 def log(msg):
@@ -346,60 +348,284 @@ def decode_leg(P, C, w, ks, dev, desc, weights, x0, steps):
                     "score of that (layer, sequence)"}
 
 
-def cpu_baseline(w, ks, layers, min_seconds=10.0):
-    """The oracle, as it stands, on whole sequences through `layers` layers.
 
-    Sequences 0, 1, ... are run one after another until at least
-    `min_seconds` have elapsed or the batch is exhausted, which bounds the
-    sample to roughly 10-30 s of CPU work on any host.
+
+KIND_DESC = {
+    "gemm_qkv": "QKV projection with bias and RoPE at the kept tokens' positions (EPI_QKV_ROPE epilogue)",
+    "gemm_o": "attention-output projection with the residual add (EPI_RESID_STORE epilogue)",
+    "gemm_up": "FFN up projection: gate|up with SwiGLU (Qwen) or up with bias and GELU (NeoX)",
+    "gemm_down": "last projection of the layer with the residual scatter (NeoX fuses W_o and W_down along K)",
+    "attn": "causal attention over the kept tokens",
+    "router": "router + per-sequence Top-K (one launch)",
+    "norm": "gather of the kept rows + normalisation",
+}
+
+
+def cpu_baseline_slice(w, ks, layer, min_seconds=8.0):
+    """The oracle, as it stands, on one layer of one sequence at the full
+    shape (router over all T tokens, Top-K, the block on the k_l kept rows,
+    the scatter), extrapolated to the whole stack over the whole batch with
+    the analytic FLOP model (costs.stack_flops over costs.layer_flops of the
+    slice). Sequences are run until `min_seconds` have elapsed (at least one).
     """
     from threadpoolctl import threadpool_info
 
     import synthetic as S
     from oracle import adadsf_oracle as O
+    from paper_2607_21291_amd import costs as C
 
     desc = dict(block=w.block, n_heads=w.n_heads, n_kv_heads=w.n_kv_heads, head_dim=w.head_dim, d_ff=w.d_ff,
                 rotary_dims=w.rotary_dims, rope_theta=w.rope_theta, norm_eps=w.norm_eps)
-    Ws = [{k: (O.f64(v) if hasattr(v, "detach") else v) for k, v in S.layer_weights(w, l).items()}
-          for l in range(layers)]
+    W = {k: (O.f64(v) if hasattr(v, "detach") else v) for k, v in S.layer_weights(w, layer).items()}
     xall = S.hidden_states(w)
+    k = ks[layer]
     dt, nseq = 0.0, 0
-    while nseq < w.batch and dt < min_seconds:
+    while nseq < w.batch and (nseq == 0 or dt < min_seconds):
         x = O.f64(xall[nseq:nseq + 1])
         t0 = time.perf_counter()
-        for l in range(layers):
-            x = O.routed_layer(desc, Ws[l], x, ks[l])["y"]
+        O.routed_layer(desc, W, x, k)
         dt += time.perf_counter() - t0
         nseq += 1
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
-    tokens = nseq * w.seq * layers / w.n_layers        # stack-equivalent tokens
-    return {"value": tokens / dt, "unit": "tokens/s", "cores": threads, "kind": "oracle",
-            "sample": f"sequences 0..{nseq - 1} of {w.batch} ({w.seq} tokens each) through layers 0..{layers - 1} "
-                      f"of {w.n_layers}, run until >= {min_seconds:.0f} s; {dt:.1f} s for {tokens:.0f} "
-                      f"stack-equivalent tokens",
-            "seconds": dt, "cpu_count": os.cpu_count()}
+    slice_flops = nseq * C.layer_flops(w, 1, w.seq, k, True)
+    stack_flops = C.stack_flops(w, w.batch, w.seq, ks, True)
+    gflops = slice_flops / dt / 1e9
+    tokens_per_s = w.batch * w.seq / (stack_flops / (slice_flops / dt))
+    return {"value": tokens_per_s, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"layer {layer} (k={k}) of {w.n_layers}, sequences 0..{nseq - 1} of {w.batch} at T={w.seq}: "
+                      f"{dt:.1f} s for {slice_flops / 1e12:.2f} TFLOP ({gflops:.0f} GFLOP/s in fp64); "
+                      f"extrapolated to the {w.n_layers}-layer stack over {w.batch} sequences by the analytic "
+                      f"FLOP model ({stack_flops / 1e12:.1f} TFLOP per step)",
+            "extrapolated": True, "seconds": dt, "gflops": gflops, "cpu_count": os.cpu_count()}
+
+
+def device_stack(P, S, w, dev):
+    layers = [P.DeviceLayer(S.layer_weights(w, l), dev) for l in range(w.n_layers)]
+    return layers, [dl.weights for dl in layers]
+
+
+def calibrate(P, C, w, dev, desc, dcode, weights, x0):
+    """Dense calibration pass with the on-GPU similarity statistic (Eq. 4):
+    returns (s per layer, wall ms of one pass, rate of the statistic's kernels)."""
+    import torch
+    B, T, L = w.batch, w.seq, w.n_layers
+    ws_cal = torch.empty(P.workspace_size(desc, dcode, B, T, T, True), dtype=torch.uint8, device=dev)
+    accum = torch.zeros(L, 2, dtype=torch.float64, device=dev)
+    xc = x0.clone()
+    P.stack_forward(desc, weights, [T] * L, xc, ws_cal, flags=P.FLAG_DENSE, sim_accum=accum)  # warm
+    accum.zero_()
+    xc.copy_(x0)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    P.stack_forward(desc, weights, [T] * L, xc, ws_cal, flags=P.FLAG_DENSE, sim_accum=accum)
+    s_meas = P.sim_finalize(accum)
+    t_cal = time.perf_counter() - t0
+    P.timing_enable(4 * L + 8, ["sim"])
+    accum.zero_()
+    xc.copy_(x0)
+    P.stack_forward(desc, weights, [T] * L, xc, ws_cal, flags=P.FLAG_DENSE, sim_accum=accum)
+    torch.cuda.synchronize()
+    n_sim, ms_sim = P.timing_read("sim")
+    P.timing_enable(0)
+    sim_rate = {"ms_per_layer": ms_sim / max(n_sim, 1), "launches": n_sim,
+                "achieved": C.sim_bytes(w, B, T) * n_sim / (ms_sim / 1e3) / 1e9 if ms_sim > 0 else None,
+                "unit": "GB/s", "peak": PEAK_HBM_GBS}
+    if sim_rate["achieved"]:
+        sim_rate["frac"] = sim_rate["achieved"] / PEAK_HBM_GBS
+    del ws_cal, xc
+    return s_meas, t_cal * 1e3, sim_rate
+
+
+def timed_steps(P, desc, weights, ks, x0, ws, steps, warmup, flags=0, dom_kind=None, L=None):
+    """Wall ms per step over `steps` stack calls (pristine input copies made
+    beforehand), the per-step event times, and (dom_kind given) the launches
+    of that kernel kind bracketed by HIP events: (launches, total ms)."""
+    import torch
+    stream = torch.cuda.current_stream()
+    xs = [x0.clone() for _ in range(steps)]
+    xw = x0.clone()
+    for _ in range(warmup):
+        xw.copy_(x0)
+        P.stack_forward(desc, weights, ks, xw, ws, flags=flags)
+    torch.cuda.synchronize()
+    if dom_kind:
+        P.timing_enable(steps * len(ks) * 2 + 8, [dom_kind])
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        marks[i].record(stream)
+        P.stack_forward(desc, weights, ks, xs[i], ws, flags=flags)
+    marks[-1].record(stream)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    dom = (0, 0.0)
+    if dom_kind:
+        dom = P.timing_read(dom_kind)
+        P.timing_enable(0)
+    status = P.workspace_status(ws)
+    if status:
+        raise RuntimeError(f"workspace status {status:#x} after the timed steps (a stream-K wait gave up)")
+    per_step = sorted(marks[i].elapsed_time(marks[i + 1]) for i in range(steps))
+    del xs, xw
+    return elapsed * 1e3 / steps, per_step, dom
+
+
+def breakdown_pass(P, C, w, desc, weights, ks, x0, ws, nb):
+    """Every launch bracketed by events (a separate pass): ms per step of each
+    kernel kind and its rate against its own roofline."""
+    import torch
+    B, T, L = w.batch, w.seq, w.n_layers
+    xw = x0.clone()
+    P.timing_enable(nb * L * 16 + 64)
+    for i in range(nb):
+        xw.copy_(x0)
+        P.stack_forward(desc, weights, ks, xw, ws)
+    torch.cuda.synchronize()
+    out = {}
+    for kind in P.KINDS:
+        n, ms = P.timing_read(kind)
+        if n:
+            out[kind] = {"ms_per_step": ms / nb, "launches_per_step": n / nb}
+    P.timing_enable(0)
+    for kind, v in out.items():
+        wk = [C.kind_work(w, kind, B, T, k) for k in ks if k > 0]
+        if not wk or wk[0] is None:
+            continue
+        total, unit = sum(x[0] for x in wk), wk[0][1]
+        secs = v["ms_per_step"] / 1e3
+        if unit == "flop":
+            v.update(achieved=total / secs / 1e12, unit="TFLOP/s", peak=PEAK_BF16_TFLOPS,
+                     frac=total / secs / 1e12 / PEAK_BF16_TFLOPS)
+        else:
+            v.update(achieved=total / secs / 1e9, unit="GB/s", peak=PEAK_HBM_GBS,
+                     frac=total / secs / 1e9 / PEAK_HBM_GBS)
+    del xw
+    return out
+
+
+def measure_stack(P, C, S, w, dev, steps, warmup, dense=True, breakdown=True, calib=True, only_sparse=False):
+    """One workload: retention (fixed, from its similarity profile, or from
+    the GPU calibration pass), the timed sparse stack with its dominant
+    kernel's roofline, the per-kind breakdown, and the dense stack with the
+    same kernels."""
+    import torch
+    B, T, L = w.batch, w.seq, w.n_layers
+    dcode = P.F32 if w.dtype == "f32" else P.BF16
+    desc = P.make_desc(w.block, w.d_model, w.n_heads, w.n_kv_heads, w.head_dim, w.d_ff, w.rotary_dims,
+                       w.d_router, w.norm_eps, w.rope_theta)
+    log(f"workload {w.name}: L={L} d={w.d_model} B={B} T={T} dtype={w.dtype}")
+    layers, weights = device_stack(P, S, w, dev)
+    x0 = S.hidden_states(w).to(dev)
+    s_meas, t_cal, sim_rate = None, None, None
+    if w.retention is None and (w.similarity is None or (calib and not only_sparse)):
+        s_meas, t_cal, sim_rate = calibrate(P, C, w, dev, desc, dcode, weights, x0)
+        log(f"calibration pass {t_cal:.2f} ms; measured similarity {[round(v, 4) for v in s_meas]}")
+    r = retention(P, w, s_meas)
+    ks = [P.k_from_retention(v, T) for v in r]
+    log(f"k per layer {ks}")
+    ws = torch.empty(P.workspace_size(desc, dcode, B, T, max(ks)), dtype=torch.uint8, device=dev)
+
+    breakdown_d = {}
+    dom_kind = "gemm_up" if only_sparse else None
+    if breakdown and not only_sparse:
+        breakdown_d = breakdown_pass(P, C, w, desc, weights, ks, x0, ws, min(steps, 5))
+        dom_kind = max(breakdown_d, key=lambda kk: breakdown_d[kk]["ms_per_step"])
+    ms_step, per_step, (n_dom, ms_dom) = timed_steps(P, desc, weights, ks, x0, ws, steps, warmup, dom_kind=dom_kind)
+    tokens_per_s = B * T / (ms_step / 1e3)
+    log(f"sparse stack {ms_step:.3f} ms/step, {tokens_per_s / 1e6:.4f} M tokens/s")
+
+    roofline = None
+    if dom_kind and n_dom:
+        work = [C.kind_work(w, dom_kind, B, T, k) for k in ks if k > 0]
+        total = sum(x[0] for x in work) * steps
+        unit = work[0][1]
+        launches_expected = len(work) * steps
+        per_launch = total / max(n_dom, 1)
+        if unit == "flop":
+            achieved = total / (ms_dom / 1e3) / 1e12
+            roofline = {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                        "frac": achieved / PEAK_BF16_TFLOPS}
+        else:
+            achieved = total / (ms_dom / 1e3) / 1e9
+            roofline = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                        "frac": achieved / PEAK_HBM_GBS}
+        roofline.update(traffic=measured_traffic(w.name, dom_kind), kernel_kind=dom_kind,
+                        kernel=KIND_DESC.get(dom_kind, dom_kind), launches=n_dom,
+                        launches_expected=launches_expected, avg_launch_us=ms_dom / max(n_dom, 1) * 1e3,
+                        work_per_launch=per_launch, work_unit=unit,
+                        share_of_gpu_time=(breakdown_d[dom_kind]["ms_per_step"] /
+                                           sum(v["ms_per_step"] for v in breakdown_d.values()))
+                        if breakdown_d else None)
+
+    gemm_ms = sum(v["ms_per_step"] for kk, v in breakdown_d.items() if kk.startswith("gemm"))
+    rates = {
+        "step_tflops": C.stack_flops(w, B, T, ks, True) / (ms_step / 1e3) / 1e12,
+        "gemm_tflops": sum(C.proj_flops(w, B, k) for k in ks) / (gemm_ms / 1e3) / 1e12 if gemm_ms else None,
+    }
+    res = {"workload": w.name, "ms_per_step": ms_step, "ms_per_step_median": per_step[len(per_step) // 2],
+           "ms_per_step_min": per_step[0], "tokens_per_s": tokens_per_s, "k_per_layer": ks,
+           "mean_retention": sum(r) / L, "roofline": roofline, "kernel_breakdown": breakdown_d, "rates": rates,
+           "calibration_ms": t_cal, "similarity_kernel": sim_rate, "similarity_measured": s_meas,
+           "flop_ratio_sparse_over_dense": C.stack_flops(w, B, T, ks, True) / C.stack_flops(w, B, T, [T] * L, False)}
+    if dense and not only_sparse:
+        wsd = torch.empty(P.workspace_size(desc, dcode, B, T, T), dtype=torch.uint8, device=dev)
+        nd = max(3, steps // 4)
+        dense_ms, _, _ = timed_steps(P, desc, weights, [T] * L, x0, wsd, nd, 1, flags=P.FLAG_DENSE)
+        res["dense"] = {"ms_per_step": dense_ms, "speedup_sparse_vs_dense": dense_ms / ms_step,
+                        "ideal_speedup": 1.0 / res["flop_ratio_sparse_over_dense"]}
+        log(f"dense stack {dense_ms:.3f} ms/step, speedup {dense_ms / ms_step:.2f}x "
+            f"(1/FLOP ratio {1.0 / res['flop_ratio_sparse_over_dense']:.2f}x)")
+        del wsd
+    ctx = {"desc": desc, "weights": weights, "layers": layers, "x0": x0, "ws": ws, "ks": ks}
+    return res, ctx
+
+
+def retention_sweep(P, C, S, w, dev, rs, steps, warmup):
+    """Uniform retention r for every layer, each r against the dense stack
+    (same kernels, same weights): ms/step, speedup and the FLOP ratio."""
+    import torch
+    B, T, L = w.batch, w.seq, w.n_layers
+    dcode = P.F32 if w.dtype == "f32" else P.BF16
+    desc = P.make_desc(w.block, w.d_model, w.n_heads, w.n_kv_heads, w.head_dim, w.d_ff, w.rotary_dims,
+                       w.d_router, w.norm_eps, w.rope_theta)
+    log(f"retention sweep {w.name}: L={L} d={w.d_model} B={B} T={T}, r in {rs}")
+    layers, weights = device_stack(P, S, w, dev)
+    x0 = S.hidden_states(w).to(dev)
+    wsd = torch.empty(P.workspace_size(desc, dcode, B, T, T), dtype=torch.uint8, device=dev)
+    dense_ms, _, _ = timed_steps(P, desc, weights, [T] * L, x0, wsd, steps, warmup, flags=P.FLAG_DENSE)
+    out = {"workload": f"{w.name}: {L} x {w.d_model}, heads {w.n_heads}/{w.n_kv_heads} x {w.head_dim}, "
+                       f"FFN {w.d_ff}, batch {B} x seq {T}", "dense_ms_per_step": dense_ms, "r": {}}
+    for r in rs:
+        ks = [P.k_from_retention(r, T)] * L
+        ms, _, _ = timed_steps(P, desc, weights, ks, x0, wsd, steps, warmup)
+        ratio = C.stack_flops(w, B, T, ks, True) / C.stack_flops(w, B, T, [T] * L, False)
+        out["r"][f"{r:g}"] = {"k": ks[0], "ms_per_step": ms, "tokens_per_s": B * T / (ms / 1e3),
+                              "speedup_vs_dense": dense_ms / ms, "flop_ratio": ratio, "ideal_speedup": 1.0 / ratio}
+        log(f"  r={r:g}: {ms:.3f} ms/step, {dense_ms / ms:.2f}x dense (1/FLOP ratio {1.0 / ratio:.2f}x)")
+    del layers, weights, x0, wsd
+    torch.cuda.empty_cache()
+    return out
 
 
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="neox160m")
+    ap.add_argument("--workload", default="qwen7b")
     ap.add_argument("--retention", type=float, default=None,
                     help="uniform retention r for every layer (skips the allocation and the calibration pass)")
     ap.add_argument("--batch", type=int, default=None, help="override the workload's batch")
     ap.add_argument("--seq", type=int, default=None, help="override the workload's sequence length")
-    ap.add_argument("--cpu-layers", type=int, default=None, help="layers of the CPU oracle sample (default all)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true", help="skip the dense-stack comparison run")
     ap.add_argument("--no-extras", action="store_true",
-                    help="skip the standalone sections (streaming entry points, router-score pathway, alignment "
-                         "objective); used for the counter passes")
+                    help="skip the other workloads and the standalone sections (used for the counter passes)")
     ap.add_argument("--only-sparse", action="store_true",
-                    help="launch only the sparse stack (warmup + timed steps): no calibration pass when the "
-                         "workload fixes its similarity profile, no dense run, no breakdown pass, no CPU "
-                         "baseline; used under rocprofv3 so every launch it sees is a timed-shape launch")
+                    help="launch only the sparse stack (calibration if the workload needs it, warmup, timed "
+                         "steps with the gate/up projection's launches timed): no dense run, no breakdown pass, "
+                         "no CPU baseline, no extras; used under rocprofv3")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -424,162 +650,23 @@ def main():
             ap.error("--retention must be in (0, 1]")
         w = w.replace(name=f"{w.name}_r{args.retention:g}", retention=(args.retention,) * w.n_layers,
                       similarity=None)
-    B, T, L = w.batch, w.seq, w.n_layers
-    dt = w.torch_dtype
-    dcode = P.F32 if w.dtype == "f32" else P.BF16
-    desc = P.make_desc(w.block, w.d_model, w.n_heads, w.n_kv_heads, w.head_dim, w.d_ff, w.rotary_dims,
-                       w.d_router, w.norm_eps, w.rope_theta)
-    log(f"workload {w.name}: L={L} d={w.d_model} B={B} T={T} dtype={w.dtype}")
-    layers = [P.DeviceLayer(S.layer_weights(w, l), dev) for l in range(L)]
-    weights = [dl.weights for dl in layers]
-    x0 = S.hidden_states(w).to(dev)
-    stream = torch.cuda.current_stream()
-
     if args.only_sparse:
-        args.no_dense = args.no_cpu_baseline = True
-    # calibration pass: dense stack + on-GPU similarity statistic (Eq. 4), allocation (Eqs. 5-8)
-    s_meas, t_cal, sim_rate = None, None, None
-    if args.retention is None and not (args.only_sparse and w.similarity is not None):
-        ws_cal = torch.empty(P.workspace_size(desc, dcode, B, T, T, True), dtype=torch.uint8, device=dev)
-        accum = torch.zeros(L, 2, dtype=torch.float64, device=dev)
-        xc = x0.clone()
-        P.stack_forward(desc, weights, [T] * L, xc, ws_cal, flags=P.FLAG_DENSE, sim_accum=accum)  # warm
-        accum.zero_()
-        xc.copy_(x0)
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        P.stack_forward(desc, weights, [T] * L, xc, ws_cal, flags=P.FLAG_DENSE, sim_accum=accum)
-        s_meas = P.sim_finalize(accum)
-        t_cal = time.perf_counter() - t0
-        # the similarity statistic's own kernels, in a second calibration pass
-        P.timing_enable(4 * L + 8, ["sim"])
-        accum.zero_()
-        xc.copy_(x0)
-        P.stack_forward(desc, weights, [T] * L, xc, ws_cal, flags=P.FLAG_DENSE, sim_accum=accum)
-        torch.cuda.synchronize()
-        n_sim, ms_sim = P.timing_read("sim")
-        P.timing_enable(0)
-        sim_rate = {"ms_per_layer": ms_sim / max(n_sim, 1), "launches": n_sim,
-                    "achieved": C.sim_bytes(w, B, T) * n_sim / (ms_sim / 1e3) / 1e9 if ms_sim > 0 else None,
-                    "unit": "GB/s", "peak": PEAK_HBM_GBS}
-        if sim_rate["achieved"]:
-            sim_rate["frac"] = sim_rate["achieved"] / PEAK_HBM_GBS
-        del ws_cal, xc
-        log(f"calibration pass {t_cal * 1e3:.2f} ms; measured similarity {[round(v, 4) for v in s_meas]}")
-    r = retention(P, w, s_meas)
-    ks = [P.k_from_retention(v, T) for v in r]
-    log(f"k per layer {ks}")
+        args.no_dense = args.no_cpu_baseline = args.no_extras = True
 
-    ws = torch.empty(P.workspace_size(desc, dcode, B, T, max(ks)), dtype=torch.uint8, device=dev)
-    xs = [x0.clone() for _ in range(args.steps)]
-    xw = x0.clone()
-    for _ in range(args.warmup):
-        xw.copy_(x0)
-        P.stack_forward(desc, weights, ks, xw, ws)
-    torch.cuda.synchronize()
-
-    # timed region: K steps, dominant-kernel launches bracketed by HIP events,
-    # and an event between consecutive steps (per-step median and minimum)
-    P.timing_enable(args.steps * L + 8, ["gemm_down"])
-    marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        marks[i].record(stream)
-        P.stack_forward(desc, weights, ks, xs[i], ws)
-    marks[-1].record(stream)
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    per_step = sorted(marks[i].elapsed_time(marks[i + 1]) for i in range(args.steps))
-    n_dom, ms_dom = P.timing_read("gemm_down")
-    P.timing_enable(0)
-    ms_step = elapsed * 1e3 / args.steps
-    tokens_per_s = B * T / (ms_step / 1e3)
-    log(f"sparse stack {ms_step:.3f} ms/step, {tokens_per_s / 1e6:.3f} M tokens/s")
-
-    # roofline of the dominant kernel: algorithmic FLOPs per launch / its average duration
-    flops_dom = sum(C.gemm_down_flops(w, B, k) for k in ks if k > 0) * args.steps
-    avg_ms = ms_dom / max(n_dom, 1)
-    achieved = flops_dom / (ms_dom / 1e3) / 1e12 if ms_dom > 0 else 0.0
-    roofline = {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                "frac": achieved / PEAK_BF16_TFLOPS, "traffic": measured_traffic(w.name),
-                "kernel": "down projection: gemm_bf16_dma_kernel<4, 128, 128, 64, 64, 2, 64> (one tile per "
-                          "workgroup) or gemm_bf16_sk_kernel<4, 128, 128, 64, 64, 2, 64> (stream-K, on layers "
-                          "whose tiles leave a short last round); residual-scatter epilogue",
-                "launches": n_dom, "avg_launch_us": avg_ms * 1e3,
-                "flops_per_launch": flops_dom / max(n_dom, 1)}
-
-    # per-kernel breakdown (a separate instrumented pass, every launch bracketed)
-    breakdown = {}
-    if not args.only_sparse:
-        nb = min(args.steps, 10)
-        P.timing_enable(nb * L * 16 + 64)
-        for i in range(nb):
-            xw.copy_(x0)
-            P.stack_forward(desc, weights, ks, xw, ws)
-        torch.cuda.synchronize()
-        for kind in P.KINDS:
-            n, ms = P.timing_read(kind)
-            if n:
-                breakdown[kind] = {"ms_per_step": ms / nb, "launches_per_step": n / nb}
-        P.timing_enable(0)
-
-    # work and achieved rates of the whole step
-    sparse_flops = C.stack_flops(w, B, T, ks, True)
-    gemm_flops = sum(C.proj_flops(w, B, k) for k in ks)
-    attn_flops = sum(C.attn_flops(w, B, k) for k in ks)
-    gemm_ms = sum(v["ms_per_step"] for k, v in breakdown.items() if k.startswith("gemm"))
-    attn_ms = breakdown.get("attn", {}).get("ms_per_step", 0.0)
-    router_ms = breakdown.get("router", {}).get("ms_per_step", 0.0)
-    # every kernel kind against its own roofline (in-situ: the inputs of a layer
-    # were written by the layer before, so reads may be served by the MALL)
-    for kind, v in breakdown.items():
-        wk = [C.kind_work(w, kind, B, T, k) for k in ks if k > 0]
-        if not wk or wk[0] is None:
-            continue
-        total, unit = sum(x[0] for x in wk), wk[0][1]
-        secs = v["ms_per_step"] / 1e3
-        if unit == "flop":
-            v.update(achieved=total / secs / 1e12, unit="TFLOP/s", peak=PEAK_BF16_TFLOPS,
-                     frac=total / secs / 1e12 / PEAK_BF16_TFLOPS)
-        else:
-            v.update(achieved=total / secs / 1e9, unit="GB/s", peak=PEAK_HBM_GBS,
-                     frac=total / secs / 1e9 / PEAK_HBM_GBS)
-    rates = {
-        "step_tflops": sparse_flops / (ms_step / 1e3) / 1e12,
-        "gemm_tflops": gemm_flops / (gemm_ms / 1e3) / 1e12 if gemm_ms else None,
-        "attn_tflops": attn_flops / (attn_ms / 1e3) / 1e12 if attn_ms else None,
-        "router_gbs": sum(C.router_bytes(w, B, T) for k in ks if k > 0) / (router_ms / 1e3) / 1e9 if router_ms else None,
-    }
-
-    dense = None
-    if not args.no_dense:
-        xd = x0.clone()
-        wsd = torch.empty(P.workspace_size(desc, dcode, B, T, T), dtype=torch.uint8, device=dev)
-        P.stack_forward(desc, weights, [T] * L, xd, wsd, flags=P.FLAG_DENSE)
-        nd = max(3, args.steps // 3)
-        xds = [x0.clone() for _ in range(nd)]
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        for i in range(nd):
-            P.stack_forward(desc, weights, [T] * L, xds[i], wsd, flags=P.FLAG_DENSE)
-        torch.cuda.synchronize()
-        dense_ms = (time.perf_counter() - t0) * 1e3 / nd
-        dense = {"ms_per_step": dense_ms, "speedup_sparse_vs_dense": dense_ms / ms_step,
-                 "flop_ratio_sparse_over_dense": C.stack_flops(w, B, T, ks, True) / C.stack_flops(w, B, T, [T] * L, False)}
-        log(f"dense stack {dense_ms:.3f} ms/step, speedup {dense_ms / ms_step:.2f}x")
-        del xds, wsd, xd
-
+    head, ctx = measure_stack(P, C, S, w, dev, args.steps, args.warmup, dense=not args.no_dense,
+                              only_sparse=args.only_sparse)
+    B, T, L = w.batch, w.seq, w.n_layers
+    ks = head["k_per_layer"]
     out = {
         "metric": METRIC,
-        "value": tokens_per_s,
+        "value": head["tokens_per_s"],
         "unit": "tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": ms_step,
-        "ms_per_step_median": per_step[len(per_step) // 2],
-        "ms_per_step_min": per_step[0],
+        "ms_per_step": head["ms_per_step"],
+        "ms_per_step_median": head["ms_per_step_median"],
+        "ms_per_step_min": head["ms_per_step_min"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -588,36 +675,60 @@ def main():
         "config": {"workload": f"{w.name}: {L}-layer {w.block} stack, d={w.d_model}, heads {w.n_heads}/{w.n_kv_heads}"
                                f"x{w.head_dim}, FFN {w.d_ff}, batch {B} x seq {T}",
                    "global_batch": B, "seq_len": T, "layers": L, "parallelism": "single GPU",
-                   "mean_retention": sum(r) / L, "k_per_layer": ks},
-        "roofline": roofline,
+                   "mean_retention": head["mean_retention"], "k_per_layer": ks},
+        "roofline": head["roofline"],
         "cpu_baseline": None,
-        "kernel_breakdown": breakdown,
-        "rates": rates,
-        "dense": dense,
-        "calibration_ms": None if t_cal is None else t_cal * 1e3,
-        "similarity_kernel": sim_rate,
-        "similarity_measured": s_meas,
+        "kernel_breakdown": head["kernel_breakdown"],
+        "rates": head["rates"],
+        "dense": head.get("dense"),
+        "flop_ratio_sparse_over_dense": head["flop_ratio_sparse_over_dense"],
+        "calibration_ms": head["calibration_ms"],
+        "similarity_kernel": head["similarity_kernel"],
+        "similarity_measured": head["similarity_measured"],
         "hip_runtime": torch.version.hip,
     }
-    if not (args.only_sparse or args.no_extras):
-        kmean = int(round(sum(ks) / len(ks)))
-        log(f"streaming entry points standalone (B={B}, T={T}, k={kmean}), cold and hot inputs")
-        out["streaming_kernels"] = streaming_rates(P, C, w, kmean, dev, S.layer_weights(w, 0))
-    if not (args.only_sparse or args.no_extras):
+    del ctx
+    torch.cuda.empty_cache()
+    if not args.no_extras:
+        extras = {}
+        # GPT-NeoX-160M shape (similarity profile) with the standalone sections
+        w2 = S.WORKLOADS["neox160m"]
+        r2, c2 = measure_stack(P, C, S, w2, dev, 20, 5)
+        kmean = int(round(sum(r2["k_per_layer"]) / len(r2["k_per_layer"])))
+        log(f"streaming entry points standalone (neox160m, k={kmean}), cold and hot inputs")
+        r2["streaming_kernels"] = streaming_rates(P, C, w2, kmean, dev, S.layer_weights(w2, 0))
         log("router-score pathway: gated stack, gate score gradient, router backward")
-        out["router_score_pathway"] = router_pathway(P, C, w, ks, dev, desc, weights, x0, ws, ms_step,
-                                                     max(3, args.steps // 3), S.layer_weights(w, 0))
-    if not (args.only_sparse or args.no_extras):
+        r2["router_score_pathway"] = router_pathway(P, C, w2, c2["ks"], dev, c2["desc"], c2["weights"], c2["x0"],
+                                                    c2["ws"], r2["ms_per_step"], 6, S.layer_weights(w2, 0))
         log("alignment objective: teacher/student stack, Eq. 9 and Eq. 10 kernels")
-        out["alignment_objective"] = alignment_objective(P, C, w, ks, dev, desc, weights, x0, ms_step,
-                                                         max(3, args.steps // 3))
-    if not (args.only_sparse or args.no_extras):
+        r2["alignment_objective"] = alignment_objective(P, C, w2, c2["ks"], dev, c2["desc"], c2["weights"], c2["x0"],
+                                                        r2["ms_per_step"], 6)
         log("incremental decoding: prefill into kept-token caches, then threshold-routed decode steps")
-        out["decode"] = decode_leg(P, C, w, ks, dev, desc, weights, x0, max(10, args.steps))
+        r2["decode"] = decode_leg(P, C, w2, c2["ks"], dev, c2["desc"], c2["weights"], c2["x0"], 20)
+        extras["neox160m"] = r2
+        del c2
+        torch.cuda.empty_cache()
+        # Qwen2.5-0.5B shape, similarity profile
+        r3, c3 = measure_stack(P, C, S, S.WORKLOADS["qwen05b"], dev, 10, 3)
+        extras["qwen05b"] = r3
+        del c3
+        torch.cuda.empty_cache()
+        # GPT-NeoX-1.4B shape, uniform retention sweep
+        extras["neox14b_sweep"] = retention_sweep(P, C, S, S.WORKLOADS["neox14b"], dev, [1.0, 0.75, 0.5, 0.25], 5, 2)
+        # the paper's evaluation shapes at its retention ratios (Tables 1b, 2)
+        paper = {}
+        for name, seq in (("neox130m", None), ("qwen05b", 2048), ("qwen15b", None)):
+            wp = S.WORKLOADS[name]
+            if seq:
+                wp = wp.replace(name=f"{name}_T{seq}", seq=seq, similarity=None, target=None, tau=None,
+                                retention=(0.8,) * wp.n_layers)
+            paper[wp.name] = retention_sweep(P, C, S, wp, dev, [0.9, 0.8, 0.7], 5, 2)
+        extras["paper_shapes"] = paper
+        out["extras"] = extras
     if not args.no_cpu_baseline:
-        layers_cpu = L if args.cpu_layers is None else min(args.cpu_layers, L)
-        log(f"cpu oracle baseline over {layers_cpu} layers of one sequence")
-        out["cpu_baseline"] = cpu_baseline(w, ks, layers_cpu)
+        layer = min(range(L), key=lambda l: abs(ks[l] - sorted(ks)[L // 2]))
+        log(f"cpu oracle baseline: layer {layer} of one sequence at full shape, extrapolated")
+        out["cpu_baseline"] = cpu_baseline_slice(w, ks, layer)
     print(json.dumps(out), flush=True)
 
 

@@ -278,7 +278,8 @@ int dsf_attention_forward(const void* q, const void* k, const void* v, int dtype
  * each call of dsf_sparse_block_forward, dsf_stack_forward,
  * dsf_stack_prefill and dsf_align_stack_forward clears at its start and that
  * its kernels OR bits into; read it with dsf_workspace_status once the call's
- * work is enqueued. DSF_WS_STATUS_SK_TIMEOUT: a stream-K workgroup that must
+ * work is enqueued. A call with nothing to do (B, T or k zero), which
+ * launches nothing, leaves the word as it was. DSF_WS_STATUS_SK_TIMEOUT: a stream-K workgroup that must
  * add an earlier workgroup's partial sum waits for it with a bounded spin of
  * 2^22 polls of its flag (the partial is normally ready within microseconds,
  * because the hardware dispatches workgroups in order); if the wait gives

@@ -103,22 +103,46 @@ def run_layer(dev, w, W, x, k, flags=0, idx_in=None):
                            idx_out=None if (dense or k == 0) else idx[:, :k],
                            idx_in=None if idx_in is None else idx_in.to(dev))
     torch.cuda.synchronize()
-    assert P.workspace_status(ws) == 0, "a stream-K wait gave up"
+    if k > 0:  # a call that launches nothing leaves the status word as it was
+        assert P.workspace_status(ws) == 0, "a stream-K wait gave up"
     return xd, scores, idx[:, :k]
 
 
+def check_selection(ref_scores, bound, sc_gpu, idx_gpu, k):
+    """Selection steps of the parity protocol, for every sequence.
+
+    GPU scores within the fp32 bound of the oracle's; the oracle's Top-K of
+    the GPU's scores equal to the GPU's indices; and, where the oracle's own
+    scores select differently, every token in the difference has an oracle
+    score within the score tolerance of the oracle's k-th score (its own
+    bound plus the largest bound of the sequence), so only near-ties can
+    change places."""
+    assert np.all(np.abs(sc_gpu - ref_scores) <= bound)
+    np.testing.assert_array_equal(idx_gpu, O.topk_select(sc_gpu, k))
+    if k == 0:
+        return
+    idx_ref = O.topk_select(ref_scores, k)
+    for b in range(ref_scores.shape[0]):
+        diff = np.setxor1d(idx_ref[b], idx_gpu[b])
+        if diff.size == 0:
+            continue
+        kth = np.min(ref_scores[b, idx_ref[b]])
+        tol = bound[b, diff] + np.max(bound[b])
+        assert np.all(np.abs(ref_scores[b, diff] - kth) <= tol), (b, diff)
+
+
 def check_layer(w, W, x, y_gpu, scores_gpu, idx_gpu, k, sample=None, gate=False):
-    """Layer protocol: router scores within the fp32 bound and the oracle's
-    Top-K of the GPU's scores equal to the GPU's indices (every sequence),
+    """Layer protocol: router scores within the fp32 bound, the oracle's Top-K
+    of the GPU's scores equal to the GPU's indices and any difference from
+    the oracle's own selection confined to near-ties (every sequence),
     skipped rows bitwise unchanged (every sequence), and the kept rows
     against the oracle teacher-forced with the GPU's indices, for the
     sequences in `sample` (None: all of them). gate: the score-gated layer."""
     xs = to_np(x)
     sc = scores_gpu.cpu().numpy()
     ref_scores = O.router_scores(x, W["router_w1"], W["router_b1"], W["router_w2"], W["router_b2"])
-    assert np.all(np.abs(sc - ref_scores) <= router_bound(xs, W, w.dtype))
     idx = idx_gpu.cpu().numpy().astype(np.int64)
-    np.testing.assert_array_equal(idx, O.topk_select(sc, k))
+    check_selection(ref_scores, router_bound(xs, W, w.dtype), sc, idx, k)
     y = to_np(y_gpu)
     B, T, _ = xs.shape
     kept = np.zeros((B, T), dtype=bool)
@@ -128,5 +152,26 @@ def check_layer(w, W, x, y_gpu, scores_gpu, idx_gpu, k, sample=None, gate=False)
     for b in (range(B) if sample is None else sample):
         res = O.routed_layer(desc_dict(w), W, xs[b:b + 1], k, idx=idx[b:b + 1], gate=gate)
         upd = res["y"][0][kept[b]] - xs[b][kept[b]]
-        assert rel_inf(y[b][kept[b]] - xs[b][kept[b]], upd) < TOL[w.dtype]
+        assert update_err(y[b][kept[b]], xs[b][kept[b]], upd, w.dtype) < TOL[w.dtype]
         assert rel_inf(y[b], res["y"][0]) < TOL[w.dtype]
+
+
+def storage_half_ulp(v, dtype: str) -> np.ndarray:
+    """Half a unit in the last place of each value in the storage format (the
+    largest error of rounding it to nearest): bf16 keeps 8 significant bits,
+    fp32 24."""
+    bits = 8 if dtype == "bf16" else 24
+    v = np.abs(np.asarray(v, dtype=np.float64))
+    e = np.floor(np.log2(np.where(v > 0, v, 1.0)))
+    return np.where(v > 0, 2.0 ** (e - bits), 0.0)
+
+
+def update_err(y, x, upd_ref, dtype: str) -> float:
+    """Relative error of a layer's update as observed through its stored
+    output: the GPU stores y = x + delta rounded to the storage format, so
+    y - x carries that rounding (half an ulp of y) on top of the kernel's own
+    error. Returns max(|(y - x) - delta_ref| - half_ulp(y), 0) / max|delta_ref|."""
+    y, x, upd_ref = (np.asarray(a, dtype=np.float64) for a in (y, x, upd_ref))
+    excess = np.maximum(np.abs((y - x) - upd_ref) - storage_half_ulp(y, dtype), 0.0)
+    den = np.max(np.abs(upd_ref))
+    return float(np.max(excess) / (den if den > 0 else 1.0)) if excess.size else 0.0

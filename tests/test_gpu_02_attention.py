@@ -68,3 +68,29 @@ def test_attention_deterministic(dev):
     P.attention_forward(q, k, v, o2)
     torch.cuda.synchronize()
     assert torch.equal(o1, o2)
+
+
+@pytest.mark.parametrize("hd,Hq,Hkv,n", [(64, 2, 1, 700), (64, 2, 2, 2100), (128, 4, 1, 1500), (128, 2, 2, 4100)])
+def test_attention_peaky_logits(dev, hd, Hq, Hkv, n):
+    """Queries scaled by 8 put the logits q.k / sqrt(hd) at a standard
+    deviation of 8, so the running maximum of the online softmax moves many
+    times along a row and most probabilities underflow: the rescaling of the
+    partial sums is exercised on every staging (DMA ring up to 2048 keys at
+    head dim 64, register prefetch beyond it and at head dim 128)."""
+    announce(f"attention peaky logits hd={hd} Hq={Hq} Hkv={Hkv} n={n}")
+    g = torch.Generator().manual_seed(7 * n + hd)
+    q = (torch.randn(1, Hq, n, hd, generator=g) * 8.0).to(torch.bfloat16)
+    k = torch.randn(1, Hkv, n, hd, generator=g).to(torch.bfloat16)
+    v = torch.randn(1, Hkv, n, hd, generator=g).to(torch.bfloat16)
+    out = torch.empty(1, n, Hq * hd, dtype=torch.bfloat16, device=dev)
+    P.attention_forward(q.to(dev), k.to(dev), v.to(dev), out)
+    torch.cuda.synchronize()
+    qn, kn, vn = (to_np(t[0]).transpose(1, 0, 2) for t in (q, k, v))
+    ref = O.causal_attention(qn, kn, vn)
+    got = to_np(out)[0]
+    assert rel_inf(got, ref) < TOL[torch.bfloat16]
+    # per row as well, against the row's own scale sum_j p_j |v_j| (the
+    # attention of |v|), so that the largest rows cannot hide a wrong small one
+    scale = O.causal_attention(qn, kn, np.abs(vn))
+    err = np.max(np.abs(got - ref), axis=1) / np.max(scale, axis=1)
+    assert np.max(err) < TOL[torch.bfloat16]
