@@ -373,6 +373,25 @@ int dsf_decode_step(const dsf_layer_desc* desc, const dsf_layer_weights* weights
                     int32_t* cache_len, int cap, void* workspace, size_t workspace_bytes,
                     hipStream_t stream);
 
+/* For callers that cannot allocate device memory: code being captured into a
+ * HIP graph, tight serving loops, harnesses that forbid hipMalloc. The same
+ * step as dsf_decode_step, with the same arguments and results, but without
+ * a workspace argument: its scratch is a static device array of
+ * dsf_decode_static_scratch_bytes() bytes (32 MiB) that the library holds on
+ * each device it runs on until the process ends. The call allocates nothing
+ * (no hipMalloc or hipFree). A step whose dsf_decode_workspace_size exceeds
+ * the array returns DSF_EWORKSPACE and enqueues nothing. Every call on one
+ * device shares that device's array and leaves its contents behind; the step
+ * clears what must start at zero itself. Two calls that can overlap on one
+ * device (different streams or host threads) race: serialise them, or give
+ * one of them dsf_decode_step with its own workspace. */
+size_t dsf_decode_static_scratch_bytes(void);
+int dsf_decode_step_static(const dsf_layer_desc* desc, const dsf_layer_weights* weights, int L,
+                           int dtype, void* x, int B, const int32_t* pos, int max_pos,
+                           const float* thr, float* scores_out, int32_t* keep_out,
+                           void* const* cache_k, void* const* cache_v, int32_t* cache_len, int cap,
+                           hipStream_t stream);
+
 /* Prefill into decode caches: dsf_stack_forward over x [B, T, d] with k[l]
  * kept tokens per layer (no flags, no similarity) that also stores each
  * layer's kept keys and values (RoPE at their positions, in position order)

@@ -35,7 +35,7 @@ EXPORTS = [
     "dsf_gate_score_grad", "dsf_router_backward_workspace_size", "dsf_router_backward",
     "dsf_align_workspace_size", "dsf_align_hidden", "dsf_kl_align", "dsf_align_stack_workspace_size",
     "dsf_align_stack_forward", "dsf_decode_workspace_size", "dsf_decode_step", "dsf_stack_prefill",
-    "dsf_workspace_status",
+    "dsf_workspace_status", "dsf_decode_static_scratch_bytes", "dsf_decode_step_static",
 ]
 WS_STATUS_SK_TIMEOUT = 1
 
@@ -106,6 +106,8 @@ def lib() -> ctypes.CDLL:
         "dsf_decode_workspace_size": ([vp, i32, i32, i32, i32], sz),
         "dsf_decode_step": ([vp, vp, i32, i32, vp, i32, vp, i32, vp, vp, vp, vp, vp, vp, i32, vp, sz, vp], i32),
         "dsf_stack_prefill": ([vp, vp, i32, i32, vp, vp, i32, i32, vp, vp, vp, i32, vp, vp, sz, vp], i32),
+        "dsf_decode_static_scratch_bytes": ([], sz),
+        "dsf_decode_step_static": ([vp, vp, i32, i32, vp, i32, vp, i32, vp, vp, vp, vp, vp, vp, i32, vp], i32),
     }
     for name, (args, res) in sig.items():
         fn = getattr(L, name)
@@ -339,6 +341,25 @@ def decode_step(desc: LayerDesc, weights: Sequence[LayerWeights], x, pos, max_po
                                  _ptr(pos), max_pos, _ptr(thr), _ptr(scores_out), _ptr(keep_out),
                                  ctypes.addressof(ck), ctypes.addressof(cv), _ptr(cache_len), cap, _ptr(workspace),
                                  workspace.numel(), _stream(stream)))
+
+
+def decode_static_scratch_bytes() -> int:
+    return lib().dsf_decode_static_scratch_bytes()
+
+
+def decode_step_static(desc: LayerDesc, weights: Sequence[LayerWeights], x, pos, max_pos: int, thr, cache_k,
+                       cache_v, cache_len, scores_out=None, keep_out=None, stream=None):
+    """dsf_decode_step on the library's static device scratch (no workspace, no allocation)."""
+    B = x.shape[0]
+    L = len(weights)
+    cap = cache_k[0].shape[2] if L else 1
+    arr = (LayerWeights * max(L, 1))(*weights)
+    ck, cv = _ptr_array(cache_k), _ptr_array(cache_v)
+    _check("dsf_decode_step_static",
+           lib().dsf_decode_step_static(ctypes.addressof(desc), ctypes.addressof(arr), L, _dtype_code(x), _ptr(x), B,
+                                        _ptr(pos), max_pos, _ptr(thr), _ptr(scores_out), _ptr(keep_out),
+                                        ctypes.addressof(ck), ctypes.addressof(cv), _ptr(cache_len), cap,
+                                        _stream(stream)))
 
 
 def stack_prefill(desc: LayerDesc, weights: Sequence[LayerWeights], ks: Sequence[int], x, cache_k, cache_v,

@@ -875,6 +875,9 @@ extern "C" int dsf_stack_forward(const dsf_layer_desc* desc, const dsf_layer_wei
 // ------------------------------------------- incremental decoding
 
 namespace {
+// Size of the static scratch array of dsf_decode_step_static.
+constexpr size_t kStaticScratchBytes = size_t(32) << 20;
+
 struct DecodePlan {
   size_t scores, keep, gate, a1, a2, q, k, v, attn, act, h, m2, rope, part, spart, counters, total;
   size_t acount, scount;  // byte offsets within the counters block (zeroed together)
@@ -1076,10 +1079,16 @@ extern "C" size_t dsf_decode_workspace_size(const dsf_layer_desc* desc, int dtyp
   return make_decode_plan(*desc, dtype, B, max_pos, cap).total;
 }
 
-extern "C" int dsf_decode_step(const dsf_layer_desc* desc, const dsf_layer_weights* weights, int L, int dtype,
-                               void* x, int B, const int32_t* pos, int max_pos, const float* thr, float* scores_out,
-                               int32_t* keep_out, void* const* cache_k, void* const* cache_v, int32_t* cache_len,
-                               int cap, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+namespace {
+// use_static: the caller passes no workspace and the step runs in the
+// device's static scratch array (dsf_decode_step_static), which get_scratch()
+// resolves after the argument checks.
+int get_scratch(void** out);
+
+int decode_step_impl(const dsf_layer_desc* desc, const dsf_layer_weights* weights, int L, int dtype, void* x, int B,
+                     const int32_t* pos, int max_pos, const float* thr, float* scores_out, int32_t* keep_out,
+                     void* const* cache_k, void* const* cache_v, int32_t* cache_len, int cap, bool use_static,
+                     void* workspace, size_t workspace_bytes, hipStream_t stream) {
   int rc = check_desc(desc);
   if (rc) return rc;
   rc = check_dtype(dtype);
@@ -1095,16 +1104,26 @@ extern "C" int dsf_decode_step(const dsf_layer_desc* desc, const dsf_layer_weigh
   rc = check_caches(cache_k, cache_v, L);
   if (rc) return rc;
   const DecodePlan plan = make_decode_plan(*desc, dtype, B, max_pos, cap);
-  DSF_CHECK(workspace_bytes >= plan.total, DSF_EWORKSPACE, "workspace needs %zu bytes, got %zu", plan.total,
-            workspace_bytes);
-  DSF_CHECK(workspace && (reinterpret_cast<uintptr_t>(workspace) & 255u) == 0, DSF_EINVAL,
-            "workspace must be non-null and 256-byte aligned");
+  if (use_static) {
+    DSF_CHECK(plan.total <= kStaticScratchBytes, DSF_EWORKSPACE,
+              "this step needs %zu bytes of scratch, above the static scratch of %zu bytes (use dsf_decode_step "
+              "with a workspace)", plan.total, kStaticScratchBytes);
+  } else {
+    DSF_CHECK(workspace_bytes >= plan.total, DSF_EWORKSPACE, "workspace needs %zu bytes, got %zu", plan.total,
+              workspace_bytes);
+    DSF_CHECK(workspace && (reinterpret_cast<uintptr_t>(workspace) & 255u) == 0, DSF_EINVAL,
+              "workspace must be non-null and 256-byte aligned");
+  }
   for (int l = 0; l < L; ++l) {
     rc = check_weights(*desc, &weights[l], l);
     if (rc) return rc;
   }
   rc = check_device();
   if (rc) return rc;
+  if (use_static) {
+    rc = get_scratch(&workspace);
+    if (rc) return rc;
+  }
   DecCtx c{desc, dtype, B, max_pos, cap, (char*)workspace, plan, stream};
   DSF_HIP(launch_rope_table(dat<float>(c, plan.rope), max_pos, desc->rotary_dims, desc->rope_theta, stream));
   DSF_HIP(launch_zero_u32(dat<uint32_t>(c, plan.counters), plan.ncounters, stream));
@@ -1115,6 +1134,51 @@ extern "C" int dsf_decode_step(const dsf_layer_desc* desc, const dsf_layer_weigh
     if (rc) return rc;
   }
   return DSF_OK;
+}
+
+// Static scratch of dsf_decode_step_static: one copy per device, loaded with
+// the library's code object and held until the process ends. In host code
+// `scratch` names a host-side stand-in, not device memory: its device address
+// comes from hipGetSymbolAddress, once per device with that device current,
+// and only that address is handed to kernels.
+__device__ __align__(256) char scratch[kStaticScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+int get_scratch(void** out) {
+  int dev = 0;
+  DSF_HIP(hipGetDevice(&dev));
+  DSF_CHECK(dev >= 0 && dev < kMaxDevices, DSF_EUNSUPPORTED, "device %d beyond the %d supported", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    DSF_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    DSF_CHECK(p && (reinterpret_cast<uintptr_t>(p) & 255u) == 0, DSF_EHIP, "static scratch has no usable address");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return DSF_OK;
+}
+}  // namespace
+
+extern "C" int dsf_decode_step(const dsf_layer_desc* desc, const dsf_layer_weights* weights, int L, int dtype,
+                               void* x, int B, const int32_t* pos, int max_pos, const float* thr, float* scores_out,
+                               int32_t* keep_out, void* const* cache_k, void* const* cache_v, int32_t* cache_len,
+                               int cap, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  return decode_step_impl(desc, weights, L, dtype, x, B, pos, max_pos, thr, scores_out, keep_out, cache_k, cache_v,
+                          cache_len, cap, false, workspace, workspace_bytes, stream);
+}
+
+extern "C" size_t dsf_decode_static_scratch_bytes(void) { return kStaticScratchBytes; }
+
+extern "C" int dsf_decode_step_static(const dsf_layer_desc* desc, const dsf_layer_weights* weights, int L,
+                                      int dtype, void* x, int B, const int32_t* pos, int max_pos, const float* thr,
+                                      float* scores_out, int32_t* keep_out, void* const* cache_k,
+                                      void* const* cache_v, int32_t* cache_len, int cap, hipStream_t stream) {
+  return decode_step_impl(desc, weights, L, dtype, x, B, pos, max_pos, thr, scores_out, keep_out, cache_k, cache_v,
+                          cache_len, cap, true, nullptr, 0, stream);
 }
 
 extern "C" int dsf_stack_prefill(const dsf_layer_desc* desc, const dsf_layer_weights* weights, int L, int dtype,
