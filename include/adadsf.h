@@ -253,7 +253,7 @@ int dsf_attention_forward(const void* q, const void* k, const void* v, int dtype
  * batch B, sequence length T and at most k_max kept tokens per sequence
  * (k_max = T for DSF_FLAG_DENSE). with_similarity != 0 adds room to keep each
  * layer's input for the similarity statistic. For DSF_BF16 it includes a
- * fixed 32 MiB (+ 2 KiB) for the partial sums and flags of the stream-K
+ * fixed 64 MiB (+ 2 KiB) for the partial sums and flags of the stream-K
  * projection schedule, followed by 4 B bytes of per-sequence counters of the
  * routing launch (below). The contents need no initialisation; each call
  * resets what it uses, so two calls that overlap in time (on different
@@ -265,8 +265,13 @@ int dsf_attention_forward(const void* q, const void* k, const void* v, int dtype
  * indices are bitwise those of the two separate kernels; the environment
  * variable DSF_UNFUSED_ROUTING=1, read at every call, runs those instead.
  *
- * Projection schedule. Each bf16 projection GEMM runs one output tile per
- * workgroup; or, with more tiles than resident workgroups, a persistent grid
+ * Projection schedule. Each bf16 projection GEMM takes 256 x 256 output
+ * tiles when they still fill the chip for more than a round (at least 320
+ * tiles), 128 x 128 tiles otherwise; the environment variable
+ * DSF_GEMM_TILE=small or =large, read at every launch, forces one size. With
+ * 256 x 256 tiles each workgroup runs one tile. With 128 x 128 tiles each
+ * GEMM runs one output tile per workgroup; or, with more tiles than resident
+ * workgroups, a persistent grid
  * taking whole tiles (same arithmetic); or, when that would end in a short
  * last round of tiles on a long reduction, a stream-K grid (workgroups split
  * the k-iterations of the last tiles and add their partial sums in a fixed

@@ -922,39 +922,35 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g) {
   gemm_epilogue<float, kFBM, kFBN, 256, EPI>(g, stage, m0, tn, threadIdx.x);
 }
 
-// Build-time tile configuration of the LDS-DMA GEMM (DSF_GEMM_USE_DMA=0 keeps
-// every bf16 GEMM on the register-staged kernel).
+// Tile configurations of the LDS-DMA GEMM (DSF_GEMM_USE_DMA=0 keeps every
+// bf16 GEMM on the register-staged kernel). Small: 128 x 128 tiles of four
+// 64 x 64 waves, two workgroups per CU. Large: 256 x 256 tiles of eight
+// 64 x 128 waves, one workgroup per CU; per flop it loads half the tile
+// bytes from L2 and reads half the fragment bytes from LDS, which pays when
+// there are enough tiles to fill the chip (the large projections).
 #ifndef DSF_GEMM_USE_DMA
 #define DSF_GEMM_USE_DMA 1
 #endif
-#ifndef DSF_GEMM_BM
-#define DSF_GEMM_BM 128
-#endif
-#ifndef DSF_GEMM_BN
-#define DSF_GEMM_BN 128
-#endif
-#ifndef DSF_GEMM_WM
-#define DSF_GEMM_WM 64
-#endif
-#ifndef DSF_GEMM_WN
-#define DSF_GEMM_WN 64
-#endif
-#ifndef DSF_GEMM_NS
-#define DSF_GEMM_NS 2
-#endif
-#ifndef DSF_GEMM_BK
-#define DSF_GEMM_BK 64
-#endif
+struct TileSmall {
+  static constexpr int BM = 128, BN = 128, WM = 64, WN = 64, NS = 2, BK = 64;
+};
+struct TileLarge {
+  static constexpr int BM = 256, BN = 256, WM = 64, WN = 128, NS = 2, BK = 64;
+};
 
 // Stream-K partial tiles: one slot per workgroup of a persistent grid, at
-// most kSkMaxSlots workgroups (2 per CU on a 256-CU device).
+// most kSkMaxSlots workgroups (2 per CU on a 256-CU device with small tiles,
+// 1 with large tiles).
 constexpr int kSkMaxSlots = 512;
 constexpr int kSkMinIters = 8;  // mean k-iterations per workgroup below which one tile per workgroup is kept
 constexpr int kSkMinK = 32;    // k-iterations per tile below which the partial sums cost more than they save
 constexpr int kGroupM = 4;      // tile rows per band of the grouped tile order
 constexpr int kGroupMinCols = 8;  // below this many tile columns row-major order is already compact
+constexpr size_t kSkPartBytes = size_t(kSkMaxSlots) / 2 * TileLarge::BM * TileLarge::BN * sizeof(float);
+static_assert(kSkPartBytes >= size_t(kSkMaxSlots) * TileSmall::BM * TileSmall::BN * sizeof(float),
+              "partial-tile slots of the small tiles");
 
-size_t gemm_partial_bytes() { return size_t(kSkMaxSlots) * DSF_GEMM_BM * DSF_GEMM_BN * sizeof(float); }
+size_t gemm_partial_bytes() { return kSkPartBytes; }
 int gemm_flag_count() { return kSkMaxSlots; }
 
 // Polls of a stream-K flag before a finisher gives up (2^22, each followed
@@ -1032,9 +1028,10 @@ static Schedule choose_schedule(int nt, int nk, int slots) {
 // The DMA kernels address each operand through a buffer resource with a
 // 32-bit byte range and 32-bit offsets: every operand, padded to whole tiles,
 // must stay below 4 GiB.
+template <class TC>
 static bool dma_addressable(const GemmArgs& g, int rows_b) {
   const int64_t lim = (int64_t(1) << 32) - 1024;
-  const int64_t mp = int64_t(g.M + DSF_GEMM_BM), np = int64_t(rows_b + DSF_GEMM_BN);
+  const int64_t mp = int64_t(g.M + TC::BM), np = int64_t(rows_b + TC::BN);
   return mp * g.lda * 2 < lim && (!g.a2 || mp * g.lda2 * 2 < lim) && np * g.ldb * 2 < lim &&
          (!g.b2 || np * g.ldb2 * 2 < lim);
 }
@@ -1206,32 +1203,47 @@ static void skinny_split(int ntn, int K, int* splits, int* kc) {
   *splits = (K + c - 1) / c;
 }
 
-template <int EPI>
-static void launch_gemm_t(const GemmArgs& g, hipStream_t s) {
-  if (g.dtype == DSF_BF16 && g.M <= kSkinnyRows && g.spart && g.scount && g.K % 32 == 0 && g.K1 % 32 == 0 &&
-      g.lda % 8 == 0 && g.ldb % 8 == 0 && (!g.a2 || g.lda2 % 8 == 0) && (!g.b2 || g.ldb2 % 8 == 0)) {
-    const int ntn = EPI == EPI_SWIGLU ? g.f / (kSkinnyBN / 2) : (g.N + kSkinnyBN - 1) / kSkinnyBN;
-    if (ntn <= kSkinnyCounters && (EPI != EPI_SWIGLU || g.f % (kSkinnyBN / 2) == 0)) {
-      int splits = 1, kc = g.K;
-      skinny_split(ntn, g.K, &splits, &kc);
-      launch_timed(gemm_skinny_kernel<EPI>, dim3(ntn * splits), dim3(256), s, g, splits, kc);
-      return;
-    }
-  }
+// Large tiles when the grid of 256 x 256 tiles still fills the chip for more
+// than a round (at least kLargeMinTiles tiles), and the SwiGLU units split
+// into whole 128-unit tiles; small tiles otherwise. Measured on one layer of
+// each workload: the large tiles win on every Qwen2.5-7B projection (gate/up
+// 0.38 -> 0.47 of peak, down 0.32 -> 0.46), on the NeoX-1.4B QKV and up, and
+// on the NeoX-160M QKV; the small ones on the 768- to 2048-wide down
+// projections, whose grids of large tiles cover the chip once or less.
+// DSF_GEMM_TILE=small|large (read at every launch) forces one of them.
+constexpr int kLargeMinTiles = 320;
 
-  if (DSF_GEMM_USE_DMA && g.dtype == DSF_BF16 && g.K % DSF_GEMM_BK == 0 && g.K1 % DSF_GEMM_BK == 0 &&
-      dma_addressable(g, EPI == EPI_SWIGLU ? 2 * g.f : g.N)) {
-    constexpr int BM = DSF_GEMM_BM, BN = DSF_GEMM_BN, WM = DSF_GEMM_WM, WN = DSF_GEMM_WN;
-    constexpr int NS = DSF_GEMM_NS, BK = DSF_GEMM_BK;
+template <int EPI>
+static bool use_large_tiles(const GemmArgs& g) {
+  if (EPI == EPI_SWIGLU && g.f % (TileLarge::BN / 2) != 0) return false;
+  const char* e = getenv("DSF_GEMM_TILE");
+  if (e && !strcmp(e, "small")) return false;
+  if (e && !strcmp(e, "large")) return true;
+  const int64_t ntm = (g.M + TileLarge::BM - 1) / TileLarge::BM;
+  const int64_t ntn = EPI == EPI_SWIGLU ? g.f / (TileLarge::BN / 2) : (g.N + TileLarge::BN - 1) / TileLarge::BN;
+  return ntm * ntn >= kLargeMinTiles;
+}
+
+template <int EPI, class TC>
+static void launch_dma(const GemmArgs& g, hipStream_t s) {
+  {
+    constexpr int BM = TC::BM, BN = TC::BN, WM = TC::WM, WN = TC::WN, NS = TC::NS, BK = TC::BK;
     using Cfg = DmaCfg<BM, BN, WM, WN, NS, BK>;
+    // partial-tile slots the workspace holds for this tile size
+    constexpr int kPartSlots = int(kSkPartBytes / (size_t(BM) * BN * sizeof(float)));
     const int ntn = EPI == EPI_SWIGLU ? g.f / (BN / 2) : (g.N + BN - 1) / BN;
     GemmArgs ga = g;
     ga.ntm = (g.M + BM - 1) / BM;
     ga.px = 0;
-    if (g.part && g.flags) {
+    // Persistent and stream-K grids only with small tiles: the large tiles'
+    // grids run many rounds (a short last round costs a few percent), and the
+    // stream-K kernel's partial-sum hand-over does not fit their register
+    // budget beside 128 accumulators per lane.
+    if constexpr (BM == TileSmall::BM && BN == TileSmall::BN) if (g.part && g.flags) {
       auto fn = gemm_bf16_sk_kernel<EPI, BM, BN, WM, WN, NS, BK>;
-      const Schedule sch = choose_schedule(ntn * ga.ntm, g.K / BK,
-                                           resident_slots<std::integral_constant<int, EPI>>((const void*)fn, Cfg::kThreads));
+      const int slots = std::min(kPartSlots, resident_slots<std::integral_constant<int, EPI * 2 + (BM > 128)>>(
+                                                 (const void*)fn, Cfg::kThreads));
+      const Schedule sch = choose_schedule(ntn * ga.ntm, g.K / BK, slots);
       ga.px = sch.px;
       ga.split = sch.split;
       ga.spin_limit = spin_limit();
@@ -1250,10 +1262,37 @@ static void launch_gemm_t(const GemmArgs& g, hipStream_t s) {
     // it measured more L2 misses on the 768-wide down projection), keeps
     // row-major order.
     auto fn = gemm_bf16_dma_kernel<EPI, BM, BN, WM, WN, NS, BK>;
-    const int slots = resident_slots<std::integral_constant<int, 16 + EPI>>((const void*)fn, Cfg::kThreads);
+    const int slots = resident_slots<std::integral_constant<int, 32 + EPI * 2 + (BM > 128)>>((const void*)fn, Cfg::kThreads);
     ga.group_m = ntn * ga.ntm > slots && ntn >= kGroupMinCols ? kGroupM : 0;
     launch_timed(fn, dim3(ntn * ga.ntm), dim3(Cfg::kThreads), s, ga);
-  } else if (g.dtype == DSF_BF16) {
+  }
+}
+
+template <int EPI>
+static void launch_gemm_t(const GemmArgs& g, hipStream_t s) {
+  if (g.dtype == DSF_BF16 && g.M <= kSkinnyRows && g.spart && g.scount && g.K % 32 == 0 && g.K1 % 32 == 0 &&
+      g.lda % 8 == 0 && g.ldb % 8 == 0 && (!g.a2 || g.lda2 % 8 == 0) && (!g.b2 || g.ldb2 % 8 == 0)) {
+    const int ntn = EPI == EPI_SWIGLU ? g.f / (kSkinnyBN / 2) : (g.N + kSkinnyBN - 1) / kSkinnyBN;
+    if (ntn <= kSkinnyCounters && (EPI != EPI_SWIGLU || g.f % (kSkinnyBN / 2) == 0)) {
+      int splits = 1, kc = g.K;
+      skinny_split(ntn, g.K, &splits, &kc);
+      launch_timed(gemm_skinny_kernel<EPI>, dim3(ntn * splits), dim3(256), s, g, splits, kc);
+      return;
+    }
+  }
+
+  if (DSF_GEMM_USE_DMA && g.dtype == DSF_BF16 && g.K % 64 == 0 && g.K1 % 64 == 0) {
+    const int rows_b = EPI == EPI_SWIGLU ? 2 * g.f : g.N;
+    if (use_large_tiles<EPI>(g) && dma_addressable<TileLarge>(g, rows_b)) {
+      launch_dma<EPI, TileLarge>(g, s);
+      return;
+    }
+    if (dma_addressable<TileSmall>(g, rows_b)) {
+      launch_dma<EPI, TileSmall>(g, s);
+      return;
+    }
+  }
+  if (g.dtype == DSF_BF16) {
     const int ntn = EPI == EPI_SWIGLU ? g.f / (kBN / 2) : (g.N + kBN - 1) / kBN;
     launch_timed(gemm_bf16_kernel<EPI>, dim3(ntn, (g.M + kBM - 1) / kBM), dim3(kThreads), s, g);
   } else {

@@ -134,3 +134,46 @@ def test_streamk_wait_timeout_is_reported(dev, monkeypatch, name, k):
     # the same stack call clears the word at its start
     P.stack_forward(make_desc(w), [dl.weights], [k], x.to(dev), ws)
     assert P.workspace_status(ws) == 0
+
+
+@pytest.mark.parametrize("name,k", CASES)
+def test_large_tiles_match_oracle(dev, monkeypatch, name, k):
+    """256 x 256 tiles (eight 64 x 128 waves) forced onto the small shapes:
+    every tile is ragged in M, most in N, and the SwiGLU grids hold whole
+    128-unit tiles; the layer must match the oracle and repeat bitwise, and
+    agree with the 128 x 128 tiles within tolerance."""
+    w = workload(name)
+    W = S.layer_weights(w, 0)
+    x = S.hidden_states(w)
+    monkeypatch.setenv("DSF_GEMM_TILE", "large")
+    announce(f"large tiles layer {name} k={k}")
+    y, scores, idx = run_layer(dev, w, W, x, k)
+    check_layer(w, W, x, y, scores, idx, k)
+    y2, _, _ = run_layer(dev, w, W, x, k)
+    assert torch.equal(y, y2)
+    monkeypatch.setenv("DSF_GEMM_TILE", "small")
+    monkeypatch.setenv("DSF_GEMM_SCHEDULE", "classic")
+    ys, _, idxs = run_layer(dev, w, W, x, k)
+    assert torch.equal(idx, idxs)
+    assert rel_inf(to_np(y) - to_np(x), to_np(ys) - to_np(x)) < TOL[w.dtype]
+
+
+@pytest.mark.parametrize("name", ["neox_bf16_small", "qwen_bf16_hd128"])
+def test_large_tile_stack_matches_layerwise(dev, monkeypatch, name):
+    w = workload(name).replace(n_layers=3)
+    monkeypatch.setenv("DSF_GEMM_TILE", "large")
+    announce(f"large tiles stack {name}")
+    Ws = S.stack_weights(w)
+    x = S.hidden_states(w)
+    T = w.seq
+    ks = [T // 2, T - 3, max(1, T // 5)]
+    dls = [P.DeviceLayer(W, dev) for W in Ws]
+    xd = x.to(dev)
+    ws = workspace(w, w.batch, T, max(ks), dev)
+    P.stack_forward(make_desc(w), [dl.weights for dl in dls], ks, xd, ws)
+    cur = x
+    for W, k in zip(Ws, ks):
+        y, _, _ = run_layer(dev, w, W, cur, k)
+        cur = y.cpu()
+    torch.cuda.synchronize()
+    assert torch.equal(xd.cpu(), cur)
