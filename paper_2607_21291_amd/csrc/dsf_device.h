@@ -144,6 +144,17 @@ __device__ __forceinline__ float erf_as7126(float x) {
 __device__ __forceinline__ float gelu_erf(float x) { return 0.5f * x * (1.0f + erf_as7126(x * 0.70710678118654752f)); }
 __device__ __forceinline__ float silu(float x) { return x / (1.0f + expf(-x)); }
 
+// SiLU for outputs stored as bf16: x * 1 / (1 + 2^(-x log2 e)) with the
+// hardware exp2 and reciprocal (each within about 1 ulp of fp32), a relative
+// error near 1e-6, far below a bf16 ulp of the result; three transcendental-
+// unit operations instead of expf's range reduction and an IEEE division.
+// Large negative x gives 2^(+big) = inf, a zero reciprocal and -0 (SiLU
+// tends to 0 from below); NaN propagates.
+__device__ __forceinline__ float silu_bf16(float x) {
+  const float e = __builtin_amdgcn_exp2f(-x * 1.4426950408889634f);
+  return x * __builtin_amdgcn_rcpf(1.0f + e);
+}
+
 // GELU for outputs stored as bf16: erf(x / sqrt 2) = x Q(x^2) on the clamped
 // argument (a degree-8 polynomial, gelu_poly.h), within 2e-5 in fp32, so
 // Phi(x) is within 1e-5, far below a bf16 ulp of the result. 13 VALU

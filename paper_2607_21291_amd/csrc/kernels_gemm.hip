@@ -92,7 +92,10 @@ __device__ void gemm_epilogue(const GemmArgs& g, const float* stage, int m0, int
       if (m >= g.M) break;
       float y[8];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) y[i] = silu(stage[rr * LD + cc + i]) * stage[rr * LD + H + cc + i];
+      for (int i = 0; i < 8; ++i) {
+        const float gt = stage[rr * LD + cc + i];
+        y[i] = (sizeof(T) == 2 ? silu_bf16(gt) : silu(gt)) * stage[rr * LD + H + cc + i];
+      }
       store8((T*)g.out + int64_t(m) * g.ldo + tn * H + cc, y);
     }
     return;
