@@ -617,3 +617,219 @@ def decode_stack(desc: Dict, Ws: List[Dict], x, thr=None, force=None,
                     row = round_to(out_dtype, row)
             y[b, t] = row
     return y, keep, scores
+
+
+# ---------------------------------------------------------------------------
+# Section 3.4, training side: the backward of the routed layer (the block's
+# adjoint on the kept rows, and the adjoints of the gather and the scatter)
+# ---------------------------------------------------------------------------
+
+def gelu_grad(x) -> np.ndarray:
+    """d/dx of x Phi(x): Phi(x) + x phi(x)."""
+    x = f64(x)
+    return 0.5 * (1.0 + erf(x / math.sqrt(2.0))) + x * np.exp(-0.5 * x * x) / math.sqrt(2.0 * math.pi)
+
+
+def silu_grad(x) -> np.ndarray:
+    """d/dx of x sigmoid(x): s (1 + x (1 - s)), s = sigmoid(x)."""
+    x = f64(x)
+    s = sigmoid(x)
+    return s * (1.0 + x * (1.0 - s))
+
+
+def layer_norm_backward(dy, x, w, eps: float):
+    """Adjoint of y = (x - mu) / sigma * w + b over the last axis (biased
+    variance, sigma = sqrt(var + eps)). Returns (dx, dw, db); dw and db are
+    summed over the rows."""
+    x, dy, w = f64(x), f64(dy), f64(w)
+    mu = np.mean(x, axis=-1, keepdims=True)
+    sig = np.sqrt(np.mean((x - mu) ** 2, axis=-1, keepdims=True) + eps)
+    xh = (x - mu) / sig
+    g = dy * w
+    dx = (g - np.mean(g, axis=-1, keepdims=True) - xh * np.mean(g * xh, axis=-1, keepdims=True)) / sig
+    return dx, np.sum(dy * xh, axis=0), np.sum(dy, axis=0)
+
+
+def rms_norm_backward(dy, x, w, eps: float):
+    """Adjoint of y = x / r * w, r = sqrt(mean(x^2) + eps). Returns (dx, dw)."""
+    x, dy, w = f64(x), f64(dy), f64(w)
+    r = np.sqrt(np.mean(x * x, axis=-1, keepdims=True) + eps)
+    xh = x / r
+    g = dy * w
+    dx = (g - xh * np.mean(g * xh, axis=-1, keepdims=True)) / r
+    return dx, np.sum(dy * xh, axis=0)
+
+
+def rope_backward(dout, pos, rotary_dims: int, theta: float) -> np.ndarray:
+    """Adjoint of rope(): each pair (i, i + R/2) was rotated by the angle
+    pos * theta^(-2i/R), so its gradient is rotated back by the same angle."""
+    d = f64(dout)
+    R = rotary_dims
+    half = R // 2
+    inv_freq = theta ** (-(2.0 * np.arange(half)) / R)
+    ang = np.asarray(pos, dtype=np.float64)[:, None] * inv_freq[None, :]
+    cos = np.cos(ang)[:, None, :]
+    sin = np.sin(ang)[:, None, :]
+    out = d.copy()
+    d1 = d[..., :half]
+    d2 = d[..., half:R]
+    out[..., :half] = d1 * cos + d2 * sin
+    out[..., half:R] = d2 * cos - d1 * sin
+    return out
+
+
+def causal_attention_backward(q, k, v, dout):
+    """Adjoint of causal_attention(q, k, v) (Eq. 1 over the kept tokens).
+
+    q [n, Hq, hd], k and v [n, Hkv, hd], dout [n, Hq * hd]. Per query head h
+    on kv head h // (Hq / Hkv): P = softmax(q k^T / sqrt(hd)) causal,
+    dV = P^T dO, dP = dO V^T, dS = P (dP - rowsum(P dP)), dQ = dS K / sqrt(hd),
+    dK = dS^T Q / sqrt(hd); the kv gradients add up over the query heads of a
+    group. Returns (dq, dk, dv) in the input layouts."""
+    q, k, v = f64(q), f64(k), f64(v)
+    n, Hq, hd = q.shape
+    Hkv = k.shape[1]
+    group = Hq // Hkv
+    do = f64(dout).reshape(n, Hq, hd)
+    dq, dk, dv = np.zeros_like(q), np.zeros_like(k), np.zeros_like(v)
+    mask = np.triu(np.ones((n, n), dtype=bool), 1)
+    sc = 1.0 / math.sqrt(hd)
+    for h in range(Hq):
+        kh = h // group
+        s = (q[:, h, :] @ k[:, kh, :].T) * sc
+        s[mask] = -np.inf
+        p = np.exp(s - np.max(s, axis=1, keepdims=True))
+        p = p / np.sum(p, axis=1, keepdims=True)
+        dov = do[:, h, :]
+        dv[:, kh, :] += p.T @ dov
+        dp = dov @ v[:, kh, :].T
+        ds = p * (dp - np.sum(p * dp, axis=1, keepdims=True))
+        dq[:, h, :] = (ds @ k[:, kh, :]) * sc
+        dk[:, kh, :] += (ds.T @ q[:, h, :]) * sc
+    return dq, dk, dv
+
+
+def block_forward_cache(desc: Dict, W: Dict, xc, pos):
+    """block_delta with its intermediate values kept for the backward.
+    Returns (delta, cache)."""
+    xc = f64(xc)
+    n = xc.shape[0]
+    Hq, Hkv, hd = desc["n_heads"], desc["n_kv_heads"], desc["head_dim"]
+    f = desc["d_ff"]
+    eps = desc["norm_eps"]
+    neox = desc["block"] == NEOX
+
+    def linear(inp, wname, bname=None):
+        y = inp @ f64(W[wname]).T
+        b = W.get(bname) if bname else None
+        return y if b is None else y + f64(b)
+
+    c = {"xc": xc, "pos": np.asarray(pos)}
+    c["a"] = layer_norm(xc, W["norm1_w"], W["norm1_b"], eps) if neox else rms_norm(xc, W["norm1_w"], eps)
+    qkv = linear(c["a"], "w_qkv", "b_qkv")
+    q = qkv[:, :Hq * hd].reshape(n, Hq, hd)
+    k = qkv[:, Hq * hd:(Hq + Hkv) * hd].reshape(n, Hkv, hd)
+    c["v"] = qkv[:, (Hq + Hkv) * hd:].reshape(n, Hkv, hd)
+    c["q"] = rope(q, pos, desc["rotary_dims"], desc["rope_theta"])
+    c["k"] = rope(k, pos, desc["rotary_dims"], desc["rope_theta"])
+    c["attn"] = causal_attention(c["q"], c["k"], c["v"])
+    ao = linear(c["attn"], "w_o", "b_o")
+    if neox:
+        c["m"] = layer_norm(xc, W["norm2_w"], W["norm2_b"], eps)
+        c["u"] = linear(c["m"], "w_up", "b_up")
+        c["act"] = gelu(c["u"])
+    else:
+        c["h"] = xc + ao
+        c["m"] = rms_norm(c["h"], W["norm2_w"], eps)
+        c["u"] = linear(c["m"], "w_up")
+        c["act"] = silu(c["u"][:, :f]) * c["u"][:, f:]
+    mo = linear(c["act"], "w_down", "b_down")
+    return ao + mo, c
+
+
+def block_backward(desc: Dict, W: Dict, cache: Dict, ddelta):
+    """Adjoint of delta = block(xc): given ddelta = dL/d delta [n, d], returns
+    (dL/dxc through the block, dict of weight gradients) for the cache of
+    block_forward_cache. Weight gradients have the weights' layouts; the
+    entries of absent biases are None."""
+    dd = f64(ddelta)
+    Hq, Hkv, hd = desc["n_heads"], desc["n_kv_heads"], desc["head_dim"]
+    f = desc["d_ff"]
+    eps = desc["norm_eps"]
+    neox = desc["block"] == NEOX
+    c = cache
+    n = dd.shape[0]
+    g = {}
+    # FFN: mo = act W_down^T + b_down
+    dact = dd @ f64(W["w_down"])
+    g["w_down"] = dd.T @ c["act"]
+    g["b_down"] = dd.sum(axis=0) if neox else None
+    if neox:
+        du = dact * gelu_grad(c["u"])
+    else:
+        gt, up = c["u"][:, :f], c["u"][:, f:]
+        du = np.concatenate([dact * up * silu_grad(gt), dact * silu(gt)], axis=1)
+    g["w_up"] = du.T @ c["m"]
+    g["b_up"] = du.sum(axis=0) if neox else None
+    dm = du @ f64(W["w_up"])
+    if neox:
+        dx_m, g["norm2_w"], g["norm2_b"] = layer_norm_backward(dm, c["xc"], W["norm2_w"], eps)
+        dao = dd
+        dx_h = 0.0
+    else:
+        dh, g["norm2_w"] = rms_norm_backward(dm, c["h"], W["norm2_w"], eps)
+        g["norm2_b"] = None
+        dao = dd + dh
+        dx_m, dx_h = 0.0, dh
+    # attention output projection: ao = attn W_o^T + b_o
+    dattn = dao @ f64(W["w_o"])
+    g["w_o"] = dao.T @ c["attn"]
+    g["b_o"] = dao.sum(axis=0) if neox else None
+    dqr, dkr, dv = causal_attention_backward(c["q"], c["k"], c["v"], dattn)
+    dq = rope_backward(dqr, c["pos"], desc["rotary_dims"], desc["rope_theta"])
+    dk = rope_backward(dkr, c["pos"], desc["rotary_dims"], desc["rope_theta"])
+    dqkv = np.concatenate([dq.reshape(n, Hq * hd), dk.reshape(n, Hkv * hd), dv.reshape(n, Hkv * hd)], axis=1)
+    g["w_qkv"] = dqkv.T @ c["a"]
+    g["b_qkv"] = dqkv.sum(axis=0)
+    da = dqkv @ f64(W["w_qkv"])
+    if neox:
+        dx_a, g["norm1_w"], g["norm1_b"] = layer_norm_backward(da, c["xc"], W["norm1_w"], eps)
+    else:
+        dx_a, g["norm1_w"] = rms_norm_backward(da, c["xc"], W["norm1_w"], eps)
+        g["norm1_b"] = None
+    return dx_a + dx_m + dx_h, g
+
+
+GRAD_NAMES = ["w_qkv", "b_qkv", "w_o", "b_o", "w_up", "b_up", "w_down", "b_down",
+              "norm1_w", "norm1_b", "norm2_w", "norm2_b"]
+
+
+def routed_layer_backward(desc: Dict, W: Dict, x, dy, idx, gate: bool = False) -> Dict:
+    """Backward of routed_layer(desc, W, x, k, idx=idx, gate=gate).
+
+    The kept rows xc = x[b, idx[b]] produce y = xc + g delta (g = 1, or
+    sigmoid of the router score with gate); skipped rows pass through, so
+    dx = dy there. At a kept row dx = dy + (dL/dxc through delta), with
+    dL/d delta = g dy. Weight gradients are summed over the sequences. The
+    router's share (through the gated scores) is not included: it is
+    gate_score_grad followed by router_backward.
+    Returns {"dx": [B, T, d], "grads": {name: array or None}}.
+    """
+    x, dy = f64(x), f64(dy)
+    idx = np.asarray(idx, dtype=np.int64)
+    B = x.shape[0]
+    dx = dy.copy()
+    tot = {name: None for name in GRAD_NAMES}
+    scores = router_scores(x, W["router_w1"], W["router_b1"], W["router_w2"], W.get("router_b2", 0.0))
+    for b in range(B):
+        p = idx[b]
+        if p.size == 0:
+            continue
+        _, cache = block_forward_cache(desc, W, x[b, p], p)
+        g = sigmoid(scores[b, p])[:, None] if gate else 1.0
+        dxc, grads = block_backward(desc, W, cache, g * dy[b, p])
+        dx[b, p] = dy[b, p] + dxc
+        for name, val in grads.items():
+            if val is not None:
+                tot[name] = val if tot[name] is None else tot[name] + val
+    return {"dx": dx, "grads": tot}
