@@ -333,6 +333,54 @@ int dsf_stack_forward(const dsf_layer_desc* desc, const dsf_layer_weights* weigh
                       double* sim_accum, void* workspace, size_t workspace_bytes,
                       hipStream_t stream);
 
+/* ------------------------- backward of the routed layer (Section 3.4) */
+
+/* Gradients of one layer's weights, device fp32 in the weights' layouts
+ * ([out, in] matrices, vectors as they are). A null entry is not computed;
+ * the entries of weights the block template lacks (Qwen: b_o, b_up, b_down,
+ * norm1_b, norm2_b) are ignored. Every computed gradient is written, not
+ * accumulated. */
+typedef struct dsf_layer_grads {
+  float* w_qkv;
+  float* b_qkv;
+  float* w_o;
+  float* b_o;
+  float* w_up;
+  float* b_up;
+  float* w_down;
+  float* b_down;
+  float* norm1_w;
+  float* norm1_b;
+  float* norm2_w;
+  float* norm2_b;
+} dsf_layer_grads;
+
+/* Workspace bytes of dsf_sparse_block_backward (0 on a bad argument or for
+ * dtype DSF_F32, which the backward does not provide). */
+size_t dsf_backward_workspace_size(const dsf_layer_desc* desc, int dtype, int B, int T, int k);
+
+/* Backward of one routed layer (the training side of Section 3.4): given the
+ * layer's input x [B, T, d], its kept positions idx [B, k] (as the forward
+ * chose them: ascending, distinct, in [0, T)) and the gradient dy [B, T, d]
+ * of the loss at the layer's output, writes
+ *   dx [B, T, d]: dy at skipped rows; at kept rows dy + the gradient through
+ *                 the block's update (the residual path carries dy);
+ *   grads: the gradients of the block's weights.
+ * With DSF_FLAG_GATE the forward was the gated layer, kept rows
+ * x + sigmoid(s) delta with s = scores [B, T] (the router's output), and the
+ * update's gradient is sigmoid(s) dy; the router's own share (through s) is
+ * dsf_gate_score_grad followed by dsf_router_backward, which adds into dx.
+ * The block's activations on the kept rows are recomputed from x (with the
+ * forward's kernels) rather than kept by the forward. bf16 only
+ * (DSF_EUNSUPPORTED for DSF_F32); fp32 accumulation, deterministic. k == 0
+ * copies dy into dx and leaves the gradients unwritten. Errors: DSF_EINVAL for
+ * null or misaligned pointers and bad sizes, DSF_EWORKSPACE for a short
+ * workspace. */
+int dsf_sparse_block_backward(const dsf_layer_desc* desc, const dsf_layer_weights* weights, int dtype,
+                              const void* x, const void* dy, int B, int T, int k, const int32_t* idx,
+                              const float* scores, int flags, void* dx, const dsf_layer_grads* grads,
+                              void* workspace, size_t workspace_bytes, hipStream_t stream);
+
 /* ---------------------- incremental decoding with kept-token KV caches */
 
 /* The paper treats the prefill only. Per-sequence Top-K (Section 3.4) needs

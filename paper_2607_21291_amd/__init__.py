@@ -11,5 +11,6 @@ from ._binding import (  # noqa: F401
     attention_forward, kl_align, gate_score_grad, gather_rows, k_from_retention, last_error, lib,
     make_desc, retention_from_similarity, router_backward, router_backward_workspace_size, router_score, scatter_residual, sim_finalize, sim_stats, sim_workspace_size,
     sparse_block_forward, stack_forward, timing_enable, timing_read, topk_select, version, workspace_size,
-    workspace_status, WS_STATUS_SK_TIMEOUT,
+    workspace_status, WS_STATUS_SK_TIMEOUT, backward_workspace_size, sparse_block_backward, GRAD_FIELDS,
+    LayerGrads,
 )

@@ -36,6 +36,7 @@ EXPORTS = [
     "dsf_align_workspace_size", "dsf_align_hidden", "dsf_kl_align", "dsf_align_stack_workspace_size",
     "dsf_align_stack_forward", "dsf_decode_workspace_size", "dsf_decode_step", "dsf_stack_prefill",
     "dsf_workspace_status", "dsf_decode_static_scratch_bytes", "dsf_decode_step_static",
+    "dsf_backward_workspace_size", "dsf_sparse_block_backward",
 ]
 WS_STATUS_SK_TIMEOUT = 1
 
@@ -55,6 +56,14 @@ class LayerDesc(ctypes.Structure):
 
 _WEIGHT_FIELDS = ["router_w1", "router_b1", "router_w2", "router_b2", "reserved", "norm1_w", "norm1_b",
                   "norm2_w", "norm2_b", "w_qkv", "b_qkv", "w_o", "b_o", "w_up", "b_up", "w_down", "b_down"]
+
+
+GRAD_FIELDS = ["w_qkv", "b_qkv", "w_o", "b_o", "w_up", "b_up", "w_down", "b_down", "norm1_w", "norm1_b",
+               "norm2_w", "norm2_b"]
+
+
+class LayerGrads(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in GRAD_FIELDS]
 
 
 class LayerWeights(ctypes.Structure):
@@ -107,6 +116,8 @@ def lib() -> ctypes.CDLL:
         "dsf_decode_step": ([vp, vp, i32, i32, vp, i32, vp, i32, vp, vp, vp, vp, vp, vp, i32, vp, sz, vp], i32),
         "dsf_stack_prefill": ([vp, vp, i32, i32, vp, vp, i32, i32, vp, vp, vp, i32, vp, vp, sz, vp], i32),
         "dsf_decode_static_scratch_bytes": ([], sz),
+        "dsf_backward_workspace_size": ([vp, i32, i32, i32, i32], sz),
+        "dsf_sparse_block_backward": ([vp, vp, i32, vp, vp, i32, i32, i32, vp, vp, i32, vp, vp, vp, sz, vp], i32),
         "dsf_decode_step_static": ([vp, vp, i32, i32, vp, i32, vp, i32, vp, vp, vp, vp, vp, vp, i32, vp], i32),
     }
     for name, (args, res) in sig.items():
@@ -256,6 +267,23 @@ def workspace_status(workspace, stream=None) -> int:
     out = ctypes.c_uint32(0)
     _check("dsf_workspace_status", lib().dsf_workspace_status(_ptr(workspace), ctypes.byref(out), _stream(stream)))
     return int(out.value)
+
+
+def backward_workspace_size(desc: LayerDesc, dtype: int, B: int, T: int, k: int) -> int:
+    return lib().dsf_backward_workspace_size(ctypes.addressof(desc), dtype, B, T, k)
+
+
+def sparse_block_backward(desc: LayerDesc, weights: LayerWeights, x, dy, idx, dx, grads: dict, workspace,
+                          scores=None, flags: int = 0, stream=None):
+    """grads: name -> fp32 device tensor (or None) for the names in GRAD_FIELDS."""
+    B, T, _ = x.shape
+    k = idx.shape[1] if idx is not None else 0
+    gs = LayerGrads(*[_ptr(grads.get(n)) for n in GRAD_FIELDS])
+    _check("dsf_sparse_block_backward",
+           lib().dsf_sparse_block_backward(ctypes.addressof(desc), ctypes.addressof(weights), _dtype_code(x),
+                                           _ptr(x), _ptr(dy), B, T, k, _ptr(idx), _ptr(scores), flags, _ptr(dx),
+                                           ctypes.addressof(gs), _ptr(workspace), workspace.numel(),
+                                           _stream(stream)))
 
 
 def sparse_block_forward(desc: LayerDesc, weights: LayerWeights, x, k: int, workspace, flags: int = 0,

@@ -18,11 +18,12 @@ BUILD = os.path.join(ROOT, "_build", "adadsf")
 LIB = os.path.join(PKG, "libadadsf.so")
 
 SOURCES = ["api.hip", "kernels_misc.hip", "kernels_router.hip", "kernels_align.hip", "kernels_gemm.hip",
-           "kernels_attn.hip", "kernels_decode.hip"]
+           "kernels_attn.hip", "kernels_decode.hip", "kernels_bwd.hip"]
 # per-source extra flags: attention keeps its MFMA accumulators in ordinary
 # VGPRs, so the softmax reads scores and rescales outputs without AGPR moves
 EXTRA = {"kernels_attn.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
-         "kernels_gemm.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+         "kernels_gemm.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+         "kernels_bwd.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
 ARCH = "gfx950"
 CFLAGS = [

@@ -3,6 +3,7 @@
 // retention allocation (Eqs. 5-8), and per-launch event timing.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -1316,5 +1317,264 @@ extern "C" int dsf_align_stack_forward(const dsf_layer_desc* desc, const dsf_lay
     DSF_HIP(launch_align_hidden(dtype, x_sparse, x_dense, int64_t(B) * T, desc->d_model, nullptr,
                                 at<double>(c, plan.alignpart), hid_accum + l, stream));
   }
+  return DSF_OK;
+}
+
+// ------------------------------ backward of the routed layer (Sec. 3.4)
+
+namespace {
+struct BwdPlan {
+  size_t rope, xc, a1, a2, h, m2, q, k, v, attn, u, dd, du, dm, dao, dattn, dqf, dkf, dvf, lse, dvec, dqkv, da, acc;
+  size_t mean1, rstd1, mean2, rstd2, wdT, wuT, woT, wqT, tdd, tact, tdu, tm, tdao, tattn, tdqkv, ta1, part, total;
+  int Np, fup, dqkv_cols;
+};
+
+BwdPlan make_bwd_plan(const dsf_layer_desc& D, int B, int T, int k) {
+  const size_t N = size_t(B) * k, d = D.d_model, dq = size_t(D.n_heads) * D.head_dim,
+               dkv = size_t(D.n_kv_heads) * D.head_dim, f = D.d_ff;
+  const bool qwen = D.block == DSF_BLOCK_QWEN_SEQ;
+  BwdPlan p{};
+  p.Np = int((N + 63) / 64 * 64);
+  p.fup = int(qwen ? 2 * f : f);
+  p.dqkv_cols = int(dq + 2 * dkv);
+  const size_t Np = size_t(p.Np), fup = size_t(p.fup), cq = size_t(p.dqkv_cols);
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t o = off;
+    off += up256(bytes > 0 ? bytes : 1);
+    return o;
+  };
+  p.rope = take(4 * size_t(T) * D.rotary_dims);
+  p.xc = take(2 * N * d);
+  p.a1 = take(2 * N * d);
+  p.a2 = qwen ? 0 : take(2 * N * d);
+  p.h = qwen ? take(2 * N * d) : 0;
+  p.m2 = qwen ? take(2 * N * d) : 0;
+  p.q = take(2 * N * dq);
+  p.k = take(2 * N * dkv);
+  p.v = take(2 * N * dkv);
+  p.attn = take(2 * N * dq);
+  p.u = take(2 * N * fup);
+  p.dd = take(2 * N * d);
+  p.du = take(2 * N * fup);
+  p.dm = take(2 * N * d);
+  p.dao = qwen ? take(2 * N * d) : p.dd;
+  p.dattn = take(2 * N * dq);
+  p.dqf = take(4 * N * dq);
+  p.dkf = take(4 * N * dkv);
+  p.dvf = take(4 * N * dkv);
+  p.lse = take(4 * size_t(B) * D.n_heads * k);
+  p.dvec = take(4 * size_t(B) * D.n_heads * k);
+  p.dqkv = take(2 * N * cq);
+  p.da = take(2 * N * d);
+  p.acc = take(4 * N * d);
+  p.mean1 = take(4 * N);
+  p.rstd1 = take(4 * N);
+  p.mean2 = take(4 * N);
+  p.rstd2 = take(4 * N);
+  p.wdT = take(2 * f * d);
+  p.wuT = take(2 * d * fup);
+  p.woT = take(2 * dq * d);
+  p.wqT = take(2 * d * cq);
+  p.tdd = take(2 * d * Np);
+  p.tact = take(2 * f * Np);
+  p.tdu = take(2 * fup * Np);
+  p.tm = take(2 * d * Np);
+  p.tdao = qwen ? take(2 * d * Np) : p.tdd;
+  p.tattn = take(2 * dq * Np);
+  p.tdqkv = take(2 * cq * Np);
+  p.ta1 = take(2 * d * Np);
+  const size_t cmax = std::max(std::max(d, fup), cq);
+  p.part = take(4 * size_t(colsum_chunks(int(N))) * cmax);
+  p.total = off;
+  return p;
+}
+
+int check_bwd(const dsf_layer_desc* desc, int dtype, int B, int T, int k) {
+  int rc = check_desc(desc);
+  if (rc) return rc;
+  DSF_CHECK(dtype == DSF_BF16, DSF_EUNSUPPORTED, "the layer backward is provided for DSF_BF16 only");
+  DSF_CHECK(B >= 0 && T >= 0 && k >= 0 && k <= T, DSF_EINVAL, "need B, T >= 0 and k in [0, T]");
+  DSF_CHECK(int64_t(B) * T < (int64_t(1) << 31) / 8, DSF_EINVAL, "B * T too large");
+  return DSF_OK;
+}
+
+// C[M, N] = A[M, K] . Bm[N, K]^T with one of the backward epilogues (plain
+// token rows: no positions, one "sequence" of M rows).
+int bwd_gemm(int epi, int M, int N, int K, const void* A, int lda, const void* Bm, int ldb, void* out, int ldo,
+             const void* bias, const void* res, int f, hipStream_t s) {
+  if (M == 0 || N == 0) return DSF_OK;
+  GemmArgs g{};
+  g.dtype = DSF_BF16;
+  g.M = M; g.N = N; g.K = K; g.K1 = K;
+  g.a = A; g.lda = lda; g.b = Bm; g.ldb = ldb;
+  g.epi = epi; g.bias = bias; g.res = res; g.f = f;
+  g.out = out; g.ldo = ldo;
+  g.B = 1; g.kk = M; g.T = M;
+  DSF_HIP(launch_gemm(g, s));
+  return DSF_OK;
+}
+}  // namespace
+
+extern "C" size_t dsf_backward_workspace_size(const dsf_layer_desc* desc, int dtype, int B, int T, int k) {
+  if (check_bwd(desc, dtype, B, T, k)) return 0;
+  return make_bwd_plan(*desc, B, T, k).total;
+}
+
+extern "C" int dsf_sparse_block_backward(const dsf_layer_desc* desc, const dsf_layer_weights* weights, int dtype,
+                                         const void* x, const void* dy, int B, int T, int k, const int32_t* idx,
+                                         const float* scores, int flags, void* dx, const dsf_layer_grads* grads,
+                                         void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  int rc = check_bwd(desc, dtype, B, T, k);
+  if (rc) return rc;
+  DSF_CHECK((flags & ~DSF_FLAG_GATE) == 0, DSF_EINVAL, "only DSF_FLAG_GATE is accepted (flags 0x%x)", flags);
+  const bool gate = flags & DSF_FLAG_GATE;
+  if (B == 0 || T == 0) return DSF_OK;
+  DSF_CHECK(x && dy && dx, DSF_EINVAL, "null x, dy or dx");
+  DSF_CHECK(aligned16(x) && aligned16(dy) && aligned16(dx), DSF_EINVAL, "x, dy and dx must be 16-byte aligned");
+  DSF_CHECK(k == 0 || idx, DSF_EINVAL, "null idx");
+  DSF_CHECK(!gate || scores, DSF_EINVAL, "DSF_FLAG_GATE needs the router scores");
+  rc = check_weights(*desc, weights, 0);
+  if (rc) return rc;
+  static const dsf_layer_grads kNone{};
+  const dsf_layer_grads& G = grads ? *grads : kNone;
+  const float* gp[] = {G.w_qkv, G.b_qkv, G.w_o, G.b_o, G.w_up, G.b_up, G.w_down, G.b_down,
+                       G.norm1_w, G.norm1_b, G.norm2_w, G.norm2_b};
+  for (const float* p : gp) DSF_CHECK(aligned16(p), DSF_EINVAL, "gradient buffers must be 16-byte aligned");
+  const dsf_layer_desc& D = *desc;
+  const bool qwen = D.block == DSF_BLOCK_QWEN_SEQ;
+  const BwdPlan p = make_bwd_plan(D, B, T, k);
+  DSF_CHECK(workspace_bytes >= p.total, DSF_EWORKSPACE, "workspace needs %zu bytes, got %zu", p.total,
+            workspace_bytes);
+  DSF_CHECK(workspace && (reinterpret_cast<uintptr_t>(workspace) & 255u) == 0, DSF_EINVAL,
+            "workspace must be non-null and 256-byte aligned");
+  rc = check_device();
+  if (rc) return rc;
+  hipStream_t s = stream;
+  const size_t xbytes = size_t(B) * T * D.d_model * 2;
+  DSF_HIP(launch_copy(dy, dx, xbytes, s));  // skipped rows: dx = dy
+  if (k == 0) return DSF_OK;                // (the weight gradients are then not written)
+  char* ws = (char*)workspace;
+  auto P = [&](size_t off) { return (void*)(ws + off); };
+  auto F = [&](size_t off) { return (float*)(ws + off); };
+  const int d = D.d_model, hd = D.head_dim, Hq = D.n_heads, Hkv = D.n_kv_heads, f = D.d_ff;
+  const int dq = Hq * hd, dkv = Hkv * hd, N = B * k, Np = p.Np, fup = p.fup, cq = p.dqkv_cols;
+
+  // ---- recompute the forward's activations of the kept rows
+  DSF_HIP(launch_rope_table(F(p.rope), T, D.rotary_dims, D.rope_theta, s));
+  DSF_HIP(launch_gather(dtype, x, B, T, d, idx, k, P(p.xc), s));
+  NormArgs na{};
+  na.dtype = dtype; na.src = P(p.xc); na.src_rows = 0; na.B = B; na.kk = k; na.d = d; na.eps = D.norm_eps;
+  na.rms = qwen; na.w1 = weights->norm1_w; na.b1 = weights->norm1_b; na.out1 = P(p.a1);
+  if (!qwen) {
+    na.w2 = weights->norm2_w; na.b2 = weights->norm2_b; na.out2 = P(p.a2);
+  }
+  DSF_HIP(launch_norm(na, s));
+  {
+    GemmArgs g{};
+    g.dtype = dtype; g.B = B; g.kk = k; g.T = T; g.idx = idx;
+    g.M = N; g.N = dq + 2 * dkv; g.K = d; g.K1 = d;
+    g.a = P(p.a1); g.lda = d; g.b = weights->w_qkv; g.ldb = d;
+    g.epi = EPI_QKV_ROPE; g.bias = weights->b_qkv;
+    g.q = P(p.q); g.k = P(p.k); g.v = P(p.v);
+    g.Hq = Hq; g.Hkv = Hkv; g.hd = hd; g.R = D.rotary_dims; g.rope = F(p.rope);
+    DSF_HIP(launch_gemm(g, s));
+  }
+  DSF_HIP(launch_attention(dtype, P(p.q), P(p.k), P(p.v), B, Hq, Hkv, k, hd, P(p.attn), s));
+  const void* mrows;  // input rows of the up projection
+  if (!qwen) {
+    mrows = P(p.a2);
+    rc = bwd_gemm(EPI_STORE, N, f, d, P(p.a2), d, weights->w_up, d, P(p.u), f, weights->b_up, nullptr, 0, s);
+    if (rc) return rc;
+  } else {
+    GemmArgs g{};  // h = x_kept + attn W_o^T
+    g.dtype = dtype; g.B = B; g.kk = k; g.T = T; g.idx = idx;
+    g.M = N; g.N = d; g.K = dq; g.K1 = dq;
+    g.a = P(p.attn); g.lda = dq; g.b = weights->w_o; g.ldb = dq;
+    g.epi = EPI_RESID_STORE; g.bias = weights->b_o;
+    g.x = const_cast<void*>(x); g.out = P(p.h); g.ldo = d;
+    DSF_HIP(launch_gemm(g, s));
+    NormArgs n2{};
+    n2.dtype = dtype; n2.src = P(p.h); n2.src_rows = 0; n2.B = B; n2.kk = k; n2.d = d; n2.eps = D.norm_eps;
+    n2.rms = 1; n2.w1 = weights->norm2_w; n2.out1 = P(p.m2);
+    DSF_HIP(launch_norm(n2, s));
+    mrows = P(p.m2);
+    rc = bwd_gemm(EPI_STORE, N, 2 * f, d, P(p.m2), d, weights->w_up, d, P(p.u), 2 * f, nullptr, nullptr, 0, s);
+    if (rc) return rc;
+  }
+
+  // ---- the adjoint: d(delta) = gate * dy at the kept rows
+  DSF_HIP(launch_gather_scale(dy, B, T, d, idx, k, gate ? scores : nullptr, P(p.dd), s));
+  // FFN down projection
+  if (G.w_down) {
+    DSF_HIP(launch_transpose(0, P(p.dd), N, d, d, P(p.tdd), Np, s));
+    DSF_HIP(launch_transpose(qwen ? 2 : 1, P(p.u), N, f, fup, P(p.tact), Np, s));
+    rc = bwd_gemm(EPI_STORE_F32, d, f, Np, P(p.tdd), Np, P(p.tact), Np, G.w_down, f, nullptr, nullptr, 0, s);
+    if (rc) return rc;
+  }
+  if (G.b_down && !qwen) DSF_HIP(launch_colsum(P(p.dd), N, d, d, nullptr, nullptr, nullptr, F(p.part), G.b_down, s));
+  DSF_HIP(launch_transpose(0, weights->w_down, d, f, f, P(p.wdT), d, s));
+  rc = bwd_gemm(qwen ? EPI_SWIGLU_BWD : EPI_GELU_BWD, N, f, d, P(p.dd), d, P(p.wdT), d, P(p.du), fup, nullptr, P(p.u),
+                f, s);
+  if (rc) return rc;
+  // FFN up projection
+  if (G.w_up) {
+    DSF_HIP(launch_transpose(0, P(p.du), N, fup, fup, P(p.tdu), Np, s));
+    DSF_HIP(launch_transpose(0, mrows, N, d, d, P(p.tm), Np, s));
+    rc = bwd_gemm(EPI_STORE_F32, fup, d, Np, P(p.tdu), Np, P(p.tm), Np, G.w_up, d, nullptr, nullptr, 0, s);
+    if (rc) return rc;
+  }
+  if (G.b_up && !qwen) DSF_HIP(launch_colsum(P(p.du), N, f, f, nullptr, nullptr, nullptr, F(p.part), G.b_up, s));
+  DSF_HIP(launch_transpose(0, weights->w_up, fup, d, d, P(p.wuT), fup, s));
+  rc = bwd_gemm(EPI_STORE, N, d, fup, P(p.du), fup, P(p.wuT), fup, P(p.dm), d, nullptr, nullptr, 0, s);
+  if (rc) return rc;
+  // second norm: NeoX's LN2 of the kept rows, Qwen's RMS2 of h = x + attention
+  if (!qwen) {
+    DSF_HIP(launch_norm_bwd(false, P(p.xc), P(p.dm), weights->norm2_w, N, d, D.norm_eps, F(p.acc), false, nullptr,
+                            nullptr, F(p.mean2), F(p.rstd2), s));
+  } else {
+    DSF_HIP(launch_norm_bwd(true, P(p.h), P(p.dm), weights->norm2_w, N, d, D.norm_eps, F(p.acc), false, P(p.dd),
+                            P(p.dao), F(p.mean2), F(p.rstd2), s));
+  }
+  if (G.norm2_w)
+    DSF_HIP(launch_colsum(P(p.dm), N, d, d, qwen ? P(p.h) : P(p.xc), qwen ? nullptr : F(p.mean2), F(p.rstd2),
+                          F(p.part), G.norm2_w, s));
+  if (G.norm2_b && !qwen) DSF_HIP(launch_colsum(P(p.dm), N, d, d, nullptr, nullptr, nullptr, F(p.part), G.norm2_b, s));
+  // attention output projection
+  if (G.w_o) {
+    if (qwen || !G.w_down) DSF_HIP(launch_transpose(0, P(p.dao), N, d, d, P(p.tdao), Np, s));
+    DSF_HIP(launch_transpose(0, P(p.attn), N, dq, dq, P(p.tattn), Np, s));
+    rc = bwd_gemm(EPI_STORE_F32, d, dq, Np, P(p.tdao), Np, P(p.tattn), Np, G.w_o, dq, nullptr, nullptr, 0, s);
+    if (rc) return rc;
+  }
+  if (G.b_o && !qwen) DSF_HIP(launch_colsum(P(p.dao), N, d, d, nullptr, nullptr, nullptr, F(p.part), G.b_o, s));
+  DSF_HIP(launch_transpose(0, weights->w_o, d, dq, dq, P(p.woT), d, s));
+  rc = bwd_gemm(EPI_STORE, N, dq, d, P(p.dao), d, P(p.woT), d, P(p.dattn), dq, nullptr, nullptr, 0, s);
+  if (rc) return rc;
+  // attention over the kept tokens, then RoPE turned back into token-major dqkv
+  DSF_HIP(launch_attention_bwd(P(p.q), P(p.k), P(p.v), P(p.attn), P(p.dattn), B, Hq, Hkv, k, hd, F(p.lse),
+                               F(p.dvec), F(p.dqf), F(p.dkf), F(p.dvf), s));
+  DSF_HIP(launch_rope_bwd(F(p.dqf), F(p.dkf), F(p.dvf), F(p.rope), idx, B, k, T, Hq, Hkv, hd, D.rotary_dims,
+                          P(p.dqkv), s));
+  // QKV projection
+  if (G.w_qkv) {
+    DSF_HIP(launch_transpose(0, P(p.dqkv), N, cq, cq, P(p.tdqkv), Np, s));
+    DSF_HIP(launch_transpose(0, P(p.a1), N, d, d, P(p.ta1), Np, s));
+    rc = bwd_gemm(EPI_STORE_F32, cq, d, Np, P(p.tdqkv), Np, P(p.ta1), Np, G.w_qkv, d, nullptr, nullptr, 0, s);
+    if (rc) return rc;
+  }
+  if (G.b_qkv) DSF_HIP(launch_colsum(P(p.dqkv), N, cq, cq, nullptr, nullptr, nullptr, F(p.part), G.b_qkv, s));
+  DSF_HIP(launch_transpose(0, weights->w_qkv, cq, d, d, P(p.wqT), cq, s));
+  rc = bwd_gemm(EPI_STORE, N, d, cq, P(p.dqkv), cq, P(p.wqT), cq, P(p.da), d, nullptr, nullptr, 0, s);
+  if (rc) return rc;
+  // first norm of the kept rows
+  DSF_HIP(launch_norm_bwd(qwen, P(p.xc), P(p.da), weights->norm1_w, N, d, D.norm_eps, F(p.acc), true, nullptr,
+                          nullptr, F(p.mean1), F(p.rstd1), s));
+  if (G.norm1_w)
+    DSF_HIP(launch_colsum(P(p.da), N, d, d, P(p.xc), qwen ? nullptr : F(p.mean1), F(p.rstd1), F(p.part), G.norm1_w,
+                          s));
+  if (G.norm1_b && !qwen) DSF_HIP(launch_colsum(P(p.da), N, d, d, nullptr, nullptr, nullptr, F(p.part), G.norm1_b, s));
+  // kept rows: dx = dy + the block's gradient (the residual path carries dy)
+  DSF_HIP(launch_scatter_grad(dy, F(p.acc), B, T, d, idx, k, dx, s));
   return DSF_OK;
 }

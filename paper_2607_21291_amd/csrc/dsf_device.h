@@ -144,6 +144,19 @@ __device__ __forceinline__ float erf_as7126(float x) {
 __device__ __forceinline__ float gelu_erf(float x) { return 0.5f * x * (1.0f + erf_as7126(x * 0.70710678118654752f)); }
 __device__ __forceinline__ float silu(float x) { return x / (1.0f + expf(-x)); }
 
+// d/dx GELU(x) = Phi(x) + x phi(x) for gradients stored as bf16: Phi from the
+// same fitted polynomial as gelu_bf16, phi from the hardware exp2.
+__device__ __forceinline__ float gelu_grad_bf16(float x) {
+  const float xc = __builtin_amdgcn_fmed3f(x, -kGeluPolyXmax, kGeluPolyXmax);
+  const float u = xc * xc;
+  float q = kGeluPolyQ[0];
+#pragma unroll
+  for (int i = 1; i < int(sizeof(kGeluPolyQ) / sizeof(float)); ++i) q = fmaf(q, u, kGeluPolyQ[i]);
+  const float cdf = fmaf(0.5f, xc * q, 0.5f);
+  const float pdf = 0.3989422804014327f * __builtin_amdgcn_exp2f(-0.5f * 1.4426950408889634f * x * x);
+  return fmaf(x, pdf, cdf);
+}
+
 // SiLU for outputs stored as bf16: x * 1 / (1 + 2^(-x log2 e)) with the
 // hardware exp2 and reciprocal (each within about 1 ulp of fp32), a relative
 // error near 1e-6, far below a bf16 ulp of the result; three transcendental-
@@ -153,6 +166,14 @@ __device__ __forceinline__ float silu(float x) { return x / (1.0f + expf(-x)); }
 __device__ __forceinline__ float silu_bf16(float x) {
   const float e = __builtin_amdgcn_exp2f(-x * 1.4426950408889634f);
   return x * __builtin_amdgcn_rcpf(1.0f + e);
+}
+// sigmoid(x) and d/dx SiLU(x) = s (1 + x (1 - s)) with the same primitives
+__device__ __forceinline__ float sigmoid_bf16(float x) {
+  return __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-x * 1.4426950408889634f));
+}
+__device__ __forceinline__ float silu_grad_bf16(float x) {
+  const float s = sigmoid_bf16(x);
+  return s * fmaf(x, 1.0f - s, 1.0f);
 }
 
 // GELU for outputs stored as bf16: erf(x / sqrt 2) = x Q(x^2) on the clamped

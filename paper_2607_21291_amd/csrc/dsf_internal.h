@@ -117,6 +117,12 @@ enum EpiKind {
   EPI_RESID_STORE = 3,    // out[m, n] = x[b, pos, n] + C (+ bias)
   EPI_RESID_SCATTER = 4,  // x[b, pos, n] = resid + C + bias + bias2, resid = x[b, pos] or res[m]
   EPI_RESID_SCATTER_GATE = 5,  // x[b, pos, n] += sigmoid(gate[b, pos]) * (resid + C + bias + bias2 - x[b, pos])
+  // backward of the block (bf16 only; one output tile per workgroup):
+  EPI_STORE = 6,       // out[m, n] = C (+ bias), bf16
+  EPI_STORE_F32 = 7,   // out[m, n] = C, fp32 (weight gradients)
+  EPI_GELU_BWD = 8,    // out[m, n] = C * gelu'(res[m, n]) (res: the up projection's pre-activation, ld = ldo)
+  EPI_SWIGLU_BWD = 9,  // N = f; res = [gate | up] pre-activations [M, 2f] (ld = ldo = 2f):
+                       // out[m, n] = C * up * silu'(gate), out[m, f + n] = C * silu(gate)
 };
 
 struct GemmArgs {
@@ -162,6 +168,35 @@ struct GemmArgs {
   int group_m;
 };
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t s);
+
+// ---- backward of the routed layer (kernels_bwd.hip) ----
+// out[c][r] = op(in[r][c]) (op 0 copy, 1 GELU, 2 SiLU(in[r][c]) * in[r][C + c]);
+// out's leading dimension ldo >= R, columns R .. ldo - 1 written as zeros.
+hipError_t launch_transpose(int op, const void* in, int R, int C, int ldi, void* out, int ldo, hipStream_t s);
+// out[c] = sum_r a[r][c] (x null) or sum_r a[r][c] (x[r][c] - mean[r]) rstd[r]
+// (mean nullable: 0), in a fixed order; partial: colsum_chunks(R) * C floats.
+int colsum_chunks(int R);
+hipError_t launch_colsum(const void* a, int R, int C, int lda, const void* x, const float* mean, const float* rstd,
+                         float* partial, float* out, hipStream_t s);
+// out[b kk + j] = (scores ? sigmoid(scores[b, idx]) : 1) * dy[b, idx[b kk + j]]
+hipError_t launch_gather_scale(const void* dy, int B, int T, int d, const int32_t* idx, int kk, const float* scores,
+                               void* out, hipStream_t s);
+// LayerNorm (rms false) or RMSNorm adjoint of M rows: acc (fp32) = or += dx;
+// sum_out = add + dx (both nullable); mean/rstd [M] of each row kept.
+hipError_t launch_norm_bwd(bool rms, const void* x, const void* dyn, const void* w, int M, int d, float eps, float* acc,
+                           bool accumulate, const void* add, void* sum_out, float* mean, float* rstd, hipStream_t s);
+// dqkv [B kk, (Hq + 2 Hkv) hd] (bf16) from head-major fp32 dq, dk, dv; RoPE turned back.
+hipError_t launch_rope_bwd(const float* dq, const float* dk, const float* dv, const float* table, const int32_t* idx,
+                           int B, int kk, int T, int Hq, int Hkv, int hd, int R, void* out, hipStream_t s);
+// dx[b, idx] = dy[b, idx] + acc (fp32 add, one rounding)
+hipError_t launch_scatter_grad(const void* dy, const float* acc, int B, int T, int d, const int32_t* idx, int kk,
+                               void* dx, hipStream_t s);
+// causal attention backward; q, k, v head-major (RoPE applied), o and dout
+// token-major [B n, Hq hd]; lse, dvec [B, Hq, n]; dq [B, Hq, n, hd], dk and
+// dv [B, Hkv, n, hd] fp32.
+hipError_t launch_attention_bwd(const void* q, const void* k, const void* v, const void* o, const void* dout, int B,
+                                int Hq, int Hkv, int n, int hd, float* lse, float* dvec, float* dq, float* dk,
+                                float* dv, hipStream_t s);
 size_t gemm_partial_bytes();
 int gemm_flag_count();
 size_t gemm_skinny_partial_bytes();

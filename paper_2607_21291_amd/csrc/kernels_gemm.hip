@@ -222,6 +222,55 @@ __device__ void gemm_epilogue(const GemmArgs& g, const float* stage, int m0, int
     }
     return;
   }
+  if constexpr (EPI == EPI_STORE_F32) {
+#pragma unroll
+    for (int q = 0; q < RPT; ++q) {
+      if (!live[q]) continue;
+      const int m = m0 + rr0 + q * RSTEP;
+      const float* row = stage + (rr0 + q * RSTEP) * LD;
+      float* dst = (float*)g.out + int64_t(m) * g.ldo + n;
+      store_vec(dst, row + cc);
+      store_vec(dst + 4, row + cc + 4);
+    }
+    return;
+  }
+  if constexpr (EPI == EPI_GELU_BWD || EPI == EPI_SWIGLU_BWD) {
+    // gradient at the activation's input from the gradient at its output (C)
+    // and the forward pre-activation(s) in res
+    Raw8<T> ra[RPT], rb[RPT];
+#pragma unroll
+    for (int q = 0; q < RPT; ++q) {
+      if (!live[q]) continue;
+      const T* aux = (const T*)g.res + int64_t(m0 + rr0 + q * RSTEP) * g.ldo + n;
+      ra[q] = load_raw8(aux);
+      if constexpr (EPI == EPI_SWIGLU_BWD) rb[q] = load_raw8(aux + g.f);
+    }
+#pragma unroll
+    for (int q = 0; q < RPT; ++q) {
+      if (!live[q]) continue;
+      const int m = m0 + rr0 + q * RSTEP;
+      const float* row = stage + (rr0 + q * RSTEP) * LD;
+      float a[8], v[8];
+      unpack8(ra[q], a);
+      T* dst = (T*)g.out + int64_t(m) * g.ldo + n;
+      if constexpr (EPI == EPI_GELU_BWD) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[i] = row[cc + i] * gelu_grad_bf16(a[i]);
+        store8(dst, v);
+      } else {
+        float up[8], w[8];
+        unpack8(rb[q], up);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          v[i] = row[cc + i] * up[i] * silu_grad_bf16(a[i]);
+          w[i] = row[cc + i] * silu_bf16(a[i]);
+        }
+        store8(dst, v);
+        store8(dst + g.f, w);
+      }
+    }
+    return;
+  }
 #pragma unroll
   for (int q = 0; q < RPT; ++q) {
     if (!live[q]) continue;
@@ -230,7 +279,9 @@ __device__ void gemm_epilogue(const GemmArgs& g, const float* stage, int m0, int
     float v[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) v[i] = row[cc + i] + bias[i];
-    if constexpr (EPI == EPI_QKV_ROPE) {
+    if constexpr (EPI == EPI_STORE) {
+      store8((T*)g.out + int64_t(m) * g.ldo + n, v);
+    } else if constexpr (EPI == EPI_QKV_ROPE) {
       // columns: Q heads, then K heads, then V heads; written head-major [B, H, kk, hd]
       T* dst = sec + ((int64_t(bq[q]) * heads + head) * g.kk + jq[q]) * g.hd + dim0;
       if (rot) {
@@ -1242,7 +1293,7 @@ static void launch_dma(const GemmArgs& g, hipStream_t s) {
     // grids run many rounds (a short last round costs a few percent), and the
     // stream-K kernel's partial-sum hand-over does not fit their register
     // budget beside 128 accumulators per lane.
-    if constexpr (BM == TileSmall::BM && BN == TileSmall::BN) if (g.part && g.flags) {
+    if constexpr (BM == TileSmall::BM && BN == TileSmall::BN && EPI < EPI_STORE) if (g.part && g.flags) {
       auto fn = gemm_bf16_sk_kernel<EPI, BM, BN, WM, WN, NS, BK>;
       const int slots = std::min(kPartSlots, resident_slots<std::integral_constant<int, EPI * 2 + (BM > 128)>>(
                                                  (const void*)fn, Cfg::kThreads));
@@ -1273,6 +1324,22 @@ static void launch_dma(const GemmArgs& g, hipStream_t s) {
 
 template <int EPI>
 static void launch_gemm_t(const GemmArgs& g, hipStream_t s) {
+  if constexpr (EPI >= EPI_STORE) {
+    // backward kinds: bf16 only, one output tile per workgroup
+    const int rows_b = g.N;
+    if (g.K % 64 == 0 && g.K1 % 64 == 0) {
+      if (use_large_tiles<EPI>(g) && dma_addressable<TileLarge>(g, rows_b)) {
+        launch_dma<EPI, TileLarge>(g, s);
+        return;
+      }
+      if (dma_addressable<TileSmall>(g, rows_b)) {
+        launch_dma<EPI, TileSmall>(g, s);
+        return;
+      }
+    }
+    launch_timed(gemm_bf16_kernel<EPI>, dim3((g.N + kBN - 1) / kBN, (g.M + kBM - 1) / kBM), dim3(kThreads), s, g);
+    return;
+  } else {
   if (g.dtype == DSF_BF16 && g.M <= kSkinnyRows && g.spart && g.scount && g.K % 32 == 0 && g.K1 % 32 == 0 &&
       g.lda % 8 == 0 && g.ldb % 8 == 0 && (!g.a2 || g.lda2 % 8 == 0) && (!g.b2 || g.ldb2 % 8 == 0)) {
     const int ntn = EPI == EPI_SWIGLU ? g.f / (kSkinnyBN / 2) : (g.N + kSkinnyBN - 1) / kSkinnyBN;
@@ -1302,6 +1369,7 @@ static void launch_gemm_t(const GemmArgs& g, hipStream_t s) {
     const int ntn = EPI == EPI_SWIGLU ? g.f / (kFBN / 2) : (g.N + kFBN - 1) / kFBN;
     launch_timed(gemm_f32_kernel<EPI>, dim3(ntn, (g.M + kFBM - 1) / kFBM), dim3(256), s, g);
   }
+  }
 }
 
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t s) {
@@ -1313,6 +1381,10 @@ hipError_t launch_gemm(const GemmArgs& g, hipStream_t s) {
     case EPI_RESID_STORE: launch_gemm_t<EPI_RESID_STORE>(g, s); break;
     case EPI_RESID_SCATTER: launch_gemm_t<EPI_RESID_SCATTER>(g, s); break;
     case EPI_RESID_SCATTER_GATE: launch_gemm_t<EPI_RESID_SCATTER_GATE>(g, s); break;
+    case EPI_STORE: launch_gemm_t<EPI_STORE>(g, s); break;
+    case EPI_STORE_F32: launch_gemm_t<EPI_STORE_F32>(g, s); break;
+    case EPI_GELU_BWD: launch_gemm_t<EPI_GELU_BWD>(g, s); break;
+    case EPI_SWIGLU_BWD: launch_gemm_t<EPI_SWIGLU_BWD>(g, s); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -251,3 +251,21 @@ def test_workspace_status_rejects_null_pointers():
     assert "null" in P.last_error()
     assert L.dsf_workspace_status(ctypes.c_void_p(256), None, None) == 1
     assert out.value == 7  # nothing written on an argument error
+
+
+def test_backward_argument_errors():
+    L = P.lib()
+    d = _desc()
+    assert L.dsf_backward_workspace_size(ctypes.addressof(d), P.F32, 2, 64, 32) == 0
+    assert L.dsf_backward_workspace_size(ctypes.addressof(d), P.BF16, 2, 64, 65) == 0
+    assert L.dsf_backward_workspace_size(ctypes.addressof(d), P.BF16, 2, 64, 32) > 0
+    w = _weights()
+    g = P.LayerGrads()
+    args = lambda dtype, x, flags, scores: (ctypes.addressof(d), ctypes.addressof(w), dtype, x, x, 2, 64, 32,
+                                            ctypes.c_void_p(256), scores, flags, x, ctypes.addressof(g),
+                                            ctypes.c_void_p(256), 1 << 30, None)
+    assert L.dsf_sparse_block_backward(*args(P.F32, ctypes.c_void_p(256), 0, None)) == 2
+    assert L.dsf_sparse_block_backward(*args(P.BF16, None, 0, None)) == 1
+    assert L.dsf_sparse_block_backward(*args(P.BF16, ctypes.c_void_p(256), P.FLAG_GATE, None)) == 1
+    assert "scores" in P.last_error()
+    assert L.dsf_sparse_block_backward(*args(P.BF16, ctypes.c_void_p(256), P.FLAG_DENSE, None)) == 1
