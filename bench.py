@@ -43,7 +43,16 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 # library's plain copy kernel of known size. A figure holds only for the
 # workload, kernel kind and GEMM source it was measured on (SHA-256 of
 # kernels_gemm.hip); for anything else `traffic` is null.
-TRAFFIC_MEASURED = []
+TRAFFIC_MEASURED = [
+    # 28-layer Qwen2.5-7B-shaped stack, B 4 x T 8192, SwiGLU gate|up launch:
+    # mean over the 112 sparse dispatches of 4 steps; FETCH_SIZE 3714118.6 KiB
+    # x 1.9998 (copy: 114698.1 KiB read for 229376 KiB copied), WRITE_SIZE
+    # 606134.0 KiB x 1.0 (equal to the bytes the launch stores). The counters
+    # count L2 misses, served by the 256 MB MALL or HBM.
+    {"workload": "qwen7b", "kind": "gemm_up", "bytes_per_launch": 8.2265e9,
+     "gemm_source_sha256": "c4443f4806376af51de4ae5b3b42d1591ff0c2b1a69efec94ec0735aeb0c414c",
+     "profile": "profiles/gemm_up_qwen7b_traffic.md"},
+]
 
 
 def gemm_source_sha256():
@@ -348,6 +357,56 @@ def decode_leg(P, C, w, ks, dev, desc, weights, x0, steps):
                     "score of that (layer, sequence)"}
 
 
+
+
+def layer_backward_leg(P, C, S, w, ks, dev, desc, weights, x0, reps=10):
+    """The routed layer's backward (training side of Section 3.4) at layer 0's
+    shape: dsf_sparse_block_backward (activations recomputed from the layer
+    input, block adjoint, every weight gradient) against the layer's forward.
+    The work of the backward is the recomputed forward plus about twice its
+    projection and attention FLOPs."""
+    import torch
+    B, T, d = w.batch, w.seq, w.d_model
+    k = ks[0]
+    dl = P.DeviceLayer(S.layer_weights(w, 0), dev)
+    g = torch.Generator().manual_seed(5)
+    dy = (torch.randn(B, T, d, generator=g) * 0.02).to(w.torch_dtype).to(dev)
+    idx = torch.stack([torch.sort(torch.randperm(T, generator=g)[:k])[0] for _ in range(B)]).to(torch.int32).to(dev)
+    dx = torch.empty_like(x0)
+    shapes = {"w_qkv": (w.d_qkv, d), "b_qkv": (w.d_qkv,), "w_o": (d, w.d_attn), "w_up": (w.d_up, d),
+              "w_down": (d, w.d_ff), "norm1_w": (d,), "norm2_w": (d,)}
+    if w.block == S.NEOX:
+        shapes.update(b_o=(d,), b_up=(w.d_ff,), b_down=(d,), norm1_b=(d,), norm2_b=(d,))
+    grads = {n: torch.empty(sh, device=dev) for n, sh in shapes.items()}
+    ws = torch.empty(P.backward_workspace_size(desc, P.BF16, B, T, k), dtype=torch.uint8, device=dev)
+    wsf = torch.empty(P.workspace_size(desc, P.BF16, B, T, k), dtype=torch.uint8, device=dev)
+    fn = lambda: P.sparse_block_backward(desc, dl.weights, x0, dy, idx, dx, grads, ws)
+    fwd = lambda xx: P.sparse_block_forward(desc, dl.weights, xx, k, wsf, idx_in=idx)
+    fn()
+    xs = [x0.clone() for _ in range(reps)]
+    fwd(xs[0])
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(reps):
+        fwd(xs[i])
+    e1.record()
+    torch.cuda.synchronize()
+    fwd_ms = e0.elapsed_time(e1) / reps
+    e0.record()
+    for _ in range(reps):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    bwd_ms = e0.elapsed_time(e1) / reps
+    fl = C.proj_flops(w, B, k) + C.attn_flops(w, B, k)
+    del ws, wsf, xs, grads
+    torch.cuda.empty_cache()
+    return {"k": k, "forward_ms": fwd_ms, "backward_ms": bwd_ms, "backward_over_forward": bwd_ms / fwd_ms,
+            "backward_tflops": 3.0 * fl / (bwd_ms / 1e3) / 1e12,
+            "note": "backward recomputes the kept rows' activations (one forward of the block) and computes the "
+                    "adjoint (about twice the forward's projection and attention FLOPs); work counted as 3x the "
+                    "block's forward FLOPs"}
 
 
 KIND_DESC = {
@@ -703,6 +762,8 @@ def main():
         log("alignment objective: teacher/student stack, Eq. 9 and Eq. 10 kernels")
         r2["alignment_objective"] = alignment_objective(P, C, w2, c2["ks"], dev, c2["desc"], c2["weights"], c2["x0"],
                                                         r2["ms_per_step"], 6)
+        log("routed layer backward at layer 0's shape")
+        r2["layer_backward"] = layer_backward_leg(P, C, S, w2, c2["ks"], dev, c2["desc"], c2["weights"], c2["x0"])
         log("incremental decoding: prefill into kept-token caches, then threshold-routed decode steps")
         r2["decode"] = decode_leg(P, C, w2, c2["ks"], dev, c2["desc"], c2["weights"], c2["x0"], 20)
         extras["neox160m"] = r2
