@@ -265,6 +265,14 @@ int dsf_attention_forward(const void* q, const void* k, const void* v, int dtype
  * indices are bitwise those of the two separate kernels; the environment
  * variable DSF_UNFUSED_ROUTING=1, read at every call, runs those instead.
  *
+ * Second stream. For GPT-NeoX blocks the FFN up projection runs on a
+ * library-owned stream beside QKV and attention on the caller's stream,
+ * ordered by event waits (which a graph capture of the caller's stream
+ * records too). There is one such stream per device and host thread,
+ * created by the thread's first call and destroyed with its events when the
+ * thread exits. DSF_SINGLE_STREAM=1, read at every call, keeps all work on
+ * the caller's stream (results are bitwise the same).
+ *
  * Projection schedule. Each bf16 projection GEMM takes 256 x 256 output
  * tiles when they still fill the chip for more than a round (at least 320
  * tiles), 128 x 128 tiles otherwise; the environment variable

@@ -539,9 +539,12 @@ namespace {
 // A second stream for work that the block's data flow lets run beside the
 // main chain: the NeoX FFN up projection needs only LN2 of the kept rows, so
 // it runs while QKV and attention run on the caller's stream. One per device
-// and host thread, non-blocking, default priority. Fork and join are event
-// waits, which a caller capturing the stream into a graph records as well.
-// DSF_SINGLE_STREAM=1 (read at every call) keeps everything on one stream.
+// and host thread, created on the thread's first such call, non-blocking,
+// default priority, and destroyed with its events when the thread exits (a
+// per-thread stream never joins another thread's graph capture). Fork and
+// join are event waits, which a caller capturing the stream into a graph
+// records as well. DSF_SINGLE_STREAM=1 (read at every call) keeps everything
+// on one stream.
 // The fork and join events only order the two streams of one device: the
 // kernels' own end-of-kernel releases make their results visible device-wide,
 // so the events skip the system-scope fence (measured 1.2 % per stack step).
@@ -551,20 +554,43 @@ struct AuxStream {
   hipEvent_t fork = nullptr, join = nullptr;
 };
 
+// The calling thread's streams, one slot per device. Thread-local objects
+// of a thread are destroyed when it exits, before the HIP runtime's own
+// teardown at process exit; a stream with work still queued is released once
+// that work completes. Errors at that point have no caller to go to.
+struct AuxStreams {
+  std::vector<AuxStream> per_dev;
+  ~AuxStreams() {
+    for (AuxStream& a : per_dev) {
+      if (a.fork) (void)hipEventDestroy(a.fork);
+      if (a.join) (void)hipEventDestroy(a.join);
+      if (a.s) (void)hipStreamDestroy(a.s);
+    }
+  }
+};
+
 int get_aux(const AuxStream** out) {
   *out = nullptr;
   const char* e = getenv("DSF_SINGLE_STREAM");
   if (e && e[0] == '1') return DSF_OK;
-  static thread_local std::vector<AuxStream> per_dev;
+  static thread_local AuxStreams streams;
+  std::vector<AuxStream>& per_dev = streams.per_dev;
   int dev = 0;
   DSF_HIP(hipGetDevice(&dev));
   if (dev < 0) return fail(DSF_EHIP, "bad device %d", dev);
   if (size_t(dev) >= per_dev.size()) per_dev.resize(size_t(dev) + 1);
   AuxStream& a = per_dev[size_t(dev)];
-  if (!a.s) {
-    DSF_HIP(hipStreamCreateWithFlags(&a.s, hipStreamNonBlocking));
-    DSF_HIP(hipEventCreateWithFlags(&a.fork, kAuxEventFlags));
-    DSF_HIP(hipEventCreateWithFlags(&a.join, kAuxEventFlags));
+  if (!a.s || !a.fork || !a.join) {  // created together; a partial set is retried whole
+    AuxStream n;
+    hipError_t err = hipStreamCreateWithFlags(&n.s, hipStreamNonBlocking);
+    if (err == hipSuccess) err = hipEventCreateWithFlags(&n.fork, kAuxEventFlags);
+    if (err == hipSuccess) err = hipEventCreateWithFlags(&n.join, kAuxEventFlags);
+    if (err != hipSuccess) {
+      if (n.fork) (void)hipEventDestroy(n.fork);
+      if (n.s) (void)hipStreamDestroy(n.s);
+      return fail(DSF_EHIP, "creating the second stream: %s", hipGetErrorString(err));
+    }
+    a = n;
   }
   *out = &a;
   return DSF_OK;

@@ -177,3 +177,52 @@ def test_large_tile_stack_matches_layerwise(dev, monkeypatch, name):
         cur = y.cpu()
     torch.cuda.synchronize()
     assert torch.equal(xd.cpu(), cur)
+
+
+def test_host_threads_get_their_own_second_streams(dev):
+    # each host thread gets its own second stream (destroyed when the thread
+    # exits); threads on their own caller streams and workspaces give the
+    # single-threaded result bitwise, and a later call on the main thread
+    # still works after the worker threads have gone
+    import threading
+    w = workload("neox_bf16_small").replace(n_layers=2)
+    Ws = S.stack_weights(w)
+    x = S.hidden_states(w)
+    ks = [w.seq // 2, w.seq // 3]
+    dls = [P.DeviceLayer(W, dev) for W in Ws]
+    weights = [dl.weights for dl in dls]
+    announce("second streams of several host threads")
+    ref = x.to(dev)
+    ws0 = workspace(w, w.batch, w.seq, max(ks), dev)
+    P.stack_forward(make_desc(w), weights, ks, ref, ws0)
+    torch.cuda.synchronize()
+    n = 4
+    xdev = x.to(dev)
+    outs = [torch.empty_like(xdev) for _ in range(n)]
+    wss = [workspace(w, w.batch, w.seq, max(ks), dev) for _ in range(n)]
+    streams = [torch.cuda.Stream(dev) for _ in range(n)]
+    torch.cuda.synchronize()
+    errors = []
+
+    def work(i):
+        try:
+            with torch.cuda.stream(streams[i]):  # the copy and the stack on one stream
+                for _ in range(3):
+                    outs[i].copy_(xdev)
+                    P.stack_forward(make_desc(w), weights, ks, outs[i], wss[i])
+            streams[i].synchronize()
+        except Exception as e:  # reported below, on the test's thread
+            errors.append(e)
+
+    threads = [threading.Thread(target=work, args=(i,)) for i in range(n)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not errors, errors
+    for i in range(n):
+        assert torch.equal(outs[i], ref), i
+    again = x.to(dev)
+    P.stack_forward(make_desc(w), weights, ks, again, ws0)
+    torch.cuda.synchronize()
+    assert torch.equal(again, ref)
