@@ -590,6 +590,20 @@ def measure_stack(P, C, S, w, dev, steps, warmup, dense=True, breakdown=True, ca
     if breakdown and not only_sparse:
         breakdown_d = breakdown_pass(P, C, w, desc, weights, ks, x0, ws, min(steps, 5))
         dom_kind = max(breakdown_d, key=lambda kk: breakdown_d[kk]["ms_per_step"])
+    breakdown_1s = None
+    if breakdown and not only_sparse and w.block == S.NEOX:
+        # the NeoX up projection shares the chip with QKV and attention on the
+        # second stream, so the in-stack rates above include each other's
+        # share; the same pass on one stream gives each kind alone
+        prev = os.environ.get("DSF_SINGLE_STREAM")
+        os.environ["DSF_SINGLE_STREAM"] = "1"
+        try:
+            breakdown_1s = breakdown_pass(P, C, w, desc, weights, ks, x0, ws, min(steps, 5))
+        finally:
+            if prev is None:
+                del os.environ["DSF_SINGLE_STREAM"]
+            else:
+                os.environ["DSF_SINGLE_STREAM"] = prev
     ms_step, per_step, (n_dom, ms_dom) = timed_steps(P, desc, weights, ks, x0, ws, steps, warmup, dom_kind=dom_kind)
     tokens_per_s = B * T / (ms_step / 1e3)
     log(f"sparse stack {ms_step:.3f} ms/step, {tokens_per_s / 1e6:.4f} M tokens/s")
@@ -627,6 +641,8 @@ def measure_stack(P, C, S, w, dev, steps, warmup, dense=True, breakdown=True, ca
            "mean_retention": sum(r) / L, "roofline": roofline, "kernel_breakdown": breakdown_d, "rates": rates,
            "calibration_ms": t_cal, "similarity_kernel": sim_rate, "similarity_measured": s_meas,
            "flop_ratio_sparse_over_dense": C.stack_flops(w, B, T, ks, True) / C.stack_flops(w, B, T, [T] * L, False)}
+    if breakdown_1s is not None:
+        res["kernel_breakdown_one_stream"] = breakdown_1s
     if dense and not only_sparse:
         wsd = torch.empty(P.workspace_size(desc, dcode, B, T, T), dtype=torch.uint8, device=dev)
         nd = max(3, steps // 4)

@@ -289,7 +289,8 @@ int dsf_attention_forward(const void* q, const void* k, const void* v, int dtype
  *
  * Call status. The first 4 bytes of the workspace hold a status word that
  * each call of dsf_sparse_block_forward, dsf_stack_forward,
- * dsf_stack_prefill and dsf_align_stack_forward clears at its start and that
+ * dsf_stack_prefill, dsf_align_stack_forward and dsf_sparse_block_backward
+ * clears at its start and that
  * its kernels OR bits into; read it with dsf_workspace_status once the call's
  * work is enqueued. A call with nothing to do (B, T or k zero), which
  * launches nothing, leaves the word as it was. DSF_WS_STATUS_SK_TIMEOUT: a stream-K workgroup that must
@@ -381,9 +382,14 @@ size_t dsf_backward_workspace_size(const dsf_layer_desc* desc, int dtype, int B,
  * The block's activations on the kept rows are recomputed from x (with the
  * forward's kernels) rather than kept by the forward. bf16 only
  * (DSF_EUNSUPPORTED for DSF_F32); fp32 accumulation, deterministic. k == 0
- * copies dy into dx and leaves the gradients unwritten. Errors: DSF_EINVAL for
- * null or misaligned pointers and bad sizes, DSF_EWORKSPACE for a short
- * workspace. */
+ * copies dy into dx and leaves the gradients unwritten. The weight gradients
+ * reduce over every kept token into few output tiles: when that would leave
+ * most of the chip idle, their GEMMs take the stream-K grid (equal pieces of
+ * the k-iterations per workgroup, partial sums added in a fixed order). The
+ * workspace starts with the same status word as the forward's (cleared by
+ * every call with B, T > 0; DSF_WS_STATUS_SK_TIMEOUT if a stream-K wait gave
+ * up), read with dsf_workspace_status. Errors: DSF_EINVAL for null or
+ * misaligned pointers and bad sizes, DSF_EWORKSPACE for a short workspace. */
 int dsf_sparse_block_backward(const dsf_layer_desc* desc, const dsf_layer_weights* weights, int dtype,
                               const void* x, const void* dy, int B, int T, int k, const int32_t* idx,
                               const float* scores, int flags, void* dx, const dsf_layer_grads* grads,

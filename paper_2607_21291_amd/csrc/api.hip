@@ -1350,7 +1350,7 @@ extern "C" int dsf_align_stack_forward(const dsf_layer_desc* desc, const dsf_lay
 
 namespace {
 struct BwdPlan {
-  size_t rope, xc, a1, a2, h, m2, q, k, v, attn, u, dd, du, dm, dao, dattn, dqf, dkf, dvf, lse, dvec, dqkv, da, acc;
+  size_t ctl, skpart, rope, xc, a1, a2, h, m2, q, k, v, attn, u, dd, du, dm, dao, dattn, dqf, dkf, dvf, lse, dvec, dqkv, da, acc;
   size_t mean1, rstd1, mean2, rstd2, wdT, wuT, woT, wqT, tdd, tact, tdu, tm, tdao, tattn, tdqkv, ta1, part, total;
   int Np, fup, dqkv_cols;
 };
@@ -1370,6 +1370,10 @@ BwdPlan make_bwd_plan(const dsf_layer_desc& D, int B, int T, int k) {
     off += up256(bytes > 0 ? bytes : 1);
     return o;
   };
+  // control block at offset 0 (status word, then the stream-K flags), as in
+  // the forward's workspace, and the stream-K partial tiles
+  p.ctl = take(sizeof(uint32_t) * (size_t(kCtlFlagsWord) + size_t(gemm_flag_count())));
+  p.skpart = take(gemm_partial_bytes());
   p.rope = take(4 * size_t(T) * D.rotary_dims);
   p.xc = take(2 * N * d);
   p.a1 = take(2 * N * d);
@@ -1425,10 +1429,21 @@ int check_bwd(const dsf_layer_desc* desc, int dtype, int B, int T, int k) {
   return DSF_OK;
 }
 
+// The stream-K state of one backward call: partial tiles, flags and status
+// word in its workspace, and the last epoch handed out since the flags were
+// zeroed.
+struct BwdSk {
+  float* part;
+  uint32_t *flags, *status;
+  uint32_t epoch;
+};
+
 // C[M, N] = A[M, K] . Bm[N, K]^T with one of the backward epilogues (plain
-// token rows: no positions, one "sequence" of M rows).
+// token rows: no positions, one "sequence" of M rows). With sk, a launch may
+// take the stream-K grid (the weight gradients, whose few output tiles would
+// leave most of the chip idle while each reduces over every kept token).
 int bwd_gemm(int epi, int M, int N, int K, const void* A, int lda, const void* Bm, int ldb, void* out, int ldo,
-             const void* bias, const void* res, int f, hipStream_t s) {
+             const void* bias, const void* res, int f, hipStream_t s, BwdSk* sk = nullptr) {
   if (M == 0 || N == 0) return DSF_OK;
   GemmArgs g{};
   g.dtype = DSF_BF16;
@@ -1437,6 +1452,12 @@ int bwd_gemm(int epi, int M, int N, int K, const void* A, int lda, const void* B
   g.epi = epi; g.bias = bias; g.res = res; g.f = f;
   g.out = out; g.ldo = ldo;
   g.B = 1; g.kk = M; g.T = M;
+  if (sk) {
+    g.part = sk->part;
+    g.flags = sk->flags;
+    g.status = sk->status;
+    g.epoch = ++sk->epoch;
+  }
   DSF_HIP(launch_gemm(g, s));
   return DSF_OK;
 }
@@ -1477,10 +1498,14 @@ extern "C" int dsf_sparse_block_backward(const dsf_layer_desc* desc, const dsf_l
   rc = check_device();
   if (rc) return rc;
   hipStream_t s = stream;
+  char* ws = (char*)workspace;
+  // zero the control block: the status word and the stream-K flags
+  BwdSk sk{reinterpret_cast<float*>(ws + p.skpart), reinterpret_cast<uint32_t*>(ws + p.ctl) + kCtlFlagsWord,
+           reinterpret_cast<uint32_t*>(ws + p.ctl), 0};
+  DSF_HIP(launch_zero_u32(sk.status, int64_t(kCtlFlagsWord) + gemm_flag_count(), s));
   const size_t xbytes = size_t(B) * T * D.d_model * 2;
   DSF_HIP(launch_copy(dy, dx, xbytes, s));  // skipped rows: dx = dy
   if (k == 0) return DSF_OK;                // (the weight gradients are then not written)
-  char* ws = (char*)workspace;
   auto P = [&](size_t off) { return (void*)(ws + off); };
   auto F = [&](size_t off) { return (float*)(ws + off); };
   const int d = D.d_model, hd = D.head_dim, Hq = D.n_heads, Hkv = D.n_kv_heads, f = D.d_ff;
@@ -1535,7 +1560,7 @@ extern "C" int dsf_sparse_block_backward(const dsf_layer_desc* desc, const dsf_l
   if (G.w_down) {
     DSF_HIP(launch_transpose(0, P(p.dd), N, d, d, P(p.tdd), Np, s));
     DSF_HIP(launch_transpose(qwen ? 2 : 1, P(p.u), N, f, fup, P(p.tact), Np, s));
-    rc = bwd_gemm(EPI_STORE_F32, d, f, Np, P(p.tdd), Np, P(p.tact), Np, G.w_down, f, nullptr, nullptr, 0, s);
+    rc = bwd_gemm(EPI_STORE_F32, d, f, Np, P(p.tdd), Np, P(p.tact), Np, G.w_down, f, nullptr, nullptr, 0, s, &sk);
     if (rc) return rc;
   }
   if (G.b_down && !qwen) DSF_HIP(launch_colsum(P(p.dd), N, d, d, nullptr, nullptr, nullptr, F(p.part), G.b_down, s));
@@ -1547,7 +1572,7 @@ extern "C" int dsf_sparse_block_backward(const dsf_layer_desc* desc, const dsf_l
   if (G.w_up) {
     DSF_HIP(launch_transpose(0, P(p.du), N, fup, fup, P(p.tdu), Np, s));
     DSF_HIP(launch_transpose(0, mrows, N, d, d, P(p.tm), Np, s));
-    rc = bwd_gemm(EPI_STORE_F32, fup, d, Np, P(p.tdu), Np, P(p.tm), Np, G.w_up, d, nullptr, nullptr, 0, s);
+    rc = bwd_gemm(EPI_STORE_F32, fup, d, Np, P(p.tdu), Np, P(p.tm), Np, G.w_up, d, nullptr, nullptr, 0, s, &sk);
     if (rc) return rc;
   }
   if (G.b_up && !qwen) DSF_HIP(launch_colsum(P(p.du), N, f, f, nullptr, nullptr, nullptr, F(p.part), G.b_up, s));
@@ -1570,7 +1595,7 @@ extern "C" int dsf_sparse_block_backward(const dsf_layer_desc* desc, const dsf_l
   if (G.w_o) {
     if (qwen || !G.w_down) DSF_HIP(launch_transpose(0, P(p.dao), N, d, d, P(p.tdao), Np, s));
     DSF_HIP(launch_transpose(0, P(p.attn), N, dq, dq, P(p.tattn), Np, s));
-    rc = bwd_gemm(EPI_STORE_F32, d, dq, Np, P(p.tdao), Np, P(p.tattn), Np, G.w_o, dq, nullptr, nullptr, 0, s);
+    rc = bwd_gemm(EPI_STORE_F32, d, dq, Np, P(p.tdao), Np, P(p.tattn), Np, G.w_o, dq, nullptr, nullptr, 0, s, &sk);
     if (rc) return rc;
   }
   if (G.b_o && !qwen) DSF_HIP(launch_colsum(P(p.dao), N, d, d, nullptr, nullptr, nullptr, F(p.part), G.b_o, s));
@@ -1586,7 +1611,7 @@ extern "C" int dsf_sparse_block_backward(const dsf_layer_desc* desc, const dsf_l
   if (G.w_qkv) {
     DSF_HIP(launch_transpose(0, P(p.dqkv), N, cq, cq, P(p.tdqkv), Np, s));
     DSF_HIP(launch_transpose(0, P(p.a1), N, d, d, P(p.ta1), Np, s));
-    rc = bwd_gemm(EPI_STORE_F32, cq, d, Np, P(p.tdqkv), Np, P(p.ta1), Np, G.w_qkv, d, nullptr, nullptr, 0, s);
+    rc = bwd_gemm(EPI_STORE_F32, cq, d, Np, P(p.tdqkv), Np, P(p.ta1), Np, G.w_qkv, d, nullptr, nullptr, 0, s, &sk);
     if (rc) return rc;
   }
   if (G.b_qkv) DSF_HIP(launch_colsum(P(p.dqkv), N, cq, cq, nullptr, nullptr, nullptr, F(p.part), G.b_qkv, s));

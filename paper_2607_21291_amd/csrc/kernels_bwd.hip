@@ -52,23 +52,147 @@ __global__ __launch_bounds__(256) void transpose_kernel(const uint16_t* __restri
   }
 }
 
+// The same with 16-byte accesses on both sides (C, ldi and ldo multiples of
+// 8, 16-byte aligned bases): a thread loads 8 columns of an input row and
+// stores 8 rows of an output row.
+template <int OP>
+__global__ __launch_bounds__(256) void transpose_vec_kernel(const uint16_t* __restrict__ in, int R, int C, int ldi,
+                                                            uint16_t* __restrict__ out, int ldo) {
+  __shared__ float tile[64][65];
+  const int c0 = blockIdx.x * 64, r0 = blockIdx.y * 64;
+  const int t = threadIdx.x, v = t & 7, q = t >> 3;  // vector index, row (column) within a pass
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int rr = q + 32 * i, r = r0 + rr, c = c0 + 8 * v;
+    float x[8];
+    if (r < R && c < C) {
+      const int64_t o = int64_t(r) * ldi + c;
+      const u32x4 raw = *reinterpret_cast<const u32x4*>(in + o);
+      u32x4 up{};
+      if constexpr (OP == 2) up = *reinterpret_cast<const u32x4*>(in + o + C);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        x[2 * e] = __uint_as_float(raw[e] << 16);
+        x[2 * e + 1] = __uint_as_float(raw[e] & 0xffff0000u);
+        if constexpr (OP == 1) {
+          x[2 * e] = gelu_bf16(x[2 * e]);
+          x[2 * e + 1] = gelu_bf16(x[2 * e + 1]);
+        }
+        if constexpr (OP == 2) {
+          x[2 * e] = silu_bf16(x[2 * e]) * __uint_as_float(up[e] << 16);
+          x[2 * e + 1] = silu_bf16(x[2 * e + 1]) * __uint_as_float(up[e] & 0xffff0000u);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) x[e] = 0.f;
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) tile[rr][8 * v + e] = x[e];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int cc = q + 32 * i, c = c0 + cc, r = r0 + 8 * v;
+    if (c < C && r < ldo) {
+      u32x4 pk;
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        pk[e] = uint32_t(f2bf(tile[8 * v + 2 * e][cc])) | (uint32_t(f2bf(tile[8 * v + 2 * e + 1][cc])) << 16);
+      *reinterpret_cast<u32x4*>(out + int64_t(c) * ldo + r) = pk;
+    }
+  }
+}
+
 hipError_t launch_transpose(int op, const void* in, int R, int C, int ldi, void* out, int ldo, hipStream_t s) {
   if (R <= 0 || C <= 0) return hipSuccess;
   const dim3 grid((C + 63) / 64, (ldo + 63) / 64);
   const auto* i = (const uint16_t*)in;
   auto* o = (uint16_t*)out;
-  if (op == 0) transpose_kernel<0><<<grid, 256, 0, s>>>(i, R, C, ldi, o, ldo);
-  else if (op == 1) transpose_kernel<1><<<grid, 256, 0, s>>>(i, R, C, ldi, o, ldo);
-  else transpose_kernel<2><<<grid, 256, 0, s>>>(i, R, C, ldi, o, ldo);
+  const bool vec = C % 8 == 0 && ldi % 8 == 0 && ldo % 8 == 0 && reinterpret_cast<uintptr_t>(in) % 16 == 0 &&
+                   reinterpret_cast<uintptr_t>(out) % 16 == 0;
+  if (vec) {
+    if (op == 0) transpose_vec_kernel<0><<<grid, 256, 0, s>>>(i, R, C, ldi, o, ldo);
+    else if (op == 1) transpose_vec_kernel<1><<<grid, 256, 0, s>>>(i, R, C, ldi, o, ldo);
+    else transpose_vec_kernel<2><<<grid, 256, 0, s>>>(i, R, C, ldi, o, ldo);
+  } else {
+    if (op == 0) transpose_kernel<0><<<grid, 256, 0, s>>>(i, R, C, ldi, o, ldo);
+    else if (op == 1) transpose_kernel<1><<<grid, 256, 0, s>>>(i, R, C, ldi, o, ldo);
+    else transpose_kernel<2><<<grid, 256, 0, s>>>(i, R, C, ldi, o, ldo);
+  }
   return hipGetLastError();
 }
 
 // ----------------------------------------------------------- column sums
 
-// partial[chunk][c] = sum over rows r of chunk (kColRows rows, in order) of
-// a[r][c] (xhat == null) or a[r][c] * (x[r][c] - mean[r]) * rstd[r]; then
-// out[c] = sum over chunks in order. Both orders are fixed by the shape.
+// partial[chunk][c] = sum over the kColRows rows of chunk of a[r][c]
+// (xhat == null) or a[r][c] * (x[r][c] - mean[r]) * rstd[r]; then out[c] =
+// sum over chunks in order. With 16-byte rows (C, lda multiples of 8, aligned
+// bases) a workgroup is 32 column vectors of 8 columns by 8 row lanes: row
+// lane j adds rows j, j + 8, ... of the chunk in order, then the 8 lane sums
+// are added in lane order. Otherwise a thread adds one column's rows in
+// order. Every order is fixed by the shape.
 constexpr int kColRows = 256;
+constexpr int kColLanes = 8;
+
+__global__ __launch_bounds__(256) void colsum_partial_vec_kernel(const uint16_t* __restrict__ a, int R, int C,
+                                                                 int lda, const uint16_t* __restrict__ x,
+                                                                 const float* __restrict__ mean,
+                                                                 const float* __restrict__ rstd,
+                                                                 float* __restrict__ partial) {
+  __shared__ float red[kColLanes][32 * 8 + 4];
+  const int cv = threadIdx.x & 31, rl = threadIdx.x >> 5;
+  const int c0 = (blockIdx.x * 32 + cv) * 8;
+  const int r0 = blockIdx.y * kColRows, r1 = min(R, r0 + kColRows);
+  float s[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) s[e] = 0.f;
+  if (c0 < C) {
+    constexpr int U = 4;  // rows of this lane loaded before they are added
+    for (int rb = r0 + rl; rb < r1; rb += U * kColLanes) {
+      u32x4 va[U], vx[U];
+      float mu[U], rs[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int r = rb + u * kColLanes;
+        if (r < r1) {
+          va[u] = *reinterpret_cast<const u32x4*>(a + int64_t(r) * lda + c0);
+          if (x) {
+            vx[u] = *reinterpret_cast<const u32x4*>(x + int64_t(r) * lda + c0);
+            mu[u] = mean ? mean[r] : 0.f;
+            rs[u] = rstd[r];
+          }
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        if (rb + u * kColLanes < r1) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const uint32_t wa = va[u][e >> 1];
+            float v = __uint_as_float((e & 1) ? (wa & 0xffff0000u) : (wa << 16));
+            if (x) {
+              const uint32_t wx = vx[u][e >> 1];
+              v *= (__uint_as_float((e & 1) ? (wx & 0xffff0000u) : (wx << 16)) - mu[u]) * rs[u];
+            }
+            s[e] += v;
+          }
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) red[rl][cv * 8 + e] = s[e];
+  __syncthreads();
+  // thread t sums column t of the workgroup's 256 over the lanes in order
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  if (c < C) {
+    float t = 0.f;
+#pragma unroll
+    for (int l = 0; l < kColLanes; ++l) t += red[l][threadIdx.x];
+    partial[int64_t(blockIdx.y) * C + c] = t;
+  }
+}
 
 __global__ __launch_bounds__(256) void colsum_partial_kernel(const uint16_t* __restrict__ a, int R, int C, int lda,
                                                              const uint16_t* __restrict__ x,
@@ -92,7 +216,16 @@ __global__ __launch_bounds__(256) void colsum_final_kernel(const float* __restri
   const int c = blockIdx.x * 256 + threadIdx.x;
   if (c >= C) return;
   float s = 0.f;
-  for (int k = 0; k < chunks; ++k) s += partial[int64_t(k) * C + c];
+  constexpr int U = 8;  // partials loaded before they are added (in order)
+  for (int k = 0; k < chunks; k += U) {
+    float v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (k + u < chunks) v[u] = partial[int64_t(k + u) * C + c];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (k + u < chunks) s += v[u];
+  }
   out[c] = s;
 }
 
@@ -102,9 +235,14 @@ hipError_t launch_colsum(const void* a, int R, int C, int lda, const void* x, co
                          float* partial, float* out, hipStream_t s) {
   if (C <= 0) return hipSuccess;
   const int chunks = colsum_chunks(R);
-  if (chunks > 0)
-    colsum_partial_kernel<<<dim3((C + 255) / 256, chunks), 256, 0, s>>>((const uint16_t*)a, R, C, lda,
-                                                                        (const uint16_t*)x, mean, rstd, partial);
+  const bool vec = C % 8 == 0 && lda % 8 == 0 && reinterpret_cast<uintptr_t>(a) % 16 == 0 &&
+                   (!x || reinterpret_cast<uintptr_t>(x) % 16 == 0);
+  if (chunks > 0) {
+    const uint16_t *ap = (const uint16_t*)a, *xp = (const uint16_t*)x;
+    const dim3 grid((C + 255) / 256, chunks);
+    if (vec) colsum_partial_vec_kernel<<<grid, 256, 0, s>>>(ap, R, C, lda, xp, mean, rstd, partial);
+    else colsum_partial_kernel<<<grid, 256, 0, s>>>(ap, R, C, lda, xp, mean, rstd, partial);
+  }
   colsum_final_kernel<<<(C + 255) / 256, 256, 0, s>>>(partial, chunks, C, out);
   return hipGetLastError();
 }

@@ -1062,7 +1062,11 @@ static int resident_slots(const void* fn, int threads) {
 struct Schedule {
   int px, split;
 };
-static Schedule choose_schedule(int nt, int nk, int slots) {
+// underfilled: also split a grid of at most half as many tiles as slots
+// whose reduction is long (the backward's weight gradients: few output
+// tiles, a reduction over every kept token), every workgroup taking an equal
+// piece of all the tiles' k-iterations.
+static Schedule choose_schedule(int nt, int nk, int slots, bool underfilled = false) {
   const int px = slots / kXcds;
   if (px < 1) return {0, 0};
   const int mode = schedule_override();
@@ -1072,6 +1076,7 @@ static Schedule choose_schedule(int nt, int nk, int slots) {
   const int64_t P = int64_t(px) * kXcds;
   const int64_t last = nt % P;
   if (nk >= kSkMinK) {
+    if (underfilled && 2 * int64_t(nt) <= P && int64_t(nt) * nk >= P * kSkMinIters) return {px, 1};
     if (nt <= P || last == 0 || 4 * last > P) return {0, 0};
     if (int64_t(nt) * nk < P * kSkMinIters) return {0, 0};
     return {px, 1};
@@ -1292,20 +1297,23 @@ static void launch_dma(const GemmArgs& g, hipStream_t s) {
     // Persistent and stream-K grids only with small tiles: the large tiles'
     // grids run many rounds (a short last round costs a few percent), and the
     // stream-K kernel's partial-sum hand-over does not fit their register
-    // budget beside 128 accumulators per lane.
-    if constexpr (BM == TileSmall::BM && BN == TileSmall::BN && EPI < EPI_STORE) if (g.part && g.flags) {
-      auto fn = gemm_bf16_sk_kernel<EPI, BM, BN, WM, WN, NS, BK>;
-      const int slots = std::min(kPartSlots, resident_slots<std::integral_constant<int, EPI * 2 + (BM > 128)>>(
-                                                 (const void*)fn, Cfg::kThreads));
-      const Schedule sch = choose_schedule(ntn * ga.ntm, g.K / BK, slots);
-      ga.px = sch.px;
-      ga.split = sch.split;
-      ga.spin_limit = spin_limit();
-      // tile order as for one tile per workgroup (the grid has more tiles than slots)
-      ga.group_m = ntn >= kGroupMinCols ? kGroupM : 0;
-      if (ga.px > 0) {
-        launch_timed(fn, dim3(ga.px * kXcds), dim3(Cfg::kThreads), s, ga);
-        return;
+    // budget beside 128 accumulators per lane. Among the backward kinds only
+    // the weight gradients (fp32 output) take them.
+    if constexpr (BM == TileSmall::BM && BN == TileSmall::BN && (EPI < EPI_STORE || EPI == EPI_STORE_F32)) {
+      if (g.part && g.flags) {
+        auto fn = gemm_bf16_sk_kernel<EPI, BM, BN, WM, WN, NS, BK>;
+        const int slots = std::min(kPartSlots, resident_slots<std::integral_constant<int, EPI * 2 + (BM > 128)>>(
+                                                   (const void*)fn, Cfg::kThreads));
+        const Schedule sch = choose_schedule(ntn * ga.ntm, g.K / BK, slots, EPI == EPI_STORE_F32);
+        ga.px = sch.px;
+        ga.split = sch.split;
+        ga.spin_limit = spin_limit();
+        // tile order as for one tile per workgroup
+        ga.group_m = ntn >= kGroupMinCols ? kGroupM : 0;
+        if (ga.px > 0) {
+          launch_timed(fn, dim3(ga.px * kXcds), dim3(Cfg::kThreads), s, ga);
+          return;
+        }
       }
     }
     // More tiles than resident workgroups: walk bands of kGroupM tile rows

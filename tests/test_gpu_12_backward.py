@@ -47,6 +47,7 @@ def run_backward(dev, w, W, x, dy, idx, gate, scores=None):
     P.sparse_block_backward(desc, dl.weights, xd, dyd, idd, dx, g, ws, scores=scores,
                             flags=P.FLAG_GATE if gate else 0)
     torch.cuda.synchronize()
+    assert P.workspace_status(ws) == 0, "a stream-K wait gave up"
     return dx, g
 
 
@@ -135,3 +136,32 @@ def test_backward_full_shapes(dev, name, B, T, k, gate):
     announce(f"backward full shape {name} B={B} T={T} k={k} gate={gate}")
     dx, gr = run_backward(dev, w, W, x, dy, idx, gate, sc)
     check_backward(w, W, x, dy, idx, gate, dx, gr)
+
+
+def test_backward_streamk_wait_timeout_is_reported(dev, monkeypatch):
+    """The weight gradients of a full-width NeoX-160M layer (B 2, k 1563 of
+    2048: 3126 kept rows) take the stream-K grid. DSF_SK_SPIN_LIMIT=0 makes
+    every wait for an earlier piece give up at once (every kernel still exits
+    normally); the status word reports it, and the next normal call clears it
+    and is correct again."""
+    w = S.WORKLOADS["neox160m"].replace(batch=2, seq=2048)
+    W = S.layer_weights(w, 0)
+    x = S.hidden_states(w)
+    g = torch.Generator().manual_seed(17)
+    dy = (torch.randn(2, 2048, w.d_model, generator=g) * 0.02).to(torch.bfloat16)
+    idx = np.stack([np.sort(torch.randperm(2048, generator=g)[:1563].numpy()) for _ in range(2)])
+    dl = P.DeviceLayer(W, dev)
+    desc = make_desc(w)
+    xd, dyd = x.to(dev).contiguous(), dy.to(dev).contiguous()
+    idd = torch.as_tensor(idx, dtype=torch.int32).to(dev).contiguous()
+    dx = torch.empty_like(xd)
+    gr = _grads(w, dev)
+    ws = torch.empty(P.backward_workspace_size(desc, P.BF16, 2, 2048, 1563), dtype=torch.uint8, device=dev)
+    announce("backward stream-K give-up reported")
+    monkeypatch.setenv("DSF_SK_SPIN_LIMIT", "0")
+    P.sparse_block_backward(desc, dl.weights, xd, dyd, idd, dx, gr, ws)
+    torch.cuda.synchronize()
+    assert P.workspace_status(ws) == P.WS_STATUS_SK_TIMEOUT
+    monkeypatch.delenv("DSF_SK_SPIN_LIMIT")
+    dx, gr = run_backward(dev, w, W, x, dy, idx, False)
+    check_backward(w, W, x, dy, idx, False, dx, gr)
