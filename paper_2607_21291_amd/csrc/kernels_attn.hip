@@ -15,19 +15,24 @@
 // cores as well: an A operand of ones gives, in every row of its output block,
 // sum_k P[query][k] over the same bf16 probabilities that weight V.
 //
-// Two ways of staging the tiles:
-// - DMA (attn_bf16_dma_kernel): K and V go global -> LDS by buffer DMA (no
-//   registers, no VALU), both row-major with each row's 16-byte chunks
-//   XOR-swizzled by the row index, in a ring of two stages; V^T is read with
-//   the LDS transpose load (ds_read_b64_tr_b16).
-// - Register prefetch (attn_bf16_staged_kernel): each tile is loaded into
-//   registers two tiles ahead and written to LDS by the waves, V transposed
-//   on the way (no transpose load needed), which leaves LDS for two query
-//   groups per wave at head dim 128.
+// K and V tiles go global -> LDS by buffer DMA (no registers, no VALU), both
+// row-major with each row's 16-byte chunks XOR-swizzled by the row index, in
+// a ring of two stages; V^T is read with the LDS transpose load
+// (ds_read_b64_tr_b16). Two forms of the kernel (attn_bf16_dma_kernel):
+// - one query group per wave, the tile's V^T fragments read before the next
+//   tile's DMA is issued (short sequences: more, shorter workgroups);
+// - two query groups per wave (each K and V fragment serves 32 queries), the
+//   next tile's DMA issued first and V^T read block by block in the
+//   product, four transpose loads and their wait at a time: two waves per
+//   SIMD at head dim 128, where holding a whole tile's V^T fragments would
+//   not fit.
 //
 // Kept positions ascend, so causal order over compacted indices is causal
 // order over original positions.
 #include <hip/hip_ext.h>
+
+#include <cstdlib>
+#include <cstring>
 
 #include "attn_sched.h"
 #include "dsf_device.h"
@@ -57,7 +62,26 @@ __device__ __forceinline__ bf16x4 lds_read_tr(const uint16_t* p) {
       (lds_bf16x4*)((__attribute__((address_space(3))) uint16_t*)(p)));
 }
 
-template <int HD, int NQ>
+// The four LDS transpose loads of one 16-dim block of V^T (keys 0-15, 16-31,
+// 32-47, 48-63 of the tile at byte stride ks) and the wait for them, as one
+// inline-assembly statement: the compiler, which cannot see whether such a
+// load overlaps an LDS DMA in flight, waits for every DMA before the
+// builtin's loads; here the caller has already made the tile's DMA visible
+// (own wait and the barrier), and the next tile's DMA writes the other stage.
+template <int HD>
+__device__ __forceinline__ void lds_read_tr4(uint32_t addr, u32x2 (&v)[4]) {
+  asm volatile(
+      "ds_read_b64_tr_b16 %0, %4\n\t"
+      "ds_read_b64_tr_b16 %1, %4 offset:%5\n\t"
+      "ds_read_b64_tr_b16 %2, %4 offset:%6\n\t"
+      "ds_read_b64_tr_b16 %3, %4 offset:%7\n\t"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(v[0]), "=&v"(v[1]), "=&v"(v[2]), "=&v"(v[3])
+      : "v"(addr), "n"(16 * HD * 2), "n"(32 * HD * 2), "n"(48 * HD * 2)
+      : "memory");
+}
+
+template <int HD, int NQ, bool LATE = false>
 __global__ __launch_bounds__(256) void attn_bf16_dma_kernel(const uint16_t* __restrict__ Q,
                                                             const uint16_t* __restrict__ K,
                                                             const uint16_t* __restrict__ V, int Hq, int Hkv,
@@ -242,13 +266,40 @@ __global__ __launch_bounds__(256) void attn_bf16_dma_kernel(const uint16_t* __re
 #pragma unroll
         for (int qi = 0; qi < NQ; ++qi)
           l_run[qi] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb[qi][ks], l_run[qi], 0, 0, 0);
+      if constexpr (LATE) {
+        // V^T fragments read block by block, the next block's loads issued
+        // after this block's MFMAs
+        const uint32_t vs = uint32_t(size_t((__attribute__((address_space(3))) char*)(
+                                smem + (t & 1) * A::kStage + A::kTileBytes + vbase)));
+        u32x2 cur[4];
+        lds_read_tr4<HD>(vs + uint32_t(((0 ^ vu) * 8) * 2), cur);
 #pragma unroll
-      for (int db = 0; db < ND; ++db)
+        for (int db = 0; db < ND; ++db) {
+          bf16x8 vv[2];
 #pragma unroll
-        for (int ks = 0; ks < 2; ++ks)
+          for (int ks = 0; ks < 2; ++ks) {
+            const u32x4 raw = {cur[2 * ks][0], cur[2 * ks][1], cur[2 * ks + 1][0], cur[2 * ks + 1][1]};
+            vv[ks] = __builtin_bit_cast(bf16x8, raw);
+          }
 #pragma unroll
-          for (int qi = 0; qi < NQ; ++qi)
-            o[qi][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[db][ks], pb[qi][ks], o[qi][db], 0, 0, 0);
+          for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+            for (int qi = 0; qi < NQ; ++qi)
+              o[qi][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vv[ks], pb[qi][ks], o[qi][db], 0, 0, 0);
+          if (db + 1 < ND) {
+            __builtin_amdgcn_sched_barrier(0);
+            lds_read_tr4<HD>(vs + uint32_t((((2 * (db + 1)) ^ vu) * 8) * 2), cur);
+          }
+        }
+      } else {
+#pragma unroll
+        for (int db = 0; db < ND; ++db)
+#pragma unroll
+          for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+            for (int qi = 0; qi < NQ; ++qi)
+              o[qi][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[db][ks], pb[qi][ks], o[qi][db], 0, 0, 0);
+      }
     }
   };
   // The barrier at the top of tile t publishes tile t and retires tile
@@ -260,13 +311,21 @@ __global__ __launch_bounds__(256) void attn_bf16_dma_kernel(const uint16_t* __re
   for (int t = 0; t < ntiles; ++t) {
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
-    if (t * kKV <= wave_qmax) {  // otherwise every key of this tile is in this wave's future
-      bf16x8 vf[ND][2];
-      read_v(t, vf);
+    if constexpr (LATE) {
       if (t + 1 < ntiles) issue(t + 1);
-      tile(t, vf);
-    } else if (t + 1 < ntiles) {
-      issue(t + 1);
+      if (t * kKV <= wave_qmax) {
+        bf16x8 none[ND][2];
+        tile(t, none);
+      }
+    } else {
+      if (t * kKV <= wave_qmax) {  // otherwise every key of this tile is in this wave's future
+        bf16x8 vf[ND][2];
+        read_v(t, vf);
+        if (t + 1 < ntiles) issue(t + 1);
+        tile(t, vf);
+      } else if (t + 1 < ntiles) {
+        issue(t + 1);
+      }
     }
   }
   // lane holds O^T[dim 16 db + 4 grp + i][query r16]
@@ -286,283 +345,6 @@ __global__ __launch_bounds__(256) void attn_bf16_dma_kernel(const uint16_t* __re
   }
 }
 
-
-// ------------------------------------------------------ register prefetch
-
-constexpr int kVtLD = kKV + 4;  // padded row of the transposed V tile (bf16 elements)
-
-template <int HD>
-struct StagedTile {
-  static constexpr int kNch = HD / 8;                              // 16-byte chunks per row
-  static constexpr int kSwz = (kNch < 8 ? kNch : 8) - 1;
-  static constexpr int kKChunks = kKV * kNch;                      // K tile chunks
-  static constexpr int kVPairs = (kKV / 2) * kNch;                 // V tile: two keys per item
-  static constexpr int kKIter = (kKChunks + 255) / 256;
-  static constexpr int kVIter = (kVPairs + 255) / 256;
-  static constexpr int kKBytes = kKV * HD * 2;
-  static constexpr int kVBytes = HD * kVtLD * 2;
-  static constexpr int kStage = kKBytes + kVBytes;
-};
-
-// A K/V tile is held in registers while earlier tiles are multiplied (loads in
-// flight during compute), then written to the other LDS buffer: one barrier
-// per tile.
-template <int HD>
-struct StagedPrefetch {
-  using A = StagedTile<HD>;
-  u32x4 k[A::kKIter];
-  u32x4 v0[A::kVIter], v1[A::kVIter];
-
-  // Tile rows are read through a buffer resource that starts at the tile's
-  // first key and ends at key n - 1: rows past the last key read as zeros
-  // (their scores are masked to -inf and their V rows weighted by zero), and
-  // each lane's offsets are the same for every tile.
-  __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t kr, __amdgpu_buffer_rsrc_t vr, int tid) {
-#pragma unroll
-    for (int i = 0; i < A::kKIter; ++i) {
-      const int c = tid + 256 * i;
-      if (A::kKChunks % 256 == 0 || c < A::kKChunks)
-        k[i] = __builtin_amdgcn_raw_buffer_load_b128(kr, (c / A::kNch) * (HD * 2) + (c % A::kNch) * 16, 0, 0);
-    }
-#pragma unroll
-    for (int i = 0; i < A::kVIter; ++i) {
-      const int c = tid + 256 * i;
-      if (A::kVPairs % 256 == 0 || c < A::kVPairs) {
-        const int kp = c % (kKV / 2), ch = c / (kKV / 2);
-        const int off = 2 * kp * (HD * 2) + ch * 16;
-        v0[i] = __builtin_amdgcn_raw_buffer_load_b128(vr, off, 0, 0);
-        v1[i] = __builtin_amdgcn_raw_buffer_load_b128(vr, off + HD * 2, 0, 0);
-      }
-    }
-  }
-  // K row-major with swizzled chunks; V transposed, Vt[dim][key], two keys per 32-bit store
-  __device__ __forceinline__ void store(uint16_t* Ks, uint16_t* Vt, int tid) const {
-#pragma unroll
-    for (int i = 0; i < A::kKIter; ++i) {
-      const int c = tid + 256 * i;
-      if (A::kKChunks % 256 == 0 || c < A::kKChunks) {
-        const int row = c / A::kNch, ch = c % A::kNch;
-        *reinterpret_cast<u32x4*>(Ks + row * HD + ((ch ^ (row & A::kSwz)) << 3)) = k[i];
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < A::kVIter; ++i) {
-      const int c = tid + 256 * i;
-      if (A::kVPairs % 256 == 0 || c < A::kVPairs) {
-        const int kp = c % (kKV / 2), ch = c / (kKV / 2);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          // lo = (v0.lo16, v1.lo16), hi = (v0.hi16, v1.hi16), one byte permute each
-          const uint32_t lo = __builtin_amdgcn_perm(v1[i][e], v0[i][e], 0x05040100u);
-          const uint32_t hi = __builtin_amdgcn_perm(v1[i][e], v0[i][e], 0x07060302u);
-          *reinterpret_cast<uint32_t*>(Vt + (ch * 8 + 2 * e) * kVtLD + 2 * kp) = lo;
-          *reinterpret_cast<uint32_t*>(Vt + (ch * 8 + 2 * e + 1) * kVtLD + 2 * kp) = hi;
-        }
-      }
-    }
-  }
-};
-
-template <int HD, int NQ>
-__global__ __launch_bounds__(256) void attn_bf16_staged_kernel(const uint16_t* __restrict__ Q,
-                                                               const uint16_t* __restrict__ K,
-                                                               const uint16_t* __restrict__ V, int Hq, int Hkv,
-                                                               int n, uint16_t* __restrict__ out) {
-  using A = StagedTile<HD>;
-  constexpr int QB = 64 * NQ;          // queries per workgroup
-  constexpr int NS = HD / 32;          // MFMA k steps over the head dim
-  constexpr int ND = HD / 16;          // 16-row blocks of the head dim
-  __shared__ __attribute__((aligned(16))) char smem[2 * A::kStage];
-
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: keeps tile tests scalar
-  const int r16 = lane & 15, grp = lane >> 4;
-  // one work item per (sequence, head, query block); the query blocks of one
-  // (sequence, head) share K/V, so they are kept on one XCD, and each XCD
-  // starts its longest blocks first
-  const int nqb = (n + QB - 1) / QB;
-  const AttnItem it = attn_item(int(blockIdx.x), int(gridDim.x), nqb);
-  const int bh = it.bh, qblk = it.qblk;
-  const int h = bh % Hq, b = bh / Hq;
-  const int kvh = h / (Hq / Hkv);
-  const int q0 = qblk * QB;
-  const int qw0 = q0 + wave * 16 * NQ;
-
-  const uint16_t* Qh = Q + (int64_t(b) * Hq + h) * n * HD;
-  const uint16_t* Kh = K + (int64_t(b) * Hkv + kvh) * n * HD;
-  const uint16_t* Vh = V + (int64_t(b) * Hkv + kvh) * n * HD;
-
-  const int kend = min(n, q0 + QB);
-  const int ntiles = (kend + kKV - 1) / kKV;
-  // Two register sets prefetch K/V two tiles ahead: tile t + 1 is written to
-  // LDS at the end of tile t, its loads having been issued during tile t - 1.
-  // Every load is issued unconditionally (tiles past the last are clamped to
-  // it, an L2 hit): with a fixed number of loads in flight the wait before a
-  // set is written covers exactly that set, not the set loaded after it.
-  const int last = ntiles - 1;
-  // buffer resources over keys kb0 .. n - 1 of this (sequence, kv head)
-  auto rows_from = [&](const uint16_t* base, int kb0) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base + int64_t(kb0) * HD), (short)0,
-                                             (n - kb0) * (HD * 2), 0x00020000);
-  };
-  auto fetch = [&](StagedPrefetch<HD>& pf, int t) {
-    const int kb0 = min(t, last) * kKV;
-    pf.load(rows_from(Kh, kb0), rows_from(Vh, kb0), tid);
-  };
-  StagedPrefetch<HD> pfA, pfB;
-  fetch(pfA, 0);
-  fetch(pfB, 1);
-
-  // Q^T operand: lane (query r16, group grp) holds Q[query][32 s + 8 grp .. +8]
-  bf16x8 qf[NQ][NS];
-#pragma unroll
-  for (int qi = 0; qi < NQ; ++qi) {
-    int qrow = qw0 + 16 * qi + r16;
-    if (qrow > n - 1) qrow = n - 1;
-#pragma unroll
-    for (int s = 0; s < NS; ++s)
-      qf[qi][s] = *reinterpret_cast<const bf16x8*>(Qh + int64_t(qrow) * HD + 32 * s + 8 * grp);
-  }
-
-  // all-ones A operand: l_run accumulates the row sums of P on the matrix cores
-  bf16x8 ones;
-#pragma unroll
-  for (int i = 0; i < 8; ++i) ones[i] = (__bf16)1.0f;
-  f32x4 o[NQ][ND], l_run[NQ];
-  float m_run[NQ];
-#pragma unroll
-  for (int qi = 0; qi < NQ; ++qi) {
-    m_run[qi] = -INFINITY;
-    l_run[qi] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int db = 0; db < ND; ++db) o[qi][db] = f32x4{0.f, 0.f, 0.f, 0.f};
-  }
-  const float sc = 1.4426950408889634f / sqrtf(float(HD));  // log2(e) / sqrt(hd)
-  const int wave_qmax = qw0 + 16 * NQ - 1;
-
-  pfA.store(reinterpret_cast<uint16_t*>(smem), reinterpret_cast<uint16_t*>(smem + A::kKBytes), tid);
-  __syncthreads();
-  fetch(pfA, 2);
-  // one tile: scores, online softmax and P V over LDS buffer t & 1
-  auto tile = [&](int t) {
-    const int kb0 = t * kKV;
-    const uint16_t* Ks = reinterpret_cast<const uint16_t*>(smem + (t & 1) * A::kStage);
-    const uint16_t* Vt = reinterpret_cast<const uint16_t*>(smem + (t & 1) * A::kStage + A::kKBytes);
-    if (kb0 <= wave_qmax) {  // otherwise every key of this tile is in this wave's future
-      // S^T blocks: lane holds S[query 16 qi + r16][key kb0 + 16 kb + 4 grp + i]
-      f32x4 s[NQ][4];
-#pragma unroll
-      for (int qi = 0; qi < NQ; ++qi)
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb) s[qi][kb] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb) {
-        const int row = 16 * kb + r16;
-#pragma unroll
-        for (int st = 0; st < NS; ++st) {
-          const int ch = 4 * st + grp;
-          bf16x8 kf = *reinterpret_cast<const bf16x8*>(Ks + row * HD + ((ch ^ (row & A::kSwz)) << 3));
-#pragma unroll
-          for (int qi = 0; qi < NQ; ++qi)
-            s[qi][kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[qi][st], s[qi][kb], 0, 0, 0);
-        }
-      }
-      const bool diag = kb0 + kKV - 1 > qw0 || kb0 + kKV > n;  // wave-uniform
-      bf16x8 pb[NQ][2];
-#pragma unroll
-      for (int qi = 0; qi < NQ; ++qi) {
-        if (diag) {
-          // key kb0 + 4 grp + (16 kb + i) is visible to query qg iff 16 kb + i <= lim
-          const int qg = qw0 + 16 * qi + r16;
-          const int lim = min(qg, n - 1) - (kb0 + 4 * grp);
-#pragma unroll
-          for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) s[qi][kb][i] = (16 * kb + i > lim) ? -INFINITY : s[qi][kb][i];
-        }
-        float mx = -INFINITY;
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) mx = fmaxf(mx, s[qi][kb][i]);
-        // running max in log2 units of the scaled scores (sc > 0 keeps the order)
-        const float m_new = fmaxf(m_run[qi], rows4_max(mx) * sc);
-        const float base = m_new == -INFINITY ? 0.f : m_new;
-        float p[4][4];
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) p[kb][i] = __builtin_amdgcn_exp2f(fmaf(s[qi][kb][i], sc, -base));
-        // rescale the running sums only when some lane's max moved (rare after the first tiles)
-        if (__builtin_amdgcn_ballot_w64(m_new != m_run[qi])) {
-          const float alpha = __builtin_amdgcn_exp2f(m_run[qi] - base);
-          l_run[qi] *= alpha;
-#pragma unroll
-          for (int db = 0; db < ND; ++db) o[qi][db] *= alpha;
-        }
-        m_run[qi] = m_new;
-#pragma unroll
-        for (int ks = 0; ks < 2; ++ks)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            pb[qi][ks][i] = (__bf16)p[2 * ks][i];
-            pb[qi][ks][4 + i] = (__bf16)p[2 * ks + 1][i];
-          }
-      }
-      // O^T[dim 16 db + r16 .. ][query] += V^T P^T over this tile's 64 keys
-#pragma unroll
-      for (int ks = 0; ks < 2; ++ks)
-#pragma unroll
-        for (int qi = 0; qi < NQ; ++qi)
-          l_run[qi] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb[qi][ks], l_run[qi], 0, 0, 0);
-#pragma unroll
-      for (int db = 0; db < ND; ++db) {
-        const int dim = 16 * db + r16;
-#pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-          const uint16_t* vrow = Vt + dim * kVtLD + 32 * ks + 4 * grp;
-          u32x2 lo = *reinterpret_cast<const u32x2*>(vrow);
-          u32x2 hi = *reinterpret_cast<const u32x2*>(vrow + 16);
-          u32x4 raw = {lo[0], lo[1], hi[0], hi[1]};
-          bf16x8 vf = __builtin_bit_cast(bf16x8, raw);
-#pragma unroll
-          for (int qi = 0; qi < NQ; ++qi)
-            o[qi][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pb[qi][ks], o[qi][db], 0, 0, 0);
-        }
-      }
-    }
-  };
-  // after tile t: write tile t + 1 (held in `held`) to the other buffer, then
-  // refill `held` with tile t + 3
-  auto advance = [&](int t, StagedPrefetch<HD>& held) {
-    held.store(reinterpret_cast<uint16_t*>(smem + ((t + 1) & 1) * A::kStage),
-               reinterpret_cast<uint16_t*>(smem + ((t + 1) & 1) * A::kStage + A::kKBytes), tid);
-    __syncthreads();
-    fetch(held, t + 3);
-  };
-  for (int t = 0; t < ntiles; t += 2) {
-    tile(t);  // pfB holds tile t + 1, pfA tile t + 2
-    advance(t, pfB);
-    if (t + 1 >= ntiles) break;
-    tile(t + 1);  // pfA holds tile t + 2, pfB tile t + 3
-    advance(t + 1, pfA);
-  }
-  // lane holds O^T[dim 16 db + 4 grp + i][query r16]
-#pragma unroll
-  for (int qi = 0; qi < NQ; ++qi) {
-    const int qg = qw0 + 16 * qi + r16;
-    if (qg >= n) continue;
-    const float inv = 1.0f / l_run[qi][0];
-    uint16_t* orow = out + (int64_t(b) * n + qg) * (int64_t(Hq) * HD) + int64_t(h) * HD;
-#pragma unroll
-    for (int db = 0; db < ND; ++db) {
-      u32x2 pk;
-      pk[0] = uint32_t(f2bf(o[qi][db][0] * inv)) | (uint32_t(f2bf(o[qi][db][1] * inv)) << 16);
-      pk[1] = uint32_t(f2bf(o[qi][db][2] * inv)) | (uint32_t(f2bf(o[qi][db][3] * inv)) << 16);
-      *reinterpret_cast<u32x2*>(orow + 16 * db + 4 * grp) = pk;
-    }
-  }
-}
 
 // fp32: one thread per query, online softmax over its causal prefix.
 template <int HD>
@@ -607,7 +389,13 @@ static void launch_timed(K kern, dim3 grid, dim3 block, hipStream_t s, A... args
   else kern<<<grid, block, 0, s>>>(args...);
 }
 
-constexpr int kAttnDmaMaxKeys = 2048;  // longest sequence sent to the DMA ring at head dim 64
+// Keys per sequence up to which one query group per wave is faster
+// (measured, per head dim): at head dim 64 the two forms are within 2 % up to
+// 2k keys and two groups win beyond (-10 % at 2362); at head dim 128 one group
+// wins at 512 keys (-20 %), two groups from about 1k (-3 % at 1024, -17 % at
+// 1638, -9 % at 4118).
+constexpr int kAttnOneGroupMaxKeys64 = 2048;
+constexpr int kAttnOneGroupMaxKeys128 = 768;
 
 hipError_t launch_attention(int dtype, const void* q, const void* k, const void* v, int B, int Hq, int Hkv,
                             int n, int hd, void* out, hipStream_t s) {
@@ -624,23 +412,24 @@ hipError_t launch_attention(int dtype, const void* q, const void* k, const void*
     }
     return hipGetLastError();
   }
-  // Measured choice between the two stagings: the DMA ring with one query
-  // group per wave is faster up to about 2k keys per sequence at head dim
-  // <= 64 (more, shorter workgroups and no staging VALU: -7 to -18 % at 600 -
-  // 1563 keys); beyond that, register prefetch with two query groups per wave,
-  // which shares each K/V tile between 128 queries, is faster (-4 to -12 % at
-  // 2362 - 3000 keys), and at head dim 128 it is the only one of the two that
-  // fits two waves per SIMD.
   auto grid = [&](int nq) { return dim3(((n + 64 * nq - 1) / (64 * nq)) * Hq * B); };
   auto Qp = (const uint16_t*)q; auto Kp = (const uint16_t*)k; auto Vp = (const uint16_t*)v; auto O = (uint16_t*)out;
-  const bool dma = n <= kAttnDmaMaxKeys;
+  // DSF_ATTN_GROUPS=1 or =2 (read at every launch) forces one form (testing)
+  int groups = hd == 32 ? 1 : n <= (hd == 64 ? kAttnOneGroupMaxKeys64 : kAttnOneGroupMaxKeys128) ? 1 : 2;
+  if (const char* e = getenv("DSF_ATTN_GROUPS")) {
+    if (!strcmp(e, "1")) groups = 1;
+    if (!strcmp(e, "2")) groups = 2;
+  }
   switch (hd) {
-    case 32: launch_timed(attn_bf16_dma_kernel<32, 1>, grid(1), dim3(256), s, Qp, Kp, Vp, Hq, Hkv, n, O); break;
-    case 64:
-      if (dma) launch_timed(attn_bf16_dma_kernel<64, 1>, grid(1), dim3(256), s, Qp, Kp, Vp, Hq, Hkv, n, O);
-      else launch_timed(attn_bf16_staged_kernel<64, 2>, grid(2), dim3(256), s, Qp, Kp, Vp, Hq, Hkv, n, O);
-      break;
-    case 128: launch_timed(attn_bf16_staged_kernel<128, 2>, grid(2), dim3(256), s, Qp, Kp, Vp, Hq, Hkv, n, O); break;
+#define DSF_ATTN_LAUNCH(H)                                                                                      \
+  case H:                                                                                                       \
+    if (groups == 1) launch_timed(attn_bf16_dma_kernel<H, 1>, grid(1), dim3(256), s, Qp, Kp, Vp, Hq, Hkv, n, O); \
+    else launch_timed(attn_bf16_dma_kernel<H, 2, true>, grid(2), dim3(256), s, Qp, Kp, Vp, Hq, Hkv, n, O);      \
+    break;
+    DSF_ATTN_LAUNCH(32)
+    DSF_ATTN_LAUNCH(64)
+    DSF_ATTN_LAUNCH(128)
+#undef DSF_ATTN_LAUNCH
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

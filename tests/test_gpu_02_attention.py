@@ -42,9 +42,9 @@ def test_attention_matches_oracle(dev, dtype, hd, B, Hq, Hkv, n):
 
 @pytest.mark.parametrize("hd,Hq,Hkv,n", [(64, 2, 1, 2048), (64, 2, 1, 2049), (64, 3, 3, 2300), (32, 2, 2, 2100)])
 def test_attention_long_sequences(dev, hd, Hq, Hkv, n):
-    """Both bf16 stagings: up to 2048 keys per sequence (head dim 64) the DMA
-    ring runs, beyond it the register-prefetch kernel with two query groups
-    per wave; head dim 32 stays on the DMA ring at any length."""
+    """Both forms of the kernel: up to 2048 keys per sequence (head dim 64)
+    one query group per wave, beyond it two groups with the V^T loads block
+    by block; head dim 32 stays on one group at any length."""
     announce(f"attention long hd={hd} Hq={Hq} Hkv={Hkv} n={n}")
     g = torch.Generator().manual_seed(n + hd)
     q = torch.randn(1, Hq, n, hd, generator=g).to(torch.bfloat16)
@@ -75,8 +75,9 @@ def test_attention_peaky_logits(dev, hd, Hq, Hkv, n):
     """Queries scaled by 8 put the logits q.k / sqrt(hd) at a standard
     deviation of 8, so the running maximum of the online softmax moves many
     times along a row and most probabilities underflow: the rescaling of the
-    partial sums is exercised on every staging (DMA ring up to 2048 keys at
-    head dim 64, register prefetch beyond it and at head dim 128)."""
+    partial sums is exercised on both forms of the kernel (one query group
+    per wave up to 2048 keys at head dim 64 and up to 768 at head dim 128,
+    two groups beyond)."""
     announce(f"attention peaky logits hd={hd} Hq={Hq} Hkv={Hkv} n={n}")
     g = torch.Generator().manual_seed(7 * n + hd)
     q = (torch.randn(1, Hq, n, hd, generator=g) * 8.0).to(torch.bfloat16)
@@ -94,3 +95,20 @@ def test_attention_peaky_logits(dev, hd, Hq, Hkv, n):
     scale = O.causal_attention(qn, kn, np.abs(vn))
     err = np.max(np.abs(got - ref), axis=1) / np.max(scale, axis=1)
     assert np.max(err) < TOL[torch.bfloat16]
+
+
+@pytest.mark.parametrize("hd,Hq,Hkv,n", [(64, 4, 2, 777), (128, 6, 2, 300), (128, 2, 1, 1100), (32, 2, 2, 129)])
+def test_attention_forms_agree_bitwise(dev, monkeypatch, hd, Hq, Hkv, n):
+    """One and two query groups per wave add the same MFMA products in the
+    same order for every query, so the outputs are equal bit for bit."""
+    announce(f"attention forms hd={hd} Hq={Hq} Hkv={Hkv} n={n}")
+    g = torch.Generator().manual_seed(3 * n + hd)
+    q, k, v = (torch.randn(2, h, n, hd, generator=g).to(torch.bfloat16).to(dev) for h in (Hq, Hkv, Hkv))
+    outs = []
+    for groups in ("1", "2"):
+        monkeypatch.setenv("DSF_ATTN_GROUPS", groups)
+        out = torch.empty(2, n, Hq * hd, dtype=torch.bfloat16, device=dev)
+        P.attention_forward(q, k, v, out)
+        torch.cuda.synchronize()
+        outs.append(out)
+    assert torch.equal(outs[0], outs[1])
