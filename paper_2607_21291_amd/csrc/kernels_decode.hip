@@ -137,38 +137,82 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const T* __restrict__ 
   const T* kbase = ck + ((int64_t(b) * Hkv + kvh) * cap) * HD + sub * VEC;
   const T* vbase = cv + ((int64_t(b) * Hkv + kvh) * cap) * HD + sub * VEC;
   const float scale = 1.0f / sqrtf(float(HD));
-#pragma unroll 4
-  for (int pass = 0; pass < NPASS; ++pass) {
-    const int j = pass * KPP + row, key = k0 + j;
-    float acc = 0.f;
-    if (key < len) {
-      T kv[VEC];
-      *reinterpret_cast<u32x4*>(kv) = *reinterpret_cast<const u32x4*>(kbase + int64_t(key) * HD);
-#pragma unroll
-      for (int i = 0; i < VEC; ++i) acc = fmaf(qv[i], DecElem<T>::to_f(kv[i]), acc);
-    }
-#pragma unroll
-    for (int o = LPK / 2; o > 0; o >>= 1) acc += __shfl_xor(acc, o, 64);
-    if (sub == 0) ps[j] = key < len ? acc * scale : -INFINITY;
-  }
-  __syncthreads();
-  const float sv = ps[tid];
-  const float m = block4_max(sv, red);
-  const float p = sv == -INFINITY ? 0.f : expf(sv - m);
-  ps[tid] = p;
-  const float l = block4_sum(p, red);  // its barriers also publish ps
   float o[VEC];
 #pragma unroll
   for (int i = 0; i < VEC; ++i) o[i] = 0.f;
-#pragma unroll 4
-  for (int pass = 0; pass < NPASS; ++pass) {
-    const int j = pass * KPP + row, key = k0 + j;
-    if (key < len) {
-      T vv[VEC];
-      *reinterpret_cast<u32x4*>(vv) = *reinterpret_cast<const u32x4*>(vbase + int64_t(key) * HD);
-      const float pp = ps[j];
+  float m, l;
+  if constexpr (NPASS <= 16) {
+    // every key and value vector of this thread's rows is requested before
+    // the first is used (up to 32 16-byte loads in flight per thread)
+    u32x4 kr[NPASS], vr[NPASS];
 #pragma unroll
-      for (int i = 0; i < VEC; ++i) o[i] = fmaf(pp, DecElem<T>::to_f(vv[i]), o[i]);
+    for (int pass = 0; pass < NPASS; ++pass) {
+      const int key = k0 + pass * KPP + row;
+      kr[pass] = key < len ? *reinterpret_cast<const u32x4*>(kbase + int64_t(key) * HD) : u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int pass = 0; pass < NPASS; ++pass) {
+      const int key = k0 + pass * KPP + row;
+      vr[pass] = key < len ? *reinterpret_cast<const u32x4*>(vbase + int64_t(key) * HD) : u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int pass = 0; pass < NPASS; ++pass) {
+      const int j = pass * KPP + row, key = k0 + j;
+      const T* kv = reinterpret_cast<const T*>(&kr[pass]);
+      float acc = 0.f;
+#pragma unroll
+      for (int i = 0; i < VEC; ++i) acc = fmaf(qv[i], DecElem<T>::to_f(kv[i]), acc);
+#pragma unroll
+      for (int sh = LPK / 2; sh > 0; sh >>= 1) acc += __shfl_xor(acc, sh, 64);
+      if (sub == 0) ps[j] = key < len ? acc * scale : -INFINITY;
+    }
+    __syncthreads();
+    const float sv = ps[tid];
+    m = block4_max(sv, red);
+    const float p = sv == -INFINITY ? 0.f : expf(sv - m);
+    ps[tid] = p;
+    l = block4_sum(p, red);  // its barriers also publish ps
+#pragma unroll
+    for (int pass = 0; pass < NPASS; ++pass) {
+      const int j = pass * KPP + row;
+      if (k0 + j < len) {
+        const T* vv = reinterpret_cast<const T*>(&vr[pass]);
+        const float pp = ps[j];
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) o[i] = fmaf(pp, DecElem<T>::to_f(vv[i]), o[i]);
+      }
+    }
+  } else {
+#pragma unroll 4
+    for (int pass = 0; pass < NPASS; ++pass) {
+      const int j = pass * KPP + row, key = k0 + j;
+      float acc = 0.f;
+      if (key < len) {
+        T kv[VEC];
+        *reinterpret_cast<u32x4*>(kv) = *reinterpret_cast<const u32x4*>(kbase + int64_t(key) * HD);
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) acc = fmaf(qv[i], DecElem<T>::to_f(kv[i]), acc);
+      }
+#pragma unroll
+      for (int sh = LPK / 2; sh > 0; sh >>= 1) acc += __shfl_xor(acc, sh, 64);
+      if (sub == 0) ps[j] = key < len ? acc * scale : -INFINITY;
+    }
+    __syncthreads();
+    const float sv = ps[tid];
+    m = block4_max(sv, red);
+    const float p = sv == -INFINITY ? 0.f : expf(sv - m);
+    ps[tid] = p;
+    l = block4_sum(p, red);  // its barriers also publish ps
+#pragma unroll 4
+    for (int pass = 0; pass < NPASS; ++pass) {
+      const int j = pass * KPP + row, key = k0 + j;
+      if (key < len) {
+        T vv[VEC];
+        *reinterpret_cast<u32x4*>(vv) = *reinterpret_cast<const u32x4*>(vbase + int64_t(key) * HD);
+        const float pp = ps[j];
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) o[i] = fmaf(pp, DecElem<T>::to_f(vv[i]), o[i]);
+      }
     }
   }
 #pragma unroll

@@ -1218,19 +1218,25 @@ __global__ __launch_bounds__(256) void gemm_skinny_kernel(GemmArgs g, int splits
   f32x4 vlo = {0.f, 0.f, 0.f, 0.f}, vhi = {0.f, 0.f, 0.f, 0.f};
   for (int s0 = 0; s0 < splits; s0 += 4) {
     f32x4 lo[4], hi[4];
+    const float* p[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const float* p = base + int64_t(min(s0 + j, splits - 1)) * (kSkinnyRows * kSkinnyBN) + e0;
-      asm volatile("global_load_dwordx4 %0, %2, off sc1\n\tglobal_load_dwordx4 %1, %2, off offset:16 sc1"
-                   : "=&v"(lo[j]), "=&v"(hi[j])
-                   : "v"(p)
-                   : "memory");
-    }
-    asm volatile("s_waitcnt vmcnt(0)"
-                 : "+v"(lo[0]), "+v"(hi[0]), "+v"(lo[1]), "+v"(hi[1]), "+v"(lo[2]), "+v"(hi[2]), "+v"(lo[3]),
-                   "+v"(hi[3])
-                 :
-                 : "memory");
+    for (int j = 0; j < 4; ++j) p[j] = base + int64_t(min(s0 + j, splits - 1)) * (kSkinnyRows * kSkinnyBN) + e0;
+    // the loads and their wait in one statement: no register they write is
+    // touched before the data has arrived
+    asm volatile(
+        "global_load_dwordx4 %0, %8, off sc1\n\t"
+        "global_load_dwordx4 %1, %8, off offset:16 sc1\n\t"
+        "global_load_dwordx4 %2, %9, off sc1\n\t"
+        "global_load_dwordx4 %3, %9, off offset:16 sc1\n\t"
+        "global_load_dwordx4 %4, %10, off sc1\n\t"
+        "global_load_dwordx4 %5, %10, off offset:16 sc1\n\t"
+        "global_load_dwordx4 %6, %11, off sc1\n\t"
+        "global_load_dwordx4 %7, %11, off offset:16 sc1\n\t"
+        "s_waitcnt vmcnt(0)"
+        : "=&v"(lo[0]), "=&v"(hi[0]), "=&v"(lo[1]), "=&v"(hi[1]), "=&v"(lo[2]), "=&v"(hi[2]), "=&v"(lo[3]),
+          "=&v"(hi[3])
+        : "v"(p[0]), "v"(p[1]), "v"(p[2]), "v"(p[3])
+        : "memory");
 #pragma unroll
     for (int j = 0; j < 4; ++j)
       if (s0 + j < splits) {
