@@ -1531,7 +1531,7 @@ extern "C" int dsf_sparse_block_backward(const dsf_layer_desc* desc, const dsf_l
     g.Hq = Hq; g.Hkv = Hkv; g.hd = hd; g.R = D.rotary_dims; g.rope = F(p.rope);
     DSF_HIP(launch_gemm(g, s));
   }
-  DSF_HIP(launch_attention(dtype, P(p.q), P(p.k), P(p.v), B, Hq, Hkv, k, hd, P(p.attn), s));
+  DSF_HIP(launch_attention(dtype, P(p.q), P(p.k), P(p.v), B, Hq, Hkv, k, hd, P(p.attn), s, F(p.lse)));
   const void* mrows;  // input rows of the up projection
   if (!qwen) {
     mrows = P(p.a2);

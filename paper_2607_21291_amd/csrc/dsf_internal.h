@@ -192,10 +192,11 @@ hipError_t launch_rope_bwd(const float* dq, const float* dk, const float* dv, co
 hipError_t launch_scatter_grad(const void* dy, const float* acc, int B, int T, int d, const int32_t* idx, int kk,
                                void* dx, hipStream_t s);
 // causal attention backward; q, k, v head-major (RoPE applied), o and dout
-// token-major [B n, Hq hd]; lse, dvec [B, Hq, n]; dq [B, Hq, n, hd], dk and
-// dv [B, Hkv, n, hd] fp32.
+// token-major [B n, Hq hd]; lse [B, Hq, n] from the forward (launch_attention);
+// dvec [B, Hq, n] (written, then read); dq [B, Hq, n, hd], dk and dv
+// [B, Hkv, n, hd] fp32.
 hipError_t launch_attention_bwd(const void* q, const void* k, const void* v, const void* o, const void* dout, int B,
-                                int Hq, int Hkv, int n, int hd, float* lse, float* dvec, float* dq, float* dk,
+                                int Hq, int Hkv, int n, int hd, const float* lse, float* dvec, float* dq, float* dk,
                                 float* dv, hipStream_t s);
 size_t gemm_partial_bytes();
 int gemm_flag_count();
@@ -204,8 +205,10 @@ int gemm_skinny_counters();
 
 // ---- attention over kept tokens (kernels_attn.hip) ----
 // q [B, Hq, n, hd], k/v [B, Hkv, n, hd] -> out [B, n, Hq*hd], causal over the n tokens.
+// lse (nullable, bf16 only): float [B, Hq, n], the log of each query's softmax
+// normaliser in natural units of q.k / sqrt(hd) (the backward's input).
 hipError_t launch_attention(int dtype, const void* q, const void* k, const void* v, int B, int Hq,
-                            int Hkv, int n, int hd, void* out, hipStream_t s);
+                            int Hkv, int n, int hd, void* out, hipStream_t s, float* lse = nullptr);
 
 // ---- incremental decoding (kernels_decode.hip) ----
 hipError_t launch_kv_append(int dtype, const void* knew, const void* vnew, const int32_t* keep, void* ck, void* cv,

@@ -35,6 +35,7 @@
 #include <cstring>
 
 #include "attn_sched.h"
+#include "attn_tiles.h"
 #include "dsf_device.h"
 #include "dsf_internal.h"
 
@@ -44,14 +45,8 @@ constexpr int kKV = 64;  // keys per tile
 
 // ------------------------------------------------------------------- DMA ring
 template <int HD>
-struct DmaTile {
-  static constexpr int kRowBytes = HD * 2;
-  static constexpr int kNch = HD / 8;                 // 16-byte chunks per row
-  static constexpr int kSwz = kNch - 1;               // chunk c of row r is stored at c ^ (r & kSwz)
-  static constexpr int kTileBytes = kKV * kRowBytes;  // one K or V tile
-  static constexpr int kStage = 2 * kTileBytes;       // K tile, then V tile
-  static constexpr int kDmaPerWave = kTileBytes / 1024 / 4;  // 1 KB per wave-wide DMA, 4 waves
-  static_assert(kDmaPerWave >= 1 && (kNch & (kNch - 1)) == 0, "head dim");
+struct DmaTile : AttnTile<HD> {
+  static constexpr int kStage = 2 * AttnTile<HD>::kTileBytes;  // K tile, then V tile
 };
 
 // LDS transpose load: within each 16-lane group G, lane 16G + 4a + b receives
@@ -62,30 +57,12 @@ __device__ __forceinline__ bf16x4 lds_read_tr(const uint16_t* p) {
       (lds_bf16x4*)((__attribute__((address_space(3))) uint16_t*)(p)));
 }
 
-// The four LDS transpose loads of one 16-dim block of V^T (keys 0-15, 16-31,
-// 32-47, 48-63 of the tile at byte stride ks) and the wait for them, as one
-// inline-assembly statement: the compiler, which cannot see whether such a
-// load overlaps an LDS DMA in flight, waits for every DMA before the
-// builtin's loads; here the caller has already made the tile's DMA visible
-// (own wait and the barrier), and the next tile's DMA writes the other stage.
-template <int HD>
-__device__ __forceinline__ void lds_read_tr4(uint32_t addr, u32x2 (&v)[4]) {
-  asm volatile(
-      "ds_read_b64_tr_b16 %0, %4\n\t"
-      "ds_read_b64_tr_b16 %1, %4 offset:%5\n\t"
-      "ds_read_b64_tr_b16 %2, %4 offset:%6\n\t"
-      "ds_read_b64_tr_b16 %3, %4 offset:%7\n\t"
-      "s_waitcnt lgkmcnt(0)"
-      : "=&v"(v[0]), "=&v"(v[1]), "=&v"(v[2]), "=&v"(v[3])
-      : "v"(addr), "n"(16 * HD * 2), "n"(32 * HD * 2), "n"(48 * HD * 2)
-      : "memory");
-}
-
 template <int HD, int NQ, bool LATE = false>
 __global__ __launch_bounds__(256) void attn_bf16_dma_kernel(const uint16_t* __restrict__ Q,
                                                             const uint16_t* __restrict__ K,
                                                             const uint16_t* __restrict__ V, int Hq, int Hkv,
-                                                            int n, uint16_t* __restrict__ out) {
+                                                            int n, uint16_t* __restrict__ out,
+                                                            float* __restrict__ lse_out) {
   using A = DmaTile<HD>;
   constexpr int QB = 64 * NQ;          // queries per workgroup
   constexpr int NS = HD / 32;          // MFMA k steps over the head dim
@@ -342,6 +319,10 @@ __global__ __launch_bounds__(256) void attn_bf16_dma_kernel(const uint16_t* __re
       pk[1] = uint32_t(f2bf(o[qi][db][2] * inv)) | (uint32_t(f2bf(o[qi][db][3] * inv)) << 16);
       *reinterpret_cast<u32x2*>(orow + 16 * db + 4 * grp) = pk;
     }
+    // log of the softmax normaliser in natural units of q.k / sqrt(hd):
+    // (max in log2 units + log2 of the row sum) ln 2
+    if (lse_out && grp == 0)
+      lse_out[(int64_t(b) * Hq + h) * n + qg] = (m_run[qi] + __log2f(l_run[qi][0])) * 0.6931471805599453f;
   }
 }
 
@@ -398,7 +379,7 @@ constexpr int kAttnOneGroupMaxKeys64 = 2048;
 constexpr int kAttnOneGroupMaxKeys128 = 768;
 
 hipError_t launch_attention(int dtype, const void* q, const void* k, const void* v, int B, int Hq, int Hkv,
-                            int n, int hd, void* out, hipStream_t s) {
+                            int n, int hd, void* out, hipStream_t s, float* lse) {
   if (n == 0 || B == 0) return hipSuccess;
   TimedScope ts(DSF_KIND_ATTN, s, true);
   if (dtype == DSF_F32) {
@@ -423,8 +404,8 @@ hipError_t launch_attention(int dtype, const void* q, const void* k, const void*
   switch (hd) {
 #define DSF_ATTN_LAUNCH(H)                                                                                      \
   case H:                                                                                                       \
-    if (groups == 1) launch_timed(attn_bf16_dma_kernel<H, 1>, grid(1), dim3(256), s, Qp, Kp, Vp, Hq, Hkv, n, O); \
-    else launch_timed(attn_bf16_dma_kernel<H, 2, true>, grid(2), dim3(256), s, Qp, Kp, Vp, Hq, Hkv, n, O);      \
+    if (groups == 1) launch_timed(attn_bf16_dma_kernel<H, 1>, grid(1), dim3(256), s, Qp, Kp, Vp, Hq, Hkv, n, O, lse); \
+    else launch_timed(attn_bf16_dma_kernel<H, 2, true>, grid(2), dim3(256), s, Qp, Kp, Vp, Hq, Hkv, n, O, lse);      \
     break;
     DSF_ATTN_LAUNCH(32)
     DSF_ATTN_LAUNCH(64)

@@ -17,6 +17,7 @@
 //   - the final scatter: dx = dy, plus the block's gradient at the kept rows.
 #include <hip/hip_ext.h>
 
+#include "attn_tiles.h"
 #include "dsf_device.h"
 #include "dsf_internal.h"
 
@@ -466,8 +467,9 @@ hipError_t launch_scatter_grad(const void* dy, const float* acc, int B, int T, i
 
 // Shapes: q [B, Hq, n, HD], k and v [B, Hkv, n, HD] (bf16, RoPE applied, as
 // the forward's QKV epilogue writes them); o and dout [B n, Hq HD] (bf16,
-// token-major: the attention output and its gradient). Query head h reads
-// kv head h / (Hq / Hkv). scale = 1 / sqrt(HD).
+// token-major: the attention output and its gradient); lse [B, Hq, n], the
+// log of each query's softmax normaliser as the forward computed it. Query
+// head h reads kv head h / (Hq / Hkv). scale = 1 / sqrt(HD).
 //
 // MFMA operand layout (v_mfma_f32_16x16x32_bf16): lane l supplies row l % 16
 // of each operand and its 8 consecutive k slots 8 (l / 16) .. + 7; output
@@ -475,47 +477,14 @@ hipError_t launch_scatter_grad(const void* dy, const float* acc, int B, int T, i
 // its 32 summed indices to the k slots in any order, the same for both
 // operands: the probabilities and score gradients are used in the order a
 // lane holds them after the score MFMA (index 16 blk + 4 grp + e of the two
-// 16-blocks of the step), and the other operand is read from a transposed
-// LDS copy in that order (two 8-byte reads).
+// 16-blocks of the step), and the other operand is read with the LDS
+// transpose load in that order (AttnTrans).
+//
+// Tiles of 64 rows go global -> LDS by buffer DMA into a ring of two stages
+// (attn_tiles.h): the next tile's DMA is issued after the barrier that
+// publishes the current one, and runs under its products.
 
-constexpr int kAB = 64;  // queries or keys per block
-
-template <int HD>
-struct AttnBwdLds {
-  static constexpr int kRow = HD + 8;   // row-major tile [64][HD + 8]
-  static constexpr int kCol = kAB + 8;  // transposed tile [HD][64 + 8]
-};
-
-// Load a 64-row tile of a head-major [n, HD] matrix (rows r0 .. r0 + 63;
-// rows >= n as zeros) into LDS row-major (row) and, if trans, transposed.
-template <int HD>
-__device__ __forceinline__ void stage_tile(const uint16_t* __restrict__ src, int64_t row_stride, int r0, int n,
-                                           uint16_t* rowt, uint16_t* trans) {
-  using L = AttnBwdLds<HD>;
-  constexpr int kChunks = kAB * HD / 8;
-  for (int e = threadIdx.x; e < kChunks; e += 256) {
-    const int r = e / (HD / 8), c = (e % (HD / 8)) * 8;
-    u32x4 v = {0u, 0u, 0u, 0u};
-    if (r0 + r < n) v = *reinterpret_cast<const u32x4*>(src + int64_t(r0 + r) * row_stride + c);
-    *reinterpret_cast<u32x4*>(rowt + r * L::kRow + c) = v;
-    if (trans) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        trans[(c + 2 * i) * L::kCol + r] = uint16_t(v[i] & 0xffffu);
-        trans[(c + 2 * i + 1) * L::kCol + r] = uint16_t(v[i] >> 16);
-      }
-    }
-  }
-}
-
-// 8 bf16 of a transposed tile row (index c), columns 32 s + 4 g + (0..3) and
-// 32 s + 16 + 4 g + (0..3): the k-slot order of the probabilities.
-__device__ __forceinline__ bf16x8 read_perm(const uint16_t* trans_row, int s, int g) {
-  const u32x2 lo = *reinterpret_cast<const u32x2*>(trans_row + 32 * s + 4 * g);
-  const u32x2 hi = *reinterpret_cast<const u32x2*>(trans_row + 32 * s + 16 + 4 * g);
-  u32x4 r = {lo[0], lo[1], hi[0], hi[1]};
-  return __builtin_bit_cast(bf16x8, r);
-}
+constexpr int kAB = kAttnTileRows;  // queries or keys per block
 
 __device__ __forceinline__ bf16x8 pack8(const float* v) {
   bf16x8 r;
@@ -527,22 +496,20 @@ __device__ __forceinline__ bf16x8 pack8(const float* v) {
 // Pass 1: one workgroup per (sequence, query head, 64-query block); wave w
 // owns queries q0 + 16 w .. + 15 (lane l: query 16 w + l % 16). Scores are
 // formed transposed (S^T = K Q^T, keys as MFMA rows), so a lane holds 16
-// scores of its own query per 64-key block. Writes the row statistics
-// lse = max + log(sum) and D = sum_c dout * o for pass 2, and
-// dQ = scale * sum_keys dS K with dS = P (dP - D), dP = dout V^T.
+// scores of its own query per 64-key block. With P = exp(S scale - lse):
+// writes D = sum_c dout * o for pass 2, and dQ = scale * sum_keys dS K with
+// dS = P (dP - D), dP = dout V^T.
 template <int HD>
 __global__ __launch_bounds__(256) void attn_bwd_dq_kernel(const uint16_t* __restrict__ Q,
                                                           const uint16_t* __restrict__ K,
                                                           const uint16_t* __restrict__ V,
                                                           const uint16_t* __restrict__ O,
                                                           const uint16_t* __restrict__ dO, int n, int Hq, int Hkv,
-                                                          float* __restrict__ lse_out, float* __restrict__ dvec_out,
-                                                          float* __restrict__ dq_out) {
-  using L = AttnBwdLds<HD>;
+                                                          const float* __restrict__ lse,
+                                                          float* __restrict__ dvec_out, float* __restrict__ dq_out) {
+  using A = AttnTile<HD>;
   constexpr int NS = HD / 32, NC = HD / 16;
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[kAB * L::kRow];
-  __shared__ __attribute__((aligned(16))) uint16_t Vs[kAB * L::kRow];
-  __shared__ __attribute__((aligned(16))) uint16_t Kt[HD * L::kCol];
+  __shared__ __attribute__((aligned(16))) char smem[2 * 2 * A::kTileBytes];  // stage: K tile, then V tile
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r16 = lane & 15, grp = lane >> 4;
   const int nqb = (n + kAB - 1) / kAB;
@@ -555,6 +522,13 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_kernel(const uint16_t* __rest
   const uint16_t* Kh = K + (int64_t(b) * Hkv + kvh) * n * HD;
   const uint16_t* Vh = V + (int64_t(b) * Hkv + kvh) * n * HD;
   const int64_t orow = (int64_t(b) * n + (qok ? query : 0)) * (int64_t(Hq) * HD) + int64_t(h) * HD;
+  const int nkb = qb + 1;
+  auto issue = [&](int kt) {
+    char* st = smem + (kt & 1) * 2 * A::kTileBytes;
+    attn_tile_dma<HD>(Kh, HD, kt * kAB, n, st, wave, lane);
+    attn_tile_dma<HD>(Vh, HD, kt * kAB, n, st + A::kTileBytes, wave, lane);
+  };
+  issue(0);
 
   // this lane's query as MFMA B operand: Q and dout rows, k slots 32 s + 8 grp ..
   bf16x8 qf[NS], df[NS];
@@ -577,73 +551,39 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_kernel(const uint16_t* __rest
     }
   }
   const float Dq = rows4_sum(dsum);
+  const float lq = qok ? lse[int64_t(bh) * n + query] : 0.f;
+  if (qok && grp == 0) dvec_out[int64_t(bh) * n + query] = Dq;
 
-  // pass over the key blocks: row maximum and sum (online, per lane, merged
-  // over the four lanes of a query at the end)
-  const int nkb = qb + 1;
-  float mx = -INFINITY, sm = 0.f;
-  for (int kb = 0; kb < nkb; ++kb) {
-    __syncthreads();
-    stage_tile<HD>(Kh, HD, kb * kAB, n, Ks, nullptr);
-    __syncthreads();
-#pragma unroll
-    for (int blk = 0; blk < 4; ++blk) {
-      f32x4 st = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int s = 0; s < NS; ++s) {
-        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(Ks + (16 * blk + r16) * L::kRow + 32 * s + 8 * grp);
-        st = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[s], st, 0, 0, 0);
-      }
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int key = kb * kAB + 16 * blk + 4 * grp + e;
-        if (key <= query && key < n) {
-          const float v = st[e] * scale;
-          if (v > mx) {
-            sm = sm * __expf(mx - v) + 1.f;
-            mx = v;
-          } else {
-            sm += __expf(v - mx);
-          }
-        }
-      }
-    }
-  }
-  const float gmx = rows4_max(mx);
-  const float gsm = rows4_sum(mx == -INFINITY ? 0.f : sm * __expf(mx - gmx));
-  const float lse = gmx + logf(gsm);
-  if (qok && grp == 0) {
-    lse_out[int64_t(bh) * n + query] = lse;
-    dvec_out[int64_t(bh) * n + query] = Dq;
-  }
-
-  // second pass: dQ^T[c][query] = scale * sum_keys K^T[c][key] dS^T[key][query]
+  // dQ^T[c][query] = scale * sum_keys K^T[c][key] dS^T[key][query]
+  const AttnTrans<HD> tr(lane);
   f32x4 acc[NC];
 #pragma unroll
   for (int cb = 0; cb < NC; ++cb) acc[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
-  for (int kb = 0; kb < nkb; ++kb) {
-    __syncthreads();
-    stage_tile<HD>(Kh, HD, kb * kAB, n, Ks, Kt);
-    stage_tile<HD>(Vh, HD, kb * kAB, n, Vs, nullptr);
-    __syncthreads();
+  for (int kt = 0; kt < nkb; ++kt) {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's share of tile kt has landed
+    __syncthreads();                                   // ... and every wave's; tile kt - 1 is retired
+    if (kt + 1 < nkb) issue(kt + 1);
+    const char* Kt = smem + (kt & 1) * 2 * A::kTileBytes;
+    const char* Vt = Kt + A::kTileBytes;
     float ds[4][4];
 #pragma unroll
     for (int blk = 0; blk < 4; ++blk) {
       f32x4 st = {0.f, 0.f, 0.f, 0.f}, dp = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int s = 0; s < NS; ++s) {
-        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(Ks + (16 * blk + r16) * L::kRow + 32 * s + 8 * grp);
-        const bf16x8 vf = *reinterpret_cast<const bf16x8*>(Vs + (16 * blk + r16) * L::kRow + 32 * s + 8 * grp);
+        const bf16x8 kf = attn_row_frag<HD>(Kt, 16 * blk + r16, 4 * s + grp);
+        const bf16x8 vf = attn_row_frag<HD>(Vt, 16 * blk + r16, 4 * s + grp);
         st = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[s], st, 0, 0, 0);
         dp = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, df[s], dp, 0, 0, 0);
       }
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const int key = kb * kAB + 16 * blk + 4 * grp + e;
-        const float p = (key <= query && key < n && qok) ? __expf(st[e] * scale - lse) : 0.f;
+        const int key = kt * kAB + 16 * blk + 4 * grp + e;
+        const float p = (key <= query && key < n && qok) ? __expf(st[e] * scale - lq) : 0.f;
         ds[blk][e] = p * (dp[e] - Dq) * scale;
       }
     }
+    bf16x8 dsb[2];
 #pragma unroll
     for (int s2 = 0; s2 < 2; ++s2) {
       float v[8];
@@ -652,12 +592,14 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_kernel(const uint16_t* __rest
         v[e] = ds[2 * s2][e];
         v[4 + e] = ds[2 * s2 + 1][e];
       }
-      const bf16x8 dsb = pack8(v);
+      dsb[s2] = pack8(v);
+    }
 #pragma unroll
-      for (int cb = 0; cb < NC; ++cb) {
-        const bf16x8 kt = read_perm(Kt + (16 * cb + r16) * L::kCol, s2, grp);
-        acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kt, dsb, acc[cb], 0, 0, 0);
-      }
+    for (int cb = 0; cb < NC; ++cb) {
+      bf16x8 kt2[2];
+      tr.read(Kt, cb, kt2);
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2) acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kt2[s2], dsb[s2], acc[cb], 0, 0, 0);
     }
   }
   // lane holds dQ^T[16 cb + 4 grp + e][query]
@@ -670,11 +612,13 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_kernel(const uint16_t* __rest
 
 // Pass 2: one workgroup per (sequence, kv head, 64-key block); wave w owns
 // keys k0 + 16 w .. + 15 (lane l: key 16 w + l % 16). For every query head of
-// the kv head's group and every query block at or after the key block, scores
-// are formed with keys as MFMA columns (S = Q K^T), so a lane holds the
-// probabilities of its own key, and
+// the kv head's group and every query block at or after the key block (one
+// work item each, in that order), scores are formed with keys as MFMA
+// columns (S = Q K^T), so a lane holds the probabilities of its own key, and
 //   dV^T[c][key] += sum_queries dout^T[c][query] P[query][key],
 //   dK^T[c][key] += scale * sum_queries Q^T[c][query] dS[query][key].
+// Each item's lse and D are loaded by wave 0 one item ahead and published in
+// LDS with the item's tiles.
 template <int HD>
 __global__ __launch_bounds__(256) void attn_bwd_dkv_kernel(const uint16_t* __restrict__ Q,
                                                            const uint16_t* __restrict__ K,
@@ -683,13 +627,10 @@ __global__ __launch_bounds__(256) void attn_bwd_dkv_kernel(const uint16_t* __res
                                                            const float* __restrict__ lse,
                                                            const float* __restrict__ dvec, int n, int Hq, int Hkv,
                                                            float* __restrict__ dk_out, float* __restrict__ dv_out) {
-  using L = AttnBwdLds<HD>;
+  using A = AttnTile<HD>;
   constexpr int NS = HD / 32, NC = HD / 16;
-  __shared__ __attribute__((aligned(16))) uint16_t Qs[kAB * L::kRow];
-  __shared__ __attribute__((aligned(16))) uint16_t Ds[kAB * L::kRow];
-  __shared__ __attribute__((aligned(16))) uint16_t Qt[HD * L::kCol];
-  __shared__ __attribute__((aligned(16))) uint16_t Dt[HD * L::kCol];
-  __shared__ float lse_s[kAB], dvec_s[kAB];
+  __shared__ __attribute__((aligned(16))) char smem[2 * 2 * A::kTileBytes];  // stage: Q tile, then dout tile
+  __shared__ float lse_s[2][kAB], dvec_s[2][kAB];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r16 = lane & 15, grp = lane >> 4;
   const int nkb = (n + kAB - 1) / kAB;
@@ -701,6 +642,27 @@ __global__ __launch_bounds__(256) void attn_bwd_dkv_kernel(const uint16_t* __res
   const float scale = 1.f / sqrtf(float(HD));
   const uint16_t* Kh = K + int64_t(bkv) * n * HD;
   const uint16_t* Vh = V + int64_t(bkv) * n * HD;
+  const int nq = nkb - kb;  // query blocks at or after the key block
+  const int items = G * nq;
+  // item i: query head kvh G + i / nq, query block kb + i % nq
+  auto issue = [&](int i) {
+    const int h = kvh * G + i / nq, qb = kb + i % nq;
+    const int64_t bh = int64_t(b) * Hq + h;
+    char* st = smem + (i & 1) * 2 * A::kTileBytes;
+    attn_tile_dma<HD>(Q + bh * n * HD, HD, qb * kAB, n, st, wave, lane);
+    attn_tile_dma<HD>(dO + int64_t(b) * n * (int64_t(Hq) * HD) + int64_t(h) * HD, int64_t(Hq) * HD, qb * kAB, n,
+                      st + A::kTileBytes, wave, lane);
+  };
+  float pl = 0.f, pd = 0.f;  // wave 0, lane = query of the next item: its lse and D
+  auto fetch_stats = [&](int i) {
+    const int h = kvh * G + i / nq, qq = (kb + i % nq) * kAB + lane;
+    const int64_t bh = int64_t(b) * Hq + h;
+    pl = qq < n ? lse[bh * n + qq] : 0.f;
+    pd = qq < n ? dvec[bh * n + qq] : 0.f;
+  };
+  issue(0);
+  if (wave == 0) fetch_stats(0);
+
   bf16x8 kf[NS], vf[NS];
 #pragma unroll
   for (int s = 0; s < NS; ++s) {
@@ -712,66 +674,71 @@ __global__ __launch_bounds__(256) void attn_bwd_dkv_kernel(const uint16_t* __res
     kf[s] = __builtin_bit_cast(bf16x8, kv);
     vf[s] = __builtin_bit_cast(bf16x8, vv);
   }
+  const AttnTrans<HD> tr(lane);
   f32x4 adk[NC], adv[NC];
 #pragma unroll
   for (int cb = 0; cb < NC; ++cb) {
     adk[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
     adv[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
-  const int nqb = nkb;
-  for (int gq = 0; gq < G; ++gq) {
-    const int h = kvh * G + gq;
-    const int64_t bh = int64_t(b) * Hq + h;
-    const uint16_t* Qh = Q + bh * n * HD;
-    const uint16_t* dOh = dO + int64_t(b) * n * (int64_t(Hq) * HD) + int64_t(h) * HD;
-    for (int qb = kb; qb < nqb; ++qb) {
-      __syncthreads();
-      stage_tile<HD>(Qh, HD, qb * kAB, n, Qs, Qt);
-      stage_tile<HD>(dOh, int64_t(Hq) * HD, qb * kAB, n, Ds, Dt);
-      if (threadIdx.x < kAB) {
-        const int qq = qb * kAB + threadIdx.x;
-        lse_s[threadIdx.x] = qq < n ? lse[bh * n + qq] : 0.f;
-        dvec_s[threadIdx.x] = qq < n ? dvec[bh * n + qq] : 0.f;
+  for (int i = 0; i < items; ++i) {
+    const int slot = i & 1;
+    if (wave == 0) {  // slot's previous readers finished item i - 2 before the last barrier
+      lse_s[slot][lane] = pl;
+      dvec_s[slot][lane] = pd;
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's share of item i's tiles has landed
+    __syncthreads();                                   // ... and every wave's; item i - 1 is retired
+    if (i + 1 < items) {
+      issue(i + 1);
+      if (wave == 0) fetch_stats(i + 1);
+    }
+    const int qb = kb + i % nq;
+    const char* Qt = smem + slot * 2 * A::kTileBytes;
+    const char* Dt = Qt + A::kTileBytes;
+    float p[4][4], ds[4][4];
+#pragma unroll
+    for (int blk = 0; blk < 4; ++blk) {
+      f32x4 st = {0.f, 0.f, 0.f, 0.f}, dp = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < NS; ++s) {
+        const bf16x8 qa = attn_row_frag<HD>(Qt, 16 * blk + r16, 4 * s + grp);
+        const bf16x8 da = attn_row_frag<HD>(Dt, 16 * blk + r16, 4 * s + grp);
+        st = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa, kf[s], st, 0, 0, 0);
+        dp = __builtin_amdgcn_mfma_f32_16x16x32_bf16(da, vf[s], dp, 0, 0, 0);
       }
-      __syncthreads();
-      float p[4][4], ds[4][4];
 #pragma unroll
-      for (int blk = 0; blk < 4; ++blk) {
-        f32x4 st = {0.f, 0.f, 0.f, 0.f}, dp = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int s = 0; s < NS; ++s) {
-          const bf16x8 qa = *reinterpret_cast<const bf16x8*>(Qs + (16 * blk + r16) * L::kRow + 32 * s + 8 * grp);
-          const bf16x8 da = *reinterpret_cast<const bf16x8*>(Ds + (16 * blk + r16) * L::kRow + 32 * s + 8 * grp);
-          st = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa, kf[s], st, 0, 0, 0);
-          dp = __builtin_amdgcn_mfma_f32_16x16x32_bf16(da, vf[s], dp, 0, 0, 0);
-        }
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int ql = 16 * blk + 4 * grp + e;
-          const int qq = qb * kAB + ql;
-          const float pv = (kok && qq < n && key <= qq) ? __expf(st[e] * scale - lse_s[ql]) : 0.f;
-          p[blk][e] = pv;
-          ds[blk][e] = pv * (dp[e] - dvec_s[ql]) * scale;
-        }
+      for (int e = 0; e < 4; ++e) {
+        const int ql = 16 * blk + 4 * grp + e;
+        const int qq = qb * kAB + ql;
+        const float pv = (kok && qq < n && key <= qq) ? __expf(st[e] * scale - lse_s[slot][ql]) : 0.f;
+        p[blk][e] = pv;
+        ds[blk][e] = pv * (dp[e] - dvec_s[slot][ql]) * scale;
       }
+    }
+    bf16x8 pb[2], db[2];
+#pragma unroll
+    for (int s2 = 0; s2 < 2; ++s2) {
+      float pv[8], dv[8];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        pv[e] = p[2 * s2][e];
+        pv[4 + e] = p[2 * s2 + 1][e];
+        dv[e] = ds[2 * s2][e];
+        dv[4 + e] = ds[2 * s2 + 1][e];
+      }
+      pb[s2] = pack8(pv);
+      db[s2] = pack8(dv);
+    }
+#pragma unroll
+    for (int cb = 0; cb < NC; ++cb) {
+      bf16x8 dt2[2], qt2[2];
+      tr.read(Dt, cb, dt2);
+      tr.read(Qt, cb, qt2);
 #pragma unroll
       for (int s2 = 0; s2 < 2; ++s2) {
-        float pv[8], dv[8];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          pv[e] = p[2 * s2][e];
-          pv[4 + e] = p[2 * s2 + 1][e];
-          dv[e] = ds[2 * s2][e];
-          dv[4 + e] = ds[2 * s2 + 1][e];
-        }
-        const bf16x8 pb = pack8(pv), db = pack8(dv);
-#pragma unroll
-        for (int cb = 0; cb < NC; ++cb) {
-          const bf16x8 dt = read_perm(Dt + (16 * cb + r16) * L::kCol, s2, grp);
-          const bf16x8 qt = read_perm(Qt + (16 * cb + r16) * L::kCol, s2, grp);
-          adv[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(dt, pb, adv[cb], 0, 0, 0);
-          adk[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qt, db, adk[cb], 0, 0, 0);
-        }
+        adv[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(dt2[s2], pb[s2], adv[cb], 0, 0, 0);
+        adk[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qt2[s2], db[s2], adk[cb], 0, 0, 0);
       }
     }
   }
@@ -787,7 +754,7 @@ __global__ __launch_bounds__(256) void attn_bwd_dkv_kernel(const uint16_t* __res
 }
 
 hipError_t launch_attention_bwd(const void* q, const void* k, const void* v, const void* o, const void* dout, int B,
-                                int Hq, int Hkv, int n, int hd, float* lse, float* dvec, float* dq, float* dk,
+                                int Hq, int Hkv, int n, int hd, const float* lse, float* dvec, float* dq, float* dk,
                                 float* dv, hipStream_t s) {
   if (B == 0 || n == 0) return hipSuccess;
   const int nb = (n + kAB - 1) / kAB;
@@ -795,18 +762,15 @@ hipError_t launch_attention_bwd(const void* q, const void* k, const void* v, con
   const auto *Op = (const uint16_t*)o, *Dp = (const uint16_t*)dout;
   const dim3 g1(B * Hq * nb), g2(B * Hkv * nb);
   switch (hd) {
-    case 32:
-      attn_bwd_dq_kernel<32><<<g1, 256, 0, s>>>(Qp, Kp, Vp, Op, Dp, n, Hq, Hkv, lse, dvec, dq);
-      attn_bwd_dkv_kernel<32><<<g2, 256, 0, s>>>(Qp, Kp, Vp, Dp, lse, dvec, n, Hq, Hkv, dk, dv);
-      break;
-    case 64:
-      attn_bwd_dq_kernel<64><<<g1, 256, 0, s>>>(Qp, Kp, Vp, Op, Dp, n, Hq, Hkv, lse, dvec, dq);
-      attn_bwd_dkv_kernel<64><<<g2, 256, 0, s>>>(Qp, Kp, Vp, Dp, lse, dvec, n, Hq, Hkv, dk, dv);
-      break;
-    case 128:
-      attn_bwd_dq_kernel<128><<<g1, 256, 0, s>>>(Qp, Kp, Vp, Op, Dp, n, Hq, Hkv, lse, dvec, dq);
-      attn_bwd_dkv_kernel<128><<<g2, 256, 0, s>>>(Qp, Kp, Vp, Dp, lse, dvec, n, Hq, Hkv, dk, dv);
-      break;
+#define DSF_ATTN_BWD(H)                                                                         \
+  case H:                                                                                       \
+    attn_bwd_dq_kernel<H><<<g1, 256, 0, s>>>(Qp, Kp, Vp, Op, Dp, n, Hq, Hkv, lse, dvec, dq);   \
+    attn_bwd_dkv_kernel<H><<<g2, 256, 0, s>>>(Qp, Kp, Vp, Dp, lse, dvec, n, Hq, Hkv, dk, dv); \
+    break;
+    DSF_ATTN_BWD(32)
+    DSF_ATTN_BWD(64)
+    DSF_ATTN_BWD(128)
+#undef DSF_ATTN_BWD
     default:
       return hipErrorInvalidValue;
   }
