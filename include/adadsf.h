@@ -243,7 +243,12 @@ int dsf_scatter_residual(void* x, const void* delta, int dtype, int B, int T, in
  *   out[b, j, h*hd:(h+1)*hd] = sum_{j' <= j} softmax_j'(q_j . k_j' / sqrt(hd)) v_j'
  * q [B, Hq, n, hd], k and v [B, Hkv, n, hd], out [B, n, Hq*hd], all dtype.
  * Query head h reads kv head h / (Hq / Hkv). Rotary embedding, if any, must
- * already be applied to q and k. hd in {32, 64, 128}. */
+ * already be applied to q and k. hd in {32, 64, 128}. bf16: flash-style
+ * online softmax in fp32, probabilities rounded to bf16 for the product with
+ * v; a workgroup takes 64 queries (one 16-query group per wavefront) for
+ * short sequences and 128 (two groups) otherwise, with bitwise the same
+ * result; the environment variable DSF_ATTN_GROUPS=1 or =2, read at every
+ * call, forces one (testing). */
 int dsf_attention_forward(const void* q, const void* k, const void* v, int dtype, int B, int Hq,
                           int Hkv, int n, int hd, void* out, hipStream_t stream);
 
