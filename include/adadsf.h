@@ -264,7 +264,7 @@ int dsf_attention_forward(const void* q, const void* k, const void* v, int dtype
  * resets what it uses, so two calls that overlap in time (on different
  * streams) need two workspaces. Returns 0 on a bad argument.
  *
- * Routing launch. With DSF_BF16, T a multiple of 64 (at most 16384) and no
+ * Routing launch. With DSF_BF16, T a multiple of 64 (at most 4096) and no
  * idx_in, the router and the per-sequence Top-K run as one launch: the last
  * of a sequence's router workgroups to finish selects its Top-K. Scores and
  * indices are bitwise those of the two separate kernels; the environment

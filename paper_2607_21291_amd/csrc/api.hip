@@ -621,11 +621,15 @@ int reset_stream_k(const Ctx& c) {
   return DSF_OK;
 }
 
-// DSF_UNFUSED_ROUTING=1 (read at every call) runs the router and the Top-K as
-// two launches.
-bool fused_routing() {
+// Router and Top-K in one launch up to this many tokens per sequence: there
+// the saved launch pays; beyond it the Top-K of the last-arriving router
+// workgroup (512 threads) is slower than the separate 1024-thread kernel
+// (Qwen2.5-7B shape, T 8192: 3.09 against 2.27 + 0.46 ms per step).
+// DSF_UNFUSED_ROUTING=1 (read at every call) always runs two launches.
+constexpr int kFusedRoutingMaxT = 4096;
+bool fused_routing(int T) {
   const char* e = getenv("DSF_UNFUSED_ROUTING");
-  return !(e && e[0] == '1');
+  return !(e && e[0] == '1') && T <= kFusedRoutingMaxT;
 }
 
 // The stream-K fields of a GEMM launch on this call's workspace.
@@ -651,7 +655,7 @@ int run_layer(const Ctx& c, const dsf_layer_weights* W, void* x, int k, bool den
   const bool qwen = D.block == DSF_BLOCK_QWEN_SEQ;
   const int32_t* idx = nullptr;
   float* scores = nullptr;
-  if (!dense && !idx_in && router_topk_fusable(c.dtype, T, D.d_router) && fused_routing()) {
+  if (!dense && !idx_in && router_topk_fusable(c.dtype, T, D.d_router) && fused_routing(T)) {
     // router and Top-K in one launch (its last workgroup of each sequence selects)
     scores = scores_out ? scores_out : at<float>(c, c.plan.scores);
     int32_t* dst = idx_out ? idx_out : at<int32_t>(c, c.plan.idx);
