@@ -285,25 +285,29 @@ __global__ __launch_bounds__(256) void attn_bf16_dma_kernel(const uint16_t* __re
   // the barrier every wave's share of the tile is in LDS. The V fragments are
   // read before the next DMA is issued: a transpose read after it would wait
   // for that DMA to land.
-  for (int t = 0; t < ntiles; ++t) {
+  // tiles this wave computes: t kKV <= wave_qmax (every key of a later tile
+  // is in the future of all its queries); the rest only keep the barriers
+  // and the DMA going for the other waves
+  const int tc = min(ntiles, wave_qmax / kKV + 1);
+  int t = 0;
+  for (; t < tc; ++t) {
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
     if constexpr (LATE) {
       if (t + 1 < ntiles) issue(t + 1);
-      if (t * kKV <= wave_qmax) {
-        bf16x8 none[ND][2];
-        tile(t, none);
-      }
+      bf16x8 none[ND][2];
+      tile(t, none);
     } else {
-      if (t * kKV <= wave_qmax) {  // otherwise every key of this tile is in this wave's future
-        bf16x8 vf[ND][2];
-        read_v(t, vf);
-        if (t + 1 < ntiles) issue(t + 1);
-        tile(t, vf);
-      } else if (t + 1 < ntiles) {
-        issue(t + 1);
-      }
+      bf16x8 vf[ND][2];
+      read_v(t, vf);
+      if (t + 1 < ntiles) issue(t + 1);
+      tile(t, vf);
     }
+  }
+  for (; t < ntiles; ++t) {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (t + 1 < ntiles) issue(t + 1);
   }
   // lane holds O^T[dim 16 db + 4 grp + i][query r16]
 #pragma unroll
