@@ -2,6 +2,7 @@
 // launchers (each defined next to its kernels) and the timing hooks.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -25,6 +26,15 @@ struct TimedScope {
   TimedScope(int k, hipStream_t st, bool deferred = false) : kind(k), s(st) { timing_begin(kind, s, deferred); }
   ~TimedScope() { timing_end(kind, s); }
 };
+
+// Launch kern<<<grid, block, 0, s>>>(args...), through hipExtLaunchKernelGGL
+// with the events of an enclosing deferred scope when it hands them over.
+template <typename K, typename... A>
+inline void launch_with_timing(K kern, dim3 grid, dim3 block, hipStream_t s, A... args) {
+  hipEvent_t e0, e1;
+  if (timing_claim(&e0, &e1)) hipExtLaunchKernelGGL(kern, grid, block, 0, s, e0, e1, 0, args...);
+  else kern<<<grid, block, 0, s>>>(args...);
+}
 
 // ---- router forward and backward (kernels_router.hip) ----
 // Decode-time routing of the scored tokens, folded into the router (thr null:

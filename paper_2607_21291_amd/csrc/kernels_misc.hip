@@ -232,9 +232,9 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(const float* __restr
 
 hipError_t launch_topk(const float* scores, int B, int T, int k, int32_t* idx, hipStream_t s) {
   if (k == 0 || B == 0) return hipSuccess;
-  TimedScope ts(DSF_KIND_TOPK, s);
-  if (T <= kTopkLdsKeys) topk_kernel<true><<<B, kTopkThreads, 0, s>>>(scores, T, k, idx);
-  else topk_kernel<false><<<B, kTopkThreads, 0, s>>>(scores, T, k, idx);
+  TimedScope ts(DSF_KIND_TOPK, s, true);
+  if (T <= kTopkLdsKeys) launch_with_timing(topk_kernel<true>, dim3(B), dim3(kTopkThreads), s, scores, T, k, idx);
+  else launch_with_timing(topk_kernel<false>, dim3(B), dim3(kTopkThreads), s, scores, T, k, idx);
   return hipGetLastError();
 }
 
@@ -284,13 +284,15 @@ hipError_t launch_gather(int dtype, const void* x, int B, int T, int d, const in
                          void* out, hipStream_t s) {
   int64_t rows = int64_t(B) * k;
   if (rows == 0) return hipSuccess;
-  TimedScope ts(DSF_KIND_GATHER, s);
+  TimedScope ts(DSF_KIND_GATHER, s, true);
   if (dtype == DSF_BF16) {
     int64_t nvec = rows * (d / 8);
-    gather_kernel<uint16_t><<<stream_grid(nvec), 256, 0, s>>>((const uint16_t*)x, T, d, idx, k, (uint16_t*)out, nvec);
+    launch_with_timing(gather_kernel<uint16_t>, dim3(stream_grid(nvec)), dim3(256), s, (const uint16_t*)x, T, d, idx,
+                       k, (uint16_t*)out, nvec);
   } else {
     int64_t nvec = rows * (d / 4);
-    gather_kernel<float><<<stream_grid(nvec), 256, 0, s>>>((const float*)x, T, d, idx, k, (float*)out, nvec);
+    launch_with_timing(gather_kernel<float>, dim3(stream_grid(nvec)), dim3(256), s, (const float*)x, T, d, idx, k,
+                       (float*)out, nvec);
   }
   return hipGetLastError();
 }
@@ -299,13 +301,15 @@ hipError_t launch_scatter(int dtype, void* x, const void* delta, int B, int T, i
                           int k, hipStream_t s) {
   int64_t rows = int64_t(B) * k;
   if (rows == 0) return hipSuccess;
-  TimedScope ts(DSF_KIND_SCATTER, s);
+  TimedScope ts(DSF_KIND_SCATTER, s, true);
   if (dtype == DSF_BF16) {
     int64_t nvec = rows * (d / 8);
-    scatter_kernel<uint16_t><<<stream_grid(nvec), 256, 0, s>>>((uint16_t*)x, (const uint16_t*)delta, T, d, idx, k, nvec);
+    launch_with_timing(scatter_kernel<uint16_t>, dim3(stream_grid(nvec)), dim3(256), s, (uint16_t*)x,
+                       (const uint16_t*)delta, T, d, idx, k, nvec);
   } else {
     int64_t nvec = rows * (d / 4);
-    scatter_kernel<float><<<stream_grid(nvec), 256, 0, s>>>((float*)x, (const float*)delta, T, d, idx, k, nvec);
+    launch_with_timing(scatter_kernel<float>, dim3(stream_grid(nvec)), dim3(256), s, (float*)x, (const float*)delta, T,
+                       d, idx, k, nvec);
   }
   return hipGetLastError();
 }
@@ -456,18 +460,18 @@ static hipError_t launch_norm_lm(const NormArgs& a, int chunks, hipStream_t s) {
   const int64_t rows = int64_t(a.B) * a.kk;
   const unsigned grid = unsigned((rows + 4 * (64 / L) - 1) / (4 * (64 / L)));
   switch (chunks) {
-    case 1: norm_kernel<T, L, 1, EXACT, MODE><<<grid, 256, 0, s>>>(a); break;
-    case 2: norm_kernel<T, L, 2, EXACT, MODE><<<grid, 256, 0, s>>>(a); break;
-    case 3: norm_kernel<T, L, 3, EXACT, MODE><<<grid, 256, 0, s>>>(a); break;
-    case 4: norm_kernel<T, L, 4, EXACT, MODE><<<grid, 256, 0, s>>>(a); break;
-    case 5: norm_kernel<T, L, 5, EXACT, MODE><<<grid, 256, 0, s>>>(a); break;
-    case 6: norm_kernel<T, L, 6, EXACT, MODE><<<grid, 256, 0, s>>>(a); break;
-    case 7: norm_kernel<T, L, 7, EXACT, MODE><<<grid, 256, 0, s>>>(a); break;
-    case 8: norm_kernel<T, L, 8, EXACT, MODE><<<grid, 256, 0, s>>>(a); break;
+    case 1: launch_with_timing(norm_kernel<T, L, 1, EXACT, MODE>, dim3(grid), dim3(256), s, a); break;
+    case 2: launch_with_timing(norm_kernel<T, L, 2, EXACT, MODE>, dim3(grid), dim3(256), s, a); break;
+    case 3: launch_with_timing(norm_kernel<T, L, 3, EXACT, MODE>, dim3(grid), dim3(256), s, a); break;
+    case 4: launch_with_timing(norm_kernel<T, L, 4, EXACT, MODE>, dim3(grid), dim3(256), s, a); break;
+    case 5: launch_with_timing(norm_kernel<T, L, 5, EXACT, MODE>, dim3(grid), dim3(256), s, a); break;
+    case 6: launch_with_timing(norm_kernel<T, L, 6, EXACT, MODE>, dim3(grid), dim3(256), s, a); break;
+    case 7: launch_with_timing(norm_kernel<T, L, 7, EXACT, MODE>, dim3(grid), dim3(256), s, a); break;
+    case 8: launch_with_timing(norm_kernel<T, L, 8, EXACT, MODE>, dim3(grid), dim3(256), s, a); break;
     default:
       if constexpr (EXACT) return hipErrorInvalidValue;
-      if (chunks <= 12) norm_kernel<T, L, 12, false, MODE><<<grid, 256, 0, s>>>(a);
-      else if (chunks <= 16) norm_kernel<T, L, 16, false, MODE><<<grid, 256, 0, s>>>(a);
+      if (chunks <= 12) launch_with_timing(norm_kernel<T, L, 12, false, MODE>, dim3(grid), dim3(256), s, a);
+      else if (chunks <= 16) launch_with_timing(norm_kernel<T, L, 16, false, MODE>, dim3(grid), dim3(256), s, a);
       else return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -500,7 +504,7 @@ static hipError_t launch_norm_t(const NormArgs& a, hipStream_t s) {
 
 hipError_t launch_norm(const NormArgs& a, hipStream_t s) {
   if (int64_t(a.B) * a.kk == 0) return hipSuccess;
-  TimedScope ts(DSF_KIND_NORM, s);
+  TimedScope ts(DSF_KIND_NORM, s, true);
   return a.dtype == DSF_BF16 ? launch_norm_t<uint16_t>(a, s) : launch_norm_t<float>(a, s);
 }
 

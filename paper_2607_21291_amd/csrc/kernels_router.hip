@@ -167,11 +167,11 @@ hipError_t launch_router(int dtype, const void* x, int64_t n, int d, int d_r, co
                          const void* b1, const void* w2, float b2, float* scores, hipStream_t s,
                          const RouteArgs* route) {
   if (n == 0) return hipSuccess;
-  TimedScope ts(DSF_KIND_ROUTER, s);
+  TimedScope ts(DSF_KIND_ROUTER, s, true);
   const RouteArgs ra = route ? *route : RouteArgs{};
   if (dtype == DSF_F32) {
-    router_f32_kernel<<<unsigned((n + 3) / 4), 256, 0, s>>>((const float*)x, n, d, d_r, (const float*)w1,
-                                                            (const float*)b1, (const float*)w2, b2, scores, ra);
+    launch_with_timing(router_f32_kernel, dim3(unsigned((n + 3) / 4)), dim3(256), s, (const float*)x, n, d, d_r,
+                       (const float*)w1, (const float*)b1, (const float*)w2, b2, scores, ra);
     return hipGetLastError();
   }
   unsigned grid = unsigned((n + kRouterTokens - 1) / kRouterTokens);
@@ -180,10 +180,10 @@ hipError_t launch_router(int dtype, const void* x, int64_t n, int d, int d_r, co
   auto B1 = (const uint16_t*)b1;
   auto W2 = (const uint16_t*)w2;
   switch (d_r) {
-    case 16: router_bf16_kernel<16><<<grid, 64 * kRouterWaves, 0, s>>>(X, n, d, W1, B1, W2, b2, scores, ra); break;
-    case 32: router_bf16_kernel<32><<<grid, 64 * kRouterWaves, 0, s>>>(X, n, d, W1, B1, W2, b2, scores, ra); break;
-    case 48: router_bf16_kernel<48><<<grid, 64 * kRouterWaves, 0, s>>>(X, n, d, W1, B1, W2, b2, scores, ra); break;
-    case 64: router_bf16_kernel<64><<<grid, 64 * kRouterWaves, 0, s>>>(X, n, d, W1, B1, W2, b2, scores, ra); break;
+    case 16: launch_with_timing(router_bf16_kernel<16>, dim3(grid), dim3(64 * kRouterWaves), s, X, n, d, W1, B1, W2, b2, scores, ra); break;
+    case 32: launch_with_timing(router_bf16_kernel<32>, dim3(grid), dim3(64 * kRouterWaves), s, X, n, d, W1, B1, W2, b2, scores, ra); break;
+    case 48: launch_with_timing(router_bf16_kernel<48>, dim3(grid), dim3(64 * kRouterWaves), s, X, n, d, W1, B1, W2, b2, scores, ra); break;
+    case 64: launch_with_timing(router_bf16_kernel<64>, dim3(grid), dim3(64 * kRouterWaves), s, X, n, d, W1, B1, W2, b2, scores, ra); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -256,7 +256,7 @@ hipError_t launch_router_topk(const void* x, int B, int T, int d, int d_r, const
                               hipStream_t s) {
   if (B == 0 || T == 0) return hipSuccess;
   if (!router_topk_fusable(DSF_BF16, T, d_r) || k < 1 || k > T) return hipErrorInvalidValue;
-  TimedScope ts(DSF_KIND_ROUTER, s);
+  TimedScope ts(DSF_KIND_ROUTER, s, true);
   const int64_t n = int64_t(B) * T;
   const unsigned grid = unsigned(n / kRouterTokens);
   auto X = (const uint16_t*)x;
@@ -264,10 +264,10 @@ hipError_t launch_router_topk(const void* x, int B, int T, int d, int d_r, const
   auto B1 = (const uint16_t*)b1;
   auto W2 = (const uint16_t*)w2;
   switch (d_r) {
-    case 16: router_topk_bf16_kernel<16><<<grid, kRouterThreads, 0, s>>>(X, n, d, W1, B1, W2, b2, scores, T, k, idx, count); break;
-    case 32: router_topk_bf16_kernel<32><<<grid, kRouterThreads, 0, s>>>(X, n, d, W1, B1, W2, b2, scores, T, k, idx, count); break;
-    case 48: router_topk_bf16_kernel<48><<<grid, kRouterThreads, 0, s>>>(X, n, d, W1, B1, W2, b2, scores, T, k, idx, count); break;
-    default: router_topk_bf16_kernel<64><<<grid, kRouterThreads, 0, s>>>(X, n, d, W1, B1, W2, b2, scores, T, k, idx, count); break;
+    case 16: launch_with_timing(router_topk_bf16_kernel<16>, dim3(grid), dim3(kRouterThreads), s, X, n, d, W1, B1, W2, b2, scores, T, k, idx, count); break;
+    case 32: launch_with_timing(router_topk_bf16_kernel<32>, dim3(grid), dim3(kRouterThreads), s, X, n, d, W1, B1, W2, b2, scores, T, k, idx, count); break;
+    case 48: launch_with_timing(router_topk_bf16_kernel<48>, dim3(grid), dim3(kRouterThreads), s, X, n, d, W1, B1, W2, b2, scores, T, k, idx, count); break;
+    default: launch_with_timing(router_topk_bf16_kernel<64>, dim3(grid), dim3(kRouterThreads), s, X, n, d, W1, B1, W2, b2, scores, T, k, idx, count); break;
   }
   return hipGetLastError();
 }
