@@ -942,9 +942,9 @@ DecodePlan make_decode_plan(const dsf_layer_desc& D, int dtype, int B, int max_p
   // few-row GEMMs (bf16, B <= 16): split-K partial tiles
   const bool few = dtype == DSF_BF16 && B <= 16;
   p.spart = few ? take(gemm_skinny_partial_bytes()) : 0;
-  // counters, zero at the start of a step: decode attention (B * Hq), then the
-  // few-row GEMMs' tile counters
-  const int64_t na = int64_t(n) * D.n_heads, ns = few ? gemm_skinny_counters() : 0;
+  // counters, zero at the start of a step: decode attention (B * Hq chunk
+  // counters, then B head counters), then the few-row GEMMs' tile counters
+  const int64_t na = int64_t(n) * D.n_heads + n, ns = few ? gemm_skinny_counters() : 0;
   p.ncounters = na + ns;
   p.counters = take(sizeof(uint32_t) * size_t(p.ncounters));
   p.acount = p.counters;
@@ -1035,11 +1035,10 @@ int run_decode_layer(const DecCtx& c, const dsf_layer_weights* W, void* x, const
     q.rope = dat<float>(c, c.plan.rope);
     DSF_HIP(launch_gemm(q, c.s));
   }
-  DSF_HIP(launch_kv_append(c.dtype, dat<char>(c, c.plan.k), dat<char>(c, c.plan.v), keep, ck, cv, len, B, Hkv, hd,
-                           c.cap, c.s));
-  DSF_HIP(launch_decode_attention(c.dtype, dat<char>(c, c.plan.q), ck, cv, len, B, Hq, Hkv, hd, c.cap,
-                                  dat<float>(c, c.plan.part), dat<uint32_t>(c, c.plan.acount),
-                                  dat<char>(c, c.plan.attn), c.s));
+  // attention over the cache and the new token, appending the kept tokens' rows
+  DSF_HIP(launch_decode_attention(c.dtype, dat<char>(c, c.plan.q), ck, cv, len, dat<char>(c, c.plan.k),
+                                  dat<char>(c, c.plan.v), keep, B, Hq, Hkv, hd, c.cap, dat<float>(c, c.plan.part),
+                                  dat<uint32_t>(c, c.plan.acount), dat<char>(c, c.plan.attn), c.s));
   if (!qwen) {  // parallel residual: [attn | act] . [W_o | W_down]^T + biases, gated by keep
     GemmArgs o = g;
     o.N = d; o.K = dq + f; o.K1 = dq;

@@ -221,16 +221,17 @@ hipError_t launch_attention(int dtype, const void* q, const void* k, const void*
                             int Hkv, int n, int hd, void* out, hipStream_t s, float* lse = nullptr);
 
 // ---- incremental decoding (kernels_decode.hip) ----
-hipError_t launch_kv_append(int dtype, const void* knew, const void* vnew, const int32_t* keep, void* ck, void* cv,
-                            int32_t* cache_len, int B, int Hkv, int hd, int cap, hipStream_t s);
 int decode_attn_chunks(int cap);
 constexpr int kDecodeMaxCap = 256 * 256;  // cache slots the decode attention supports
 // q [B, Hq, hd]; caches [B, Hkv, cap, hd] with cache_len[b] valid slots;
-// part: B * Hq * decode_attn_chunks(cap) * (hd + 2) floats; count: B * Hq
+// part: B * Hq * decode_attn_chunks(cap) * (hd + 2) floats; count: B * Hq + B
 // words, zero before the launch (the launch leaves them zero); out [B, Hq * hd].
-hipError_t launch_decode_attention(int dtype, const void* q, const void* ck, const void* cv,
-                                   const int32_t* cache_len, int B, int Hq, int Hkv, int hd, int cap, float* part,
-                                   uint32_t* count, void* out, hipStream_t s);
+// keep (nullable): a kept sequence's new rows knew / vnew [B, Hkv, hd] join
+// the attention as slot cache_len[b], are copied into that slot, and
+// cache_len[b] grows by one (the cache append of a decode step).
+hipError_t launch_decode_attention(int dtype, const void* q, const void* ck, const void* cv, int32_t* cache_len,
+                                   const void* knew, const void* vnew, const int32_t* keep, int B, int Hq, int Hkv,
+                                   int hd, int cap, float* part, uint32_t* count, void* out, hipStream_t s);
 hipError_t launch_kv_fill(int dtype, const void* ks, const void* vs, void* ck, void* cv, int32_t* cache_len, int B,
                           int Hkv, int hd, int k, int cap, hipStream_t s);
 hipError_t launch_kept_min_score(const float* scores, const int32_t* idx, int B, int T, int k, float* thr,

@@ -6,10 +6,10 @@
 // The projections of a decode step run on the few-row GEMM and the routing
 // flags come from the router kernel; the kernels here are the other pieces
 // decoding adds:
-// - the append of the kept tokens' keys and values to the caches;
-// - attention of one query per (sequence, head) over its cache, split into
-//   chunks of keys whose last-arriving workgroup combines them in chunk
-//   order (memory-bound: it reads the cache once);
+// - attention of one query per (sequence, head) over its cache and the new
+//   token, split into chunks of keys whose last-arriving workgroup combines
+//   them in chunk order (memory-bound: it reads the cache once), which also
+//   appends the kept tokens' keys and values to the caches;
 // - for a prefill: copying each layer's kept keys/values into the caches and
 //   the lowest kept score per sequence (the threshold that continues the
 //   prompt's selection).
@@ -19,37 +19,6 @@
 #include "dsf_internal.h"
 
 namespace dsf {
-
-// One workgroup per sequence: a kept token's key and value rows (all kv heads)
-// go to slot cache_len[b] of its caches, then the length grows by one (after
-// every head has been written, so readers of the length see whole rows).
-__global__ __launch_bounds__(256) void kv_append_kernel(const u32x4* __restrict__ knew, const u32x4* __restrict__ vnew,
-                                                        const int32_t* __restrict__ keep, u32x4* __restrict__ ck,
-                                                        u32x4* __restrict__ cv, int32_t* __restrict__ cache_len,
-                                                        int Hkv, int row_vecs, int cap) {
-  const int b = blockIdx.x;
-  if (!keep[b]) return;  // uniform over the workgroup
-  const int slot = cache_len[b];
-  const int n = Hkv * row_vecs;
-  for (int i = threadIdx.x; i < n; i += blockDim.x) {
-    const int h = i / row_vecs, e = i - h * row_vecs;
-    const int64_t src = (int64_t(b) * Hkv + h) * row_vecs + e;
-    const int64_t dst = ((int64_t(b) * Hkv + h) * cap + slot) * row_vecs + e;
-    ck[dst] = knew[src];
-    cv[dst] = vnew[src];
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) cache_len[b] = slot + 1;
-}
-
-hipError_t launch_kv_append(int dtype, const void* knew, const void* vnew, const int32_t* keep, void* ck, void* cv,
-                            int32_t* cache_len, int B, int Hkv, int hd, int cap, hipStream_t s) {
-  if (B == 0) return hipSuccess;
-  const int row_vecs = hd * (dtype == DSF_BF16 ? 2 : 4) / 16;
-  kv_append_kernel<<<B, 256, 0, s>>>((const u32x4*)knew, (const u32x4*)vnew, keep, (u32x4*)ck, (u32x4*)cv,
-                                     cache_len, Hkv, row_vecs, cap);
-  return hipGetLastError();
-}
 
 // ------------------------------------------------------- decode attention
 
@@ -106,10 +75,22 @@ constexpr int kDecChunk = 256;  // keys per workgroup of the decode attention
 // last chunk of (b, h) to arrive resets the counter and combines the chunks in
 // chunk order: out = sum_c o_c e^(m_c - M) / sum_c l_c e^(m_c - M), M the
 // largest m_c (0 for an empty cache). No workgroup waits for another.
+//
+// With keep non-null the launch also appends the step's new key and value
+// rows (knew, vnew [B, Hkv, HD]) of every kept sequence: attention runs over
+// the cache_len[b] cached slots plus the new token, whose rows every
+// workgroup reads from knew / vnew (so no workgroup reads the slot being
+// written); the workgroup of the first query head of each kv head whose
+// chunk holds slot cache_len[b] copies them into that slot; and once the
+// last head of sequence b has combined (a second counter, count[B Hq + b]),
+// cache_len[b] grows by one. Every workgroup of b has read cache_len[b]
+// before it counted itself, so none sees the new length.
 template <typename T, int HD>
 __global__ __launch_bounds__(256) void decode_attn_kernel(const T* __restrict__ q, const T* __restrict__ ck,
                                                           const T* __restrict__ cv,
-                                                          const int32_t* __restrict__ cache_len, int Hq, int Hkv,
+                                                          int32_t* __restrict__ cache_len, const T* __restrict__ knew,
+                                                          const T* __restrict__ vnew,
+                                                          const int32_t* __restrict__ keep, int Hq, int Hkv,
                                                           int cap, float* __restrict__ part,
                                                           uint32_t* __restrict__ count, T* __restrict__ out) {
   constexpr int VEC = 16 / int(sizeof(T));  // elements per 16-byte vector
@@ -126,7 +107,9 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const T* __restrict__ 
   const int c = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const int nch = gridDim.x;
   const int tid = threadIdx.x, sub = tid % LPK, row = tid / LPK;
-  const int len = min(cache_len[b], cap);
+  const int len_old = min(cache_len[b], cap);
+  const int kp = keep && keep[b] && len_old < cap ? 1 : 0;  // the new token joins at slot len_old
+  const int len = len_old + kp;
   const int k0 = c * kDecChunk;
   const int64_t bh = int64_t(b) * Hq + h;
   const int kvh = h / (Hq / Hkv);
@@ -136,6 +119,19 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const T* __restrict__ 
   for (int i = 0; i < VEC; ++i) qv[i] = DecElem<T>::to_f(qr[i]);
   const T* kbase = ck + ((int64_t(b) * Hkv + kvh) * cap) * HD + sub * VEC;
   const T* vbase = cv + ((int64_t(b) * Hkv + kvh) * cap) * HD + sub * VEC;
+  // the new token's rows (read only when kp)
+  const T* knb = knew + (int64_t(b) * Hkv + kvh) * HD + sub * VEC;
+  const T* vnb = vnew + (int64_t(b) * Hkv + kvh) * HD + sub * VEC;
+  // key row `key` (< len): a cached slot, or the new token at slot len_old
+  auto krow = [&](int key) { return key < len_old ? kbase + int64_t(key) * HD : knb; };
+  auto vrow = [&](int key) { return key < len_old ? vbase + int64_t(key) * HD : vnb; };
+  if (kp && c == len_old / kDecChunk && h % (Hq / Hkv) == 0 && row == 0) {
+    // one row group copies the new rows into slot len_old (nobody reads that slot here)
+    T* kd = const_cast<T*>(kbase) + int64_t(len_old) * HD;
+    T* vd = const_cast<T*>(vbase) + int64_t(len_old) * HD;
+    *reinterpret_cast<u32x4*>(kd) = *reinterpret_cast<const u32x4*>(knb);
+    *reinterpret_cast<u32x4*>(vd) = *reinterpret_cast<const u32x4*>(vnb);
+  }
   const float scale = 1.0f / sqrtf(float(HD));
   float o[VEC];
 #pragma unroll
@@ -148,12 +144,12 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const T* __restrict__ 
 #pragma unroll
     for (int pass = 0; pass < NPASS; ++pass) {
       const int key = k0 + pass * KPP + row;
-      kr[pass] = key < len ? *reinterpret_cast<const u32x4*>(kbase + int64_t(key) * HD) : u32x4{0u, 0u, 0u, 0u};
+      kr[pass] = key < len ? *reinterpret_cast<const u32x4*>(krow(key)) : u32x4{0u, 0u, 0u, 0u};
     }
 #pragma unroll
     for (int pass = 0; pass < NPASS; ++pass) {
       const int key = k0 + pass * KPP + row;
-      vr[pass] = key < len ? *reinterpret_cast<const u32x4*>(vbase + int64_t(key) * HD) : u32x4{0u, 0u, 0u, 0u};
+      vr[pass] = key < len ? *reinterpret_cast<const u32x4*>(vrow(key)) : u32x4{0u, 0u, 0u, 0u};
     }
 #pragma unroll
     for (int pass = 0; pass < NPASS; ++pass) {
@@ -189,7 +185,7 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const T* __restrict__ 
       float acc = 0.f;
       if (key < len) {
         T kv[VEC];
-        *reinterpret_cast<u32x4*>(kv) = *reinterpret_cast<const u32x4*>(kbase + int64_t(key) * HD);
+        *reinterpret_cast<u32x4*>(kv) = *reinterpret_cast<const u32x4*>(krow(key));
 #pragma unroll
         for (int i = 0; i < VEC; ++i) acc = fmaf(qv[i], DecElem<T>::to_f(kv[i]), acc);
       }
@@ -208,7 +204,7 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const T* __restrict__ 
       const int j = pass * KPP + row, key = k0 + j;
       if (key < len) {
         T vv[VEC];
-        *reinterpret_cast<u32x4*>(vv) = *reinterpret_cast<const u32x4*>(vbase + int64_t(key) * HD);
+        *reinterpret_cast<u32x4*>(vv) = *reinterpret_cast<const u32x4*>(vrow(key));
         const float pp = ps[j];
 #pragma unroll
         for (int i = 0; i < VEC; ++i) o[i] = fmaf(pp, DecElem<T>::to_f(vv[i]), o[i]);
@@ -268,13 +264,22 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(const T* __restrict__ 
     }
     out[bh * HD + tid] = DecElem<T>::from_f(L > 0.f ? O / L : 0.f);
   }
+  if (keep && tid == 0) {
+    // the last head of sequence b to combine moves its cache length
+    uint32_t* cb = count + int64_t(gridDim.z) * Hq + b;
+    const uint32_t old = __hip_atomic_fetch_add(cb, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (old == uint32_t(Hq - 1)) {
+      __hip_atomic_store(cb, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (kp) cache_len[b] = len;
+    }
+  }
 }
 
 int decode_attn_chunks(int cap) { return (cap + kDecChunk - 1) / kDecChunk; }
 
-hipError_t launch_decode_attention(int dtype, const void* q, const void* ck, const void* cv,
-                                   const int32_t* cache_len, int B, int Hq, int Hkv, int hd, int cap, float* part,
-                                   uint32_t* count, void* out, hipStream_t s) {
+hipError_t launch_decode_attention(int dtype, const void* q, const void* ck, const void* cv, int32_t* cache_len,
+                                   const void* knew, const void* vnew, const int32_t* keep, int B, int Hq, int Hkv,
+                                   int hd, int cap, float* part, uint32_t* count, void* out, hipStream_t s) {
   if (B == 0) return hipSuccess;
   if (cap > kDecodeMaxCap) return hipErrorInvalidValue;
   const int nch = decode_attn_chunks(cap);
@@ -282,8 +287,9 @@ hipError_t launch_decode_attention(int dtype, const void* q, const void* ck, con
   auto run = [&](auto tag, auto hdc) -> hipError_t {
     using T = decltype(tag);
     constexpr int HD = decltype(hdc)::value;
-    decode_attn_kernel<T, HD><<<grid, 256, 0, s>>>((const T*)q, (const T*)ck, (const T*)cv, cache_len, Hq, Hkv, cap,
-                                                   part, count, (T*)out);
+    decode_attn_kernel<T, HD><<<grid, 256, 0, s>>>((const T*)q, (const T*)ck, (const T*)cv, cache_len,
+                                                   (const T*)knew, (const T*)vnew, keep, Hq, Hkv, cap, part, count,
+                                                   (T*)out);
     return hipGetLastError();
   };
   const bool bf = dtype == DSF_BF16;
