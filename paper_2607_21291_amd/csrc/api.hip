@@ -113,6 +113,22 @@ bool timing_claim(hipEvent_t* start, hipEvent_t* stop) {
   *stop = r.stop;
   return true;
 }
+void timing_continue(hipStream_t s) {
+  std::lock_guard<std::mutex> lock(g_tmu);
+  if (g_open < 0) return;
+  TimingRec& r = g_recs[g_open];
+  if (!r.deferred || !r.claimed) return;
+  const int kind = r.kind;
+  ++g_used;
+  g_open = -1;
+  if (g_used >= g_recs.size()) return;
+  TimingRec& n = g_recs[g_used];
+  n.kind = kind;
+  n.deferred = true;
+  n.claimed = false;
+  g_open = long(g_used);
+  (void)s;
+}
 void timing_end(int kind, hipStream_t s) {
   std::lock_guard<std::mutex> lock(g_tmu);
   if (g_open < 0 || g_recs[g_open].kind != kind) return;

@@ -174,9 +174,17 @@ struct GemmArgs {
   // grid (0: one tile per workgroup); 1 if its last round is split along K
   int ntm; int px; int split;
   // set by the launcher for one-tile-per-workgroup grids: tiles are taken in
-  // bands of group_m tile rows, column by column (0: row-major)
-  int group_m;
+  // bands of group_m tile rows, column by column (0: row-major); ntn is the
+  // number of N tiles
+  int group_m; int ntn;
+  // set by the launcher for the split last round (gemm_bf16_tail_kernel):
+  // tiles tail0 .. tail0 + tail_r - 1 of the tile order, each split into
+  // tail_s pieces of its k-tiles
+  int tail0, tail_r, tail_s;
 };
+// Timing of a GEMM launched as two kernels: closes the record the first
+// launch claimed and opens another of the same kind for the second.
+void timing_continue(hipStream_t s);
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t s);
 
 // ---- backward of the routed layer (kernels_bwd.hip) ----

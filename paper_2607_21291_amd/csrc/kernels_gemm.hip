@@ -544,6 +544,38 @@ __device__ __forceinline__ void dma16(const RowSrc& src, uint32_t voff, uint32_t
 
 // Device-side pieces of the LDS-DMA GEMM: the main loop over a range of
 // k-tiles of one output tile, and the fused epilogue of a finished tile.
+// Tile configurations of the LDS-DMA GEMM (DSF_GEMM_USE_DMA=0 keeps every
+// bf16 GEMM on the register-staged kernel). Small: 128 x 128 tiles of four
+// 64 x 64 waves, two workgroups per CU. Large: 256 x 256 tiles of eight
+// 64 x 128 waves, one workgroup per CU; per flop it loads half the tile
+// bytes from L2 and reads half the fragment bytes from LDS, which pays when
+// there are enough tiles to fill the chip (the large projections).
+#ifndef DSF_GEMM_USE_DMA
+#define DSF_GEMM_USE_DMA 1
+#endif
+struct TileSmall {
+  static constexpr int BM = 128, BN = 128, WM = 64, WN = 64, NS = 2, BK = 64;
+};
+struct TileLarge {
+  static constexpr int BM = 256, BN = 256, WM = 64, WN = 128, NS = 2, BK = 64;
+};
+
+// Stream-K partial tiles: one slot per workgroup of a persistent grid, at
+// most kSkMaxSlots workgroups (2 per CU on a 256-CU device with small tiles,
+// 1 with large tiles).
+constexpr int kSkMaxSlots = 512;
+constexpr int kSkMinIters = 8;  // mean k-iterations per workgroup below which one tile per workgroup is kept
+constexpr int kSkMinK = 32;    // k-iterations per tile below which the partial sums cost more than they save
+// Split last round (choose_tail): at most this many pieces per tile, each at
+// least this many k-iterations long.
+constexpr int kTailMaxSplit = 4;
+constexpr int kTailMinK = 8;
+constexpr int kGroupM = 4;      // tile rows per band of the grouped tile order
+constexpr int kGroupMinCols = 8;  // below this many tile columns row-major order is already compact
+constexpr size_t kSkPartBytes = size_t(kSkMaxSlots) / 2 * TileLarge::BM * TileLarge::BN * sizeof(float);
+static_assert(kSkPartBytes >= size_t(kSkMaxSlots) * TileSmall::BM * TileSmall::BN * sizeof(float),
+              "partial-tile slots of the small tiles");
+
 template <int EPI, int BM, int BN, int WM, int WN, int NS, int BK>
 struct DmaGemm {
   using C = DmaCfg<BM, BN, WM, WN, NS, BK>;
@@ -695,7 +727,14 @@ struct DmaGemm {
   }
 
   // Stage the finished tile (tm, tn) through LDS and apply the fused epilogue.
-  __device__ static __forceinline__ void epilogue(const GemmArgs& g, char* smem, int tm, int tn, Acc& acc) {
+  // NP > 0 (wave-staged tiles only): the tile's sum also takes the partials
+  // in slots slot0 .. slot0 + np - 1 (np <= NP, published before the call),
+  // added in slot order to each fragment as it is staged, a few fragments'
+  // loads in flight at a time; a partial beyond np is read beyond the end of
+  // the buffer, out of the resource's range, where every load returns zeros.
+  template <int NP = 0>
+  __device__ static __forceinline__ void epilogue(const GemmArgs& g, char* smem, int tm, int tn, Acc& acc,
+                                                  int slot0 = 0, int np = 0) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / (BN / WN), wn = wave % (BN / WN);
     const int r16 = lane & 15, grp = lane >> 4;
@@ -711,10 +750,27 @@ struct DmaGemm {
 #pragma unroll
         for (int ii = 0; ii < 2; ++ii)
 #pragma unroll
-          for (int j = 0; j < NI; ++j)
+          for (int j0 = 0; j0 < NI; j0 += kAddGroup) {
+            if constexpr (NP > 0) {
+              const auto r = part_rsrc(g);
+              const int vo = lane_offset();
 #pragma unroll
-            for (int e = 0; e < 4; ++e)
-              stage[(16 * ii + 4 * grp + e) * C::kStageLD + 16 * j + r16] = acc[2 * rnd + ii][j][e];
+              for (int pp = 0; pp < NP; ++pp) {
+                const int so = __builtin_amdgcn_readfirstlane(pp < np ? (slot0 + pp) * kSlotBytes : int(kSkPartBytes));
+#pragma unroll
+                for (int j = j0; j < j0 + kAddGroup; ++j)
+                  acc[2 * rnd + ii][j] += __builtin_bit_cast(
+                      f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, vo + ((2 * rnd + ii) * NI + j) * kFragBytes, so,
+                                                                   kCoherent));
+              }
+            }
+#pragma unroll
+            for (int j = j0; j < j0 + kAddGroup; ++j)
+#pragma unroll
+              for (int e = 0; e < 4; ++e)
+                stage[(16 * ii + 4 * grp + e) * C::kStageLD + 16 * j + r16] = acc[2 * rnd + ii][j][e];
+            if constexpr (NP > 0) __builtin_amdgcn_sched_barrier(0);
+          }
         __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS writes are done
         __builtin_amdgcn_wave_barrier();
         gemm_epilogue<uint16_t, 32, 128, 64, EPI>(g, stage, m0 + wm * WM + 32 * rnd, vtn, lane);
@@ -736,71 +792,67 @@ struct DmaGemm {
   }
 
   // Partial tiles of the stream-K schedule live in slot-major order, each in
-  // the accumulators' own register layout: (slot, wave, i, j, lane) -> f32x4.
-  __device__ static __forceinline__ f32x4* slot_ptr(const GemmArgs& g, int slot) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    return reinterpret_cast<f32x4*>(g.part) + (int64_t(slot) * C::kWaves + wave) * (MI * NI * 64) + lane;
-  }
+  // the accumulators' own register layout: (slot, wave, i, j, lane) -> f32x4,
+  // so fragment f = i * NI + j of a wave's partial sits kFragBytes * f after
+  // the lane's first one, and slot s starts kSlotBytes * s into the buffer.
+  static constexpr int kFragBytes = 64 * 16;
+  static constexpr int kSlotBytes = C::kWaves * MI * NI * kFragBytes;
 
   // The partial sums go from one workgroup to another, possibly on another
   // XCD (each XCD has its own L2). They are stored and loaded with
-  // device-scope coherent accesses (sc1), which is what the relaxed
-  // device-scope atomics on the flags use as well, so the hand-over needs only
-  // a completion wait: no write-back of the writer's whole L2 before the flag,
-  // no invalidation of the reader's L2 after it (both would cost every other
-  // workgroup on those XCDs its cached tiles).
-  // Fragment f = i * NI + j of a wave's partial sits at slot_ptr + 64 f. The
-  // accesses go 8 fragments per statement (2 address registers, immediate
-  // offsets of 1, 2, 3 KiB), and each statement waits for its own accesses, so
-  // no register it names is touched while its memory operation is in flight.
-  static_assert((MI * NI) % 8 == 0, "partials move in groups of 8 fragments");
-
-  __device__ static __forceinline__ void store_partial(const GemmArgs& g, const Acc& acc) {
-    const f32x4* a = &acc[0][0];
-    f32x4* p = slot_ptr(g, int(blockIdx.x));
-#pragma unroll
-    for (int c = 0; c < MI * NI; c += 8) {
-      const f32x4* v = a + c;
-      asm volatile(
-          "global_store_dwordx4 %0, %2, off sc1\n\t"
-          "global_store_dwordx4 %0, %3, off offset:1024 sc1\n\t"
-          "global_store_dwordx4 %0, %4, off offset:2048 sc1\n\t"
-          "global_store_dwordx4 %0, %5, off offset:3072 sc1\n\t"
-          "global_store_dwordx4 %1, %6, off sc1\n\t"
-          "global_store_dwordx4 %1, %7, off offset:1024 sc1\n\t"
-          "global_store_dwordx4 %1, %8, off offset:2048 sc1\n\t"
-          "global_store_dwordx4 %1, %9, off offset:3072 sc1\n\t"
-          "s_waitcnt vmcnt(0)"
-          :
-          : "v"(p + (c + 0) * 64), "v"(p + (c + 4) * 64), "v"(v[0]), "v"(v[1]), "v"(v[2]), "v"(v[3]), "v"(v[4]),
-            "v"(v[5]), "v"(v[6]), "v"(v[7])
-          : "memory");
-    }
+  // device-scope coherent accesses (sc1 in the buffer instructions' cache
+  // policy), which is what the relaxed device-scope atomics on the flags use
+  // as well, so the hand-over needs only a completion wait: no write-back of
+  // the writer's whole L2 before the flag, no invalidation of the reader's L2
+  // after it (both would cost every other workgroup on those XCDs its cached
+  // tiles). The accesses are compiler intrinsics, so the compiler places the
+  // waits for the loads and overlaps as many of them as registers allow.
+  static constexpr int kCoherent = 16;  // cache policy: sc1
+  static constexpr int kAddGroup = 8;
+  __device__ static __forceinline__ __amdgpu_buffer_rsrc_t part_rsrc(const GemmArgs& g) {
+    return __builtin_amdgcn_make_buffer_rsrc(g.part, (short)0, int(kSkPartBytes), 0x00020000);
+  }
+  __device__ static __forceinline__ int lane_offset() {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    return wave * (MI * NI * kFragBytes) + lane * 16;
   }
 
-  // acc += the partial in slot (published before this call)
-  __device__ static __forceinline__ void add_partial(const GemmArgs& g, int slot, Acc& acc) {
+  // Store the partial into slot; returns once every store has completed.
+  __device__ static __forceinline__ void store_partial(const GemmArgs& g, const Acc& acc, int slot) {
+    const f32x4* a = &acc[0][0];
+    const auto r = part_rsrc(g);
+    const int vo = lane_offset(), so = slot * kSlotBytes;
+#pragma unroll
+    for (int f = 0; f < MI * NI; ++f)
+      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, a[f]), r, vo + f * kFragBytes, so, kCoherent);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  }
+
+  // acc += the partials in slots slot0 .. slot0 + n - 1 (published before
+  // this call), added in slot order, n <= NMAX. Straight-line code over NMAX
+  // partials, so that the accumulators stay in place and the loads overlap:
+  // a partial beyond n is read at the end of the buffer, out of the
+  // resource's range, where every load returns zeros.
+  template <int NMAX>
+  __device__ static __forceinline__ void add_partials(const GemmArgs& g, int slot0, int n, Acc& acc) {
     f32x4* a = &acc[0][0];
-    const f32x4* p = slot_ptr(g, slot);
+    const auto r = part_rsrc(g);
+    const int vo = lane_offset();
+    int so[NMAX];
 #pragma unroll
-    for (int c = 0; c < MI * NI; c += 8) {
-      f32x4 v[8];
-      asm volatile(
-          "global_load_dwordx4 %0, %8, off sc1\n\t"
-          "global_load_dwordx4 %1, %8, off offset:1024 sc1\n\t"
-          "global_load_dwordx4 %2, %8, off offset:2048 sc1\n\t"
-          "global_load_dwordx4 %3, %8, off offset:3072 sc1\n\t"
-          "global_load_dwordx4 %4, %9, off sc1\n\t"
-          "global_load_dwordx4 %5, %9, off offset:1024 sc1\n\t"
-          "global_load_dwordx4 %6, %9, off offset:2048 sc1\n\t"
-          "global_load_dwordx4 %7, %9, off offset:3072 sc1\n\t"
-          "s_waitcnt vmcnt(0)"
-          : "=&v"(v[0]), "=&v"(v[1]), "=&v"(v[2]), "=&v"(v[3]), "=&v"(v[4]), "=&v"(v[5]), "=&v"(v[6]),
-            "=&v"(v[7])
-          : "v"(p + (c + 0) * 64), "v"(p + (c + 4) * 64)
-          : "memory");
+    for (int pp = 0; pp < NMAX; ++pp)
+      so[pp] = __builtin_amdgcn_readfirstlane(pp < n ? (slot0 + pp) * kSlotBytes : int(kSkPartBytes));
+    // kAddGroup fragments of every partial in flight at a time (their loads
+    // are not hoisted past the group boundary, which would spill)
 #pragma unroll
-      for (int f = 0; f < 8; ++f) a[c + f] = a[c + f] + v[f];
+    for (int f0 = 0; f0 < MI * NI; f0 += kAddGroup) {
+#pragma unroll
+      for (int f = f0; f < f0 + kAddGroup; ++f)
+#pragma unroll
+        for (int pp = 0; pp < NMAX; ++pp)
+          a[f] += __builtin_bit_cast(f32x4,
+                                     __builtin_amdgcn_raw_buffer_load_b128(r, vo + f * kFragBytes, so[pp], kCoherent));
+      __builtin_amdgcn_sched_barrier(0);
     }
   }
 };
@@ -813,12 +865,69 @@ template <int EPI, int BM, int BN, int WM, int WN, int NS, int BK>
 __global__ __launch_bounds__((DmaCfg<BM, BN, WM, WN, NS, BK>::kThreads)) void gemm_bf16_dma_kernel(GemmArgs g) {
   using G = DmaGemm<EPI, BM, BN, WM, WN, NS, BK>;
   __shared__ __attribute__((aligned(1024))) char smem[G::C::kSmem];
-  const int ntn = int(gridDim.x) / g.ntm;
-  const GemmTile t = gemm_tile(xcd_remap(int(blockIdx.x), int(gridDim.x)), g.ntm, ntn, g.group_m);
+  // the grid covers the first gridDim.x tiles of the order (all of them, or
+  // all but a split last round)
+  const GemmTile t = gemm_tile(xcd_remap(int(blockIdx.x), int(gridDim.x)), g.ntm, g.ntn, g.group_m);
   const int tm = t.tm, tn = t.tn;
   typename G::Acc acc;
   G::mainloop(g, smem, tm, tn, 0, g.K / BK, acc);
   G::epilogue(g, smem, tm, tn, acc);
+}
+
+// The last round of a one-tile-per-workgroup grid, split along K: tiles
+// tail0 .. tail0 + tail_r - 1 of the tile order, each cut into tail_s
+// contiguous pieces of its k-tiles, tail_s * tail_r pieces for at most as many
+// resident workgroups, so the round takes about 1 / tail_s of a tile. The
+// pieces of a tile run on one XCD (tile t on XCD t % 8, its pieces at
+// launch indices 8 (tail_s q + p) + t % 8 with q = t / 8), the last piece
+// at the highest index. The other pieces publish partial sums (slot
+// t (tail_s - 1) + p) with device-coherent stores and a flag; the last piece
+// waits for them in piece order, adds them and runs the fused epilogue. Only
+// the last piece waits, and only for workgroups of its XCD dispatched before
+// it that never wait: the waits end. The bounded spin of the stream-K kernel
+// guards them the same way (status word on a give-up).
+template <int EPI, int BM, int BN, int WM, int WN, int NS, int BK>
+__global__ __launch_bounds__((DmaCfg<BM, BN, WM, WN, NS, BK>::kThreads)) void gemm_bf16_tail_kernel(GemmArgs g) {
+  using G = DmaGemm<EPI, BM, BN, WM, WN, NS, BK>;
+  __shared__ __attribute__((aligned(1024))) char smem[G::C::kSmem];
+  __shared__ int n_seen;
+  const int s = g.tail_s;
+  const int x = int(blockIdx.x) % kXcds, m = int(blockIdx.x) / kXcds;
+  const int q = m / s, p = m - q * s, t = x + kXcds * q;
+  if (t >= g.tail_r) return;  // padding of the last group (uniform)
+  const int nk = g.K / BK;
+  const int kb = int(int64_t(nk) * p / s), ke = int(int64_t(nk) * (p + 1) / s);
+  const GemmTile tt = gemm_tile(g.tail0 + t, g.ntm, g.ntn, g.group_m);
+  typename G::Acc acc;
+  G::mainloop(g, smem, tt.tm, tt.tn, kb, ke, acc);
+  if (p < s - 1) {
+    const int slot = t * (s - 1) + p;
+    G::store_partial(g, acc, slot);
+    __syncthreads();  // every wave's partial stores have completed
+    if (threadIdx.x == 0) __hip_atomic_store(g.flags + slot, g.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return;
+  }
+  // the finisher (highest workgroup id of its tile) waits for the partials
+  // in piece order, then adds those it has seen
+  if (threadIdx.x == 0) {
+    int seen = 0;
+    for (; seen < s - 1; ++seen) {
+      int it = 0;
+      while (it < g.spin_limit &&
+             __hip_atomic_load(g.flags + t * (s - 1) + seen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != g.epoch) {
+        __builtin_amdgcn_s_sleep(2);
+        ++it;
+      }
+      if (it == g.spin_limit) break;
+    }
+    n_seen = seen;
+    if (seen < s - 1 && g.status)
+      __hip_atomic_fetch_or(g.status, uint32_t(DSF_WS_STATUS_SK_TIMEOUT), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  __syncthreads();  // the partials' loads below are issued after their flags were seen
+  // a partial not seen is left out (and reported) rather than waited for
+  G::template epilogue<kTailMaxSplit - 1>(g, smem, tt.tm, tt.tn, acc, t * (s - 1),
+                                          __builtin_amdgcn_readfirstlane(n_seen));
 }
 
 // Persistent grid of 8 * px workgroups (workgroup w runs on XCD w % 8 as the
@@ -874,7 +983,7 @@ __global__ __launch_bounds__((DmaCfg<BM, BN, WM, WN, NS, BK>::kThreads)) void ge
     G::mainloop(g, smem, tm, tn, kb, ke, acc);
     if (ke < nk) {
       // top of the piece, short of the tile's end: publish the partial sum
-      G::store_partial(g, acc);
+      G::store_partial(g, acc, int(blockIdx.x));
       __syncthreads();  // every wave's partial stores have completed
       if (threadIdx.x == 0) __hip_atomic_store(g.flags + blockIdx.x, g.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     } else {
@@ -900,7 +1009,7 @@ __global__ __launch_bounds__((DmaCfg<BM, BN, WM, WN, NS, BK>::kThreads)) void ge
         }
         __syncthreads();  // the partial's loads below are issued after its flag was seen
         if (spin_failed) break;  // left unfinished (and reported) rather than hang
-        G::add_partial(g, slot, acc);
+        G::template add_partials<1>(g, slot, 1, acc);
       }
       G::epilogue(g, smem, tm, tn, acc);
     }
@@ -975,34 +1084,6 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g) {
   __syncthreads();
   gemm_epilogue<float, kFBM, kFBN, 256, EPI>(g, stage, m0, tn, threadIdx.x);
 }
-
-// Tile configurations of the LDS-DMA GEMM (DSF_GEMM_USE_DMA=0 keeps every
-// bf16 GEMM on the register-staged kernel). Small: 128 x 128 tiles of four
-// 64 x 64 waves, two workgroups per CU. Large: 256 x 256 tiles of eight
-// 64 x 128 waves, one workgroup per CU; per flop it loads half the tile
-// bytes from L2 and reads half the fragment bytes from LDS, which pays when
-// there are enough tiles to fill the chip (the large projections).
-#ifndef DSF_GEMM_USE_DMA
-#define DSF_GEMM_USE_DMA 1
-#endif
-struct TileSmall {
-  static constexpr int BM = 128, BN = 128, WM = 64, WN = 64, NS = 2, BK = 64;
-};
-struct TileLarge {
-  static constexpr int BM = 256, BN = 256, WM = 64, WN = 128, NS = 2, BK = 64;
-};
-
-// Stream-K partial tiles: one slot per workgroup of a persistent grid, at
-// most kSkMaxSlots workgroups (2 per CU on a 256-CU device with small tiles,
-// 1 with large tiles).
-constexpr int kSkMaxSlots = 512;
-constexpr int kSkMinIters = 8;  // mean k-iterations per workgroup below which one tile per workgroup is kept
-constexpr int kSkMinK = 32;    // k-iterations per tile below which the partial sums cost more than they save
-constexpr int kGroupM = 4;      // tile rows per band of the grouped tile order
-constexpr int kGroupMinCols = 8;  // below this many tile columns row-major order is already compact
-constexpr size_t kSkPartBytes = size_t(kSkMaxSlots) / 2 * TileLarge::BM * TileLarge::BN * sizeof(float);
-static_assert(kSkPartBytes >= size_t(kSkMaxSlots) * TileSmall::BM * TileSmall::BN * sizeof(float),
-              "partial-tile slots of the small tiles");
 
 size_t gemm_partial_bytes() { return kSkPartBytes; }
 int gemm_flag_count() { return kSkMaxSlots; }
@@ -1082,6 +1163,31 @@ static Schedule choose_schedule(int nt, int nk, int slots, bool underfilled = fa
     return {px, 1};
   }
   return {0, 0};
+}
+
+// Split last round of a one-tile-per-workgroup grid of large tiles: with nt
+// tiles on P resident workgroups, the last nt mod P tiles would run alone in
+// a last round that leaves most CUs idle (the 3584-wide O and down
+// projections of the Qwen2.5-7B shape end 3.2-4.1 rounds). They go to a
+// second launch, each cut along K into s pieces, the largest s <= 4 with
+// s * r <= P and at least kTailMinK k-tiles per piece, so that round takes
+// about 1 / s of a tile. DSF_GEMM_TAIL (read at every launch): 0 turns the
+// split off; force splits as if 8 workgroups were resident (tests on small
+// grids).
+struct TailSplit {
+  int r, s;
+};
+static TailSplit choose_tail(int nt, int nk, int slots, int part_slots, bool avail) {
+  const char* e = getenv("DSF_GEMM_TAIL");
+  if (!avail || (e && e[0] == '0')) return {0, 1};
+  const bool force = e && !strcmp(e, "force");
+  const int P = force ? kXcds : slots;
+  if (P <= 0 || nt <= P) return {0, 1};
+  const int r = nt % P;
+  if (r == 0) return {0, 1};
+  for (int sp = kTailMaxSplit; sp >= 2; --sp)
+    if (sp * r <= P && r * (sp - 1) <= part_slots && nk / sp >= kTailMinK) return {r, sp};
+  return {0, 1};
 }
 
 // The DMA kernels address each operand through a buffer resource with a
@@ -1331,8 +1437,28 @@ static void launch_dma(const GemmArgs& g, hipStream_t s) {
     // row-major order.
     auto fn = gemm_bf16_dma_kernel<EPI, BM, BN, WM, WN, NS, BK>;
     const int slots = resident_slots<std::integral_constant<int, 32 + EPI * 2 + (BM > 128)>>((const void*)fn, Cfg::kThreads);
-    ga.group_m = ntn * ga.ntm > slots && ntn >= kGroupMinCols ? kGroupM : 0;
-    launch_timed(fn, dim3(ntn * ga.ntm), dim3(Cfg::kThreads), s, ga);
+    const int nt = ntn * ga.ntm;
+    ga.ntn = ntn;
+    ga.group_m = nt > slots && ntn >= kGroupMinCols ? kGroupM : 0;
+    // Large tiles of the forward epilogues, on a call's stream-K workspace:
+    // the last round of tiles split along K in a second launch. SwiGLU keeps
+    // one launch, so that a launch of that kind is always the whole gate|up
+    // projection (the duration its roofline figure is computed from).
+    if constexpr (BM == TileLarge::BM && BN == TileLarge::BN && EPI < EPI_STORE && EPI != EPI_SWIGLU) {
+      const TailSplit ts = choose_tail(nt, g.K / BK, slots, std::min(kPartSlots, gemm_flag_count()), g.part && g.flags);
+      if (ts.s > 1) {
+        ga.tail0 = nt - ts.r;
+        ga.tail_r = ts.r;
+        ga.tail_s = ts.s;
+        ga.spin_limit = spin_limit();
+        launch_timed(fn, dim3(nt - ts.r), dim3(Cfg::kThreads), s, ga);
+        timing_continue(s);
+        launch_timed(gemm_bf16_tail_kernel<EPI, BM, BN, WM, WN, NS, BK>,
+                     dim3(kXcds * ts.s * ((ts.r + kXcds - 1) / kXcds)), dim3(Cfg::kThreads), s, ga);
+        return;
+      }
+    }
+    launch_timed(fn, dim3(nt), dim3(Cfg::kThreads), s, ga);
   }
 }
 

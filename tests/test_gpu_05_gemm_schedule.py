@@ -179,6 +179,53 @@ def test_large_tile_stack_matches_layerwise(dev, monkeypatch, name):
     assert torch.equal(xd.cpu(), cur)
 
 
+# Shapes whose large-tile grids leave a ragged last round when 8 workgroups
+# are taken as resident (DSF_GEMM_TAIL=force), with K deep enough to cut:
+# NeoX (2200 kept rows, 9 tile rows): QKV 108 tiles and the fused O + down
+# projection 36 tiles, each 4 tiles in 2 pieces; Qwen (2 x 600 kept rows, 5
+# tile rows): QKV 35 tiles, 3 in 2 pieces; O 25 tiles, 1 in 2 pieces; down
+# (K 2560) 25 tiles, 1 in 4 pieces. The up projections (16 x 9 tiles; the
+# SwiGLU launch) are never split.
+TAIL = {
+    "neox_bf16_tail": (S.WORKLOADS["neox14b"].replace(
+        name="neox_bf16_tail", n_layers=1, d_model=1024, n_heads=8, n_kv_heads=8, head_dim=128, d_ff=4096,
+        rotary_dims=32, batch=1, seq=2400), 2200, {"gemm_qkv": 2, "gemm_up": 1, "gemm_down": 2}),
+    "qwen_bf16_tail": (S.WORKLOADS["qwen7b"].replace(
+        name="qwen_bf16_tail", n_layers=1, d_model=1280, n_heads=10, n_kv_heads=2, head_dim=128, d_ff=2560,
+        rotary_dims=128, batch=2, seq=700), 600, {"gemm_qkv": 2, "gemm_o": 2, "gemm_up": 1, "gemm_down": 2}),
+}
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("name", list(TAIL))
+def test_split_last_round_matches_oracle(dev, monkeypatch, name):
+    """The last round of large tiles cut along K into 2 or 4 pieces (a second
+    launch whose finishers add the others' partial sums in piece order): the
+    layer matches the oracle, repeats bitwise, and agrees with the unsplit
+    grid within tolerance; the timing records show two launches for each
+    split projection."""
+    w, k, launches = TAIL[name]
+    W = S.layer_weights(w, 0)
+    x = S.hidden_states(w)
+    monkeypatch.setenv("DSF_GEMM_TILE", "large")
+    monkeypatch.setenv("DSF_GEMM_TAIL", "force")
+    announce(f"split last round {name} k={k}")
+    P.timing_enable(64)
+    try:
+        y, scores, idx = run_layer(dev, w, W, x, k)
+        seen = {kind: P.timing_read(kind)[0] for kind in launches}
+    finally:
+        P.timing_enable(0)
+    assert seen == launches
+    check_layer(w, W, x, y, scores, idx, k)
+    y2, _, _ = run_layer(dev, w, W, x, k)
+    assert torch.equal(y, y2)
+    monkeypatch.setenv("DSF_GEMM_TAIL", "0")
+    y0, _, idx0 = run_layer(dev, w, W, x, k)
+    assert torch.equal(idx, idx0)
+    assert rel_inf(to_np(y) - to_np(x), to_np(y0) - to_np(x)) < TOL[w.dtype]
+
+
 def test_host_threads_get_their_own_second_streams(dev):
     # each host thread gets its own second stream (destroyed when the thread
     # exits); threads on their own caller streams and workspaces give the
