@@ -75,12 +75,58 @@ __device__ __forceinline__ void unpack8(const Raw8<T>& r, float* out) {
   }
 }
 
+// Rows of one thread in an epilogue of BM rows, BN columns, NT threads: its
+// chunk column, then rows rr0, rr0 + RSTEP, ... with their sequence, slot in
+// the kept list and position, and (residual kinds) the residual rows, read
+// ahead of the staged tile by epi_prefetch so that their memory latency
+// overlaps other work.
+template <typename T, int BM, int BN, int NT>
+struct EpiPre {
+  static constexpr int CPR = BN / 8, RSTEP = NT / CPR, RPT = (BM + RSTEP - 1) / RSTEP;
+  int bq[RPT], jq[RPT], pq[RPT];
+  bool live[RPT];
+  Raw8<T> xr[RPT];
+};
+
+template <typename T, int BM, int BN, int NT, int EPI>
+__device__ __forceinline__ void epi_prefetch(const GemmArgs& g, int m0, int tn, int tid, EpiPre<T, BM, BN, NT>& e) {
+  using E = EpiPre<T, BM, BN, NT>;
+  const int rr0 = tid / E::CPR, n = tn * BN + (tid % E::CPR) * 8;
+#pragma unroll
+  for (int q = 0; q < E::RPT; ++q) {
+    const int m = m0 + rr0 + q * E::RSTEP;
+    e.live[q] = rr0 + q * E::RSTEP < BM && m < g.M;
+    // a dead slot reads the last row (M > 0); m0 itself can be past M where
+    // a wave's part of a ragged tile holds no row at all
+    const int mm = e.live[q] ? m : g.M - 1;
+    e.bq[q] = mm / g.kk;
+    e.jq[q] = mm - e.bq[q] * g.kk;
+    e.pq[q] = g.idx ? clamp_pos(g.idx[mm], g.T) : e.jq[q];
+  }
+  if constexpr (EPI == EPI_RESID_STORE || EPI == EPI_RESID_SCATTER) {
+    if (n < g.N) {
+#pragma unroll
+      for (int q = 0; q < E::RPT; ++q) {
+        if (!e.live[q]) continue;  // residual rows of live slots only
+        const int m = m0 + rr0 + q * E::RSTEP;
+        const T* src = (EPI == EPI_RESID_SCATTER && g.res)
+                           ? (const T*)g.res + int64_t(m) * g.N + n
+                           : (const T*)g.x + (int64_t(e.bq[q]) * g.T + e.pq[q]) * g.N + n;
+        e.xr[q] = load_raw8(src);
+      }
+    }
+  }
+}
+
 // stage: fp32 tile [BM][BN + 4] in LDS; tile origin (m0, tn). Each thread owns
 // one 8-column chunk and walks the tile's rows, so everything that depends
 // only on the column (bias, head, RoPE partner) is computed once. EPI is an
-// EpiKind.
-template <typename T, int BM, int BN, int NT, int EPI>
-__device__ void gemm_epilogue(const GemmArgs& g, const float* stage, int m0, int tn, int tid) {
+// EpiKind. rows: the thread's rows as epi_prefetch read them for this
+// (m0, tn, tid); PRE: they include the residual rows (else these are loaded
+// here).
+template <typename T, int BM, int BN, int NT, int EPI, bool PRE>
+__device__ __forceinline__ void gemm_epilogue_rows(const GemmArgs& g, const float* stage, int m0, int tn, int tid,
+                                                   const EpiPre<T, BM, BN, NT>& rows) {
   constexpr int LD = BN + 4;
   if constexpr (EPI == EPI_SWIGLU) {
     // tile columns [0, BN/2) are gate units, [BN/2, BN) the matching up units
@@ -151,17 +197,10 @@ __device__ void gemm_epilogue(const GemmArgs& g, const float* stage, int m0, int
   // is finished, so the rows' memory latencies overlap instead of adding up.
   constexpr int RPT = (BM + RSTEP - 1) / RSTEP;
   const int rr0 = tid / CPR;
-  int bq[RPT], jq[RPT], pq[RPT];
-  bool live[RPT];
-#pragma unroll
-  for (int q = 0; q < RPT; ++q) {
-    const int m = m0 + rr0 + q * RSTEP;
-    live[q] = rr0 + q * RSTEP < BM && m < g.M;
-    const int mm = live[q] ? m : m0;  // m0 < M: a valid row to read for dead slots
-    bq[q] = mm / g.kk;
-    jq[q] = mm - bq[q] * g.kk;
-    pq[q] = g.idx ? clamp_pos(g.idx[mm], g.T) : jq[q];
-  }
+  const int(&bq)[RPT] = rows.bq;
+  const int(&jq)[RPT] = rows.jq;
+  const int(&pq)[RPT] = rows.pq;
+  const bool(&live)[RPT] = rows.live;
   if constexpr (EPI == EPI_RESID_SCATTER_GATE) {
     // Gated scatter (Section 3.4): the block's update of each kept row,
     // delta = (resid + C + biases) - x[b, pos], is scaled by sigmoid of the
@@ -204,6 +243,10 @@ __device__ void gemm_epilogue(const GemmArgs& g, const float* stage, int m0, int
 #pragma unroll
     for (int q = 0; q < RPT; ++q) {
       if (!live[q]) continue;
+      if constexpr (PRE) {
+        unpack8(rows.xr[q], xr[q]);
+        continue;
+      }
       const int m = m0 + rr0 + q * RSTEP;
       const T* src = (EPI == EPI_RESID_SCATTER && g.res) ? (const T*)g.res + int64_t(m) * g.N + n
                                                          : (const T*)g.x + (int64_t(bq[q]) * g.T + pq[q]) * g.N + n;
@@ -329,6 +372,13 @@ __device__ void gemm_epilogue(const GemmArgs& g, const float* stage, int m0, int
       store8((T*)g.out + int64_t(m) * g.ldo + n, v);
     }
   }
+}
+
+template <typename T, int BM, int BN, int NT, int EPI>
+__device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, const float* stage, int m0, int tn, int tid) {
+  EpiPre<T, BM, BN, NT> rows;
+  if constexpr (EPI != EPI_SWIGLU) epi_prefetch<T, BM, BN, NT, EPI_STORE>(g, m0, tn, tid, rows);  // positions only
+  gemm_epilogue_rows<T, BM, BN, NT, EPI, false>(g, stage, m0, tn, tid, rows);
 }
 
 // ----------------------------------------------------------- bf16 MFMA GEMM
@@ -739,6 +789,18 @@ struct DmaGemm {
     const int wm = wave / (BN / WN), wn = wave % (BN / WN);
     const int r16 = lane & 15, grp = lane >> 4;
     const int m0 = tm * BM;
+    // wave-staged tiles: the rows' positions (and residual rows) of every
+    // round are requested first, so that their latency overlaps the barrier
+    // and the staging instead of starting each round (not beside the
+    // partials' loads, which take those registers)
+    using Pre = EpiPre<uint16_t, 32, 128, 64>;
+    constexpr bool kPre = C::kWaveEpi && EPI != EPI_SWIGLU && NP == 0;
+    Pre pre[kPre ? MI / 2 : 1];
+    if constexpr (kPre) {
+#pragma unroll
+      for (int rnd = 0; rnd < MI / 2; ++rnd)
+        epi_prefetch<uint16_t, 32, 128, 64, EPI>(g, m0 + wm * WM + 32 * rnd, tn * (BN / 128) + wn, lane, pre[rnd]);
+    }
     __syncthreads();  // all waves are done reading the ring before it becomes the epilogue tile
     if constexpr (C::kWaveEpi) {
       // each wave stages and finishes its own tile, 32 rows at a time, as a
@@ -773,7 +835,10 @@ struct DmaGemm {
           }
         __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS writes are done
         __builtin_amdgcn_wave_barrier();
-        gemm_epilogue<uint16_t, 32, 128, 64, EPI>(g, stage, m0 + wm * WM + 32 * rnd, vtn, lane);
+        if constexpr (kPre)
+          gemm_epilogue_rows<uint16_t, 32, 128, 64, EPI, true>(g, stage, m0 + wm * WM + 32 * rnd, vtn, lane, pre[rnd]);
+        else
+          gemm_epilogue<uint16_t, 32, 128, 64, EPI>(g, stage, m0 + wm * WM + 32 * rnd, vtn, lane);
         __builtin_amdgcn_s_waitcnt(0xc07f);
         __builtin_amdgcn_wave_barrier();
       }
@@ -817,14 +882,20 @@ struct DmaGemm {
     return wave * (MI * NI * kFragBytes) + lane * 16;
   }
 
-  // Store the partial into slot; returns once every store has completed.
+  // Store the partial into slot; returns once every store has completed. The
+  // slot offset goes into the vector offset and the scalar offset is the
+  // constant 0: the compiler then keeps the store-data hazard of 128-bit
+  // buffer stores (a VALU write to a store's data registers right after it
+  // changes what the later lanes store) with a wait state. With a register
+  // scalar offset it assumes no hazard and reuses the data registers at
+  // once, which corrupted a few elements of some partials.
   __device__ static __forceinline__ void store_partial(const GemmArgs& g, const Acc& acc, int slot) {
     const f32x4* a = &acc[0][0];
     const auto r = part_rsrc(g);
-    const int vo = lane_offset(), so = slot * kSlotBytes;
+    const int vo = lane_offset() + slot * kSlotBytes;
 #pragma unroll
     for (int f = 0; f < MI * NI; ++f)
-      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, a[f]), r, vo + f * kFragBytes, so, kCoherent);
+      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, a[f]), r, vo + f * kFragBytes, 0, kCoherent);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   }
 

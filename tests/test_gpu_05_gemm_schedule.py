@@ -226,6 +226,37 @@ def test_split_last_round_matches_oracle(dev, monkeypatch, name):
     assert rel_inf(to_np(y) - to_np(x), to_np(y0) - to_np(x)) < TOL[w.dtype]
 
 
+@pytest.mark.slow
+def test_split_last_round_repeats_bitwise_at_full_size(dev):
+    """GPT-NeoX-1.4B layer shape (4 x 1024 kept rows, QKV 16 x 24 large tiles
+    on 256 resident workgroups: the last 128 tiles cut in 2), in the default
+    launch configuration: the split runs, and repeated calls give the same
+    bits. Every partial tile moves through 32 stores per lane, so a partial
+    whose data registers were overwritten while being stored shows here."""
+    w = S.WORKLOADS["neox14b"].replace(n_layers=1)
+    k = 1024
+    W = S.layer_weights(w, 0)
+    dl = P.DeviceLayer(W, dev)
+    x0 = S.hidden_states(w).to(dev)
+    ws = workspace(w, w.batch, w.seq, k, dev)
+    announce(f"split last round repeat neox14b k={k}")
+    outs = []
+    P.timing_enable(64)
+    try:
+        for i in range(4):
+            x = x0.clone()
+            P.stack_forward(make_desc(w), [dl.weights], [k], x, ws)
+            torch.cuda.synchronize()
+            assert P.workspace_status(ws) == 0
+            if i == 0:
+                assert P.timing_read("gemm_qkv")[0] == 2  # the split ran
+            outs.append(x)
+    finally:
+        P.timing_enable(0)
+    for y in outs[1:]:
+        assert torch.equal(y, outs[0])
+
+
 def test_host_threads_get_their_own_second_streams(dev):
     # each host thread gets its own second stream (destroyed when the thread
     # exits); threads on their own caller streams and workspaces give the
