@@ -88,7 +88,14 @@ struct EpiPre {
   Raw8<T> xr[RPT];
 };
 
-template <typename T, int BM, int BN, int NT, int EPI>
+// Kinds whose epilogue reads the rows' sequence positions.
+constexpr bool epi_uses_positions(int epi) {
+  return epi == EPI_QKV_ROPE || epi == EPI_RESID_STORE || epi == EPI_RESID_SCATTER || epi == EPI_RESID_SCATTER_GATE;
+}
+
+// EPI: the kind whose rows are read; RES: also read its residual rows
+// (residual kinds).
+template <typename T, int BM, int BN, int NT, int EPI, bool RES>
 __device__ __forceinline__ void epi_prefetch(const GemmArgs& g, int m0, int tn, int tid, EpiPre<T, BM, BN, NT>& e) {
   using E = EpiPre<T, BM, BN, NT>;
   const int rr0 = tid / E::CPR, n = tn * BN + (tid % E::CPR) * 8;
@@ -101,9 +108,9 @@ __device__ __forceinline__ void epi_prefetch(const GemmArgs& g, int m0, int tn, 
     const int mm = e.live[q] ? m : g.M - 1;
     e.bq[q] = mm / g.kk;
     e.jq[q] = mm - e.bq[q] * g.kk;
-    e.pq[q] = g.idx ? clamp_pos(g.idx[mm], g.T) : e.jq[q];
+    e.pq[q] = epi_uses_positions(EPI) && g.idx ? clamp_pos(g.idx[mm], g.T) : e.jq[q];
   }
-  if constexpr (EPI == EPI_RESID_STORE || EPI == EPI_RESID_SCATTER) {
+  if constexpr (RES && (EPI == EPI_RESID_STORE || EPI == EPI_RESID_SCATTER)) {
     if (n < g.N) {
 #pragma unroll
       for (int q = 0; q < E::RPT; ++q) {
@@ -377,7 +384,7 @@ __device__ __forceinline__ void gemm_epilogue_rows(const GemmArgs& g, const floa
 template <typename T, int BM, int BN, int NT, int EPI>
 __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, const float* stage, int m0, int tn, int tid) {
   EpiPre<T, BM, BN, NT> rows;
-  if constexpr (EPI != EPI_SWIGLU) epi_prefetch<T, BM, BN, NT, EPI_STORE>(g, m0, tn, tid, rows);  // positions only
+  if constexpr (EPI != EPI_SWIGLU) epi_prefetch<T, BM, BN, NT, EPI, false>(g, m0, tn, tid, rows);  // rows only
   gemm_epilogue_rows<T, BM, BN, NT, EPI, false>(g, stage, m0, tn, tid, rows);
 }
 
@@ -794,12 +801,12 @@ struct DmaGemm {
     // and the staging instead of starting each round (not beside the
     // partials' loads, which take those registers)
     using Pre = EpiPre<uint16_t, 32, 128, 64>;
-    constexpr bool kPre = C::kWaveEpi && EPI != EPI_SWIGLU && NP == 0;
+    constexpr bool kPre = C::kWaveEpi && epi_uses_positions(EPI) && NP == 0;
     Pre pre[kPre ? MI / 2 : 1];
     if constexpr (kPre) {
 #pragma unroll
       for (int rnd = 0; rnd < MI / 2; ++rnd)
-        epi_prefetch<uint16_t, 32, 128, 64, EPI>(g, m0 + wm * WM + 32 * rnd, tn * (BN / 128) + wn, lane, pre[rnd]);
+        epi_prefetch<uint16_t, 32, 128, 64, EPI, true>(g, m0 + wm * WM + 32 * rnd, tn * (BN / 128) + wn, lane, pre[rnd]);
     }
     __syncthreads();  // all waves are done reading the ring before it becomes the epilogue tile
     if constexpr (C::kWaveEpi) {
