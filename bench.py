@@ -45,12 +45,12 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 # kernels_gemm.hip); for anything else `traffic` is null.
 TRAFFIC_MEASURED = [
     # 28-layer Qwen2.5-7B-shaped stack, B 4 x T 8192, SwiGLU gate|up launch:
-    # mean over the 112 sparse dispatches of 4 steps; FETCH_SIZE 3709629.1 KiB
+    # mean over the 112 sparse dispatches of 4 steps; FETCH_SIZE 3654136.9 KiB
     # x 1.9998 (copy: 114698.1 KiB read for 229376 KiB copied), WRITE_SIZE
     # 606134.0 KiB x 1.0 (equal to the bytes the launch stores). The counters
     # count L2 misses, served by the 256 MB MALL or HBM.
-    {"workload": "qwen7b", "kind": "gemm_up", "bytes_per_launch": 8.2173e9,
-     "gemm_source_sha256": "315d2ce0ba78fe517564449b2d0776c9339ccef609a9a772ee8dbda2a23b1544",
+    {"workload": "qwen7b", "kind": "gemm_up", "bytes_per_launch": 8.1037e9,
+     "gemm_source_sha256": "e9ac21d35dcd5f68223a9cd21e25ffd104f9cb220e8389f90222308a5dd1a3d1",
      "profile": "profiles/gemm_up_qwen7b_traffic.md"},
 ]
 
