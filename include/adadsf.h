@@ -282,7 +282,14 @@ int dsf_attention_forward(const void* q, const void* k, const void* v, int dtype
  * tiles when they still fill the chip for more than a round (at least 320
  * tiles), 128 x 128 tiles otherwise; the environment variable
  * DSF_GEMM_TILE=small or =large, read at every launch, forces one size. With
- * 256 x 256 tiles each workgroup runs one tile. With 128 x 128 tiles each
+ * 256 x 256 tiles each workgroup runs one tile; for the forward projections
+ * other than the SwiGLU gate|up (bf16, on the call's workspace), when the
+ * tiles would end in a last round at most half as many as the resident
+ * workgroups, those last tiles go to a second launch that cuts each along K
+ * into 2-4 pieces, the last piece adding the others' partial sums in a
+ * fixed order (deterministic; rounds differently from the unsplit grid).
+ * DSF_GEMM_TAIL=0, read at every launch, turns that split off. With
+ * 128 x 128 tiles each
  * GEMM runs one output tile per workgroup; or, with more tiles than resident
  * workgroups, a persistent grid
  * taking whole tiles (same arithmetic); or, when that would end in a short
@@ -298,8 +305,8 @@ int dsf_attention_forward(const void* q, const void* k, const void* v, int dtype
  * clears at its start and that
  * its kernels OR bits into; read it with dsf_workspace_status once the call's
  * work is enqueued. A call with nothing to do (B, T or k zero), which
- * launches nothing, leaves the word as it was. DSF_WS_STATUS_SK_TIMEOUT: a stream-K workgroup that must
- * add an earlier workgroup's partial sum waits for it with a bounded spin of
+ * launches nothing, leaves the word as it was. DSF_WS_STATUS_SK_TIMEOUT: a stream-K workgroup, or the last
+ * piece of a split tile, that must add an earlier workgroup's partial sum waits for it with a bounded spin of
  * 2^22 polls of its flag (the partial is normally ready within microseconds,
  * because the hardware dispatches workgroups in order); if the wait gives
  * up, the tile is written without that partial, so the call's output is
