@@ -50,7 +50,7 @@ TRAFFIC_MEASURED = [
     # 606134.0 KiB x 1.0 (equal to the bytes the launch stores). The counters
     # count L2 misses, served by the 256 MB MALL or HBM.
     {"workload": "qwen7b", "kind": "gemm_up", "bytes_per_launch": 8.1037e9,
-     "gemm_source_sha256": "e9ac21d35dcd5f68223a9cd21e25ffd104f9cb220e8389f90222308a5dd1a3d1",
+     "gemm_source_sha256": "2bb295f1fd10fb94ff7ead56068b177e1b758f6fe325ddb3a1575a581c6508d6",
      "profile": "profiles/gemm_up_qwen7b_traffic.md"},
 ]
 

@@ -113,7 +113,7 @@ bool timing_claim(hipEvent_t* start, hipEvent_t* stop) {
   *stop = r.stop;
   return true;
 }
-void timing_continue(hipStream_t s) {
+void timing_continue() {
   std::lock_guard<std::mutex> lock(g_tmu);
   if (g_open < 0) return;
   TimingRec& r = g_recs[g_open];
@@ -127,7 +127,6 @@ void timing_continue(hipStream_t s) {
   n.deferred = true;
   n.claimed = false;
   g_open = long(g_used);
-  (void)s;
 }
 void timing_end(int kind, hipStream_t s) {
   std::lock_guard<std::mutex> lock(g_tmu);

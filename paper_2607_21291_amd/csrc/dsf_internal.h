@@ -184,7 +184,7 @@ struct GemmArgs {
 };
 // Timing of a GEMM launched as two kernels: closes the record the first
 // launch claimed and opens another of the same kind for the second.
-void timing_continue(hipStream_t s);
+void timing_continue();
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t s);
 
 // ---- backward of the routed layer (kernels_bwd.hip) ----

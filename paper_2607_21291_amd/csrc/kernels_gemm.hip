@@ -1530,7 +1530,7 @@ static void launch_dma(const GemmArgs& g, hipStream_t s) {
         ga.tail_s = ts.s;
         ga.spin_limit = spin_limit();
         launch_timed(fn, dim3(nt - ts.r), dim3(Cfg::kThreads), s, ga);
-        timing_continue(s);
+        timing_continue();
         launch_timed(gemm_bf16_tail_kernel<EPI, BM, BN, WM, WN, NS, BK>,
                      dim3(kXcds * ts.s * ((ts.r + kXcds - 1) / kXcds)), dim3(Cfg::kThreads), s, ga);
         return;
