@@ -48,9 +48,10 @@ TRAFFIC_MEASURED = [
     # mean over the 112 sparse dispatches of 4 steps; FETCH_SIZE 3654136.9 KiB
     # x 1.9998 (copy: 114698.1 KiB read for 229376 KiB copied), WRITE_SIZE
     # 606134.0 KiB x 1.0 (equal to the bytes the launch stores). The counters
-    # count L2 misses, served by the 256 MB MALL or HBM.
+    # count L2 misses, served by the 256 MB MALL or HBM. Later edits of the
+    # source that left this kernel's device assembly unchanged keep the figure.
     {"workload": "qwen7b", "kind": "gemm_up", "bytes_per_launch": 8.1037e9,
-     "gemm_source_sha256": "2bb295f1fd10fb94ff7ead56068b177e1b758f6fe325ddb3a1575a581c6508d6",
+     "gemm_source_sha256": "ecf6cf5e039f74f0e1e925507666d796c5a528897e2e2c15d92826e3fb5e69d7",
      "profile": "profiles/gemm_up_qwen7b_traffic.md"},
 ]
 

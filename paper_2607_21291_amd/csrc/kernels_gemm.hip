@@ -789,7 +789,9 @@ struct DmaGemm {
   // added in slot order to each fragment as it is staged, a few fragments'
   // loads in flight at a time; a partial beyond np is read beyond the end of
   // the buffer, out of the resource's range, where every load returns zeros.
-  template <int NP = 0>
+  // PF: request the rows' positions and residual rows before the barrier
+  // (off in the persistent stream-K kernel, whose registers are taken).
+  template <int NP = 0, bool PF = true>
   __device__ static __forceinline__ void epilogue(const GemmArgs& g, char* smem, int tm, int tn, Acc& acc,
                                                   int slot0 = 0, int np = 0) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -801,13 +803,18 @@ struct DmaGemm {
     // and the staging instead of starting each round (not beside the
     // partials' loads, which take those registers)
     using Pre = EpiPre<uint16_t, 32, 128, 64>;
-    constexpr bool kPre = C::kWaveEpi && epi_uses_positions(EPI) && NP == 0;
+    constexpr bool kPre = C::kWaveEpi && PF && epi_uses_positions(EPI) && NP == 0;
     Pre pre[kPre ? MI / 2 : 1];
     if constexpr (kPre) {
 #pragma unroll
       for (int rnd = 0; rnd < MI / 2; ++rnd)
         epi_prefetch<uint16_t, 32, 128, 64, EPI, true>(g, m0 + wm * WM + 32 * rnd, tn * (BN / 128) + wn, lane, pre[rnd]);
     }
+    // workgroup-staged tiles: the same for the thread's rows of the whole tile
+    using PreT = EpiPre<uint16_t, BM, BN, C::kThreads>;
+    constexpr bool kPreT = !C::kWaveEpi && PF && epi_uses_positions(EPI) && NP == 0;
+    PreT pre_t;
+    if constexpr (kPreT) epi_prefetch<uint16_t, BM, BN, C::kThreads, EPI, true>(g, m0, tn, tid, pre_t);
     __syncthreads();  // all waves are done reading the ring before it becomes the epilogue tile
     if constexpr (C::kWaveEpi) {
       // each wave stages and finishes its own tile, 32 rows at a time, as a
@@ -859,7 +866,10 @@ struct DmaGemm {
           for (int e = 0; e < 4; ++e)
             stage[(wm * WM + 16 * i + 4 * grp + e) * C::kStageLD + wn * WN + 16 * j + r16] = acc[i][j][e];
       __syncthreads();
-      gemm_epilogue<uint16_t, BM, BN, C::kThreads, EPI>(g, stage, m0, tn, threadIdx.x);
+      if constexpr (kPreT)
+        gemm_epilogue_rows<uint16_t, BM, BN, C::kThreads, EPI, true>(g, stage, m0, tn, tid, pre_t);
+      else
+        gemm_epilogue<uint16_t, BM, BN, C::kThreads, EPI>(g, stage, m0, tn, threadIdx.x);
     }
   }
 
@@ -1046,7 +1056,7 @@ __global__ __launch_bounds__((DmaCfg<BM, BN, WM, WN, NS, BK>::kThreads)) void ge
     const GemmTile tt = gemm_tile(t0 + t, g.ntm, ntn, g.group_m);
     const int tm = tt.tm, tn = tt.tn;
     G::mainloop(g, smem, tm, tn, 0, nk, acc);
-    G::epilogue(g, smem, tm, tn, acc);
+    G::template epilogue<0, false>(g, smem, tm, tn, acc);
   }
   const int64_t usk = int64_t(ntx - dp) * nk;
   auto piece = [&](int w) { return usk * w / px; };  // first k-iteration of workgroup w's piece
@@ -1089,7 +1099,7 @@ __global__ __launch_bounds__((DmaCfg<BM, BN, WM, WN, NS, BK>::kThreads)) void ge
         if (spin_failed) break;  // left unfinished (and reported) rather than hang
         G::template add_partials<1>(g, slot, 1, acc);
       }
-      G::epilogue(g, smem, tm, tn, acc);
+      G::template epilogue<0, false>(g, smem, tm, tn, acc);
     }
     u = tb + kb;
   }
