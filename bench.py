@@ -51,7 +51,7 @@ TRAFFIC_MEASURED = [
     # count L2 misses, served by the 256 MB MALL or HBM. Later edits of the
     # source that left this kernel's device assembly unchanged keep the figure.
     {"workload": "qwen7b", "kind": "gemm_up", "bytes_per_launch": 8.1037e9,
-     "gemm_source_sha256": "ecf6cf5e039f74f0e1e925507666d796c5a528897e2e2c15d92826e3fb5e69d7",
+     "gemm_source_sha256": "af8b22a124d5e4774286d7589223c7bdc6acd704b973aaaa7f6c493f8b1a996f",
      "profile": "profiles/gemm_up_qwen7b_traffic.md"},
 ]
 

@@ -1467,10 +1467,19 @@ static void skinny_split(int ntn, int K, int* splits, int* kc) {
 // into whole 128-unit tiles; small tiles otherwise. Measured on one layer of
 // each workload: the large tiles win on every Qwen2.5-7B projection (gate/up
 // 0.38 -> 0.47 of peak, down 0.32 -> 0.46), on the NeoX-1.4B QKV and up, and
-// on the NeoX-160M QKV; the small ones on the 768- to 2048-wide down
-// projections, whose grids of large tiles cover the chip once or less.
+// on the NeoX-160M QKV alone; the small ones on the 768- to 2048-wide down
+// projections, whose grids of large tiles cover the chip once or less. In
+// the stacks, the forward projections with shallow reductions (K below
+// kLargeMinDepth) keep the small tiles up to kLargeShallowMinTiles tiles:
+// with K 768-1536 (NeoX-160M, Qwen2.5-0.5B, Qwen2.5-1.5B) each large tile's
+// main loop is short beside its epilogue, and the NeoX QKV and up
+// projections share the chip on two streams, where two small-tile
+// workgroups per CU interleave better (stacks 1.5, 0.8 and 0.6 % faster);
+// with K 2048 (NeoX-1.4B) the large tiles stay ahead (5 %).
 // DSF_GEMM_TILE=small|large (read at every launch) forces one of them.
 constexpr int kLargeMinTiles = 320;
+constexpr int kLargeMinDepth = 2048;
+constexpr int kLargeShallowMinTiles = 640;
 
 template <int EPI>
 static bool use_large_tiles(const GemmArgs& g) {
@@ -1480,7 +1489,9 @@ static bool use_large_tiles(const GemmArgs& g) {
   if (e && !strcmp(e, "large")) return true;
   const int64_t ntm = (g.M + TileLarge::BM - 1) / TileLarge::BM;
   const int64_t ntn = EPI == EPI_SWIGLU ? g.f / (TileLarge::BN / 2) : (g.N + TileLarge::BN - 1) / TileLarge::BN;
-  return ntm * ntn >= kLargeMinTiles;
+  const int64_t nt = ntm * ntn;
+  if (EPI < EPI_STORE && g.K < kLargeMinDepth) return nt >= kLargeShallowMinTiles;
+  return nt >= kLargeMinTiles;
 }
 
 template <int EPI, class TC>
