@@ -45,13 +45,12 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 # kernels_gemm.hip); for anything else `traffic` is null.
 TRAFFIC_MEASURED = [
     # 28-layer Qwen2.5-7B-shaped stack, B 4 x T 8192, SwiGLU gate|up launch:
-    # mean over the 112 sparse dispatches of 4 steps; FETCH_SIZE 3654136.9 KiB
+    # mean over the 112 sparse dispatches of 4 steps; FETCH_SIZE 3692362.8 KiB
     # x 1.9998 (copy: 114698.1 KiB read for 229376 KiB copied), WRITE_SIZE
     # 606134.0 KiB x 1.0 (equal to the bytes the launch stores). The counters
-    # count L2 misses, served by the 256 MB MALL or HBM. Later edits of the
-    # source that left this kernel's device assembly unchanged keep the figure.
-    {"workload": "qwen7b", "kind": "gemm_up", "bytes_per_launch": 8.1037e9,
-     "gemm_source_sha256": "af8b22a124d5e4774286d7589223c7bdc6acd704b973aaaa7f6c493f8b1a996f",
+    # count L2 misses, served by the 256 MB MALL or HBM.
+    {"workload": "qwen7b", "kind": "gemm_up", "bytes_per_launch": 8.1820e9,
+     "gemm_source_sha256": "7470e0d09e28ef3bbe532ada0a3c93f2ae0b8787314635848284817f10a3064f",
      "profile": "profiles/gemm_up_qwen7b_traffic.md"},
 ]
 

@@ -280,8 +280,9 @@ int dsf_attention_forward(const void* q, const void* k, const void* v, int dtype
  *
  * Projection schedule. Each bf16 projection GEMM takes 256 x 256 output
  * tiles when they still fill the chip for more than a round (at least 320
- * tiles; 640 for forward projections with a reduction shorter than 2048),
- * 128 x 128 tiles otherwise; the environment variable
+ * tiles; 640 for forward projections with a reduction shorter than 2048;
+ * the GPT-NeoX QKV and up projections, which run side by side, take one size
+ * for both), 128 x 128 tiles otherwise; the environment variable
  * DSF_GEMM_TILE=small or =large, read at every launch, forces one size. With
  * 256 x 256 tiles each workgroup runs one tile; for the forward projections
  * other than the SwiGLU gate|up (bf16, on the call's workspace), when the

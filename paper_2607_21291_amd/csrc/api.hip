@@ -731,8 +731,11 @@ int run_layer(const Ctx& c, const dsf_layer_weights* W, void* x, int k, bool den
     DSF_HIP(hipStreamWaitEvent(c.aux->s, c.aux->fork, 0));
     us = c.aux->s;
   }
+  // NeoX: the up and QKV projections share the chip; one tile size for both
+  const int pair_hint = qwen ? 0 : gemm_pair_tile_hint(M, dq + 2 * dkv, d);
   if (!qwen) {  // FFN up + GELU on LN2 of the kept rows
     GemmArgs u = g;
+    u.tile_hint = pair_hint;
     u.M = M; u.N = f; u.K = d; u.K1 = d;
     u.a = na.out2; u.lda = d;
     u.b = W->w_up; u.ldb = d;
@@ -748,6 +751,7 @@ int run_layer(const Ctx& c, const dsf_layer_weights* W, void* x, int k, bool den
     q.a = na.out1; q.lda = d;
     q.b = W->w_qkv; q.ldb = d;
     q.epi = EPI_QKV_ROPE;
+    q.tile_hint = pair_hint;
     q.bias = W->b_qkv;
     q.q = at<char>(c, c.plan.q); q.k = at<char>(c, c.plan.k); q.v = at<char>(c, c.plan.v);
     q.Hq = Hq; q.Hkv = Hkv; q.hd = hd; q.R = D.rotary_dims;

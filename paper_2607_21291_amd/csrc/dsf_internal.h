@@ -181,11 +181,17 @@ struct GemmArgs {
   // tiles tail0 .. tail0 + tail_r - 1 of the tile order, each split into
   // tail_s pieces of its k-tiles
   int tail0, tail_r, tail_s;
+  // tile size chosen by the caller for a pair of GEMMs that share the chip
+  // (0: the launcher's own rule, 1: 128 x 128, 2: 256 x 256)
+  int tile_hint;
 };
 // Timing of a GEMM launched as two kernels: closes the record the first
 // launch claimed and opens another of the same kind for the second.
 void timing_continue();
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t s);
+// GemmArgs::tile_hint for two forward projections run side by side, from the
+// leading one's M x N and reduction K (0: leave each launch its own rule).
+int gemm_pair_tile_hint(int M, int N, int K);
 
 // ---- backward of the routed layer (kernels_bwd.hip) ----
 // out[c][r] = op(in[r][c]) (op 0 copy, 1 GELU, 2 SiLU(in[r][c]) * in[r][C + c]);

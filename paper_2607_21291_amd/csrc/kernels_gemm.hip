@@ -1469,17 +1469,33 @@ static void skinny_split(int ntn, int K, int* splits, int* kc) {
 // 0.38 -> 0.47 of peak, down 0.32 -> 0.46), on the NeoX-1.4B QKV and up, and
 // on the NeoX-160M QKV alone; the small ones on the 768- to 2048-wide down
 // projections, whose grids of large tiles cover the chip once or less. In
-// the stacks, the forward projections with shallow reductions (K below
-// kLargeMinDepth) keep the small tiles up to kLargeShallowMinTiles tiles:
-// with K 768-1536 (NeoX-160M, Qwen2.5-0.5B, Qwen2.5-1.5B) each large tile's
-// main loop is short beside its epilogue, and the NeoX QKV and up
-// projections share the chip on two streams, where two small-tile
-// workgroups per CU interleave better (stacks 1.5, 0.8 and 0.6 % faster);
-// with K 2048 (NeoX-1.4B) the large tiles stay ahead (5 %).
+// the stacks, forward projections with shallow reductions (K below
+// kLargeMinDepth: 896 and 1536 on the Qwen2.5-0.5B and -1.5B shapes) keep
+// the small tiles up to kLargeShallowMinTiles tiles, where a large tile's
+// short main loop leaves its epilogue a bigger share (stacks 1.5 and 0.6 %
+// faster). A caller that runs two projections side by side on two streams
+// picks one size for both (GemmArgs::tile_hint, gemm_pair_tile_hint): a
+// 256 x 256 workgroup takes most of a CU's LDS and cannot share the CU with
+// a 128 x 128 one, so mixed sizes starve the large-tile launch.
 // DSF_GEMM_TILE=small|large (read at every launch) forces one of them.
 constexpr int kLargeMinTiles = 320;
 constexpr int kLargeMinDepth = 2048;
 constexpr int kLargeShallowMinTiles = 640;
+constexpr int kLargePairMinTiles = 400;
+
+// The tile size for a pair of forward projections that share the chip,
+// from the leading one's shape (M x N, reduction K): deep reductions keep
+// each launch's own rule (large from kLargeMinTiles tiles for both NeoX-1.4B
+// projections); shallow ones take one size for both, large from
+// kLargePairMinTiles tiles of the leading grid. NeoX-130M shape (QKV grids
+// of 405-522 large tiles): large for both 2-8 % faster than small for both;
+// NeoX-160M (171-441): small for both 1.5 % faster than the sizes chosen
+// one launch at a time.
+int gemm_pair_tile_hint(int M, int N, int K) {
+  if (K >= kLargeMinDepth) return 0;
+  const int64_t nt = int64_t((M + TileLarge::BM - 1) / TileLarge::BM) * ((N + TileLarge::BN - 1) / TileLarge::BN);
+  return nt >= kLargePairMinTiles ? 2 : 1;
+}
 
 template <int EPI>
 static bool use_large_tiles(const GemmArgs& g) {
@@ -1487,6 +1503,7 @@ static bool use_large_tiles(const GemmArgs& g) {
   const char* e = getenv("DSF_GEMM_TILE");
   if (e && !strcmp(e, "small")) return false;
   if (e && !strcmp(e, "large")) return true;
+  if (g.tile_hint) return g.tile_hint == 2;
   const int64_t ntm = (g.M + TileLarge::BM - 1) / TileLarge::BM;
   const int64_t ntn = EPI == EPI_SWIGLU ? g.f / (TileLarge::BN / 2) : (g.N + TileLarge::BN - 1) / TileLarge::BN;
   const int64_t nt = ntm * ntn;
